@@ -1,0 +1,188 @@
+"""CPU oracle for the thinning hot path -- TEST INFRASTRUCTURE ONLY.
+
+A plain, single-threaded float64 C implementation (``oracle.c``) of kernel
+halving under kappa_att, the Compress level structure, stratified subsampling
+and softmax attention, written from the paper ("Express Language Modeling").
+This wrapper only marshals numpy arrays.  Only ``tests/``, the smoke check and
+the benchmark's CPU-baseline leg may import it; the HIP library never does.
+
+Pinned by ``tests/test_oracle_pins.py`` (closed forms, invariants, special
+cases, an explicit feature-space route and brute force on tiny inputs).
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+import subprocess
+from typing import Optional
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SO = os.path.join(_HERE, "liboracle.so")
+_lib = None
+
+KERNELS = {"katt": 0, "linear": 1}
+
+
+class Stats(C.Structure):
+    _fields_ = [
+        ("decisions", C.c_int64),
+        ("swaps", C.c_int64),
+        ("near_ties", C.c_int64),
+        ("hard_mismatch", C.c_int64),
+        ("zero_threshold", C.c_int64),
+        ("min_abs_rho", C.c_double),
+    ]
+
+    def as_dict(self):
+        return {k: getattr(self, k) for k, _ in self._fields_}
+
+
+class Plan(C.Structure):
+    _fields_ = [
+        ("n_kept", C.c_int64),
+        ("rounds", C.c_int32),
+        ("compress_levels", C.c_int32),
+        ("uniforms", C.c_int64),
+        ("subsample", C.c_int32),
+    ]
+
+
+def build() -> str:
+    """Compile liboracle.so with gcc (no fast-math: IEEE float64 throughout)."""
+    src = os.path.join(_HERE, "oracle.c")
+    cmd = ["gcc", "-O2", "-std=c11", "-fPIC", "-shared", "-o", _SO, src, "-lm"]
+    subprocess.run(cmd, check=True)
+    return _SO
+
+
+def lib():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_SO) or os.path.getmtime(_SO) < os.path.getmtime(
+                os.path.join(_HERE, "oracle.c")):
+            build()
+        L = C.CDLL(_SO)
+        P = C.c_void_p
+        L.or_plan.argtypes = [C.c_int64, C.c_int64, C.c_int32, C.POINTER(Plan)]
+        L.or_plan.restype = C.c_int
+        L.or_vmax2.argtypes = [P, C.c_int64, C.c_int64]
+        L.or_vmax2.restype = C.c_double
+        L.or_subsample.argtypes = [C.c_int64, C.c_int64, P, P]
+        L.or_subsample.restype = None
+        L.or_kernel_halving.argtypes = [P, P, C.c_int64, C.c_double, C.c_int, C.c_double, P,
+                                        C.c_int64, P, P, P, C.c_double, P, P, P, P,
+                                        C.POINTER(Stats)]
+        L.or_kernel_halving.restype = C.c_int
+        L.or_compress.argtypes = [P, P, C.c_int64, C.c_int64, C.c_int64, C.c_int32, C.c_int, P,
+                                  P, P, C.c_double, P, P, C.POINTER(Stats)]
+        L.or_compress.restype = C.c_int
+        L.or_attention.argtypes = [P, P, P, C.c_int64, C.c_int64, P, C.c_int64, P]
+        L.or_attention.restype = None
+        _lib = L
+    return _lib
+
+
+def _p(a: Optional[np.ndarray]):
+    return None if a is None else a.ctypes.data_as(C.c_void_p)
+
+
+def _f64(a) -> np.ndarray:
+    if hasattr(a, "detach"):  # torch tensor: exact upcast
+        import torch
+        a = a.detach().to("cpu", torch.float64).numpy()
+    return np.ascontiguousarray(a, dtype=np.float64)
+
+
+def _f32(a) -> np.ndarray:
+    if hasattr(a, "detach"):
+        a = a.detach().cpu().numpy()
+    return np.ascontiguousarray(a, dtype=np.float32)
+
+
+def plan(n: int, n_out: int, g: int) -> Optional[dict]:
+    p = Plan()
+    if lib().or_plan(n, n_out, g, C.byref(p)) != 0:
+        return None
+    return {k: getattr(p, k) for k, _ in Plan._fields_}
+
+
+def vmax2(V) -> float:
+    V = _f64(V)
+    return lib().or_vmax2(_p(V), V.shape[0], V.shape[1])
+
+
+def subsample(n: int, n_kept: int, u) -> np.ndarray:
+    u = _f32(u)
+    assert u.size >= n_kept
+    out = np.empty(n_kept, dtype=np.int32)
+    lib().or_subsample(n, n_kept, _p(u), _p(out))
+    return out
+
+
+def kernel_halving(K, V, rows, u, *, vmax2_value: Optional[float] = None,
+                   kernel: str = "katt", delta: float = 0.5, follow=None,
+                   tol: float = 1e-5) -> dict:
+    """KH(delta) on one bucket `rows` (indices into K/V rows)."""
+    K, V = _f64(K), _f64(V)
+    rows = np.ascontiguousarray(rows, dtype=np.int32)
+    u = _f32(u)
+    N = rows.size
+    h = N // 2
+    assert u.size >= h
+    vm = vmax2(V) if vmax2_value is None else float(vmax2_value)
+    out = np.empty(h, dtype=np.int32)
+    bits = np.empty(h, dtype=np.uint8)
+    rho = np.empty(h)
+    alpha = np.empty(h)
+    thresh = np.empty(h)
+    fol = None if follow is None else np.ascontiguousarray(follow, dtype=np.uint8)
+    st = Stats()
+    rc = lib().or_kernel_halving(_p(K), _p(V), K.shape[1], vm, KERNELS[kernel], delta,
+                                 _p(rows), N, _p(u), _p(out), _p(fol), tol, _p(bits),
+                                 _p(rho), _p(alpha), _p(thresh), C.byref(st))
+    if rc != 0:
+        raise ValueError(f"or_kernel_halving failed ({rc})")
+    return {"out": out, "bits": bits, "rho": rho, "alpha": alpha, "thresh": thresh,
+            "stats": st.as_dict()}
+
+
+def compress(K, V, n_out: int, g: int, U, *, kernel: str = "katt", follow=None,
+             tol: float = 1e-5) -> dict:
+    """One slice: K, V [n, d]; U = this slice's uniforms."""
+    K, V = _f64(K), _f64(V)
+    n, d = K.shape
+    pl = plan(n, n_out, g)
+    if pl is None:
+        raise ValueError("no valid level structure for these arguments")
+    U = _f32(U)
+    assert U.size >= pl["uniforms"], (U.size, pl["uniforms"])
+    cnt = max(int(pl["uniforms"]), 1)
+    idx = np.empty(n_out, dtype=np.int32)
+    bits = np.zeros(cnt, dtype=np.uint8)
+    rho = np.zeros(cnt)
+    fol = None if follow is None else np.ascontiguousarray(follow, dtype=np.uint8)
+    if fol is not None:
+        assert fol.size >= pl["uniforms"]
+    st = Stats()
+    rc = lib().or_compress(_p(K), _p(V), n, d, n_out, g, KERNELS[kernel], _p(U), _p(idx),
+                           _p(fol), tol, _p(bits), _p(rho), C.byref(st))
+    if rc != 0:
+        raise ValueError(f"or_compress failed ({rc})")
+    return {"idx": idx, "bits": bits, "rho": rho, "stats": st.as_dict(), "plan": pl}
+
+
+def attention(Q, K, V, rows) -> np.ndarray:
+    """Softmax attention of every query over the rows `rows` of K/V (float64)."""
+    Q, K, V = _f64(Q), _f64(K), _f64(V)
+    rows = np.ascontiguousarray(rows, dtype=np.int32)
+    n_q, d = Q.shape
+    O = np.empty((n_q, d))
+    lib().or_attention(_p(Q), _p(K), _p(V), n_q, d, _p(rows), rows.size, _p(O))
+    return O
+
+
+def exact_attention(Q, K, V) -> np.ndarray:
+    K = _f64(K)
+    return attention(Q, K, V, np.arange(K.shape[0], dtype=np.int32))

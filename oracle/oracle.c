@@ -1,0 +1,299 @@
+/*
+ * CPU oracle for the thinning hot path -- TEST INFRASTRUCTURE ONLY.
+ * See oracle.h.  Everything is float64, single-threaded and written in the
+ * order the paper states it; no blocking, no incremental reformulation.
+ */
+#include "oracle.h"
+
+#include <math.h>
+#include <stdlib.h>
+#include <string.h>
+
+/* ------------------------------------------------------------------ */
+/* Level structure.                                                    */
+/*                                                                     */
+/* The output size n_out and the oversampling parameter g are read as  */
+/* follows.  L = floor(log2(n / n_out)) halving rounds take            */
+/* n_kept = n_out 2^L rows down to n_out.  If n_kept < n, a stratified */
+/* subsample (one draw per contiguous stratum) first keeps n_kept rows */
+/* (Sec. 3.1: Express subsamples first, then runs Compress2).  The     */
+/* first m_c = L - min(g, L) rounds are Offline-Compress2 (App. H,     */
+/* Algorithm H.2) with output size 2^g n_out; the remaining rounds      */
+/* halve the whole set, as Express halves its coreset twice (Alg. 1).  */
+/* Compress2 at level m partitions its 2^m n_out' input into 4^(m-1)    */
+/* equal groups, so every group must hold an even number >= 2 of rows. */
+/* ------------------------------------------------------------------ */
+int or_plan(int64_t n, int64_t n_out, int32_t g, or_plan_t* plan) {
+  if (n < 1 || n_out < 1 || n_out > n || g < 0 || plan == NULL) return -1;
+  int32_t L = 0;
+  while (n_out * ((int64_t)1 << (L + 1)) <= n) L++;
+  int64_t n_kept = n_out * ((int64_t)1 << L);
+  int32_t g_eff = g < L ? g : L;
+  int32_t mc = L - g_eff;
+  /* every Compress2 group at every level: n_in(m) / 4^(m-1), n_in(m) = 2^m 2^g_eff n_out */
+  for (int32_t m = mc; m >= 1; --m) {
+    int64_t n_in = n_out * ((int64_t)1 << (g_eff + m));
+    int64_t groups = (int64_t)1 << (2 * (m - 1));
+    if (n_in % groups != 0) return -1;
+    int64_t size = n_in / groups;
+    if (size < 2 || size % 2 != 0) return -1;
+  }
+  plan->n_kept = n_kept;
+  plan->rounds = L;
+  plan->compress_levels = mc;
+  plan->subsample = n_kept < n ? 1 : 0;
+  plan->uniforms = (plan->subsample ? n_kept : 0) + (n_kept - n_out);
+  return 0;
+}
+
+/* v_max = max_i ||v_i||_inf over all n rows (Sec. 2.1, eq. katt). */
+double or_vmax2(const double* V, int64_t n, int64_t d) {
+  double m = 0.0;
+  for (int64_t i = 0; i < n * d; ++i) {
+    double a = fabs(V[i]);
+    if (a > m) m = a;
+  }
+  return m * m;
+}
+
+/*
+ * Stratified subsample (Alg. 3 / Algorithm H.1: keep one uniformly drawn
+ * point per group).  Strata are the contiguous ranges
+ * [floor(t n / n_kept), floor((t+1) n / n_kept)); with u = k 2^-24 the draw
+ * floor(u len) is computed exactly in integers.
+ */
+void or_subsample(int64_t n, int64_t n_kept, const float* u, int32_t* out) {
+  for (int64_t t = 0; t < n_kept; ++t) {
+    int64_t start = (t * n) / n_kept;
+    int64_t end = ((t + 1) * n) / n_kept;
+    int64_t len = end - start;
+    int64_t k = (int64_t)((double)u[t] * 16777216.0);
+    int64_t pick = (k * len) >> 24;
+    if (pick > len - 1) pick = len - 1;
+    out[t] = (int32_t)(start + pick);
+  }
+}
+
+/* ------------------------------------------------------------------ */
+/* Kernels.                                                            */
+/* ------------------------------------------------------------------ */
+typedef struct {
+  const double* K;
+  const double* V;
+  int64_t d;
+  double vmax2;
+  double inv_sqrt_d;
+  int kernel;
+} kctx_t;
+
+static double dot(const double* a, const double* b, int64_t d) {
+  double s = 0.0;
+  for (int64_t c = 0; c < d; ++c) s += a[c] * b[c];
+  return s;
+}
+
+/* Sec. 2.1, eq. katt. */
+static double kap(const kctx_t* c, int32_t i, int32_t j) {
+  const double* ki = c->K + (int64_t)i * c->d;
+  const double* kj = c->K + (int64_t)j * c->d;
+  const double* vi = c->V + (int64_t)i * c->d;
+  const double* vj = c->V + (int64_t)j * c->d;
+  if (c->kernel == OR_KERNEL_LINEAR) return dot(ki, kj, c->d) + dot(vi, vj, c->d);
+  return exp(dot(ki, kj, c->d) * c->inv_sqrt_d) * (dot(vi, vj, c->d) + c->vmax2);
+}
+
+/*
+ * KH(delta), App. A Algorithm A.1.  Pair i takes the next two points
+ * (x, x') = (y_{2i-1}, y_{2i}) in input order.  Its RKHS distance b_i and the
+ * running maximum b_max give the threshold a_i = b_i b_max (1/2 + log(2N/delta))
+ * (natural log).  The balance score alpha_i sums f_i = k(x,.) - k(x',.) over
+ * all earlier points and subtracts twice the sum over coreset 1.  The pair is
+ * swapped with probability min(1, (1 - alpha_i/a_i)_+ / 2), realised as
+ * "u_i < p_i"; coreset 1 then receives the first element.  When a_i = 0 the
+ * ratio is undefined and p_i = 1/2 is used.
+ */
+int or_kernel_halving(const double* K, const double* V, int64_t d, double vmax2,
+                      int kernel, double delta, const int32_t* rows, int64_t N,
+                      const float* u, int32_t* out, const uint8_t* follow, double tol,
+                      uint8_t* bits, double* rho, double* alpha_tr, double* thresh_tr,
+                      or_stats_t* st) {
+  if (N < 2 || (N % 2) != 0 || d < 1 || !(delta > 0.0)) return -1;
+  kctx_t c = {K, V, d, vmax2, 1.0 / sqrt((double)d), kernel};
+  int64_t half = N / 2;
+  double* f = (double*)malloc(sizeof(double) * (size_t)N);
+  uint8_t* sw = (uint8_t*)malloc((size_t)half);
+  if (!f || !sw) {
+    free(f);
+    free(sw);
+    return -2;
+  }
+  const double logterm = 0.5 + log(2.0 * (double)N / delta);
+  double bmax = 0.0;
+  for (int64_t i = 0; i < half; ++i) {
+    int32_t x = rows[2 * i], xp = rows[2 * i + 1];
+    double b2 = kap(&c, x, x) + kap(&c, xp, xp) - 2.0 * kap(&c, x, xp);
+    double b = sqrt(b2 > 0.0 ? b2 : 0.0);
+    if (b > bmax) bmax = b;
+    double a = b * bmax * logterm;
+
+    double alpha = 0.0;
+    for (int64_t j = 0; j < 2 * i; ++j) {
+      f[j] = kap(&c, rows[j], x) - kap(&c, rows[j], xp);
+      alpha += f[j];
+    }
+    double s1 = 0.0;
+    for (int64_t ip = 0; ip < i; ++ip) s1 += f[2 * ip + sw[ip]];
+    alpha -= 2.0 * s1;
+
+    double ui = (double)u[i];
+    double ratio = 0.0, p;
+    if (a > 0.0) {
+      ratio = alpha / a;
+      p = 0.5 * (1.0 - ratio);
+      if (p < 0.0) p = 0.0;
+      if (p > 1.0) p = 1.0;
+    } else {
+      p = 0.5;
+      if (st) st->zero_threshold++;
+    }
+    int swap = ui < p;
+    double r = ratio - (1.0 - 2.0 * ui);
+    if (st) {
+      double ar = fabs(r);
+      if (st->decisions == 0 || ar < st->min_abs_rho) st->min_abs_rho = ar;
+    }
+    if (follow) {
+      int fb = follow[i] ? 1 : 0;
+      if (fabs(r) < tol) {
+        if (st) st->near_ties++;
+        swap = fb;
+      } else if (fb != swap) {
+        if (st) st->hard_mismatch++;
+        swap = fb;
+      }
+    }
+    sw[i] = (uint8_t)swap;
+    out[i] = swap ? xp : x;
+    if (bits) bits[i] = (uint8_t)swap;
+    if (rho) rho[i] = r;
+    if (alpha_tr) alpha_tr[i] = alpha;
+    if (thresh_tr) thresh_tr[i] = a;
+    if (st) {
+      st->decisions++;
+      st->swaps += swap;
+    }
+  }
+  free(f);
+  free(sw);
+  return 0;
+}
+
+/* ------------------------------------------------------------------ */
+/* Compress.                                                           */
+/* ------------------------------------------------------------------ */
+typedef struct {
+  const double* K;
+  const double* V;
+  int64_t d;
+  double vmax2;
+  int kernel;
+  const float* U;
+  int64_t upos;          /* next unread uniform of this slice */
+  const uint8_t* follow; /* indexed like U */
+  double tol;
+  uint8_t* bits;
+  double* rho;
+  or_stats_t* st;
+} cctx_t;
+
+static int halve_group(cctx_t* c, const int32_t* rows, int64_t N, int32_t* out) {
+  int64_t o = c->upos;
+  int rc = or_kernel_halving(c->K, c->V, c->d, c->vmax2, c->kernel, 0.5, rows, N, c->U + o,
+                             out, c->follow ? c->follow + o : NULL, c->tol,
+                             c->bits ? c->bits + o : NULL, c->rho ? c->rho + o : NULL,
+                             NULL, NULL, c->st);
+  c->upos += N / 2;
+  return rc;
+}
+
+/*
+ * Offline-Compress2 (App. H, Algorithm H.2): with m = 0 return the input;
+ * otherwise split the 2^m n_out' input into 4^(m-1) equal contiguous groups,
+ * halve every group, concatenate the halves in group order and recurse on
+ * m - 1.  `rows` is consumed; the result is written to `rows` itself.
+ */
+static int compress2(cctx_t* c, int32_t m, int32_t* rows, int64_t n_in, int32_t* tmp) {
+  if (m == 0) return 0;
+  int64_t groups = (int64_t)1 << (2 * (m - 1));
+  int64_t size = n_in / groups;
+  for (int64_t k = 0; k < groups; ++k) {
+    int rc = halve_group(c, rows + k * size, size, tmp + k * (size / 2));
+    if (rc) return rc;
+  }
+  memcpy(rows, tmp, sizeof(int32_t) * (size_t)(n_in / 2));
+  return compress2(c, m - 1, rows, n_in / 2, tmp);
+}
+
+int or_compress(const double* K, const double* V, int64_t n, int64_t d, int64_t n_out,
+                int32_t g, int kernel, const float* U, int32_t* idx_out,
+                const uint8_t* follow, double tol, uint8_t* bits, double* rho,
+                or_stats_t* st) {
+  or_plan_t plan;
+  if (or_plan(n, n_out, g, &plan) != 0) return -1;
+  int32_t* rows = (int32_t*)malloc(sizeof(int32_t) * (size_t)n);
+  int32_t* tmp = (int32_t*)malloc(sizeof(int32_t) * (size_t)n);
+  if (!rows || !tmp) {
+    free(rows);
+    free(tmp);
+    return -2;
+  }
+  cctx_t c = {K, V, d, or_vmax2(V, n, d), kernel, U, 0, follow, tol, bits, rho, st};
+  int64_t cur = n;
+  if (plan.subsample) {
+    or_subsample(n, plan.n_kept, U, rows);
+    c.upos = plan.n_kept;
+    cur = plan.n_kept;
+  } else {
+    for (int64_t i = 0; i < n; ++i) rows[i] = (int32_t)i;
+  }
+  int rc = compress2(&c, plan.compress_levels, rows, cur, tmp);
+  cur >>= plan.compress_levels;
+  for (int32_t r = plan.compress_levels; rc == 0 && r < plan.rounds; ++r) {
+    rc = halve_group(&c, rows, cur, tmp);
+    memcpy(rows, tmp, sizeof(int32_t) * (size_t)(cur / 2));
+    cur /= 2;
+  }
+  if (rc == 0) memcpy(idx_out, rows, sizeof(int32_t) * (size_t)n_out);
+  free(rows);
+  free(tmp);
+  return rc;
+}
+
+/* ------------------------------------------------------------------ */
+/* Attention over a coreset (eq. unmaskedatt; eq. def:att_approx with   */
+/* equal weights, which cancel in the ratio).                          */
+/* ------------------------------------------------------------------ */
+void or_attention(const double* Q, const double* K, const double* V, int64_t n_q,
+                  int64_t d, const int32_t* rows, int64_t m, double* O) {
+  double* s = (double*)malloc(sizeof(double) * (size_t)(m > 0 ? m : 1));
+  double inv = 1.0 / sqrt((double)d);
+  for (int64_t q = 0; q < n_q; ++q) {
+    const double* qq = Q + q * d;
+    double mx = -INFINITY;
+    for (int64_t j = 0; j < m; ++j) {
+      s[j] = dot(qq, K + (int64_t)rows[j] * d, d) * inv;
+      if (s[j] > mx) mx = s[j];
+    }
+    double den = 0.0;
+    double* o = O + q * d;
+    for (int64_t c = 0; c < d; ++c) o[c] = 0.0;
+    for (int64_t j = 0; j < m; ++j) {
+      double w = exp(s[j] - mx);
+      den += w;
+      const double* v = V + (int64_t)rows[j] * d;
+      for (int64_t c = 0; c < d; ++c) o[c] += w * v[c];
+    }
+    for (int64_t c = 0; c < d; ++c) o[c] /= den;
+  }
+  free(s);
+}

@@ -1,0 +1,408 @@
+"""Pins of the CPU oracle against what the paper and the mathematics fix.
+
+Each test checks the oracle by a route other than its own formulas: a worked
+example derived by hand, explicit RKHS feature maps, closed forms of the
+level structure, library routines and invariants.  All CPU-only.
+"""
+import json
+import math
+import os
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+# ---------------------------------------------------------------------------
+# Kernel halving
+# ---------------------------------------------------------------------------
+def test_kh_worked_example_golden():
+    """Hand-derived KH example (App. A, Algorithm A.1 under eq. katt, delta=1/2)."""
+    with open(os.path.join(GOLDEN, "kh_worked_example.json")) as f:
+        ex = json.load(f)
+    K = np.array(ex["K"])[:, None]
+    V = np.array(ex["V"])[:, None]
+    rows = np.arange(4)
+    for case in ex["cases"]:
+        r = oracle.kernel_halving(K, V, rows, np.array(case["u"], np.float32))
+        assert list(r["out"]) == case["out"], case
+        assert r["alpha"][0] == 0.0
+        ratio = r["alpha"][1] / r["thresh"][1]
+        want = ex["ratio_after_swap"] if case["u"][0] < 0.5 else ex["ratio_after_no_swap"]
+        assert ratio == pytest.approx(want, rel=1e-13)
+
+
+def test_kh_size2_bucket_is_a_fair_coin():
+    """N = 2: no earlier points, alpha = 0, p = 1/2 -> keep the second iff u < 1/2."""
+    rng = np.random.default_rng(0)
+    K = rng.standard_normal((2, 8))
+    V = rng.standard_normal((2, 8))
+    for u in [0.0, 0.1, 0.49999997, 0.5, 0.7, 1 - 2 ** -24]:
+        r = oracle.kernel_halving(K, V, [0, 1], np.array([u], np.float32))
+        assert r["alpha"][0] == 0.0
+        assert r["out"][0] == (1 if np.float32(u) < 0.5 else 0)
+
+
+def test_kh_first_pair_of_any_bucket_has_zero_score():
+    rng = np.random.default_rng(1)
+    K = rng.standard_normal((32, 4))
+    V = rng.standard_normal((32, 4))
+    u = rng.random(16).astype(np.float32)
+    r = oracle.kernel_halving(K, V, np.arange(32), u)
+    assert r["alpha"][0] == 0.0
+    assert np.all(r["alpha"][1:] != 0.0)
+
+
+@pytest.mark.parametrize("N", [2, 4, 10, 64])
+def test_kh_output_is_one_of_each_pair(N):
+    rng = np.random.default_rng(N)
+    K = rng.standard_normal((N, 3))
+    V = rng.standard_normal((N, 3))
+    rows = np.sort(rng.choice(1000, size=N, replace=False)).astype(np.int32)
+    Kf = np.zeros((1000, 3)); Kf[rows] = K
+    Vf = np.zeros((1000, 3)); Vf[rows] = V
+    r = oracle.kernel_halving(Kf, Vf, rows, rng.random(N // 2).astype(np.float32),
+                              vmax2_value=float(np.abs(V).max() ** 2))
+    out = r["out"]
+    assert out.size == N // 2                       # Def. 1: halving keeps floor(N/2)
+    for i in range(N // 2):
+        assert out[i] in (rows[2 * i], rows[2 * i + 1])
+    assert np.all(np.diff(out) > 0)
+
+
+def _kh_feature_space(Phi, u, delta=0.5):
+    """KH in an explicit feature space: alpha_i = <psi, f_i>, b_i = ||f_i||,
+    psi = sum_{S2} phi - sum_{S1} phi (the RKHS form of App. A's score)."""
+    N = Phi.shape[0]
+    psi = np.zeros(Phi.shape[1])
+    bmax = 0.0
+    c = 0.5 + math.log(2 * N / delta)
+    out, alphas, ths = [], [], []
+    for i in range(N // 2):
+        x, xp = 2 * i, 2 * i + 1
+        f = Phi[x] - Phi[xp]
+        b = math.sqrt(max(float(f @ f), 0.0))
+        bmax = max(bmax, b)
+        a = b * bmax * c
+        alpha = float(psi @ f)
+        p = 0.5 if a == 0 else min(1.0, max(0.0, 0.5 * (1 - alpha / a)))
+        swap = float(u[i]) < p
+        s1, s2 = (xp, x) if swap else (x, xp)
+        psi += Phi[s2] - Phi[s1]
+        out.append(s1)
+        alphas.append(alpha)
+        ths.append(a)
+    return np.array(out), np.array(alphas), np.array(ths)
+
+
+def test_kh_linear_kernel_matches_feature_space():
+    rng = np.random.default_rng(2)
+    N, d = 40, 3
+    K = rng.standard_normal((N, d))
+    V = rng.standard_normal((N, d))
+    u = rng.random(N // 2).astype(np.float32)
+    r = oracle.kernel_halving(K, V, np.arange(N), u, kernel="linear")
+    out, al, th = _kh_feature_space(np.hstack([K, V]), u)
+    assert np.array_equal(r["out"], out)
+    np.testing.assert_allclose(r["alpha"], al, rtol=1e-10, atol=1e-12)
+    np.testing.assert_allclose(r["thresh"], th, rtol=1e-12)
+
+
+def _katt_features(K, V, vmax, terms):
+    """Explicit features of kappa_att (eq. katt): the exponential factor by its
+    Taylor series over tensor powers, the value factor by [v, v_max]."""
+    N, d = K.shape
+    blocks = []
+    for n in range(terms):
+        scale = 1.0 / math.sqrt(math.factorial(n) * d ** (n / 2))
+        t = np.ones((N, 1))
+        for _ in range(n):
+            t = (t[:, :, None] * K[:, None, :]).reshape(N, -1)
+        blocks.append(t * scale)
+    fk = np.hstack(blocks)
+    fv = np.hstack([V, np.full((N, 1), vmax)])
+    return (fk[:, :, None] * fv[:, None, :]).reshape(N, -1)
+
+
+@pytest.mark.parametrize("d,terms,N", [(1, 40, 24), (2, 15, 12)])
+def test_kh_katt_matches_feature_space(d, terms, N):
+    rng = np.random.default_rng(3 + d)
+    K = rng.uniform(-0.8, 0.8, size=(N, d))
+    V = rng.standard_normal((N, d))
+    vmax = float(np.abs(V).max())
+    u = rng.random(N // 2).astype(np.float32)
+    r = oracle.kernel_halving(K, V, np.arange(N), u)
+    out, al, th = _kh_feature_space(_katt_features(K, V, vmax, terms), u)
+    assert np.array_equal(r["out"], out)
+    np.testing.assert_allclose(r["alpha"], al, rtol=1e-9, atol=1e-12)
+    np.testing.assert_allclose(r["thresh"], th, rtol=1e-12)
+
+
+def test_kh_incremental_pair_scores_match_literal_sums():
+    """The pair-score recursion the GPU uses (alpha_p += sgn_i E(i,p)) agrees
+    with the literal double sums of App. A, Algorithm A.1."""
+    rng = np.random.default_rng(5)
+    N, d = 64, 6
+    K = rng.standard_normal((N, d)) * 0.6
+    V = rng.standard_normal((N, d))
+    vm2 = float(np.abs(V).max() ** 2)
+    u = rng.random(N // 2).astype(np.float32)
+    G = np.exp(K @ K.T / math.sqrt(d)) * (V @ V.T + vm2)
+    r = oracle.kernel_halving(K, V, np.arange(N), u)
+    P = N // 2
+    alpha = np.zeros(P)
+    for i in range(P):
+        x, xp = 2 * i, 2 * i + 1
+        np.testing.assert_allclose(alpha[i], r["alpha"][i], rtol=1e-10, atol=1e-9)
+        sgn = -1.0 if r["bits"][i] else 1.0
+        for p in range(i + 1, P):
+            y, yp = 2 * p, 2 * p + 1
+            E = G[xp, y] - G[x, y] - G[xp, yp] + G[x, yp]
+            alpha[p] += sgn * E
+
+
+def _mmd2(G, keep):
+    N = G.shape[0]
+    w = np.full(N, 1.0 / N)
+    w[keep] -= 2.0 / N
+    return float(w @ G @ w)
+
+
+def test_kh_balances_far_better_than_uniform_halving():
+    """Sec. 2.1: KH balances the two halves far better than uniform halving.
+    In one dimension with the linear kernel the signed sum psi = sum_S2 x -
+    sum_S1 x is a self-balancing walk; a wrong sign anywhere in the score or
+    the swap rule turns it into an anti-balancing walk."""
+    rng = np.random.default_rng(6)
+    N = 1024
+    kh, uni = [], []
+    for _ in range(20):
+        K = rng.standard_normal((N, 1))
+        V = np.zeros((N, 1))
+        u = rng.random(N // 2).astype(np.float32)
+        out = oracle.kernel_halving(K, V, np.arange(N), u, kernel="linear")["out"]
+        w = np.ones(N)
+        w[out] -= 2.0
+        kh.append(float(w @ K[:, 0]) ** 2)
+        keep = np.arange(0, N, 2) + (rng.random(N // 2) < 0.5)
+        w = np.ones(N)
+        w[keep] -= 2.0
+        uni.append(float(w @ K[:, 0]) ** 2)
+    assert np.mean(kh) * 10 < np.mean(uni)
+
+
+def test_kh_katt_coreset_beats_uniform_halving_on_average():
+    rng = np.random.default_rng(6)
+    N, d = 512, 2
+    kh, uni = [], []
+    for _ in range(20):
+        K = rng.standard_normal((N, d)) * 0.5
+        V = rng.standard_normal((N, d))
+        vm2 = float(np.abs(V).max() ** 2)
+        G = np.exp(K @ K.T / math.sqrt(d)) * (V @ V.T + vm2)
+        u = rng.random(N // 2).astype(np.float32)
+        kh.append(_mmd2(G, oracle.kernel_halving(K, V, np.arange(N), u)["out"]))
+        uni.append(_mmd2(G, np.arange(0, N, 2) + (rng.random(N // 2) < 0.5)))
+    assert np.mean(kh) * 1.5 < np.mean(uni)
+
+
+def test_kh_value_scaling_leaves_decisions_unchanged():
+    """V -> cV multiplies every kappa_att value by c^2 (v_max scales too), so
+    every ratio alpha/a and hence every decision is unchanged."""
+    rng = np.random.default_rng(7)
+    N, d = 48, 5
+    K = rng.standard_normal((N, d))
+    V = rng.standard_normal((N, d))
+    u = rng.random(N // 2).astype(np.float32)
+    r1 = oracle.kernel_halving(K, V, np.arange(N), u)
+    r2 = oracle.kernel_halving(K, 4.0 * V, np.arange(N), u)
+    assert np.array_equal(r1["out"], r2["out"])
+    np.testing.assert_allclose(r2["alpha"], 16 * r1["alpha"], rtol=1e-12, atol=1e-300)
+
+
+# ---------------------------------------------------------------------------
+# Compress level structure
+# ---------------------------------------------------------------------------
+def test_plan_uniform_counts_for_the_five_workloads():
+    # n_kept - n_out halving draws, plus n_kept subsample draws when n_kept < n
+    assert oracle.plan(1024, 32, 2)["uniforms"] == 992
+    assert oracle.plan(3136, 64, 2)["uniforms"] == 2048 + 1984
+    assert oracle.plan(1024, 64, 3)["uniforms"] == 960
+    assert oracle.plan(16384, 128, 3)["uniforms"] == 16256
+    assert oracle.plan(65536, 256, 4)["uniforms"] == 65280
+
+
+def _bucket_sizes_from_trace(res, n_kept, n_out, subsample):
+    """Bucket boundaries are where the score is exactly zero (first pair of a
+    KH call): there rho = 0 - (1 - 2u) exactly."""
+    U = res["U"]
+    rho = res["rho"]
+    off = n_kept if subsample else 0
+    rounds = []
+    n_r = n_kept
+    while n_r > n_out:
+        seg = slice(off, off + n_r // 2)
+        zero = rho[seg] == 0.0 - (1.0 - 2.0 * U[seg].astype(np.float64))
+        starts = np.flatnonzero(zero)
+        sizes = 2 * np.diff(np.append(starts, n_r // 2))
+        rounds.append(list(sizes))
+        off += n_r // 2
+        n_r //= 2
+    return rounds
+
+
+def _run_compress(n, n_out, g, d=3, seed=0):
+    rng = np.random.default_rng(seed)
+    K = rng.standard_normal((n, d))
+    V = rng.standard_normal((n, d))
+    pl = oracle.plan(n, n_out, g)
+    U = rng.random(pl["uniforms"]).astype(np.float32)
+    res = oracle.compress(K, V, n_out, g, U)
+    res["U"] = U
+    return res, pl
+
+
+def test_compress2_bucket_counts_match_theorem1_runtime_sum():
+    """Thm 1: Compress2(m, 2^m n_out) runs 4^j Halve calls on 2^(1-j) n_out
+    points, j = 0..m-1 (g = 0: no trailing halvings)."""
+    m, n_out = 3, 16
+    res, pl = _run_compress(n_out * 2 ** m, n_out, 0)
+    rounds = _bucket_sizes_from_trace(res, pl["n_kept"], n_out, False)
+    got = sorted(s for r in rounds for s in r)
+    want = sorted([int(2 ** (1 - j) * n_out) for j in range(m) for _ in range(4 ** j)])
+    assert got == want
+
+
+def _shetty_compress_calls(n, g):
+    """Halving-call sizes of Compress with oversampling g (base case 4^g
+    points returned as they are), followed by g halvings to sqrt(n)."""
+    calls = []
+
+    def comp(size):
+        if size <= 4 ** g:
+            return size
+        out = sum(comp(size // 4) for _ in range(4))
+        calls.append(out)
+        return out // 2
+
+    top = comp(n)
+    while top > math.isqrt(n):
+        calls.append(top)
+        top //= 2
+    return calls
+
+
+@pytest.mark.parametrize("k,g", [(5, 2), (4, 1), (5, 0), (3, 3), (6, 2)])
+def test_compress_matches_recursive_compress_with_oversampling(k, g):
+    n = 4 ** k
+    n_out = 2 ** k
+    res, pl = _run_compress(n, n_out, g, seed=k + g)
+    rounds = _bucket_sizes_from_trace(res, n, n_out, False)
+    got = sorted(s for r in rounds for s in r)
+    assert got == sorted(_shetty_compress_calls(n, g))
+    if g < k:
+        assert rounds[0][0] == 4 ** (g + 1)
+
+
+def test_compress_output_size_order_and_identity_case():
+    res, _ = _run_compress(3000, 40, 2)
+    idx = res["idx"]
+    assert idx.size == 40 and np.all(np.diff(idx) > 0) and idx.min() >= 0 and idx.max() < 3000
+    res, pl = _run_compress(96, 96, 3)
+    assert pl["rounds"] == 0 and np.array_equal(res["idx"], np.arange(96))
+
+
+def test_plan_rejects_buckets_below_two_rows():
+    assert oracle.plan(1024, 1, 0) is None       # 4^9 groups of a 1024-row input
+    assert oracle.plan(10, 11, 1) is None
+    assert oracle.plan(1024, 1, 4) is None       # groups of one row
+    assert oracle.plan(1024, 1, 5) is not None   # groups of four rows
+
+
+# ---------------------------------------------------------------------------
+# Stratified subsample
+# ---------------------------------------------------------------------------
+def test_subsample_equal_groups_is_offline_subsample():
+    """Algorithm H.1: one uniform draw from each group of 2^k consecutive points."""
+    rng = np.random.default_rng(8)
+    n_kept, k = 100, 3
+    u = rng.integers(0, 2 ** 24, size=n_kept) * 2.0 ** -24
+    out = oracle.subsample(n_kept * 2 ** k, n_kept, u.astype(np.float32))
+    t = np.arange(n_kept)
+    assert np.array_equal(out, t * 2 ** k + np.floor(u * 2 ** k).astype(np.int64))
+
+
+def test_subsample_unequal_strata_cover_and_are_uniform():
+    n, n_kept = 3136, 2048
+    u = np.zeros(n_kept, np.float32)
+    lo = oracle.subsample(n, n_kept, u)
+    hi = oracle.subsample(n, n_kept, np.full(n_kept, 1 - 2 ** -24, np.float32))
+    # first/last element of each stratum; strata tile [0, n)
+    assert lo[0] == 0 and hi[-1] == n - 1
+    assert np.array_equal(lo[1:], hi[:-1] + 1)
+    assert set(np.unique(hi - lo + 1)) == {1, 2}
+    # uniformity within a stratum of length 2: half of the u-grid picks each
+    grid = (np.arange(1 << 12) * 2.0 ** -12).astype(np.float32)
+    s = int(np.flatnonzero(hi - lo == 1)[0])
+    picks = [oracle.subsample(n, n_kept, np.full(n_kept, g, np.float32))[s] for g in grid[::64]]
+    assert np.bincount(np.array(picks) - lo[s]).tolist() == [32, 32]
+
+
+def test_vmax2_is_max_abs_squared():
+    rng = np.random.default_rng(9)
+    V = rng.standard_normal((77, 13))
+    assert oracle.vmax2(V) == np.abs(V).max() ** 2
+
+
+# ---------------------------------------------------------------------------
+# Attention
+# ---------------------------------------------------------------------------
+def test_exact_attention_matches_library_sdpa():
+    rng = np.random.default_rng(10)
+    Q = rng.standard_normal((37, 16))
+    K = rng.standard_normal((53, 16))
+    V = rng.standard_normal((53, 16))
+    O = oracle.exact_attention(Q, K, V)
+    ref = torch.nn.functional.scaled_dot_product_attention(
+        torch.from_numpy(Q)[None], torch.from_numpy(K)[None], torch.from_numpy(V)[None])[0]
+    np.testing.assert_allclose(O, ref.numpy(), rtol=1e-12, atol=1e-13)
+
+
+def test_attention_over_one_key_returns_its_value():
+    rng = np.random.default_rng(11)
+    Q = rng.standard_normal((5, 8)) * 10
+    K = rng.standard_normal((9, 8))
+    V = rng.standard_normal((9, 8))
+    O = oracle.attention(Q, K, V, [4])
+    assert np.array_equal(O, np.repeat(V[4:5], 5, axis=0))
+
+
+def test_attention_invariant_to_a_common_key_shift():
+    rng = np.random.default_rng(12)
+    Q = rng.standard_normal((6, 8))
+    K = rng.standard_normal((20, 8))
+    V = rng.standard_normal((20, 8))
+    rows = [1, 3, 4, 9, 15]
+    O1 = oracle.attention(Q, K, V, rows)
+    O2 = oracle.attention(Q, K + rng.standard_normal(8) * 3, V, rows)
+    np.testing.assert_allclose(O1, O2, rtol=1e-11, atol=1e-12)
+
+
+def test_thinned_attention_with_nout_equal_n_is_exact_attention():
+    rng = np.random.default_rng(13)
+    n, d = 64, 8
+    Q, K, V = (rng.standard_normal((n, d)) for _ in range(3))
+    res = oracle.compress(K, V, n, 2, np.zeros(1, np.float32))
+    assert np.array_equal(oracle.attention(Q, K, V, res["idx"]), oracle.exact_attention(Q, K, V))
+
+
+def test_attention_value_scaling_is_linear():
+    rng = np.random.default_rng(14)
+    Q, K, V = (rng.standard_normal((30, 8)) for _ in range(3))
+    rows = np.arange(0, 30, 3)
+    np.testing.assert_array_equal(oracle.attention(Q, K, 2 * V, rows),
+                                  2 * oracle.attention(Q, K, V, rows))

@@ -1,0 +1,152 @@
+/*
+ * thin -- thinned attention on AMD Instinct MI355X (gfx950).
+ *
+ * C ABI of the non-causal thinning path of "Express Language Modeling":
+ * for every (batch, head) slice, kernel halving (KH) under the attention
+ * kernel kappa_att thins the n key/value rows to n_out coreset rows
+ * (thin_compress), then every query attends over the coreset only
+ * (thin_attention).
+ *
+ * Conventions shared by every entry point
+ *   - Tensors are contiguous row-major [B, H, rows, d] (d fastest); the slice
+ *     s = b*H + h owns rows [s*rows, (s+1)*rows).  K and V have n rows, Q and
+ *     O have n_q rows.
+ *   - Pointers marked (device) are HIP device pointers; (host) are host
+ *     pointers.  The caller owns every buffer; the library allocates nothing
+ *     and keeps no state between calls.
+ *   - `stream` is a hipStream_t (NULL = the default stream).  Work is enqueued
+ *     asynchronously; nothing synchronises.  Calls on one stream are ordered.
+ *   - Arguments are validated on the host before anything is enqueued.  On any
+ *     error nothing is launched and no output is written.  THIN_EHIP reports a
+ *     launch error; faults inside a kernel surface at the caller's next
+ *     synchronisation.
+ *   - Supported: dtype THIN_FP32 or THIN_BF16 (Q, K, V share it), d in
+ *     {32, 64, 128}.
+ */
+#ifndef THIN_H
+#define THIN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  THIN_OK = 0,
+  THIN_EINVAL = 1,     /* bad size, pointer, or no valid level structure   */
+  THIN_EDTYPE = 2,     /* unsupported dtype / output dtype                  */
+  THIN_EUNIFORMS = 3,  /* uniforms buffer shorter than the plan requires    */
+  THIN_EWORKSPACE = 4, /* workspace missing or smaller than the plan's size */
+  THIN_EHIP = 5        /* the HIP runtime reported an error                 */
+} thin_status_t;
+
+typedef enum { THIN_FP32 = 0, THIN_BF16 = 1 } thin_dtype_t;
+
+/*
+ * Level structure of one compress call (identical for every slice).
+ *
+ * Reading of the output size n_out and the oversampling parameter g
+ * (Sec. 3.1; App. H, Algorithm H.2 Offline-Compress2; Alg. 1's final
+ * Halve(Halve(.))): L = floor(log2(n / n_out)) halving rounds take
+ * n_kept = n_out * 2^L rows to n_out.  If n_kept < n a stratified subsample
+ * (one uniform draw per contiguous stratum; Alg. 3 / Algorithm H.1) keeps
+ * n_kept rows first.  Round r = 0..L-1 splits the current n_kept / 2^r rows
+ * of a slice into G_r = 4^max(L-g-1-r, 0) contiguous equal buckets and runs
+ * KH(1/2) (App. A, Algorithm A.1) on each: the first L - min(g, L) rounds are
+ * Offline-Compress2 with output size 2^g n_out, the rest halve the whole set.
+ * Every bucket must hold an even number >= 2 of rows.
+ */
+typedef struct {
+  int64_t n_kept;             /* rows entering round 0                        */
+  int32_t rounds;             /* L                                            */
+  int32_t compress_levels;    /* rounds with more than one bucket possible    */
+  int64_t uniforms_per_slice; /* U: uniforms one slice consumes               */
+  int64_t uniforms_total;     /* B * H * U                                    */
+  int64_t max_bucket;         /* largest bucket (rows) of any round           */
+  size_t workspace_bytes;     /* device workspace thin_compress needs         */
+} thin_plan_t;
+
+/*
+ * Plan a compress call.  Host-only; touches no device.
+ * Returns THIN_OK and fills *plan (host), or THIN_EINVAL when B, H, n, d,
+ * n_out, g are out of range (n_out < 1, n_out > n, g < 0, d unsupported) or
+ * when some bucket would hold fewer than two rows or an odd number of rows.
+ */
+int thin_plan(int64_t B, int64_t H, int64_t n, int64_t d, int64_t n_out, int32_t g,
+              thin_plan_t* plan);
+
+/*
+ * Compress every slice's key/value rows to n_out coreset rows.
+ *
+ *   K, V        (device) [B,H,n,d] of `dtype`.
+ *   uniforms    (device) float32 in [0,1), at least B*H*U of them, slice-major:
+ *               slice s reads [s*U, (s+1)*U).  Within a slice: first the
+ *               n_kept subsample draws (only when n_kept < n), then for each
+ *               round r the n_r/2 pair draws (n_r = n_kept / 2^r) in bucket
+ *               order, pair order within a bucket.  Pair i of a bucket swaps
+ *               iff u_i < min(1, (1 - alpha_i/a_i)_+ / 2) (App. A).
+ *               Values k * 2^-24 make every derived quantity exact.
+ *   idx_out     (device) int32 [B,H,n_out]: kept row indices in [0,n),
+ *               strictly increasing within a slice.
+ *   workspace   (device) at least plan.workspace_bytes bytes, 256-byte
+ *               aligned; contents on entry are irrelevant.
+ *
+ * kappa_att((k,v),(k',v')) = exp(<k,k'>/sqrt(d)) (<v,v'> + v_max^2) with
+ * v_max = max over all n rows of ||v||_inf (Sec. 2.1, eq. katt); delta = 1/2
+ * (App. I).  With n_out == n the result is 0..n-1.
+ * Errors: THIN_EINVAL (sizes / null pointers / no level structure),
+ * THIN_EDTYPE, THIN_EUNIFORMS (n_uniforms < plan.uniforms_total),
+ * THIN_EWORKSPACE, THIN_EHIP.
+ */
+int thin_compress(const void* K, const void* V, int32_t dtype, int64_t B, int64_t H, int64_t n,
+                  int64_t d, int64_t n_out, int32_t g, const float* uniforms,
+                  int64_t n_uniforms, int32_t* idx_out, void* workspace,
+                  size_t workspace_bytes, void* stream);
+
+/*
+ * thin_compress plus a record of every swap decision, for checking a run
+ * against a reference implementation.
+ *   swap_trace  (device) uint8 [B*H*U], indexed exactly like `uniforms`:
+ *               1 if that pair swapped, 0 otherwise; the subsample entries
+ *               are written as 0.  trace_len must be >= B*H*U (THIN_EINVAL).
+ */
+int thin_compress_traced(const void* K, const void* V, int32_t dtype, int64_t B, int64_t H,
+                         int64_t n, int64_t d, int64_t n_out, int32_t g,
+                         const float* uniforms, int64_t n_uniforms, int32_t* idx_out,
+                         void* workspace, size_t workspace_bytes, uint8_t* swap_trace,
+                         int64_t trace_len, void* stream);
+
+/*
+ * Attention of every query over its slice's coreset (Sec. 2.1 eq.
+ * unmaskedatt restricted to the coreset; eq. def:att_approx with equal
+ * weights, which cancel):
+ *   O[s,q,:] = sum_j exp(<Q[s,q],K[s,I_j]>/sqrt d) V[s,I_j] / sum_j exp(...)
+ * with I = idx[s, 0..n_out).
+ *   Q           (device) [B,H,n_q,d] of `dtype`;  K, V (device) [B,H,n,d].
+ *   idx         (device) int32 [B,H,n_out], every entry in [0,n) (entries
+ *               outside are clamped to the nearest row; duplicates allowed).
+ *   O           (device) [B,H,n_q,d] of `out_dtype` (THIN_FP32 or THIN_BF16).
+ * Scores and the softmax are accumulated in float32.
+ * Errors: THIN_EINVAL, THIN_EDTYPE, THIN_EHIP.
+ */
+int thin_attention(const void* Q, const void* K, const void* V, int32_t dtype, int64_t B,
+                   int64_t H, int64_t n_q, int64_t n, int64_t d, const int32_t* idx,
+                   int64_t n_out, void* O, int32_t out_dtype, void* stream);
+
+/*
+ * Diagnostic: out[m*16 + n] = <rows[m], rows[16 + n]> for m, n < 16, computed
+ * through the MFMA row-fragment path the halving kernel uses.
+ *   rows (device) [32, d] of `dtype`;  out (device) float32 [16, 16].
+ * Errors: THIN_EINVAL, THIN_EDTYPE, THIN_EHIP.
+ */
+int thin_selftest_gram16(int32_t dtype, int64_t d, const void* rows, float* out, void* stream);
+
+/* Static, human-readable text for a status code. */
+const char* thin_status_str(int status);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* THIN_H */

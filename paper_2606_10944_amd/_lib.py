@@ -1,0 +1,171 @@
+"""ctypes binding of libthin.so (see include/thin.h).
+
+Argument marshalling only: every step of the path runs in the HIP library.
+Tensors are PyTorch tensors on the GPU (PyTorch provides device memory and the
+current HIP stream).  The library must have been built (``__graft_entry__.
+build()`` or ``python paper_2606_10944_amd/build.py``); importing works without
+it, but every call fails loudly if it is missing.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+from typing import Optional, Tuple
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libthin.so")
+
+THIN_OK, THIN_EINVAL, THIN_EDTYPE, THIN_EUNIFORMS, THIN_EWORKSPACE, THIN_EHIP = range(6)
+THIN_FP32, THIN_BF16 = 0, 1
+
+# Every symbol include/thin.h declares.
+EXPORTS = ("thin_plan", "thin_compress", "thin_compress_traced", "thin_attention",
+           "thin_selftest_gram16", "thin_status_str")
+
+
+class ThinError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        self.status = status
+        super().__init__(f"{where}: {thin_status_str(status)} (status {status})")
+
+
+class Plan(C.Structure):
+    _fields_ = [
+        ("n_kept", C.c_int64),
+        ("rounds", C.c_int32),
+        ("compress_levels", C.c_int32),
+        ("uniforms_per_slice", C.c_int64),
+        ("uniforms_total", C.c_int64),
+        ("max_bucket", C.c_int64),
+        ("workspace_bytes", C.c_size_t),
+    ]
+
+
+_lib = None
+
+
+def lib():
+    """Load libthin.so; raises if it has not been built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(f"{LIB_PATH} is missing: build it with __graft_entry__.build()")
+    L = C.CDLL(LIB_PATH)
+    P, I64, I32, SZ = C.c_void_p, C.c_int64, C.c_int32, C.c_size_t
+    L.thin_plan.argtypes = [I64, I64, I64, I64, I64, I32, C.POINTER(Plan)]
+    L.thin_compress.argtypes = [P, P, I32, I64, I64, I64, I64, I64, I32, P, I64, P, P, SZ, P]
+    L.thin_compress_traced.argtypes = [P, P, I32, I64, I64, I64, I64, I64, I32, P, I64, P, P,
+                                       SZ, P, I64, P]
+    L.thin_attention.argtypes = [P, P, P, I32, I64, I64, I64, I64, I64, P, I64, P, I32, P]
+    L.thin_selftest_gram16.argtypes = [I32, I64, P, P, P]
+    L.thin_status_str.argtypes = [C.c_int]
+    L.thin_status_str.restype = C.c_char_p
+    for f in ("thin_plan", "thin_compress", "thin_compress_traced", "thin_attention",
+              "thin_selftest_gram16"):
+        getattr(L, f).restype = C.c_int
+    _lib = L
+    return L
+
+
+def thin_status_str(status: int) -> str:
+    return lib().thin_status_str(int(status)).decode()
+
+
+def _dtype_code(t: torch.dtype) -> int:
+    if t == torch.float32:
+        return THIN_FP32
+    if t == torch.bfloat16:
+        return THIN_BF16
+    raise ThinError(THIN_EDTYPE, f"dtype {t}")
+
+
+def _ptr(t: Optional[torch.Tensor]):
+    return None if t is None else C.c_void_p(t.data_ptr())
+
+
+def _stream(stream) -> C.c_void_p:
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return C.c_void_p(stream.cuda_stream)
+
+
+def _check(rc: int, where: str):
+    if rc != THIN_OK:
+        raise ThinError(rc, where)
+
+
+def thin_plan(B: int, H: int, n: int, d: int, n_out: int, g: int) -> dict:
+    p = Plan()
+    _check(lib().thin_plan(B, H, n, d, n_out, g, C.byref(p)), "thin_plan")
+    return {k: getattr(p, k) for k, _ in Plan._fields_}
+
+
+def _shape4(t: torch.Tensor, name: str) -> Tuple[int, int, int, int]:
+    if t.dim() != 4 or not t.is_contiguous():
+        raise ThinError(THIN_EINVAL, f"{name} must be a contiguous [B,H,rows,d] tensor")
+    return tuple(t.shape)
+
+
+def thin_compress(K: torch.Tensor, V: torch.Tensor, n_out: int, g: int,
+                  uniforms: torch.Tensor, *, idx_out: Optional[torch.Tensor] = None,
+                  workspace: Optional[torch.Tensor] = None, trace: bool = False,
+                  stream=None):
+    """Kernel-halving compress of every slice; returns idx [B,H,n_out] int32
+    (and the uint8 swap trace when trace=True)."""
+    B, H, n, d = _shape4(K, "K")
+    if tuple(V.shape) != (B, H, n, d) or V.dtype != K.dtype or not V.is_contiguous():
+        raise ThinError(THIN_EINVAL, "V must match K")
+    if uniforms.dtype != torch.float32 or not uniforms.is_contiguous():
+        raise ThinError(THIN_EINVAL, "uniforms must be contiguous float32")
+    plan = thin_plan(B, H, n, d, n_out, g)
+    dev = K.device
+    if idx_out is None:
+        idx_out = torch.empty((B, H, n_out), dtype=torch.int32, device=dev)
+    if workspace is None:
+        workspace = torch.empty(max(plan["workspace_bytes"], 256), dtype=torch.uint8, device=dev)
+    tr = None
+    args = [_ptr(K), _ptr(V), _dtype_code(K.dtype), B, H, n, d, n_out, g, _ptr(uniforms),
+            uniforms.numel(), _ptr(idx_out), _ptr(workspace), workspace.numel()]
+    if trace:
+        tr = torch.empty(max(plan["uniforms_total"], 1), dtype=torch.uint8, device=dev)
+        rc = lib().thin_compress_traced(*args, _ptr(tr), tr.numel(), _stream(stream))
+        _check(rc, "thin_compress_traced")
+        return idx_out, tr[: plan["uniforms_total"]]
+    _check(lib().thin_compress(*args, _stream(stream)), "thin_compress")
+    return idx_out
+
+
+def thin_attention(Q: torch.Tensor, K: torch.Tensor, V: torch.Tensor, idx: torch.Tensor, *,
+                   out_dtype: torch.dtype = torch.float32, O: Optional[torch.Tensor] = None,
+                   stream=None) -> torch.Tensor:
+    """Attention of every query over its slice's coreset rows idx[b,h,:]."""
+    B, H, n_q, d = _shape4(Q, "Q")
+    Bk, Hk, n, dk = _shape4(K, "K")
+    if (Bk, Hk, dk) != (B, H, d) or tuple(V.shape) != tuple(K.shape):
+        raise ThinError(THIN_EINVAL, "Q/K/V shapes disagree")
+    if K.dtype != Q.dtype or V.dtype != Q.dtype:
+        raise ThinError(THIN_EDTYPE, "Q, K, V must share a dtype")
+    if idx.dtype != torch.int32 or idx.dim() != 3 or tuple(idx.shape[:2]) != (B, H):
+        raise ThinError(THIN_EINVAL, "idx must be int32 [B,H,n_out]")
+    idx = idx.contiguous()
+    n_out = idx.shape[2]
+    if O is None:
+        O = torch.empty((B, H, n_q, d), dtype=out_dtype, device=Q.device)
+    rc = lib().thin_attention(_ptr(Q), _ptr(K), _ptr(V), _dtype_code(Q.dtype), B, H, n_q, n, d,
+                              _ptr(idx), n_out, _ptr(O), _dtype_code(O.dtype), _stream(stream))
+    _check(rc, "thin_attention")
+    return O
+
+
+def thin_selftest_gram16(rows: torch.Tensor, stream=None) -> torch.Tensor:
+    """<rows[m], rows[16+n]> for m, n < 16 through the MFMA fragment path."""
+    if rows.dim() != 2 or rows.shape[0] != 32 or not rows.is_contiguous():
+        raise ThinError(THIN_EINVAL, "rows must be a contiguous [32, d] tensor")
+    out = torch.empty((16, 16), dtype=torch.float32, device=rows.device)
+    rc = lib().thin_selftest_gram16(_dtype_code(rows.dtype), rows.shape[1], _ptr(rows),
+                                    _ptr(out), _stream(stream))
+    _check(rc, "thin_selftest_gram16")
+    return out

@@ -1,0 +1,224 @@
+// C ABI of the thinning library: planning, argument validation and the
+// level-synchronous launch sequence of the compress path.
+#include <math.h>
+#include <stdint.h>
+#include <string.h>
+
+#include "../../include/thin.h"
+#include "launch.hpp"
+
+namespace {
+
+constexpr int64_t kMaxBucket = 16384;  // per-pair state of a bucket lives in LDS
+constexpr int64_t kMaxRows = (int64_t)1 << 30;
+
+struct Levels {
+  int64_t n_kept = 0;
+  int32_t L = 0;
+  int32_t mc = 0;
+  bool sub = false;
+  int64_t U = 0;
+  int64_t n_r[64];
+  int64_t G[64];
+  int64_t N[64];
+  int64_t max_bucket = 0;
+};
+
+size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+bool supported_d(int64_t d) { return d == 32 || d == 64 || d == 128; }
+
+// Integer planning of one compress call; false if no valid level structure.
+bool make_levels(int64_t n, int64_t n_out, int32_t g, Levels* lv) {
+  if (n < 1 || n > kMaxRows || n_out < 1 || n_out > n || g < 0) return false;
+  int32_t L = 0;
+  while ((n_out << (L + 1)) <= n) ++L;
+  lv->L = L;
+  lv->n_kept = n_out << L;
+  lv->sub = lv->n_kept < n;
+  lv->mc = L - (g < L ? g : L);
+  lv->U = (lv->sub ? lv->n_kept : 0) + (lv->n_kept - n_out);
+  lv->max_bucket = 0;
+  for (int32_t r = 0; r < L; ++r) {
+    const int64_t n_r = lv->n_kept >> r;
+    const int32_t e = L - g - 1 - r;
+    const int64_t G = e > 0 ? ((int64_t)1 << (2 * e)) : 1;
+    if (n_r % G != 0) return false;
+    const int64_t N = n_r / G;
+    if (N < 2 || (N & 1)) return false;
+    lv->n_r[r] = n_r;
+    lv->G[r] = G;
+    lv->N[r] = N;
+    if (N > lv->max_bucket) lv->max_bucket = N;
+  }
+  return true;
+}
+
+struct Workspace {
+  uint32_t* vmax_bits;
+  int32_t* buf_a;  // [S, n_kept]
+  int32_t* buf_b;  // [S, n_kept / 2]
+  size_t bytes;
+};
+
+size_t workspace_size(int64_t S, int64_t n_kept) {
+  return align256((size_t)S * 4) + align256((size_t)S * (size_t)n_kept * 4) +
+         align256((size_t)S * (size_t)(n_kept / 2) * 4);
+}
+
+Workspace carve(void* base, int64_t S, int64_t n_kept) {
+  Workspace w;
+  unsigned char* p = static_cast<unsigned char*>(base);
+  size_t off = 0;
+  w.vmax_bits = reinterpret_cast<uint32_t*>(p + off);
+  off += align256((size_t)S * 4);
+  w.buf_a = reinterpret_cast<int32_t*>(p + off);
+  off += align256((size_t)S * (size_t)n_kept * 4);
+  w.buf_b = reinterpret_cast<int32_t*>(p + off);
+  off += align256((size_t)S * (size_t)(n_kept / 2) * 4);
+  w.bytes = off;
+  return w;
+}
+
+int check_shape(int64_t B, int64_t H, int64_t n, int64_t d) {
+  if (B < 1 || H < 1 || n < 1 || n > kMaxRows) return THIN_EINVAL;
+  if (B * H > ((int64_t)1 << 31)) return THIN_EINVAL;
+  if (!supported_d(d)) return THIN_EINVAL;
+  return THIN_OK;
+}
+
+int compress_impl(const void* K, const void* V, int32_t dtype, int64_t B, int64_t H, int64_t n,
+                  int64_t d, int64_t n_out, int32_t g, const float* uniforms, int64_t n_uniforms,
+                  int32_t* idx_out, void* workspace, size_t workspace_bytes, uint8_t* trace,
+                  int64_t trace_len, void* stream) {
+  int rc = check_shape(B, H, n, d);
+  if (rc) return rc;
+  if (dtype != THIN_FP32 && dtype != THIN_BF16) return THIN_EDTYPE;
+  Levels lv;
+  if (!make_levels(n, n_out, g, &lv) || lv.max_bucket > kMaxBucket) return THIN_EINVAL;
+  if (!K || !V || !idx_out) return THIN_EINVAL;
+  const int64_t S = B * H;
+  const int64_t Utot = S * lv.U;
+  if (Utot > 0 && !uniforms) return THIN_EINVAL;
+  if (n_uniforms < Utot) return THIN_EUNIFORMS;
+  if (trace && trace_len < Utot) return THIN_EINVAL;
+  if (!workspace || workspace_bytes < workspace_size(S, lv.n_kept)) return THIN_EWORKSPACE;
+  if ((reinterpret_cast<uintptr_t>(workspace) & 255u) != 0) return THIN_EWORKSPACE;
+  Workspace ws = carve(workspace, S, lv.n_kept);
+  hipStream_t st = static_cast<hipStream_t>(stream);
+
+  hipError_t e = hipSuccess;
+  auto ok = [&](hipError_t x) {
+    if (x != hipSuccess && e == hipSuccess) e = x;
+    return e == hipSuccess;
+  };
+  if (trace) ok(thin::launch_zero_u8(trace, Utot, st));
+  if (lv.sub) ok(thin::launch_subsample(S, n, lv.n_kept, uniforms, lv.U, ws.buf_a, st));
+  const int32_t* cur = lv.sub ? ws.buf_a : nullptr;
+  if (lv.L == 0) {
+    ok(thin::launch_fill_rows(S, n_out, cur, lv.n_kept, idx_out, st));
+  } else {
+    ok(thin::launch_vmax(dtype, V, S, n, d, ws.vmax_bits, st));
+    int64_t u_off = lv.sub ? lv.n_kept : 0;
+    for (int32_t r = 0; r < lv.L && e == hipSuccess; ++r) {
+      int32_t* out = (r == lv.L - 1) ? idx_out : (cur == ws.buf_b ? ws.buf_a : ws.buf_b);
+      thin::HalveArgs a;
+      a.K = K;
+      a.V = V;
+      a.n = n;
+      a.vmax_bits = ws.vmax_bits;
+      a.idx_in = cur;
+      a.n_r = lv.n_r[r];
+      a.N = (int32_t)lv.N[r];
+      a.G = (int32_t)lv.G[r];
+      a.S = S;
+      a.idx_out = out;
+      a.U = uniforms;
+      a.u_slice = lv.U;
+      a.u_off = u_off;
+      a.trace = trace;
+      a.log_c = log(0.5 + log(2.0 * (double)lv.N[r] / 0.5));
+      ok(thin::launch_halve(dtype, d, a, st));
+      u_off += lv.n_r[r] / 2;
+      cur = out;
+    }
+  }
+  return e == hipSuccess ? THIN_OK : THIN_EHIP;
+}
+
+}  // namespace
+
+extern "C" {
+
+int thin_plan(int64_t B, int64_t H, int64_t n, int64_t d, int64_t n_out, int32_t g,
+              thin_plan_t* plan) {
+  if (!plan) return THIN_EINVAL;
+  int rc = check_shape(B, H, n, d);
+  if (rc) return rc;
+  Levels lv;
+  if (!make_levels(n, n_out, g, &lv) || lv.max_bucket > kMaxBucket) return THIN_EINVAL;
+  const int64_t S = B * H;
+  memset(plan, 0, sizeof(*plan));
+  plan->n_kept = lv.n_kept;
+  plan->rounds = lv.L;
+  plan->compress_levels = lv.mc;
+  plan->uniforms_per_slice = lv.U;
+  plan->uniforms_total = S * lv.U;
+  plan->max_bucket = lv.max_bucket;
+  plan->workspace_bytes = workspace_size(S, lv.n_kept);
+  return THIN_OK;
+}
+
+int thin_compress(const void* K, const void* V, int32_t dtype, int64_t B, int64_t H, int64_t n,
+                  int64_t d, int64_t n_out, int32_t g, const float* uniforms,
+                  int64_t n_uniforms, int32_t* idx_out, void* workspace,
+                  size_t workspace_bytes, void* stream) {
+  return compress_impl(K, V, dtype, B, H, n, d, n_out, g, uniforms, n_uniforms, idx_out,
+                       workspace, workspace_bytes, nullptr, 0, stream);
+}
+
+int thin_compress_traced(const void* K, const void* V, int32_t dtype, int64_t B, int64_t H,
+                         int64_t n, int64_t d, int64_t n_out, int32_t g,
+                         const float* uniforms, int64_t n_uniforms, int32_t* idx_out,
+                         void* workspace, size_t workspace_bytes, uint8_t* swap_trace,
+                         int64_t trace_len, void* stream) {
+  if (!swap_trace) return THIN_EINVAL;
+  return compress_impl(K, V, dtype, B, H, n, d, n_out, g, uniforms, n_uniforms, idx_out,
+                       workspace, workspace_bytes, swap_trace, trace_len, stream);
+}
+
+int thin_attention(const void* Q, const void* K, const void* V, int32_t dtype, int64_t B,
+                   int64_t H, int64_t n_q, int64_t n, int64_t d, const int32_t* idx,
+                   int64_t n_out, void* O, int32_t out_dtype, void* stream) {
+  int rc = check_shape(B, H, n, d);
+  if (rc) return rc;
+  if (n_q < 1 || n_q > kMaxRows || n_out < 1 || n_out > ((int64_t)1 << 30)) return THIN_EINVAL;
+  if (dtype != THIN_FP32 && dtype != THIN_BF16) return THIN_EDTYPE;
+  if (out_dtype != THIN_FP32 && out_dtype != THIN_BF16) return THIN_EDTYPE;
+  if (!Q || !K || !V || !idx || !O) return THIN_EINVAL;
+  hipError_t e = thin::launch_attention(dtype, d, out_dtype, Q, K, V, idx, B * H, n, n_q, n_out,
+                                        O, static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? THIN_OK : THIN_EHIP;
+}
+
+int thin_selftest_gram16(int32_t dtype, int64_t d, const void* rows, float* out, void* stream) {
+  if (dtype != THIN_FP32 && dtype != THIN_BF16) return THIN_EDTYPE;
+  if (!supported_d(d)) return THIN_EINVAL;
+  if (!rows || !out) return THIN_EINVAL;
+  hipError_t e = thin::launch_gram16(dtype, d, rows, out, static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? THIN_OK : THIN_EHIP;
+}
+
+const char* thin_status_str(int status) {
+  switch (status) {
+    case THIN_OK: return "THIN_OK: success";
+    case THIN_EINVAL: return "THIN_EINVAL: invalid size, pointer or level structure";
+    case THIN_EDTYPE: return "THIN_EDTYPE: unsupported dtype";
+    case THIN_EUNIFORMS: return "THIN_EUNIFORMS: uniforms buffer too short";
+    case THIN_EWORKSPACE: return "THIN_EWORKSPACE: workspace missing, too small or misaligned";
+    case THIN_EHIP: return "THIN_EHIP: HIP runtime error";
+    default: return "THIN: unknown status";
+  }
+}
+
+}  // extern "C"

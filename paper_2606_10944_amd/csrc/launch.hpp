@@ -1,0 +1,45 @@
+// Host-side launchers of the thinning kernels (defined in the .hip files).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace thin {
+
+// One Halve round over all buckets of all slices.
+struct HalveArgs {
+  const void* K;
+  const void* V;
+  int64_t n;                  // rows per slice of K/V
+  const uint32_t* vmax_bits;  // [S] bit pattern of v_max (non-negative float)
+  const int32_t* idx_in;      // [S, n_r] rows entering this round, or null = identity
+  int64_t n_r;                // rows per slice entering this round
+  int32_t N;                  // bucket size (even, >= 2)
+  int32_t G;                  // buckets per slice
+  int64_t S;                  // slices
+  int32_t* idx_out;           // [S, n_r / 2]
+  const float* U;             // uniforms
+  int64_t u_slice;            // uniforms per slice
+  int64_t u_off;              // offset of this round's draws within a slice
+  uint8_t* trace;             // nullable, indexed like U
+  double log_c;               // log(1/2 + log(2N/delta))
+};
+
+// dtype: 0 = fp32, 1 = bf16.  Returns a hipError_t.
+hipError_t launch_vmax(int dtype, const void* V, int64_t S, int64_t n, int64_t d,
+                       uint32_t* vmax_bits, hipStream_t st);
+hipError_t launch_subsample(int64_t S, int64_t n, int64_t n_kept, const float* U,
+                            int64_t u_slice, int32_t* idx0, hipStream_t st);
+hipError_t launch_fill_rows(int64_t S, int64_t n_out, const int32_t* src, int64_t src_stride,
+                            int32_t* dst, hipStream_t st);
+hipError_t launch_zero_u8(uint8_t* p, int64_t count, hipStream_t st);
+hipError_t launch_halve(int dtype, int64_t d, const HalveArgs& a, hipStream_t st);
+size_t halve_lds_bytes(int dtype, int64_t d, int32_t N);
+
+hipError_t launch_attention(int dtype, int64_t d, int out_dtype, const void* Q, const void* K,
+                            const void* V, const int32_t* idx, int64_t S, int64_t n,
+                            int64_t n_q, int64_t n_out, void* O, hipStream_t st);
+
+hipError_t launch_gram16(int dtype, int64_t d, const void* rows, float* out, hipStream_t st);
+
+}  // namespace thin

@@ -1,0 +1,134 @@
+"""C-ABI library checks that need no GPU: it loads, exports every declared
+symbol, plans like the oracle, and rejects bad arguments before launching."""
+import ctypes as C
+import os
+import re
+
+import pytest
+
+import oracle
+from paper_2606_10944_amd import _lib
+from paper_2606_10944_amd import workloads as W
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+FAKE = C.c_void_p(0x10000)  # never dereferenced: every call below fails validation
+
+
+def _declared_symbols():
+    with open(os.path.join(ROOT, "include", "thin.h")) as f:
+        text = f.read()
+    return sorted(set(re.findall(r"^\s*(?:int|const char\*)\s+(thin_\w+)\(", text, re.M)))
+
+
+def test_library_exports_every_declared_symbol():
+    L = _lib.lib()
+    declared = _declared_symbols()
+    assert set(declared) == set(_lib.EXPORTS)
+    for name in declared:
+        assert hasattr(L, name), name
+
+
+def test_status_strings():
+    for s in range(6):
+        assert _lib.thin_status_str(s).startswith("THIN_")
+    assert "unknown" in _lib.thin_status_str(99)
+
+
+@pytest.mark.parametrize("n,n_out,g", [
+    (1024, 32, 2), (3136, 64, 2), (1024, 64, 3), (16384, 128, 3), (65536, 256, 4),
+    (1000, 7, 3), (96, 96, 1), (97, 48, 0), (5000, 40, 5), (2, 1, 0), (130, 64, 0),
+])
+def test_plan_agrees_with_oracle(n, n_out, g):
+    p = _lib.thin_plan(3, 2, n, 64, n_out, g)
+    o = oracle.plan(n, n_out, g)
+    assert o is not None
+    assert p["n_kept"] == o["n_kept"]
+    assert p["rounds"] == o["rounds"]
+    assert p["compress_levels"] == o["compress_levels"]
+    assert p["uniforms_per_slice"] == o["uniforms"]
+    assert p["uniforms_total"] == 6 * o["uniforms"]
+    assert p["workspace_bytes"] >= 6 * p["n_kept"] * 4
+
+
+@pytest.mark.parametrize("n,n_out,g", [(1024, 1, 0), (1024, 1, 4), (10, 11, 1), (10, 0, 1),
+                                       (10, 2, -1), (1000, 7, 2), (200, 3, 2)])
+def test_plan_rejects_what_the_oracle_rejects(n, n_out, g):
+    with pytest.raises(_lib.ThinError) as e:
+        _lib.thin_plan(1, 1, n, 64, n_out, g)
+    assert e.value.status == _lib.THIN_EINVAL
+    if n_out >= 1 and g >= 0:
+        assert oracle.plan(n, n_out, g) is None
+
+
+def test_plan_rejects_unsupported_head_dim_and_oversized_buckets():
+    for d in (16, 48, 256):
+        with pytest.raises(_lib.ThinError):
+            _lib.thin_plan(1, 1, 1024, d, 32, 2)
+    with pytest.raises(_lib.ThinError):           # one bucket of 32768 rows
+        _lib.thin_plan(1, 1, 65536, 64, 16384, 0)
+
+
+def _compress(**kw):
+    a = dict(K=FAKE, V=FAKE, dtype=1, B=1, H=2, n=1024, d=64, n_out=32, g=2, U=FAKE,
+             nU=2 * 992, idx=FAKE, ws=C.c_void_p(0x100000), wsb=1 << 20)
+    a.update(kw)
+    return _lib.lib().thin_compress(a["K"], a["V"], a["dtype"], a["B"], a["H"], a["n"], a["d"],
+                                    a["n_out"], a["g"], a["U"], a["nU"], a["idx"], a["ws"],
+                                    a["wsb"], None)
+
+
+def test_compress_validates_before_launch():
+    assert _compress(n_out=2000) == _lib.THIN_EINVAL
+    assert _compress(d=96) == _lib.THIN_EINVAL
+    assert _compress(K=None) == _lib.THIN_EINVAL
+    assert _compress(idx=None) == _lib.THIN_EINVAL
+    assert _compress(dtype=5) == _lib.THIN_EDTYPE
+    assert _compress(nU=2 * 992 - 1) == _lib.THIN_EUNIFORMS
+    assert _compress(U=None) == _lib.THIN_EINVAL
+    assert _compress(wsb=100) == _lib.THIN_EWORKSPACE
+    assert _compress(ws=None) == _lib.THIN_EWORKSPACE
+    assert _compress(ws=C.c_void_p(0x100010)) == _lib.THIN_EWORKSPACE   # misaligned
+    assert _compress(B=0) == _lib.THIN_EINVAL
+
+
+def test_traced_compress_checks_trace_length():
+    L = _lib.lib()
+    rc = L.thin_compress_traced(FAKE, FAKE, 1, 1, 1, 1024, 64, 32, 2, FAKE, 992, FAKE,
+                                C.c_void_p(0x100000), 1 << 20, FAKE, 991, None)
+    assert rc == _lib.THIN_EINVAL
+    rc = L.thin_compress_traced(FAKE, FAKE, 1, 1, 1, 1024, 64, 32, 2, FAKE, 992, FAKE,
+                                C.c_void_p(0x100000), 1 << 20, None, 992, None)
+    assert rc == _lib.THIN_EINVAL
+
+
+def test_attention_validates_before_launch():
+    L = _lib.lib()
+
+    def call(**kw):
+        a = dict(Q=FAKE, K=FAKE, V=FAKE, dtype=1, B=1, H=1, n_q=8, n=16, d=64, idx=FAKE,
+                 n_out=4, O=FAKE, od=0)
+        a.update(kw)
+        return L.thin_attention(a["Q"], a["K"], a["V"], a["dtype"], a["B"], a["H"], a["n_q"],
+                                a["n"], a["d"], a["idx"], a["n_out"], a["O"], a["od"], None)
+
+    assert call(d=80) == _lib.THIN_EINVAL
+    assert call(n_out=0) == _lib.THIN_EINVAL
+    assert call(n_q=0) == _lib.THIN_EINVAL
+    assert call(O=None) == _lib.THIN_EINVAL
+    assert call(dtype=3) == _lib.THIN_EDTYPE
+    assert call(od=2) == _lib.THIN_EDTYPE
+
+
+def test_workloads_are_seeded_and_shaped():
+    w = W.WORKLOADS["tiny"]
+    Q1, K1, V1 = W.make_qkv(w)
+    Q2, K2, V2 = W.make_qkv(w)
+    assert tuple(K1.shape) == (1, 1, 1024, 64) and K1.dtype.is_floating_point
+    assert (K1 == K2).all() and (Q1 == Q2).all() and (V1 == V2).all()
+    u = W.make_uniforms(w, 992)
+    assert u.numel() == 992 and float(u.min()) >= 0 and float(u.max()) < 1
+    assert ((u.double() * 2 ** 24) % 1 == 0).all()
+    w3 = W.WORKLOADS["imggen"].with_(B=2)
+    Q, K, V = W.make_qkv(w3)
+    assert tuple(Q.shape) == (2, 1, 4096, 64) and tuple(K.shape) == (2, 1, 1024, 64)
+    assert float(V.abs().max()) <= 1.0

@@ -1,0 +1,207 @@
+"""Parity of the HIP path (through the C ABI) with the CPU oracle.
+
+Indices: bit-exact, except decisions whose margin |alpha/a - (1 - 2u)| is
+below 1e-5 (relative to the threshold a), where either branch is correct; the
+oracle then follows the GPU's branch ("follow mode") and counts it.  Any other
+disagreement is a hard mismatch and fails.  Attention: max-abs error 2e-3
+(bf16 inputs, fp32 accumulation) and 1e-5 (fp32 inputs) against the float64
+oracle on the same coreset.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2606_10944_amd import thin_attention, thin_compress, thin_plan, thin_selftest_gram16
+from paper_2606_10944_amd import workloads as W
+
+pytestmark = pytest.mark.gpu
+DEV = torch.device("cuda:0")
+MARGIN = 1e-5
+
+
+def _tol(w):
+    return 2e-3 if w.dtype == "bf16" else 1e-5
+
+
+def _compress_gpu(w, Q, K, V):
+    plan = thin_plan(w.B, w.H, w.n, w.d, w.n_out, w.g)
+    U = W.make_uniforms(w, plan["uniforms_total"])
+    idx, tr = thin_compress(K.to(DEV), V.to(DEV), w.n_out, w.g, U.to(DEV), trace=True)
+    torch.cuda.synchronize()
+    return plan, U, idx.cpu().numpy(), tr.cpu().numpy()
+
+
+def _check_compress(w, K, V, U, idx, tr, slices):
+    Us = U.numpy().reshape(w.S, -1) if U.numel() else np.zeros((w.S, 1), np.float32)
+    ts = tr.reshape(w.S, -1) if tr.size else np.zeros((w.S, 1), np.uint8)
+    near = 0
+    for s in slices:
+        b, h = divmod(s, w.H)
+        got = idx[b, h]
+        assert got.shape == (w.n_out,)
+        assert np.all(np.diff(got) > 0) and got.min() >= 0 and got.max() < w.n
+        r = oracle.compress(K[b, h], V[b, h], w.n_out, w.g, Us[s], follow=ts[s], tol=MARGIN)
+        st = r["stats"]
+        assert st["hard_mismatch"] == 0, (w.name, s, st)
+        assert np.array_equal(r["idx"], got), (w.name, s)
+        near += st["near_ties"]
+    return near
+
+
+def _check_attention(w, Q, K, V, idx, O, slices, rows=None):
+    tol = _tol(w)
+    worst = 0.0
+    for s in slices:
+        b, h = divmod(s, w.H)
+        q = np.arange(w.n_q) if rows is None else rows
+        ref = oracle.attention(Q[b, h][q], K[b, h], V[b, h], idx[b, h])
+        err = float(np.abs(ref - O[b, h][q].astype(np.float64)).max())
+        worst = max(worst, err)
+    assert worst <= tol, (w.name, worst)
+    return worst
+
+
+# ---------------------------------------------------------------------------
+@pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
+@pytest.mark.parametrize("d", [32, 64, 128])
+def test_mfma_fragment_gram_matches_matmul(dtype, d):
+    g = torch.Generator().manual_seed(d)
+    rows = torch.randn(32, d, generator=g).to(dtype)
+    got = thin_selftest_gram16(rows.to(DEV)).cpu().double()
+    r = rows.double()
+    want = r[:16] @ r[16:].T
+    assert torch.allclose(got, want, rtol=1e-5, atol=1e-4 * d), (got - want).abs().max()
+
+
+@pytest.mark.parametrize("name", ["tiny", "vit", "imggen"])
+def test_named_workload_full_parity(name):
+    w = W.WORKLOADS[name]
+    Q, K, V = W.make_qkv(w)
+    plan, U, idx, tr = _compress_gpu(w, Q, K, V)
+    near = _check_compress(w, K, V, U, idx, tr, range(w.S))
+    O = thin_attention(Q.to(DEV), K.to(DEV), V.to(DEV), torch.from_numpy(idx).to(DEV))
+    torch.cuda.synchronize()
+    err = _check_attention(w, Q, K, V, idx, O.cpu().numpy(), range(w.S))
+    print(f"{name}: near-ties {near}, attention max err {err:.3g}")
+
+
+def test_long_workload_sampled_parity():
+    """Full-size long-sequence workload (the benchmark's configuration):
+    compress parity on sampled slices, attention on sampled queries."""
+    w = W.WORKLOADS["long"]
+    Q, K, V = W.make_qkv(w)
+    plan, U, idx, tr = _compress_gpu(w, Q, K, V)
+    assert np.all(np.diff(idx, axis=-1) > 0)
+    near = _check_compress(w, K, V, U, idx, tr, [0, 37, 63])
+    O = thin_attention(Q.to(DEV), K.to(DEV), V.to(DEV), torch.from_numpy(idx).to(DEV))
+    torch.cuda.synchronize()
+    rows = np.random.default_rng(0).choice(w.n_q, 512, replace=False)
+    err = _check_attention(w, Q, K, V, idx, O.cpu().numpy(), [0, 37, 63], rows)
+    print(f"long: near-ties {near}, attention max err {err:.3g}")
+
+
+def test_stress_workload_sampled_parity():
+    w = W.WORKLOADS["stress"]
+    Q, K, V = W.make_qkv(w)
+    plan, U, idx, tr = _compress_gpu(w, Q, K, V)
+    assert np.all(np.diff(idx, axis=-1) > 0)
+    near = _check_compress(w, K, V, U, idx, tr, [5])
+    O = thin_attention(Q.to(DEV), K.to(DEV), V.to(DEV), torch.from_numpy(idx).to(DEV))
+    torch.cuda.synchronize()
+    rows = np.random.default_rng(1).choice(w.n_q, 256, replace=False)
+    err = _check_attention(w, Q, K, V, idx, O.cpu().numpy(), [5, 31], rows)
+    print(f"stress: near-ties {near}, attention max err {err:.3g}")
+
+
+CUSTOM = [
+    # ragged buckets (40 rows < one 64-row block), subsample, bf16 d=64
+    dict(B=1, H=2, n=5000, n_out=40, g=2, d=64, dtype="bf16", kind="gauss"),
+    # single 2560-row bucket (eight-wave kernel), subsample
+    dict(B=1, H=1, n=5000, n_out=40, g=5, d=64, dtype="bf16", kind="layernorm"),
+    # odd n_out, d=32, many tiny buckets
+    dict(B=2, H=3, n=1000, n_out=7, g=3, d=32, dtype="bf16", kind="gauss"),
+    dict(B=1, H=1, n=1000, n_out=7, g=4, d=32, dtype="fp32", kind="gauss_d4"),
+    # one round, subsample of 97 rows to 96
+    dict(B=2, H=1, n=97, n_out=48, g=0, d=64, dtype="fp32", kind="gauss_d4"),
+    # smallest case: two rows
+    dict(B=3, H=1, n=2, n_out=1, g=0, d=64, dtype="fp32", kind="gauss"),
+    dict(B=1, H=2, n=130, n_out=64, g=0, d=128, dtype="bf16", kind="gauss"),
+    # fp32 with d = 128 (32-row blocks)
+    dict(B=1, H=2, n=600, n_out=32, g=1, d=128, dtype="fp32", kind="gauss_d4"),
+    # heavy-tailed keys at a small size
+    dict(B=2, H=1, n=2048, n_out=32, g=2, d=128, dtype="bf16", kind="heavy_tail"),
+    # clustered keys, one bucket per round
+    dict(B=2, H=1, n=512, n_out=16, g=4, d=64, dtype="fp32", kind="mixture"),
+]
+
+
+@pytest.mark.parametrize("cfg", CUSTOM, ids=lambda c: f"n{c['n']}-o{c['n_out']}-g{c['g']}-d{c['d']}-{c['dtype']}")
+def test_custom_shapes_parity(cfg):
+    w = W.custom("custom", seed=11, **cfg)
+    Q, K, V = W.make_qkv(w)
+    plan, U, idx, tr = _compress_gpu(w, Q, K, V)
+    _check_compress(w, K, V, U, idx, tr, range(w.S))
+    O = thin_attention(Q.to(DEV), K.to(DEV), V.to(DEV), torch.from_numpy(idx).to(DEV))
+    torch.cuda.synchronize()
+    _check_attention(w, Q, K, V, idx, O.cpu().numpy(), range(w.S))
+
+
+def test_nout_equal_n_is_identity_and_exact_attention():
+    w = W.custom("ident", B=2, H=1, n=96, n_out=96, g=1, d=64, dtype="fp32")
+    Q, K, V = W.make_qkv(w)
+    plan, U, idx, tr = _compress_gpu(w, Q, K, V)
+    assert plan["rounds"] == 0
+    assert np.array_equal(idx, np.broadcast_to(np.arange(96, dtype=np.int32), idx.shape))
+    O = thin_attention(Q.to(DEV), K.to(DEV), V.to(DEV), torch.from_numpy(idx).to(DEV)).cpu()
+    for s in range(2):
+        ref = oracle.exact_attention(Q[s, 0], K[s, 0], V[s, 0])
+        assert np.abs(ref - O[s, 0].numpy()).max() <= 1e-5
+
+
+def test_compress_is_deterministic_and_stream_ordered():
+    w = W.custom("det", B=2, H=2, n=3000, n_out=32, g=2, d=128, dtype="bf16", kind="gauss")
+    Q, K, V = W.make_qkv(w)
+    plan = thin_plan(w.B, w.H, w.n, w.d, w.n_out, w.g)
+    U = W.make_uniforms(w, plan["uniforms_total"]).to(DEV)
+    Kd, Vd = K.to(DEV), V.to(DEV)
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        a, ta = thin_compress(Kd, Vd, w.n_out, w.g, U, trace=True, stream=side)
+        b, tb = thin_compress(Kd, Vd, w.n_out, w.g, U, trace=True, stream=side)
+    side.synchronize()
+    assert torch.equal(a, b) and torch.equal(ta, tb)
+
+
+def test_attention_edge_cases():
+    w = W.custom("edge", B=1, H=2, n=700, n_q=333, d=64, dtype="bf16", kind="gauss")
+    Q, K, V = W.make_qkv(w)
+    Qd, Kd, Vd = Q.to(DEV), K.to(DEV), V.to(DEV)
+    rng = np.random.default_rng(3)
+    cases = {
+        "one key": np.array([[[5]], [[600]]], np.int32),
+        "many chunks, ragged": np.sort(rng.choice(700, size=(1, 2, 301)), axis=-1).astype(np.int32),
+        "duplicates": np.full((1, 2, 70), 3, np.int32),
+    }
+    for name, idx in cases.items():
+        O = thin_attention(Qd, Kd, Vd, torch.from_numpy(idx).to(DEV)).cpu().numpy()
+        for h in range(2):
+            ref = oracle.attention(Q[0, h], K[0, h], V[0, h], idx[0, h])
+            assert np.abs(ref - O[0, h]).max() <= 2e-3, name
+    O = thin_attention(Qd, Kd, Vd, torch.from_numpy(cases["one key"]).to(DEV)).cpu().numpy()
+    assert np.array_equal(O[0, 0], np.repeat(V[0, 0, 5:6].float().numpy(), 333, axis=0))
+
+
+def test_attention_bf16_output():
+    w = W.custom("bo", B=2, H=1, n=1024, n_q=1000, d=128, dtype="bf16", kind="gauss")
+    Q, K, V = W.make_qkv(w)
+    idx = np.sort(np.random.default_rng(4).choice(1024, size=(2, 1, 128), replace=False),
+                  axis=-1).astype(np.int32)
+    O = thin_attention(Q.to(DEV), K.to(DEV), V.to(DEV), torch.from_numpy(idx).to(DEV),
+                       out_dtype=torch.bfloat16)
+    O = O.float().cpu().numpy()
+    for s in range(2):
+        ref = oracle.attention(Q[s, 0], K[s, 0], V[s, 0], idx[s, 0])
+        # fp32 accumulation error plus one bf16 rounding of the output
+        assert np.all(np.abs(ref - O[s, 0]) <= 2e-3 + 2.0 ** -8 * np.abs(ref))

@@ -6,8 +6,9 @@
 // in chunks of 64 keys staged in LDS (gathered through idx); scores S^T =
 // K_I Q^T come from 16x16 MFMA tiles (keys x queries), the softmax is online
 // in float32, and O^T += V_I^T P^T reuses the score tile's register layout as
-// the B operand.  For bf16 inputs P is rounded to bf16 for the P.V MFMA and
-// the denominator sums exactly those rounded weights.
+// the B operand.  For bf16 inputs the weights P (float32) enter the bf16 P.V
+// MFMA as two terms, P = hi + lo with hi = bf16(P), lo = bf16(P - hi), so the
+// product keeps about 16 significant bits of P instead of 8.
 #include <math.h>
 
 #include "common.hpp"
@@ -145,8 +146,7 @@ __global__ __launch_bounds__(64 * WAVES) void coreset_attn_kernel(
       for (int kt = 0; kt < 4; ++kt)
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          float pv = sc[kt][i] == -INFINITY ? 0.0f : __builtin_amdgcn_exp2f((sc[kt][i] - mnew) * c2);
-          if (BF) pv = bf16_to_float(float_to_bf16(pv));
+          const float pv = sc[kt][i] == -INFINITY ? 0.0f : __builtin_amdgcn_exp2f((sc[kt][i] - mnew) * c2);
           pr[kt][i] = pv;
           psum += pv;
         }
@@ -157,20 +157,32 @@ __global__ __launch_bounds__(64 * WAVES) void coreset_attn_kernel(
       if (BF) {
 #pragma unroll
         for (int c = 0; c < 2; ++c) {
-          uint4 bw;
-          bw.x = (uint32_t)float_to_bf16(pr[2 * c][0]) | ((uint32_t)float_to_bf16(pr[2 * c][1]) << 16);
-          bw.y = (uint32_t)float_to_bf16(pr[2 * c][2]) | ((uint32_t)float_to_bf16(pr[2 * c][3]) << 16);
-          bw.z = (uint32_t)float_to_bf16(pr[2 * c + 1][0]) | ((uint32_t)float_to_bf16(pr[2 * c + 1][1]) << 16);
-          bw.w = (uint32_t)float_to_bf16(pr[2 * c + 1][2]) | ((uint32_t)float_to_bf16(pr[2 * c + 1][3]) << 16);
-          const bf16x8_t bfrag = __builtin_bit_cast(bf16x8_t, bw);
+          uint16_t hb[8], lb[8];
+#pragma unroll
+          for (int j = 0; j < 8; ++j) {
+            const float pv = pr[2 * c + (j >> 2)][j & 3];
+            hb[j] = float_to_bf16(pv);
+            lb[j] = float_to_bf16(pv - bf16_to_float(hb[j]));
+          }
+          uint4 hw, lw;
+          hw.x = (uint32_t)hb[0] | ((uint32_t)hb[1] << 16);
+          hw.y = (uint32_t)hb[2] | ((uint32_t)hb[3] << 16);
+          hw.z = (uint32_t)hb[4] | ((uint32_t)hb[5] << 16);
+          hw.w = (uint32_t)hb[6] | ((uint32_t)hb[7] << 16);
+          lw.x = (uint32_t)lb[0] | ((uint32_t)lb[1] << 16);
+          lw.y = (uint32_t)lb[2] | ((uint32_t)lb[3] << 16);
+          lw.z = (uint32_t)lb[4] | ((uint32_t)lb[5] << 16);
+          lw.w = (uint32_t)lb[6] | ((uint32_t)lb[7] << 16);
+          const bf16x8_t bhi = __builtin_bit_cast(bf16x8_t, hw);
+          const bf16x8_t blo = __builtin_bit_cast(bf16x8_t, lw);
 #pragma unroll
           for (int dt = 0; dt < D / 16; ++dt) {
             const unsigned char* row = sV + (dt * 16 + m16) * L::v_stride;
             uint2 lo = *reinterpret_cast<const uint2*>(row + (32 * c + 4 * g) * 2);
             uint2 hi = *reinterpret_cast<const uint2*>(row + (32 * c + 16 + 4 * g) * 2);
-            uint4 aw = make_uint4(lo.x, lo.y, hi.x, hi.y);
-            acc[qt][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-                __builtin_bit_cast(bf16x8_t, aw), bfrag, acc[qt][dt], 0, 0, 0);
+            const bf16x8_t av = __builtin_bit_cast(bf16x8_t, make_uint4(lo.x, lo.y, hi.x, hi.y));
+            acc[qt][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, bhi, acc[qt][dt], 0, 0, 0);
+            acc[qt][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, blo, acc[qt][dt], 0, 0, 0);
           }
         }
       } else {

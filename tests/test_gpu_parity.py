@@ -180,7 +180,7 @@ def test_attention_edge_cases():
     Qd, Kd, Vd = Q.to(DEV), K.to(DEV), V.to(DEV)
     rng = np.random.default_rng(3)
     cases = {
-        "one key": np.array([[[5]], [[600]]], np.int32),
+        "one key": np.array([[[5], [600]]], np.int32),
         "many chunks, ragged": np.sort(rng.choice(700, size=(1, 2, 301)), axis=-1).astype(np.int32),
         "duplicates": np.full((1, 2, 70), 3, np.int32),
     }

@@ -9,7 +9,7 @@
 
 namespace {
 
-constexpr int64_t kMaxBucket = 16384;  // per-pair state of a bucket lives in LDS
+constexpr int64_t kMaxBucket = 8192;  // per-pair state and row indices of a bucket live in LDS
 constexpr int64_t kMaxRows = (int64_t)1 << 30;
 
 struct Levels {

@@ -114,10 +114,9 @@ __global__ __launch_bounds__(64 * WAVES) void coreset_attn_kernel(
     uint4 Ak[4][NV];
 #pragma unroll
     for (int kt = 0; kt < 4; ++kt) {
-      const uint4* p = reinterpret_cast<const uint4*>(sK + (kt * 16 + m16) * L::k_stride +
-                                                      g * (D / 4) * Elem<T>::bytes);
+      const uint4* p = reinterpret_cast<const uint4*>(sK + (kt * 16 + m16) * L::k_stride);
 #pragma unroll
-      for (int v = 0; v < NV; ++v) Ak[kt][v] = p[v];
+      for (int v = 0; v < NV; ++v) Ak[kt][v] = p[4 * v + g];
     }
 
 #pragma unroll

@@ -1,12 +1,13 @@
 // Device-side building blocks shared by the thinning kernels (gfx950 / CDNA4).
 //
 // Row fragments.  A 64-lane wavefront covers 16 rows of a d-wide matrix:
-// lane l holds row (l % 16) and the contiguous quarter g = l / 16 of its
-// columns, [g*d/4, (g+1)*d/4), as NV 16-byte words.  The same lane layout
-// serves as the A operand (rows = M) and as the B operand (rows = N) of the
-// 16x16 MFMA instructions: within one instruction, lane group g feeds the
-// same k-slots to A and B, so the product of two fragments is the matrix of
-// row dot products <row_m, row_n> whatever the internal k order is.
+// lane l holds row (l % 16) and, in its v-th 16-byte word, the row's word
+// 4v + l/16.  One load instruction therefore reads 64 contiguous bytes of
+// each row.  The same lane layout serves as the A operand (rows = M) and as
+// the B operand (rows = N) of the 16x16 MFMA instructions: within one
+// instruction, lane group l/16 feeds the same k-slots to A and B, so the
+// product of two fragments is the matrix of row dot products <row_m, row_n>
+// whatever the internal k order is.
 //
 // 16x16 MFMA outputs: lane l holds D[4*(l/16) + i][l % 16], i = 0..3.
 #pragma once
@@ -115,9 +116,9 @@ template <typename T, int D>
 __device__ __forceinline__ void load_frag(const T* base, int64_t row, int g, bool valid, uint4* out) {
   constexpr int NV = Frag<T, D>::NV;
   if (valid) {
-    const uint4* p = reinterpret_cast<const uint4*>(base + row * D + g * (D / 4));
+    const uint4* p = reinterpret_cast<const uint4*>(base + row * D);
 #pragma unroll
-    for (int v = 0; v < NV; ++v) out[v] = p[v];
+    for (int v = 0; v < NV; ++v) out[v] = p[4 * v + g];
   } else {
 #pragma unroll
     for (int v = 0; v < NV; ++v) out[v] = make_uint4(0, 0, 0, 0);

@@ -111,6 +111,39 @@ __device__ __forceinline__ floatx4_t mma_rows<float, 128>(const uint4* a, const 
   return mma_rows_f32<8>(a, b, acc);
 }
 
+// acc += A_word x B_word for one 16-byte word of the row fragments (one
+// k-chunk): 16x16x32 bf16 (one MFMA) or 16x16x4 f32 (four MFMAs).
+template <typename T>
+__device__ __forceinline__ floatx4_t mma_word(const uint4& a, const uint4& b, floatx4_t acc);
+
+template <>
+__device__ __forceinline__ floatx4_t mma_word<bf16_t>(const uint4& a, const uint4& b, floatx4_t acc) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, a),
+                                                 __builtin_bit_cast(bf16x8_t, b), acc, 0, 0, 0);
+}
+template <>
+__device__ __forceinline__ floatx4_t mma_word<float>(const uint4& a, const uint4& b, floatx4_t acc) {
+  acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.x), __uint_as_float(b.x), acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.y), __uint_as_float(b.y), acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.z), __uint_as_float(b.z), acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.w), __uint_as_float(b.w), acc, 0, 0, 0);
+  return acc;
+}
+
+// acc += A_word x B_word using only k-slot 0 of lane group 0 (one MFMA).
+template <typename T>
+__device__ __forceinline__ floatx4_t mma_aug(const uint4& a, const uint4& b, floatx4_t acc);
+
+template <>
+__device__ __forceinline__ floatx4_t mma_aug<bf16_t>(const uint4& a, const uint4& b, floatx4_t acc) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, a),
+                                                 __builtin_bit_cast(bf16x8_t, b), acc, 0, 0, 0);
+}
+template <>
+__device__ __forceinline__ floatx4_t mma_aug<float>(const uint4& a, const uint4& b, floatx4_t acc) {
+  return __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.x), __uint_as_float(b.x), acc, 0, 0, 0);
+}
+
 // Load this lane's quarter of row `row` (d columns of T) or zeros if !valid.
 template <typename T, int D>
 __device__ __forceinline__ void load_frag(const T* base, int64_t row, int g, bool valid, uint4* out) {

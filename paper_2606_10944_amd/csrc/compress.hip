@@ -301,9 +301,9 @@ __device__ __forceinline__ void frag_pair_terms(const uint4* fk, const uint4* fv
 //      alpha < a (1 - 2u), the exact form of "u < min(1, (1 - alpha/a)_+/2)");
 //   3. all waves add the block's contribution to every later pair: a
 //      [block rows] x [later rows] Gram tile on MFMA, exp, signed reduction.
-// The bucket's row indices are staged in LDS; the next column tile is loaded
-// while the current one is used; the pair terms of every pair are formed the
-// first time its rows are loaded (block 0's pass).  Two waves share a SIMD.
+// The bucket's row indices are staged in LDS; the next column tiles are
+// loaded while the current one is used; the float64 pair terms of every pair
+// are formed the first time its rows are loaded (block 0's pass).
 // Scaling: all kappa values feeding pair p are multiplied by exp(-h_p), h_p =
 // the larger of the pair's two diagonal exponents ||k||^2/sqrt d.  This keeps
 // fp32 exps in range (kappa_att overflows fp32 for large keys); the decision
@@ -385,6 +385,10 @@ void halve_kernel(HalveArgs a) {
       }
     }
   }
+  // v_max enters the V Gram as one extra k-chunk: B holds v_max in slot 0 of
+  // lane group 0, A holds +-v_max (the row's sign) there.
+  uint4 Baug = make_uint4(0, 0, 0, 0);
+  if (g == 0) Baug.x = Elem<T>::bytes == 2 ? (__float_as_uint(vmax) >> 16) : __float_as_uint(vmax);
   __syncthreads();
 
   double carry = -INFINITY;  // log b_max over the pairs already decided (wave 0)
@@ -482,14 +486,15 @@ void halve_kernel(HalveArgs a) {
     // ---- 3. Contribution of this block to every later pair. ----
     const uint64_t smask = (uint64_t)s_mask[0] | ((uint64_t)s_mask[1] << 32);
     // Row weights: +1 for the element that went to coreset 2, -1 for coreset 1.
-    // V rows carry the sign; the v_max^2 term enters as the MFMA accumulator.
-    float cw[RT][4];
+    // V rows and their v_max slot carry the sign.
+    uint4 Aaug[RT];
 #pragma unroll
     for (int rt = 0; rt < RT; ++rt) {
       const int jl = rt * 16 + m16;
       const uint32_t bit = (uint32_t)((smask >> (jl >> 1)) & 1ull);
       const bool neg = (bit != 0) == ((jl & 1) != 0);
-      if (jl < nrows && neg) {
+      const bool live = jl < nrows;
+      if (live && neg) {
 #pragma unroll
         for (int v = 0; v < NV; ++v) {
           Av[rt][v].x ^= Elem<T>::sign_mask;
@@ -498,13 +503,8 @@ void halve_kernel(HalveArgs a) {
           Av[rt][v].w ^= Elem<T>::sign_mask;
         }
       }
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int jr = rt * 16 + 4 * g + i;
-        const uint32_t b2 = (uint32_t)((smask >> (jr >> 1)) & 1ull);
-        const bool n2 = (b2 != 0) == ((jr & 1) != 0);
-        cw[rt][i] = jr < nrows ? (n2 ? -vm2f : vm2f) : 0.0f;
-      }
+      Aaug[rt] = make_uint4(0, 0, 0, 0);
+      if (live) Aaug[rt].x = Baug.x ^ (neg ? (Elem<T>::bytes == 2 ? 0x8000u : 0x80000000u) : 0u);
     }
     const int later0 = rows0 + BR;
     const int ntiles = (N - later0 + 15) >> 4;
@@ -526,7 +526,7 @@ void halve_kernel(HalveArgs a) {
         const int tl = later0 + ct * 16 + m16;
         const bool valid = tl < N;
         float h2;
-        if (blk == 0) {
+        if (blk == 0) {  // first time these rows are loaded: their pair terms
           float lbt;
           frag_pair_terms<T, D>(Bk[u], Bv[u], vm2d, inv_sqrt_d, h2, lbt);
           if (g == 0 && valid && (tl & 1) == 0) {
@@ -538,17 +538,27 @@ void halve_kernel(HalveArgs a) {
           const float h2_in = s_h2[min(tl, N - 1) >> 1];
           h2 = valid ? h2_in : 0.0f;
         }
-        float acc = 0.0f;
+        // 2*RT independent accumulators, k-chunk outermost, so consecutive
+        // MFMAs never depend on each other.
+        floatx4_t gk[RT], gv[RT];
 #pragma unroll
         for (int rt = 0; rt < RT; ++rt) {
-          floatx4_t gk = {0.f, 0.f, 0.f, 0.f};
-          floatx4_t gv = {cw[rt][0], cw[rt][1], cw[rt][2], cw[rt][3]};
-          gk = mma_rows<T, D>(Ak[rt], Bk[u], gk);
-          gv = mma_rows<T, D>(Av[rt], Bv[u], gv);
+          gk[rt] = (floatx4_t){0.f, 0.f, 0.f, 0.f};
+          gv[rt] = mma_aug<T>(Aaug[rt], Baug, (floatx4_t){0.f, 0.f, 0.f, 0.f});
+        }
+#pragma unroll
+        for (int v = 0; v < NV; ++v)
+#pragma unroll
+          for (int rt = 0; rt < RT; ++rt) {
+            gk[rt] = mma_word<T>(Ak[rt][v], Bk[u][v], gk[rt]);
+            gv[rt] = mma_word<T>(Av[rt][v], Bv[u][v], gv[rt]);
+          }
+        float acc = 0.0f;
+#pragma unroll
+        for (int rt = 0; rt < RT; ++rt)
 #pragma unroll
           for (int i = 0; i < 4; ++i)
-            acc = fmaf(__builtin_amdgcn_exp2f(fminf(gk[i] * c2 - h2, kExpClamp)), gv[i], acc);
-        }
+            acc = fmaf(__builtin_amdgcn_exp2f(fminf(gk[rt][i] * c2 - h2, kExpClamp)), gv[rt][i], acc);
         // Refill this slot with the tile PF steps ahead.
         {
           // (rows past the bucket end load a valid row; their results are unused)
@@ -562,7 +572,7 @@ void halve_kernel(HalveArgs a) {
         if (g == 0 && valid && (tl & 1) == 0) atomicAdd(&s_alpha[tl >> 1], (double)dt - (double)dp);
       }
     }
-    // Next block's rows (its pair terms were formed in block 0's pass).
+    // Next block's rows.
     {
       const int rows1 = rows0 + BR;
       const int nrows1 = min(BR, N - rows1);

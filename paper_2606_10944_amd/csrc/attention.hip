@@ -43,10 +43,9 @@ __device__ __forceinline__ void store4<float>(float* p, float a, float b, float 
 }
 template <>
 __device__ __forceinline__ void store4<bf16_t>(bf16_t* p, float a, float b, float c, float d) {
-  uint2 w;
-  w.x = (uint32_t)float_to_bf16(a) | ((uint32_t)float_to_bf16(b) << 16);
-  w.y = (uint32_t)float_to_bf16(c) | ((uint32_t)float_to_bf16(d) << 16);
-  *reinterpret_cast<uint2*>(p) = w;
+  typedef __bf16 b2 __attribute__((ext_vector_type(2)));
+  const b2 lo = {(__bf16)a, (__bf16)b}, hi = {(__bf16)c, (__bf16)d};
+  *reinterpret_cast<uint2*>(p) = make_uint2(__builtin_bit_cast(uint32_t, lo), __builtin_bit_cast(uint32_t, hi));
 }
 
 template <typename T, int D, typename TO>
@@ -217,6 +216,271 @@ __global__ __launch_bounds__(64 * WAVES) void coreset_attn_kernel(
   }
 }
 
+// ---------------------------------------------------------------------------
+// bf16, coreset resident in LDS (n_out <= 16*NKT).  One workgroup (WR waves)
+// stays on one slice and walks a contiguous range of queries, 16*QTR per wave
+// per step, with the next step's query fragments loaded during the current
+// one; the coreset is staged once: K row-major, V transposed (each thread
+// transposes an 8-key x 8-column block in registers).  Softmax is one pass
+// over all keys.
+// ---------------------------------------------------------------------------
+// Row paddings of the staged coreset.  K fragments are read 16 bytes per lane
+// from 16 rows at once: a stride of 68 words puts the rows on disjoint banks.
+// V^T fragments are read 8 bytes per lane from 16 rows: a stride of 2 (mod 32)
+// words keeps those disjoint too (a 16-byte pad gave two-way conflicts).
+template <int D, int NKT>
+struct ResLds {
+  static constexpr int NK = 16 * NKT;          // padded key count
+  static constexpr int k_stride = D * 2 + 16;  // bytes per K row
+  static constexpr int v_stride = NK * 2 + 8;  // bytes per V^T row (8-byte aligned)
+  static constexpr int bytes = NK * k_stride + D * v_stride;
+};
+
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+// Two floats to packed bf16 (round to nearest even, v_cvt_pk_bf16_f32).
+__device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
+  const bf16x2_t v = {(__bf16)a, (__bf16)b};
+  return __builtin_bit_cast(uint32_t, v);
+}
+__device__ __forceinline__ float bf16_lo_to_float(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf16_hi_to_float(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
+
+__device__ __forceinline__ uint32_t pack_lo(uint32_t x, uint32_t y) { return (x & 0xffffu) | (y << 16); }
+__device__ __forceinline__ uint32_t pack_hi(uint32_t x, uint32_t y) { return (x >> 16) | (y & 0xffff0000u); }
+
+template <int D, int NKT, int QTR, int WR, typename TO>
+__global__ __launch_bounds__(64 * WR) void coreset_attn_res_kernel(
+    const bf16_t* __restrict__ Q, const bf16_t* __restrict__ K, const bf16_t* __restrict__ V,
+    const int32_t* __restrict__ idx, int64_t n, int64_t n_q, int n_out, int64_t q_per_wg,
+    TO* __restrict__ O) {
+  using L = ResLds<D, NKT>;
+  constexpr int NK = L::NK;
+  constexpr int NV = Frag<bf16_t, D>::NV;
+  extern __shared__ __align__(16) unsigned char lds[];
+  unsigned char* sK = lds;
+  unsigned char* sV = lds + NK * L::k_stride;
+
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int m16 = lane & 15, g = lane >> 4;
+  const int64_t s = blockIdx.y;
+  const bf16_t* Ks = K + s * n * D;
+  const bf16_t* Vs = V + s * n * D;
+  const int32_t* Is = idx + s * (int64_t)n_out;
+  const float c2 = (float)(kLog2e / sqrt((double)D));
+
+  // ---- stage the coreset ----
+  constexpr int WPR = D / 8;  // 16-byte words per row
+  for (int w = threadIdx.x; w < NK * WPR; w += 64 * WR) {
+    const int key = w / WPR, wi = w % WPR;
+    uint4 kw = make_uint4(0, 0, 0, 0);
+    if (key < n_out) {
+      int64_t r = Is[key];
+      r = r < 0 ? 0 : (r >= n ? n - 1 : r);
+      kw = reinterpret_cast<const uint4*>(Ks + r * D)[wi];
+    }
+    *reinterpret_cast<uint4*>(sK + key * L::k_stride + wi * 16) = kw;
+  }
+  for (int b = threadIdx.x; b < (NK / 8) * WPR; b += 64 * WR) {
+    const int kb = b / WPR, db = b % WPR;  // keys 8kb..8kb+7, columns 8db..8db+7
+    uint32_t w[8][4];
+#pragma unroll
+    for (int r8 = 0; r8 < 8; ++r8) {
+      const int key = kb * 8 + r8;
+      uint4 vw = make_uint4(0, 0, 0, 0);
+      if (key < n_out) {
+        int64_t r = Is[key];
+        r = r < 0 ? 0 : (r >= n ? n - 1 : r);
+        vw = reinterpret_cast<const uint4*>(Vs + r * D)[db];
+      }
+      w[r8][0] = vw.x; w[r8][1] = vw.y; w[r8][2] = vw.z; w[r8][3] = vw.w;
+    }
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {  // column 8db + e: the 8 keys' values
+      const int k = e >> 1;
+      uint4 o;
+      if ((e & 1) == 0) {
+        o.x = pack_lo(w[0][k], w[1][k]); o.y = pack_lo(w[2][k], w[3][k]);
+        o.z = pack_lo(w[4][k], w[5][k]); o.w = pack_lo(w[6][k], w[7][k]);
+      } else {
+        o.x = pack_hi(w[0][k], w[1][k]); o.y = pack_hi(w[2][k], w[3][k]);
+        o.z = pack_hi(w[4][k], w[5][k]); o.w = pack_hi(w[6][k], w[7][k]);
+      }
+      unsigned char* dst = sV + (db * 8 + e) * L::v_stride + kb * 16;
+      if constexpr (L::v_stride % 16 == 0) {
+        *reinterpret_cast<uint4*>(dst) = o;
+      } else {
+        reinterpret_cast<uint2*>(dst)[0] = make_uint2(o.x, o.y);
+        reinterpret_cast<uint2*>(dst)[1] = make_uint2(o.z, o.w);
+      }
+    }
+  }
+  __syncthreads();
+
+  const int64_t q_begin = (int64_t)blockIdx.x * q_per_wg;
+  const int64_t q_end = min(q_begin + q_per_wg, n_q);
+  const bf16_t* Qs = Q + s * n_q * D;
+  constexpr int QSTEP = 16 * QTR * WR;  // queries per workgroup step
+
+  uint4 Bq[QTR][NV];
+#pragma unroll
+  for (int qt = 0; qt < QTR; ++qt) {
+    const int64_t q = q_begin + wave * 16 * QTR + qt * 16 + m16;
+    load_frag<bf16_t, D>(Qs, min(q, n_q - 1), g, true, Bq[qt]);
+  }
+  for (int64_t q0 = q_begin; q0 < q_end; q0 += QSTEP) {
+    const int64_t qw = q0 + wave * 16 * QTR;
+    uint4 Nq[QTR][NV];
+#pragma unroll
+    for (int qt = 0; qt < QTR; ++qt) {
+      const int64_t q = qw + QSTEP + qt * 16 + m16;
+      load_frag<bf16_t, D>(Qs, min(q, n_q - 1), g, true, Nq[qt]);
+    }
+    // scores S^T[key][query]; the next key tile's fragment is read while the
+    // current one multiplies, and no further (the scheduling barrier keeps
+    // the compiler from hoisting every tile's LDS reads at once)
+    floatx4_t sc[QTR][NKT];
+    uint4 a[2][NV];
+#pragma unroll
+    for (int v = 0; v < NV; ++v)
+      a[0][v] = reinterpret_cast<const uint4*>(sK + m16 * L::k_stride)[4 * v + g];
+#pragma unroll
+    for (int kt = 0; kt < NKT; ++kt) {
+      if (kt + 1 < NKT) {
+        const uint4* pk = reinterpret_cast<const uint4*>(sK + ((kt + 1) * 16 + m16) * L::k_stride);
+#pragma unroll
+        for (int v = 0; v < NV; ++v) a[(kt + 1) & 1][v] = pk[4 * v + g];
+      }
+#pragma unroll
+      for (int qt = 0; qt < QTR; ++qt) {
+        floatx4_t z = {0.f, 0.f, 0.f, 0.f};
+        sc[qt][kt] = mma_rows<bf16_t, D>(a[kt & 1], Bq[qt], z);
+      }
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    float inv_l[QTR];
+    floatx4_t acc[QTR][D / 16];
+#pragma unroll
+    for (int qt = 0; qt < QTR; ++qt) {
+      float mx = -INFINITY;
+#pragma unroll
+      for (int kt = 0; kt < NKT; ++kt)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int key = kt * 16 + 4 * g + i;
+          if (key >= n_out) sc[qt][kt][i] = -INFINITY;
+          mx = fmaxf(mx, sc[qt][kt][i]);
+        }
+      mx = fmaxf(mx, __shfl_xor(mx, 16));
+      mx = fmaxf(mx, __shfl_xor(mx, 32));
+      float l = 0.f;
+#pragma unroll
+      for (int kt = 0; kt < NKT; ++kt)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const float pv = __builtin_amdgcn_exp2f((sc[qt][kt][i] - mx) * c2);
+          sc[qt][kt][i] = pv;
+          l += pv;
+        }
+      l += __shfl_xor(l, 16);
+      l += __shfl_xor(l, 32);
+      inv_l[qt] = 1.0f / l;
+#pragma unroll
+      for (int dt = 0; dt < D / 16; ++dt) acc[qt][dt] = (floatx4_t){0.f, 0.f, 0.f, 0.f};
+    }
+    // O^T += V^T P^T, 32 keys per MFMA; P = hi + lo in bf16
+#pragma unroll
+    for (int c = 0; c < NKT / 2; ++c) {
+      bf16x8_t bhi[QTR], blo[QTR];
+#pragma unroll
+      for (int qt = 0; qt < QTR; ++qt) {
+        uint32_t hw[4], lw[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const float p0 = sc[qt][2 * c + (j >> 1)][2 * (j & 1)];
+          const float p1 = sc[qt][2 * c + (j >> 1)][2 * (j & 1) + 1];
+          hw[j] = pack_bf16x2(p0, p1);
+          lw[j] = pack_bf16x2(p0 - bf16_lo_to_float(hw[j]), p1 - bf16_hi_to_float(hw[j]));
+        }
+        bhi[qt] = __builtin_bit_cast(bf16x8_t, make_uint4(hw[0], hw[1], hw[2], hw[3]));
+        blo[qt] = __builtin_bit_cast(bf16x8_t, make_uint4(lw[0], lw[1], lw[2], lw[3]));
+      }
+#pragma unroll
+      for (int dt = 0; dt < D / 16; ++dt) {
+        const unsigned char* row = sV + (dt * 16 + m16) * L::v_stride;
+        const uint2 lo = *reinterpret_cast<const uint2*>(row + (32 * c + 4 * g) * 2);
+        const uint2 hi = *reinterpret_cast<const uint2*>(row + (32 * c + 16 + 4 * g) * 2);
+        const bf16x8_t av = __builtin_bit_cast(bf16x8_t, make_uint4(lo.x, lo.y, hi.x, hi.y));
+#pragma unroll
+        for (int qt = 0; qt < QTR; ++qt) {
+          acc[qt][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, bhi[qt], acc[qt][dt], 0, 0, 0);
+          acc[qt][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, blo[qt], acc[qt][dt], 0, 0, 0);
+        }
+      }
+      __builtin_amdgcn_sched_barrier(0);
+    }
+#pragma unroll
+    for (int qt = 0; qt < QTR; ++qt) {
+      const int64_t q = qw + qt * 16 + m16;
+      if (q < q_end) {
+        TO* orow = O + (s * n_q + q) * D;
+#pragma unroll
+        for (int dt = 0; dt < D / 16; ++dt)
+          store4<TO>(orow + dt * 16 + 4 * g, acc[qt][dt][0] * inv_l[qt], acc[qt][dt][1] * inv_l[qt],
+                     acc[qt][dt][2] * inv_l[qt], acc[qt][dt][3] * inv_l[qt]);
+      }
+#pragma unroll
+      for (int v = 0; v < NV; ++v) Bq[qt][v] = Nq[qt][v];
+    }
+  }
+}
+
+template <int D, int NKT, int QTR, int WR, typename TO>
+hipError_t launch_attn_res(const void* Q, const void* K, const void* V, const int32_t* idx,
+                           int64_t S, int64_t n, int64_t n_q, int64_t n_out, void* O,
+                           hipStream_t st) {
+  using L = ResLds<D, NKT>;
+  auto kern = coreset_attn_res_kernel<D, NKT, QTR, WR, TO>;
+  const size_t lds = L::bytes;
+  if (lds > 64 * 1024) {
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e != hipSuccess) return e;
+  }
+  constexpr int64_t QSTEP = 16 * QTR * WR;
+  // about two workgroups per CU in total, whole steps of queries per workgroup
+  int64_t per_slice = (512 + S - 1) / S;
+  const int64_t steps = (n_q + QSTEP - 1) / QSTEP;
+  if (per_slice > steps) per_slice = steps;
+  if (per_slice < 1) per_slice = 1;
+  const int64_t q_per_wg = ((steps + per_slice - 1) / per_slice) * QSTEP;
+  const int64_t wgs = (n_q + q_per_wg - 1) / q_per_wg;
+  dim3 grid((unsigned)wgs, (unsigned)S), block(64 * WR);
+  hipLaunchKernelGGL(kern, grid, block, lds, st, (const bf16_t*)Q, (const bf16_t*)K,
+                     (const bf16_t*)V, idx, n, n_q, (int)n_out, q_per_wg, (TO*)O);
+  return hipGetLastError();
+}
+
+// 16-query tiles per wave per step and waves per workgroup of the resident kernel
+#ifndef ATTN_RES_QTR
+#define ATTN_RES_QTR 1
+#endif
+#ifndef ATTN_RES_WAVES
+#define ATTN_RES_WAVES 4
+#endif
+
+template <int D, typename TO>
+hipError_t launch_attn_res_d(int64_t n_out, const void* Q, const void* K, const void* V,
+                             const int32_t* idx, int64_t S, int64_t n, int64_t n_q, void* O,
+                             hipStream_t st, bool* used) {
+  *used = true;
+  if (n_out <= 32) return launch_attn_res<D, 2, ATTN_RES_QTR, ATTN_RES_WAVES, TO>(Q, K, V, idx, S, n, n_q, n_out, O, st);
+  if (n_out <= 64) return launch_attn_res<D, 4, ATTN_RES_QTR, ATTN_RES_WAVES, TO>(Q, K, V, idx, S, n, n_q, n_out, O, st);
+  if (n_out <= 128) return launch_attn_res<D, 8, ATTN_RES_QTR, ATTN_RES_WAVES, TO>(Q, K, V, idx, S, n, n_q, n_out, O, st);
+  if (n_out <= 256 && D <= 128) return launch_attn_res<D, 16, ATTN_RES_QTR, ATTN_RES_WAVES, TO>(Q, K, V, idx, S, n, n_q, n_out, O, st);
+  *used = false;
+  return hipSuccess;
+}
+
 template <typename T, int D, typename TO>
 hipError_t launch_attn_t(const void* Q, const void* K, const void* V, const int32_t* idx,
                          int64_t S, int64_t n, int64_t n_q, int64_t n_out, void* O,
@@ -248,6 +512,15 @@ hipError_t launch_attention(int dtype, int64_t d, int out_dtype, const void* Q, 
     if (out_dtype == 0) return launch_attn_d<float, float>(d, Q, K, V, idx, S, n, n_q, n_out, O, st);
     return launch_attn_d<float, bf16_t>(d, Q, K, V, idx, S, n, n_q, n_out, O, st);
   }
+  bool used = false;
+  hipError_t e = hipSuccess;
+  if (d == 64)
+    e = out_dtype == 0 ? launch_attn_res_d<64, float>(n_out, Q, K, V, idx, S, n, n_q, O, st, &used)
+                       : launch_attn_res_d<64, bf16_t>(n_out, Q, K, V, idx, S, n, n_q, O, st, &used);
+  else if (d == 128)
+    e = out_dtype == 0 ? launch_attn_res_d<128, float>(n_out, Q, K, V, idx, S, n, n_q, O, st, &used)
+                       : launch_attn_res_d<128, bf16_t>(n_out, Q, K, V, idx, S, n, n_q, O, st, &used);
+  if (used) return e;
   if (out_dtype == 0) return launch_attn_d<bf16_t, float>(d, Q, K, V, idx, S, n, n_q, n_out, O, st);
   return launch_attn_d<bf16_t, bf16_t>(d, Q, K, V, idx, S, n, n_q, n_out, O, st);
 }

@@ -9,7 +9,7 @@
 
 namespace {
 
-constexpr int64_t kMaxBucket = 8192;  // per-pair state and row indices of a bucket live in LDS
+constexpr int64_t kMaxBucket = 8192;  // the decision pass keeps a bucket's per-pair alpha in LDS
 constexpr int64_t kMaxRows = (int64_t)1 << 30;
 
 struct Levels {
@@ -54,30 +54,60 @@ bool make_levels(int64_t n, int64_t n_out, int32_t g, Levels* lv) {
   return true;
 }
 
+// Pair scores of one round live in a region of at most kScoreCap bytes (or
+// one bucket's worth, if larger); rounds whose buckets need more run in
+// several launches.
+constexpr size_t kScoreCap = (size_t)512 << 20;
+
+size_t score_bytes(int64_t N) { return thin::halve_score_bytes(N); }
+
+size_t score_region(int64_t S, int64_t d, const Levels& lv) {
+  size_t region = 0;
+  for (int32_t r = 0; r < lv.L; ++r) {
+    const size_t per = score_bytes(lv.N[r]);
+    const size_t all = (size_t)(S * lv.G[r]) * per;
+    const size_t cap = per > kScoreCap ? per : kScoreCap;
+    const size_t need = all < cap ? all : cap;
+    if (need > region) region = need;
+  }
+  return region;
+}
+
 struct Workspace {
   uint32_t* vmax_bits;
   int32_t* buf_a;  // [S, n_kept]
   int32_t* buf_b;  // [S, n_kept / 2]
+  float* lbt;      // [S, n_kept / 2]
+  float* h2;       // [S, n_kept / 2]
+  float* E;        // score region
+  size_t e_bytes;
   size_t bytes;
 };
 
-size_t workspace_size(int64_t S, int64_t n_kept) {
-  return align256((size_t)S * 4) + align256((size_t)S * (size_t)n_kept * 4) +
-         align256((size_t)S * (size_t)(n_kept / 2) * 4);
-}
-
-Workspace carve(void* base, int64_t S, int64_t n_kept) {
+Workspace carve(void* base, int64_t S, int64_t d, const Levels& lv) {
   Workspace w;
   unsigned char* p = static_cast<unsigned char*>(base);
+  const size_t pairs = (size_t)S * (size_t)(lv.n_kept / 2);
   size_t off = 0;
   w.vmax_bits = reinterpret_cast<uint32_t*>(p + off);
   off += align256((size_t)S * 4);
   w.buf_a = reinterpret_cast<int32_t*>(p + off);
-  off += align256((size_t)S * (size_t)n_kept * 4);
+  off += align256((size_t)S * (size_t)lv.n_kept * 4);
   w.buf_b = reinterpret_cast<int32_t*>(p + off);
-  off += align256((size_t)S * (size_t)(n_kept / 2) * 4);
+  off += align256(pairs * 4);
+  w.lbt = reinterpret_cast<float*>(p + off);
+  off += align256(pairs * 4);
+  w.h2 = reinterpret_cast<float*>(p + off);
+  off += align256(pairs * 4);
+  w.E = reinterpret_cast<float*>(p + off);
+  w.e_bytes = score_region(S, d, lv);
+  off += align256(w.e_bytes);
   w.bytes = off;
   return w;
+}
+
+size_t workspace_size(int64_t S, int64_t d, const Levels& lv) {
+  return carve(nullptr, S, d, lv).bytes;
 }
 
 int check_shape(int64_t B, int64_t H, int64_t n, int64_t d) {
@@ -102,9 +132,9 @@ int compress_impl(const void* K, const void* V, int32_t dtype, int64_t B, int64_
   if (Utot > 0 && !uniforms) return THIN_EINVAL;
   if (n_uniforms < Utot) return THIN_EUNIFORMS;
   if (trace && trace_len < Utot) return THIN_EINVAL;
-  if (!workspace || workspace_bytes < workspace_size(S, lv.n_kept)) return THIN_EWORKSPACE;
+  if (!workspace || workspace_bytes < workspace_size(S, d, lv)) return THIN_EWORKSPACE;
   if ((reinterpret_cast<uintptr_t>(workspace) & 255u) != 0) return THIN_EWORKSPACE;
-  Workspace ws = carve(workspace, S, lv.n_kept);
+  Workspace ws = carve(workspace, S, d, lv);
   hipStream_t st = static_cast<hipStream_t>(stream);
 
   hipError_t e = hipSuccess;
@@ -138,7 +168,18 @@ int compress_impl(const void* K, const void* V, int32_t dtype, int64_t B, int64_
       a.u_off = u_off;
       a.trace = trace;
       a.log_c = log(0.5 + log(2.0 * (double)lv.N[r] / 0.5));
-      ok(thin::launch_halve(dtype, d, a, st));
+      a.E = ws.E;
+      a.lbt = ws.lbt;
+      a.h2 = ws.h2;
+      const int64_t buckets = S * lv.G[r];
+      const size_t per = thin::halve_score_bytes(lv.N[r]);
+      int64_t chunk = (int64_t)(ws.e_bytes / per);
+      if (chunk < 1) chunk = 1;
+      for (int64_t b0 = 0; b0 < buckets && e == hipSuccess; b0 += chunk) {
+        a.b0 = b0;
+        const int64_t nbk = buckets - b0 < chunk ? buckets - b0 : chunk;
+        ok(thin::launch_halve(dtype, d, a, nbk, st));
+      }
       u_off += lv.n_r[r] / 2;
       cur = out;
     }
@@ -165,7 +206,7 @@ int thin_plan(int64_t B, int64_t H, int64_t n, int64_t d, int64_t n_out, int32_t
   plan->uniforms_per_slice = lv.U;
   plan->uniforms_total = S * lv.U;
   plan->max_bucket = lv.max_bucket;
-  plan->workspace_bytes = workspace_size(S, lv.n_kept);
+  plan->workspace_bytes = workspace_size(S, d, lv);
   return THIN_OK;
 }
 

@@ -19,6 +19,9 @@ namespace thin {
 
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float floatx4_t __attribute__((ext_vector_type(4)));
+// Native 16-byte vector: arrays of it stay in registers where arrays of the
+// HIP uint4 class can be demoted to scratch memory.
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 struct bf16_t {
   uint16_t bits;

@@ -189,93 +189,106 @@ __device__ __forceinline__ double sum_quarters(double x) {
 }
 
 // ---------------------------------------------------------------------------
-// Row-pair terms.  For the 16-row tile held as fragments (lane l: row l%16,
-// column quarter l/16): the float64 self dots <k,k>, <v,v> of every row and
-// the cross dots <k,k'>, <v,v'> of every pair (rows 2q, 2q+1).  bf16: each
-// v_dot2 gives two exact products summed in fp32, accumulated in fp64; fp32:
-// fp64 FMAs.  The cross dot is split between the two partner lanes (each
-// takes half of the quarter).  From them: h2 = the pair's larger diagonal
-// exponent ||k||^2/sqrt(d) in base 2, rounded to float (that float is used
-// wherever the pair's kappa values are scaled by exp(-h)), and lbt = log of
-// the RKHS distance b (Algorithm A.1) scaled by exp(-h/2).  The
-// exponentials and the log are float32 (about 1e-7 relative) on float64
-// arguments; the sums are float64.
+// Row-pair terms.  For a 16-row tile held as fragments (lane l: row l%16,
+// column quarter l/16): float64 self dots <k,k>, <v,v> of every row and the
+// cross dots <k,k'>, <v,v'> of every pair (rows 2q, 2q+1).  bf16: each
+// v_dot2 gives two exact products summed in fp32, a partial covers 8
+// elements and is accumulated in fp64; fp32: fp64 FMAs.  The cross dots use
+// the partner lane's words (DPP).
 // ---------------------------------------------------------------------------
-// Float64 partial dots of this lane's quarter of its row with itself (sk,
-// sv) and with the partner row's quarter (ck, cv).
-// bf16: each v_dot2 adds two exact products to an fp32 partial; a partial
-// covers 8 elements and is then added in fp64.
+// This lane's quarter of <k,k>.  Every place that forms a pair's scale h
+// runs this same instruction sequence, so all of them see identical bits.
 template <typename T, int D>
-__device__ __forceinline__ void quarter_dots_bf16(const uint4* fk, const uint4* fv, double& sk,
-                                                  double& sv, double& ck, double& cv) {
+__device__ __forceinline__ double quarter_self_dot(const uint4* f) {
   constexpr int NW = Frag<T, D>::NV * 4;
-  const uint32_t* wk = reinterpret_cast<const uint32_t*>(fk);
-  const uint32_t* wv = reinterpret_cast<const uint32_t*>(fv);
-  sk = 0.0; sv = 0.0; ck = 0.0; cv = 0.0;
+  const uint32_t* w = reinterpret_cast<const uint32_t*>(f);
+  double s = 0.0;
+  if constexpr (Elem<T>::bytes == 2) {
 #pragma unroll
-  for (int c = 0; c < NW / 4; ++c) {
-    float a0 = 0.f, a1 = 0.f, a2 = 0.f, a3 = 0.f;
+    for (int c = 0; c < NW / 4; ++c) {
+      float a = 0.f;
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const uint32_t xk = wk[4 * c + q], xv = wv[4 * c + q];
-      const bf16x2_t bk = __builtin_bit_cast(bf16x2_t, xk);
-      const bf16x2_t bv = __builtin_bit_cast(bf16x2_t, xv);
-      const bf16x2_t pk = __builtin_bit_cast(bf16x2_t, from_partner(xk));
-      const bf16x2_t pv = __builtin_bit_cast(bf16x2_t, from_partner(xv));
-      a0 = __builtin_amdgcn_fdot2_f32_bf16(bk, bk, a0, false);
-      a1 = __builtin_amdgcn_fdot2_f32_bf16(bv, bv, a1, false);
-      a2 = __builtin_amdgcn_fdot2_f32_bf16(bk, pk, a2, false);
-      a3 = __builtin_amdgcn_fdot2_f32_bf16(bv, pv, a3, false);
+      for (int q = 0; q < 4; ++q) {
+        const bf16x2_t b = __builtin_bit_cast(bf16x2_t, w[4 * c + q]);
+        a = __builtin_amdgcn_fdot2_f32_bf16(b, b, a, false);
+      }
+      s += (double)a;
     }
-    sk += (double)a0;
-    sv += (double)a1;
-    ck += (double)a2;
-    cv += (double)a3;
+  } else {
+#pragma unroll
+    for (int i = 0; i < NW; ++i) {
+      const double x = (double)__uint_as_float(w[i]);
+      s = fma(x, x, s);
+    }
   }
+  return s;
 }
 
-// fp32: exact products in fp64.
+// This lane's quarters of <v,v>, <k,k'> and <v,v'> (k', v' = partner row).
 template <typename T, int D>
-__device__ __forceinline__ void quarter_dots_f32(const uint4* fk, const uint4* fv, double& sk,
-                                                 double& sv, double& ck, double& cv) {
+__device__ __forceinline__ void quarter_pair_dots(const uint4* fk, const uint4* fv, double& sv,
+                                                  double& ck, double& cv) {
   constexpr int NW = Frag<T, D>::NV * 4;
   const uint32_t* wk = reinterpret_cast<const uint32_t*>(fk);
   const uint32_t* wv = reinterpret_cast<const uint32_t*>(fv);
-  sk = 0.0; sv = 0.0; ck = 0.0; cv = 0.0;
+  sv = 0.0; ck = 0.0; cv = 0.0;
+  if constexpr (Elem<T>::bytes == 2) {
 #pragma unroll
-  for (int w = 0; w < NW; ++w) {
-    const double xk = (double)__uint_as_float(wk[w]), xv = (double)__uint_as_float(wv[w]);
-    const double pk = (double)__uint_as_float(from_partner(wk[w]));
-    const double pv = (double)__uint_as_float(from_partner(wv[w]));
-    sk = fma(xk, xk, sk);
-    sv = fma(xv, xv, sv);
-    ck = fma(xk, pk, ck);
-    cv = fma(xv, pv, cv);
+    for (int c = 0; c < NW / 4; ++c) {
+      float a1 = 0.f, a2 = 0.f, a3 = 0.f;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const uint32_t xk = wk[4 * c + q], xv = wv[4 * c + q];
+        const bf16x2_t bk = __builtin_bit_cast(bf16x2_t, xk);
+        const bf16x2_t bv = __builtin_bit_cast(bf16x2_t, xv);
+        const bf16x2_t pk = __builtin_bit_cast(bf16x2_t, from_partner(xk));
+        const bf16x2_t pv = __builtin_bit_cast(bf16x2_t, from_partner(xv));
+        a1 = __builtin_amdgcn_fdot2_f32_bf16(bv, bv, a1, false);
+        a2 = __builtin_amdgcn_fdot2_f32_bf16(bk, pk, a2, false);
+        a3 = __builtin_amdgcn_fdot2_f32_bf16(bv, pv, a3, false);
+      }
+      sv += (double)a1;
+      ck += (double)a2;
+      cv += (double)a3;
+    }
+  } else {
+#pragma unroll
+    for (int w = 0; w < NW; ++w) {
+      const double xk = (double)__uint_as_float(wk[w]), xv = (double)__uint_as_float(wv[w]);
+      const double pk = (double)__uint_as_float(from_partner(wk[w]));
+      const double pv = (double)__uint_as_float(from_partner(wv[w]));
+      sv = fma(xv, xv, sv);
+      ck = fma(xk, pk, ck);
+      cv = fma(xv, pv, cv);
+    }
   }
 }
 
-// Row-pair terms of the 16-row tile held as fragments: h2f = the pair's
-// larger diagonal exponent ||k||^2/sqrt(d) in base 2, rounded to float (that
-// float is used wherever the pair's kappa values are scaled by exp(-h)), and
-// lbt = log of the RKHS distance b (Algorithm A.1) scaled by exp(-h/2).
-// Dots in float64; the exponentials and the log are float32 (about 1e-7
-// relative) on float64 arguments; the sums are float64.
+// Scale exponent of the pair: h = the larger of the two diagonal exponents
+// ||k||^2/sqrt(d), in base 2, rounded to float.  That float is used wherever
+// the pair's kappa values are scaled by exp(-h).  sk = this row's <k,k>.
+__device__ __forceinline__ float pair_h2f(double sk, double inv_sqrt_d) {
+  const double ex = sk * inv_sqrt_d, exp_ = from_partner(sk) * inv_sqrt_d;
+  const double h = ex > exp_ ? ex : exp_;
+  return (float)(h * kLog2e);
+}
+
+// Row-pair terms of the 16-row tile: h2f (above) and lbt = log of the RKHS
+// distance b (Algorithm A.1) scaled by exp(-h/2).  The exponentials and the
+// log are float32 (about 1e-7 relative) on float64 arguments; the sums are
+// float64.
 template <typename T, int D>
 __device__ __forceinline__ void frag_pair_terms(const uint4* fk, const uint4* fv, double vm2d,
                                                 double inv_sqrt_d, float& h2f, float& lbt) {
-  double sk, sv, ck, cv;
-  if (Elem<T>::bytes == 2)
-    quarter_dots_bf16<T, D>(fk, fv, sk, sv, ck, cv);
-  else
-    quarter_dots_f32<T, D>(fk, fv, sk, sv, ck, cv);
-  sk = sum_quarters(sk);
+  double sv, ck, cv;
+  const double sk = sum_quarters(quarter_self_dot<T, D>(fk));
+  quarter_pair_dots<T, D>(fk, fv, sv, ck, cv);
   sv = sum_quarters(sv);
   ck = sum_quarters(ck);
   cv = sum_quarters(cv);
-  const double skp = from_partner(sk), svp = from_partner(sv);
-  const double ex = sk * inv_sqrt_d, exp_ = skp * inv_sqrt_d, exx = ck * inv_sqrt_d;
-  const double h = ex > exp_ ? ex : exp_;
-  h2f = (float)(h * kLog2e);
+  h2f = pair_h2f(sk, inv_sqrt_d);
+  const double svp = from_partner(sv);
+  const double ex = sk * inv_sqrt_d, exp_ = from_partner(sk) * inv_sqrt_d, exx = ck * inv_sqrt_d;
   const double h2 = (double)h2f;
   const double t1 = (double)__builtin_amdgcn_exp2f((float)(ex * kLog2e - h2)) * (sv + vm2d);
   const double t2 = (double)__builtin_amdgcn_exp2f((float)(exp_ * kLog2e - h2)) * (svp + vm2d);
@@ -288,155 +301,302 @@ __device__ __forceinline__ void frag_pair_terms(const uint4* fk, const uint4* fv
 }
 
 // ---------------------------------------------------------------------------
-// One Halve round: KH(1/2) (App. A, Algorithm A.1) on every bucket.
+// One Halve round: KH(1/2) (App. A, Algorithm A.1) on every bucket, in two
+// launches.
 //
-// One workgroup per bucket of N rows y_0..y_{N-1} (pair p = (y_{2p}, y_{2p+1})).
-// The literal score alpha_p = sum_{S2} f_p - sum_{S1} f_p is kept per pair and
-// grown incrementally: once pair i is decided with sign sgn_i (+1 kept the
-// first element, -1 swapped), every later pair p receives
-//     sgn_i E(i,p),  E(i,p) = k(y'_i,y_p) - k(y_i,y_p) - k(y'_i,y'_p) + k(y_i,y'_p),
-// which is the same sum, reordered.  Pairs are processed in blocks of BP:
-//   1. the E(i,p) of the block's own pairs come from one MFMA Gram tile;
-//   2. wave 0 takes the BP decisions one after the other (ballot on
-//      alpha < a (1 - 2u), the exact form of "u < min(1, (1 - alpha/a)_+/2)");
-//   3. all waves add the block's contribution to every later pair: a
-//      [block rows] x [later rows] Gram tile on MFMA, exp, signed reduction.
-// The bucket's row indices are staged in LDS; the next column tiles are
-// loaded while the current one is used; the float64 pair terms of every pair
-// are formed the first time its rows are loaded (block 0's pass).
-// Scaling: all kappa values feeding pair p are multiplied by exp(-h_p), h_p =
-// the larger of the pair's two diagonal exponents ||k||^2/sqrt d.  This keeps
-// fp32 exps in range (kappa_att overflows fp32 for large keys); the decision
-// only depends on alpha/a, which the common factor leaves unchanged.  alpha
-// accumulates in float64.
+// Bucket rows y_0..y_{N-1}; pair p = (y_{2p}, y_{2p+1}).  The score of
+// Algorithm A.1, alpha_p = sum_{S2} f_p - sum_{S1} f_p, is the signed sum
+//     alpha_p = sum_{i<p} sgn_i E(i,p),
+//     E(i,p) = k(y'_i,y_p) - k(y_i,y_p) - k(y'_i,y'_p) + k(y_i,y'_p),
+// sgn_i = -1 if pair i was swapped, else +1 (the same sum, regrouped by
+// earlier pair).  E does not depend on any decision, so:
+//   1. pair_scores_kernel evaluates every E(i,p), i < p, of every bucket at
+//      once (MFMA Gram tiles + exp), plus the per-pair terms b_i and h_i;
+//   2. halve_pass_kernel takes the decisions pair by pair, in blocks of BP
+//      pairs: one wavefront decides a block (ballot on alpha < a (1 - 2u),
+//      the exact form of "u < min(1, (1 - alpha/a)_+ / 2)"), then every
+//      wavefront adds the block's signed scores to the later pairs' alpha.
+// Scaling: all kappa values feeding pair p are multiplied by exp(-h_p) (h_p
+// as in pair_h2f).  This keeps fp32 exps in range (kappa_att overflows fp32
+// for large keys); the decision only depends on alpha/a, which the common
+// factor leaves unchanged.  E is float32; alpha accumulates in float64.
+//
+// Score layout of one bucket (BR = 16 RT rows = BP pairs per block, NT =
+// ceil(N/16) row tiles): panel B (the block's BP pairs as i) holds one tile
+// per column tile jt = B RT .. NT-1, each tile 8 columns p x BP rows i,
+// column-major ([p][i]), so a column's BP scores are contiguous.  Panel B
+// starts panel_tiles(B) tiles into the bucket's array.
 // ---------------------------------------------------------------------------
-#ifndef HALVE_PF
-#define HALVE_PF 2
-#endif
-#ifndef HALVE_WPE
-#define HALVE_WPE 1
-#endif
-template <typename T, int D, int RT, int WAVES>
-__global__ __launch_bounds__(64 * WAVES) __attribute__((amdgpu_waves_per_eu(HALVE_WPE)))
-void halve_kernel(HalveArgs a) {
-  constexpr int NV = Frag<T, D>::NV;
-  constexpr int BR = 16 * RT;  // rows per block
-  constexpr int BP = BR / 2;   // pairs per block
-  constexpr int ES = BP + 1;   // padded row stride of the E tile
-  static_assert(BP <= 64, "decisions use one wavefront");
+__host__ __device__ inline int64_t panel_tiles(int64_t B, int64_t NT, int64_t RT) {
+  return B * NT - RT * B * (B - 1) / 2;
+}
 
+// Waves per pair_scores_kernel workgroup, column tiles in flight (registers)
+// and column-tile stages in LDS.
+#ifndef SCORE_WAVES
+#define SCORE_WAVES 8
+#endif
+constexpr int kScoreWaves = SCORE_WAVES;
+#ifndef SCORE_DEPTH
+#define SCORE_DEPTH 6
+#endif
+constexpr int kScoreStages = 3;
+// Column tiles per pair_scores_kernel workgroup.
+constexpr int kScoreChunk = 32;
+
+// Per-wave A rows: WRT row tiles (about 64 registers of fragments); WPB waves
+// cover one 64-row decision block; a workgroup covers BLOCKS blocks.  A
+// column tile (16 rows of K and V) is CHUNKS 1 KB fragment chunks.
+template <typename T, int D>
+struct ScoreShape {
+  static constexpr int NV = Frag<T, D>::NV;
+  static constexpr int WRT = NV >= 8 ? 1 : (NV == 4 ? 2 : 4);
+  static constexpr int WPB = 4 / WRT;
+  static constexpr int BLOCKS = kScoreWaves / WPB;
+  static constexpr int CHUNKS = 2 * NV;
+  static constexpr int LPT = (CHUNKS + kScoreWaves - 1) / kScoreWaves;
+  // stages, scale exponents, row indices of the column rows
+  static constexpr int LDS = kScoreStages * CHUNKS * 1024 + kScoreStages * 16 * 4 +
+                             (kScoreChunk + SCORE_DEPTH + 2) * 16 * 8;
+};
+
+// Scores of BLOCKS consecutive decision blocks of one bucket against column
+// tiles [jt0, jt1): grid (bucket, block group, column chunk).  Column tiles
+// stream through LDS: each is loaded once per workgroup (every thread loads
+// its share into registers DEPTH tiles ahead, then writes it to a stage), and
+// the LDS copy keeps the fragment lane order, so every wave reads it back
+// with one conflict-free 16-byte access per lane and chunk.  The column
+// pairs' scale h is formed once per tile by one wave.
+template <typename T, int D>
+__global__ __launch_bounds__(64 * kScoreWaves) void pair_scores_kernel(HalveArgs a) {
+  using SS = ScoreShape<T, D>;
+  constexpr int NV = SS::NV, WRT = SS::WRT, WPB = SS::WPB, NBW = SS::BLOCKS;
+  constexpr int CH = SS::CHUNKS, LPT = SS::LPT;
+  constexpr int BP = 32;
+  constexpr int TILE = 8 * BP;
+  constexpr int DEPTH = SCORE_DEPTH;
+  constexpr int NS = kScoreStages;
+  static_assert(DEPTH % NS == 0, "the unrolled ring keeps stage indices static");
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
   const int m16 = lane & 15;
   const int g = lane >> 4;
 
-  const int64_t s = (int64_t)blockIdx.x / a.G;
-  const int64_t t = (int64_t)blockIdx.x % a.G;
   const int N = a.N;
   const int P = N >> 1;
+  const int NT = (N + 15) >> 4;
+  const int nb = (N + 63) >> 6;
+  // Work item: (bucket, block group, column chunk).
+  const int64_t bl = blockIdx.x;
+  const int grp = blockIdx.y, chunk = blockIdx.z;
+  const int64_t bucket = a.b0 + bl;
+  const int64_t s = bucket / a.G;
+  const int64_t t = bucket % a.G;
+  const int jt0 = grp * NBW * 4 + chunk * a.ch;
+  if (jt0 >= NT) return;
+  const int jt1 = min(jt0 + a.ch, NT);
+  const int blk = grp * NBW + wave / WPB;  // this wave's decision block
+  const int sub = wave % WPB;                          // its part of the block
+  const bool has_blk = blk < nb;
+
   const T* K = reinterpret_cast<const T*>(a.K) + s * a.n * D;
   const T* V = reinterpret_cast<const T*>(a.V) + s * a.n * D;
   const int32_t* rows_in = a.idx_in ? a.idx_in + s * a.n_r + t * (int64_t)N : nullptr;
   const int64_t row_base = t * (int64_t)N;
-  const float* Ub = a.U + s * a.u_slice + a.u_off + t * (int64_t)P;
-  uint8_t* trace = a.trace ? a.trace + s * a.u_slice + a.u_off + t * (int64_t)P : nullptr;
-  int32_t* out = a.idx_out + s * (a.n_r >> 1) + t * (int64_t)P;
-
-  extern __shared__ __align__(16) unsigned char smem[];
-  double* s_alpha = reinterpret_cast<double*>(smem);
-  float* s_lbt = reinterpret_cast<float*>(s_alpha + P);
-  float* s_h2 = s_lbt + P;
-  float* s_E = s_h2 + P;
-  uint32_t* s_mask = reinterpret_cast<uint32_t*>(s_E + BP * ES);
-  int32_t* s_rows = reinterpret_cast<int32_t*>(s_mask + 4);
-
   const float vmax = __uint_as_float(a.vmax_bits[s]);
   const float vm2f = vmax * vmax;
   const double vm2d = (double)vmax * (double)vmax;
   const double inv_sqrt_d = 1.0 / sqrt((double)D);
   const float c2 = (float)(kLog2e * inv_sqrt_d);
 
-  for (int j = threadIdx.x; j < N; j += 64 * WAVES)
-    s_rows[j] = rows_in ? rows_in[j] : (int32_t)(row_base + j);
-  for (int p = threadIdx.x; p < P; p += 64 * WAVES) s_alpha[p] = 0.0;
-  __syncthreads();
+  extern __shared__ __align__(16) unsigned char smem[];
+  float* s_h2 = reinterpret_cast<float*>(smem + NS * CH * 1024);
+  int64_t* s_rows = reinterpret_cast<int64_t*>(s_h2 + NS * 16);
+  // Row indices of every column row this workgroup loads, staged first: a
+  // data load then never waits on an index load issued behind the ring's
+  // outstanding loads.
+  const int j_end = min(N, (jt1 + DEPTH + 2) * 16);
+  for (int j = jt0 * 16 + (int)threadIdx.x; j < j_end; j += 64 * kScoreWaves)
+    s_rows[j - jt0 * 16] = rows_in ? (int64_t)rows_in[j] : row_base + j;
 
-  const int nblk = (N + BR - 1) / BR;
-  uint4 Ak[RT][NV], Av[RT][NV];
-  {
-    const int nrows = min(BR, N);
+  // ---- this wave's A rows and, in the first chunk, their pair terms ----
+  uint4 Ak[WRT][NV], Av[WRT][NV];
 #pragma unroll
-    for (int rt = 0; rt < RT; ++rt) {
-      const int jl = rt * 16 + m16;
-      const bool valid = jl < nrows;
-      const int64_t r = valid ? s_rows[jl] : 0;
-      load_frag<T, D>(K, r, g, valid, Ak[rt]);
-      load_frag<T, D>(V, r, g, valid, Av[rt]);
-    }
+  for (int rt = 0; rt < WRT; ++rt) {
+    const int j = blk * 64 + (sub * WRT + rt) * 16 + m16;
+    const bool valid = has_blk && j < N;
+    const int64_t r = valid ? (rows_in ? (int64_t)rows_in[j] : row_base + j) : 0;
+    load_frag<T, D>(K, r, g, valid, Ak[rt]);
+    load_frag<T, D>(V, r, g, valid, Av[rt]);
+  }
+  if (chunk == 0 && has_blk) {
+    const int64_t pb = s * (a.n_r >> 1) + t * (int64_t)P;
 #pragma unroll
-    for (int rt = 0; rt < RT; ++rt) {
-      if (rt % WAVES != wave) continue;
+    for (int rt = 0; rt < WRT; ++rt) {
       float h2f, lbt;
       frag_pair_terms<T, D>(Ak[rt], Av[rt], vm2d, inv_sqrt_d, h2f, lbt);
-      const int jl = rt * 16 + m16;
-      if (g == 0 && jl < nrows && (jl & 1) == 0) {
-        s_h2[jl >> 1] = h2f;
-        s_lbt[jl >> 1] = lbt;
+      const int j = blk * 64 + (sub * WRT + rt) * 16 + m16;
+      if (g == 0 && j < N && (j & 1) == 0) {
+        a.h2[pb + (j >> 1)] = h2f;
+        a.lbt[pb + (j >> 1)] = lbt;
       }
     }
   }
-  // v_max enters the V Gram as one extra k-chunk: B holds v_max in slot 0 of
-  // lane group 0, A holds +-v_max (the row's sign) there.
-  uint4 Baug = make_uint4(0, 0, 0, 0);
-  if (g == 0) Baug.x = Elem<T>::bytes == 2 ? (__float_as_uint(vmax) >> 16) : __float_as_uint(vmax);
+
+  // ---- column tile pipeline ----
+  // chunk c of tile jt: lane l holds row jt*16 + l%16 (clamped to the
+  // bucket; rows past the end are never read back), word 4(c%NV) + l/16, of
+  // K (c < NV) or V.
+  u32x4 stg[DEPTH][LPT];
+#define SCORE_ISSUE(JT, SLOT)                                                        \
+  do {                                                                               \
+    const int j_ = min((JT) * 16 + m16, N - 1);                                      \
+    const int64_t row_ = s_rows[j_ - jt0 * 16];                                      \
+    _Pragma("unroll") for (int k_ = 0; k_ < LPT; ++k_) {                             \
+      const int c_ = min(wave + k_ * kScoreWaves, CH - 1);                           \
+      const T* src_ = c_ < NV ? K : V;                                               \
+      stg[SLOT][k_] = reinterpret_cast<const u32x4*>(src_ + row_ * D)[4 * (c_ % NV) + g]; \
+    }                                                                                \
+  } while (0)
+#define SCORE_COMMIT(STAGE, SLOT)                                                    \
+  do {                                                                               \
+    _Pragma("unroll") for (int k_ = 0; k_ < LPT; ++k_) {                             \
+      const int c_ = wave + k_ * kScoreWaves;                                        \
+      if (c_ < CH) reinterpret_cast<u32x4*>(smem + ((STAGE) * CH + c_) * 1024)[lane] = stg[SLOT][k_]; \
+    }                                                                                \
+  } while (0)
+  auto tile_h2 = [&](int stage) {  // scale exponents of a staged tile's 16 rows
+    uint4 bk[NV];
+#pragma unroll
+    for (int v = 0; v < NV; ++v) bk[v] = reinterpret_cast<const uint4*>(smem + (stage * CH + v) * 1024)[lane];
+    const float h = pair_h2f(sum_quarters(quarter_self_dot<T, D>(bk)), inv_sqrt_d);
+    if (g == 0) s_h2[stage * 16 + m16] = h;
+  };
+
+  __syncthreads();
+#pragma unroll
+  for (int k = 0; k < DEPTH; ++k) SCORE_ISSUE(jt0 + k, k);
+  SCORE_COMMIT(0, 0);
+  SCORE_COMMIT(1, 1);
+  SCORE_ISSUE(jt0 + DEPTH, 0);
+  SCORE_ISSUE(jt0 + DEPTH + 1, 1);
+  __syncthreads();
+  if (wave == 0) tile_h2(0);
+  __syncthreads();
+
+  float* Eb = a.E + (bl * a.e_tiles + panel_tiles(blk, NT, 4) - (int64_t)blk * 4) * TILE;
+  const int jt_own = blk * 4;  // the block's first column tile
+  const int ntile = jt1 - jt0;
+  // Gram accumulators of two tiles: the MFMAs of tile i+1 are issued before
+  // the exp epilogue of tile i, so the two overlap.
+  floatx4_t gk[2][WRT], gv[2][WRT];
+#define SCORE_MMA(STAGE, SLOT)                                                          \
+  do {                                                                                  \
+    uint4 bk_[NV], bv_[NV];                                                             \
+    _Pragma("unroll") for (int v_ = 0; v_ < NV; ++v_) {                                 \
+      bk_[v_] = reinterpret_cast<const uint4*>(smem + ((STAGE) * CH + v_) * 1024)[lane]; \
+      bv_[v_] = reinterpret_cast<const uint4*>(smem + ((STAGE) * CH + NV + v_) * 1024)[lane]; \
+    }                                                                                   \
+    _Pragma("unroll") for (int rt_ = 0; rt_ < WRT; ++rt_) {                             \
+      gk[SLOT][rt_] = (floatx4_t){0.f, 0.f, 0.f, 0.f};                                  \
+      gv[SLOT][rt_] = (floatx4_t){vm2f, vm2f, vm2f, vm2f}; /* <v,v'> + v_max^2 */      \
+    }                                                                                   \
+    _Pragma("unroll") for (int v_ = 0; v_ < NV; ++v_)                                   \
+      _Pragma("unroll") for (int rt_ = 0; rt_ < WRT; ++rt_) {                           \
+        gk[SLOT][rt_] = mma_word<T>(Ak[rt_][v_], bk_[v_], gk[SLOT][rt_]);               \
+        gv[SLOT][rt_] = mma_word<T>(Av[rt_][v_], bv_[v_], gv[SLOT][rt_]);               \
+      }                                                                                 \
+  } while (0)
+
+  if (has_blk && jt0 >= jt_own) SCORE_MMA(0, 0);
+  for (int ib = 0; ib < ntile; ib += DEPTH) {
+#pragma unroll
+    for (int u = 0; u < DEPTH; ++u) {
+      const int i = ib + u;
+      const int jt = jt0 + i;
+      if (i < ntile) {  // uniform over the workgroup
+        // scale of tile i+1; stage tile i+2; load tile i+2+DEPTH
+        if (wave == i % kScoreWaves) tile_h2((u + 1) % NS);
+        SCORE_COMMIT((u + 2) % NS, (u + 2) % DEPTH);
+        SCORE_ISSUE(jt + 2 + DEPTH, (u + 2) % DEPTH);
+        // Gram of tile i+1 (staged and visible since the last barrier)
+        if (has_blk && i + 1 < ntile && jt + 1 >= jt_own) SCORE_MMA((u + 1) % NS, (u + 1) & 1);
+        // scores of tile i
+        if (has_blk && jt >= jt_own) {
+          const float h2 = jt * 16 + m16 < N ? s_h2[(u % NS) * 16 + m16] : 0.0f;
+          float* tile = Eb + (int64_t)jt * TILE;
+#pragma unroll
+          for (int rt = 0; rt < WRT; ++rt) {
+            float kap[4];
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+              kap[e] = __builtin_amdgcn_exp2f(fminf(gk[u & 1][rt][e] * c2 - h2, kExpClamp)) *
+                       gv[u & 1][rt][e];
+            // lane (g, m16) holds kappa(A row 4g+e, column row m16): A pairs
+            // 2g, 2g+1 of the row tile against column row m16
+            const float F0 = kap[1] - kap[0];
+            const float F1 = kap[3] - kap[2];
+            const float F0p = from_partner(F0);
+            const float F1p = from_partner(F1);
+            if ((m16 & 1) == 0)
+              *reinterpret_cast<float2*>(tile + (m16 >> 1) * BP + (sub * WRT + rt) * 8 + 2 * g) =
+                  make_float2(F0 - F0p, F1 - F1p);
+          }
+        }
+        __syncthreads();
+      }
+    }
+  }
+#undef SCORE_MMA
+#undef SCORE_ISSUE
+#undef SCORE_COMMIT
+}
+
+template <int RT, int WAVES>
+__global__ __launch_bounds__(64 * WAVES) void halve_pass_kernel(HalveArgs a) {
+  constexpr int BR = 16 * RT;
+  constexpr int BP = BR / 2;
+  constexpr int TILE = 8 * BP;
+  static_assert(BP <= 32, "decisions use lanes 0..31 of one wavefront");
+
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const int64_t bl = blockIdx.x;
+  const int64_t bucket = a.b0 + bl;
+  const int64_t s = bucket / a.G;
+  const int64_t t = bucket % a.G;
+  const int N = a.N;
+  const int P = N >> 1;
+  const int NT = (N + 15) >> 4;
+  const int nblk = (P + BP - 1) / BP;
+  const int32_t* rows_in = a.idx_in ? a.idx_in + s * a.n_r + t * (int64_t)N : nullptr;
+  const int64_t row_base = t * (int64_t)N;
+  const float* Ub = a.U + s * a.u_slice + a.u_off + t * (int64_t)P;
+  uint8_t* trace = a.trace ? a.trace + s * a.u_slice + a.u_off + t * (int64_t)P : nullptr;
+  int32_t* out = a.idx_out + s * (a.n_r >> 1) + t * (int64_t)P;
+  const int64_t pb = s * (a.n_r >> 1) + t * (int64_t)P;
+  const float* Eb = a.E + bl * a.e_tiles * (int64_t)TILE;
+
+  extern __shared__ __align__(16) unsigned char smem[];
+  double* s_alpha = reinterpret_cast<double*>(smem);
+  uint32_t* s_mask = reinterpret_cast<uint32_t*>(s_alpha + P);
+  for (int p = threadIdx.x; p < P; p += 64 * WAVES) s_alpha[p] = 0.0;
   __syncthreads();
 
   double carry = -INFINITY;  // log b_max over the pairs already decided (wave 0)
   for (int blk = 0; blk < nblk; ++blk) {
-    const int rows0 = blk * BR;
-    const int nrows = min(BR, N - rows0);
-    const int npb = nrows >> 1;
-    const bool has_next = blk + 1 < nblk;
-    const float u_blk = (wave == 0 && lane < npb) ? Ub[blk * BP + lane] : 0.5f;
+    const int npb = min(BP, P - blk * BP);
+    const float* Ep = Eb + panel_tiles(blk, NT, RT) * TILE;  // column tile blk*RT first
 
-    // ---- 1. E(i,p) for the block's own pairs. ----
-#pragma unroll
-    for (int rtm = 0; rtm < RT; ++rtm)
-#pragma unroll
-      for (int rtn = rtm; rtn < RT; ++rtn) {
-        if ((rtm * RT + rtn) % WAVES != wave) continue;
-        floatx4_t gk = {0.f, 0.f, 0.f, 0.f}, gv = {0.f, 0.f, 0.f, 0.f};
-        gk = mma_rows<T, D>(Ak[rtm], Ak[rtn], gk);
-        gv = mma_rows<T, D>(Av[rtm], Av[rtn], gv);
-        const int tl = rtn * 16 + m16;  // column row (block-local)
-        const float h2_in = s_h2[min(blk * BP + (tl >> 1), P - 1)];
-        const float h2 = tl < nrows ? h2_in : 0.0f;
-        float kap[4];
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-          kap[i] = __builtin_amdgcn_exp2f(fminf(gk[i] * c2 - h2, kExpClamp)) * (gv[i] + vm2f);
-        const float F0 = kap[1] - kap[0];
-        const float F1 = kap[3] - kap[2];
-        const float F0p = from_partner(F0);
-        const float F1p = from_partner(F1);
-        if ((m16 & 1) == 0) {
-          const int i0 = rtm * 8 + 2 * g;
-          const int p = rtn * 8 + (m16 >> 1);
-          s_E[i0 * ES + p] = F0 - F0p;
-          s_E[(i0 + 1) * ES + p] = F1 - F1p;
-        }
-      }
-    __syncthreads();
-
-    // ---- 2. Sequential decisions (wave 0). ----
     if (wave == 0) {
       const int p = lane;
       const bool active = p < npb;
       const int gp = blk * BP + p;
       const int gpc = min(gp, P - 1);
       const double alpha_in = s_alpha[gpc];
-      const float lbt_in = s_lbt[gpc];
-      const float h2_in = s_h2[gpc];
+      const float lbt_in = a.lbt[pb + gpc];
+      const float h2_in = a.h2[pb + gpc];
+      const float u_blk = active ? Ub[gp] : 0.5f;
       double alpha = active ? alpha_in : 0.0;
       const float lbtf = active ? lbt_in : -INFINITY;
       const float h2f = active ? h2_in : 0.0f;
@@ -451,11 +611,16 @@ void halve_kernel(HalveArgs a) {
       } else {
         thr = exp_fast((double)lbtf + lbmax + a.log_c - half_h) * (1.0 - 2.0 * (double)u_blk);
       }
-      // unconditional LDS reads (in bounds for every lane), masked afterwards
-      const int pc = p < BP ? p : BP - 1;
+      // this pair's scores against the block's earlier pairs (lanes past the
+      // block's last pair read that pair's column, then are masked)
+      const int pc = p < npb ? p : npb - 1;
+      const float4* col = reinterpret_cast<const float4*>(Ep + (pc >> 3) * TILE + (pc & 7) * BP);
       float ecol[BP];
 #pragma unroll
-      for (int i = 0; i < BP; ++i) ecol[i] = s_E[i * ES + pc];
+      for (int q = 0; q < BP / 4; ++q) {
+        const float4 x = col[q];
+        ecol[4 * q] = x.x; ecol[4 * q + 1] = x.y; ecol[4 * q + 2] = x.z; ecol[4 * q + 3] = x.w;
+      }
 #pragma unroll
       for (int i = 0; i < BP; ++i) ecol[i] = (active && p > i) ? ecol[i] : 0.0f;
       uint64_t smask = 0;
@@ -472,117 +637,31 @@ void halve_kernel(HalveArgs a) {
       carry = __shfl(lbmax, npb - 1);
       if (active) {
         const uint32_t bit = (uint32_t)((smask >> p) & 1ull);
-        out[gp] = s_rows[rows0 + 2 * p + (int)bit];
+        const int j = blk * BR + 2 * p + (int)bit;
+        out[gp] = rows_in ? rows_in[j] : (int32_t)(row_base + j);
         if (trace) trace[gp] = (uint8_t)bit;
       }
-      if (lane == 0) {
-        s_mask[0] = (uint32_t)smask;
-        s_mask[1] = (uint32_t)(smask >> 32);
-      }
+      if (lane == 0) s_mask[0] = (uint32_t)smask;
     }
     __syncthreads();
-    if (!has_next) break;
+    if (blk + 1 == nblk) break;
 
-    // ---- 3. Contribution of this block to every later pair. ----
-    const uint64_t smask = (uint64_t)s_mask[0] | ((uint64_t)s_mask[1] << 32);
-    // Row weights: +1 for the element that went to coreset 2, -1 for coreset 1.
-    // V rows and their v_max slot carry the sign.
-    uint4 Aaug[RT];
+    // The block's signed scores, added to every later pair (one lane per pair).
+    const uint32_t smask = s_mask[0];
+    for (int cb = (blk + 1) * BP + wave * 64; cb < P; cb += 64 * WAVES) {
+      const int p = cb + lane;
+      if (p < P) {
+        const float4* col =
+            reinterpret_cast<const float4*>(Ep + ((p >> 3) - blk * RT) * TILE + (p & 7) * BP);
+        float sum = 0.0f;
 #pragma unroll
-    for (int rt = 0; rt < RT; ++rt) {
-      const int jl = rt * 16 + m16;
-      const uint32_t bit = (uint32_t)((smask >> (jl >> 1)) & 1ull);
-      const bool neg = (bit != 0) == ((jl & 1) != 0);
-      const bool live = jl < nrows;
-      if (live && neg) {
+        for (int q = 0; q < BP / 4; ++q) {
+          const float4 x = col[q];
+          const float e[4] = {x.x, x.y, x.z, x.w};
 #pragma unroll
-        for (int v = 0; v < NV; ++v) {
-          Av[rt][v].x ^= Elem<T>::sign_mask;
-          Av[rt][v].y ^= Elem<T>::sign_mask;
-          Av[rt][v].z ^= Elem<T>::sign_mask;
-          Av[rt][v].w ^= Elem<T>::sign_mask;
+          for (int c = 0; c < 4; ++c) sum += ((smask >> (4 * q + c)) & 1u) ? -e[c] : e[c];
         }
-      }
-      Aaug[rt] = make_uint4(0, 0, 0, 0);
-      if (live) Aaug[rt].x = Baug.x ^ (neg ? (Elem<T>::bytes == 2 ? 0x8000u : 0x80000000u) : 0u);
-    }
-    const int later0 = rows0 + BR;
-    const int ntiles = (N - later0 + 15) >> 4;
-    // Ring of PF column tiles in flight (tile ct + u * WAVES sits in slot u).
-    constexpr int PF = HALVE_PF;
-    uint4 Bk[PF][NV], Bv[PF][NV];
-#pragma unroll
-    for (int u = 0; u < PF; ++u) {
-      const int ct = wave + u * WAVES;
-      const int64_t r = s_rows[min(later0 + ct * 16 + m16, N - 1)];
-      load_frag<T, D>(K, r, g, true, Bk[u]);
-      load_frag<T, D>(V, r, g, true, Bv[u]);
-    }
-    for (int ct0 = wave; ct0 < ntiles; ct0 += PF * WAVES) {
-#pragma unroll
-      for (int u = 0; u < PF; ++u) {
-        const int ct = ct0 + u * WAVES;
-        if (ct >= ntiles) break;
-        const int tl = later0 + ct * 16 + m16;
-        const bool valid = tl < N;
-        float h2;
-        if (blk == 0) {  // first time these rows are loaded: their pair terms
-          float lbt;
-          frag_pair_terms<T, D>(Bk[u], Bv[u], vm2d, inv_sqrt_d, h2, lbt);
-          if (g == 0 && valid && (tl & 1) == 0) {
-            s_h2[tl >> 1] = h2;
-            s_lbt[tl >> 1] = lbt;
-          }
-          if (!valid) h2 = 0.0f;
-        } else {
-          const float h2_in = s_h2[min(tl, N - 1) >> 1];
-          h2 = valid ? h2_in : 0.0f;
-        }
-        // 2*RT independent accumulators, k-chunk outermost, so consecutive
-        // MFMAs never depend on each other.
-        floatx4_t gk[RT], gv[RT];
-#pragma unroll
-        for (int rt = 0; rt < RT; ++rt) {
-          gk[rt] = (floatx4_t){0.f, 0.f, 0.f, 0.f};
-          gv[rt] = mma_aug<T>(Aaug[rt], Baug, (floatx4_t){0.f, 0.f, 0.f, 0.f});
-        }
-#pragma unroll
-        for (int v = 0; v < NV; ++v)
-#pragma unroll
-          for (int rt = 0; rt < RT; ++rt) {
-            gk[rt] = mma_word<T>(Ak[rt][v], Bk[u][v], gk[rt]);
-            gv[rt] = mma_word<T>(Av[rt][v], Bv[u][v], gv[rt]);
-          }
-        float acc = 0.0f;
-#pragma unroll
-        for (int rt = 0; rt < RT; ++rt)
-#pragma unroll
-          for (int i = 0; i < 4; ++i)
-            acc = fmaf(__builtin_amdgcn_exp2f(fminf(gk[rt][i] * c2 - h2, kExpClamp)), gv[rt][i], acc);
-        // Refill this slot with the tile PF steps ahead.
-        {
-          // (rows past the bucket end load a valid row; their results are unused)
-          const int nct = ct + PF * WAVES;
-          const int64_t r2 = s_rows[min(later0 + nct * 16 + m16, N - 1)];
-          load_frag<T, D>(K, r2, g, true, Bk[u]);
-          load_frag<T, D>(V, r2, g, true, Bv[u]);
-        }
-        const float dt = sum_quarters(acc);
-        const float dp = from_partner(dt);
-        if (g == 0 && valid && (tl & 1) == 0) atomicAdd(&s_alpha[tl >> 1], (double)dt - (double)dp);
-      }
-    }
-    // Next block's rows.
-    {
-      const int rows1 = rows0 + BR;
-      const int nrows1 = min(BR, N - rows1);
-#pragma unroll
-      for (int rt = 0; rt < RT; ++rt) {
-        const int jl = rt * 16 + m16;
-        const bool valid = jl < nrows1;
-        const int64_t r = valid ? s_rows[rows1 + jl] : 0;
-        load_frag<T, D>(K, r, g, valid, Ak[rt]);
-        load_frag<T, D>(V, r, g, valid, Av[rt]);
+        s_alpha[p] += (double)sum;
       }
     }
     __syncthreads();
@@ -604,64 +683,71 @@ __global__ __launch_bounds__(64) void gram16_kernel(const T* rows, float* out) {
   for (int i = 0; i < 4; ++i) out[(4 * g + i) * 16 + m16] = acc[i];
 }
 
-#ifndef HALVE_RT128
-#define HALVE_RT128 4
-#endif
 template <typename T, int D>
-constexpr int rt_for() {
-  return (Elem<T>::bytes == 4 && D == 128) ? 2 : (D == 128 ? HALVE_RT128 : 4);
-}
-
-template <typename T, int D, int WAVES>
-hipError_t launch_halve_t(const HalveArgs& a, size_t lds, hipStream_t st) {
-  constexpr int RT = rt_for<T, D>();
-  auto kern = halve_kernel<T, D, RT, WAVES>;
+hipError_t launch_scores_td(const HalveArgs& a, int64_t nbk, hipStream_t st) {
+  using SS = ScoreShape<T, D>;
+  auto kern = pair_scores_kernel<T, D>;
+  const size_t lds = SS::LDS;
   if (lds > 64 * 1024) {
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess) return e;
   }
-  dim3 grid((unsigned)(a.S * a.G)), block(64 * WAVES);
-  hipLaunchKernelGGL(kern, grid, block, lds, st, a);
+  const int64_t NT = (a.N + 15) / 16;
+  const int64_t nb = (a.N + 63) / 64;
+  const int64_t groups = (nb + SS::BLOCKS - 1) / SS::BLOCKS;
+  const int64_t nch = (NT + a.ch - 1) / a.ch;
+  dim3 grid((unsigned)nbk, (unsigned)groups, (unsigned)nch);
+  hipLaunchKernelGGL(kern, grid, dim3(64 * kScoreWaves), lds, st, a);
   return hipGetLastError();
 }
 
-template <typename T, int D>
-hipError_t launch_halve_d(const HalveArgs& a, size_t lds, hipStream_t st) {
-  // Enough waves in flight for the 256 CUs x 4 SIMDs x HALVE_WPE waves, at
-  // most eight per bucket.
-  const int64_t slots = 1024 * HALVE_WPE;  // one wave per SIMD per unit
-  const int64_t buckets = a.S * (int64_t)a.G;
-  if (buckets >= slots || a.N <= 64) return launch_halve_t<T, D, 1>(a, lds, st);
-  if (buckets * 2 >= slots) return launch_halve_t<T, D, 2>(a, lds, st);
-  if (buckets * 4 >= slots || HALVE_WPE == 1) return launch_halve_t<T, D, 4>(a, lds, st);
-  return launch_halve_t<T, D, 8>(a, lds, st);
-}
-
 template <typename T>
-hipError_t launch_halve_dt(int64_t d, const HalveArgs& a, size_t lds, hipStream_t st) {
+hipError_t launch_scores_t(int64_t d, const HalveArgs& a, int64_t nbk, hipStream_t st) {
   switch (d) {
-    case 32: return launch_halve_d<T, 32>(a, lds, st);
-    case 64: return launch_halve_d<T, 64>(a, lds, st);
-    case 128: return launch_halve_d<T, 128>(a, lds, st);
+    case 32: return launch_scores_td<T, 32>(a, nbk, st);
+    case 64: return launch_scores_td<T, 64>(a, nbk, st);
+    case 128: return launch_scores_td<T, 128>(a, nbk, st);
     default: return hipErrorInvalidValue;
   }
 }
 
-}  // namespace
-
-size_t halve_lds_bytes(int dtype, int64_t d, int32_t N) {
-  const int RT = (dtype == 0 && d == 128) ? 2 : (d == 128 ? HALVE_RT128 : 4);
-  const int BP = 8 * RT;
-  const size_t P = (size_t)N / 2;
-  // alpha (f64), lbt, h2 per pair; E tile; mask words; row indices
-  return P * (8 + 4 + 4) + (size_t)BP * (BP + 1) * 4 + 16 + (size_t)N * 4;
+template <int WAVES>
+hipError_t launch_pass_w(const HalveArgs& a, int64_t nbk, hipStream_t st) {
+  const size_t lds = (size_t)(a.N / 2) * 8 + 16;  // alpha per pair, decision mask
+  auto kern = halve_pass_kernel<4, WAVES>;
+  if (lds > 64 * 1024) {
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e != hipSuccess) return e;
+  }
+  hipLaunchKernelGGL(kern, dim3((unsigned)nbk), dim3(64 * WAVES), lds, st, a);
+  return hipGetLastError();
 }
 
-hipError_t launch_halve(int dtype, int64_t d, const HalveArgs& a, hipStream_t st) {
-  const size_t lds = halve_lds_bytes(dtype, d, a.N);
-  if (dtype == 0) return launch_halve_dt<float>(d, a, lds, st);
-  return launch_halve_dt<bf16_t>(d, a, lds, st);
+}  // namespace
+
+int64_t halve_score_tiles(int64_t N) {
+  const int64_t NT = (N + 15) / 16;
+  const int64_t nb = (N + 63) / 64;
+  return panel_tiles(nb, NT, 4);
+}
+
+size_t halve_score_bytes(int64_t N) {
+  return (size_t)halve_score_tiles(N) * 8 * 32 * 4;  // tiles of 8 columns x 32 rows, float32
+}
+
+hipError_t launch_halve(int dtype, int64_t d, const HalveArgs& a0, int64_t nbk, hipStream_t st) {
+  HalveArgs a = a0;
+  a.ch = kScoreChunk;
+  a.e_tiles = halve_score_tiles(a.N);
+  hipError_t e = dtype == 0 ? launch_scores_t<float>(d, a, nbk, st)
+                            : launch_scores_t<bf16_t>(d, a, nbk, st);
+  if (e != hipSuccess) return e;
+  const int64_t later = a.N / 2 - 32;  // pairs after the first block
+  if (later <= 64) return launch_pass_w<1>(a, nbk, st);
+  if (later <= 128) return launch_pass_w<2>(a, nbk, st);
+  return launch_pass_w<4>(a, nbk, st);
 }
 
 hipError_t launch_vmax(int dtype, const void* V, int64_t S, int64_t n, int64_t d,

@@ -6,7 +6,7 @@
 
 namespace thin {
 
-// One Halve round over all buckets of all slices.
+// One Halve round over buckets b0 .. b0 + nbk - 1 (bucket = slice * G + t).
 struct HalveArgs {
   const void* K;
   const void* V;
@@ -23,6 +23,12 @@ struct HalveArgs {
   int64_t u_off;              // offset of this round's draws within a slice
   uint8_t* trace;             // nullable, indexed like U
   double log_c;               // log(1/2 + log(2N/delta))
+  float* E;                   // pair scores of the launched buckets (halve_score_bytes each)
+  float* lbt;                 // [S, n_r / 2] scaled log b per pair
+  float* h2;                  // [S, n_r / 2] scale exponent per pair
+  int64_t b0;                 // first bucket of this launch
+  int64_t e_tiles;            // score tiles per bucket (set by launch_halve)
+  int32_t ch;                 // column tiles per score workgroup (set by launch_halve)
 };
 
 // dtype: 0 = fp32, 1 = bf16.  Returns a hipError_t.
@@ -33,8 +39,11 @@ hipError_t launch_subsample(int64_t S, int64_t n, int64_t n_kept, const float* U
 hipError_t launch_fill_rows(int64_t S, int64_t n_out, const int32_t* src, int64_t src_stride,
                             int32_t* dst, hipStream_t st);
 hipError_t launch_zero_u8(uint8_t* p, int64_t count, hipStream_t st);
-hipError_t launch_halve(int dtype, int64_t d, const HalveArgs& a, hipStream_t st);
-size_t halve_lds_bytes(int dtype, int64_t d, int32_t N);
+// Score tiles and score bytes of one N-row bucket (64-row decision blocks).
+int64_t halve_score_tiles(int64_t N);
+size_t halve_score_bytes(int64_t N);
+// Pair scores, then decisions, for nbk buckets starting at a.b0.
+hipError_t launch_halve(int dtype, int64_t d, const HalveArgs& a, int64_t nbk, hipStream_t st);
 
 hipError_t launch_attention(int dtype, int64_t d, int out_dtype, const void* Q, const void* K,
                             const void* V, const int32_t* idx, int64_t S, int64_t n,

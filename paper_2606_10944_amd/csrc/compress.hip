@@ -552,15 +552,56 @@ __global__ __launch_bounds__(64 * kScoreWaves) void pair_scores_kernel(HalveArgs
 #undef SCORE_COMMIT
 }
 
-template <int RT, int WAVES>
-__global__ __launch_bounds__(64 * WAVES) void halve_pass_kernel(HalveArgs a) {
+// Decision pass of one bucket per workgroup, in three roles that run ahead
+// of or behind each other, synchronised by progress counters in LDS:
+//  - wave 0 (decider) takes the decisions block after block;
+//  - wave 1 adds each decided block's scores to the next block's pairs (the
+//    only update on the decider's critical path) and fetches the decider's
+//    inputs two blocks ahead;
+//  - waves 2.. (bulk) add each decided block's scores to all pairs two or
+//    more blocks later.
+// alpha of a pair in block m = (contributions of blocks <= m-2, summed by the
+// bulk waves in block order) + (contribution of block m-1, from wave 1).
+// Everything read from global memory is independent of the decisions and is
+// fetched ahead; the decider never waits on global memory.  Every wait is
+// bounded.
+constexpr int kSpinLimit = 1 << 16;
+
+__device__ __forceinline__ void wait_at_least(const int* flag, int target) {
+  for (int it = 0; it < kSpinLimit; ++it) {
+    if (__hip_atomic_load(flag, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_WORKGROUP) >= target) return;
+    __builtin_amdgcn_s_sleep(1);
+  }
+}
+__device__ __forceinline__ void publish(int* flag, int value) {
+  __hip_atomic_store(flag, value, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
+}
+
+template <int BW, int NCB>
+struct PassLds {
+  static constexpr int BP = 32, QW = 8;
+  // alpha [P] | near alpha [2][BP] | mask ring [4] | counters [2 + BW] |
+  // decision inputs [3]: scores [BP][QW] words, then lbt, h2, u, row0, row1 [BP]
+  __host__ __device__ static size_t near_off(int P) { return ((size_t)P * 8 + 15) & ~(size_t)15; }
+  __host__ __device__ static size_t mask_off(int P) { return near_off(P) + 2 * BP * 8; }
+  __host__ __device__ static size_t flag_off(int P) { return mask_off(P) + 16; }
+  __host__ __device__ static size_t dcol_off(int P) { return (flag_off(P) + (2 + BW) * 4 + 15) & ~(size_t)15; }
+  __host__ __device__ static size_t dsc_off(int P) { return dcol_off(P) + 3 * BP * QW * 16; }
+  __host__ __device__ static size_t bytes(int P) { return dsc_off(P) + 3 * 5 * BP * 4; }
+};
+
+template <int BW, int NCB>
+__global__ __launch_bounds__(64 * (BW + 2)) void halve_pass_kernel(HalveArgs a) {
+  using L = PassLds<BW, NCB>;
+  constexpr int RT = 4;
   constexpr int BR = 16 * RT;
   constexpr int BP = BR / 2;
   constexpr int TILE = 8 * BP;
-  static_assert(BP <= 32, "decisions use lanes 0..31 of one wavefront");
+  constexpr int QW = BP / 4;  // 16-byte words per score column
+  static_assert(BP == L::BP && QW == L::QW, "layout");
 
   const int lane = threadIdx.x & 63;
-  const int wave = threadIdx.x >> 6;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int64_t bl = blockIdx.x;
   const int64_t bucket = a.b0 + bl;
   const int64_t s = bucket / a.G;
@@ -576,30 +617,124 @@ __global__ __launch_bounds__(64 * WAVES) void halve_pass_kernel(HalveArgs a) {
   int32_t* out = a.idx_out + s * (a.n_r >> 1) + t * (int64_t)P;
   const int64_t pb = s * (a.n_r >> 1) + t * (int64_t)P;
   const float* Eb = a.E + bl * a.e_tiles * (int64_t)TILE;
+  // a valid address for the row loads of round 0 (their values are replaced)
+  const int32_t* rsrc = rows_in ? rows_in : reinterpret_cast<const int32_t*>(Ub);
 
   extern __shared__ __align__(16) unsigned char smem[];
   double* s_alpha = reinterpret_cast<double*>(smem);
-  uint32_t* s_mask = reinterpret_cast<uint32_t*>(s_alpha + P);
-  for (int p = threadIdx.x; p < P; p += 64 * WAVES) s_alpha[p] = 0.0;
+  double* s_anear = reinterpret_cast<double*>(smem + L::near_off(P));
+  uint32_t* s_mask = reinterpret_cast<uint32_t*>(smem + L::mask_off(P));
+  int* s_flag = reinterpret_cast<int*>(smem + L::flag_off(P));  // decided, near, bulk[BW]
+  u32x4* s_dcol = reinterpret_cast<u32x4*>(smem + L::dcol_off(P));
+  uint32_t* s_dsc = reinterpret_cast<uint32_t*>(smem + L::dsc_off(P));
+
+  for (int p = threadIdx.x; p < P; p += 64 * (BW + 2)) s_alpha[p] = 0.0;
+  if (threadIdx.x < 2 + BW) s_flag[threadIdx.x] = -1;
+
+  // Signed sum of a column's BP scores (decision bits in SMASK).
+#define PASS_SUM(SRC, SMASK, SUM)                                                       \
+  do {                                                                                 \
+    SUM = 0.0f;                                                                        \
+    _Pragma("unroll") for (int q_ = 0; q_ < QW; ++q_) {                                \
+      const float e_[4] = {__uint_as_float(SRC[q_].x), __uint_as_float(SRC[q_].y),     \
+                           __uint_as_float(SRC[q_].z), __uint_as_float(SRC[q_].w)};    \
+      _Pragma("unroll") for (int c_ = 0; c_ < 4; ++c_)                                 \
+        SUM += (((SMASK) >> (4 * q_ + c_)) & 1u) ? -e_[c_] : e_[c_];                   \
+    }                                                                                  \
+  } while (0)
+  // Column of pair P_ in block B's score panel (P_ after block B).
+#define PASS_COL(B, P_)                                                                 \
+  reinterpret_cast<const u32x4*>(Eb + (panel_tiles(B, NT, RT) + ((P_) >> 3) - (B) * RT) * TILE + \
+                                 ((P_) & 7) * BP)
+  // Decision inputs of block B (wave 1): lane l loads word l%QW of the
+  // columns of pairs l/QW + 8r; lanes < BP also the pair terms, uniform and
+  // rows of pair l.  Lanes past the block's last pair read that pair's.
+#define PASS_FETCH_DEC(B)                                                               \
+  do {                                                                                 \
+    const int npb_ = min(BP, P - (B) * BP);                                            \
+    const float* e_ = Eb + panel_tiles(B, NT, RT) * TILE;                              \
+    _Pragma("unroll") for (int r_ = 0; r_ < 4; ++r_) {                                 \
+      const int pc_ = min(lane / QW + 8 * r_, npb_ - 1);                               \
+      fdc[r_] = reinterpret_cast<const u32x4*>(e_ + (pc_ >> 3) * TILE + (pc_ & 7) * BP)[lane % QW]; \
+    }                                                                                  \
+    const int gp_ = (B) * BP + min(lane & (BP - 1), npb_ - 1);                         \
+    fsc[0] = __float_as_uint(a.lbt[pb + gp_]);                                         \
+    fsc[1] = __float_as_uint(a.h2[pb + gp_]);                                          \
+    fsc[2] = __float_as_uint(Ub[gp_]);                                                 \
+    fsc[3] = (uint32_t)rsrc[rows_in ? 2 * gp_ : 0];                                    \
+    fsc[4] = (uint32_t)rsrc[rows_in ? 2 * gp_ + 1 : 0];                                \
+    if (!rows_in) {                                                                    \
+      fsc[3] = (uint32_t)(row_base + 2 * gp_);                                         \
+      fsc[4] = (uint32_t)(row_base + 2 * gp_ + 1);                                     \
+    }                                                                                  \
+  } while (0)
+#define PASS_STORE_DEC(B)                                                               \
+  do {                                                                                 \
+    u32x4* d_ = s_dcol + ((B) % 3) * BP * QW;                                          \
+    _Pragma("unroll") for (int r_ = 0; r_ < 4; ++r_) d_[(lane / QW + 8 * r_) * QW + lane % QW] = fdc[r_]; \
+    if (lane < BP) {                                                                   \
+      uint32_t* c_ = s_dsc + ((B) % 3) * 5 * BP;                                       \
+      _Pragma("unroll") for (int k_ = 0; k_ < 5; ++k_) c_[k_ * BP + lane] = fsc[k_];   \
+    }                                                                                  \
+  } while (0)
+  // Near update data of block B: the columns of block B+1's pairs (lanes
+  // 32..63 repeat lanes 0..31; lanes past the last pair read the last pair).
+#define PASS_FETCH_NEAR(B)                                                              \
+  do {                                                                                 \
+    const int p_ = min(((B) + 1) * BP + (lane & (BP - 1)), P - 1);                     \
+    const u32x4* c_ = PASS_COL(B, p_);                                                 \
+    _Pragma("unroll") for (int q_ = 0; q_ < QW; ++q_) fnr[q_] = c_[q_];                \
+  } while (0)
+  // Bulk chunk k of block B for bulk wave w: pairs (B+2) BP + (w + k BW) 64 + lane.
+#define PASS_FETCH_CHUNK(B, K, DST)                                                     \
+  do {                                                                                 \
+    const int p_ = min(((B) + 2) * BP + (wave - 2 + (K) * BW) * 64 + lane, P - 1);     \
+    const u32x4* c_ = PASS_COL(B, p_);                                                 \
+    _Pragma("unroll") for (int q_ = 0; q_ < QW; ++q_) DST[q_] = c_[q_];                \
+  } while (0)
+
+  u32x4 fdc[4], fnr[QW], cb[NCB][QW];
+  uint32_t fsc[5];
+  if (wave == 1) {
+    PASS_FETCH_DEC(0);
+    PASS_STORE_DEC(0);
+    if (nblk > 1) {
+      PASS_FETCH_DEC(1);
+      PASS_STORE_DEC(1);
+      PASS_FETCH_NEAR(0);
+    }
+    if (nblk > 2) PASS_FETCH_DEC(2);
+  } else if (wave >= 2 && nblk > 2) {
+#pragma unroll
+    for (int k = 0; k < NCB; ++k) PASS_FETCH_CHUNK(0, k, cb[k]);
+  }
   __syncthreads();
 
-  double carry = -INFINITY;  // log b_max over the pairs already decided (wave 0)
-  for (int blk = 0; blk < nblk; ++blk) {
-    const int npb = min(BP, P - blk * BP);
-    const float* Ep = Eb + panel_tiles(blk, NT, RT) * TILE;  // column tile blk*RT first
-
-    if (wave == 0) {
+  if (wave == 0) {
+    // ---- decider ----
+    double carry = -INFINITY;  // log b_max over the pairs already decided
+    for (int m = 0; m < nblk; ++m) {
+      const int npb = min(BP, P - m * BP);
+      if (m >= 1) wait_at_least(&s_flag[1], m - 1);
+      if (m >= 2)
+        for (int w = 0; w < BW; ++w) wait_at_least(&s_flag[2 + w], m - 2);
       const int p = lane;
       const bool active = p < npb;
-      const int gp = blk * BP + p;
-      const int gpc = min(gp, P - 1);
-      const double alpha_in = s_alpha[gpc];
-      const float lbt_in = a.lbt[pb + gpc];
-      const float h2_in = a.h2[pb + gpc];
-      const float u_blk = active ? Ub[gp] : 0.5f;
+      const int gp = m * BP + p;
+      const int pl = lane & (BP - 1);
+      const uint32_t* sc = s_dsc + (m % 3) * 5 * BP;
+      const u32x4* dc = s_dcol + (m % 3) * BP * QW + pl * QW;
+      const double anear = m >= 1 ? s_anear[(m & 1) * BP + pl] : 0.0;
+      const double alpha_in = s_alpha[min(gp, P - 1)] + anear;
+      const float lbt_in = __uint_as_float(sc[pl]);
+      const float h2_in = __uint_as_float(sc[BP + pl]);
+      const float u_in = __uint_as_float(sc[2 * BP + pl]);
+      const int32_t r0 = (int32_t)sc[3 * BP + pl];
+      const int32_t r1 = (int32_t)sc[4 * BP + pl];
       double alpha = active ? alpha_in : 0.0;
       const float lbtf = active ? lbt_in : -INFINITY;
       const float h2f = active ? h2_in : 0.0f;
+      const float u_blk = active ? u_in : 0.5f;
       const double half_h = (double)h2f * (0.5 * kLn2);
       // running maximum of log b over this block's pairs (pair order), then
       // combined with the maximum over all earlier blocks
@@ -611,15 +746,15 @@ __global__ __launch_bounds__(64 * WAVES) void halve_pass_kernel(HalveArgs a) {
       } else {
         thr = exp_fast((double)lbtf + lbmax + a.log_c - half_h) * (1.0 - 2.0 * (double)u_blk);
       }
-      // this pair's scores against the block's earlier pairs (lanes past the
-      // block's last pair read that pair's column, then are masked)
-      const int pc = p < npb ? p : npb - 1;
-      const float4* col = reinterpret_cast<const float4*>(Ep + (pc >> 3) * TILE + (pc & 7) * BP);
+      // this pair's scores against the block's earlier pairs
       float ecol[BP];
 #pragma unroll
-      for (int q = 0; q < BP / 4; ++q) {
-        const float4 x = col[q];
-        ecol[4 * q] = x.x; ecol[4 * q + 1] = x.y; ecol[4 * q + 2] = x.z; ecol[4 * q + 3] = x.w;
+      for (int q = 0; q < QW; ++q) {
+        const u32x4 x = dc[q];
+        ecol[4 * q] = __uint_as_float(x.x);
+        ecol[4 * q + 1] = __uint_as_float(x.y);
+        ecol[4 * q + 2] = __uint_as_float(x.z);
+        ecol[4 * q + 3] = __uint_as_float(x.w);
       }
 #pragma unroll
       for (int i = 0; i < BP; ++i) ecol[i] = (active && p > i) ? ecol[i] : 0.0f;
@@ -635,41 +770,67 @@ __global__ __launch_bounds__(64 * WAVES) void halve_pass_kernel(HalveArgs a) {
         }
       }
       carry = __shfl(lbmax, npb - 1);
+      const uint32_t bit = (uint32_t)((smask >> p) & 1ull);
       if (active) {
-        const uint32_t bit = (uint32_t)((smask >> p) & 1ull);
-        const int j = blk * BR + 2 * p + (int)bit;
-        out[gp] = rows_in ? rows_in[j] : (int32_t)(row_base + j);
+        out[gp] = bit ? r1 : r0;
         if (trace) trace[gp] = (uint8_t)bit;
       }
-      if (lane == 0) s_mask[0] = (uint32_t)smask;
+      if (lane == 0) s_mask[m & 3] = (uint32_t)smask;
+      publish(&s_flag[0], m);
     }
-    __syncthreads();
-    if (blk + 1 == nblk) break;
-
-    // The block's signed scores, added to every later pair (one lane per pair).
-    const uint32_t smask = s_mask[0];
-    for (int cb = (blk + 1) * BP + wave * 64; cb < P; cb += 64 * WAVES) {
-      const int p = cb + lane;
-      if (p < P) {
-        const float4* col =
-            reinterpret_cast<const float4*>(Ep + ((p >> 3) - blk * RT) * TILE + (p & 7) * BP);
-        float sum = 0.0f;
+  } else if (wave == 1) {
+    // ---- next-block updates and the decider's inputs ----
+    for (int b = 0; b + 1 < nblk; ++b) {
+      wait_at_least(&s_flag[0], b);
+      const uint32_t smask = s_mask[b & 3];
+      float sum;
+      PASS_SUM(fnr, smask, sum);
+      if (lane < BP) s_anear[((b + 1) & 1) * BP + lane] = (double)sum;
+      publish(&s_flag[1], b);
+      if (b + 2 < nblk) {
+        PASS_STORE_DEC(b + 2);
+        PASS_FETCH_NEAR(b + 1);
+      }
+      if (b + 3 < nblk) PASS_FETCH_DEC(b + 3);
+    }
+  } else {
+    // ---- bulk updates, blocks 0 .. nblk-3 ----
+    for (int b = 0; b + 2 < nblk; ++b) {
+      wait_at_least(&s_flag[0], b);
+      const uint32_t smask = s_mask[b & 3];
+      const int p0 = (b + 2) * BP + (wave - 2) * 64 + lane;
 #pragma unroll
-        for (int q = 0; q < BP / 4; ++q) {
-          const float4 x = col[q];
-          const float e[4] = {x.x, x.y, x.z, x.w};
+      for (int k = 0; k < NCB; ++k) {
+        float sum;
+        PASS_SUM(cb[k], smask, sum);
+        const int p = p0 + 64 * BW * k;
+        if (p < P) s_alpha[p] += (double)sum;
+      }
+      for (int k = NCB; (b + 2) * BP + (wave - 2 + k * BW) * 64 < P; ++k) {  // large buckets
+        u32x4 cx[QW];
+        PASS_FETCH_CHUNK(b, k, cx);
+        float sum;
+        PASS_SUM(cx, smask, sum);
+        const int p = p0 + 64 * BW * k;
+        if (p < P) s_alpha[p] += (double)sum;
+      }
+      publish(&s_flag[2 + wave - 2], b);
+      if (b + 3 < nblk) {
 #pragma unroll
-          for (int c = 0; c < 4; ++c) sum += ((smask >> (4 * q + c)) & 1u) ? -e[c] : e[c];
-        }
-        s_alpha[p] += (double)sum;
+        for (int k = 0; k < NCB; ++k) PASS_FETCH_CHUNK(b + 1, k, cb[k]);
       }
     }
-    __syncthreads();
   }
+#undef PASS_SUM
+#undef PASS_COL
+#undef PASS_FETCH_DEC
+#undef PASS_STORE_DEC
+#undef PASS_FETCH_NEAR
+#undef PASS_FETCH_CHUNK
 }
 
 // Gram of rows [0,16) against rows [16,32) through the fragment path used by
-// the halving kernel (lane-layout self-check).
+// the score kernel (lane-layout self-check).
 template <typename T, int D>
 __global__ __launch_bounds__(64) void gram16_kernel(const T* rows, float* out) {
   constexpr int NV = Frag<T, D>::NV;
@@ -712,16 +873,16 @@ hipError_t launch_scores_t(int64_t d, const HalveArgs& a, int64_t nbk, hipStream
   }
 }
 
-template <int WAVES>
+template <int BW, int NCB>
 hipError_t launch_pass_w(const HalveArgs& a, int64_t nbk, hipStream_t st) {
-  const size_t lds = (size_t)(a.N / 2) * 8 + 16;  // alpha per pair, decision mask
-  auto kern = halve_pass_kernel<4, WAVES>;
+  const size_t lds = PassLds<BW, NCB>::bytes((int)(a.N / 2));
+  auto kern = halve_pass_kernel<BW, NCB>;
   if (lds > 64 * 1024) {
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess) return e;
   }
-  hipLaunchKernelGGL(kern, dim3((unsigned)nbk), dim3(64 * WAVES), lds, st, a);
+  hipLaunchKernelGGL(kern, dim3((unsigned)nbk), dim3(64 * (BW + 2)), lds, st, a);
   return hipGetLastError();
 }
 
@@ -744,10 +905,13 @@ hipError_t launch_halve(int dtype, int64_t d, const HalveArgs& a0, int64_t nbk, 
   hipError_t e = dtype == 0 ? launch_scores_t<float>(d, a, nbk, st)
                             : launch_scores_t<bf16_t>(d, a, nbk, st);
   if (e != hipSuccess) return e;
-  const int64_t later = a.N / 2 - 32;  // pairs after the first block
-  if (later <= 64) return launch_pass_w<1>(a, nbk, st);
-  if (later <= 128) return launch_pass_w<2>(a, nbk, st);
-  return launch_pass_w<4>(a, nbk, st);
+  // bulk waves x prefetched chunks x 64 pairs should cover the pairs after
+  // the first two blocks
+  const int64_t later = a.N / 2 - 64;
+  if (later <= 64) return launch_pass_w<1, 1>(a, nbk, st);
+  if (later <= 256) return launch_pass_w<2, 2>(a, nbk, st);
+  if (later <= 512) return launch_pass_w<4, 2>(a, nbk, st);
+  return launch_pass_w<6, 3>(a, nbk, st);
 }
 
 hipError_t launch_vmax(int dtype, const void* V, int64_t S, int64_t n, int64_t d,

@@ -1,16 +1,22 @@
 """Benchmark of the thinning hot path on one MI355X.
 
-One step = thin_compress (v_max scan + every kernel-halving round) +
-thin_attention (fp32 output) over one batch of the long-sequence workload
-(B=4, H=16, n=16384 keys and queries, d=128, bf16, n_out=128, g=3), inputs
-resident in HBM.  Prints one JSON line.
+One step = thin_compress (v_max scan + every kernel-halving round: pair
+scores, then decisions) + thin_attention (fp32 output) over one batch of the
+long-sequence workload (B=4, H=16, n=16384 keys and queries, d=128, bf16,
+n_out=128, g=3), inputs resident in HBM.  The K timed steps run with nothing
+between kernels; the same K steps then run again with every kernel launch
+bracketed by HIP events on its stream (thin_set_launch_hook), which gives the
+per-kernel times and the roofline figures.  Prints one JSON line.
 
   python bench.py [--gpus 1] [--steps 20] [--warmup 100] [--workload long]
                   [--no-cpu-baseline]
 """
 import argparse
+import collections
+import hashlib
 import json
 import os
+import re
 import statistics
 import sys
 import time
@@ -64,6 +70,54 @@ def kappa_evals(plan, w) -> int:
     return tot * w.S
 
 
+def score_bytes(w, plan) -> list:
+    """Algorithmic HBM bytes of each round's pair-score launch: the round's K and
+    V rows read once, their int32 indices (not in round 0 without subsample),
+    the float32 pair scores written (8 x 32 tiles over each 64-row block and
+    the columns from its diagonal on) and two float32 pair terms per pair."""
+    b = elem_bytes(w.dtype)
+    n_kept, L, g = plan["n_kept"], plan["rounds"], w.g
+    sub = n_kept < w.n
+    out = []
+    for r in range(L):
+        n_r = n_kept >> r
+        e = L - g - 1 - r
+        G = 4 ** e if e > 0 else 1
+        N = n_r // G
+        NT, nb = (N + 15) // 16, (N + 63) // 64
+        tiles = nb * NT - 4 * nb * (nb - 1) // 2
+        by = n_r * 2 * w.d * b + G * tiles * 1024 + (n_r // 2) * 8
+        if r > 0 or sub:
+            by += n_r * 4
+        out.append(w.S * by)
+    return out
+
+
+def kernel_sources_sha256() -> str:
+    """Hash of the compress kernels' sources (a stored traffic measurement is
+    only reported while it matches)."""
+    h = hashlib.sha256()
+    for f in ("compress.hip", "common.hpp", "launch.hpp"):
+        with open(os.path.join(ROOT, "paper_2606_10944_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def stored_traffic(workload: str):
+    """HBM bytes per pair-score launch measured with rocprofv3 counters
+    (profiles/pair_scores_<workload>_traffic.md), or None if absent or taken
+    on other kernel sources."""
+    path = os.path.join(ROOT, "profiles", f"pair_scores_{workload}_traffic.md")
+    if not os.path.exists(path):
+        return None
+    text = open(path).read()
+    m_sha = re.search(r"^source_sha256:\s*([0-9a-f]{64})", text, re.M)
+    m_val = re.search(r"^traffic_bytes_per_launch:\s*([0-9.eE+]+)", text, re.M)
+    if not m_sha or not m_val or m_sha.group(1) != kernel_sources_sha256():
+        return None
+    return float(m_val.group(1))
+
+
 def attention_bytes(w, out_bytes: int) -> int:
     b = elem_bytes(w.dtype)
     return w.S * (w.n_q * w.d * (b + out_bytes) + w.n_out * (2 * w.d * b + 4))
@@ -113,7 +167,7 @@ def main():
 
     import torch
 
-    from paper_2606_10944_amd import thin_attention, thin_compress, thin_plan
+    from paper_2606_10944_amd import LaunchTimer, thin_attention, thin_compress, thin_plan
     from paper_2606_10944_amd import workloads as W
 
     w = W.WORKLOADS[args.workload]
@@ -127,39 +181,50 @@ def main():
     O = torch.empty((w.B, w.H, w.n_q, w.d), dtype=torch.float32, device=dev)
     stream = torch.cuda.current_stream()
 
-    def step(ev=None):
-        if ev is not None:
-            ev[0].record(stream)
+    def step():
         thin_compress(Kd, Vd, w.n_out, w.g, Ud, idx_out=idx, workspace=ws, stream=stream)
-        if ev is not None:
-            ev[1].record(stream)
         thin_attention(Qd, Kd, Vd, idx, O=O, stream=stream)
-        if ev is not None:
-            ev[2].record(stream)
 
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
+    # Timed region: K steps, nothing recorded between kernels.
     t0 = torch.cuda.Event(enable_timing=True)
     t1 = torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     t0.record(stream)
-    for k in range(args.steps):
-        step(evs[k])
+    for _ in range(args.steps):
+        step()
     t1.record(stream)
     torch.cuda.synchronize()
+    # The same K steps again with every kernel launch bracketed by events on
+    # its stream (each event adds a few microseconds between kernels, so this
+    # pass gives the per-kernel times, not the step time).
+    launches = 3 + 2 * plan["rounds"]  # subsample, v_max, scores + decide per round, attention
+    with LaunchTimer(stream, capacity=launches * args.steps + 16) as lt:
+        for _ in range(args.steps):
+            step()
+        torch.cuda.synchronize()
     ms_total = t0.elapsed_time(t1)
     ms_step = ms_total / args.steps
-    t_c = [e[0].elapsed_time(e[1]) for e in evs]
-    t_a = [e[1].elapsed_time(e[2]) for e in evs]
-    tc, ta = statistics.mean(t_c), statistics.mean(t_a)
+    rec = lt.records()
+    per_step = collections.defaultdict(float)
+    for name, _, ms in rec:
+        per_step[name] += ms / args.steps
+    score_ms = [ms for name, _, ms in rec if name == "scores"]
+    L = plan["rounds"]
+    tc = sum(v for k, v in per_step.items() if k != "attention")
+    ta = per_step["attention"]
 
     cb = compress_bytes(w, plan)
+    sb = score_bytes(w, plan)
     ab = attention_bytes(w, 4)
     af = attention_flops(w)
     kev = kappa_evals(plan, w)
-    comp_gbs = cb / (tc * 1e-3) / 1e9
+    sc_ms_launch = statistics.mean(score_ms)
+    sc_bytes_launch = sum(sb) / L
+    sc_gbs = sc_bytes_launch / (sc_ms_launch * 1e-3) / 1e9
+    traffic = stored_traffic(w.name)
     attn_gbs = ab / (ta * 1e-3) / 1e9
     attn_tflops = af / (ta * 1e-3) / 1e12
     value = w.S * w.n_q / (ms_step * 1e-3)
@@ -180,11 +245,16 @@ def main():
         "config": {"workload": w.name, "B": w.B, "H": w.H, "n": w.n, "n_q": w.n_q, "d": w.d,
                    "n_out": w.n_out, "g": w.g, "out_dtype": "fp32"},
         "roofline": {
-            "kernel": "compress stage (v_max scan + every halve_kernel round of one call)",
-            "bound": "hbm", "achieved": comp_gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-            "frac": comp_gbs / HBM_PEAK_GBS, "traffic": None,
-            "algorithmic_bytes": cb, "ms_per_launch": tc,
+            "kernel": "pair_scores_kernel (one launch per Halve round)",
+            "bound": "hbm", "achieved": sc_gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+            "frac": sc_gbs / HBM_PEAK_GBS,
+            "traffic": traffic,
+            "algorithmic_bytes_per_launch": sc_bytes_launch, "ms_per_launch": sc_ms_launch,
+            "launches_per_step": L,
         },
+        "compress": {"ms": tc, "kappa_evals": kev, "kappa_evals_per_s": kev / (tc * 1e-3),
+                     "algorithmic_bytes": cb, "hbm_gbs": cb / (tc * 1e-3) / 1e9,
+                     "hbm_frac": cb / (tc * 1e-3) / 1e9 / HBM_PEAK_GBS},
         "attention": {
             "ms": ta, "hbm_gbs": attn_gbs, "hbm_frac": attn_gbs / HBM_PEAK_GBS,
             "mfma_tflops": attn_tflops,
@@ -192,8 +262,7 @@ def main():
                                         else FP32_MFMA_PEAK_TFLOPS),
             "algorithmic_bytes": ab, "flops": af,
         },
-        "compress": {"ms": tc, "kappa_evals": kev,
-                     "kappa_evals_per_s": kev / (tc * 1e-3)},
+        "ms_per_step_by_kernel": dict(per_step),
         "gpu": torch.cuda.get_device_name(0),
     }
     if not args.no_cpu_baseline:

@@ -137,7 +137,7 @@ int thin_attention(const void* Q, const void* K, const void* V, int32_t dtype, i
 
 /*
  * Diagnostic: out[m*16 + n] = <rows[m], rows[16 + n]> for m, n < 16, computed
- * through the MFMA row-fragment path the halving kernel uses.
+ * through the MFMA row-fragment path the pair-score kernel uses.
  *   rows (device) [32, d] of `dtype`;  out (device) float32 [16, 16].
  * Errors: THIN_EINVAL, THIN_EDTYPE, THIN_EHIP.
  */
@@ -145,6 +145,32 @@ int thin_selftest_gram16(int32_t dtype, int64_t d, const void* rows, float* out,
 
 /* Static, human-readable text for a status code. */
 const char* thin_status_str(int status);
+
+/*
+ * Launch observer, for tracing and per-kernel timing.  While a hook is set,
+ * every kernel launch made by thin_compress, thin_compress_traced and
+ * thin_attention is bracketed by two calls on the calling thread:
+ * hook(ctx, kernel, round, 0, stream) right before the launch is enqueued and
+ * hook(ctx, kernel, round, 1, stream) right after.  The hook may enqueue
+ * stream-ordered work of its own (for instance record an event on `stream`),
+ * so that consecutive records time one kernel.  `kernel` is a
+ * thin_kernel_t, `round` the Halve round 0..L-1 of a THIN_KERNEL_SCORES or
+ * THIN_KERNEL_DECIDE launch and -1 otherwise.  The setting is process-wide:
+ * change it only while no other thread is inside the library.  hook = NULL
+ * turns it off (the default).  Returns THIN_OK.
+ */
+typedef enum {
+  THIN_KERNEL_TRACE_CLEAR = 0, /* zeroing of the swap trace               */
+  THIN_KERNEL_SUBSAMPLE = 1,   /* stratified subsample                    */
+  THIN_KERNEL_FILL = 2,        /* index copy when no round runs           */
+  THIN_KERNEL_VMAX = 3,        /* v_max scan (with its zeroing)           */
+  THIN_KERNEL_SCORES = 4,      /* pair scores of one round                */
+  THIN_KERNEL_DECIDE = 5,      /* decision pass of one round              */
+  THIN_KERNEL_ATTENTION = 6    /* coreset attention                       */
+} thin_kernel_t;
+typedef void (*thin_launch_hook_t)(void* ctx, int32_t kernel, int32_t round, int32_t phase,
+                                   void* stream);
+int thin_set_launch_hook(thin_launch_hook_t hook, void* ctx);
 
 #ifdef __cplusplus
 }

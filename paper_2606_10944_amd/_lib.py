@@ -22,7 +22,12 @@ THIN_FP32, THIN_BF16 = 0, 1
 
 # Every symbol include/thin.h declares.
 EXPORTS = ("thin_plan", "thin_compress", "thin_compress_traced", "thin_attention",
-           "thin_selftest_gram16", "thin_status_str")
+           "thin_selftest_gram16", "thin_status_str", "thin_set_launch_hook")
+
+# thin_kernel_t
+KERNEL_NAMES = {0: "trace_clear", 1: "subsample", 2: "fill", 3: "vmax", 4: "scores",
+                5: "decide", 6: "attention"}
+LaunchHook = C.CFUNCTYPE(None, C.c_void_p, C.c_int32, C.c_int32, C.c_int32, C.c_void_p)
 
 
 class ThinError(RuntimeError):
@@ -63,6 +68,8 @@ def lib():
     L.thin_selftest_gram16.argtypes = [I32, I64, P, P, P]
     L.thin_status_str.argtypes = [C.c_int]
     L.thin_status_str.restype = C.c_char_p
+    L.thin_set_launch_hook.argtypes = [LaunchHook, P]
+    L.thin_set_launch_hook.restype = C.c_int
     for f in ("thin_plan", "thin_compress", "thin_compress_traced", "thin_attention",
               "thin_selftest_gram16"):
         getattr(L, f).restype = C.c_int
@@ -169,3 +176,43 @@ def thin_selftest_gram16(rows: torch.Tensor, stream=None) -> torch.Tensor:
                                     _ptr(out), _stream(stream))
     _check(rc, "thin_selftest_gram16")
     return out
+
+
+class LaunchTimer:
+    """Times every kernel launch of the library on one stream with HIP events
+    (thin_set_launch_hook): inside ``with LaunchTimer(stream) as lt:`` each
+    launch is bracketed by two events recorded on ``stream``; after
+    synchronising, ``lt.records()`` lists (kernel name, round, milliseconds)
+    in launch order.  Events come from a pool created up front, so the hook
+    only records."""
+
+    def __init__(self, stream, capacity: int = 4096):
+        self.stream = stream
+        self._raw = stream.cuda_stream
+        self._events = [torch.cuda.Event(enable_timing=True) for _ in range(2 * capacity)]
+        self._n = 0
+        self._meta = []
+        self._cb = LaunchHook(self._hook)
+
+    def _hook(self, ctx, kernel, rnd, phase, stream_ptr):
+        if (stream_ptr or 0) != self._raw:
+            raise RuntimeError("LaunchTimer: launch on another stream")
+        if self._n >= len(self._events):
+            raise RuntimeError("LaunchTimer: event pool exhausted")
+        self._events[self._n].record(self.stream)
+        self._n += 1
+        if phase == 1:
+            self._meta.append((kernel, rnd))
+
+    def __enter__(self):
+        _check(lib().thin_set_launch_hook(self._cb, None), "thin_set_launch_hook")
+        return self
+
+    def __exit__(self, *exc):
+        lib().thin_set_launch_hook(LaunchHook(), None)
+        return False
+
+    def records(self):
+        ev = self._events
+        return [(KERNEL_NAMES.get(k, str(k)), r, ev[2 * i].elapsed_time(ev[2 * i + 1]))
+                for i, (k, r) in enumerate(self._meta)]

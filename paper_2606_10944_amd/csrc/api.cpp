@@ -110,6 +110,18 @@ size_t workspace_size(int64_t S, int64_t d, const Levels& lv) {
   return carve(nullptr, S, d, lv).bytes;
 }
 
+thin_launch_hook_t g_hook = nullptr;
+void* g_hook_ctx = nullptr;
+
+// Enqueue one launch between the observer's two calls.
+template <typename F>
+hipError_t observed(int32_t kernel, int32_t round, hipStream_t st, F&& launch) {
+  if (g_hook) g_hook(g_hook_ctx, kernel, round, 0, st);
+  const hipError_t e = launch();
+  if (g_hook) g_hook(g_hook_ctx, kernel, round, 1, st);
+  return e;
+}
+
 int check_shape(int64_t B, int64_t H, int64_t n, int64_t d) {
   if (B < 1 || H < 1 || n < 1 || n > kMaxRows) return THIN_EINVAL;
   if (B * H > ((int64_t)1 << 31)) return THIN_EINVAL;
@@ -142,13 +154,20 @@ int compress_impl(const void* K, const void* V, int32_t dtype, int64_t B, int64_
     if (x != hipSuccess && e == hipSuccess) e = x;
     return e == hipSuccess;
   };
-  if (trace) ok(thin::launch_zero_u8(trace, Utot, st));
-  if (lv.sub) ok(thin::launch_subsample(S, n, lv.n_kept, uniforms, lv.U, ws.buf_a, st));
+  if (trace)
+    ok(observed(THIN_KERNEL_TRACE_CLEAR, -1, st, [&] { return thin::launch_zero_u8(trace, Utot, st); }));
+  if (lv.sub)
+    ok(observed(THIN_KERNEL_SUBSAMPLE, -1, st, [&] {
+      return thin::launch_subsample(S, n, lv.n_kept, uniforms, lv.U, ws.buf_a, st);
+    }));
   const int32_t* cur = lv.sub ? ws.buf_a : nullptr;
   if (lv.L == 0) {
-    ok(thin::launch_fill_rows(S, n_out, cur, lv.n_kept, idx_out, st));
+    ok(observed(THIN_KERNEL_FILL, -1, st, [&] {
+      return thin::launch_fill_rows(S, n_out, cur, lv.n_kept, idx_out, st);
+    }));
   } else {
-    ok(thin::launch_vmax(dtype, V, S, n, d, ws.vmax_bits, st));
+    ok(observed(THIN_KERNEL_VMAX, -1, st,
+                [&] { return thin::launch_vmax(dtype, V, S, n, d, ws.vmax_bits, st); }));
     int64_t u_off = lv.sub ? lv.n_kept : 0;
     for (int32_t r = 0; r < lv.L && e == hipSuccess; ++r) {
       int32_t* out = (r == lv.L - 1) ? idx_out : (cur == ws.buf_b ? ws.buf_a : ws.buf_b);
@@ -178,7 +197,9 @@ int compress_impl(const void* K, const void* V, int32_t dtype, int64_t B, int64_
       for (int64_t b0 = 0; b0 < buckets && e == hipSuccess; b0 += chunk) {
         a.b0 = b0;
         const int64_t nbk = buckets - b0 < chunk ? buckets - b0 : chunk;
-        ok(thin::launch_halve(dtype, d, a, nbk, st));
+        ok(observed(THIN_KERNEL_SCORES, r, st, [&] { return thin::launch_scores(dtype, d, a, nbk, st); }));
+        if (e == hipSuccess)
+          ok(observed(THIN_KERNEL_DECIDE, r, st, [&] { return thin::launch_decide(a, nbk, st); }));
       }
       u_off += lv.n_r[r] / 2;
       cur = out;
@@ -237,8 +258,10 @@ int thin_attention(const void* Q, const void* K, const void* V, int32_t dtype, i
   if (dtype != THIN_FP32 && dtype != THIN_BF16) return THIN_EDTYPE;
   if (out_dtype != THIN_FP32 && out_dtype != THIN_BF16) return THIN_EDTYPE;
   if (!Q || !K || !V || !idx || !O) return THIN_EINVAL;
-  hipError_t e = thin::launch_attention(dtype, d, out_dtype, Q, K, V, idx, B * H, n, n_q, n_out,
-                                        O, static_cast<hipStream_t>(stream));
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  hipError_t e = observed(THIN_KERNEL_ATTENTION, -1, st, [&] {
+    return thin::launch_attention(dtype, d, out_dtype, Q, K, V, idx, B * H, n, n_q, n_out, O, st);
+  });
   return e == hipSuccess ? THIN_OK : THIN_EHIP;
 }
 
@@ -248,6 +271,12 @@ int thin_selftest_gram16(int32_t dtype, int64_t d, const void* rows, float* out,
   if (!rows || !out) return THIN_EINVAL;
   hipError_t e = thin::launch_gram16(dtype, d, rows, out, static_cast<hipStream_t>(stream));
   return e == hipSuccess ? THIN_OK : THIN_EHIP;
+}
+
+int thin_set_launch_hook(thin_launch_hook_t hook, void* ctx) {
+  g_hook = hook;
+  g_hook_ctx = ctx;
+  return THIN_OK;
 }
 
 const char* thin_status_str(int status) {

@@ -898,13 +898,20 @@ size_t halve_score_bytes(int64_t N) {
   return (size_t)halve_score_tiles(N) * 8 * 32 * 4;  // tiles of 8 columns x 32 rows, float32
 }
 
-hipError_t launch_halve(int dtype, int64_t d, const HalveArgs& a0, int64_t nbk, hipStream_t st) {
+static HalveArgs with_layout(const HalveArgs& a0) {
   HalveArgs a = a0;
   a.ch = kScoreChunk;
   a.e_tiles = halve_score_tiles(a.N);
-  hipError_t e = dtype == 0 ? launch_scores_t<float>(d, a, nbk, st)
-                            : launch_scores_t<bf16_t>(d, a, nbk, st);
-  if (e != hipSuccess) return e;
+  return a;
+}
+
+hipError_t launch_scores(int dtype, int64_t d, const HalveArgs& a0, int64_t nbk, hipStream_t st) {
+  const HalveArgs a = with_layout(a0);
+  return dtype == 0 ? launch_scores_t<float>(d, a, nbk, st) : launch_scores_t<bf16_t>(d, a, nbk, st);
+}
+
+hipError_t launch_decide(const HalveArgs& a0, int64_t nbk, hipStream_t st) {
+  const HalveArgs a = with_layout(a0);
   // bulk waves x prefetched chunks x 64 pairs should cover the pairs after
   // the first two blocks
   const int64_t later = a.N / 2 - 64;

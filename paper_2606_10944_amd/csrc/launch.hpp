@@ -42,8 +42,9 @@ hipError_t launch_zero_u8(uint8_t* p, int64_t count, hipStream_t st);
 // Score tiles and score bytes of one N-row bucket (64-row decision blocks).
 int64_t halve_score_tiles(int64_t N);
 size_t halve_score_bytes(int64_t N);
-// Pair scores, then decisions, for nbk buckets starting at a.b0.
-hipError_t launch_halve(int dtype, int64_t d, const HalveArgs& a, int64_t nbk, hipStream_t st);
+// Pair scores, then the decision pass, for nbk buckets starting at a.b0.
+hipError_t launch_scores(int dtype, int64_t d, const HalveArgs& a, int64_t nbk, hipStream_t st);
+hipError_t launch_decide(const HalveArgs& a, int64_t nbk, hipStream_t st);
 
 hipError_t launch_attention(int dtype, int64_t d, int out_dtype, const void* Q, const void* K,
                             const void* V, const int32_t* idx, int64_t S, int64_t n,

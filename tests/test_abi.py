@@ -132,3 +132,14 @@ def test_workloads_are_seeded_and_shaped():
     Q, K, V = W.make_qkv(w3)
     assert tuple(Q.shape) == (2, 1, 4096, 64) and tuple(K.shape) == (2, 1, 1024, 64)
     assert float(V.abs().max()) <= 1.0
+
+
+def test_launch_hook_can_be_set_and_cleared():
+    L = _lib.lib()
+    calls = []
+    cb = _lib.LaunchHook(lambda *a: calls.append(a))
+    assert L.thin_set_launch_hook(cb, None) == _lib.THIN_OK
+    # a call rejected during validation launches nothing, so the hook is silent
+    assert _compress(dtype=5) == _lib.THIN_EDTYPE
+    assert L.thin_set_launch_hook(_lib.LaunchHook(), None) == _lib.THIN_OK
+    assert calls == []

@@ -12,7 +12,8 @@ import pytest
 import torch
 
 import oracle
-from paper_2606_10944_amd import thin_attention, thin_compress, thin_plan, thin_selftest_gram16
+from paper_2606_10944_amd import (LaunchTimer, thin_attention, thin_compress, thin_plan,
+                                  thin_selftest_gram16)
 from paper_2606_10944_amd import workloads as W
 
 pytestmark = pytest.mark.gpu
@@ -205,3 +206,23 @@ def test_attention_bf16_output():
         ref = oracle.attention(Q[s, 0], K[s, 0], V[s, 0], idx[s, 0])
         # fp32 accumulation error plus one bf16 rounding of the output
         assert np.all(np.abs(ref - O[s, 0]) <= 2e-3 + 2.0 ** -8 * np.abs(ref))
+
+
+def test_launch_timer_sees_every_kernel_in_order():
+    w = W.custom("lt", B=1, H=2, n=5000, n_out=40, g=2, d=64, dtype="bf16", kind="gauss")
+    Q, K, V = W.make_qkv(w)
+    plan = thin_plan(w.B, w.H, w.n, w.d, w.n_out, w.g)
+    U = W.make_uniforms(w, plan["uniforms_total"]).to(DEV)
+    stream = torch.cuda.current_stream()
+    with LaunchTimer(stream) as lt:
+        idx = thin_compress(K.to(DEV), V.to(DEV), w.n_out, w.g, U, stream=stream)
+        thin_attention(Q.to(DEV), K.to(DEV), V.to(DEV), idx, stream=stream)
+        torch.cuda.synchronize()
+    rec = lt.records()
+    L = plan["rounds"]
+    want = [("subsample", -1), ("vmax", -1)]
+    for r in range(L):
+        want += [("scores", r), ("decide", r)]
+    want += [("attention", -1)]
+    assert [(k, r) for k, r, _ in rec] == want
+    assert all(ms > 0 for _, _, ms in rec)

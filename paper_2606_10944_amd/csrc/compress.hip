@@ -34,24 +34,36 @@ __global__ __launch_bounds__(256) void vmax_kernel(const T* V, int64_t words_per
   int64_t w0 = (int64_t)blockIdx.x * words_per_block;
   int64_t w1 = w0 + words_per_block;
   if (w1 > words_per_slice) w1 = words_per_slice;
-  float m = 0.0f;
-  for (int64_t w = w0 + threadIdx.x; w < w1; w += blockDim.x) {
-    uint4 x = base[w];
-    const uint32_t* u = reinterpret_cast<const uint32_t*>(&x);
+  // The magnitude bits of a (non-NaN) float order like the magnitudes
+  // themselves, so max |x| is taken on the bit patterns as unsigned integers
+  uint32_t m = 0u;
+  auto fold = [&](const u32x4& x) {
 #pragma unroll
     for (int c = 0; c < 4; ++c) {
       if (Elem<T>::bytes == 4) {
-        m = fmaxf(m, __uint_as_float(u[c] & 0x7fffffffu));
+        m = max(m, x[c] & 0x7fffffffu);
       } else {
-        m = fmaxf(m, __uint_as_float((u[c] << 16) & 0x7fffffffu));
-        m = fmaxf(m, __uint_as_float(u[c] & 0x7fff0000u));
+        m = max(m, (x[c] << 16) & 0x7fffffffu);
+        m = max(m, x[c] & 0x7fff0000u);
       }
     }
+  };
+  // eight independent 16-byte loads in flight per thread
+  constexpr int U = 8;
+  const u32x4* vb = reinterpret_cast<const u32x4*>(base);
+  int64_t w = w0 + threadIdx.x;
+  for (; w + (U - 1) * (int64_t)blockDim.x < w1; w += U * (int64_t)blockDim.x) {
+    u32x4 x[U];
+#pragma unroll
+    for (int k = 0; k < U; ++k) x[k] = vb[w + k * (int64_t)blockDim.x];
+#pragma unroll
+    for (int k = 0; k < U; ++k) fold(x[k]);
   }
-  m = wave_max_f(m);
+  for (; w < w1; w += blockDim.x) fold(vb[w]);
+  const float mf = wave_max_f(__uint_as_float(m));
   __shared__ float part[4];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  if (lane == 0) part[wave] = m;
+  if (lane == 0) part[wave] = mf;
   __syncthreads();
   if (threadIdx.x == 0) {
     float r = part[0];
@@ -331,46 +343,57 @@ __host__ __device__ inline int64_t panel_tiles(int64_t B, int64_t NT, int64_t RT
   return B * NT - RT * B * (B - 1) / 2;
 }
 
-// Waves per pair_scores_kernel workgroup, column tiles in flight (registers)
-// and column-tile stages in LDS.
+// Work decomposition of pair_scores_kernel.  A group is BLOCKS consecutive
+// decision blocks (64 rows each) of one bucket; the group's waves hold its
+// rows as MFMA fragments, HB half-blocks (32 rows) per wave, paired so that
+// every wave has the same amount of work: with HB = 2, wave w holds the first
+// half of block w and the second half of block BLOCKS-1-w.  Workgroups are
+// small enough (4 waves) that two fit on a CU, so one's row loads overlap the
+// other's arithmetic.  A workgroup handles one
+// (bucket, group, chunk): chunk 0 covers the group's own column tiles, which
+// the owning waves write to LDS from their registers (so the bucket's rows
+// are read from HBM once); chunk c >= 1 covers kScoreChunk column tiles after
+// the group, streamed from global memory through registers DEPTH tiles ahead.
 #ifndef SCORE_WAVES
-#define SCORE_WAVES 8
+#define SCORE_WAVES 4
 #endif
 constexpr int kScoreWaves = SCORE_WAVES;
 #ifndef SCORE_DEPTH
-#define SCORE_DEPTH 6
+#define SCORE_DEPTH 3
 #endif
 constexpr int kScoreStages = 3;
-// Column tiles per pair_scores_kernel workgroup.
 constexpr int kScoreChunk = 32;
 
-// Per-wave A rows: WRT row tiles (about 64 registers of fragments); WPB waves
-// cover one 64-row decision block; a workgroup covers BLOCKS blocks.  A
-// column tile (16 rows of K and V) is CHUNKS 1 KB fragment chunks.
 template <typename T, int D>
 struct ScoreShape {
   static constexpr int NV = Frag<T, D>::NV;
-  static constexpr int WRT = NV >= 8 ? 1 : (NV == 4 ? 2 : 4);
-  static constexpr int WPB = 4 / WRT;
-  static constexpr int BLOCKS = kScoreWaves / WPB;
-  static constexpr int CHUNKS = 2 * NV;
+  static constexpr int HB = NV >= 8 ? 1 : 2;   // half-blocks per wave
+  static constexpr int BLOCKS = kScoreWaves * HB / 2;  // decision blocks per group
+  static constexpr int GT = 4 * BLOCKS;        // 16-row tiles per group
+  static constexpr int CHUNKS = 2 * NV;        // 1 KB fragment chunks per tile (K, then V)
   static constexpr int LPT = (CHUNKS + kScoreWaves - 1) / kScoreWaves;
-  // stages, scale exponents, row indices of the column rows
+  // stages, scale exponents, row indices of the streamed column rows
   static constexpr int LDS = kScoreStages * CHUNKS * 1024 + kScoreStages * 16 * 4 +
                              (kScoreChunk + SCORE_DEPTH + 2) * 16 * 8;
 };
 
-// Scores of BLOCKS consecutive decision blocks of one bucket against column
-// tiles [jt0, jt1): grid (bucket, block group, column chunk).  Column tiles
-// stream through LDS: each is loaded once per workgroup (every thread loads
-// its share into registers DEPTH tiles ahead, then writes it to a stage), and
-// the LDS copy keeps the fragment lane order, so every wave reads it back
-// with one conflict-free 16-byte access per lane and chunk.  The column
-// pairs' scale h is formed once per tile by one wave.
+// Block (group-local) and half of half-block slot h of wave w.
+template <int HB>
+__device__ __forceinline__ void half_block(int w, int h, int& b, int& half) {
+  if (HB == 2) {
+    b = h == 0 ? w : kScoreWaves - 1 - w;
+    half = h;
+  } else {
+    b = w >> 1;
+    half = w & 1;
+  }
+}
+
 template <typename T, int D>
-__global__ __launch_bounds__(64 * kScoreWaves) void pair_scores_kernel(HalveArgs a) {
+__global__ __launch_bounds__(64 * kScoreWaves) __attribute__((amdgpu_waves_per_eu(2)))
+void pair_scores_kernel(HalveArgs a) {
   using SS = ScoreShape<T, D>;
-  constexpr int NV = SS::NV, WRT = SS::WRT, WPB = SS::WPB, NBW = SS::BLOCKS;
+  constexpr int NV = SS::NV, HB = SS::HB, NBW = SS::BLOCKS, GT = SS::GT;
   constexpr int CH = SS::CHUNKS, LPT = SS::LPT;
   constexpr int BP = 32;
   constexpr int TILE = 8 * BP;
@@ -378,26 +401,26 @@ __global__ __launch_bounds__(64 * kScoreWaves) void pair_scores_kernel(HalveArgs
   constexpr int NS = kScoreStages;
   static_assert(DEPTH % NS == 0, "the unrolled ring keeps stage indices static");
   const int lane = threadIdx.x & 63;
-  const int wave = threadIdx.x >> 6;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int m16 = lane & 15;
   const int g = lane >> 4;
 
+  const int64_t bl = blockIdx.x;
+  const int64_t bucket = a.b0 + bl;
+  const int64_t s = bucket / a.G;
+  const int64_t t = bucket % a.G;
   const int N = a.N;
   const int P = N >> 1;
   const int NT = (N + 15) >> 4;
   const int nb = (N + 63) >> 6;
-  // Work item: (bucket, block group, column chunk).
-  const int64_t bl = blockIdx.x;
   const int grp = blockIdx.y, chunk = blockIdx.z;
-  const int64_t bucket = a.b0 + bl;
-  const int64_t s = bucket / a.G;
-  const int64_t t = bucket % a.G;
-  const int jt0 = grp * NBW * 4 + chunk * a.ch;
+  const int gt0 = grp * GT;  // the group's first tile
+  if (gt0 >= NT) return;
+  const bool own = chunk == 0;
+  const int jt0 = own ? gt0 : gt0 + GT + (chunk - 1) * a.ch;
   if (jt0 >= NT) return;
-  const int jt1 = min(jt0 + a.ch, NT);
-  const int blk = grp * NBW + wave / WPB;  // this wave's decision block
-  const int sub = wave % WPB;                          // its part of the block
-  const bool has_blk = blk < nb;
+  const int jt1 = min(jt0 + (own ? GT : a.ch), NT);
+  const int ntile = jt1 - jt0;
 
   const T* K = reinterpret_cast<const T*>(a.K) + s * a.n * D;
   const T* V = reinterpret_cast<const T*>(a.V) + s * a.n * D;
@@ -412,41 +435,57 @@ __global__ __launch_bounds__(64 * kScoreWaves) void pair_scores_kernel(HalveArgs
   extern __shared__ __align__(16) unsigned char smem[];
   float* s_h2 = reinterpret_cast<float*>(smem + NS * CH * 1024);
   int64_t* s_rows = reinterpret_cast<int64_t*>(s_h2 + NS * 16);
-  // Row indices of every column row this workgroup loads, staged first: a
-  // data load then never waits on an index load issued behind the ring's
-  // outstanding loads.
-  const int j_end = min(N, (jt1 + DEPTH + 2) * 16);
-  for (int j = jt0 * 16 + (int)threadIdx.x; j < j_end; j += 64 * kScoreWaves)
-    s_rows[j - jt0 * 16] = rows_in ? (int64_t)rows_in[j] : row_base + j;
 
-  // ---- this wave's A rows and, in the first chunk, their pair terms ----
-  uint4 Ak[WRT][NV], Av[WRT][NV];
+  // ---- this wave's half-blocks: fragments and, in chunk 0, pair terms ----
+  int hb_blk[HB], hb_half[HB];
+  bool hb_ok[HB];
 #pragma unroll
-  for (int rt = 0; rt < WRT; ++rt) {
-    const int j = blk * 64 + (sub * WRT + rt) * 16 + m16;
-    const bool valid = has_blk && j < N;
-    const int64_t r = valid ? (rows_in ? (int64_t)rows_in[j] : row_base + j) : 0;
-    load_frag<T, D>(K, r, g, valid, Ak[rt]);
-    load_frag<T, D>(V, r, g, valid, Av[rt]);
+  for (int h = 0; h < HB; ++h) {
+    int b, half;
+    half_block<HB>(wave, h, b, half);
+    hb_blk[h] = grp * NBW + b;
+    hb_half[h] = half;
+    hb_ok[h] = hb_blk[h] < nb;
   }
-  if (chunk == 0 && has_blk) {
+  uint4 Ak[HB][2][NV], Av[HB][2][NV];
+#pragma unroll
+  for (int h = 0; h < HB; ++h)
+#pragma unroll
+    for (int rt = 0; rt < 2; ++rt) {
+      const int j = hb_blk[h] * 64 + hb_half[h] * 32 + rt * 16 + m16;
+      const bool valid = hb_ok[h] && j < N;
+      const int64_t r = valid ? (rows_in ? (int64_t)rows_in[j] : row_base + j) : 0;
+      load_frag<T, D>(K, r, g, valid, Ak[h][rt]);
+      load_frag<T, D>(V, r, g, valid, Av[h][rt]);
+    }
+  if (own) {
     const int64_t pb = s * (a.n_r >> 1) + t * (int64_t)P;
 #pragma unroll
-    for (int rt = 0; rt < WRT; ++rt) {
-      float h2f, lbt;
-      frag_pair_terms<T, D>(Ak[rt], Av[rt], vm2d, inv_sqrt_d, h2f, lbt);
-      const int j = blk * 64 + (sub * WRT + rt) * 16 + m16;
-      if (g == 0 && j < N && (j & 1) == 0) {
-        a.h2[pb + (j >> 1)] = h2f;
-        a.lbt[pb + (j >> 1)] = lbt;
+    for (int h = 0; h < HB; ++h) {
+      if (!hb_ok[h]) continue;
+#pragma unroll
+      for (int rt = 0; rt < 2; ++rt) {
+        float h2f, lbt;
+        frag_pair_terms<T, D>(Ak[h][rt], Av[h][rt], vm2d, inv_sqrt_d, h2f, lbt);
+        const int j = hb_blk[h] * 64 + hb_half[h] * 32 + rt * 16 + m16;
+        if (g == 0 && j < N && (j & 1) == 0) {
+          a.h2[pb + (j >> 1)] = h2f;
+          a.lbt[pb + (j >> 1)] = lbt;
+        }
       }
     }
+  } else {
+    // row indices of every streamed column row, staged first: a data load
+    // then never waits on an index load issued behind the ring's loads
+    const int j_end = min(N, (jt1 + DEPTH + 2) * 16);
+    for (int j = jt0 * 16 + (int)threadIdx.x; j < j_end; j += 64 * kScoreWaves)
+      s_rows[j - jt0 * 16] = rows_in ? (int64_t)rows_in[j] : row_base + j;
   }
 
-  // ---- column tile pipeline ----
-  // chunk c of tile jt: lane l holds row jt*16 + l%16 (clamped to the
-  // bucket; rows past the end are never read back), word 4(c%NV) + l/16, of
-  // K (c < NV) or V.
+  // ---- column tiles ----
+  // Streamed chunk c of tile jt: lane l holds row jt*16 + l%16 (clamped to
+  // the bucket; rows past the end are never read back), word 4(c%NV) + l/16,
+  // of K (c < NV) or V.  Own tiles are the owners' fragments, same layout.
   u32x4 stg[DEPTH][LPT];
 #define SCORE_ISSUE(JT, SLOT)                                                        \
   do {                                                                               \
@@ -465,6 +504,27 @@ __global__ __launch_bounds__(64 * kScoreWaves) void pair_scores_kernel(HalveArgs
       if (c_ < CH) reinterpret_cast<u32x4*>(smem + ((STAGE) * CH + c_) * 1024)[lane] = stg[SLOT][k_]; \
     }                                                                                \
   } while (0)
+#define SCORE_OWN_WRITE(STAGE, H, RT)                                                \
+  do {                                                                               \
+    _Pragma("unroll") for (int v_ = 0; v_ < NV; ++v_) {                              \
+      reinterpret_cast<uint4*>(smem + ((STAGE) * CH + v_) * 1024)[lane] = Ak[H][RT][v_]; \
+      reinterpret_cast<uint4*>(smem + ((STAGE) * CH + NV + v_) * 1024)[lane] = Av[H][RT][v_]; \
+    }                                                                                \
+  } while (0)
+  // own tile TL (group-local) into a stage, by the wave holding it
+#define SCORE_OWN_COMMIT(STAGE, TL)                                                  \
+  do {                                                                               \
+    const int b_ = (TL) >> 2, half_ = ((TL) >> 1) & 1, rt_ = (TL) & 1;              \
+    const int owner_ = HB == 2 ? (half_ == 0 ? b_ : kScoreWaves - 1 - b_) : 2 * b_ + half_; \
+    const int slot_ = HB == 2 ? half_ : 0;                                           \
+    if (wave == owner_) {                                                            \
+      if (slot_ == 0) {                                                              \
+        if (rt_ == 0) SCORE_OWN_WRITE(STAGE, 0, 0); else SCORE_OWN_WRITE(STAGE, 0, 1); \
+      } else {                                                                       \
+        if (rt_ == 0) SCORE_OWN_WRITE(STAGE, HB - 1, 0); else SCORE_OWN_WRITE(STAGE, HB - 1, 1); \
+      }                                                                              \
+    }                                                                                \
+  } while (0)
   auto tile_h2 = [&](int stage) {  // scale exponents of a staged tile's 16 rows
     uint4 bk[NV];
 #pragma unroll
@@ -473,74 +533,92 @@ __global__ __launch_bounds__(64 * kScoreWaves) void pair_scores_kernel(HalveArgs
     if (g == 0) s_h2[stage * 16 + m16] = h;
   };
 
+  // Gram accumulators; a half-block slot h takes part in tile jt from its
+  // block's diagonal on.  (Two waves per SIMD overlap one wave's MFMAs with
+  // the other's exp epilogue; double-buffered accumulators would not fit.)
+  floatx4_t gk[1][HB][2], gv[1][HB][2];
+#define SCORE_ACTIVE(H, JT) (hb_ok[H] && (JT) >= hb_blk[H] * 4)
+#define SCORE_MMA(STAGE, JT, SLOT)                                                      \
+  do {                                                                                 \
+    uint4 bk_[NV], bv_[NV];                                                            \
+    _Pragma("unroll") for (int v_ = 0; v_ < NV; ++v_) {                                \
+      bk_[v_] = reinterpret_cast<const uint4*>(smem + ((STAGE) * CH + v_) * 1024)[lane]; \
+      bv_[v_] = reinterpret_cast<const uint4*>(smem + ((STAGE) * CH + NV + v_) * 1024)[lane]; \
+    }                                                                                  \
+    _Pragma("unroll") for (int h_ = 0; h_ < HB; ++h_) {                                \
+      if (!SCORE_ACTIVE(h_, JT)) continue;                                             \
+      _Pragma("unroll") for (int rt_ = 0; rt_ < 2; ++rt_) {                            \
+        gk[SLOT][h_][rt_] = (floatx4_t){0.f, 0.f, 0.f, 0.f};                           \
+        gv[SLOT][h_][rt_] = (floatx4_t){vm2f, vm2f, vm2f, vm2f}; /* <v,v'> + v_max^2 */ \
+      }                                                                                \
+      _Pragma("unroll") for (int v_ = 0; v_ < NV; ++v_)                                \
+        _Pragma("unroll") for (int rt_ = 0; rt_ < 2; ++rt_) {                          \
+          gk[SLOT][h_][rt_] = mma_word<T>(Ak[h_][rt_][v_], bk_[v_], gk[SLOT][h_][rt_]); \
+          gv[SLOT][h_][rt_] = mma_word<T>(Av[h_][rt_][v_], bv_[v_], gv[SLOT][h_][rt_]); \
+        }                                                                              \
+    }                                                                                  \
+  } while (0)
+
   __syncthreads();
+  if (own) {
+    SCORE_OWN_COMMIT(0, 0);
+    if (ntile > 1) SCORE_OWN_COMMIT(1, 1);
+  } else {
 #pragma unroll
-  for (int k = 0; k < DEPTH; ++k) SCORE_ISSUE(jt0 + k, k);
-  SCORE_COMMIT(0, 0);
-  SCORE_COMMIT(1, 1);
-  SCORE_ISSUE(jt0 + DEPTH, 0);
-  SCORE_ISSUE(jt0 + DEPTH + 1, 1);
+    for (int k = 0; k < DEPTH; ++k) SCORE_ISSUE(jt0 + k, k);
+    SCORE_COMMIT(0, 0);
+    SCORE_COMMIT(1, 1);
+    SCORE_ISSUE(jt0 + DEPTH, 0);
+    SCORE_ISSUE(jt0 + DEPTH + 1, 1);
+  }
   __syncthreads();
   if (wave == 0) tile_h2(0);
   __syncthreads();
 
-  float* Eb = a.E + (bl * a.e_tiles + panel_tiles(blk, NT, 4) - (int64_t)blk * 4) * TILE;
-  const int jt_own = blk * 4;  // the block's first column tile
-  const int ntile = jt1 - jt0;
-  // Gram accumulators of two tiles: the MFMAs of tile i+1 are issued before
-  // the exp epilogue of tile i, so the two overlap.
-  floatx4_t gk[2][WRT], gv[2][WRT];
-#define SCORE_MMA(STAGE, SLOT)                                                          \
-  do {                                                                                  \
-    uint4 bk_[NV], bv_[NV];                                                             \
-    _Pragma("unroll") for (int v_ = 0; v_ < NV; ++v_) {                                 \
-      bk_[v_] = reinterpret_cast<const uint4*>(smem + ((STAGE) * CH + v_) * 1024)[lane]; \
-      bv_[v_] = reinterpret_cast<const uint4*>(smem + ((STAGE) * CH + NV + v_) * 1024)[lane]; \
-    }                                                                                   \
-    _Pragma("unroll") for (int rt_ = 0; rt_ < WRT; ++rt_) {                             \
-      gk[SLOT][rt_] = (floatx4_t){0.f, 0.f, 0.f, 0.f};                                  \
-      gv[SLOT][rt_] = (floatx4_t){vm2f, vm2f, vm2f, vm2f}; /* <v,v'> + v_max^2 */      \
-    }                                                                                   \
-    _Pragma("unroll") for (int v_ = 0; v_ < NV; ++v_)                                   \
-      _Pragma("unroll") for (int rt_ = 0; rt_ < WRT; ++rt_) {                           \
-        gk[SLOT][rt_] = mma_word<T>(Ak[rt_][v_], bk_[v_], gk[SLOT][rt_]);               \
-        gv[SLOT][rt_] = mma_word<T>(Av[rt_][v_], bv_[v_], gv[SLOT][rt_]);               \
-      }                                                                                 \
-  } while (0)
-
-  if (has_blk && jt0 >= jt_own) SCORE_MMA(0, 0);
   for (int ib = 0; ib < ntile; ib += DEPTH) {
 #pragma unroll
     for (int u = 0; u < DEPTH; ++u) {
       const int i = ib + u;
       const int jt = jt0 + i;
       if (i < ntile) {  // uniform over the workgroup
-        // scale of tile i+1; stage tile i+2; load tile i+2+DEPTH
+        // scale of tile i+1; stage tile i+2 (and load tile i+2+DEPTH)
         if (wave == i % kScoreWaves) tile_h2((u + 1) % NS);
-        SCORE_COMMIT((u + 2) % NS, (u + 2) % DEPTH);
-        SCORE_ISSUE(jt + 2 + DEPTH, (u + 2) % DEPTH);
-        // Gram of tile i+1 (staged and visible since the last barrier)
-        if (has_blk && i + 1 < ntile && jt + 1 >= jt_own) SCORE_MMA((u + 1) % NS, (u + 1) & 1);
-        // scores of tile i
-        if (has_blk && jt >= jt_own) {
-          const float h2 = jt * 16 + m16 < N ? s_h2[(u % NS) * 16 + m16] : 0.0f;
-          float* tile = Eb + (int64_t)jt * TILE;
+        if (own) {
+          if (i + 2 < ntile) SCORE_OWN_COMMIT((u + 2) % NS, i + 2);
+        } else {
+          SCORE_COMMIT((u + 2) % NS, (u + 2) % DEPTH);
+          SCORE_ISSUE(jt + 2 + DEPTH, (u + 2) % DEPTH);
+        }
+        // Grams and scores of tile i
+        SCORE_MMA(u % NS, jt, 0);
+        const float h2 = jt * 16 + m16 < N ? s_h2[(u % NS) * 16 + m16] : 0.0f;
 #pragma unroll
-          for (int rt = 0; rt < WRT; ++rt) {
+        for (int h = 0; h < HB; ++h) {
+          if (!SCORE_ACTIVE(h, jt)) continue;
+          const int b = hb_blk[h];
+          float* tile = a.E + (bl * a.e_tiles + panel_tiles(b, NT, 4) + jt - 4 * b) * (int64_t)TILE;
+#pragma unroll
+          for (int rt = 0; rt < 2; ++rt) {
             float kap[4];
 #pragma unroll
             for (int e = 0; e < 4; ++e)
-              kap[e] = __builtin_amdgcn_exp2f(fminf(gk[u & 1][rt][e] * c2 - h2, kExpClamp)) *
-                       gv[u & 1][rt][e];
+              kap[e] = __builtin_amdgcn_exp2f(fminf(gk[0][h][rt][e] * c2 - h2, kExpClamp)) *
+                       gv[0][h][rt][e];
             // lane (g, m16) holds kappa(A row 4g+e, column row m16): A pairs
-            // 2g, 2g+1 of the row tile against column row m16
+            // 2g, 2g+1 of the row tile against column row m16; the even
+            // lane of a column pair forms E, lane groups g and g+1 (g even)
+            // combine into four consecutive pairs
             const float F0 = kap[1] - kap[0];
             const float F1 = kap[3] - kap[2];
-            const float F0p = from_partner(F0);
-            const float F1p = from_partner(F1);
-            if ((m16 & 1) == 0)
-              *reinterpret_cast<float2*>(tile + (m16 >> 1) * BP + (sub * WRT + rt) * 8 + 2 * g) =
-                  make_float2(F0 - F0p, F1 - F1p);
+            const float E0 = F0 - from_partner(F0);
+            const float E1 = F1 - from_partner(F1);
+            const float E2 = __uint_as_float(
+                __builtin_amdgcn_permlane16_swap(__float_as_uint(E0), __float_as_uint(E0), false, false)[1]);
+            const float E3 = __uint_as_float(
+                __builtin_amdgcn_permlane16_swap(__float_as_uint(E1), __float_as_uint(E1), false, false)[1]);
+            if ((m16 & 1) == 0 && (g & 1) == 0)
+              *reinterpret_cast<float4*>(tile + (m16 >> 1) * BP + hb_half[h] * 16 + rt * 8 + 2 * g) =
+                  make_float4(E0, E1, E2, E3);
           }
         }
         __syncthreads();
@@ -548,8 +626,11 @@ __global__ __launch_bounds__(64 * kScoreWaves) void pair_scores_kernel(HalveArgs
     }
   }
 #undef SCORE_MMA
+#undef SCORE_ACTIVE
 #undef SCORE_ISSUE
 #undef SCORE_COMMIT
+#undef SCORE_OWN_WRITE
+#undef SCORE_OWN_COMMIT
 }
 
 // Decision pass of one bucket per workgroup, in three roles that run ahead
@@ -580,12 +661,13 @@ __device__ __forceinline__ void publish(int* flag, int value) {
 template <int BW, int NCB>
 struct PassLds {
   static constexpr int BP = 32, QW = 8;
-  // alpha [P] | near alpha [2][BP] | mask ring [4] | counters [2 + BW] |
+  // alpha [P] | near alpha [2][BP] | mask ring [4] | counters: decided,
+  // near, bulk completions per block [4] |
   // decision inputs [3]: scores [BP][QW] words, then lbt, h2, u, row0, row1 [BP]
   __host__ __device__ static size_t near_off(int P) { return ((size_t)P * 8 + 15) & ~(size_t)15; }
   __host__ __device__ static size_t mask_off(int P) { return near_off(P) + 2 * BP * 8; }
   __host__ __device__ static size_t flag_off(int P) { return mask_off(P) + 16; }
-  __host__ __device__ static size_t dcol_off(int P) { return (flag_off(P) + (2 + BW) * 4 + 15) & ~(size_t)15; }
+  __host__ __device__ static size_t dcol_off(int P) { return (flag_off(P) + 6 * 4 + 15) & ~(size_t)15; }
   __host__ __device__ static size_t dsc_off(int P) { return dcol_off(P) + 3 * BP * QW * 16; }
   __host__ __device__ static size_t bytes(int P) { return dsc_off(P) + 3 * 5 * BP * 4; }
 };
@@ -624,12 +706,12 @@ __global__ __launch_bounds__(64 * (BW + 2)) void halve_pass_kernel(HalveArgs a) 
   double* s_alpha = reinterpret_cast<double*>(smem);
   double* s_anear = reinterpret_cast<double*>(smem + L::near_off(P));
   uint32_t* s_mask = reinterpret_cast<uint32_t*>(smem + L::mask_off(P));
-  int* s_flag = reinterpret_cast<int*>(smem + L::flag_off(P));  // decided, near, bulk[BW]
+  int* s_flag = reinterpret_cast<int*>(smem + L::flag_off(P));  // decided, near, bulk count[4]
   u32x4* s_dcol = reinterpret_cast<u32x4*>(smem + L::dcol_off(P));
   uint32_t* s_dsc = reinterpret_cast<uint32_t*>(smem + L::dsc_off(P));
 
   for (int p = threadIdx.x; p < P; p += 64 * (BW + 2)) s_alpha[p] = 0.0;
-  if (threadIdx.x < 2 + BW) s_flag[threadIdx.x] = -1;
+  if (threadIdx.x < 6) s_flag[threadIdx.x] = threadIdx.x < 2 ? -1 : 0;
 
   // Signed sum of a column's BP scores (decision bits in SMASK).
 #define PASS_SUM(SRC, SMASK, SUM)                                                       \
@@ -677,13 +759,14 @@ __global__ __launch_bounds__(64 * (BW + 2)) void halve_pass_kernel(HalveArgs a) 
       _Pragma("unroll") for (int k_ = 0; k_ < 5; ++k_) c_[k_ * BP + lane] = fsc[k_];   \
     }                                                                                  \
   } while (0)
-  // Near update data of block B: the columns of block B+1's pairs (lanes
-  // 32..63 repeat lanes 0..31; lanes past the last pair read the last pair).
-#define PASS_FETCH_NEAR(B)                                                              \
+  // Near update data of block B (< nblk - 1): the columns of block B+1's
+  // pairs (lanes 32..63 repeat lanes 0..31; lanes past the last pair read
+  // the last pair).
+#define PASS_FETCH_NEAR(B, DST)                                                         \
   do {                                                                                 \
     const int p_ = min(((B) + 1) * BP + (lane & (BP - 1)), P - 1);                     \
     const u32x4* c_ = PASS_COL(B, p_);                                                 \
-    _Pragma("unroll") for (int q_ = 0; q_ < QW; ++q_) fnr[q_] = c_[q_];                \
+    _Pragma("unroll") for (int q_ = 0; q_ < QW; ++q_) DST[q_] = c_[q_];                \
   } while (0)
   // Bulk chunk k of block B for bulk wave w: pairs (B+2) BP + (w + k BW) 64 + lane.
 #define PASS_FETCH_CHUNK(B, K, DST)                                                     \
@@ -693,7 +776,7 @@ __global__ __launch_bounds__(64 * (BW + 2)) void halve_pass_kernel(HalveArgs a) 
     _Pragma("unroll") for (int q_ = 0; q_ < QW; ++q_) DST[q_] = c_[q_];                \
   } while (0)
 
-  u32x4 fdc[4], fnr[QW], cb[NCB][QW];
+  u32x4 fdc[4], fnr0[QW], fnr1[QW], cb[NCB][QW];
   uint32_t fsc[5];
   if (wave == 1) {
     PASS_FETCH_DEC(0);
@@ -701,9 +784,10 @@ __global__ __launch_bounds__(64 * (BW + 2)) void halve_pass_kernel(HalveArgs a) 
     if (nblk > 1) {
       PASS_FETCH_DEC(1);
       PASS_STORE_DEC(1);
-      PASS_FETCH_NEAR(0);
+      PASS_FETCH_NEAR(0, fnr0);
+      PASS_FETCH_NEAR(min(1, nblk - 2), fnr1);
+      PASS_FETCH_DEC(min(2, nblk - 1));
     }
-    if (nblk > 2) PASS_FETCH_DEC(2);
   } else if (wave >= 2 && nblk > 2) {
 #pragma unroll
     for (int k = 0; k < NCB; ++k) PASS_FETCH_CHUNK(0, k, cb[k]);
@@ -712,12 +796,19 @@ __global__ __launch_bounds__(64 * (BW + 2)) void halve_pass_kernel(HalveArgs a) 
 
   if (wave == 0) {
     // ---- decider ----
+    // the decider and the near-update wave are the critical path: they are
+    // issued ahead of the bulk waves sharing their SIMDs
+    __builtin_amdgcn_s_setprio(3);
     double carry = -INFINITY;  // log b_max over the pairs already decided
     for (int m = 0; m < nblk; ++m) {
       const int npb = min(BP, P - m * BP);
       if (m >= 1) wait_at_least(&s_flag[1], m - 1);
-      if (m >= 2)
-        for (int w = 0; w < BW; ++w) wait_at_least(&s_flag[2 + w], m - 2);
+      if (m >= 2) {
+        // every bulk wave has added block m-2; the slot is free again once
+        // block m+2's bulk starts, which needs this block's decisions
+        wait_at_least(&s_flag[2 + ((m - 2) & 3)], BW);
+        s_flag[2 + ((m - 2) & 3)] = 0;
+      }
       const int p = lane;
       const bool active = p < npb;
       const int gp = m * BP + p;
@@ -746,27 +837,31 @@ __global__ __launch_bounds__(64 * (BW + 2)) void halve_pass_kernel(HalveArgs a) 
       } else {
         thr = exp_fast((double)lbtf + lbmax + a.log_c - half_h) * (1.0 - 2.0 * (double)u_blk);
       }
-      // this pair's scores against the block's earlier pairs
-      float ecol[BP];
+      // this pair's scores against the block's earlier pairs, masked and
+      // widened before the loop (held in registers: the loop below is the
+      // decider's critical path and must not wait on LDS)
+      double ed[BP];
 #pragma unroll
       for (int q = 0; q < QW; ++q) {
         const u32x4 x = dc[q];
-        ecol[4 * q] = __uint_as_float(x.x);
-        ecol[4 * q + 1] = __uint_as_float(x.y);
-        ecol[4 * q + 2] = __uint_as_float(x.z);
-        ecol[4 * q + 3] = __uint_as_float(x.w);
-      }
 #pragma unroll
-      for (int i = 0; i < BP; ++i) ecol[i] = (active && p > i) ? ecol[i] : 0.0f;
-      uint64_t smask = 0;
+        for (int c = 0; c < 4; ++c) {
+          const int i = 4 * q + c;
+          ed[i] = (active && p > i) ? (double)__uint_as_float(x[c]) : 0.0;
+          asm volatile("" : "+v"(ed[i]));
+        }
+      }
+      // decision i: ballot of alpha < threshold, then every later pair's
+      // alpha takes +-E(i,p) (the sign bit flipped when pair i swaps)
+      uint32_t smask = 0;
 #pragma unroll
       for (int i = 0; i < BP; ++i) {
         if (i < npb) {
           const uint64_t bal = __ballot(alpha < thr);
-          const uint64_t si = (bal >> i) & 1ull;
+          const uint32_t si = (uint32_t)(bal >> i) & 1u;
           smask |= si << i;
-          const double e = (double)ecol[i];
-          alpha += si ? -e : e;
+          const double e = __hiloint2double(__double2hiint(ed[i]) ^ (int)(si << 31), __double2loint(ed[i]));
+          alpha += e;
         }
       }
       carry = __shfl(lbmax, npb - 1);
@@ -780,19 +875,27 @@ __global__ __launch_bounds__(64 * (BW + 2)) void halve_pass_kernel(HalveArgs a) 
     }
   } else if (wave == 1) {
     // ---- next-block updates and the decider's inputs ----
-    for (int b = 0; b + 1 < nblk; ++b) {
-      wait_at_least(&s_flag[0], b);
-      const uint32_t smask = s_mask[b & 3];
-      float sum;
-      PASS_SUM(fnr, smask, sum);
-      if (lane < BP) s_anear[((b + 1) & 1) * BP + lane] = (double)sum;
-      publish(&s_flag[1], b);
-      if (b + 2 < nblk) {
-        PASS_STORE_DEC(b + 2);
-        PASS_FETCH_NEAR(b + 1);
-      }
-      if (b + 3 < nblk) PASS_FETCH_DEC(b + 3);
+    __builtin_amdgcn_s_setprio(2);
+    // Near data two blocks ahead (two buffers), decision inputs three ahead;
+    // fetches past the end repeat the last valid block (harmless, and the
+    // loads stay unconditional).
+#define PASS_NEAR_STEP(B, BUF)                                                          \
+  do {                                                                                 \
+    wait_at_least(&s_flag[0], B);                                                      \
+    const uint32_t smask_ = s_mask[(B) & 3];                                           \
+    float sum_;                                                                        \
+    PASS_SUM(BUF, smask_, sum_);                                                       \
+    if (lane < BP) s_anear[(((B) + 1) & 1) * BP + lane] = (double)sum_;                \
+    publish(&s_flag[1], B);                                                            \
+    if ((B) + 2 < nblk) PASS_STORE_DEC((B) + 2);                                       \
+    PASS_FETCH_NEAR(min((B) + 2, nblk - 2), BUF);                                      \
+    PASS_FETCH_DEC(min((B) + 3, nblk - 1));                                            \
+  } while (0)
+    for (int b = 0; b + 1 < nblk; b += 2) {
+      PASS_NEAR_STEP(b, fnr0);
+      if (b + 2 < nblk) PASS_NEAR_STEP(b + 1, fnr1);
     }
+#undef PASS_NEAR_STEP
   } else {
     // ---- bulk updates, blocks 0 .. nblk-3 ----
     for (int b = 0; b + 2 < nblk; ++b) {
@@ -814,7 +917,7 @@ __global__ __launch_bounds__(64 * (BW + 2)) void halve_pass_kernel(HalveArgs a) 
         const int p = p0 + 64 * BW * k;
         if (p < P) s_alpha[p] += (double)sum;
       }
-      publish(&s_flag[2 + wave - 2], b);
+      __hip_atomic_fetch_add(&s_flag[2 + (b & 3)], 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
       if (b + 3 < nblk) {
 #pragma unroll
         for (int k = 0; k < NCB; ++k) PASS_FETCH_CHUNK(b + 1, k, cb[k]);
@@ -855,9 +958,9 @@ hipError_t launch_scores_td(const HalveArgs& a, int64_t nbk, hipStream_t st) {
     if (e != hipSuccess) return e;
   }
   const int64_t NT = (a.N + 15) / 16;
-  const int64_t nb = (a.N + 63) / 64;
-  const int64_t groups = (nb + SS::BLOCKS - 1) / SS::BLOCKS;
-  const int64_t nch = (NT + a.ch - 1) / a.ch;
+  const int64_t groups = (NT + SS::GT - 1) / SS::GT;
+  const int64_t rest = NT > SS::GT ? NT - SS::GT : 0;  // tiles after the first group
+  const int64_t nch = 1 + (rest + a.ch - 1) / a.ch;
   dim3 grid((unsigned)nbk, (unsigned)groups, (unsigned)nch);
   hipLaunchKernelGGL(kern, grid, dim3(64 * kScoreWaves), lds, st, a);
   return hipGetLastError();

@@ -635,17 +635,19 @@ void pair_scores_kernel(HalveArgs a) {
 
 // Decision pass of one bucket per workgroup, in three roles that run ahead
 // of or behind each other, synchronised by progress counters in LDS:
-//  - wave 0 (decider) takes the decisions block after block;
-//  - wave 1 adds each decided block's scores to the next block's pairs (the
-//    only update on the decider's critical path) and fetches the decider's
-//    inputs two blocks ahead;
+//  - wave 1 (fetcher) stages each block's inputs in a ring of three LDS
+//    slots, up to two blocks ahead of the decider: the block's own scores, the scores
+//    against the next block's pairs, the row indices, and the thresholds
+//    a(1 - 2u), which depend on no decision (the running maximum of b over
+//    the bucket is carried from block to block);
+//  - wave 0 (decider) takes the decisions of a block two at a time (the
+//    second decision is evaluated for both outcomes of the first), publishes
+//    them, then adds the block's scores to the next block's pairs itself;
 //  - waves 2.. (bulk) add each decided block's scores to all pairs two or
-//    more blocks later.
+//    more blocks later, with their next column chunks fetched in advance.
 // alpha of a pair in block m = (contributions of blocks <= m-2, summed by the
-// bulk waves in block order) + (contribution of block m-1, from wave 1).
-// Everything read from global memory is independent of the decisions and is
-// fetched ahead; the decider never waits on global memory.  Every wait is
-// bounded.
+// bulk waves in block order) + (contribution of block m-1, from the decider).
+// The decider never waits on global memory.  Every wait is bounded.
 constexpr int kSpinLimit = 1 << 16;
 
 __device__ __forceinline__ void wait_at_least(const int* flag, int target) {
@@ -660,16 +662,16 @@ __device__ __forceinline__ void publish(int* flag, int value) {
 
 template <int BW, int NCB>
 struct PassLds {
-  static constexpr int BP = 32, QW = 8;
-  // alpha [P] | near alpha [2][BP] | mask ring [4] | counters: decided,
-  // near, bulk completions per block [4] |
-  // decision inputs [3]: scores [BP][QW] words, then lbt, h2, u, row0, row1 [BP]
-  __host__ __device__ static size_t near_off(int P) { return ((size_t)P * 8 + 15) & ~(size_t)15; }
-  __host__ __device__ static size_t mask_off(int P) { return near_off(P) + 2 * BP * 8; }
+  static constexpr int BP = 32, QW = 8, NSLOT = 3;
+  // alpha [P] | mask ring [4] | counters [8]: decided, staged, bulk
+  // completions per block (ring of 4) | NSLOT input slots, each: thresholds
+  // [BP] f64, rows [2][BP] i32, own scores [BP][QW] and next-block scores
+  // [BP][QW] 16-byte words
+  static constexpr size_t kSlot = BP * 8 + 2 * BP * 4 + 2 * BP * QW * 16;
+  __host__ __device__ static size_t mask_off(int P) { return ((size_t)P * 8 + 15) & ~(size_t)15; }
   __host__ __device__ static size_t flag_off(int P) { return mask_off(P) + 16; }
-  __host__ __device__ static size_t dcol_off(int P) { return (flag_off(P) + 6 * 4 + 15) & ~(size_t)15; }
-  __host__ __device__ static size_t dsc_off(int P) { return dcol_off(P) + 3 * BP * QW * 16; }
-  __host__ __device__ static size_t bytes(int P) { return dsc_off(P) + 3 * 5 * BP * 4; }
+  __host__ __device__ static size_t slot_off(int P) { return flag_off(P) + 32; }
+  __host__ __device__ static size_t bytes(int P) { return slot_off(P) + NSLOT * kSlot; }
 };
 
 template <int BW, int NCB>
@@ -704,14 +706,18 @@ __global__ __launch_bounds__(64 * (BW + 2)) void halve_pass_kernel(HalveArgs a) 
 
   extern __shared__ __align__(16) unsigned char smem[];
   double* s_alpha = reinterpret_cast<double*>(smem);
-  double* s_anear = reinterpret_cast<double*>(smem + L::near_off(P));
   uint32_t* s_mask = reinterpret_cast<uint32_t*>(smem + L::mask_off(P));
-  int* s_flag = reinterpret_cast<int*>(smem + L::flag_off(P));  // decided, near, bulk count[4]
-  u32x4* s_dcol = reinterpret_cast<u32x4*>(smem + L::dcol_off(P));
-  uint32_t* s_dsc = reinterpret_cast<uint32_t*>(smem + L::dsc_off(P));
+  int* s_cnt = reinterpret_cast<int*>(smem + L::flag_off(P));  // decided, staged, bulk[4]
+  auto slot = [&](int m) { return smem + L::slot_off(P) + (size_t)(m % L::NSLOT) * L::kSlot; };
+  // slot fields
+  auto sl_thr = [&](unsigned char* b) { return reinterpret_cast<double*>(b); };
+  auto sl_rows = [&](unsigned char* b) { return reinterpret_cast<int32_t*>(b + BP * 8); };
+  auto sl_own = [&](unsigned char* b) { return reinterpret_cast<u32x4*>(b + BP * 8 + 2 * BP * 4); };
+  auto sl_next = [&](unsigned char* b) { return reinterpret_cast<u32x4*>(b + BP * 8 + 2 * BP * 4 + BP * QW * 16); };
 
   for (int p = threadIdx.x; p < P; p += 64 * (BW + 2)) s_alpha[p] = 0.0;
-  if (threadIdx.x < 6) s_flag[threadIdx.x] = threadIdx.x < 2 ? -1 : 0;
+  if (threadIdx.x < 8) s_cnt[threadIdx.x] = threadIdx.x < 2 ? -1 : 0;
+  __syncthreads();
 
   // Signed sum of a column's BP scores (decision bits in SMASK).
 #define PASS_SUM(SRC, SMASK, SUM)                                                       \
@@ -724,126 +730,41 @@ __global__ __launch_bounds__(64 * (BW + 2)) void halve_pass_kernel(HalveArgs a) 
         SUM += (((SMASK) >> (4 * q_ + c_)) & 1u) ? -e_[c_] : e_[c_];                   \
     }                                                                                  \
   } while (0)
-  // Column of pair P_ in block B's score panel (P_ after block B).
+  // Column of pair P_ in block B's score panel (P_ at or after block B).
 #define PASS_COL(B, P_)                                                                 \
   reinterpret_cast<const u32x4*>(Eb + (panel_tiles(B, NT, RT) + ((P_) >> 3) - (B) * RT) * TILE + \
                                  ((P_) & 7) * BP)
-  // Decision inputs of block B (wave 1): lane l loads word l%QW of the
-  // columns of pairs l/QW + 8r; lanes < BP also the pair terms, uniform and
-  // rows of pair l.  Lanes past the block's last pair read that pair's.
-#define PASS_FETCH_DEC(B)                                                               \
-  do {                                                                                 \
-    const int npb_ = min(BP, P - (B) * BP);                                            \
-    const float* e_ = Eb + panel_tiles(B, NT, RT) * TILE;                              \
-    _Pragma("unroll") for (int r_ = 0; r_ < 4; ++r_) {                                 \
-      const int pc_ = min(lane / QW + 8 * r_, npb_ - 1);                               \
-      fdc[r_] = reinterpret_cast<const u32x4*>(e_ + (pc_ >> 3) * TILE + (pc_ & 7) * BP)[lane % QW]; \
-    }                                                                                  \
-    const int gp_ = (B) * BP + min(lane & (BP - 1), npb_ - 1);                         \
-    fsc[0] = __float_as_uint(a.lbt[pb + gp_]);                                         \
-    fsc[1] = __float_as_uint(a.h2[pb + gp_]);                                          \
-    fsc[2] = __float_as_uint(Ub[gp_]);                                                 \
-    fsc[3] = (uint32_t)rsrc[rows_in ? 2 * gp_ : 0];                                    \
-    fsc[4] = (uint32_t)rsrc[rows_in ? 2 * gp_ + 1 : 0];                                \
-    if (!rows_in) {                                                                    \
-      fsc[3] = (uint32_t)(row_base + 2 * gp_);                                         \
-      fsc[4] = (uint32_t)(row_base + 2 * gp_ + 1);                                     \
-    }                                                                                  \
-  } while (0)
-#define PASS_STORE_DEC(B)                                                               \
-  do {                                                                                 \
-    u32x4* d_ = s_dcol + ((B) % 3) * BP * QW;                                          \
-    _Pragma("unroll") for (int r_ = 0; r_ < 4; ++r_) d_[(lane / QW + 8 * r_) * QW + lane % QW] = fdc[r_]; \
-    if (lane < BP) {                                                                   \
-      uint32_t* c_ = s_dsc + ((B) % 3) * 5 * BP;                                       \
-      _Pragma("unroll") for (int k_ = 0; k_ < 5; ++k_) c_[k_ * BP + lane] = fsc[k_];   \
-    }                                                                                  \
-  } while (0)
-  // Near update data of block B (< nblk - 1): the columns of block B+1's
-  // pairs (lanes 32..63 repeat lanes 0..31; lanes past the last pair read
-  // the last pair).
-#define PASS_FETCH_NEAR(B, DST)                                                         \
-  do {                                                                                 \
-    const int p_ = min(((B) + 1) * BP + (lane & (BP - 1)), P - 1);                     \
-    const u32x4* c_ = PASS_COL(B, p_);                                                 \
-    _Pragma("unroll") for (int q_ = 0; q_ < QW; ++q_) DST[q_] = c_[q_];                \
-  } while (0)
-  // Bulk chunk k of block B for bulk wave w: pairs (B+2) BP + (w + k BW) 64 + lane.
-#define PASS_FETCH_CHUNK(B, K, DST)                                                     \
-  do {                                                                                 \
-    const int p_ = min(((B) + 2) * BP + (wave - 2 + (K) * BW) * 64 + lane, P - 1);     \
-    const u32x4* c_ = PASS_COL(B, p_);                                                 \
-    _Pragma("unroll") for (int q_ = 0; q_ < QW; ++q_) DST[q_] = c_[q_];                \
-  } while (0)
-
-  u32x4 fdc[4], fnr0[QW], fnr1[QW], cb[NCB][QW];
-  uint32_t fsc[5];
-  if (wave == 1) {
-    PASS_FETCH_DEC(0);
-    PASS_STORE_DEC(0);
-    if (nblk > 1) {
-      PASS_FETCH_DEC(1);
-      PASS_STORE_DEC(1);
-      PASS_FETCH_NEAR(0, fnr0);
-      PASS_FETCH_NEAR(min(1, nblk - 2), fnr1);
-      PASS_FETCH_DEC(min(2, nblk - 1));
-    }
-  } else if (wave >= 2 && nblk > 2) {
-#pragma unroll
-    for (int k = 0; k < NCB; ++k) PASS_FETCH_CHUNK(0, k, cb[k]);
-  }
-  __syncthreads();
 
   if (wave == 0) {
     // ---- decider ----
-    // the decider and the near-update wave are the critical path: they are
-    // issued ahead of the bulk waves sharing their SIMDs
-    __builtin_amdgcn_s_setprio(3);
-    double carry = -INFINITY;  // log b_max over the pairs already decided
+    __builtin_amdgcn_s_setprio(3);  // ahead of the bulk waves sharing its SIMD
+    double anear = 0.0;             // this lane's pair: the previous block's contribution
     for (int m = 0; m < nblk; ++m) {
       const int npb = min(BP, P - m * BP);
-      if (m >= 1) wait_at_least(&s_flag[1], m - 1);
+      wait_at_least(&s_cnt[1], m);
       if (m >= 2) {
-        // every bulk wave has added block m-2; the slot is free again once
-        // block m+2's bulk starts, which needs this block's decisions
-        wait_at_least(&s_flag[2 + ((m - 2) & 3)], BW);
-        s_flag[2 + ((m - 2) & 3)] = 0;
+        // every bulk wave has added block m-2; the counter slot is free again
+        // once block m+2's bulk starts, which needs this block's decisions
+        wait_at_least(&s_cnt[2 + ((m - 2) & 3)], BW);
+        s_cnt[2 + ((m - 2) & 3)] = 0;
       }
+      unsigned char* sb = slot(m);
       const int p = lane;
+      const int pl = lane & (BP - 1);
       const bool active = p < npb;
       const int gp = m * BP + p;
-      const int pl = lane & (BP - 1);
-      const uint32_t* sc = s_dsc + (m % 3) * 5 * BP;
-      const u32x4* dc = s_dcol + (m % 3) * BP * QW + pl * QW;
-      const double anear = m >= 1 ? s_anear[(m & 1) * BP + pl] : 0.0;
       const double alpha_in = s_alpha[min(gp, P - 1)] + anear;
-      const float lbt_in = __uint_as_float(sc[pl]);
-      const float h2_in = __uint_as_float(sc[BP + pl]);
-      const float u_in = __uint_as_float(sc[2 * BP + pl]);
-      const int32_t r0 = (int32_t)sc[3 * BP + pl];
-      const int32_t r1 = (int32_t)sc[4 * BP + pl];
+      const double thr = sl_thr(sb)[pl];
+      const int32_t r0 = sl_rows(sb)[pl], r1 = sl_rows(sb)[BP + pl];
       double alpha = active ? alpha_in : 0.0;
-      const float lbtf = active ? lbt_in : -INFINITY;
-      const float h2f = active ? h2_in : 0.0f;
-      const float u_blk = active ? u_in : 0.5f;
-      const double half_h = (double)h2f * (0.5 * kLn2);
-      // running maximum of log b over this block's pairs (pair order), then
-      // combined with the maximum over all earlier blocks
-      const double pm = prefix_max32(active ? (double)lbtf + half_h : -INFINITY, lane);
-      const double lbmax = fmax(carry, pm);
-      double thr;
-      if (!(lbtf > -INFINITY) || !(lbmax > -INFINITY)) {
-        thr = (u_blk < 0.5f) ? INFINITY : -INFINITY;  // a = 0: p = 1/2
-      } else {
-        thr = exp_fast((double)lbtf + lbmax + a.log_c - half_h) * (1.0 - 2.0 * (double)u_blk);
-      }
       // this pair's scores against the block's earlier pairs, masked and
-      // widened before the loop (held in registers: the loop below is the
+      // widened before the loop (held in registers: the loop is the
       // decider's critical path and must not wait on LDS)
       double ed[BP];
+      const u32x4* oc = sl_own(sb) + pl * QW;
 #pragma unroll
       for (int q = 0; q < QW; ++q) {
-        const u32x4 x = dc[q];
+        const u32x4 x = oc[q];
 #pragma unroll
         for (int c = 0; c < 4; ++c) {
           const int i = 4 * q + c;
@@ -851,55 +772,130 @@ __global__ __launch_bounds__(64 * (BW + 2)) void halve_pass_kernel(HalveArgs a) 
           asm volatile("" : "+v"(ed[i]));
         }
       }
-      // decision i: ballot of alpha < threshold, then every later pair's
-      // alpha takes +-E(i,p) (the sign bit flipped when pair i swaps)
+      // Decisions i and i+1 per step: alpha < thr for pair i, and for pair
+      // i+1 under both signs of pair i's score; alpha then takes the two
+      // signed scores (pair i swapped: -E(i,.), else +E(i,.)).
       uint32_t smask = 0;
 #pragma unroll
-      for (int i = 0; i < BP; ++i) {
+      for (int i = 0; i < BP; i += 2) {
         if (i < npb) {
-          const uint64_t bal = __ballot(alpha < thr);
-          const uint32_t si = (uint32_t)(bal >> i) & 1u;
-          smask |= si << i;
-          const double e = __hiloint2double(__double2hiint(ed[i]) ^ (int)(si << 31), __double2loint(ed[i]));
-          alpha += e;
+          const double ap = alpha + ed[i], am = alpha - ed[i];
+          const uint64_t b0 = __ballot(alpha < thr);
+          const uint64_t bp = __ballot(ap < thr);
+          const uint64_t bm = __ballot(am < thr);
+          const uint32_t s0 = (uint32_t)(b0 >> i) & 1u;
+          const uint32_t s1 = i + 1 < npb ? (uint32_t)((s0 ? bm : bp) >> (i + 1)) & 1u : 0u;
+          smask |= (s0 << i) | (s1 << (i + 1));
+          const double a1 = s0 ? am : ap;
+          alpha = a1 + __hiloint2double(__double2hiint(ed[i + 1]) ^ (int)(s1 << 31), __double2loint(ed[i + 1]));
         }
       }
-      carry = __shfl(lbmax, npb - 1);
-      const uint32_t bit = (uint32_t)((smask >> p) & 1ull);
+      const uint32_t bit = (smask >> (p & 31)) & 1u;
       if (active) {
         out[gp] = bit ? r1 : r0;
         if (trace) trace[gp] = (uint8_t)bit;
       }
-      if (lane == 0) s_mask[m & 3] = (uint32_t)smask;
-      publish(&s_flag[0], m);
+      if (lane == 0) s_mask[m & 3] = smask;
+      publish(&s_cnt[0], m);
+      // the next block's pairs take this block's signed scores
+      if (m + 1 < nblk) {
+        const u32x4* nc = sl_next(sb) + pl * QW;
+        u32x4 col[QW];
+#pragma unroll
+        for (int q = 0; q < QW; ++q) col[q] = nc[q];
+        float sum;
+        PASS_SUM(col, smask, sum);
+        anear = (double)sum;
+      }
     }
   } else if (wave == 1) {
-    // ---- next-block updates and the decider's inputs ----
+    // ---- fetcher: block m's inputs into slot m % 3 ----
+    // Lane l fetches word l%QW of the columns of pairs l/QW + 8r (r < 4) of
+    // the block's own scores and of its scores against the next block; lanes
+    // < BP also the pair terms, uniform and rows of pair l.  Lanes past a
+    // block's last pair read that pair's inputs.  One block is fetched while
+    // the previous one is staged.
     __builtin_amdgcn_s_setprio(2);
-    // Near data two blocks ahead (two buffers), decision inputs three ahead;
-    // fetches past the end repeat the last valid block (harmless, and the
-    // loads stay unconditional).
-#define PASS_NEAR_STEP(B, BUF)                                                          \
+    u32x4 fo[2][4], fn[2][4];
+    float flbt[2], fh2[2], fu[2];
+    int32_t fr0[2], fr1[2];
+#define PASS_FETCH(B, K)                                                                \
   do {                                                                                 \
-    wait_at_least(&s_flag[0], B);                                                      \
-    const uint32_t smask_ = s_mask[(B) & 3];                                           \
-    float sum_;                                                                        \
-    PASS_SUM(BUF, smask_, sum_);                                                       \
-    if (lane < BP) s_anear[(((B) + 1) & 1) * BP + lane] = (double)sum_;                \
-    publish(&s_flag[1], B);                                                            \
-    if ((B) + 2 < nblk) PASS_STORE_DEC((B) + 2);                                       \
-    PASS_FETCH_NEAR(min((B) + 2, nblk - 2), BUF);                                      \
-    PASS_FETCH_DEC(min((B) + 3, nblk - 1));                                            \
+    const int b_ = min(B, nblk - 1);                                                   \
+    const int npb_ = min(BP, P - b_ * BP);                                             \
+    const float* e_ = Eb + panel_tiles(b_, NT, RT) * TILE;                             \
+    _Pragma("unroll") for (int r_ = 0; r_ < 4; ++r_) {                                 \
+      const int pc_ = min(lane / QW + 8 * r_, npb_ - 1);                               \
+      fo[K][r_] = reinterpret_cast<const u32x4*>(e_ + (pc_ >> 3) * TILE + (pc_ & 7) * BP)[lane % QW]; \
+      /* next block's pairs (the last block reads its own last column) */           \
+      const int pn_ = min((b_ + 1) * BP + lane / QW + 8 * r_, P - 1);                  \
+      fn[K][r_] = PASS_COL(b_, pn_)[lane % QW];                                        \
+    }                                                                                  \
+    const int gp_ = b_ * BP + min(lane & (BP - 1), npb_ - 1);                          \
+    flbt[K] = a.lbt[pb + gp_];                                                         \
+    fh2[K] = a.h2[pb + gp_];                                                           \
+    fu[K] = Ub[gp_];                                                                   \
+    fr0[K] = rsrc[rows_in ? 2 * gp_ : 0];                                              \
+    fr1[K] = rsrc[rows_in ? 2 * gp_ + 1 : 0];                                          \
   } while (0)
-    for (int b = 0; b + 1 < nblk; b += 2) {
-      PASS_NEAR_STEP(b, fnr0);
-      if (b + 2 < nblk) PASS_NEAR_STEP(b + 1, fnr1);
+    double carry = -INFINITY;  // log b_max over the pairs of earlier blocks
+#define PASS_STAGE(B, K)                                                                \
+  do {                                                                                 \
+    const int npb_ = min(BP, P - (B) * BP);                                            \
+    const bool act_ = lane < npb_;                                                     \
+    const float lbtf_ = act_ ? flbt[K] : -INFINITY;                                    \
+    const float h2f_ = act_ ? fh2[K] : 0.0f;                                           \
+    const double half_h_ = (double)h2f_ * (0.5 * kLn2);                                \
+    const double pm_ = prefix_max32(act_ ? (double)lbtf_ + half_h_ : -INFINITY, lane);  \
+    const double lbmax_ = fmax(carry, pm_);                                            \
+    double thr_;                                                                       \
+    if (!(lbtf_ > -INFINITY) || !(lbmax_ > -INFINITY))                                 \
+      thr_ = (fu[K] < 0.5f) ? INFINITY : -INFINITY; /* a = 0: p = 1/2 */              \
+    else                                                                               \
+      thr_ = exp_fast((double)lbtf_ + lbmax_ + a.log_c - half_h_) * (1.0 - 2.0 * (double)fu[K]); \
+    carry = __shfl(lbmax_, npb_ - 1);                                                  \
+    /* slot B%3 held block B-3, which the decider has left once B-2 is decided */    \
+    if ((B) >= L::NSLOT) wait_at_least(&s_cnt[0], (B) - (L::NSLOT - 1));              \
+    unsigned char* sb_ = slot(B);                                                      \
+    _Pragma("unroll") for (int r_ = 0; r_ < 4; ++r_) {                                 \
+      sl_own(sb_)[(lane / QW + 8 * r_) * QW + lane % QW] = fo[K][r_];                  \
+      sl_next(sb_)[(lane / QW + 8 * r_) * QW + lane % QW] = fn[K][r_];                 \
+    }                                                                                  \
+    if (lane < BP) {                                                                   \
+      sl_thr(sb_)[lane] = thr_;                                                        \
+      sl_rows(sb_)[lane] = rows_in ? fr0[K] : (int32_t)(row_base + 2 * ((B) * BP + lane)); \
+      sl_rows(sb_)[BP + lane] = rows_in ? fr1[K] : (int32_t)(row_base + 2 * ((B) * BP + lane) + 1); \
+    }                                                                                  \
+    publish(&s_cnt[1], B);                                                             \
+  } while (0)
+    PASS_FETCH(0, 0);
+    for (int m = 0; m < nblk; m += 2) {
+      PASS_FETCH(m + 1, 1);
+      PASS_STAGE(m, 0);
+      if (m + 1 < nblk) {
+        PASS_FETCH(m + 2, 0);
+        PASS_STAGE(m + 1, 1);
+      }
     }
-#undef PASS_NEAR_STEP
+#undef PASS_FETCH
+#undef PASS_STAGE
   } else {
     // ---- bulk updates, blocks 0 .. nblk-3 ----
+    // Bulk wave w = wave-2, chunk k of block B: pairs (B+2) BP + (w + k BW) 64
+    // + lane (lanes past the last pair load the last pair's column).
+#define PASS_FETCH_CHUNK(B, K, DST)                                                     \
+  do {                                                                                 \
+    const int p_ = min(((B) + 2) * BP + (wave - 2 + (K) * BW) * 64 + lane, P - 1);     \
+    const u32x4* c_ = PASS_COL(B, p_);                                                 \
+    _Pragma("unroll") for (int q_ = 0; q_ < QW; ++q_) DST[q_] = c_[q_];                \
+  } while (0)
+    u32x4 cb[NCB][QW];
+    if (nblk > 2) {
+#pragma unroll
+      for (int k = 0; k < NCB; ++k) PASS_FETCH_CHUNK(0, k, cb[k]);
+    }
     for (int b = 0; b + 2 < nblk; ++b) {
-      wait_at_least(&s_flag[0], b);
+      wait_at_least(&s_cnt[0], b);
       const uint32_t smask = s_mask[b & 3];
       const int p0 = (b + 2) * BP + (wave - 2) * 64 + lane;
 #pragma unroll
@@ -917,19 +913,16 @@ __global__ __launch_bounds__(64 * (BW + 2)) void halve_pass_kernel(HalveArgs a) 
         const int p = p0 + 64 * BW * k;
         if (p < P) s_alpha[p] += (double)sum;
       }
-      __hip_atomic_fetch_add(&s_flag[2 + (b & 3)], 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
+      __hip_atomic_fetch_add(&s_cnt[2 + (b & 3)], 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
       if (b + 3 < nblk) {
 #pragma unroll
         for (int k = 0; k < NCB; ++k) PASS_FETCH_CHUNK(b + 1, k, cb[k]);
       }
     }
+#undef PASS_FETCH_CHUNK
   }
 #undef PASS_SUM
 #undef PASS_COL
-#undef PASS_FETCH_DEC
-#undef PASS_STORE_DEC
-#undef PASS_FETCH_NEAR
-#undef PASS_FETCH_CHUNK
 }
 
 // Gram of rows [0,16) against rows [16,32) through the fragment path used by

@@ -363,6 +363,9 @@ constexpr int kScoreWaves = SCORE_WAVES;
 #endif
 constexpr int kScoreStages = 3;
 constexpr int kScoreChunk = 32;
+// Streamed rows whose indices a workgroup stages: its chunk, rounded up to
+// whole ring turns, plus the ring's look-ahead.
+constexpr int kScoreRowsStaged = (kScoreChunk + 2 * SCORE_DEPTH + 1) * 16;
 
 template <typename T, int D>
 struct ScoreShape {
@@ -374,7 +377,7 @@ struct ScoreShape {
   static constexpr int LPT = (CHUNKS + kScoreWaves - 1) / kScoreWaves;
   // stages, scale exponents, row indices of the streamed column rows
   static constexpr int LDS = kScoreStages * CHUNKS * 1024 + kScoreStages * 16 * 4 +
-                             (kScoreChunk + SCORE_DEPTH + 2) * 16 * 8;
+                             kScoreRowsStaged * 8;
 };
 
 // Block (group-local) and half of half-block slot h of wave w.
@@ -388,6 +391,9 @@ __device__ __forceinline__ void half_block(int w, int h, int& b, int& half) {
     half = w & 1;
   }
 }
+
+// Target of the stores of a streamed chunk's padding tiles (never read).
+__device__ float g_score_sink[256];
 
 template <typename T, int D>
 __global__ __launch_bounds__(64 * kScoreWaves) __attribute__((amdgpu_waves_per_eu(2)))
@@ -458,6 +464,10 @@ void pair_scores_kernel(HalveArgs a) {
       load_frag<T, D>(K, r, g, valid, Ak[h][rt]);
       load_frag<T, D>(V, r, g, valid, Av[h][rt]);
     }
+  // Wait for the fragments here (vmcnt(0)).  Otherwise the first use sits in
+  // the tile loop, whose wait then also covers the score stores of earlier
+  // tiles on every iteration (stores count in vmcnt on this architecture).
+  __builtin_amdgcn_s_waitcnt(0x0F70);
   if (own) {
     const int64_t pb = s * (a.n_r >> 1) + t * (int64_t)P;
 #pragma unroll
@@ -477,7 +487,7 @@ void pair_scores_kernel(HalveArgs a) {
   } else {
     // row indices of every streamed column row, staged first: a data load
     // then never waits on an index load issued behind the ring's loads
-    const int j_end = min(N, (jt1 + DEPTH + 2) * 16);
+    const int j_end = min(N, (jt1 + 2 * DEPTH + 1) * 16);
     for (int j = jt0 * 16 + (int)threadIdx.x; j < j_end; j += 64 * kScoreWaves)
       s_rows[j - jt0 * 16] = rows_in ? (int64_t)rows_in[j] : row_base + j;
   }
@@ -534,11 +544,12 @@ void pair_scores_kernel(HalveArgs a) {
   };
 
   // Gram accumulators; a half-block slot h takes part in tile jt from its
-  // block's diagonal on.  (Two waves per SIMD overlap one wave's MFMAs with
-  // the other's exp epilogue; double-buffered accumulators would not fit.)
+  // block's diagonal on (always, in a streamed chunk).  (Two waves per SIMD
+  // overlap one wave's MFMAs with the other's exp epilogue; double-buffered
+  // accumulators would not fit.)
   floatx4_t gk[1][HB][2], gv[1][HB][2];
-#define SCORE_ACTIVE(H, JT) (hb_ok[H] && (JT) >= hb_blk[H] * 4)
-#define SCORE_MMA(STAGE, JT, SLOT)                                                      \
+#define SCORE_ACTIVE(OWN, H, JT) (!(OWN) || (hb_ok[H] && (JT) >= hb_blk[H] * 4))
+#define SCORE_MMA(OWN, STAGE, JT, SLOT)                                                 \
   do {                                                                                 \
     uint4 bk_[NV], bv_[NV];                                                            \
     _Pragma("unroll") for (int v_ = 0; v_ < NV; ++v_) {                                \
@@ -546,7 +557,7 @@ void pair_scores_kernel(HalveArgs a) {
       bv_[v_] = reinterpret_cast<const uint4*>(smem + ((STAGE) * CH + NV + v_) * 1024)[lane]; \
     }                                                                                  \
     _Pragma("unroll") for (int h_ = 0; h_ < HB; ++h_) {                                \
-      if (!SCORE_ACTIVE(h_, JT)) continue;                                             \
+      if (!SCORE_ACTIVE(OWN, h_, JT)) continue;                                        \
       _Pragma("unroll") for (int rt_ = 0; rt_ < 2; ++rt_) {                            \
         gk[SLOT][h_][rt_] = (floatx4_t){0.f, 0.f, 0.f, 0.f};                           \
         gv[SLOT][h_][rt_] = (floatx4_t){vm2f, vm2f, vm2f, vm2f}; /* <v,v'> + v_max^2 */ \
@@ -559,10 +570,63 @@ void pair_scores_kernel(HalveArgs a) {
     }                                                                                  \
   } while (0)
 
+  // One column tile (tile I of the chunk, ring position U): scale of tile
+  // I+1, staging of tile I+2 (and, streamed, the load of tile I+2+DEPTH),
+  // Grams and scores of tile I.  Lane (g, m16) holds kappa(A row 4g+e,
+  // column row m16) for e = 0..3, i.e. A pairs 2g and 2g+1 of the row tile
+  // against column row m16.  With F = kappa(y'_i, .) - kappa(y_i, .), the
+  // even lane of a column pair stores E(2g, p) = F0 - F0(partner) and the
+  // odd lane E(2g+1, p) = F1(partner) - F1, so every lane stores one score.
+  // A streamed chunk runs whole ring turns: its padding tiles (I >= ntile)
+  // store to a sink.
+#define SCORE_TILE(OWN, I, U)                                                           \
+  do {                                                                                 \
+    const int i_ = (I);                                                                \
+    const int jt_ = jt0 + i_;                                                          \
+    if (wave == i_ % kScoreWaves) tile_h2(((U) + 1) % NS);                             \
+    if (OWN) {                                                                         \
+      if (i_ + 2 < ntile) SCORE_OWN_COMMIT(((U) + 2) % NS, i_ + 2);                    \
+    } else {                                                                           \
+      SCORE_COMMIT(((U) + 2) % NS, ((U) + 2) % DEPTH);                                 \
+      SCORE_ISSUE(jt_ + 2 + DEPTH, ((U) + 2) % DEPTH);                                 \
+    }                                                                                  \
+    SCORE_MMA(OWN, (U) % NS, jt_, 0);                                                  \
+    const float h2_ = jt_ * 16 + m16 < N ? s_h2[((U) % NS) * 16 + m16] : 0.0f;         \
+    _Pragma("unroll") for (int h = 0; h < HB; ++h) {                                   \
+      if (!SCORE_ACTIVE(OWN, h, jt_)) continue;                                        \
+      const int b = hb_blk[h];                                                         \
+      float* tile_ = (OWN) || i_ < ntile                                               \
+          ? a.E + (bl * a.e_tiles + panel_tiles(b, NT, 4) + jt_ - 4 * b) * (int64_t)TILE \
+          : g_score_sink;                                                              \
+      _Pragma("unroll") for (int rt = 0; rt < 2; ++rt) {                               \
+        float kap[4];                                                                  \
+        _Pragma("unroll") for (int e = 0; e < 4; ++e)                                  \
+          kap[e] = __builtin_amdgcn_exp2f(fminf(gk[0][h][rt][e] * c2 - h2_, kExpClamp)) * \
+                   gv[0][h][rt][e];                                                    \
+        const float F0 = kap[1] - kap[0];                                              \
+        const float F1 = kap[3] - kap[2];                                              \
+        const float mine_ = odd ? F1 : F0;                                             \
+        const float other_ = from_partner(odd ? F0 : F1);                              \
+        tile_[(m16 >> 1) * BP + hb_half[h] * 16 + rt * 8 + 2 * g + (m16 & 1)] =        \
+            odd ? other_ - mine_ : mine_ - other_;                                     \
+      }                                                                                \
+    }                                                                                  \
+    __syncthreads();                                                                   \
+  } while (0)
+
+  const bool odd = (m16 & 1) != 0;
   __syncthreads();
   if (own) {
     SCORE_OWN_COMMIT(0, 0);
     if (ntile > 1) SCORE_OWN_COMMIT(1, 1);
+    __syncthreads();
+    if (wave == 0) tile_h2(0);
+    __syncthreads();
+    for (int ib = 0; ib < ntile; ib += DEPTH) {
+#pragma unroll
+      for (int u = 0; u < DEPTH; ++u)
+        if (ib + u < ntile) SCORE_TILE(true, ib + u, u);  // uniform over the workgroup
+    }
   } else {
 #pragma unroll
     for (int k = 0; k < DEPTH; ++k) SCORE_ISSUE(jt0 + k, k);
@@ -570,61 +634,21 @@ void pair_scores_kernel(HalveArgs a) {
     SCORE_COMMIT(1, 1);
     SCORE_ISSUE(jt0 + DEPTH, 0);
     SCORE_ISSUE(jt0 + DEPTH + 1, 1);
-  }
-  __syncthreads();
-  if (wave == 0) tile_h2(0);
-  __syncthreads();
-
-  for (int ib = 0; ib < ntile; ib += DEPTH) {
+    __syncthreads();
+    if (wave == 0) tile_h2(0);
+    __syncthreads();
+    // The first ring turn is peeled: the loop is then entered with the same
+    // loads and stores in flight as at its back edge, so the compiler's wait
+    // for a staged tile is for that tile's loads only, not for the stores
+    // issued after them (stores count in vmcnt on this architecture).
 #pragma unroll
-    for (int u = 0; u < DEPTH; ++u) {
-      const int i = ib + u;
-      const int jt = jt0 + i;
-      if (i < ntile) {  // uniform over the workgroup
-        // scale of tile i+1; stage tile i+2 (and load tile i+2+DEPTH)
-        if (wave == i % kScoreWaves) tile_h2((u + 1) % NS);
-        if (own) {
-          if (i + 2 < ntile) SCORE_OWN_COMMIT((u + 2) % NS, i + 2);
-        } else {
-          SCORE_COMMIT((u + 2) % NS, (u + 2) % DEPTH);
-          SCORE_ISSUE(jt + 2 + DEPTH, (u + 2) % DEPTH);
-        }
-        // Grams and scores of tile i
-        SCORE_MMA(u % NS, jt, 0);
-        const float h2 = jt * 16 + m16 < N ? s_h2[(u % NS) * 16 + m16] : 0.0f;
+    for (int u = 0; u < DEPTH; ++u) SCORE_TILE(false, u, u);
+    for (int ib = DEPTH; ib < ntile; ib += DEPTH) {
 #pragma unroll
-        for (int h = 0; h < HB; ++h) {
-          if (!SCORE_ACTIVE(h, jt)) continue;
-          const int b = hb_blk[h];
-          float* tile = a.E + (bl * a.e_tiles + panel_tiles(b, NT, 4) + jt - 4 * b) * (int64_t)TILE;
-#pragma unroll
-          for (int rt = 0; rt < 2; ++rt) {
-            float kap[4];
-#pragma unroll
-            for (int e = 0; e < 4; ++e)
-              kap[e] = __builtin_amdgcn_exp2f(fminf(gk[0][h][rt][e] * c2 - h2, kExpClamp)) *
-                       gv[0][h][rt][e];
-            // lane (g, m16) holds kappa(A row 4g+e, column row m16): A pairs
-            // 2g, 2g+1 of the row tile against column row m16; the even
-            // lane of a column pair forms E, lane groups g and g+1 (g even)
-            // combine into four consecutive pairs
-            const float F0 = kap[1] - kap[0];
-            const float F1 = kap[3] - kap[2];
-            const float E0 = F0 - from_partner(F0);
-            const float E1 = F1 - from_partner(F1);
-            const float E2 = __uint_as_float(
-                __builtin_amdgcn_permlane16_swap(__float_as_uint(E0), __float_as_uint(E0), false, false)[1]);
-            const float E3 = __uint_as_float(
-                __builtin_amdgcn_permlane16_swap(__float_as_uint(E1), __float_as_uint(E1), false, false)[1]);
-            if ((m16 & 1) == 0 && (g & 1) == 0)
-              *reinterpret_cast<float4*>(tile + (m16 >> 1) * BP + hb_half[h] * 16 + rt * 8 + 2 * g) =
-                  make_float4(E0, E1, E2, E3);
-          }
-        }
-        __syncthreads();
-      }
+      for (int u = 0; u < DEPTH; ++u) SCORE_TILE(false, ib + u, u);
     }
   }
+#undef SCORE_TILE
 #undef SCORE_MMA
 #undef SCORE_ACTIVE
 #undef SCORE_ISSUE

@@ -13,6 +13,7 @@ constexpr int64_t kMaxBucket = 8192;  // the decision pass keeps a bucket's per-
 constexpr int64_t kMaxRows = (int64_t)1 << 30;
 
 struct Levels {
+  int64_t n = 0;
   int64_t n_kept = 0;
   int32_t L = 0;
   int32_t mc = 0;
@@ -34,6 +35,7 @@ bool make_levels(int64_t n, int64_t n_out, int32_t g, Levels* lv) {
   int32_t L = 0;
   while ((n_out << (L + 1)) <= n) ++L;
   lv->L = L;
+  lv->n = n;
   lv->n_kept = n_out << L;
   lv->sub = lv->n_kept < n;
   lv->mc = L - (g < L ? g : L);
@@ -79,6 +81,7 @@ struct Workspace {
   int32_t* buf_b;  // [S, n_kept / 2]
   float* lbt;      // [S, n_kept / 2]
   float* h2;       // [S, n_kept / 2]
+  float* rowh2;    // [S, n]
   float* E;        // score region
   size_t e_bytes;
   size_t bytes;
@@ -99,6 +102,8 @@ Workspace carve(void* base, int64_t S, int64_t d, const Levels& lv) {
   off += align256(pairs * 4);
   w.h2 = reinterpret_cast<float*>(p + off);
   off += align256(pairs * 4);
+  w.rowh2 = reinterpret_cast<float*>(p + off);
+  off += align256((size_t)S * (size_t)lv.n * 4);
   w.E = reinterpret_cast<float*>(p + off);
   w.e_bytes = score_region(S, d, lv);
   off += align256(w.e_bytes);
@@ -190,6 +195,9 @@ int compress_impl(const void* K, const void* V, int32_t dtype, int64_t B, int64_
       a.E = ws.E;
       a.lbt = ws.lbt;
       a.h2 = ws.h2;
+      a.rowh2 = ws.rowh2;
+      a.rowh2_write = r == 0;
+      a.chunk0 = 0;
       const int64_t buckets = S * lv.G[r];
       const size_t per = thin::halve_score_bytes(lv.N[r]);
       int64_t chunk = (int64_t)(ws.e_bytes / per);

@@ -276,29 +276,34 @@ __device__ __forceinline__ void quarter_pair_dots(const uint4* fk, const uint4* 
   }
 }
 
-// Scale exponent of the pair: h = the larger of the two diagonal exponents
-// ||k||^2/sqrt(d), in base 2, rounded to float.  That float is used wherever
-// the pair's kappa values are scaled by exp(-h).  sk = this row's <k,k>.
-__device__ __forceinline__ float pair_h2f(double sk, double inv_sqrt_d) {
-  const double ex = sk * inv_sqrt_d, exp_ = from_partner(sk) * inv_sqrt_d;
-  const double h = ex > exp_ ? ex : exp_;
-  return (float)(h * kLog2e);
+// Scale exponent of a row: its diagonal exponent ||k||^2/sqrt(d) in base 2,
+// rounded to float (sk = <k,k>).  The scale of a pair is the larger of its
+// two rows' values; that float is used wherever the pair's kappa values are
+// scaled by exp(-h).  Rounding is monotonic, so the larger rounded value is
+// the rounded larger exponent, whichever side forms it.
+__device__ __forceinline__ float row_h2f(double sk, double inv_sqrt_d) {
+  return (float)((sk * inv_sqrt_d) * kLog2e);
+}
+__device__ __forceinline__ float pair_h2f(float row_h2) {
+  return fmaxf(row_h2, from_partner(row_h2));
 }
 
-// Row-pair terms of the 16-row tile: h2f (above) and lbt = log of the RKHS
-// distance b (Algorithm A.1) scaled by exp(-h/2).  The exponentials and the
-// log are float32 (about 1e-7 relative) on float64 arguments; the sums are
-// float64.
+// Row-pair terms of the 16-row tile: the row's scale exponent rh2 and its
+// pair's h2f (above), and lbt = log of the RKHS distance b (Algorithm A.1)
+// scaled by exp(-h/2).  The exponentials and the log are float32 (about 1e-7
+// relative) on float64 arguments; the sums are float64.
 template <typename T, int D>
 __device__ __forceinline__ void frag_pair_terms(const uint4* fk, const uint4* fv, double vm2d,
-                                                double inv_sqrt_d, float& h2f, float& lbt) {
+                                                double inv_sqrt_d, float& rh2, float& h2f,
+                                                float& lbt) {
   double sv, ck, cv;
   const double sk = sum_quarters(quarter_self_dot<T, D>(fk));
   quarter_pair_dots<T, D>(fk, fv, sv, ck, cv);
   sv = sum_quarters(sv);
   ck = sum_quarters(ck);
   cv = sum_quarters(cv);
-  h2f = pair_h2f(sk, inv_sqrt_d);
+  rh2 = row_h2f(sk, inv_sqrt_d);
+  h2f = pair_h2f(rh2);
   const double svp = from_partner(sv);
   const double ex = sk * inv_sqrt_d, exp_ = from_partner(sk) * inv_sqrt_d, exx = ck * inv_sqrt_d;
   const double h2 = (double)h2f;
@@ -375,9 +380,9 @@ struct ScoreShape {
   static constexpr int GT = 4 * BLOCKS;        // 16-row tiles per group
   static constexpr int CHUNKS = 2 * NV;        // 1 KB fragment chunks per tile (K, then V)
   static constexpr int LPT = (CHUNKS + kScoreWaves - 1) / kScoreWaves;
-  // stages, scale exponents, row indices of the streamed column rows
-  static constexpr int LDS = kScoreStages * CHUNKS * 1024 + kScoreStages * 16 * 4 +
-                             kScoreRowsStaged * 8;
+  // stages, pair scale exponents of the group's rows, row indices of the
+  // streamed column rows
+  static constexpr int LDS = kScoreStages * CHUNKS * 1024 + GT * 16 * 4 + kScoreRowsStaged * 8;
 };
 
 // Block (group-local) and half of half-block slot h of wave w.
@@ -419,7 +424,7 @@ void pair_scores_kernel(HalveArgs a) {
   const int P = N >> 1;
   const int NT = (N + 15) >> 4;
   const int nb = (N + 63) >> 6;
-  const int grp = blockIdx.y, chunk = blockIdx.z;
+  const int grp = blockIdx.y, chunk = blockIdx.z + a.chunk0;
   const int gt0 = grp * GT;  // the group's first tile
   if (gt0 >= NT) return;
   const bool own = chunk == 0;
@@ -439,8 +444,8 @@ void pair_scores_kernel(HalveArgs a) {
   const float c2 = (float)(kLog2e * inv_sqrt_d);
 
   extern __shared__ __align__(16) unsigned char smem[];
-  float* s_h2 = reinterpret_cast<float*>(smem + NS * CH * 1024);
-  int64_t* s_rows = reinterpret_cast<int64_t*>(s_h2 + NS * 16);
+  float* s_h2 = reinterpret_cast<float*>(smem + NS * CH * 1024);  // [GT * 16], own rows
+  int64_t* s_rows = reinterpret_cast<int64_t*>(s_h2 + GT * 16);
 
   // ---- this wave's half-blocks: fragments and, in chunk 0, pair terms ----
   int hb_blk[HB], hb_half[HB];
@@ -475,13 +480,16 @@ void pair_scores_kernel(HalveArgs a) {
       if (!hb_ok[h]) continue;
 #pragma unroll
       for (int rt = 0; rt < 2; ++rt) {
-        float h2f, lbt;
-        frag_pair_terms<T, D>(Ak[h][rt], Av[h][rt], vm2d, inv_sqrt_d, h2f, lbt);
+        float rh2, h2f, lbt;
+        frag_pair_terms<T, D>(Ak[h][rt], Av[h][rt], vm2d, inv_sqrt_d, rh2, h2f, lbt);
         const int j = hb_blk[h] * 64 + hb_half[h] * 32 + rt * 16 + m16;
+        if (g == 0) s_h2[((hb_blk[h] - grp * NBW) * 4 + hb_half[h] * 2 + rt) * 16 + m16] = h2f;
         if (g == 0 && j < N && (j & 1) == 0) {
           a.h2[pb + (j >> 1)] = h2f;
           a.lbt[pb + (j >> 1)] = lbt;
         }
+        if (a.rowh2_write && g == 0 && j < N)
+          a.rowh2[s * a.n + (rows_in ? (int64_t)rows_in[j] : row_base + j)] = rh2;
       }
     }
   } else {
@@ -496,11 +504,15 @@ void pair_scores_kernel(HalveArgs a) {
   // Streamed chunk c of tile jt: lane l holds row jt*16 + l%16 (clamped to
   // the bucket; rows past the end are never read back), word 4(c%NV) + l/16,
   // of K (c < NV) or V.  Own tiles are the owners' fragments, same layout.
+  // Streamed rows also bring their scale exponents from the per-row table
+  // (hst, then hcm once staged; written by the first round's own chunks).
   u32x4 stg[DEPTH][LPT];
+  float hst[DEPTH], hcm[NS];
 #define SCORE_ISSUE(JT, SLOT)                                                        \
   do {                                                                               \
     const int j_ = min((JT) * 16 + m16, N - 1);                                      \
     const int64_t row_ = s_rows[j_ - jt0 * 16];                                      \
+    hst[SLOT] = a.rowh2[s * a.n + row_];                                             \
     _Pragma("unroll") for (int k_ = 0; k_ < LPT; ++k_) {                             \
       const int c_ = min(wave + k_ * kScoreWaves, CH - 1);                           \
       const T* src_ = c_ < NV ? K : V;                                               \
@@ -509,6 +521,7 @@ void pair_scores_kernel(HalveArgs a) {
   } while (0)
 #define SCORE_COMMIT(STAGE, SLOT)                                                    \
   do {                                                                               \
+    hcm[STAGE] = hst[SLOT];                                                          \
     _Pragma("unroll") for (int k_ = 0; k_ < LPT; ++k_) {                             \
       const int c_ = wave + k_ * kScoreWaves;                                        \
       if (c_ < CH) reinterpret_cast<u32x4*>(smem + ((STAGE) * CH + c_) * 1024)[lane] = stg[SLOT][k_]; \
@@ -535,13 +548,6 @@ void pair_scores_kernel(HalveArgs a) {
       }                                                                              \
     }                                                                                \
   } while (0)
-  auto tile_h2 = [&](int stage) {  // scale exponents of a staged tile's 16 rows
-    uint4 bk[NV];
-#pragma unroll
-    for (int v = 0; v < NV; ++v) bk[v] = reinterpret_cast<const uint4*>(smem + (stage * CH + v) * 1024)[lane];
-    const float h = pair_h2f(sum_quarters(quarter_self_dot<T, D>(bk)), inv_sqrt_d);
-    if (g == 0) s_h2[stage * 16 + m16] = h;
-  };
 
   // Gram accumulators; a half-block slot h takes part in tile jt from its
   // block's diagonal on (always, in a streamed chunk).  (Two waves per SIMD
@@ -570,9 +576,9 @@ void pair_scores_kernel(HalveArgs a) {
     }                                                                                  \
   } while (0)
 
-  // One column tile (tile I of the chunk, ring position U): scale of tile
-  // I+1, staging of tile I+2 (and, streamed, the load of tile I+2+DEPTH),
-  // Grams and scores of tile I.  Lane (g, m16) holds kappa(A row 4g+e,
+  // One column tile (tile I of the chunk, ring position U): staging of tile
+  // I+2 (and, streamed, the load of tile I+2+DEPTH), Grams and scores of
+  // tile I.  Lane (g, m16) holds kappa(A row 4g+e,
   // column row m16) for e = 0..3, i.e. A pairs 2g and 2g+1 of the row tile
   // against column row m16.  With F = kappa(y'_i, .) - kappa(y_i, .), the
   // even lane of a column pair stores E(2g, p) = F0 - F0(partner) and the
@@ -583,7 +589,6 @@ void pair_scores_kernel(HalveArgs a) {
   do {                                                                                 \
     const int i_ = (I);                                                                \
     const int jt_ = jt0 + i_;                                                          \
-    if (wave == i_ % kScoreWaves) tile_h2(((U) + 1) % NS);                             \
     if (OWN) {                                                                         \
       if (i_ + 2 < ntile) SCORE_OWN_COMMIT(((U) + 2) % NS, i_ + 2);                    \
     } else {                                                                           \
@@ -591,7 +596,8 @@ void pair_scores_kernel(HalveArgs a) {
       SCORE_ISSUE(jt_ + 2 + DEPTH, ((U) + 2) % DEPTH);                                 \
     }                                                                                  \
     SCORE_MMA(OWN, (U) % NS, jt_, 0);                                                  \
-    const float h2_ = jt_ * 16 + m16 < N ? s_h2[((U) % NS) * 16 + m16] : 0.0f;         \
+    const float h2_ = jt_ * 16 + m16 >= N ? 0.0f                                       \
+                      : (OWN) ? s_h2[i_ * 16 + m16] : pair_h2f(hcm[(U) % NS]);        \
     _Pragma("unroll") for (int h = 0; h < HB; ++h) {                                   \
       if (!SCORE_ACTIVE(OWN, h, jt_)) continue;                                        \
       const int b = hb_blk[h];                                                         \
@@ -620,8 +626,6 @@ void pair_scores_kernel(HalveArgs a) {
     SCORE_OWN_COMMIT(0, 0);
     if (ntile > 1) SCORE_OWN_COMMIT(1, 1);
     __syncthreads();
-    if (wave == 0) tile_h2(0);
-    __syncthreads();
     for (int ib = 0; ib < ntile; ib += DEPTH) {
 #pragma unroll
       for (int u = 0; u < DEPTH; ++u)
@@ -634,8 +638,6 @@ void pair_scores_kernel(HalveArgs a) {
     SCORE_COMMIT(1, 1);
     SCORE_ISSUE(jt0 + DEPTH, 0);
     SCORE_ISSUE(jt0 + DEPTH + 1, 1);
-    __syncthreads();
-    if (wave == 0) tile_h2(0);
     __syncthreads();
     // The first ring turn is peeled: the loop is then entered with the same
     // loads and stores in flight as at its back edge, so the compiler's wait
@@ -978,8 +980,23 @@ hipError_t launch_scores_td(const HalveArgs& a, int64_t nbk, hipStream_t st) {
   const int64_t groups = (NT + SS::GT - 1) / SS::GT;
   const int64_t rest = NT > SS::GT ? NT - SS::GT : 0;  // tiles after the first group
   const int64_t nch = 1 + (rest + a.ch - 1) / a.ch;
+  if (a.rowh2_write && nch > 1) {
+    // the streamed chunks read the row scales the own chunks write: two launches
+    HalveArgs own = a;
+    own.chunk0 = 0;
+    hipLaunchKernelGGL(kern, dim3((unsigned)nbk, (unsigned)groups, 1u), dim3(64 * kScoreWaves), lds, st,
+                       own);
+    HalveArgs rest_a = a;
+    rest_a.chunk0 = 1;
+    rest_a.rowh2_write = 0;
+    hipLaunchKernelGGL(kern, dim3((unsigned)nbk, (unsigned)groups, (unsigned)(nch - 1)),
+                       dim3(64 * kScoreWaves), lds, st, rest_a);
+    return hipGetLastError();
+  }
+  HalveArgs one = a;
+  one.chunk0 = 0;
   dim3 grid((unsigned)nbk, (unsigned)groups, (unsigned)nch);
-  hipLaunchKernelGGL(kern, grid, dim3(64 * kScoreWaves), lds, st, a);
+  hipLaunchKernelGGL(kern, grid, dim3(64 * kScoreWaves), lds, st, one);
   return hipGetLastError();
 }
 

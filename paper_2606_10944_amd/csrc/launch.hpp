@@ -27,8 +27,11 @@ struct HalveArgs {
   float* lbt;                 // [S, n_r / 2] scaled log b per pair
   float* h2;                  // [S, n_r / 2] scale exponent per pair
   int64_t b0;                 // first bucket of this launch
-  int64_t e_tiles;            // score tiles per bucket (set by launch_halve)
-  int32_t ch;                 // column tiles per score workgroup (set by launch_halve)
+  int64_t e_tiles;            // score tiles per bucket (set by launch_scores)
+  int32_t ch;                 // column tiles per score workgroup (set by launch_scores)
+  float* rowh2;               // [S, n] scale exponent of every row, written by the first round
+  int32_t rowh2_write;        // this round writes rowh2 (and reads it only after writing)
+  int32_t chunk0;             // first column chunk of a score launch (set by launch_scores)
 };
 
 // dtype: 0 = fp32, 1 = bf16.  Returns a hipError_t.

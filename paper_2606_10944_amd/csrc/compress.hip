@@ -371,6 +371,11 @@ constexpr int kScoreChunk = 32;
 // Streamed rows whose indices a workgroup stages: its chunk, rounded up to
 // whole ring turns, plus the ring's look-ahead.
 constexpr int kScoreRowsStaged = (kScoreChunk + 2 * SCORE_DEPTH + 1) * 16;
+// A score tile (8 column pairs x 32 row pairs) in LDS: column stride 36
+// floats, so the scattered single-float writes of a half-wave hit 32
+// different banks.
+constexpr int kETileStride = 36;
+constexpr int kETileLds = 8 * kETileStride;
 
 template <typename T, int D>
 struct ScoreShape {
@@ -380,9 +385,10 @@ struct ScoreShape {
   static constexpr int GT = 4 * BLOCKS;        // 16-row tiles per group
   static constexpr int CHUNKS = 2 * NV;        // 1 KB fragment chunks per tile (K, then V)
   static constexpr int LPT = (CHUNKS + kScoreWaves - 1) / kScoreWaves;
-  // stages, pair scale exponents of the group's rows, row indices of the
-  // streamed column rows
-  static constexpr int LDS = kScoreStages * CHUNKS * 1024 + GT * 16 * 4 + kScoreRowsStaged * 8;
+  // stages, score tile buffers, pair scale exponents of the group's rows,
+  // row scale exponents of the stages, row indices of the streamed rows
+  static constexpr int LDS = kScoreStages * CHUNKS * 1024 + kScoreStages * BLOCKS * kETileLds * 4 +
+                             GT * 16 * 4 + kScoreStages * 16 * 4 + kScoreRowsStaged * 8;
 };
 
 // Block (group-local) and half of half-block slot h of wave w.
@@ -398,7 +404,7 @@ __device__ __forceinline__ void half_block(int w, int h, int& b, int& half) {
 }
 
 // Target of the stores of a streamed chunk's padding tiles (never read).
-__device__ float g_score_sink[256];
+__device__ __align__(16) float g_score_sink[256];
 
 template <typename T, int D>
 __global__ __launch_bounds__(64 * kScoreWaves) __attribute__((amdgpu_waves_per_eu(2)))
@@ -444,8 +450,10 @@ void pair_scores_kernel(HalveArgs a) {
   const float c2 = (float)(kLog2e * inv_sqrt_d);
 
   extern __shared__ __align__(16) unsigned char smem[];
-  float* s_h2 = reinterpret_cast<float*>(smem + NS * CH * 1024);  // [GT * 16], own rows
-  int64_t* s_rows = reinterpret_cast<int64_t*>(s_h2 + GT * 16);
+  float* s_e = reinterpret_cast<float*>(smem + NS * CH * 1024);    // [NS][NBW] tile buffers
+  float* s_h2 = s_e + NS * NBW * kETileLds;                          // [GT * 16], own rows
+  float* s_hst = s_h2 + GT * 16;                                     // [NS * 16], staged rows
+  int64_t* s_rows = reinterpret_cast<int64_t*>(s_hst + NS * 16);
 
   // ---- this wave's half-blocks: fragments and, in chunk 0, pair terms ----
   int hb_blk[HB], hb_half[HB];
@@ -505,9 +513,9 @@ void pair_scores_kernel(HalveArgs a) {
   // the bucket; rows past the end are never read back), word 4(c%NV) + l/16,
   // of K (c < NV) or V.  Own tiles are the owners' fragments, same layout.
   // Streamed rows also bring their scale exponents from the per-row table
-  // (hst, then hcm once staged; written by the first round's own chunks).
+  // (written by the first round's own chunks), staged in LDS with the rows.
   u32x4 stg[DEPTH][LPT];
-  float hst[DEPTH], hcm[NS];
+  float hst[DEPTH];
 #define SCORE_ISSUE(JT, SLOT)                                                        \
   do {                                                                               \
     const int j_ = min((JT) * 16 + m16, N - 1);                                      \
@@ -521,7 +529,7 @@ void pair_scores_kernel(HalveArgs a) {
   } while (0)
 #define SCORE_COMMIT(STAGE, SLOT)                                                    \
   do {                                                                               \
-    hcm[STAGE] = hst[SLOT];                                                          \
+    if (wave == 0 && g == 0) s_hst[(STAGE) * 16 + m16] = hst[SLOT];                  \
     _Pragma("unroll") for (int k_ = 0; k_ < LPT; ++k_) {                             \
       const int c_ = wave + k_ * kScoreWaves;                                        \
       if (c_ < CH) reinterpret_cast<u32x4*>(smem + ((STAGE) * CH + c_) * 1024)[lane] = stg[SLOT][k_]; \
@@ -554,69 +562,122 @@ void pair_scores_kernel(HalveArgs a) {
   // overlap one wave's MFMAs with the other's exp epilogue; double-buffered
   // accumulators would not fit.)
   floatx4_t gk[1][HB][2], gv[1][HB][2];
+  uint4 bk_[NV], bv_[NV];
 #define SCORE_ACTIVE(OWN, H, JT) (!(OWN) || (hb_ok[H] && (JT) >= hb_blk[H] * 4))
-#define SCORE_MMA(OWN, STAGE, JT, SLOT)                                                 \
+#define SCORE_BFRAG(STAGE)                                                              \
   do {                                                                                 \
-    uint4 bk_[NV], bv_[NV];                                                            \
     _Pragma("unroll") for (int v_ = 0; v_ < NV; ++v_) {                                \
       bk_[v_] = reinterpret_cast<const uint4*>(smem + ((STAGE) * CH + v_) * 1024)[lane]; \
       bv_[v_] = reinterpret_cast<const uint4*>(smem + ((STAGE) * CH + NV + v_) * 1024)[lane]; \
     }                                                                                  \
-    _Pragma("unroll") for (int h_ = 0; h_ < HB; ++h_) {                                \
-      if (!SCORE_ACTIVE(OWN, h_, JT)) continue;                                        \
+  } while (0)
+#define SCORE_MMA_H(H)                                                                  \
+  do {                                                                                 \
+    _Pragma("unroll") for (int rt_ = 0; rt_ < 2; ++rt_) {                              \
+      gk[0][H][rt_] = (floatx4_t){0.f, 0.f, 0.f, 0.f};                                 \
+      gv[0][H][rt_] = (floatx4_t){vm2f, vm2f, vm2f, vm2f}; /* <v,v'> + v_max^2 */      \
+    }                                                                                  \
+    _Pragma("unroll") for (int v_ = 0; v_ < NV; ++v_)                                  \
       _Pragma("unroll") for (int rt_ = 0; rt_ < 2; ++rt_) {                            \
-        gk[SLOT][h_][rt_] = (floatx4_t){0.f, 0.f, 0.f, 0.f};                           \
-        gv[SLOT][h_][rt_] = (floatx4_t){vm2f, vm2f, vm2f, vm2f}; /* <v,v'> + v_max^2 */ \
+        gk[0][H][rt_] = mma_word<T>(Ak[H][rt_][v_], bk_[v_], gk[0][H][rt_]);           \
+        gv[0][H][rt_] = mma_word<T>(Av[H][rt_][v_], bv_[v_], gv[0][H][rt_]);           \
       }                                                                                \
-      _Pragma("unroll") for (int v_ = 0; v_ < NV; ++v_)                                \
-        _Pragma("unroll") for (int rt_ = 0; rt_ < 2; ++rt_) {                          \
-          gk[SLOT][h_][rt_] = mma_word<T>(Ak[h_][rt_][v_], bk_[v_], gk[SLOT][h_][rt_]); \
-          gv[SLOT][h_][rt_] = mma_word<T>(Av[h_][rt_][v_], bv_[v_], gv[SLOT][h_][rt_]); \
-        }                                                                              \
+  } while (0)
+  // Scores of slot H into the tile buffer BUF.  Lane (g, m16) holds
+  // kappa(A row 4g+e, column row m16) for e = 0..3, i.e. A pairs 2g and 2g+1
+  // of the row tile against column row m16.  With F = kappa(y'_i, .) -
+  // kappa(y_i, .), the even lane of a column pair forms E(2g, p) =
+  // F0 - F0(partner) and the odd lane E(2g+1, p) = F1(partner) - F1.
+#define SCORE_EPI_H(H, H2, BUF)                                                         \
+  do {                                                                                 \
+    float* eb_ = s_e + ((BUF) * NBW + hb_blk[H] - grp * NBW) * kETileLds;              \
+    _Pragma("unroll") for (int rt = 0; rt < 2; ++rt) {                                 \
+      float kap[4];                                                                    \
+      _Pragma("unroll") for (int e = 0; e < 4; ++e)                                    \
+        kap[e] = __builtin_amdgcn_exp2f(fminf(gk[0][H][rt][e] * c2 - (H2), kExpClamp)) * \
+                 gv[0][H][rt][e];                                                      \
+      const float F0 = kap[1] - kap[0];                                                \
+      const float F1 = kap[3] - kap[2];                                                \
+      const float mine_ = odd ? F1 : F0;                                               \
+      const float other_ = from_partner(odd ? F0 : F1);                                \
+      eb_[(m16 >> 1) * kETileStride + hb_half[H] * 16 + rt * 8 + 2 * g + (m16 & 1)] =  \
+          odd ? other_ - mine_ : mine_ - other_;                                       \
+    }                                                                                  \
+  } while (0)
+  // Wave w < NBW writes block w's completed tile IF (buffer BUF) to the score
+  // array: 16 bytes per lane, 128 contiguous bytes per column pair.  A
+  // streamed chunk's padding tiles go to the sink.
+#define SCORE_FLUSH(OWN, IF, BUF)                                                       \
+  do {                                                                                 \
+    if (NBW == kScoreWaves || wave < NBW) {                                            \
+      const int bw_ = grp * NBW + wave;                                                \
+      const int jtf_ = jt0 + (IF);                                                     \
+      if (!(OWN) || (bw_ < nb && jtf_ >= 4 * bw_)) {                                   \
+        float* dst_ = (OWN) || (IF) < ntile                                            \
+            ? a.E + (bl * a.e_tiles + panel_tiles(bw_, NT, 4) + jtf_ - 4 * bw_) * (int64_t)TILE \
+            : g_score_sink;                                                            \
+        const float4 v_ = *reinterpret_cast<const float4*>(                            \
+            s_e + ((BUF) * NBW + wave) * kETileLds + (lane >> 3) * kETileStride + (lane & 7) * 4); \
+        *reinterpret_cast<float4*>(dst_ + (lane >> 3) * BP + (lane & 7) * 4) = v_;     \
+      }                                                                                \
+    }                                                                                  \
+  } while (0)
+  // 16 MFMAs, each followed by up to 3 vector (or transcendental) instructions
+#define SCORE_INTERLEAVE()                                                              \
+  do {                                                                                 \
+    _Pragma("unroll") for (int k_ = 0; k_ < 2 * NV * 2; ++k_) {                        \
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                               \
+      __builtin_amdgcn_sched_group_barrier(0x402, 3, 0);                               \
     }                                                                                  \
   } while (0)
 
-  // One column tile (tile I of the chunk, ring position U): staging of tile
-  // I+2 (and, streamed, the load of tile I+2+DEPTH), Grams and scores of
-  // tile I.  Lane (g, m16) holds kappa(A row 4g+e,
-  // column row m16) for e = 0..3, i.e. A pairs 2g and 2g+1 of the row tile
-  // against column row m16.  With F = kappa(y'_i, .) - kappa(y_i, .), the
-  // even lane of a column pair stores E(2g, p) = F0 - F0(partner) and the
-  // odd lane E(2g+1, p) = F1(partner) - F1, so every lane stores one score.
-  // A streamed chunk runs whole ring turns: its padding tiles (I >= ntile)
-  // store to a sink.
+  // One column tile (tile I of the chunk, ring position U = I mod 3): the
+  // previous tile is written out, tile I+2 staged (and, streamed, tile
+  // I+2+DEPTH loaded), then Grams and scores of tile I.
 #define SCORE_TILE(OWN, I, U)                                                           \
   do {                                                                                 \
     const int i_ = (I);                                                                \
     const int jt_ = jt0 + i_;                                                          \
+    if (i_ > 0) SCORE_FLUSH(OWN, i_ - 1, ((U) + NS - 1) % NS);                         \
     if (OWN) {                                                                         \
       if (i_ + 2 < ntile) SCORE_OWN_COMMIT(((U) + 2) % NS, i_ + 2);                    \
     } else {                                                                           \
       SCORE_COMMIT(((U) + 2) % NS, ((U) + 2) % DEPTH);                                 \
       SCORE_ISSUE(jt_ + 2 + DEPTH, ((U) + 2) % DEPTH);                                 \
     }                                                                                  \
-    SCORE_MMA(OWN, (U) % NS, jt_, 0);                                                  \
+    SCORE_BFRAG((U) % NS);                                                             \
     const float h2_ = jt_ * 16 + m16 >= N ? 0.0f                                       \
-                      : (OWN) ? s_h2[i_ * 16 + m16] : pair_h2f(hcm[(U) % NS]);        \
+                      : (OWN) ? s_h2[i_ * 16 + m16] : pair_h2f(s_hst[((U) % NS) * 16 + m16]);        \
     _Pragma("unroll") for (int h = 0; h < HB; ++h) {                                   \
       if (!SCORE_ACTIVE(OWN, h, jt_)) continue;                                        \
-      const int b = hb_blk[h];                                                         \
-      float* tile_ = (OWN) || i_ < ntile                                               \
-          ? a.E + (bl * a.e_tiles + panel_tiles(b, NT, 4) + jt_ - 4 * b) * (int64_t)TILE \
-          : g_score_sink;                                                              \
-      _Pragma("unroll") for (int rt = 0; rt < 2; ++rt) {                               \
-        float kap[4];                                                                  \
-        _Pragma("unroll") for (int e = 0; e < 4; ++e)                                  \
-          kap[e] = __builtin_amdgcn_exp2f(fminf(gk[0][h][rt][e] * c2 - h2_, kExpClamp)) * \
-                   gv[0][h][rt][e];                                                    \
-        const float F0 = kap[1] - kap[0];                                              \
-        const float F1 = kap[3] - kap[2];                                              \
-        const float mine_ = odd ? F1 : F0;                                             \
-        const float other_ = from_partner(odd ? F0 : F1);                              \
-        tile_[(m16 >> 1) * BP + hb_half[h] * 16 + rt * 8 + 2 * g + (m16 & 1)] =        \
-            odd ? other_ - mine_ : mine_ - other_;                                     \
-      }                                                                                \
+      SCORE_MMA_H(h);                                                                  \
+      SCORE_EPI_H(h, h2_, (U) % NS);                                                   \
     }                                                                                  \
+    __syncthreads();                                                                   \
+  } while (0)
+  // Streamed tiles with two half-block slots are software-pipelined across
+  // the slots: the MFMAs of one slot are interleaved with the exp epilogue of
+  // the other (slot 1 of the previous tile, then slot 0 of this tile), so
+  // the matrix core and the vector ALU of a SIMD work at the same time.  A
+  // tile's scores are then complete one tile later, and written one more
+  // tile later.
+  float h2_prev = 0.0f;
+#define SCORE_TILE_P(I, U, FIRST)                                                       \
+  do {                                                                                 \
+    const int i_ = (I);                                                                \
+    const int jt_ = jt0 + i_;                                                          \
+    if (i_ >= 2) SCORE_FLUSH(false, i_ - 2, ((U) + 1) % NS);                           \
+    SCORE_COMMIT(((U) + 2) % NS, ((U) + 2) % DEPTH);                                   \
+    SCORE_ISSUE(jt_ + 2 + DEPTH, ((U) + 2) % DEPTH);                                   \
+    SCORE_BFRAG((U) % NS);                                                             \
+    const float h2c_ = jt_ * 16 + m16 >= N ? 0.0f : pair_h2f(s_hst[((U) % NS) * 16 + m16]);           \
+    SCORE_MMA_H(0);                                                                    \
+    if (!(FIRST)) SCORE_EPI_H(1, h2_prev, ((U) + NS - 1) % NS);                        \
+    SCORE_INTERLEAVE();                                                                \
+    SCORE_MMA_H(1);                                                                    \
+    SCORE_EPI_H(0, h2c_, (U) % NS);                                                    \
+    SCORE_INTERLEAVE();                                                                \
+    h2_prev = h2c_;                                                                    \
     __syncthreads();                                                                   \
   } while (0)
 
@@ -631,6 +692,7 @@ void pair_scores_kernel(HalveArgs a) {
       for (int u = 0; u < DEPTH; ++u)
         if (ib + u < ntile) SCORE_TILE(true, ib + u, u);  // uniform over the workgroup
     }
+    SCORE_FLUSH(true, ntile - 1, (ntile - 1) % NS);
   } else {
 #pragma unroll
     for (int k = 0; k < DEPTH; ++k) SCORE_ISSUE(jt0 + k, k);
@@ -642,16 +704,39 @@ void pair_scores_kernel(HalveArgs a) {
     // The first ring turn is peeled: the loop is then entered with the same
     // loads and stores in flight as at its back edge, so the compiler's wait
     // for a staged tile is for that tile's loads only, not for the stores
-    // issued after them (stores count in vmcnt on this architecture).
+    // issued after them (stores count in vmcnt on this architecture).  The
+    // chunk runs whole ring turns (tiles past ntile are padding).
+    const int nturn = (ntile + DEPTH - 1) / DEPTH;
+    if constexpr (HB == 2) {
+      SCORE_TILE_P(0, 0, true);
 #pragma unroll
-    for (int u = 0; u < DEPTH; ++u) SCORE_TILE(false, u, u);
-    for (int ib = DEPTH; ib < ntile; ib += DEPTH) {
+      for (int u = 1; u < DEPTH; ++u) SCORE_TILE_P(u, u, false);
+      for (int ib = DEPTH; ib < nturn * DEPTH; ib += DEPTH) {
 #pragma unroll
-      for (int u = 0; u < DEPTH; ++u) SCORE_TILE(false, ib + u, u);
+        for (int u = 0; u < DEPTH; ++u) SCORE_TILE_P(ib + u, u, false);
+      }
+      const int last = nturn * DEPTH - 1;
+      SCORE_EPI_H(1, h2_prev, last % NS);
+      __syncthreads();
+      SCORE_FLUSH(false, last - 1, (last - 1) % NS);
+      SCORE_FLUSH(false, last, last % NS);
+    } else {
+#pragma unroll
+      for (int u = 0; u < DEPTH; ++u) SCORE_TILE(false, u, u);
+      for (int ib = DEPTH; ib < nturn * DEPTH; ib += DEPTH) {
+#pragma unroll
+        for (int u = 0; u < DEPTH; ++u) SCORE_TILE(false, ib + u, u);
+      }
+      SCORE_FLUSH(false, nturn * DEPTH - 1, (nturn * DEPTH - 1) % NS);
     }
   }
 #undef SCORE_TILE
-#undef SCORE_MMA
+#undef SCORE_TILE_P
+#undef SCORE_INTERLEAVE
+#undef SCORE_FLUSH
+#undef SCORE_EPI_H
+#undef SCORE_MMA_H
+#undef SCORE_BFRAG
 #undef SCORE_ACTIVE
 #undef SCORE_ISSUE
 #undef SCORE_COMMIT

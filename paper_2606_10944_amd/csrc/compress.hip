@@ -867,40 +867,48 @@ __global__ __launch_bounds__(64 * (BW + 2)) void halve_pass_kernel(HalveArgs a) 
       const double alpha_in = s_alpha[min(gp, P - 1)] + anear;
       const double thr = sl_thr(sb)[pl];
       const int32_t r0 = sl_rows(sb)[pl], r1 = sl_rows(sb)[BP + pl];
-      double alpha = active ? alpha_in : 0.0;
-      // this pair's scores against the block's earlier pairs, masked and
-      // widened before the loop (held in registers: the loop is the
-      // decider's critical path and must not wait on LDS)
-      double ed[BP];
+      double alpha = alpha_in;
+      // this pair's scores against the block's pairs, held in registers
+      // before the loop (the loop is the decider's critical path and must
+      // not wait on LDS); widened to float64 inside the loop, off the chain.
+      // No masking: lane p's alpha is read only at its own decision (step
+      // p), before any score of a pair i >= p has been added to it, and the
+      // decisions of lanes past the block's last pair are dropped below.
+      float ef[BP];
       const u32x4* oc = sl_own(sb) + pl * QW;
+      u32x4 xs[QW];
 #pragma unroll
-      for (int q = 0; q < QW; ++q) {
-        const u32x4 x = oc[q];
+      for (int q = 0; q < QW; ++q) xs[q] = oc[q];
+#pragma unroll
+      for (int q = 0; q < QW; ++q)
 #pragma unroll
         for (int c = 0; c < 4; ++c) {
-          const int i = 4 * q + c;
-          ed[i] = (active && p > i) ? (double)__uint_as_float(x[c]) : 0.0;
-          asm volatile("" : "+v"(ed[i]));
+          ef[4 * q + c] = __uint_as_float(xs[q][c]);
+          asm volatile("" : "+v"(ef[4 * q + c]));
         }
-      }
+      __builtin_amdgcn_sched_barrier(0);
       // Decisions i and i+1 per step: alpha < thr for pair i, and for pair
-      // i+1 under both signs of pair i's score; alpha then takes the two
-      // signed scores (pair i swapped: -E(i,.), else +E(i,.)).
+      // i+1 under both signs of pair i's score (pair i swapped: -E(i,.),
+      // else +E(i,.)).  The four sums alpha +- E(i,.) +- E(i+1,.) are formed
+      // while the decisions are taken; the decisions only select one.
       uint32_t smask = 0;
 #pragma unroll
       for (int i = 0; i < BP; i += 2) {
-        if (i < npb) {
-          const double ap = alpha + ed[i], am = alpha - ed[i];
-          const uint64_t b0 = __ballot(alpha < thr);
-          const uint64_t bp = __ballot(ap < thr);
-          const uint64_t bm = __ballot(am < thr);
-          const uint32_t s0 = (uint32_t)(b0 >> i) & 1u;
-          const uint32_t s1 = i + 1 < npb ? (uint32_t)((s0 ? bm : bp) >> (i + 1)) & 1u : 0u;
-          smask |= (s0 << i) | (s1 << (i + 1));
-          const double a1 = s0 ? am : ap;
-          alpha = a1 + __hiloint2double(__double2hiint(ed[i + 1]) ^ (int)(s1 << 31), __double2loint(ed[i + 1]));
-        }
+        const double e0 = (double)ef[i], e1 = (double)ef[i + 1];
+        const double ap = alpha + e0, am = alpha - e0;
+        double pp = ap + e1, pm = ap - e1, mp = am + e1, mm = am - e1;
+        // kept as four values (not refactored into one add after the selects)
+        asm volatile("" : "+v"(pp), "+v"(pm), "+v"(mp), "+v"(mm));
+        const uint64_t b0 = __ballot(alpha < thr);
+        const uint64_t bp = __ballot(ap < thr);
+        const uint64_t bm = __ballot(am < thr);
+        const uint32_t s0 = (uint32_t)(b0 >> i) & 1u;
+        const double up = s0 ? mp : pp, um = s0 ? mm : pm;
+        const uint32_t s1 = (uint32_t)((s0 ? bm : bp) >> (i + 1)) & 1u;
+        smask |= (s0 << i) | (s1 << (i + 1));
+        alpha = s1 ? um : up;
       }
+      if (npb < BP) smask &= (1u << npb) - 1u;
       const uint32_t bit = (smask >> (p & 31)) & 1u;
       if (active) {
         out[gp] = bit ? r1 : r0;

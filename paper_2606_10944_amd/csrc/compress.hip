@@ -874,19 +874,28 @@ __global__ __launch_bounds__(64 * (BW + 2)) void halve_pass_kernel(HalveArgs a) 
       // No masking: lane p's alpha is read only at its own decision (step
       // p), before any score of a pair i >= p has been added to it, and the
       // decisions of lanes past the block's last pair are dropped below.
-      float ef[BP];
+      // The same for this block's scores against the next block's pair pl:
+      // their signed sum (the next block's contribution from this block) is
+      // accumulated inside the loop, in the order of the bulk sums.
+      float ef[BP], en[BP];
       const u32x4* oc = sl_own(sb) + pl * QW;
-      u32x4 xs[QW];
+      const u32x4* nc = sl_next(sb) + pl * QW;
+      u32x4 xs[QW], xn[QW];
 #pragma unroll
-      for (int q = 0; q < QW; ++q) xs[q] = oc[q];
+      for (int q = 0; q < QW; ++q) {
+        xs[q] = oc[q];
+        xn[q] = nc[q];
+      }
 #pragma unroll
       for (int q = 0; q < QW; ++q)
 #pragma unroll
         for (int c = 0; c < 4; ++c) {
           ef[4 * q + c] = __uint_as_float(xs[q][c]);
-          asm volatile("" : "+v"(ef[4 * q + c]));
+          en[4 * q + c] = __uint_as_float(xn[q][c]);
+          asm volatile("" : "+v"(ef[4 * q + c]), "+v"(en[4 * q + c]));
         }
       __builtin_amdgcn_sched_barrier(0);
+      float near = 0.0f;
       // Decisions i and i+1 per step: alpha < thr for pair i, and for pair
       // i+1 under both signs of pair i's score (pair i swapped: -E(i,.),
       // else +E(i,.)).  The four sums alpha +- E(i,.) +- E(i+1,.) are formed
@@ -907,25 +916,19 @@ __global__ __launch_bounds__(64 * (BW + 2)) void halve_pass_kernel(HalveArgs a) 
         const uint32_t s1 = (uint32_t)((s0 ? bm : bp) >> (i + 1)) & 1u;
         smask |= (s0 << i) | (s1 << (i + 1));
         alpha = s1 ? um : up;
+        near += s0 ? -en[i] : en[i];
+        near += s1 ? -en[i + 1] : en[i + 1];
       }
       if (npb < BP) smask &= (1u << npb) - 1u;
+      if (lane == 0) s_mask[m & 3] = smask;
+      publish(&s_cnt[0], m);
       const uint32_t bit = (smask >> (p & 31)) & 1u;
       if (active) {
         out[gp] = bit ? r1 : r0;
         if (trace) trace[gp] = (uint8_t)bit;
       }
-      if (lane == 0) s_mask[m & 3] = smask;
-      publish(&s_cnt[0], m);
       // the next block's pairs take this block's signed scores
-      if (m + 1 < nblk) {
-        const u32x4* nc = sl_next(sb) + pl * QW;
-        u32x4 col[QW];
-#pragma unroll
-        for (int q = 0; q < QW; ++q) col[q] = nc[q];
-        float sum;
-        PASS_SUM(col, smask, sum);
-        anear = (double)sum;
-      }
+      anear = (double)near;
     }
   } else if (wave == 1) {
     // ---- fetcher: block m's inputs into slot m % 3 ----

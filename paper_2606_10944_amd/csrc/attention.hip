@@ -248,6 +248,9 @@ __device__ __forceinline__ float bf16_hi_to_float(uint32_t w) { return __uint_as
 __device__ __forceinline__ uint32_t pack_lo(uint32_t x, uint32_t y) { return (x & 0xffffu) | (y << 16); }
 __device__ __forceinline__ uint32_t pack_hi(uint32_t x, uint32_t y) { return (x >> 16) | (y & 0xffff0000u); }
 
+// Target of the output stores of query rows past a workgroup's range (never read).
+__device__ __align__(16) float g_attn_sink[256];
+
 template <int D, int NKT, int QTR, int WR, typename TO>
 __global__ __launch_bounds__(64 * WR) void coreset_attn_res_kernel(
     const bf16_t* __restrict__ Q, const bf16_t* __restrict__ K, const bf16_t* __restrict__ V,
@@ -327,6 +330,14 @@ __global__ __launch_bounds__(64 * WR) void coreset_attn_res_kernel(
     const int64_t q = q_begin + wave * 16 * QTR + qt * 16 + m16;
     load_frag<bf16_t, D>(Qs, min(q, n_q - 1), g, true, Bq[qt]);
   }
+  // The first queries are consumed here (the compiler waits for them before
+  // the loop): the loop is then entered with nothing in flight, so its waits
+  // (stores count in vmcnt) are for the next queries' loads only.
+#pragma unroll
+  for (int qt = 0; qt < QTR; ++qt)
+#pragma unroll
+    for (int v = 0; v < NV; ++v)
+      asm volatile("" : "+v"(Bq[qt][v].x), "+v"(Bq[qt][v].y), "+v"(Bq[qt][v].z), "+v"(Bq[qt][v].w));
   for (int64_t q0 = q_begin; q0 < q_end; q0 += QSTEP) {
     const int64_t qw = q0 + wave * 16 * QTR;
     uint4 Nq[QTR][NV];
@@ -420,13 +431,43 @@ __global__ __launch_bounds__(64 * WR) void coreset_attn_res_kernel(
     }
 #pragma unroll
     for (int qt = 0; qt < QTR; ++qt) {
-      const int64_t q = qw + qt * 16 + m16;
-      if (q < q_end) {
-        TO* orow = O + (s * n_q + q) * D;
+      if constexpr (sizeof(TO) == 4) {
+        // Whole 128-byte lines: for columns 32j..32j+31, lanes m16 < 8 hold
+        // the first 16 (O^T tile 2j) and lanes m16 >= 8 the last 16 (tile
+        // 2j+1) of rows m16 & 7 (store A) and (m16 & 7) + 8 (store B); the
+        // missing halves come from lane l ^ 8 (DPP row rotation by 8).
+        const bool upper = m16 >= 8;
+        const int64_t qa = qw + qt * 16 + (m16 & 7), qb = qa + 8;
+        float* ra = reinterpret_cast<float*>(O) + (s * n_q + qa) * D;
+        float* rb = ra + 8 * D;
 #pragma unroll
-        for (int dt = 0; dt < D / 16; ++dt)
-          store4<TO>(orow + dt * 16 + 4 * g, acc[qt][dt][0] * inv_l[qt], acc[qt][dt][1] * inv_l[qt],
-                     acc[qt][dt][2] * inv_l[qt], acc[qt][dt][3] * inv_l[qt]);
+        for (int j = 0; j < D / 32; ++j) {
+          float va[4], vb[4];
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const float a = acc[qt][2 * j][i] * inv_l[qt], b = acc[qt][2 * j + 1][i] * inv_l[qt];
+            const float y = __uint_as_float((uint32_t)__builtin_amdgcn_mov_dpp(
+                (int)__float_as_uint(upper ? a : b), 0x128, 0xF, 0xF, false));
+            va[i] = upper ? y : a;
+            vb[i] = upper ? b : y;
+          }
+          const int col = 32 * j + (upper ? 16 : 0) + 4 * g;
+          // rows past the range store to a sink: the stores stay unconditional,
+          // so the wait for the next queries' loads never covers them
+          float* da = qa < q_end ? ra + col : g_attn_sink + 4 * lane;
+          float* db = qb < q_end ? rb + col : g_attn_sink + 4 * lane;
+          *reinterpret_cast<float4*>(da) = make_float4(va[0], va[1], va[2], va[3]);
+          *reinterpret_cast<float4*>(db) = make_float4(vb[0], vb[1], vb[2], vb[3]);
+        }
+      } else {
+        const int64_t q = qw + qt * 16 + m16;
+        if (q < q_end) {
+          TO* orow = O + (s * n_q + q) * D;
+#pragma unroll
+          for (int dt = 0; dt < D / 16; ++dt)
+            store4<TO>(orow + dt * 16 + 4 * g, acc[qt][dt][0] * inv_l[qt], acc[qt][dt][1] * inv_l[qt],
+                       acc[qt][dt][2] * inv_l[qt], acc[qt][dt][3] * inv_l[qt]);
+        }
       }
 #pragma unroll
       for (int v = 0; v < NV; ++v) Bq[qt][v] = Nq[qt][v];

@@ -200,7 +200,12 @@ def main():
     # The same K steps again with every kernel launch bracketed by events on
     # its stream (each event adds a few microseconds between kernels, so this
     # pass gives the per-kernel times, not the step time).
-    launches = 3 + 2 * plan["rounds"]  # subsample, v_max, scores + decide per round, attention
+    # Launches per step (rounds whose score buffer exceeds the workspace's score
+    # region run in several launches), counted on one extra step.
+    with LaunchTimer(stream, capacity=4096) as probe:
+        step()
+    torch.cuda.synchronize()
+    launches = len(probe.records())
     with LaunchTimer(stream, capacity=launches * args.steps + 16) as lt:
         for _ in range(args.steps):
             step()
@@ -221,8 +226,11 @@ def main():
     ab = attention_bytes(w, 4)
     af = attention_flops(w)
     kev = kappa_evals(plan, w)
+    # per launch: averages over every score launch of the K steps (a round may
+    # take several launches; bytes and time are both summed over the step)
+    n_sc = len(score_ms) // args.steps
     sc_ms_launch = statistics.mean(score_ms)
-    sc_bytes_launch = sum(sb) / L
+    sc_bytes_launch = sum(sb) / n_sc
     sc_gbs = sc_bytes_launch / (sc_ms_launch * 1e-3) / 1e9
     traffic = stored_traffic(w.name)
     attn_gbs = ab / (ta * 1e-3) / 1e9
@@ -250,7 +258,7 @@ def main():
             "frac": sc_gbs / HBM_PEAK_GBS,
             "traffic": traffic,
             "algorithmic_bytes_per_launch": sc_bytes_launch, "ms_per_launch": sc_ms_launch,
-            "launches_per_step": L,
+            "launches_per_step": n_sc,
         },
         "compress": {"ms": tc, "kappa_evals": kev, "kappa_evals_per_s": kev / (tc * 1e-3),
                      "algorithmic_bytes": cb, "hbm_gbs": cb / (tc * 1e-3) / 1e9,

@@ -59,7 +59,7 @@ bool make_levels(int64_t n, int64_t n_out, int32_t g, Levels* lv) {
 // Pair scores of one round live in a region of at most kScoreCap bytes (or
 // one bucket's worth, if larger); rounds whose buckets need more run in
 // several launches.
-constexpr size_t kScoreCap = (size_t)512 << 20;
+constexpr size_t kScoreCap = (size_t)2 << 30;
 
 size_t score_bytes(int64_t N) { return thin::halve_score_bytes(N); }
 

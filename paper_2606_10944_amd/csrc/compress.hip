@@ -1003,43 +1003,52 @@ __global__ __launch_bounds__(64 * (BW + 2)) void halve_pass_kernel(HalveArgs a) 
 #undef PASS_STAGE
   } else {
     // ---- bulk updates, blocks 0 .. nblk-3 ----
-    // Bulk wave w = wave-2, chunk k of block B: pairs (B+2) BP + (w + k BW) 64
-    // + lane (lanes past the last pair load the last pair's column).
+    // Chunk k of block B for bulk wave w = wave-2: pairs (B+2) BP + (w + k BW)
+    // 64 + lane (lanes past the last pair load the last pair's column).  The
+    // wave's chunks of all blocks form one stream, padded to whole turns of
+    // the NCB-slot register ring per block; every consumed slot is refilled
+    // at once with the next chunk of the stream, so NCB chunks are always in
+    // flight and every load is issued the same distance ahead of its use.
 #define PASS_FETCH_CHUNK(B, K, DST)                                                     \
   do {                                                                                 \
-    const int p_ = min(((B) + 2) * BP + (wave - 2 + (K) * BW) * 64 + lane, P - 1);     \
-    const u32x4* c_ = PASS_COL(B, p_);                                                 \
+    const int b_ = min(B, nblk - 1);                                                   \
+    const int p_ = min((b_ + 2) * BP + (wave - 2 + (K) * BW) * 64 + lane, P - 1);      \
+    const u32x4* c_ = PASS_COL(b_, p_);                                                \
     _Pragma("unroll") for (int q_ = 0; q_ < QW; ++q_) DST[q_] = c_[q_];                \
   } while (0)
+    auto nk_of = [&](int B) {  // this wave's chunks of block B
+      const int first = (B + 2) * BP + (wave - 2) * 64;
+      return first < P ? (P - first + 64 * BW - 1) / (64 * BW) : 0;
+    };
+    auto nkp_of = [&](int B) { return (nk_of(B) + NCB - 1) / NCB * NCB; };
+    int fb = 0, fk = 0;  // next chunk of the stream to load
+    auto fetch_next = [&](u32x4* dst) {
+      while (fb + 2 < nblk && fk >= nkp_of(fb)) {
+        ++fb;
+        fk = 0;
+      }
+      PASS_FETCH_CHUNK(fb, fk, dst);
+      ++fk;
+    };
     u32x4 cb[NCB][QW];
-    if (nblk > 2) {
 #pragma unroll
-      for (int k = 0; k < NCB; ++k) PASS_FETCH_CHUNK(0, k, cb[k]);
-    }
+    for (int r = 0; r < NCB; ++r) fetch_next(cb[r]);
     for (int b = 0; b + 2 < nblk; ++b) {
       wait_at_least(&s_cnt[0], b);
       const uint32_t smask = s_mask[b & 3];
-      const int p0 = (b + 2) * BP + (wave - 2) * 64 + lane;
+      const int nk = nk_of(b), nkp = nkp_of(b);
+      for (int k0 = 0; k0 < nkp; k0 += NCB) {
 #pragma unroll
-      for (int k = 0; k < NCB; ++k) {
-        float sum;
-        PASS_SUM(cb[k], smask, sum);
-        const int p = p0 + 64 * BW * k;
-        if (p < P) s_alpha[p] += (double)sum;
-      }
-      for (int k = NCB; (b + 2) * BP + (wave - 2 + k * BW) * 64 < P; ++k) {  // large buckets
-        u32x4 cx[QW];
-        PASS_FETCH_CHUNK(b, k, cx);
-        float sum;
-        PASS_SUM(cx, smask, sum);
-        const int p = p0 + 64 * BW * k;
-        if (p < P) s_alpha[p] += (double)sum;
+        for (int r = 0; r < NCB; ++r) {
+          const int k = k0 + r;
+          float sum;
+          PASS_SUM(cb[r], smask, sum);
+          const int p = (b + 2) * BP + (wave - 2 + k * BW) * 64 + lane;
+          if (k < nk && p < P) s_alpha[p] += (double)sum;
+          fetch_next(cb[r]);
+        }
       }
       __hip_atomic_fetch_add(&s_cnt[2 + (b & 3)], 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
-      if (b + 3 < nblk) {
-#pragma unroll
-        for (int k = 0; k < NCB; ++k) PASS_FETCH_CHUNK(b + 1, k, cb[k]);
-      }
     }
 #undef PASS_FETCH_CHUNK
   }

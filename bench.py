@@ -229,8 +229,9 @@ def main():
     # per launch: averages over every score launch of the K steps (a round may
     # take several launches; bytes and time are both summed over the step)
     n_sc = len(score_ms) // args.steps
+    sc_rounds = sorted({r for name, r, _ in rec if name == "scores"})  # the others run local
     sc_ms_launch = statistics.mean(score_ms)
-    sc_bytes_launch = sum(sb) / n_sc
+    sc_bytes_launch = sum(sb[r] for r in sc_rounds) / n_sc
     sc_gbs = sc_bytes_launch / (sc_ms_launch * 1e-3) / 1e9
     traffic = stored_traffic(w.name)
     attn_gbs = ab / (ta * 1e-3) / 1e9
@@ -253,12 +254,13 @@ def main():
         "config": {"workload": w.name, "B": w.B, "H": w.H, "n": w.n, "n_q": w.n_q, "d": w.d,
                    "n_out": w.n_out, "g": w.g, "out_dtype": "fp32"},
         "roofline": {
-            "kernel": "pair_scores_kernel (one launch per Halve round)",
+            "kernel": "pair_scores_kernel (one launch per Halve round with buckets above "
+                      "the local size)",
             "bound": "hbm", "achieved": sc_gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
             "frac": sc_gbs / HBM_PEAK_GBS,
             "traffic": traffic,
             "algorithmic_bytes_per_launch": sc_bytes_launch, "ms_per_launch": sc_ms_launch,
-            "launches_per_step": n_sc,
+            "launches_per_step": n_sc, "rounds": sc_rounds,
         },
         "compress": {"ms": tc, "kappa_evals": kev, "kappa_evals_per_s": kev / (tc * 1e-3),
                      "algorithmic_bytes": cb, "hbm_gbs": cb / (tc * 1e-3) / 1e9,

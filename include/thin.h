@@ -154,8 +154,11 @@ const char* thin_status_str(int status);
  * hook(ctx, kernel, round, 1, stream) right after.  The hook may enqueue
  * stream-ordered work of its own (for instance record an event on `stream`),
  * so that consecutive records time one kernel.  `kernel` is a
- * thin_kernel_t, `round` the Halve round 0..L-1 of a THIN_KERNEL_SCORES or
- * THIN_KERNEL_DECIDE launch and -1 otherwise.  The setting is process-wide:
+ * thin_kernel_t, `round` the Halve round 0..L-1 of a THIN_KERNEL_SCORES,
+ * THIN_KERNEL_DECIDE or THIN_KERNEL_LOCAL launch and -1 otherwise.  A round
+ * runs either as SCORES + DECIDE launches or, when its buckets are small
+ * enough for one workgroup to hold all their scores in LDS, as one LOCAL
+ * launch.  The setting is process-wide:
  * change it only while no other thread is inside the library.  hook = NULL
  * turns it off (the default).  Returns THIN_OK.
  */
@@ -166,7 +169,8 @@ typedef enum {
   THIN_KERNEL_VMAX = 3,        /* v_max scan (with its zeroing)           */
   THIN_KERNEL_SCORES = 4,      /* pair scores of one round                */
   THIN_KERNEL_DECIDE = 5,      /* decision pass of one round              */
-  THIN_KERNEL_ATTENTION = 6    /* coreset attention                       */
+  THIN_KERNEL_ATTENTION = 6,   /* coreset attention                       */
+  THIN_KERNEL_LOCAL = 7        /* scores and decisions of one round        */
 } thin_kernel_t;
 typedef void (*thin_launch_hook_t)(void* ctx, int32_t kernel, int32_t round, int32_t phase,
                                    void* stream);

@@ -26,7 +26,7 @@ EXPORTS = ("thin_plan", "thin_compress", "thin_compress_traced", "thin_attention
 
 # thin_kernel_t
 KERNEL_NAMES = {0: "trace_clear", 1: "subsample", 2: "fill", 3: "vmax", 4: "scores",
-                5: "decide", 6: "attention"}
+                5: "decide", 6: "attention", 7: "local"}
 LaunchHook = C.CFUNCTYPE(None, C.c_void_p, C.c_int32, C.c_int32, C.c_int32, C.c_void_p)
 
 

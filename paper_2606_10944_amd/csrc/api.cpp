@@ -1,6 +1,8 @@
 // C ABI of the thinning library: planning, argument validation and the
 // level-synchronous launch sequence of the compress path.
 #include <math.h>
+
+#include <algorithm>
 #include <stdint.h>
 #include <string.h>
 
@@ -65,7 +67,10 @@ size_t score_bytes(int64_t N) { return thin::halve_score_bytes(N); }
 
 size_t score_region(int64_t S, int64_t d, const Levels& lv) {
   size_t region = 0;
+  // rounds whose buckets run as one local launch (for either dtype) need none
+  const int64_t local = std::min(thin::halve_local_rows(0, d), thin::halve_local_rows(1, d));
   for (int32_t r = 0; r < lv.L; ++r) {
+    if (lv.N[r] <= local) continue;
     const size_t per = score_bytes(lv.N[r]);
     const size_t all = (size_t)(S * lv.G[r]) * per;
     const size_t cap = per > kScoreCap ? per : kScoreCap;
@@ -199,6 +204,15 @@ int compress_impl(const void* K, const void* V, int32_t dtype, int64_t B, int64_
       a.rowh2_write = r == 0;
       a.chunk0 = 0;
       const int64_t buckets = S * lv.G[r];
+      if (lv.N[r] <= thin::halve_local_rows(dtype, d)) {
+        ok(observed(THIN_KERNEL_LOCAL, r, st, [&] {
+          a.b0 = 0;
+          return thin::launch_local(dtype, d, a, buckets, st);
+        }));
+        u_off += lv.n_r[r] / 2;
+        cur = out;
+        continue;
+      }
       const size_t per = thin::halve_score_bytes(lv.N[r]);
       int64_t chunk = (int64_t)(ws.e_bytes / per);
       if (chunk < 1) chunk = 1;

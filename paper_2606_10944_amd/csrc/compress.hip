@@ -403,10 +403,75 @@ __device__ __forceinline__ void half_block(int w, int h, int& b, int& half) {
   }
 }
 
+// The decisions of one block of 32 pairs (lane p: pair p of the block, with
+// alpha = its score from earlier blocks, thr = a(1 - 2u), ef[i] = E(i, p)).
+// Two decisions per step: alpha < thr for pair i, and for pair i+1 under
+// both signs of pair i's score (pair i swapped: -E(i,.), else +E(i,.)).  The
+// four sums alpha +- E(i,.) +- E(i+1,.) are formed while the ballots
+// resolve; the decisions only select one.  No masking: lane p's alpha is
+// read only at its own decision (step p), before any score of a pair i >= p
+// has been added; decisions past the block's npb pairs are dropped.  With
+// NEAR, en[i] = E(i, q) for a pair q of the next block, and near receives
+// q's signed sum over the block (float32, in ascending i).
+template <bool NEAR>
+__device__ __forceinline__ uint32_t decide_block(double alpha, double thr, const float* ef,
+                                                 const float* en, int npb, float& near) {
+  uint32_t smask = 0;
+#pragma unroll
+  for (int i = 0; i < 32; i += 2) {
+    const double e0 = (double)ef[i], e1 = (double)ef[i + 1];
+    const double ap = alpha + e0, am = alpha - e0;
+    double pp = ap + e1, pm = ap - e1, mp = am + e1, mm = am - e1;
+    // kept as four values (not refactored into one add after the selects)
+    asm volatile("" : "+v"(pp), "+v"(pm), "+v"(mp), "+v"(mm));
+    const uint64_t b0 = __ballot(alpha < thr);
+    const uint64_t bp = __ballot(ap < thr);
+    const uint64_t bm = __ballot(am < thr);
+    const uint32_t s0 = (uint32_t)(b0 >> i) & 1u;
+    const double up = s0 ? mp : pp, um = s0 ? mm : pm;
+    const uint32_t s1 = (uint32_t)((s0 ? bm : bp) >> (i + 1)) & 1u;
+    smask |= (s0 << i) | (s1 << (i + 1));
+    alpha = s1 ? um : up;
+    if (NEAR) {
+      near += s0 ? -en[i] : en[i];
+      near += s1 ? -en[i + 1] : en[i + 1];
+    }
+  }
+  if (npb < 32) smask &= (1u << npb) - 1u;
+  return smask;
+}
+
+// Threshold a(1 - 2u) of the pair of lane l < 32 in a block of npb pairs
+// (Algorithm A.1: a = b b_max (1/2 + log(2N/delta))), in the log domain:
+// lbt = log of the pair's scaled b (-inf if b = 0), h2 = its scale exponent
+// (base 2), carry = log b_max over the bucket's earlier blocks (updated to
+// include this block).  a = 0 (b = 0 or b_max = 0) gives p = 1/2: swap iff
+// u < 1/2.  Lanes >= 32 return values of no meaning.
+__device__ __forceinline__ double block_threshold(float lbt, float h2, float u, int npb, int lane,
+                                                  double log_c, double& carry) {
+  const bool act = lane < npb;
+  const float lbtf = act ? lbt : -INFINITY;
+  const float h2f = act ? h2 : 0.0f;
+  const double half_h = (double)h2f * (0.5 * kLn2);
+  const double pm = prefix_max32(act ? (double)lbtf + half_h : -INFINITY, lane);
+  const double lbmax = fmax(carry, pm);
+  double thr;
+  if (!(lbtf > -INFINITY) || !(lbmax > -INFINITY))
+    thr = (u < 0.5f) ? INFINITY : -INFINITY;
+  else
+    thr = exp_fast((double)lbtf + lbmax + log_c - half_h) * (1.0 - 2.0 * (double)u);
+  carry = __shfl(lbmax, npb - 1);
+  return thr;
+}
+
 // Target of the stores of a streamed chunk's padding tiles (never read).
 __device__ __align__(16) float g_score_sink[256];
 
-template <typename T, int D>
+// LOCAL: the whole round for buckets of at most GT*16 rows in one launch:
+// one workgroup per bucket computes the bucket's scores into LDS (its own
+// chunk is the whole bucket), then wave 0 takes the decisions from LDS with
+// the same arithmetic as halve_pass_kernel (the scores never leave the CU).
+template <typename T, int D, bool LOCAL>
 __global__ __launch_bounds__(64 * kScoreWaves) __attribute__((amdgpu_waves_per_eu(2)))
 void pair_scores_kernel(HalveArgs a) {
   using SS = ScoreShape<T, D>;
@@ -450,10 +515,13 @@ void pair_scores_kernel(HalveArgs a) {
   const float c2 = (float)(kLog2e * inv_sqrt_d);
 
   extern __shared__ __align__(16) unsigned char smem[];
-  float* s_e = reinterpret_cast<float*>(smem + NS * CH * 1024);    // [NS][NBW] tile buffers
-  float* s_h2 = s_e + NS * NBW * kETileLds;                          // [GT * 16], own rows
+  // [NS][NBW] tile buffers, or (LOCAL) every score tile of the bucket
+  float* s_e = reinterpret_cast<float*>(smem + NS * CH * 1024);
+  float* s_h2 = s_e + (LOCAL ? (int)panel_tiles(nb, NT, 4) : NS * NBW) * kETileLds;  // [GT * 16]
   float* s_hst = s_h2 + GT * 16;                                     // [NS * 16], staged rows
   int64_t* s_rows = reinterpret_cast<int64_t*>(s_hst + NS * 16);
+  float* s_lbt = s_hst + NS * 16;  // LOCAL: pair terms [P] and [P] (no staged rows there)
+  float* s_h2p = s_lbt + P;
 
   // ---- this wave's half-blocks: fragments and, in chunk 0, pair terms ----
   int hb_blk[HB], hb_half[HB];
@@ -493,8 +561,13 @@ void pair_scores_kernel(HalveArgs a) {
         const int j = hb_blk[h] * 64 + hb_half[h] * 32 + rt * 16 + m16;
         if (g == 0) s_h2[((hb_blk[h] - grp * NBW) * 4 + hb_half[h] * 2 + rt) * 16 + m16] = h2f;
         if (g == 0 && j < N && (j & 1) == 0) {
-          a.h2[pb + (j >> 1)] = h2f;
-          a.lbt[pb + (j >> 1)] = lbt;
+          if (LOCAL) {
+            s_h2p[j >> 1] = h2f;
+            s_lbt[j >> 1] = lbt;
+          } else {
+            a.h2[pb + (j >> 1)] = h2f;
+            a.lbt[pb + (j >> 1)] = lbt;
+          }
         }
         if (a.rowh2_write && g == 0 && j < N)
           a.rowh2[s * a.n + (rows_in ? (int64_t)rows_in[j] : row_base + j)] = rh2;
@@ -590,7 +663,8 @@ void pair_scores_kernel(HalveArgs a) {
   // F0 - F0(partner) and the odd lane E(2g+1, p) = F1(partner) - F1.
 #define SCORE_EPI_H(H, H2, BUF)                                                         \
   do {                                                                                 \
-    float* eb_ = s_e + ((BUF) * NBW + hb_blk[H] - grp * NBW) * kETileLds;              \
+    float* eb_ = LOCAL ? s_e + (panel_tiles(hb_blk[H], NT, 4) + jt_ - 4 * hb_blk[H]) * kETileLds \
+                       : s_e + ((BUF) * NBW + hb_blk[H] - grp * NBW) * kETileLds;      \
     _Pragma("unroll") for (int rt = 0; rt < 2; ++rt) {                                 \
       float kap[4];                                                                    \
       _Pragma("unroll") for (int e = 0; e < 4; ++e)                                    \
@@ -609,7 +683,7 @@ void pair_scores_kernel(HalveArgs a) {
   // streamed chunk's padding tiles go to the sink.
 #define SCORE_FLUSH(OWN, IF, BUF)                                                       \
   do {                                                                                 \
-    if (NBW == kScoreWaves || wave < NBW) {                                            \
+    if (!LOCAL && (NBW == kScoreWaves || wave < NBW)) {                                \
       const int bw_ = grp * NBW + wave;                                                \
       const int jtf_ = jt0 + (IF);                                                     \
       if (!(OWN) || (bw_ < nb && jtf_ >= 4 * bw_)) {                                   \
@@ -681,6 +755,49 @@ void pair_scores_kernel(HalveArgs a) {
     __syncthreads();                                                                   \
   } while (0)
 
+  // LOCAL: the decisions of the bucket's P <= 32 NBW pairs from the scores
+  // in LDS (wave 0).  Block m: thresholds as in halve_pass_kernel; alpha =
+  // the float32 signed sums of every earlier block, added in block order in
+  // float64 (the order of the separate pass); then decide_block.
+  auto local_decisions = [&]() {
+    const int nblk = (P + 31) / 32;
+    const float* Ub = a.U + s * a.u_slice + a.u_off + t * (int64_t)P;
+    uint8_t* trace = a.trace ? a.trace + s * a.u_slice + a.u_off + t * (int64_t)P : nullptr;
+    int32_t* out = a.idx_out + s * (a.n_r >> 1) + t * (int64_t)P;
+    const int pl = lane & 31;
+    double carry = -INFINITY;
+    uint32_t masks[NBW];
+#pragma unroll
+    for (int m = 0; m < NBW; ++m) {
+      if (m >= nblk) break;
+      const int npb = min(32, P - 32 * m);
+      const int gp = 32 * m + min(pl, npb - 1);
+      const double thr = block_threshold(s_lbt[gp], s_h2p[gp], Ub[gp], npb, lane, a.log_c, carry);
+      double alpha = 0.0;
+#pragma unroll
+      for (int b = 0; b < m; ++b) {
+        const float* col = s_e + (panel_tiles(b, NT, 4) + (gp >> 3) - 4 * b) * kETileLds + (gp & 7) * kETileStride;
+        float sum = 0.0f;
+#pragma unroll
+        for (int i = 0; i < 32; ++i) sum += ((masks[b] >> i) & 1u) ? -col[i] : col[i];
+        alpha += (double)sum;
+      }
+      float ef[32];
+      const float* oc = s_e + (panel_tiles(m, NT, 4) + (gp >> 3) - 4 * m) * kETileLds + (gp & 7) * kETileStride;
+#pragma unroll
+      for (int i = 0; i < 32; ++i) ef[i] = oc[i];
+      float unused = 0.0f;
+      masks[m] = decide_block<false>(alpha, thr, ef, ef, npb, unused);
+      const uint32_t bit = (masks[m] >> pl) & 1u;
+      if (lane < npb) {
+        const int32_t r0 = rows_in ? rows_in[2 * gp] : (int32_t)(row_base + 2 * gp);
+        const int32_t r1 = rows_in ? rows_in[2 * gp + 1] : (int32_t)(row_base + 2 * gp + 1);
+        out[gp] = bit ? r1 : r0;
+        if (trace) trace[gp] = (uint8_t)bit;
+      }
+    }
+  };
+
   const bool odd = (m16 & 1) != 0;
   __syncthreads();
   if (own) {
@@ -693,7 +810,11 @@ void pair_scores_kernel(HalveArgs a) {
         if (ib + u < ntile) SCORE_TILE(true, ib + u, u);  // uniform over the workgroup
     }
     SCORE_FLUSH(true, ntile - 1, (ntile - 1) % NS);
-  } else {
+    if constexpr (LOCAL) {
+      __syncthreads();
+      if (wave == 0) local_decisions();
+    }
+  } else if constexpr (!LOCAL) {
 #pragma unroll
     for (int k = 0; k < DEPTH; ++k) SCORE_ISSUE(jt0 + k, k);
     SCORE_COMMIT(0, 0);
@@ -716,7 +837,10 @@ void pair_scores_kernel(HalveArgs a) {
         for (int u = 0; u < DEPTH; ++u) SCORE_TILE_P(ib + u, u, false);
       }
       const int last = nturn * DEPTH - 1;
-      SCORE_EPI_H(1, h2_prev, last % NS);
+      {
+        const int jt_ = jt0 + last;  // (names the tile for the LOCAL layout only)
+        SCORE_EPI_H(1, h2_prev, last % NS);
+      }
       __syncthreads();
       SCORE_FLUSH(false, last - 1, (last - 1) % NS);
       SCORE_FLUSH(false, last, last % NS);
@@ -896,30 +1020,7 @@ __global__ __launch_bounds__(64 * (BW + 2)) void halve_pass_kernel(HalveArgs a) 
         }
       __builtin_amdgcn_sched_barrier(0);
       float near = 0.0f;
-      // Decisions i and i+1 per step: alpha < thr for pair i, and for pair
-      // i+1 under both signs of pair i's score (pair i swapped: -E(i,.),
-      // else +E(i,.)).  The four sums alpha +- E(i,.) +- E(i+1,.) are formed
-      // while the decisions are taken; the decisions only select one.
-      uint32_t smask = 0;
-#pragma unroll
-      for (int i = 0; i < BP; i += 2) {
-        const double e0 = (double)ef[i], e1 = (double)ef[i + 1];
-        const double ap = alpha + e0, am = alpha - e0;
-        double pp = ap + e1, pm = ap - e1, mp = am + e1, mm = am - e1;
-        // kept as four values (not refactored into one add after the selects)
-        asm volatile("" : "+v"(pp), "+v"(pm), "+v"(mp), "+v"(mm));
-        const uint64_t b0 = __ballot(alpha < thr);
-        const uint64_t bp = __ballot(ap < thr);
-        const uint64_t bm = __ballot(am < thr);
-        const uint32_t s0 = (uint32_t)(b0 >> i) & 1u;
-        const double up = s0 ? mp : pp, um = s0 ? mm : pm;
-        const uint32_t s1 = (uint32_t)((s0 ? bm : bp) >> (i + 1)) & 1u;
-        smask |= (s0 << i) | (s1 << (i + 1));
-        alpha = s1 ? um : up;
-        near += s0 ? -en[i] : en[i];
-        near += s1 ? -en[i + 1] : en[i + 1];
-      }
-      if (npb < BP) smask &= (1u << npb) - 1u;
+      const uint32_t smask = decide_block<true>(alpha, thr, ef, en, npb, near);
       if (lane == 0) s_mask[m & 3] = smask;
       publish(&s_cnt[0], m);
       const uint32_t bit = (smask >> (p & 31)) & 1u;
@@ -964,18 +1065,7 @@ __global__ __launch_bounds__(64 * (BW + 2)) void halve_pass_kernel(HalveArgs a) 
 #define PASS_STAGE(B, K)                                                                \
   do {                                                                                 \
     const int npb_ = min(BP, P - (B) * BP);                                            \
-    const bool act_ = lane < npb_;                                                     \
-    const float lbtf_ = act_ ? flbt[K] : -INFINITY;                                    \
-    const float h2f_ = act_ ? fh2[K] : 0.0f;                                           \
-    const double half_h_ = (double)h2f_ * (0.5 * kLn2);                                \
-    const double pm_ = prefix_max32(act_ ? (double)lbtf_ + half_h_ : -INFINITY, lane);  \
-    const double lbmax_ = fmax(carry, pm_);                                            \
-    double thr_;                                                                       \
-    if (!(lbtf_ > -INFINITY) || !(lbmax_ > -INFINITY))                                 \
-      thr_ = (fu[K] < 0.5f) ? INFINITY : -INFINITY; /* a = 0: p = 1/2 */              \
-    else                                                                               \
-      thr_ = exp_fast((double)lbtf_ + lbmax_ + a.log_c - half_h_) * (1.0 - 2.0 * (double)fu[K]); \
-    carry = __shfl(lbmax_, npb_ - 1);                                                  \
+    const double thr_ = block_threshold(flbt[K], fh2[K], fu[K], npb_, lane, a.log_c, carry); \
     /* slot B%3 held block B-3, which the decider has left once B-2 is decided */    \
     if ((B) >= L::NSLOT) wait_at_least(&s_cnt[0], (B) - (L::NSLOT - 1));              \
     unsigned char* sb_ = slot(B);                                                      \
@@ -1074,7 +1164,7 @@ __global__ __launch_bounds__(64) void gram16_kernel(const T* rows, float* out) {
 template <typename T, int D>
 hipError_t launch_scores_td(const HalveArgs& a, int64_t nbk, hipStream_t st) {
   using SS = ScoreShape<T, D>;
-  auto kern = pair_scores_kernel<T, D>;
+  auto kern = pair_scores_kernel<T, D, false>;
   const size_t lds = SS::LDS;
   if (lds > 64 * 1024) {
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
@@ -1103,6 +1193,47 @@ hipError_t launch_scores_td(const HalveArgs& a, int64_t nbk, hipStream_t st) {
   dim3 grid((unsigned)nbk, (unsigned)groups, (unsigned)nch);
   hipLaunchKernelGGL(kern, grid, dim3(64 * kScoreWaves), lds, st, one);
   return hipGetLastError();
+}
+
+template <typename T, int D>
+hipError_t launch_local_td(const HalveArgs& a0, int64_t nbk, hipStream_t st) {
+  using SS = ScoreShape<T, D>;
+  auto kern = pair_scores_kernel<T, D, true>;
+  const int64_t NT = (a0.N + 15) / 16, nb = (a0.N + 63) / 64, P = a0.N / 2;
+  const size_t lds = (size_t)kScoreStages * SS::CHUNKS * 1024 +
+                     (size_t)panel_tiles(nb, NT, 4) * kETileLds * 4 + SS::GT * 16 * 4 +
+                     kScoreStages * 16 * 4 + 2 * P * 4;
+  if (lds > 64 * 1024) {
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e != hipSuccess) return e;
+  }
+  HalveArgs a = a0;
+  a.chunk0 = 0;
+  a.ch = kScoreChunk;
+  a.e_tiles = 0;
+  hipLaunchKernelGGL(kern, dim3((unsigned)nbk), dim3(64 * kScoreWaves), lds, st, a);
+  return hipGetLastError();
+}
+
+template <typename T>
+hipError_t launch_local_t(int64_t d, const HalveArgs& a, int64_t nbk, hipStream_t st) {
+  switch (d) {
+    case 32: return launch_local_td<T, 32>(a, nbk, st);
+    case 64: return launch_local_td<T, 64>(a, nbk, st);
+    case 128: return launch_local_td<T, 128>(a, nbk, st);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+template <typename T>
+int64_t local_rows_t(int64_t d) {
+  switch (d) {
+    case 32: return ScoreShape<T, 32>::GT * 16;
+    case 64: return ScoreShape<T, 64>::GT * 16;
+    case 128: return ScoreShape<T, 128>::GT * 16;
+    default: return 0;
+  }
 }
 
 template <typename T>
@@ -1150,6 +1281,15 @@ static HalveArgs with_layout(const HalveArgs& a0) {
 hipError_t launch_scores(int dtype, int64_t d, const HalveArgs& a0, int64_t nbk, hipStream_t st) {
   const HalveArgs a = with_layout(a0);
   return dtype == 0 ? launch_scores_t<float>(d, a, nbk, st) : launch_scores_t<bf16_t>(d, a, nbk, st);
+}
+
+int64_t halve_local_rows(int dtype, int64_t d) {
+  return dtype == 0 ? local_rows_t<float>(d) : local_rows_t<bf16_t>(d);
+}
+
+hipError_t launch_local(int dtype, int64_t d, const HalveArgs& a, int64_t nbk, hipStream_t st) {
+  if (a.N > halve_local_rows(dtype, d)) return hipErrorInvalidValue;
+  return dtype == 0 ? launch_local_t<float>(d, a, nbk, st) : launch_local_t<bf16_t>(d, a, nbk, st);
 }
 
 hipError_t launch_decide(const HalveArgs& a0, int64_t nbk, hipStream_t st) {

@@ -48,6 +48,10 @@ size_t halve_score_bytes(int64_t N);
 // Pair scores, then the decision pass, for nbk buckets starting at a.b0.
 hipError_t launch_scores(int dtype, int64_t d, const HalveArgs& a, int64_t nbk, hipStream_t st);
 hipError_t launch_decide(const HalveArgs& a, int64_t nbk, hipStream_t st);
+// Buckets of at most halve_local_rows(dtype, d) rows: the whole round (scores
+// in LDS, then the decisions) in one launch, no score buffer.
+int64_t halve_local_rows(int dtype, int64_t d);
+hipError_t launch_local(int dtype, int64_t d, const HalveArgs& a, int64_t nbk, hipStream_t st);
 
 hipError_t launch_attention(int dtype, int64_t d, int out_dtype, const void* Q, const void* K,
                             const void* V, const int32_t* idx, int64_t S, int64_t n,

@@ -453,11 +453,15 @@ __global__ __launch_bounds__(64 * WR) void coreset_attn_res_kernel(
           }
           const int col = 32 * j + (upper ? 16 : 0) + 4 * g;
           // rows past the range store to a sink: the stores stay unconditional,
-          // so the wait for the next queries' loads never covers them
+          // so the wait for the next queries' loads never covers them.  The
+          // output is written once and not read here: non-temporal stores keep
+          // it out of the caches, which the next kernels' reads would
+          // otherwise first have to write back.
           float* da = qa < q_end ? ra + col : g_attn_sink + 4 * lane;
           float* db = qb < q_end ? rb + col : g_attn_sink + 4 * lane;
-          *reinterpret_cast<float4*>(da) = make_float4(va[0], va[1], va[2], va[3]);
-          *reinterpret_cast<float4*>(db) = make_float4(vb[0], vb[1], vb[2], vb[3]);
+          typedef float f4_t __attribute__((ext_vector_type(4)));
+          __builtin_nontemporal_store((f4_t){va[0], va[1], va[2], va[3]}, reinterpret_cast<f4_t*>(da));
+          __builtin_nontemporal_store((f4_t){vb[0], vb[1], vb[2], vb[3]}, reinterpret_cast<f4_t*>(db));
         }
       } else {
         const int64_t q = qw + qt * 16 + m16;

@@ -94,10 +94,10 @@ def score_bytes(w, plan) -> list:
 
 
 def kernel_sources_sha256() -> str:
-    """Hash of the compress kernels' sources (a stored traffic measurement is
-    only reported while it matches)."""
+    """Hash of the compress kernels' sources and of the launch sequence (a
+    stored traffic measurement is only reported while it matches)."""
     h = hashlib.sha256()
-    for f in ("compress.hip", "common.hpp", "launch.hpp"):
+    for f in ("compress.hip", "common.hpp", "launch.hpp", "api.cpp"):
         with open(os.path.join(ROOT, "paper_2606_10944_amd", "csrc", f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()

@@ -63,6 +63,12 @@ bool make_levels(int64_t n, int64_t n_out, int32_t g, Levels* lv) {
 // several launches.
 constexpr size_t kScoreCap = (size_t)2 << 30;
 
+// Rounds of small buckets run as one local launch (scores in LDS, then the
+// decisions) up to this many buckets.  Beyond it the two-launch path is as
+// fast (its score kernel overlaps loads and arithmetic across workgroups and
+// its decision pass runs more buckets per CU), so many-bucket rounds keep it.
+constexpr int64_t kLocalMaxBuckets = 2048;
+
 size_t score_bytes(int64_t N) { return thin::halve_score_bytes(N); }
 
 size_t score_region(int64_t S, int64_t d, const Levels& lv) {
@@ -70,7 +76,7 @@ size_t score_region(int64_t S, int64_t d, const Levels& lv) {
   // rounds whose buckets run as one local launch (for either dtype) need none
   const int64_t local = std::min(thin::halve_local_rows(0, d), thin::halve_local_rows(1, d));
   for (int32_t r = 0; r < lv.L; ++r) {
-    if (lv.N[r] <= local) continue;
+    if (lv.N[r] <= local && S * lv.G[r] < kLocalMaxBuckets) continue;
     const size_t per = score_bytes(lv.N[r]);
     const size_t all = (size_t)(S * lv.G[r]) * per;
     const size_t cap = per > kScoreCap ? per : kScoreCap;
@@ -204,7 +210,7 @@ int compress_impl(const void* K, const void* V, int32_t dtype, int64_t B, int64_
       a.rowh2_write = r == 0;
       a.chunk0 = 0;
       const int64_t buckets = S * lv.G[r];
-      if (lv.N[r] <= thin::halve_local_rows(dtype, d)) {
+      if (lv.N[r] <= thin::halve_local_rows(dtype, d) && buckets < kLocalMaxBuckets) {
         ok(observed(THIN_KERNEL_LOCAL, r, st, [&] {
           a.b0 = 0;
           return thin::launch_local(dtype, d, a, buckets, st);

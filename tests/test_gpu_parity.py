@@ -134,6 +134,11 @@ CUSTOM = [
     dict(B=2, H=1, n=2048, n_out=32, g=2, d=128, dtype="bf16", kind="heavy_tail"),
     # clustered keys, one bucket per round
     dict(B=2, H=1, n=512, n_out=16, g=4, d=64, dtype="fp32", kind="mixture"),
+    # fp32 d = 128 with buckets above its 128-row local size: score launches
+    # with streamed chunks from round 0 on (own chunks first, then the rest)
+    dict(B=1, H=1, n=1024, n_out=64, g=2, d=128, dtype="fp32", kind="gauss_d4"),
+    # bf16 d = 32: local rounds, then 512- and 1024-row buckets
+    dict(B=1, H=2, n=4096, n_out=8, g=6, d=32, dtype="bf16", kind="gauss"),
 ]
 
 

@@ -534,6 +534,20 @@ void pair_scores_kernel(HalveArgs a) {
     hb_half[h] = half;
     hb_ok[h] = hb_blk[h] < nb;
   }
+  // Streamed chunk: the row indices of its column rows are requested first,
+  // so that their latency and the fragments' overlap (the index loads are
+  // the older ones, and staging them in LDS waits for them only).
+  constexpr int RPT = (kScoreRowsStaged + 64 * kScoreWaves - 1) / (64 * kScoreWaves);
+  const int j_end = own ? 0 : min(N, (jt1 + 2 * DEPTH + 1) * 16);
+  int64_t ridx[RPT];
+  if (!own) {
+#pragma unroll
+    for (int k = 0; k < RPT; ++k) {
+      const int j = jt0 * 16 + (int)threadIdx.x + k * 64 * kScoreWaves;
+      ridx[k] = j < j_end ? (rows_in ? (int64_t)rows_in[j] : row_base + j) : 0;
+    }
+  }
+  __builtin_amdgcn_sched_barrier(0);
   uint4 Ak[HB][2][NV], Av[HB][2][NV];
 #pragma unroll
   for (int h = 0; h < HB; ++h)
@@ -545,11 +559,12 @@ void pair_scores_kernel(HalveArgs a) {
       load_frag<T, D>(K, r, g, valid, Ak[h][rt]);
       load_frag<T, D>(V, r, g, valid, Av[h][rt]);
     }
-  // Wait for the fragments here (vmcnt(0)).  Otherwise the first use sits in
-  // the tile loop, whose wait then also covers the score stores of earlier
-  // tiles on every iteration (stores count in vmcnt on this architecture).
-  __builtin_amdgcn_s_waitcnt(0x0F70);
   if (own) {
+    // Wait for the fragments here (vmcnt(0)).  Otherwise the first use sits
+    // in the tile loop, whose wait then also covers the score stores of
+    // earlier tiles on every iteration (stores count in vmcnt on this
+    // architecture).  Streamed chunks first use them in the peeled ring turn.
+    __builtin_amdgcn_s_waitcnt(0x0F70);
     const int64_t pb = s * (a.n_r >> 1) + t * (int64_t)P;
 #pragma unroll
     for (int h = 0; h < HB; ++h) {
@@ -574,11 +589,14 @@ void pair_scores_kernel(HalveArgs a) {
       }
     }
   } else {
-    // row indices of every streamed column row, staged first: a data load
-    // then never waits on an index load issued behind the ring's loads
-    const int j_end = min(N, (jt1 + 2 * DEPTH + 1) * 16);
-    for (int j = jt0 * 16 + (int)threadIdx.x; j < j_end; j += 64 * kScoreWaves)
-      s_rows[j - jt0 * 16] = rows_in ? (int64_t)rows_in[j] : row_base + j;
+    // row indices of every streamed column row, staged in LDS before the
+    // ring starts: a data load then never waits on an index load issued
+    // behind the ring's loads
+#pragma unroll
+    for (int k = 0; k < RPT; ++k) {
+      const int j = jt0 * 16 + (int)threadIdx.x + k * 64 * kScoreWaves;
+      if (j < j_end) s_rows[j - jt0 * 16] = ridx[k];
+    }
   }
 
   // ---- column tiles ----

@@ -405,37 +405,29 @@ __device__ __forceinline__ void half_block(int w, int h, int& b, int& half) {
 
 // The decisions of one block of 32 pairs (lane p: pair p of the block, with
 // alpha = its score from earlier blocks, thr = a(1 - 2u), ef[i] = E(i, p)).
-// Two decisions per step: alpha < thr for pair i, and for pair i+1 under
-// both signs of pair i's score (pair i swapped: -E(i,.), else +E(i,.)).  The
-// four sums alpha +- E(i,.) +- E(i+1,.) are formed while the ballots
-// resolve; the decisions only select one.  No masking: lane p's alpha is
-// read only at its own decision (step p), before any score of a pair i >= p
-// has been added; decisions past the block's npb pairs are dropped.  With
-// NEAR, en[i] = E(i, q) for a pair q of the next block, and near receives
-// q's signed sum over the block (float32, in ascending i).
+// One decision per step: the ballot of alpha < thr gives pair i's decision
+// (swap: -E(i,.), else +E(i,.)), and every lane adds its signed score as one
+// fused multiply-add by a uniform +-1 (the product is exact, so the result
+// is the rounded sum alpha +- E).  Between the ballot and the add there are
+// only scalar operations: the wave's instruction stream per decision is a
+// handful of instructions, which sets this loop's speed.  No masking: lane
+// p's alpha is read only at its own decision (step p), before any score of a
+// pair i >= p has been added; decisions past the block's npb pairs are
+// dropped.  With NEAR, en[i] = E(i, q) for a pair q of the next block, and
+// near receives q's signed sum over the block (float32, in ascending i).
 template <bool NEAR>
 __device__ __forceinline__ uint32_t decide_block(double alpha, double thr, const float* ef,
                                                  const float* en, int npb, float& near) {
   uint32_t smask = 0;
 #pragma unroll
-  for (int i = 0; i < 32; i += 2) {
-    const double e0 = (double)ef[i], e1 = (double)ef[i + 1];
-    const double ap = alpha + e0, am = alpha - e0;
-    double pp = ap + e1, pm = ap - e1, mp = am + e1, mm = am - e1;
-    // kept as four values (not refactored into one add after the selects)
-    asm volatile("" : "+v"(pp), "+v"(pm), "+v"(mp), "+v"(mm));
-    const uint64_t b0 = __ballot(alpha < thr);
-    const uint64_t bp = __ballot(ap < thr);
-    const uint64_t bm = __ballot(am < thr);
-    const uint32_t s0 = (uint32_t)(b0 >> i) & 1u;
-    const double up = s0 ? mp : pp, um = s0 ? mm : pm;
-    const uint32_t s1 = (uint32_t)((s0 ? bm : bp) >> (i + 1)) & 1u;
-    smask |= (s0 << i) | (s1 << (i + 1));
-    alpha = s1 ? um : up;
-    if (NEAR) {
-      near += s0 ? -en[i] : en[i];
-      near += s1 ? -en[i + 1] : en[i + 1];
-    }
+  for (int i = 0; i < 32; ++i) {
+    const double e = (double)ef[i];
+    const uint32_t d = (uint32_t)(__ballot(alpha < thr) >> i) & 1u;
+    smask |= d << i;
+    // +-1 built as bits (the sign bit from d): scalar integer operations
+    // only, no select between two vector values
+    alpha = __builtin_fma(e, __hiloint2double((int)(0x3ff00000u | (d << 31)), 0), alpha);
+    if (NEAR) near = __builtin_fmaf(en[i], __uint_as_float(0x3f800000u | (d << 31)), near);
   }
   if (npb < 32) smask &= (1u << npb) - 1u;
   return smask;
@@ -897,17 +889,23 @@ void pair_scores_kernel(HalveArgs a) {
 //    second decision is evaluated for both outcomes of the first), publishes
 //    them, then adds the block's scores to the next block's pairs itself;
 //  - waves 2.. (bulk) add each decided block's scores to all pairs two or
-//    more blocks later, with their next column chunks fetched in advance.
+//    more blocks later.  Each pair belongs to one bulk wave (64-pair chunks,
+//    dealt round robin), which adds the blocks in order; the column chunks
+//    are fetched ahead in one stream per wave, across blocks.
 // alpha of a pair in block m = (contributions of blocks <= m-2, summed by the
 // bulk waves in block order) + (contribution of block m-1, from the decider).
 // The decider never waits on global memory.  Every wait is bounded.
 constexpr int kSpinLimit = 1 << 16;
 
-__device__ __forceinline__ void wait_at_least(const int* flag, int target) {
+// Returns the last value read (>= target unless the spin limit ran out).
+__device__ __forceinline__ int wait_at_least(const int* flag, int target) {
+  int v = 0;
   for (int it = 0; it < kSpinLimit; ++it) {
-    if (__hip_atomic_load(flag, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_WORKGROUP) >= target) return;
+    v = __hip_atomic_load(flag, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_WORKGROUP);
+    if (v >= target) break;
     __builtin_amdgcn_s_sleep(1);
   }
+  return v;
 }
 __device__ __forceinline__ void publish(int* flag, int value) {
   __hip_atomic_store(flag, value, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
@@ -916,15 +914,28 @@ __device__ __forceinline__ void publish(int* flag, int value) {
 template <int BW, int NCB>
 struct PassLds {
   static constexpr int BP = 32, QW = 8, NSLOT = 3;
-  // alpha [P] | mask ring [4] | counters [8]: decided, staged, bulk
-  // completions per block (ring of 4) | NSLOT input slots, each: thresholds
-  // [BP] f64, rows [2][BP] i32, own scores [BP][QW] and next-block scores
-  // [BP][QW] 16-byte words
-  static constexpr size_t kSlot = BP * 8 + 2 * BP * 4 + 2 * BP * QW * 16;
+  // alpha [P] f64 | decisions of every block [nblk] u32 | counters [16]:
+  // last decided block, last staged block, rows completed by each bulk wave |
+  // NSLOT input slots, each: thresholds [BP] f64, rows [2][BP] i32, own
+  // scores [BP][CW] and next-block scores [BP][CW] 16-byte words | with
+  // COAL, per bulk wave a column buffer [64][CW] 16-byte words.  A column of
+  // BP scores is QW words plus one of padding (CW): reads of whole columns
+  // by consecutive lanes then fall in different banks.  COAL: the bulk waves
+  // load their chunks coalesced and transpose them in LDS (with four or more
+  // bulk waves the loads, not the LDS, limit them); else each lane loads its
+  // own column, and the workgroup needs less LDS.
+  static constexpr int CW = QW + 1;
+  static constexpr bool COAL = BW >= 4;
+  static constexpr size_t kSlot = BP * 8 + 2 * BP * 4 + 2 * BP * CW * 16;
+  static constexpr size_t kColBuf = COAL ? 64 * CW * 16 : 0;
+  static_assert(2 + BW <= 16, "counter block");
   __host__ __device__ static size_t mask_off(int P) { return ((size_t)P * 8 + 15) & ~(size_t)15; }
-  __host__ __device__ static size_t flag_off(int P) { return mask_off(P) + 16; }
-  __host__ __device__ static size_t slot_off(int P) { return flag_off(P) + 32; }
-  __host__ __device__ static size_t bytes(int P) { return slot_off(P) + NSLOT * kSlot; }
+  __host__ __device__ static size_t flag_off(int P) {
+    return mask_off(P) + (((size_t)(P + BP - 1) / BP * 4 + 15) & ~(size_t)15);
+  }
+  __host__ __device__ static size_t slot_off(int P) { return flag_off(P) + 64; }
+  __host__ __device__ static size_t colbuf_off(int P) { return slot_off(P) + NSLOT * kSlot; }
+  __host__ __device__ static size_t bytes(int P) { return colbuf_off(P) + BW * kColBuf; }
 };
 
 template <int BW, int NCB>
@@ -960,16 +971,16 @@ __global__ __launch_bounds__(64 * (BW + 2)) void halve_pass_kernel(HalveArgs a) 
   extern __shared__ __align__(16) unsigned char smem[];
   double* s_alpha = reinterpret_cast<double*>(smem);
   uint32_t* s_mask = reinterpret_cast<uint32_t*>(smem + L::mask_off(P));
-  int* s_cnt = reinterpret_cast<int*>(smem + L::flag_off(P));  // decided, staged, bulk[4]
+  int* s_cnt = reinterpret_cast<int*>(smem + L::flag_off(P));  // decided, staged, rows[BW]
   auto slot = [&](int m) { return smem + L::slot_off(P) + (size_t)(m % L::NSLOT) * L::kSlot; };
   // slot fields
   auto sl_thr = [&](unsigned char* b) { return reinterpret_cast<double*>(b); };
   auto sl_rows = [&](unsigned char* b) { return reinterpret_cast<int32_t*>(b + BP * 8); };
   auto sl_own = [&](unsigned char* b) { return reinterpret_cast<u32x4*>(b + BP * 8 + 2 * BP * 4); };
-  auto sl_next = [&](unsigned char* b) { return reinterpret_cast<u32x4*>(b + BP * 8 + 2 * BP * 4 + BP * QW * 16); };
+  auto sl_next = [&](unsigned char* b) { return reinterpret_cast<u32x4*>(b + BP * 8 + 2 * BP * 4 + BP * L::CW * 16); };
 
   for (int p = threadIdx.x; p < P; p += 64 * (BW + 2)) s_alpha[p] = 0.0;
-  if (threadIdx.x < 8) s_cnt[threadIdx.x] = threadIdx.x < 2 ? -1 : 0;
+  if (threadIdx.x < 16) s_cnt[threadIdx.x] = threadIdx.x < 2 ? -1 : 0;
   __syncthreads();
 
   // Signed sum of a column's BP scores (decision bits in SMASK).
@@ -995,12 +1006,9 @@ __global__ __launch_bounds__(64 * (BW + 2)) void halve_pass_kernel(HalveArgs a) 
     for (int m = 0; m < nblk; ++m) {
       const int npb = min(BP, P - m * BP);
       wait_at_least(&s_cnt[1], m);
-      if (m >= 2) {
-        // every bulk wave has added block m-2; the counter slot is free again
-        // once block m+2's bulk starts, which needs this block's decisions
-        wait_at_least(&s_cnt[2 + ((m - 2) & 3)], BW);
-        s_cnt[2 + ((m - 2) & 3)] = 0;
-      }
+      // the bulk wave that owns this block's pairs (64-pair chunk m / 2) has
+      // added blocks 0 .. m-2 to them
+      if (m >= 2) wait_at_least(&s_cnt[2 + (m >> 1) % BW], m - 1);
       unsigned char* sb = slot(m);
       const int p = lane;
       const int pl = lane & (BP - 1);
@@ -1020,8 +1028,8 @@ __global__ __launch_bounds__(64 * (BW + 2)) void halve_pass_kernel(HalveArgs a) 
       // their signed sum (the next block's contribution from this block) is
       // accumulated inside the loop, in the order of the bulk sums.
       float ef[BP], en[BP];
-      const u32x4* oc = sl_own(sb) + pl * QW;
-      const u32x4* nc = sl_next(sb) + pl * QW;
+      const u32x4* oc = sl_own(sb) + pl * L::CW;
+      const u32x4* nc = sl_next(sb) + pl * L::CW;
       u32x4 xs[QW], xn[QW];
 #pragma unroll
       for (int q = 0; q < QW; ++q) {
@@ -1039,7 +1047,7 @@ __global__ __launch_bounds__(64 * (BW + 2)) void halve_pass_kernel(HalveArgs a) 
       __builtin_amdgcn_sched_barrier(0);
       float near = 0.0f;
       const uint32_t smask = decide_block<true>(alpha, thr, ef, en, npb, near);
-      if (lane == 0) s_mask[m & 3] = smask;
+      if (lane == 0) s_mask[m] = smask;
       publish(&s_cnt[0], m);
       const uint32_t bit = (smask >> (p & 31)) & 1u;
       if (active) {
@@ -1088,8 +1096,8 @@ __global__ __launch_bounds__(64 * (BW + 2)) void halve_pass_kernel(HalveArgs a) 
     if ((B) >= L::NSLOT) wait_at_least(&s_cnt[0], (B) - (L::NSLOT - 1));              \
     unsigned char* sb_ = slot(B);                                                      \
     _Pragma("unroll") for (int r_ = 0; r_ < 4; ++r_) {                                 \
-      sl_own(sb_)[(lane / QW + 8 * r_) * QW + lane % QW] = fo[K][r_];                  \
-      sl_next(sb_)[(lane / QW + 8 * r_) * QW + lane % QW] = fn[K][r_];                 \
+      sl_own(sb_)[(lane / QW + 8 * r_) * L::CW + lane % QW] = fo[K][r_];               \
+      sl_next(sb_)[(lane / QW + 8 * r_) * L::CW + lane % QW] = fn[K][r_];              \
     }                                                                                  \
     if (lane < BP) {                                                                   \
       sl_thr(sb_)[lane] = thr_;                                                        \
@@ -1111,54 +1119,89 @@ __global__ __launch_bounds__(64 * (BW + 2)) void halve_pass_kernel(HalveArgs a) 
 #undef PASS_STAGE
   } else {
     // ---- bulk updates, blocks 0 .. nblk-3 ----
-    // Chunk k of block B for bulk wave w = wave-2: pairs (B+2) BP + (w + k BW)
-    // 64 + lane (lanes past the last pair load the last pair's column).  The
-    // wave's chunks of all blocks form one stream, padded to whole turns of
-    // the NCB-slot register ring per block; every consumed slot is refilled
-    // at once with the next chunk of the stream, so NCB chunks are always in
-    // flight and every load is issued the same distance ahead of its use.
-#define PASS_FETCH_CHUNK(B, K, DST)                                                     \
-  do {                                                                                 \
-    const int b_ = min(B, nblk - 1);                                                   \
-    const int p_ = min((b_ + 2) * BP + (wave - 2 + (K) * BW) * 64 + lane, P - 1);      \
-    const u32x4* c_ = PASS_COL(b_, p_);                                                \
-    _Pragma("unroll") for (int q_ = 0; q_ < QW; ++q_) DST[q_] = c_[q_];                \
-  } while (0)
-    auto nk_of = [&](int B) {  // this wave's chunks of block B
-      const int first = (B + 2) * BP + (wave - 2) * 64;
-      return first < P ? (P - first + 64 * BW - 1) / (64 * BW) : 0;
+    // Bulk wave w = wave-2 owns the 64-pair chunks c = w, w + BW, ... of the
+    // bucket.  Row b (block b's signed scores) adds to the pairs of block
+    // b+2 on; the wave's items are (row, chunk) in row order, chunks from the
+    // one holding block b+2's first pair (its lanes before that pair, in
+    // block b+1, load but do not add).  The items form one stream held in an
+    // NCB-slot register ring: each consumed slot is refilled at once with the
+    // item NCB later, so the loads run ahead across rows whatever the
+    // decisions.  Lane l sums column l of the chunk in ascending order (the
+    // order of the decider's sums); with COAL the chunk is loaded a score
+    // tile (8 columns, 1 KiB) per instruction, 8 lanes to a column, and
+    // turned through the wave's LDS column buffer.  Entering row b the wave
+    // publishes b (rows completed); past its last item, nblk.
+    const int w = wave - 2;
+    const int nch = (P + 63) >> 6;
+    const int nrow = nblk - 2;
+    auto first_c = [&](int b) {  // this wave's first chunk in row b (>= nch: none)
+      const int c0 = (b + 2) >> 1;
+      return c0 + ((w - c0) % BW + BW) % BW;
     };
-    auto nkp_of = [&](int B) { return (nk_of(B) + NCB - 1) / NCB * NCB; };
-    int fb = 0, fk = 0;  // next chunk of the stream to load
+    int fb = 0, fc = first_c(0);  // next item to load
+    u32x4* colbuf = reinterpret_cast<u32x4*>(smem + L::colbuf_off(P) + (size_t)w * L::kColBuf);
     auto fetch_next = [&](u32x4* dst) {
-      while (fb + 2 < nblk && fk >= nkp_of(fb)) {
-        ++fb;
-        fk = 0;
+      const bool live = fb < nrow && fc < nch;
+      // COAL: word lane % QW of column 8 k + lane / QW of the chunk; else
+      // word k of column lane (past the stream's end: valid columns, never
+      // used)
+      if constexpr (L::COAL) {
+#pragma unroll
+        for (int k = 0; k < 8; ++k)
+          dst[k] = (live ? PASS_COL(fb, min(64 * fc + 8 * k + lane / QW, P - 1))
+                         : PASS_COL(0, lane / QW))[lane % QW];
+      } else {
+        const u32x4* c_ = live ? PASS_COL(fb, min(64 * fc + lane, P - 1)) : PASS_COL(0, 0);
+#pragma unroll
+        for (int k = 0; k < 8; ++k) dst[k] = c_[k];
       }
-      PASS_FETCH_CHUNK(fb, fk, dst);
-      ++fk;
+      if (live) {
+        fc += BW;
+        if (fc >= nch) fc = first_c(++fb);
+      }
     };
-    u32x4 cb[NCB][QW];
+    u32x4 cb[NCB][8];
 #pragma unroll
     for (int r = 0; r < NCB; ++r) fetch_next(cb[r]);
-    for (int b = 0; b + 2 < nblk; ++b) {
-      wait_at_least(&s_cnt[0], b);
-      const uint32_t smask = s_mask[b & 3];
-      const int nk = nk_of(b), nkp = nkp_of(b);
-      for (int k0 = 0; k0 < nkp; k0 += NCB) {
+    int b = 0, c = first_c(0);  // next item to use
+    int decided = -1;           // last decided block seen
+    bool more = nrow > 0 && c < nch;
+    // Every slot of a turn is used and refilled whether or not the stream
+    // has ended (loads past the end are of valid columns, nothing is added):
+    // all paths then issue the same loads, and the wait before a slot's use
+    // is for that slot's loads only.
+    while (more) {
 #pragma unroll
-        for (int r = 0; r < NCB; ++r) {
-          const int k = k0 + r;
-          float sum;
-          PASS_SUM(cb[r], smask, sum);
-          const int p = (b + 2) * BP + (wave - 2 + k * BW) * 64 + lane;
-          if (k < nk && p < P) s_alpha[p] += (double)sum;
-          fetch_next(cb[r]);
+      for (int r = 0; r < NCB; ++r) {
+        const bool live = more;
+        if (live && decided < b) decided = wait_at_least(&s_cnt[0], b);
+        const uint32_t smask = s_mask[min(b, nblk - 1)];
+        u32x4 col[QW];
+        if constexpr (L::COAL) {
+#pragma unroll
+          for (int k = 0; k < 8; ++k) colbuf[(8 * k + lane / QW) * L::CW + lane % QW] = cb[r][k];
+#pragma unroll
+          for (int q = 0; q < QW; ++q) col[q] = colbuf[lane * L::CW + q];
+        } else {
+#pragma unroll
+          for (int q = 0; q < QW; ++q) col[q] = cb[r][q];
+        }
+        float sum;
+        PASS_SUM(col, smask, sum);
+        const int p = 64 * c + lane;
+        if (live && p >= (b + 2) * BP && p < P) s_alpha[p] += (double)sum;
+        fetch_next(cb[r]);
+        if (live) {
+          c += BW;
+          if (c >= nch) {
+            c = first_c(++b);
+            more = b < nrow && c < nch;
+            if (more) publish(&s_cnt[2 + w], b);
+          }
         }
       }
-      __hip_atomic_fetch_add(&s_cnt[2 + (b & 3)], 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
     }
-#undef PASS_FETCH_CHUNK
+    publish(&s_cnt[2 + w], nblk);
   }
 #undef PASS_SUM
 #undef PASS_COL

@@ -2,6 +2,8 @@
 // kernel-halving round (KH(1/2) under kappa_att), one launch per round.
 #include <math.h>
 
+#include <algorithm>
+
 #include "common.hpp"
 #include "launch.hpp"
 
@@ -479,15 +481,44 @@ void pair_scores_kernel(HalveArgs a) {
   const int m16 = lane & 15;
   const int g = lane >> 4;
 
-  const int64_t bl = blockIdx.x;
-  const int64_t bucket = a.b0 + bl;
-  const int64_t s = bucket / a.G;
-  const int64_t t = bucket % a.G;
   const int N = a.N;
   const int P = N >> 1;
   const int NT = (N + 15) >> 4;
   const int nb = (N + 63) >> 6;
-  const int grp = blockIdx.y, chunk = blockIdx.z + a.chunk0;
+  // Workgroup -> (bucket, group, chunk).  Workgroups are dealt to the eight
+  // XCDs in turn (linear id mod 8); XCD x takes buckets x, x+8, ... in sets
+  // of il buckets whose workgroups are interleaved, set after set, so the
+  // workgroups that share a bucket's rows share one L2 and run close
+  // together.  A bucket's workgroups are its (group, chunk) pairs that have
+  // work, group by group (a workgroup with nothing to do would still take a
+  // dispatch slot).
+  int64_t bl;
+  int grp = 0, chunk = 0;
+  if constexpr (LOCAL) {
+    bl = blockIdx.x;
+  } else {
+    const int64_t id = blockIdx.x;
+    const int64_t k = id >> 3;
+    const int64_t per = (int64_t)a.ipb * a.il;
+    const int r_ = (int)(k % per);
+    bl = (id & 7) + 8 * ((k / per) * a.il + r_ % a.il);
+    if (bl >= a.nbk) return;
+    int item = r_ / a.il;
+    for (int g_ = 0; g_ < a.ngrp; ++g_) {
+      const int rest_ = NT - (g_ + 1) * GT;
+      const int nsc_ = rest_ > 0 ? (rest_ + a.ch - 1) / a.ch : 0;  // streamed chunks
+      const int cnt_ = max(0, min(a.chunk0 + a.nz, 1 + nsc_) - a.chunk0);
+      if (item < cnt_) {
+        grp = g_;
+        chunk = a.chunk0 + item;
+        break;
+      }
+      item -= cnt_;
+    }
+  }
+  const int64_t bucket = a.b0 + bl;
+  const int64_t s = bucket / a.G;
+  const int64_t t = bucket % a.G;
   const int gt0 = grp * GT;  // the group's first tile
   if (gt0 >= NT) return;
   const bool own = chunk == 0;
@@ -1222,6 +1253,12 @@ __global__ __launch_bounds__(64) void gram16_kernel(const T* rows, float* out) {
   for (int i = 0; i < 4; ++i) out[(4 * g + i) * 16 + m16] = acc[i];
 }
 
+// Buckets interleaved per XCD in a score launch (at most the XCD's share):
+// enough to stagger the workgroups' ends, few enough that their rows stay in
+// the XCD's L2.
+#ifndef SCORE_IL
+#define SCORE_IL 16
+#endif
 template <typename T, int D>
 hipError_t launch_scores_td(const HalveArgs& a, int64_t nbk, hipStream_t st) {
   using SS = ScoreShape<T, D>;
@@ -1236,23 +1273,34 @@ hipError_t launch_scores_td(const HalveArgs& a, int64_t nbk, hipStream_t st) {
   const int64_t groups = (NT + SS::GT - 1) / SS::GT;
   const int64_t rest = NT > SS::GT ? NT - SS::GT : 0;  // tiles after the first group
   const int64_t nch = 1 + (rest + a.ch - 1) / a.ch;
+  // one workgroup per (bucket, group, chunk) with work, buckets padded to a
+  // multiple of the eight XCDs (the padding workgroups return at once)
+  auto launch = [&](HalveArgs x, int chunk0, int nz) {
+    x.chunk0 = chunk0;
+    x.nz = nz;
+    x.ngrp = (int32_t)groups;
+    x.nbk = nbk;
+    int64_t ipb = 0;
+    for (int64_t g = 0; g < groups; ++g) {
+      const int64_t rest_g = NT - (g + 1) * SS::GT;
+      const int64_t nsc = rest_g > 0 ? (rest_g + a.ch - 1) / a.ch : 0;
+      ipb += std::max<int64_t>(0, std::min<int64_t>(chunk0 + nz, 1 + nsc) - chunk0);
+    }
+    x.ipb = (int32_t)ipb;
+    x.il = (int32_t)std::min<int64_t>(SCORE_IL, (nbk + 7) / 8);
+    const int64_t per_xcd = ((nbk + 7) / 8 + x.il - 1) / x.il * x.il;
+    const int64_t wgs = 8 * per_xcd * ipb;
+    hipLaunchKernelGGL(kern, dim3((unsigned)wgs), dim3(64 * kScoreWaves), lds, st, x);
+  };
   if (a.rowh2_write && nch > 1) {
     // the streamed chunks read the row scales the own chunks write: two launches
-    HalveArgs own = a;
-    own.chunk0 = 0;
-    hipLaunchKernelGGL(kern, dim3((unsigned)nbk, (unsigned)groups, 1u), dim3(64 * kScoreWaves), lds, st,
-                       own);
+    launch(a, 0, 1);
     HalveArgs rest_a = a;
-    rest_a.chunk0 = 1;
     rest_a.rowh2_write = 0;
-    hipLaunchKernelGGL(kern, dim3((unsigned)nbk, (unsigned)groups, (unsigned)(nch - 1)),
-                       dim3(64 * kScoreWaves), lds, st, rest_a);
+    launch(rest_a, 1, (int)(nch - 1));
     return hipGetLastError();
   }
-  HalveArgs one = a;
-  one.chunk0 = 0;
-  dim3 grid((unsigned)nbk, (unsigned)groups, (unsigned)nch);
-  hipLaunchKernelGGL(kern, grid, dim3(64 * kScoreWaves), lds, st, one);
+  launch(a, 0, (int)nch);
   return hipGetLastError();
 }
 

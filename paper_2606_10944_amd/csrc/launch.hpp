@@ -32,6 +32,11 @@ struct HalveArgs {
   float* rowh2;               // [S, n] scale exponent of every row, written by the first round
   int32_t rowh2_write;        // this round writes rowh2 (and reads it only after writing)
   int32_t chunk0;             // first column chunk of a score launch (set by launch_scores)
+  int32_t nz;                 // column chunks per group in a score launch (set by launch_scores)
+  int32_t ngrp;               // row groups per bucket (set by launch_scores)
+  int64_t nbk;                // buckets of a score launch (set by launch_scores)
+  int32_t ipb;                // score workgroups per bucket in a launch (set by launch_scores)
+  int32_t il;                 // buckets interleaved per XCD in a score launch (set by launch_scores)
 };
 
 // dtype: 0 = fp32, 1 = bf16.  Returns a hipError_t.

@@ -313,10 +313,16 @@ __device__ __forceinline__ void frag_pair_terms(const uint4* fk, const uint4* fv
   const double t2 = (double)__builtin_amdgcn_exp2f((float)(exp_ * kLog2e - h2)) * (svp + vm2d);
   const double t3 = (double)__builtin_amdgcn_exp2f((float)(exx * kLog2e - h2)) * (cv + vm2d);
   const double bt2 = t1 + t2 - 2.0 * t3;
-  if (bt2 >= 1e-30)
+  if (bt2 >= 1e-30) {
     lbt = (float)(0.5 * kLn2) * __builtin_amdgcn_logf((float)bt2);
-  else
-    lbt = bt2 > 0.0 ? (float)(0.5 * log(bt2)) : -INFINITY;
+  } else if (bt2 > 0.0) {
+    // below float range: bt2 = m 2^e (hardware frexp), log2 bt2 = log2 m + e
+    const float m = (float)__builtin_amdgcn_frexp_mant(bt2);
+    const int e = __builtin_amdgcn_frexp_exp(bt2);
+    lbt = (float)(0.5 * kLn2) * (__builtin_amdgcn_logf(m) + (float)e);
+  } else {
+    lbt = -INFINITY;
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -702,6 +708,7 @@ void pair_scores_kernel(HalveArgs a) {
   // of the row tile against column row m16.  With F = kappa(y'_i, .) -
   // kappa(y_i, .), the even lane of a column pair forms E(2g, p) =
   // F0 - F0(partner) and the odd lane E(2g+1, p) = F1(partner) - F1.
+  const int epi_lane = (m16 >> 1) * kETileStride + 2 * g + (m16 & 1);
 #define SCORE_EPI_H(H, H2, BUF)                                                         \
   do {                                                                                 \
     float* eb_ = LOCAL ? s_e + (panel_tiles(hb_blk[H], NT, 4) + jt_ - 4 * hb_blk[H]) * kETileLds \
@@ -715,7 +722,7 @@ void pair_scores_kernel(HalveArgs a) {
       const float F1 = kap[3] - kap[2];                                                \
       const float mine_ = odd ? F1 : F0;                                               \
       const float other_ = from_partner(odd ? F0 : F1);                                \
-      eb_[(m16 >> 1) * kETileStride + hb_half[H] * 16 + rt * 8 + 2 * g + (m16 & 1)] =  \
+      eb_[epi_lane + hb_half[H] * 16 + rt * 8] =                                       \
           odd ? other_ - mine_ : mine_ - other_;                                       \
     }                                                                                  \
   } while (0)

@@ -471,7 +471,9 @@ __device__ __align__(16) float g_score_sink[256];
 // one workgroup per bucket computes the bucket's scores into LDS (its own
 // chunk is the whole bucket), then wave 0 takes the decisions from LDS with
 // the same arithmetic as halve_pass_kernel (the scores never leave the CU).
-template <typename T, int D, bool LOCAL>
+// OWN_ONLY: a launch of own chunks only (no streamed code, so the register
+// budget allows the own tiles to be software-pipelined as the streamed ones).
+template <typename T, int D, bool LOCAL, bool OWN_ONLY>
 __global__ __launch_bounds__(64 * kScoreWaves) __attribute__((amdgpu_waves_per_eu(2)))
 void pair_scores_kernel(HalveArgs a) {
   using SS = ScoreShape<T, D>;
@@ -527,7 +529,7 @@ void pair_scores_kernel(HalveArgs a) {
   const int64_t t = bucket % a.G;
   const int gt0 = grp * GT;  // the group's first tile
   if (gt0 >= NT) return;
-  const bool own = chunk == 0;
+  const bool own = OWN_ONLY || chunk == 0;
   const int jt0 = own ? gt0 : gt0 + GT + (chunk - 1) * a.ch;
   if (jt0 >= NT) return;
   const int jt1 = min(jt0 + (own ? GT : a.ch), NT);
@@ -803,6 +805,27 @@ void pair_scores_kernel(HalveArgs a) {
     __syncthreads();                                                                   \
   } while (0)
 
+  // Own tiles with two half-block slots (own-only launches), pipelined the
+  // same way; a slot's MFMAs and epilogue are skipped before its block's
+  // diagonal tile.
+#define SCORE_TILE_OP(I, U, FIRST)                                                      \
+  do {                                                                                 \
+    const int i_ = (I);                                                                \
+    const int jt_ = jt0 + i_;                                                          \
+    if (i_ >= 2) SCORE_FLUSH(true, i_ - 2, ((U) + 1) % NS);                            \
+    if (i_ + 2 < ntile) SCORE_OWN_COMMIT(((U) + 2) % NS, i_ + 2);                      \
+    SCORE_BFRAG((U) % NS);                                                             \
+    const float h2c_ = jt_ * 16 + m16 >= N ? 0.0f : s_h2[i_ * 16 + m16];               \
+    if (SCORE_ACTIVE(true, 0, jt_)) SCORE_MMA_H(0);                                    \
+    if (!(FIRST) && SCORE_ACTIVE(true, 1, jt_ - 1)) SCORE_EPI_H(1, h2_prev, ((U) + NS - 1) % NS); \
+    SCORE_INTERLEAVE();                                                                \
+    if (SCORE_ACTIVE(true, 1, jt_)) SCORE_MMA_H(1);                                    \
+    if (SCORE_ACTIVE(true, 0, jt_)) SCORE_EPI_H(0, h2c_, (U) % NS);                    \
+    SCORE_INTERLEAVE();                                                                \
+    h2_prev = h2c_;                                                                    \
+    __syncthreads();                                                                   \
+  } while (0)
+
   // LOCAL: the decisions of the bucket's P <= 32 NBW pairs from the scores
   // in LDS (wave 0).  Block m: thresholds as in halve_pass_kernel; alpha =
   // the float32 signed sums of every earlier block, added in block order in
@@ -852,17 +875,33 @@ void pair_scores_kernel(HalveArgs a) {
     SCORE_OWN_COMMIT(0, 0);
     if (ntile > 1) SCORE_OWN_COMMIT(1, 1);
     __syncthreads();
-    for (int ib = 0; ib < ntile; ib += DEPTH) {
+    if constexpr (OWN_ONLY && !LOCAL && HB == 2) {
+      for (int ib = 0; ib < ntile; ib += DEPTH) {
 #pragma unroll
-      for (int u = 0; u < DEPTH; ++u)
-        if (ib + u < ntile) SCORE_TILE(true, ib + u, u);  // uniform over the workgroup
+        for (int u = 0; u < DEPTH; ++u)
+          if (ib + u < ntile) SCORE_TILE_OP(ib + u, u, ib + u == 0);  // uniform over the workgroup
+      }
+      const int last = ntile - 1;
+      {
+        const int jt_ = jt0 + last;
+        if (SCORE_ACTIVE(true, 1, jt_)) SCORE_EPI_H(1, h2_prev, last % NS);
+      }
+      __syncthreads();
+      if (last >= 1) SCORE_FLUSH(true, last - 1, (last - 1) % NS);
+      SCORE_FLUSH(true, last, last % NS);
+    } else {
+      for (int ib = 0; ib < ntile; ib += DEPTH) {
+#pragma unroll
+        for (int u = 0; u < DEPTH; ++u)
+          if (ib + u < ntile) SCORE_TILE(true, ib + u, u);  // uniform over the workgroup
+      }
+      SCORE_FLUSH(true, ntile - 1, (ntile - 1) % NS);
     }
-    SCORE_FLUSH(true, ntile - 1, (ntile - 1) % NS);
     if constexpr (LOCAL) {
       __syncthreads();
       if (wave == 0) local_decisions();
     }
-  } else if constexpr (!LOCAL) {
+  } else if constexpr (!LOCAL && !OWN_ONLY) {
 #pragma unroll
     for (int k = 0; k < DEPTH; ++k) SCORE_ISSUE(jt0 + k, k);
     SCORE_COMMIT(0, 0);
@@ -904,6 +943,7 @@ void pair_scores_kernel(HalveArgs a) {
   }
 #undef SCORE_TILE
 #undef SCORE_TILE_P
+#undef SCORE_TILE_OP
 #undef SCORE_INTERLEAVE
 #undef SCORE_FLUSH
 #undef SCORE_EPI_H
@@ -1269,12 +1309,14 @@ __global__ __launch_bounds__(64) void gram16_kernel(const T* rows, float* out) {
 template <typename T, int D>
 hipError_t launch_scores_td(const HalveArgs& a, int64_t nbk, hipStream_t st) {
   using SS = ScoreShape<T, D>;
-  auto kern = pair_scores_kernel<T, D, false>;
+  auto kern_mixed = pair_scores_kernel<T, D, false, false>;
+  auto kern_own = pair_scores_kernel<T, D, false, true>;
   const size_t lds = SS::LDS;
   if (lds > 64 * 1024) {
-    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-    if (e != hipSuccess) return e;
+    for (const void* k : {reinterpret_cast<const void*>(kern_mixed), reinterpret_cast<const void*>(kern_own)}) {
+      hipError_t e = hipFuncSetAttribute(k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+      if (e != hipSuccess) return e;
+    }
   }
   const int64_t NT = (a.N + 15) / 16;
   const int64_t groups = (NT + SS::GT - 1) / SS::GT;
@@ -1297,7 +1339,11 @@ hipError_t launch_scores_td(const HalveArgs& a, int64_t nbk, hipStream_t st) {
     x.il = (int32_t)std::min<int64_t>(SCORE_IL, (nbk + 7) / 8);
     const int64_t per_xcd = ((nbk + 7) / 8 + x.il - 1) / x.il * x.il;
     const int64_t wgs = 8 * per_xcd * ipb;
-    hipLaunchKernelGGL(kern, dim3((unsigned)wgs), dim3(64 * kScoreWaves), lds, st, x);
+    // a launch of own chunks only takes the own-only instantiation
+    if (chunk0 == 0 && nz == 1)
+      hipLaunchKernelGGL(kern_own, dim3((unsigned)wgs), dim3(64 * kScoreWaves), lds, st, x);
+    else
+      hipLaunchKernelGGL(kern_mixed, dim3((unsigned)wgs), dim3(64 * kScoreWaves), lds, st, x);
   };
   if (a.rowh2_write && nch > 1) {
     // the streamed chunks read the row scales the own chunks write: two launches
@@ -1314,7 +1360,7 @@ hipError_t launch_scores_td(const HalveArgs& a, int64_t nbk, hipStream_t st) {
 template <typename T, int D>
 hipError_t launch_local_td(const HalveArgs& a0, int64_t nbk, hipStream_t st) {
   using SS = ScoreShape<T, D>;
-  auto kern = pair_scores_kernel<T, D, true>;
+  auto kern = pair_scores_kernel<T, D, true, true>;
   const int64_t NT = (a0.N + 15) / 16, nb = (a0.N + 63) / 64, P = a0.N / 2;
   const size_t lds = (size_t)kScoreStages * SS::CHUNKS * 1024 +
                      (size_t)panel_tiles(nb, NT, 4) * kETileLds * 4 + SS::GT * 16 * 4 +

@@ -119,6 +119,48 @@ int thin_compress_traced(const void* K, const void* V, int32_t dtype, int64_t B,
                          int64_t trace_len, void* stream);
 
 /*
+ * Halving algorithm of thin_compress_ex.
+ *   THIN_HALVE_KH       kernel halving KH(delta) under kappa_att (App. A,
+ *                       Algorithm A.1), as in thin_compress.
+ *   THIN_HALVE_UNIFORM  every pair keeps one of its two rows with
+ *                       probability 1/2: the second iff u_i < 1/2.  No kernel
+ *                       is evaluated; this is the rule KH applies to a pair
+ *                       whose threshold a_i is 0, and the simplest base
+ *                       halving the construction accepts (Sec. 5: any halving
+ *                       algorithm can be used).
+ */
+typedef enum { THIN_HALVE_KH = 0, THIN_HALVE_UNIFORM = 1 } thin_halve_t;
+
+/*
+ * Options of thin_compress_ex; {THIN_HALVE_KH, NULL} gives thin_compress.
+ *   halve   a thin_halve_t.
+ *   delta   (host, nullable) float64 [plan.rounds]: the failure probability
+ *           of every KH call of round r (its threshold carries the factor
+ *           1/2 + log(2 N_r / delta[r]), App. A), each in (0, 1]; read during
+ *           the call only.  NULL = 1/2 for every round (App. I).  Ignored by
+ *           THIN_HALVE_UNIFORM.
+ */
+typedef struct {
+  int32_t halve;
+  const double* delta;
+} thin_compress_opts_t;
+
+/*
+ * thin_compress with a choice of halving algorithm and of KH's delta per
+ * round.  Same arguments, uniforms layout (the pair draws of a round are
+ * consumed the same way by either algorithm), workspace and level structure
+ * as thin_compress; opts (host) must not be NULL.  swap_trace (device,
+ * nullable): as in thin_compress_traced, with trace_len >= B*H*U when given.
+ * Errors: those of thin_compress, and THIN_EINVAL for an unknown halve or a
+ * delta[r] outside (0, 1].
+ */
+int thin_compress_ex(const void* K, const void* V, int32_t dtype, int64_t B, int64_t H,
+                     int64_t n, int64_t d, int64_t n_out, int32_t g, const float* uniforms,
+                     int64_t n_uniforms, int32_t* idx_out, void* workspace,
+                     size_t workspace_bytes, const thin_compress_opts_t* opts,
+                     uint8_t* swap_trace, int64_t trace_len, void* stream);
+
+/*
  * Attention of every query over its slice's coreset (Sec. 2.1 eq.
  * unmaskedatt restricted to the coreset; eq. def:att_approx with equal
  * weights, which cancel):
@@ -148,14 +190,16 @@ const char* thin_status_str(int status);
 
 /*
  * Launch observer, for tracing and per-kernel timing.  While a hook is set,
- * every kernel launch made by thin_compress, thin_compress_traced and
- * thin_attention is bracketed by two calls on the calling thread:
+ * every kernel launch made by thin_compress, thin_compress_traced,
+ * thin_compress_ex and thin_attention is bracketed by two calls on the
+ * calling thread:
  * hook(ctx, kernel, round, 0, stream) right before the launch is enqueued and
  * hook(ctx, kernel, round, 1, stream) right after.  The hook may enqueue
  * stream-ordered work of its own (for instance record an event on `stream`),
  * so that consecutive records time one kernel.  `kernel` is a
  * thin_kernel_t, `round` the Halve round 0..L-1 of a THIN_KERNEL_SCORES,
- * THIN_KERNEL_DECIDE or THIN_KERNEL_LOCAL launch and -1 otherwise.  A round
+ * THIN_KERNEL_DECIDE, THIN_KERNEL_LOCAL or THIN_KERNEL_UNIFORM launch and -1
+ * otherwise.  A round
  * runs either as SCORES + DECIDE launches or, when its buckets are small
  * enough for one workgroup to hold all their scores in LDS, as one LOCAL
  * launch.  The setting is process-wide:
@@ -170,7 +214,8 @@ typedef enum {
   THIN_KERNEL_SCORES = 4,      /* pair scores of one round                */
   THIN_KERNEL_DECIDE = 5,      /* decision pass of one round              */
   THIN_KERNEL_ATTENTION = 6,   /* coreset attention                       */
-  THIN_KERNEL_LOCAL = 7        /* scores and decisions of one round        */
+  THIN_KERNEL_LOCAL = 7,       /* scores and decisions of one round       */
+  THIN_KERNEL_UNIFORM = 8      /* one round of uniform halving            */
 } thin_kernel_t;
 typedef void (*thin_launch_hook_t)(void* ctx, int32_t kernel, int32_t round, int32_t phase,
                                    void* stream);

@@ -78,6 +78,11 @@ def lib():
         L.or_compress.argtypes = [P, P, C.c_int64, C.c_int64, C.c_int64, C.c_int32, C.c_int, P,
                                   P, P, C.c_double, P, P, C.POINTER(Stats)]
         L.or_compress.restype = C.c_int
+        L.or_compress_ex.argtypes = [P, P, C.c_int64, C.c_int64, C.c_int64, C.c_int32, C.c_int,
+                                     C.c_int, P, P, P, P, C.c_double, P, P, C.POINTER(Stats)]
+        L.or_compress_ex.restype = C.c_int
+        L.or_uniform_halving.argtypes = [P, C.c_int64, P, P, P, C.POINTER(Stats)]
+        L.or_uniform_halving.restype = C.c_int
         L.or_attention.argtypes = [P, P, P, C.c_int64, C.c_int64, P, C.c_int64, P]
         L.or_attention.restype = None
         _lib = L
@@ -148,9 +153,28 @@ def kernel_halving(K, V, rows, u, *, vmax2_value: Optional[float] = None,
             "stats": st.as_dict()}
 
 
+HALVES = {"kh": 0, "uniform": 1}
+
+
+def uniform_halving(rows, u) -> dict:
+    """One bucket: pair i keeps rows[2i+1] iff u[i] < 1/2, else rows[2i]."""
+    rows = np.ascontiguousarray(rows, dtype=np.int32)
+    u = _f32(u)
+    N = rows.size
+    out = np.empty(N // 2, dtype=np.int32)
+    bits = np.zeros(N // 2, dtype=np.uint8)
+    st = Stats()
+    rc = lib().or_uniform_halving(_p(rows), N, _p(u), _p(out), _p(bits), C.byref(st))
+    if rc != 0:
+        raise ValueError(f"or_uniform_halving failed ({rc})")
+    return {"out": out, "bits": bits, "stats": st.as_dict()}
+
+
 def compress(K, V, n_out: int, g: int, U, *, kernel: str = "katt", follow=None,
-             tol: float = 1e-5) -> dict:
-    """One slice: K, V [n, d]; U = this slice's uniforms."""
+             tol: float = 1e-5, halve: str = "kh", delta=None) -> dict:
+    """One slice: K, V [n, d]; U = this slice's uniforms.  halve: "kh" (KH(delta),
+    delta[r] per round, default 1/2) or "uniform" (one point of each pair, each
+    with probability 1/2)."""
     K, V = _f64(K), _f64(V)
     n, d = K.shape
     pl = plan(n, n_out, g)
@@ -166,10 +190,15 @@ def compress(K, V, n_out: int, g: int, U, *, kernel: str = "katt", follow=None,
     if fol is not None:
         assert fol.size >= pl["uniforms"]
     st = Stats()
-    rc = lib().or_compress(_p(K), _p(V), n, d, n_out, g, KERNELS[kernel], _p(U), _p(idx),
-                           _p(fol), tol, _p(bits), _p(rho), C.byref(st))
+    dl = None
+    if delta is not None:
+        dl = np.ascontiguousarray(delta, dtype=np.float64)
+        assert dl.size >= pl["rounds"]
+    rc = lib().or_compress_ex(_p(K), _p(V), n, d, n_out, g, KERNELS[kernel], HALVES[halve],
+                              _p(dl), _p(U), _p(idx), _p(fol), tol, _p(bits), _p(rho),
+                              C.byref(st))
     if rc != 0:
-        raise ValueError(f"or_compress failed ({rc})")
+        raise ValueError(f"or_compress_ex failed ({rc})")
     return {"idx": idx, "bits": bits, "rho": rho, "stats": st.as_dict(), "plan": pl}
 
 

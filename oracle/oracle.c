@@ -188,6 +188,28 @@ int or_kernel_halving(const double* K, const double* V, int64_t d, double vmax2,
   return 0;
 }
 
+/*
+ * Uniform halving: each pair (x, x') = (y_{2i-1}, y_{2i}) keeps one of its
+ * two points with probability 1/2, the second iff u_i < 1/2.  It uses no
+ * kernel: the simplest of the base halving algorithms the streaming
+ * construction admits (Sec. 5, Conclusion: any halving algorithm), and the
+ * rule KH(delta) applies to a pair whose threshold a_i is 0.
+ */
+int or_uniform_halving(const int32_t* rows, int64_t N, const float* u, int32_t* out,
+                       uint8_t* bits, or_stats_t* st) {
+  if (N < 2 || (N % 2) != 0) return -1;
+  for (int64_t i = 0; i < N / 2; ++i) {
+    int swap = u[i] < 0.5f;
+    out[i] = rows[2 * i + swap];
+    if (bits) bits[i] = (uint8_t)swap;
+    if (st) {
+      st->decisions++;
+      st->swaps += swap;
+    }
+  }
+  return 0;
+}
+
 /* ------------------------------------------------------------------ */
 /* Compress.                                                           */
 /* ------------------------------------------------------------------ */
@@ -204,14 +226,23 @@ typedef struct {
   uint8_t* bits;
   double* rho;
   or_stats_t* st;
+  int halve;            /* OR_HALVE_KH or OR_HALVE_UNIFORM */
+  const double* delta;  /* KH failure probability per round, or NULL = 1/2 */
+  int32_t round;        /* round of the calls being made */
 } cctx_t;
 
 static int halve_group(cctx_t* c, const int32_t* rows, int64_t N, int32_t* out) {
   int64_t o = c->upos;
-  int rc = or_kernel_halving(c->K, c->V, c->d, c->vmax2, c->kernel, 0.5, rows, N, c->U + o,
-                             out, c->follow ? c->follow + o : NULL, c->tol,
-                             c->bits ? c->bits + o : NULL, c->rho ? c->rho + o : NULL,
-                             NULL, NULL, c->st);
+  int rc;
+  if (c->halve == OR_HALVE_UNIFORM) {
+    rc = or_uniform_halving(rows, N, c->U + o, out, c->bits ? c->bits + o : NULL, c->st);
+  } else {
+    const double delta = c->delta ? c->delta[c->round] : 0.5;
+    rc = or_kernel_halving(c->K, c->V, c->d, c->vmax2, c->kernel, delta, rows, N, c->U + o,
+                           out, c->follow ? c->follow + o : NULL, c->tol,
+                           c->bits ? c->bits + o : NULL, c->rho ? c->rho + o : NULL, NULL,
+                           NULL, c->st);
+  }
   c->upos += N / 2;
   return rc;
 }
@@ -231,6 +262,7 @@ static int compress2(cctx_t* c, int32_t m, int32_t* rows, int64_t n_in, int32_t*
     if (rc) return rc;
   }
   memcpy(rows, tmp, sizeof(int32_t) * (size_t)(n_in / 2));
+  c->round++;
   return compress2(c, m - 1, rows, n_in / 2, tmp);
 }
 
@@ -238,6 +270,14 @@ int or_compress(const double* K, const double* V, int64_t n, int64_t d, int64_t 
                 int32_t g, int kernel, const float* U, int32_t* idx_out,
                 const uint8_t* follow, double tol, uint8_t* bits, double* rho,
                 or_stats_t* st) {
+  return or_compress_ex(K, V, n, d, n_out, g, kernel, OR_HALVE_KH, NULL, U, idx_out, follow,
+                        tol, bits, rho, st);
+}
+
+int or_compress_ex(const double* K, const double* V, int64_t n, int64_t d, int64_t n_out,
+                   int32_t g, int kernel, int halve, const double* delta, const float* U,
+                   int32_t* idx_out, const uint8_t* follow, double tol, uint8_t* bits,
+                   double* rho, or_stats_t* st) {
   or_plan_t plan;
   if (or_plan(n, n_out, g, &plan) != 0) return -1;
   int32_t* rows = (int32_t*)malloc(sizeof(int32_t) * (size_t)n);
@@ -247,7 +287,13 @@ int or_compress(const double* K, const double* V, int64_t n, int64_t d, int64_t 
     free(tmp);
     return -2;
   }
-  cctx_t c = {K, V, d, or_vmax2(V, n, d), kernel, U, 0, follow, tol, bits, rho, st};
+  if (halve != OR_HALVE_KH && halve != OR_HALVE_UNIFORM) {
+    free(rows);
+    free(tmp);
+    return -1;
+  }
+  cctx_t c = {K, V, d, halve == OR_HALVE_KH ? or_vmax2(V, n, d) : 0.0, kernel, U, 0, follow,
+              tol, bits, rho, st, halve, delta, 0};
   int64_t cur = n;
   if (plan.subsample) {
     or_subsample(n, plan.n_kept, U, rows);
@@ -259,6 +305,7 @@ int or_compress(const double* K, const double* V, int64_t n, int64_t d, int64_t 
   int rc = compress2(&c, plan.compress_levels, rows, cur, tmp);
   cur >>= plan.compress_levels;
   for (int32_t r = plan.compress_levels; rc == 0 && r < plan.rounds; ++r) {
+    c.round = r;
     rc = halve_group(&c, rows, cur, tmp);
     memcpy(rows, tmp, sizeof(int32_t) * (size_t)(cur / 2));
     cur /= 2;

@@ -75,6 +75,24 @@ int or_compress(const double* K, const double* V, int64_t n, int64_t d,
                 int32_t* idx_out, const uint8_t* follow, double tol,
                 uint8_t* bits, double* rho, or_stats_t* st);
 
+/* Halving algorithm of a compress call. */
+#define OR_HALVE_KH 0      /* KH(delta), App. A Algorithm A.1 */
+#define OR_HALVE_UNIFORM 1 /* one point of each pair, each with probability 1/2 */
+
+/* Uniform halving of one bucket: out[i] = rows[2i + (u[i] < 1/2)]. */
+int or_uniform_halving(const int32_t* rows, int64_t N, const float* u, int32_t* out,
+                       uint8_t* bits, or_stats_t* st);
+
+/*
+ * or_compress with a choice of halving algorithm and, for KH, the failure
+ * probability delta[r] of every call of round r (delta NULL = 1/2).  Round r
+ * counts the halving rounds from 0 as in or_plan.
+ */
+int or_compress_ex(const double* K, const double* V, int64_t n, int64_t d,
+                   int64_t n_out, int32_t g, int kernel, int halve, const double* delta,
+                   const float* U, int32_t* idx_out, const uint8_t* follow, double tol,
+                   uint8_t* bits, double* rho, or_stats_t* st);
+
 /* O[q] = sum_j exp(<Q_q,K_rows[j]>/sqrt d) V_rows[j] / sum_j exp(...), j < m. */
 void or_attention(const double* Q, const double* K, const double* V, int64_t n_q,
                   int64_t d, const int32_t* rows, int64_t m, double* O);

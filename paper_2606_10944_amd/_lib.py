@@ -21,12 +21,13 @@ THIN_OK, THIN_EINVAL, THIN_EDTYPE, THIN_EUNIFORMS, THIN_EWORKSPACE, THIN_EHIP = 
 THIN_FP32, THIN_BF16 = 0, 1
 
 # Every symbol include/thin.h declares.
-EXPORTS = ("thin_plan", "thin_compress", "thin_compress_traced", "thin_attention",
+EXPORTS = ("thin_plan", "thin_compress", "thin_compress_traced", "thin_compress_ex", "thin_attention",
            "thin_selftest_gram16", "thin_status_str", "thin_set_launch_hook")
 
 # thin_kernel_t
 KERNEL_NAMES = {0: "trace_clear", 1: "subsample", 2: "fill", 3: "vmax", 4: "scores",
-                5: "decide", 6: "attention", 7: "local"}
+                5: "decide", 6: "attention", 7: "local", 8: "uniform"}
+HALVE = {"kh": 0, "uniform": 1}  # thin_halve_t
 LaunchHook = C.CFUNCTYPE(None, C.c_void_p, C.c_int32, C.c_int32, C.c_int32, C.c_void_p)
 
 
@@ -34,6 +35,10 @@ class ThinError(RuntimeError):
     def __init__(self, status: int, where: str):
         self.status = status
         super().__init__(f"{where}: {thin_status_str(status)} (status {status})")
+
+
+class CompressOpts(C.Structure):
+    _fields_ = [("halve", C.c_int32), ("delta", C.c_void_p)]
 
 
 class Plan(C.Structure):
@@ -64,14 +69,16 @@ def lib():
     L.thin_compress.argtypes = [P, P, I32, I64, I64, I64, I64, I64, I32, P, I64, P, P, SZ, P]
     L.thin_compress_traced.argtypes = [P, P, I32, I64, I64, I64, I64, I64, I32, P, I64, P, P,
                                        SZ, P, I64, P]
+    L.thin_compress_ex.argtypes = [P, P, I32, I64, I64, I64, I64, I64, I32, P, I64, P, P, SZ,
+                                   C.POINTER(CompressOpts), P, I64, P]
     L.thin_attention.argtypes = [P, P, P, I32, I64, I64, I64, I64, I64, P, I64, P, I32, P]
     L.thin_selftest_gram16.argtypes = [I32, I64, P, P, P]
     L.thin_status_str.argtypes = [C.c_int]
     L.thin_status_str.restype = C.c_char_p
     L.thin_set_launch_hook.argtypes = [LaunchHook, P]
     L.thin_set_launch_hook.restype = C.c_int
-    for f in ("thin_plan", "thin_compress", "thin_compress_traced", "thin_attention",
-              "thin_selftest_gram16"):
+    for f in ("thin_plan", "thin_compress", "thin_compress_traced", "thin_compress_ex",
+              "thin_attention", "thin_selftest_gram16"):
         getattr(L, f).restype = C.c_int
     _lib = L
     return L
@@ -119,9 +126,11 @@ def _shape4(t: torch.Tensor, name: str) -> Tuple[int, int, int, int]:
 def thin_compress(K: torch.Tensor, V: torch.Tensor, n_out: int, g: int,
                   uniforms: torch.Tensor, *, idx_out: Optional[torch.Tensor] = None,
                   workspace: Optional[torch.Tensor] = None, trace: bool = False,
-                  stream=None):
-    """Kernel-halving compress of every slice; returns idx [B,H,n_out] int32
-    (and the uint8 swap trace when trace=True)."""
+                  halve: str = "kh", delta=None, stream=None):
+    """Compress of every slice; returns idx [B,H,n_out] int32 (and the uint8
+    swap trace when trace=True).  halve="kh" (kernel halving, KH's delta per
+    round in `delta`, default 1/2) or "uniform"; anything but the defaults
+    goes through thin_compress_ex."""
     B, H, n, d = _shape4(K, "K")
     if tuple(V.shape) != (B, H, n, d) or V.dtype != K.dtype or not V.is_contiguous():
         raise ThinError(THIN_EINVAL, "V must match K")
@@ -136,6 +145,21 @@ def thin_compress(K: torch.Tensor, V: torch.Tensor, n_out: int, g: int,
     tr = None
     args = [_ptr(K), _ptr(V), _dtype_code(K.dtype), B, H, n, d, n_out, g, _ptr(uniforms),
             uniforms.numel(), _ptr(idx_out), _ptr(workspace), workspace.numel()]
+    if halve != "kh" or delta is not None:
+        if halve not in HALVE:
+            raise ThinError(THIN_EINVAL, f"unknown halving {halve!r}")
+        dl = None
+        if delta is not None:
+            dl = (C.c_double * max(len(delta), 1))(*[float(x) for x in delta])
+            if len(delta) < plan["rounds"]:
+                raise ThinError(THIN_EINVAL, "delta needs one value per round")
+        opts = CompressOpts(HALVE[halve], C.cast(dl, C.c_void_p) if dl is not None else None)
+        if trace:
+            tr = torch.empty(max(plan["uniforms_total"], 1), dtype=torch.uint8, device=dev)
+        rc = lib().thin_compress_ex(*args, C.byref(opts), _ptr(tr) if trace else None,
+                                    tr.numel() if trace else 0, _stream(stream))
+        _check(rc, "thin_compress_ex")
+        return (idx_out, tr[: plan["uniforms_total"]]) if trace else idx_out
     if trace:
         tr = torch.empty(max(plan["uniforms_total"], 1), dtype=torch.uint8, device=dev)
         rc = lib().thin_compress_traced(*args, _ptr(tr), tr.numel(), _stream(stream))

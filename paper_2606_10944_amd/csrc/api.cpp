@@ -148,7 +148,7 @@ int check_shape(int64_t B, int64_t H, int64_t n, int64_t d) {
 int compress_impl(const void* K, const void* V, int32_t dtype, int64_t B, int64_t H, int64_t n,
                   int64_t d, int64_t n_out, int32_t g, const float* uniforms, int64_t n_uniforms,
                   int32_t* idx_out, void* workspace, size_t workspace_bytes, uint8_t* trace,
-                  int64_t trace_len, void* stream) {
+                  int64_t trace_len, int32_t halve, const double* delta, void* stream) {
   int rc = check_shape(B, H, n, d);
   if (rc) return rc;
   if (dtype != THIN_FP32 && dtype != THIN_BF16) return THIN_EDTYPE;
@@ -160,6 +160,10 @@ int compress_impl(const void* K, const void* V, int32_t dtype, int64_t B, int64_
   if (Utot > 0 && !uniforms) return THIN_EINVAL;
   if (n_uniforms < Utot) return THIN_EUNIFORMS;
   if (trace && trace_len < Utot) return THIN_EINVAL;
+  if (halve != THIN_HALVE_KH && halve != THIN_HALVE_UNIFORM) return THIN_EINVAL;
+  if (halve == THIN_HALVE_KH && delta)
+    for (int32_t r = 0; r < lv.L; ++r)
+      if (!(delta[r] > 0.0 && delta[r] <= 1.0)) return THIN_EINVAL;
   if (!workspace || workspace_bytes < workspace_size(S, d, lv)) return THIN_EWORKSPACE;
   if ((reinterpret_cast<uintptr_t>(workspace) & 255u) != 0) return THIN_EWORKSPACE;
   Workspace ws = carve(workspace, S, d, lv);
@@ -181,6 +185,17 @@ int compress_impl(const void* K, const void* V, int32_t dtype, int64_t B, int64_
     ok(observed(THIN_KERNEL_FILL, -1, st, [&] {
       return thin::launch_fill_rows(S, n_out, cur, lv.n_kept, idx_out, st);
     }));
+  } else if (halve == THIN_HALVE_UNIFORM) {
+    int64_t u_off = lv.sub ? lv.n_kept : 0;
+    for (int32_t r = 0; r < lv.L && e == hipSuccess; ++r) {
+      int32_t* out = (r == lv.L - 1) ? idx_out : (cur == ws.buf_b ? ws.buf_a : ws.buf_b);
+      ok(observed(THIN_KERNEL_UNIFORM, r, st, [&] {
+        return thin::launch_uniform_halve(S, lv.n_r[r], cur, uniforms, lv.U, u_off, out, trace,
+                                          st);
+      }));
+      u_off += lv.n_r[r] / 2;
+      cur = out;
+    }
   } else {
     ok(observed(THIN_KERNEL_VMAX, -1, st,
                 [&] { return thin::launch_vmax(dtype, V, S, n, d, ws.vmax_bits, st); }));
@@ -202,7 +217,7 @@ int compress_impl(const void* K, const void* V, int32_t dtype, int64_t B, int64_
       a.u_slice = lv.U;
       a.u_off = u_off;
       a.trace = trace;
-      a.log_c = log(0.5 + log(2.0 * (double)lv.N[r] / 0.5));
+      a.log_c = log(0.5 + log(2.0 * (double)lv.N[r] / (delta ? delta[r] : 0.5)));
       a.E = ws.E;
       a.lbt = ws.lbt;
       a.h2 = ws.h2;
@@ -264,7 +279,7 @@ int thin_compress(const void* K, const void* V, int32_t dtype, int64_t B, int64_
                   int64_t n_uniforms, int32_t* idx_out, void* workspace,
                   size_t workspace_bytes, void* stream) {
   return compress_impl(K, V, dtype, B, H, n, d, n_out, g, uniforms, n_uniforms, idx_out,
-                       workspace, workspace_bytes, nullptr, 0, stream);
+                       workspace, workspace_bytes, nullptr, 0, THIN_HALVE_KH, nullptr, stream);
 }
 
 int thin_compress_traced(const void* K, const void* V, int32_t dtype, int64_t B, int64_t H,
@@ -274,7 +289,19 @@ int thin_compress_traced(const void* K, const void* V, int32_t dtype, int64_t B,
                          int64_t trace_len, void* stream) {
   if (!swap_trace) return THIN_EINVAL;
   return compress_impl(K, V, dtype, B, H, n, d, n_out, g, uniforms, n_uniforms, idx_out,
-                       workspace, workspace_bytes, swap_trace, trace_len, stream);
+                       workspace, workspace_bytes, swap_trace, trace_len, THIN_HALVE_KH, nullptr,
+                       stream);
+}
+
+int thin_compress_ex(const void* K, const void* V, int32_t dtype, int64_t B, int64_t H,
+                     int64_t n, int64_t d, int64_t n_out, int32_t g, const float* uniforms,
+                     int64_t n_uniforms, int32_t* idx_out, void* workspace,
+                     size_t workspace_bytes, const thin_compress_opts_t* opts,
+                     uint8_t* swap_trace, int64_t trace_len, void* stream) {
+  if (!opts) return THIN_EINVAL;
+  return compress_impl(K, V, dtype, B, H, n, d, n_out, g, uniforms, n_uniforms, idx_out,
+                       workspace, workspace_bytes, swap_trace, trace_len, opts->halve,
+                       opts->delta, stream);
 }
 
 int thin_attention(const void* Q, const void* K, const void* V, int32_t dtype, int64_t B,

@@ -1497,6 +1497,34 @@ hipError_t launch_fill_rows(int64_t S, int64_t n_out, const int32_t* src, int64_
   return hipGetLastError();
 }
 
+// Uniform halving: pair p of slice s keeps idx_in[2p+1] iff u < 1/2, else
+// idx_in[2p] (idx_in null = the identity).  The pairs of a round are
+// consecutive in the slice's current order, bucket after bucket, as are
+// their draws, so the buckets need no separate treatment.
+__global__ void uniform_halve_kernel(int64_t n_r, const int32_t* idx_in, const float* U,
+                                     int64_t u_slice, int64_t u_off, int32_t* idx_out,
+                                     uint8_t* trace) {
+  const int64_t s = blockIdx.y;
+  const int64_t p = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int64_t P = n_r >> 1;
+  if (p >= P) return;
+  const int64_t ui = s * u_slice + u_off + p;
+  const int swap = U[ui] < 0.5f;
+  const int64_t j = 2 * p + swap;
+  idx_out[s * P + p] = idx_in ? idx_in[s * n_r + j] : (int32_t)j;
+  if (trace) trace[ui] = (uint8_t)swap;
+}
+
+hipError_t launch_uniform_halve(int64_t S, int64_t n_r, const int32_t* idx_in, const float* U,
+                                int64_t u_slice, int64_t u_off, int32_t* idx_out,
+                                uint8_t* trace, hipStream_t st) {
+  const int64_t P = n_r / 2;
+  dim3 grid((unsigned)((P + 255) / 256), (unsigned)S);
+  hipLaunchKernelGGL(uniform_halve_kernel, grid, dim3(256), 0, st, n_r, idx_in, U, u_slice,
+                     u_off, idx_out, trace);
+  return hipGetLastError();
+}
+
 hipError_t launch_zero_u8(uint8_t* p, int64_t count, hipStream_t st) {
   if (count <= 0) return hipSuccess;
   hipLaunchKernelGGL(zero_u8_kernel, dim3((unsigned)((count + 255) / 256)), dim3(256), 0, st, p,

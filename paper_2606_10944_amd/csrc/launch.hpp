@@ -47,6 +47,11 @@ hipError_t launch_subsample(int64_t S, int64_t n, int64_t n_kept, const float* U
 hipError_t launch_fill_rows(int64_t S, int64_t n_out, const int32_t* src, int64_t src_stride,
                             int32_t* dst, hipStream_t st);
 hipError_t launch_zero_u8(uint8_t* p, int64_t count, hipStream_t st);
+// One round of uniform halving of every slice: pair p of a slice keeps row
+// 2p+1 of the round's input iff its uniform is below 1/2.
+hipError_t launch_uniform_halve(int64_t S, int64_t n_r, const int32_t* idx_in, const float* U,
+                                int64_t u_slice, int64_t u_off, int32_t* idx_out,
+                                uint8_t* trace, hipStream_t st);
 // Score tiles and score bytes of one N-row bucket (64-row decision blocks).
 int64_t halve_score_tiles(int64_t N);
 size_t halve_score_bytes(int64_t N);

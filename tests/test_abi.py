@@ -91,6 +91,24 @@ def test_compress_validates_before_launch():
     assert _compress(B=0) == _lib.THIN_EINVAL
 
 
+def test_compress_ex_validates_options_before_launch():
+    L = _lib.lib()
+
+    def call(halve, delta, opts=True):
+        dl = None if delta is None else (C.c_double * len(delta))(*delta)
+        o = _lib.CompressOpts(halve, C.cast(dl, C.c_void_p) if dl is not None else None)
+        return L.thin_compress_ex(FAKE, FAKE, 1, 1, 1, 1024, 64, 32, 2, FAKE, 992, FAKE,
+                                  C.c_void_p(0x100000), 1 << 20, C.byref(o) if opts else None,
+                                  None, 0, None)
+
+    assert call(0, None, opts=False) == _lib.THIN_EINVAL
+    assert call(2, None) == _lib.THIN_EINVAL
+    assert call(-1, None) == _lib.THIN_EINVAL
+    assert call(0, [0.5, 0.5, 0.0, 0.5, 0.5]) == _lib.THIN_EINVAL      # delta = 0
+    assert call(0, [0.5, 1.5, 0.5, 0.5, 0.5]) == _lib.THIN_EINVAL      # delta > 1
+    assert call(0, [0.5, 0.5, 0.5, 0.5, float("nan")]) == _lib.THIN_EINVAL
+
+
 def test_traced_compress_checks_trace_length():
     L = _lib.lib()
     rc = L.thin_compress_traced(FAKE, FAKE, 1, 1, 1, 1024, 64, 32, 2, FAKE, 992, FAKE,

@@ -241,3 +241,63 @@ def test_launch_timer_sees_every_kernel_in_order():
     assert i == len(body)
     assert "local" in kinds and "split" in kinds
     assert all(ms > 0 for _, _, ms in rec)
+
+
+# ---------------------------------------------------------------------------
+# thin_compress_ex: uniform halving and KH's delta per round
+# ---------------------------------------------------------------------------
+def _compress_gpu_ex(w, K, V, **kw):
+    plan = thin_plan(w.B, w.H, w.n, w.d, w.n_out, w.g)
+    U = W.make_uniforms(w, plan["uniforms_total"])
+    idx, tr = thin_compress(K.to(DEV), V.to(DEV), w.n_out, w.g, U.to(DEV), trace=True, **kw)
+    torch.cuda.synchronize()
+    return plan, U, idx.cpu().numpy(), tr.cpu().numpy()
+
+
+@pytest.mark.parametrize("name", ["tiny", "vit", "imggen", "long"])
+def test_uniform_halving_parity(name):
+    """Uniform halving (no floating point but u < 1/2): indices and swap bits
+    bit-exact against the oracle."""
+    w = W.WORKLOADS[name]
+    Q, K, V = W.make_qkv(w)
+    plan, U, idx, tr = _compress_gpu_ex(w, K, V, halve="uniform")
+    Us = U.numpy().reshape(w.S, -1)
+    ts = tr.reshape(w.S, -1)
+    slices = range(w.S) if w.S <= 32 else [0, 37, 63]
+    for s in slices:
+        b, h = divmod(s, w.H)
+        r = oracle.compress(K[b, h], V[b, h], w.n_out, w.g, Us[s], halve="uniform")
+        assert np.array_equal(r["idx"], idx[b, h]), (name, s)
+        assert np.array_equal(r["bits"], ts[s]), (name, s)
+
+
+@pytest.mark.parametrize("name", ["tiny", "imggen"])
+def test_kh_delta_schedule_parity(name):
+    """KH with a different delta in every round, against the oracle with the
+    same schedule (same margin rule as the default path)."""
+    w = W.WORKLOADS[name]
+    Q, K, V = W.make_qkv(w)
+    L = thin_plan(w.B, w.H, w.n, w.d, w.n_out, w.g)["rounds"]
+    delta = [1e-4 + (1.0 - 1e-4) * r / max(L - 1, 1) for r in range(L)]
+    plan, U, idx, tr = _compress_gpu_ex(w, K, V, delta=delta)
+    Us = U.numpy().reshape(w.S, -1)
+    ts = tr.reshape(w.S, -1)
+    for s in range(w.S):
+        b, h = divmod(s, w.H)
+        r = oracle.compress(K[b, h], V[b, h], w.n_out, w.g, Us[s], delta=delta, follow=ts[s],
+                            tol=MARGIN)
+        assert r["stats"]["hard_mismatch"] == 0, (name, s, r["stats"])
+        assert np.array_equal(r["idx"], idx[b, h]), (name, s)
+
+
+def test_uniform_halving_launches_one_kernel_per_round():
+    w = W.custom("lu", B=1, H=2, n=5000, n_out=40, g=2, d=64, dtype="bf16", kind="gauss")
+    Q, K, V = W.make_qkv(w)
+    plan = thin_plan(w.B, w.H, w.n, w.d, w.n_out, w.g)
+    U = W.make_uniforms(w, plan["uniforms_total"]).to(DEV)
+    stream = torch.cuda.current_stream()
+    with LaunchTimer(stream) as lt:
+        thin_compress(K.to(DEV), V.to(DEV), w.n_out, w.g, U, halve="uniform", stream=stream)
+        torch.cuda.synchronize()
+    got = [(k, r) for k, r, _ in lt.records()]
+    assert got == [("subsample", -1)] + [("uniform", r) for r in range(plan["rounds"])]

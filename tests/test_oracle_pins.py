@@ -225,6 +225,66 @@ def test_kh_value_scaling_leaves_decisions_unchanged():
 
 
 # ---------------------------------------------------------------------------
+# Alternative halving (uniform) and KH's delta
+# ---------------------------------------------------------------------------
+def test_uniform_halving_is_kh_where_every_threshold_is_zero():
+    """Identical rows give b_i = 0, hence a_i = 0, and KH takes p = 1/2: it
+    then is uniform halving, decision for decision.  Ties the uniform rule to
+    KH's own a = 0 case (App. A), through a whole compress."""
+    rng = np.random.default_rng(11)
+    n, d, n_out, g = 256, 4, 8, 2
+    K = np.tile(rng.standard_normal((1, d)), (n, 1))
+    V = np.tile(rng.standard_normal((1, d)), (n, 1))
+    pl = oracle.plan(n, n_out, g)
+    U = (rng.integers(0, 1 << 24, pl["uniforms"]) * 2.0 ** -24).astype(np.float32)
+    kh = oracle.compress(K, V, n_out, g, U)
+    un = oracle.compress(K, V, n_out, g, U, halve="uniform")
+    assert kh["stats"]["zero_threshold"] == pl["uniforms"]
+    assert np.array_equal(kh["idx"], un["idx"])
+    assert np.array_equal(kh["bits"], un["bits"])
+
+
+def test_uniform_halving_keeps_each_row_of_a_pair_half_the_time():
+    rng = np.random.default_rng(12)
+    rows = rng.permutation(4096).astype(np.int32)
+    u = rng.random(2048).astype(np.float32)
+    r = oracle.uniform_halving(rows, u)
+    pairs = rows.reshape(-1, 2)
+    assert np.all((r["out"] == pairs[:, 0]) | (r["out"] == pairs[:, 1]))
+    assert abs(r["bits"].mean() - 0.5) < 0.05
+
+
+def test_kh_delta_scales_every_threshold_by_the_log_term():
+    """a_i = b_i b_max (1/2 + log(2N/delta)): delta enters through one factor
+    common to every pair of the call; alpha does not depend on it."""
+    rng = np.random.default_rng(13)
+    N, d = 64, 3
+    K = rng.standard_normal((N, d)) * 0.5
+    V = rng.standard_normal((N, d))
+    u = rng.random(N // 2).astype(np.float32)
+    r0 = oracle.kernel_halving(K, V, np.arange(N), u, delta=0.5)
+    for delta in (1e-6, 0.05, 1.0):
+        r = oracle.kernel_halving(K, V, np.arange(N), u, delta=delta)
+        ratio = (0.5 + math.log(2 * N / delta)) / (0.5 + math.log(4 * N))
+        pos = r0["thresh"] > 0
+        np.testing.assert_allclose(r["thresh"][pos] / r0["thresh"][pos], ratio, rtol=1e-12)
+        # alpha sums the scores of the earlier pairs, whose decisions may differ
+        assert r["alpha"][0] == r0["alpha"][0] == 0.0
+
+
+def test_compress_with_delta_half_every_round_is_the_default():
+    rng = np.random.default_rng(14)
+    n, d, n_out, g = 512, 4, 16, 2
+    K = rng.standard_normal((n, d)) * 0.7
+    V = rng.standard_normal((n, d))
+    pl = oracle.plan(n, n_out, g)
+    U = (rng.integers(0, 1 << 24, pl["uniforms"]) * 2.0 ** -24).astype(np.float32)
+    a = oracle.compress(K, V, n_out, g, U)
+    b = oracle.compress(K, V, n_out, g, U, delta=[0.5] * pl["rounds"])
+    assert np.array_equal(a["idx"], b["idx"]) and np.array_equal(a["bits"], b["bits"])
+
+
+# ---------------------------------------------------------------------------
 # Compress level structure
 # ---------------------------------------------------------------------------
 def test_plan_uniform_counts_for_the_five_workloads():

@@ -57,6 +57,20 @@ def compress_bytes(w, plan) -> int:
     return total
 
 
+def uniform_compress_bytes(w, plan) -> int:
+    """Algorithmic HBM bytes of one compress call with uniform halving: the
+    subsample (n_kept uniforms read, n_kept indices written), then per slice
+    the kept indices read once, one float32 uniform per pair of every round
+    and the n_out indices written (no row of K or V is read)."""
+    S, n = w.S, w.n
+    n_kept, L = plan["n_kept"], plan["rounds"]
+    sub = n_kept < n
+    total = S * n_kept * (4 + 4 + 4) if sub else 0
+    total += S * sum((n_kept >> r) // 2 for r in range(L)) * 4
+    total += S * w.n_out * 4
+    return total
+
+
 def kappa_evals(plan, w) -> int:
     """kappa_att evaluations of one compress call: N^2/2 + N/2 per bucket."""
     n_kept, L, g = plan["n_kept"], plan["rounds"], w.g
@@ -127,7 +141,7 @@ def attention_flops(w) -> int:
     return w.S * w.n_q * 4 * w.n_out * w.d
 
 
-def cpu_baseline(w, Q, K, V, U, plan, budget_s: float = 20.0):
+def cpu_baseline(w, Q, K, V, U, plan, budget_s: float = 20.0, halve: str = "kh"):
     """The oracle, single-threaded, on as many whole slices as fit the budget."""
     import numpy as np
     import oracle
@@ -138,7 +152,7 @@ def cpu_baseline(w, Q, K, V, U, plan, budget_s: float = 20.0):
         b, h = divmod(s, w.H)
         Ks, Vs, Qs = K[b, h], V[b, h], Q[b, h]
         t0 = time.perf_counter()
-        r = oracle.compress(Ks, Vs, w.n_out, w.g, Us[s])
+        r = oracle.compress(Ks, Vs, w.n_out, w.g, Us[s], halve=halve)
         oracle.attention(Qs, Ks, Vs, r["idx"])
         t_used += time.perf_counter() - t0
         done += 1
@@ -159,6 +173,9 @@ def main():
     ap.add_argument("--warmup", type=int, default=100)
     ap.add_argument("--workload", default="long")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--halve", choices=["kh", "uniform"], default="kh",
+                    help="halving algorithm of compress (kernel halving, the paper's; or "
+                         "uniform halving)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: the thinning path runs each (batch, head) "
@@ -182,7 +199,8 @@ def main():
     stream = torch.cuda.current_stream()
 
     def step():
-        thin_compress(Kd, Vd, w.n_out, w.g, Ud, idx_out=idx, workspace=ws, stream=stream)
+        thin_compress(Kd, Vd, w.n_out, w.g, Ud, idx_out=idx, workspace=ws, halve=args.halve,
+                      stream=stream)
         thin_attention(Qd, Kd, Vd, idx, O=O, stream=stream)
 
     for _ in range(args.warmup):
@@ -221,19 +239,20 @@ def main():
     tc = sum(v for k, v in per_step.items() if k != "attention")
     ta = per_step["attention"]
 
-    cb = compress_bytes(w, plan)
+    cb = compress_bytes(w, plan) if args.halve == "kh" else uniform_compress_bytes(w, plan)
     sb = score_bytes(w, plan)
     ab = attention_bytes(w, 4)
     af = attention_flops(w)
-    kev = kappa_evals(plan, w)
+    kev = kappa_evals(plan, w) if args.halve == "kh" else 0
     # per launch: averages over every score launch of the K steps (a round may
     # take several launches; bytes and time are both summed over the step)
     n_sc = len(score_ms) // args.steps
     sc_rounds = sorted({r for name, r, _ in rec if name == "scores"})  # the others run local
-    sc_ms_launch = statistics.mean(score_ms)
-    sc_bytes_launch = sum(sb[r] for r in sc_rounds) / n_sc
-    sc_gbs = sc_bytes_launch / (sc_ms_launch * 1e-3) / 1e9
-    traffic = stored_traffic(w.name)
+    if n_sc:
+        sc_ms_launch = statistics.mean(score_ms)
+        sc_bytes_launch = sum(sb[r] for r in sc_rounds) / n_sc
+        sc_gbs = sc_bytes_launch / (sc_ms_launch * 1e-3) / 1e9
+    traffic = stored_traffic(w.name) if args.halve == "kh" else None
     attn_gbs = ab / (ta * 1e-3) / 1e9
     attn_tflops = af / (ta * 1e-3) / 1e12
     value = w.S * w.n_q / (ms_step * 1e-3)
@@ -252,7 +271,7 @@ def main():
         "dtype": w.dtype,
         "data": "synthetic",
         "config": {"workload": w.name, "B": w.B, "H": w.H, "n": w.n, "n_q": w.n_q, "d": w.d,
-                   "n_out": w.n_out, "g": w.g, "out_dtype": "fp32"},
+                   "n_out": w.n_out, "g": w.g, "out_dtype": "fp32", "halve": args.halve},
         "roofline": {
             "kernel": "pair_scores_kernel (one launch per Halve round with buckets above "
                       "the local size)",
@@ -261,6 +280,12 @@ def main():
             "traffic": traffic,
             "algorithmic_bytes_per_launch": sc_bytes_launch, "ms_per_launch": sc_ms_launch,
             "launches_per_step": n_sc, "rounds": sc_rounds,
+        } if n_sc else {
+            # uniform halving evaluates no kernel: attention is the dominant kernel
+            "kernel": "coreset attention (one launch per step)",
+            "bound": "hbm", "achieved": attn_gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+            "frac": attn_gbs / HBM_PEAK_GBS, "traffic": None,
+            "algorithmic_bytes_per_launch": ab, "ms_per_launch": ta, "launches_per_step": 1,
         },
         "compress": {"ms": tc, "kappa_evals": kev, "kappa_evals_per_s": kev / (tc * 1e-3),
                      "algorithmic_bytes": cb, "hbm_gbs": cb / (tc * 1e-3) / 1e9,
@@ -276,7 +301,7 @@ def main():
         "gpu": torch.cuda.get_device_name(0),
     }
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(w, Q, K, V, U, plan)
+        out["cpu_baseline"] = cpu_baseline(w, Q, K, V, U, plan, halve=args.halve)
     print(json.dumps(out), flush=True)
 
 

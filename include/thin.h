@@ -198,8 +198,9 @@ const char* thin_status_str(int status);
  * stream-ordered work of its own (for instance record an event on `stream`),
  * so that consecutive records time one kernel.  `kernel` is a
  * thin_kernel_t, `round` the Halve round 0..L-1 of a THIN_KERNEL_SCORES,
- * THIN_KERNEL_DECIDE, THIN_KERNEL_LOCAL or THIN_KERNEL_UNIFORM launch and -1
- * otherwise.  A round
+ * THIN_KERNEL_DECIDE, THIN_KERNEL_LOCAL or per-round THIN_KERNEL_UNIFORM
+ * launch and -1 otherwise (uniform halving runs every round in one launch
+ * when a slice keeps at most 32768 rows, else one launch per round).  A round
  * runs either as SCORES + DECIDE launches or, when its buckets are small
  * enough for one workgroup to hold all their scores in LDS, as one LOCAL
  * launch.  The setting is process-wide:
@@ -215,7 +216,7 @@ typedef enum {
   THIN_KERNEL_DECIDE = 5,      /* decision pass of one round              */
   THIN_KERNEL_ATTENTION = 6,   /* coreset attention                       */
   THIN_KERNEL_LOCAL = 7,       /* scores and decisions of one round       */
-  THIN_KERNEL_UNIFORM = 8      /* one round of uniform halving            */
+  THIN_KERNEL_UNIFORM = 8      /* uniform halving (all rounds, or one)    */
 } thin_kernel_t;
 typedef void (*thin_launch_hook_t)(void* ctx, int32_t kernel, int32_t round, int32_t phase,
                                    void* stream);

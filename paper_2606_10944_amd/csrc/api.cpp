@@ -185,6 +185,11 @@ int compress_impl(const void* K, const void* V, int32_t dtype, int64_t B, int64_
     ok(observed(THIN_KERNEL_FILL, -1, st, [&] {
       return thin::launch_fill_rows(S, n_out, cur, lv.n_kept, idx_out, st);
     }));
+  } else if (halve == THIN_HALVE_UNIFORM && thin::uniform_fused_ok(lv.n_kept)) {
+    ok(observed(THIN_KERNEL_UNIFORM, -1, st, [&] {
+      return thin::launch_uniform_compress(S, lv.n_kept, lv.L, cur, uniforms, lv.U,
+                                           lv.sub ? lv.n_kept : 0, idx_out, n_out, trace, st);
+    }));
   } else if (halve == THIN_HALVE_UNIFORM) {
     int64_t u_off = lv.sub ? lv.n_kept : 0;
     for (int32_t r = 0; r < lv.L && e == hipSuccess; ++r) {

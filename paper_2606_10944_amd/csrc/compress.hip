@@ -1525,6 +1525,67 @@ hipError_t launch_uniform_halve(int64_t S, int64_t n_r, const int32_t* idx_in, c
   return hipGetLastError();
 }
 
+// Every round of uniform halving of one slice per workgroup, the slice's
+// indices held in LDS (n_kept <= kUniformFusedRows): in round r each thread
+// reads its pairs' kept indices, the workgroup synchronises, and the halved
+// list is written back in place.
+constexpr int kUniformThreads = 1024;
+constexpr int64_t kUniformFusedRows = 32768;
+__global__ __launch_bounds__(kUniformThreads) void uniform_compress_kernel(
+    int64_t n_kept, int32_t L, const int32_t* idx0, const float* U, int64_t u_slice,
+    int64_t u_off0, int32_t* idx_out, int64_t n_out, uint8_t* trace) {
+  extern __shared__ int32_t s_idx[];
+  constexpr int PPT = (int)(kUniformFusedRows / 2 / kUniformThreads);  // pairs per thread, round 0
+  const int64_t s = blockIdx.x;
+  const int tid = threadIdx.x;
+  for (int64_t i = tid; i < n_kept; i += kUniformThreads)
+    s_idx[i] = idx0 ? idx0[s * n_kept + i] : (int32_t)i;
+  __syncthreads();
+  int64_t n_r = n_kept, u_off = u_off0;
+  for (int32_t r = 0; r < L; ++r) {
+    const int64_t P = n_r >> 1;
+    int32_t keep[PPT];
+#pragma unroll
+    for (int k = 0; k < PPT; ++k) {
+      const int64_t p = tid + (int64_t)k * kUniformThreads;
+      if (p < P) {
+        const int64_t ui = s * u_slice + u_off + p;
+        const int swap = U[ui] < 0.5f;
+        keep[k] = s_idx[2 * p + swap];
+        if (trace) trace[ui] = (uint8_t)swap;
+      }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int k = 0; k < PPT; ++k) {
+      const int64_t p = tid + (int64_t)k * kUniformThreads;
+      if (p < P) s_idx[p] = keep[k];
+    }
+    __syncthreads();
+    n_r = P;
+    u_off += P;
+  }
+  for (int64_t i = tid; i < n_out; i += kUniformThreads) idx_out[s * n_out + i] = s_idx[i];
+}
+
+bool uniform_fused_ok(int64_t n_kept) { return n_kept <= kUniformFusedRows; }
+
+hipError_t launch_uniform_compress(int64_t S, int64_t n_kept, int32_t L, const int32_t* idx0,
+                                   const float* U, int64_t u_slice, int64_t u_off0,
+                                   int32_t* idx_out, int64_t n_out, uint8_t* trace,
+                                   hipStream_t st) {
+  if (!uniform_fused_ok(n_kept)) return hipErrorInvalidValue;
+  const size_t lds = (size_t)n_kept * 4;
+  if (lds > 64 * 1024) {
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(uniform_compress_kernel),
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e != hipSuccess) return e;
+  }
+  hipLaunchKernelGGL(uniform_compress_kernel, dim3((unsigned)S), dim3(kUniformThreads), lds, st,
+                     n_kept, L, idx0, U, u_slice, u_off0, idx_out, n_out, trace);
+  return hipGetLastError();
+}
+
 hipError_t launch_zero_u8(uint8_t* p, int64_t count, hipStream_t st) {
   if (count <= 0) return hipSuccess;
   hipLaunchKernelGGL(zero_u8_kernel, dim3((unsigned)((count + 255) / 256)), dim3(256), 0, st, p,

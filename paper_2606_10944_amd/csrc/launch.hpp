@@ -52,6 +52,13 @@ hipError_t launch_zero_u8(uint8_t* p, int64_t count, hipStream_t st);
 hipError_t launch_uniform_halve(int64_t S, int64_t n_r, const int32_t* idx_in, const float* U,
                                 int64_t u_slice, int64_t u_off, int32_t* idx_out,
                                 uint8_t* trace, hipStream_t st);
+// Every round of uniform halving in one launch (one workgroup per slice,
+// indices in LDS); only for n_kept <= 32768 (uniform_fused_ok).
+bool uniform_fused_ok(int64_t n_kept);
+hipError_t launch_uniform_compress(int64_t S, int64_t n_kept, int32_t L, const int32_t* idx0,
+                                   const float* U, int64_t u_slice, int64_t u_off0,
+                                   int32_t* idx_out, int64_t n_out, uint8_t* trace,
+                                   hipStream_t st);
 // Score tiles and score bytes of one N-row bucket (64-row decision blocks).
 int64_t halve_score_tiles(int64_t N);
 size_t halve_score_bytes(int64_t N);

@@ -254,7 +254,7 @@ def _compress_gpu_ex(w, K, V, **kw):
     return plan, U, idx.cpu().numpy(), tr.cpu().numpy()
 
 
-@pytest.mark.parametrize("name", ["tiny", "vit", "imggen", "long"])
+@pytest.mark.parametrize("name", ["tiny", "vit", "imggen", "long", "stress"])
 def test_uniform_halving_parity(name):
     """Uniform halving (no floating point but u < 1/2): indices and swap bits
     bit-exact against the oracle."""
@@ -263,7 +263,9 @@ def test_uniform_halving_parity(name):
     plan, U, idx, tr = _compress_gpu_ex(w, K, V, halve="uniform")
     Us = U.numpy().reshape(w.S, -1)
     ts = tr.reshape(w.S, -1)
-    slices = range(w.S) if w.S <= 32 else [0, 37, 63]
+    # (every round in one launch up to 32768 kept rows per slice, one launch
+    # per round beyond: the stress workload keeps 65536)
+    slices = range(w.S) if w.S <= 16 else [0, w.S // 2 + 5, w.S - 1]
     for s in slices:
         b, h = divmod(s, w.H)
         r = oracle.compress(K[b, h], V[b, h], w.n_out, w.g, Us[s], halve="uniform")
@@ -290,7 +292,7 @@ def test_kh_delta_schedule_parity(name):
         assert np.array_equal(r["idx"], idx[b, h]), (name, s)
 
 
-def test_uniform_halving_launches_one_kernel_per_round():
+def test_uniform_halving_runs_every_round_in_one_launch():
     w = W.custom("lu", B=1, H=2, n=5000, n_out=40, g=2, d=64, dtype="bf16", kind="gauss")
     Q, K, V = W.make_qkv(w)
     plan = thin_plan(w.B, w.H, w.n, w.d, w.n_out, w.g)
@@ -300,4 +302,4 @@ def test_uniform_halving_launches_one_kernel_per_round():
         thin_compress(K.to(DEV), V.to(DEV), w.n_out, w.g, U, halve="uniform", stream=stream)
         torch.cuda.synchronize()
     got = [(k, r) for k, r, _ in lt.records()]
-    assert got == [("subsample", -1)] + [("uniform", r) for r in range(plan["rounds"])]
+    assert got == [("subsample", -1), ("uniform", -1)]

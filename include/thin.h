@@ -21,7 +21,7 @@
  *     launch error; faults inside a kernel surface at the caller's next
  *     synchronisation.
  *   - Supported: dtype THIN_FP32 or THIN_BF16 (Q, K, V share it), d in
- *     {32, 64, 128}.
+ *     {32, 64, 128}, B*H <= 65535 slices (THIN_EINVAL beyond).
  */
 #ifndef THIN_H
 #define THIN_H

@@ -13,6 +13,7 @@ namespace {
 
 constexpr int64_t kMaxBucket = 8192;  // the decision pass keeps a bucket's per-pair alpha in LDS
 constexpr int64_t kMaxRows = (int64_t)1 << 30;
+constexpr int64_t kMaxSlices = 65535;  // the per-slice kernels index slices by grid y
 
 struct Levels {
   int64_t n = 0;
@@ -140,7 +141,7 @@ hipError_t observed(int32_t kernel, int32_t round, hipStream_t st, F&& launch) {
 
 int check_shape(int64_t B, int64_t H, int64_t n, int64_t d) {
   if (B < 1 || H < 1 || n < 1 || n > kMaxRows) return THIN_EINVAL;
-  if (B * H > ((int64_t)1 << 31)) return THIN_EINVAL;
+  if (B * H > kMaxSlices) return THIN_EINVAL;
   if (!supported_d(d)) return THIN_EINVAL;
   return THIN_OK;
 }

@@ -89,6 +89,7 @@ def test_compress_validates_before_launch():
     assert _compress(ws=None) == _lib.THIN_EWORKSPACE
     assert _compress(ws=C.c_void_p(0x100010)) == _lib.THIN_EWORKSPACE   # misaligned
     assert _compress(B=0) == _lib.THIN_EINVAL
+    assert _compress(B=65536) == _lib.THIN_EINVAL      # more slices than grid y holds
 
 
 def test_compress_ex_validates_options_before_launch():

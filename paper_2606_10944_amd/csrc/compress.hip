@@ -999,11 +999,12 @@ struct PassLds {
   // COAL, per bulk wave a column buffer [64][CW] 16-byte words.  A column of
   // BP scores is QW words plus one of padding (CW): reads of whole columns
   // by consecutive lanes then fall in different banks.  COAL: the bulk waves
-  // load their chunks coalesced and transpose them in LDS (with four or more
-  // bulk waves the loads, not the LDS, limit them); else each lane loads its
-  // own column, and the workgroup needs less LDS.
+  // load their chunks coalesced and transpose them in LDS (with six bulk
+  // waves, on the largest buckets, the loads limit the bulk); else each lane
+  // loads its own column: less LDS, and the decider's LDS accesses do not
+  // queue behind the transposes.
   static constexpr int CW = QW + 1;
-  static constexpr bool COAL = BW >= 4;
+  static constexpr bool COAL = BW >= 6;
   static constexpr size_t kSlot = BP * 8 + 2 * BP * 4 + 2 * BP * CW * 16;
   static constexpr size_t kColBuf = COAL ? 64 * CW * 16 : 0;
   static_assert(2 + BW <= 16, "counter block");

@@ -80,6 +80,8 @@ def lib():
         L.or_compress.restype = C.c_int
         L.or_compress_ex.argtypes = [P, P, C.c_int64, C.c_int64, C.c_int64, C.c_int32, C.c_int,
                                      C.c_int, P, P, P, P, C.c_double, P, P, C.POINTER(Stats)]
+        L.or_attention_weighted.argtypes = [P, P, P, C.c_int64, C.c_int64, P, P, C.c_int64, P]
+        L.or_attention_weighted.restype = None
         L.or_compress_ex.restype = C.c_int
         L.or_uniform_halving.argtypes = [P, C.c_int64, P, P, P, C.POINTER(Stats)]
         L.or_uniform_halving.restype = C.c_int
@@ -171,11 +173,31 @@ def uniform_halving(rows, u) -> dict:
 
 
 def compress(K, V, n_out: int, g: int, U, *, kernel: str = "katt", follow=None,
-             tol: float = 1e-5, halve: str = "kh", delta=None) -> dict:
+             tol: float = 1e-5, halve: str = "kh", delta=None, n_sinks: int = 0,
+             n_window: int = 0) -> dict:
     """One slice: K, V [n, d]; U = this slice's uniforms.  halve: "kh" (KH(delta),
     delta[r] per round, default 1/2) or "uniform" (one point of each pair, each
-    with probability 1/2)."""
+    with probability 1/2).  With n_sinks / n_window the first and last rows are
+    kept exactly and the n_mid rows between them are thinned to n_out as a
+    dataset of their own (v_max of eq. eq:katt over those rows, U drawn for a
+    slice of n_mid rows); "idx" is then sinks + coreset + window and "logw"
+    their log-weights for eq. def:att_approx: 0 for an exact row and
+    log(n_mid / n_out) for a coreset row, which stands for that many rows."""
     K, V = _f64(K), _f64(V)
+    if n_sinks or n_window:
+        n = K.shape[0]
+        mid = slice(n_sinks, n - n_window)
+        r = _compress_rows(K[mid], V[mid], n_out, g, U, kernel, follow, tol, halve, delta)
+        n_mid = n - n_sinks - n_window
+        r["idx"] = np.concatenate([np.arange(n_sinks, dtype=np.int32), r["idx"] + n_sinks,
+                                   np.arange(n - n_window, n, dtype=np.int32)])
+        r["logw"] = np.concatenate([np.zeros(n_sinks), np.full(n_out, np.log(n_mid / n_out)),
+                                    np.zeros(n_window)])
+        return r
+    return _compress_rows(K, V, n_out, g, U, kernel, follow, tol, halve, delta)
+
+
+def _compress_rows(K, V, n_out, g, U, kernel, follow, tol, halve, delta):
     n, d = K.shape
     pl = plan(n, n_out, g)
     if pl is None:
@@ -209,6 +231,18 @@ def attention(Q, K, V, rows) -> np.ndarray:
     n_q, d = Q.shape
     O = np.empty((n_q, d))
     lib().or_attention(_p(Q), _p(K), _p(V), n_q, d, _p(rows), rows.size, _p(O))
+    return O
+
+
+def weighted_attention(Q, K, V, rows, logw) -> np.ndarray:
+    """Weighted attention (eq. def:att_approx): key rows[j] weighs exp(logw[j])."""
+    Q, K, V = _f64(Q), _f64(K), _f64(V)
+    rows = np.ascontiguousarray(rows, dtype=np.int32)
+    lw = np.ascontiguousarray(logw, dtype=np.float64)
+    assert lw.size == rows.size
+    n_q, d = Q.shape
+    O = np.empty((n_q, d))
+    lib().or_attention_weighted(_p(Q), _p(K), _p(V), n_q, d, _p(rows), _p(lw), rows.size, _p(O))
     return O
 
 

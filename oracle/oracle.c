@@ -344,3 +344,35 @@ void or_attention(const double* Q, const double* K, const double* V, int64_t n_q
   }
   free(s);
 }
+
+/*
+ * Weighted attention over a weighted coreset (eq. def:att_approx): key j
+ * carries weight w_j = exp(logw[j]) (logw[j] = -inf drops it),
+ *   O[q] = sum_j w_j exp(<Q_q,K_rows[j]>/sqrt d) V_rows[j] / sum_j w_j exp(...).
+ */
+void or_attention_weighted(const double* Q, const double* K, const double* V, int64_t n_q,
+                           int64_t d, const int32_t* rows, const double* logw, int64_t m,
+                           double* O) {
+  double* s = (double*)malloc(sizeof(double) * (size_t)(m > 0 ? m : 1));
+  double inv = 1.0 / sqrt((double)d);
+  for (int64_t q = 0; q < n_q; ++q) {
+    const double* qq = Q + q * d;
+    double mx = -INFINITY;
+    for (int64_t j = 0; j < m; ++j) {
+      s[j] = dot(qq, K + (int64_t)rows[j] * d, d) * inv + logw[j];
+      if (s[j] > mx) mx = s[j];
+    }
+    double den = 0.0;
+    double* o = O + q * d;
+    for (int64_t c = 0; c < d; ++c) o[c] = 0.0;
+    for (int64_t j = 0; j < m; ++j) {
+      if (!(s[j] > -INFINITY)) continue;
+      double w = exp(s[j] - mx);
+      den += w;
+      const double* v = V + (int64_t)rows[j] * d;
+      for (int64_t c = 0; c < d; ++c) o[c] += w * v[c];
+    }
+    for (int64_t c = 0; c < d; ++c) o[c] /= den;
+  }
+  free(s);
+}

@@ -97,6 +97,11 @@ int or_compress_ex(const double* K, const double* V, int64_t n, int64_t d,
 void or_attention(const double* Q, const double* K, const double* V, int64_t n_q,
                   int64_t d, const int32_t* rows, int64_t m, double* O);
 
+/* Weighted attention (eq. def:att_approx): key j weighs exp(logw[j]). */
+void or_attention_weighted(const double* Q, const double* K, const double* V, int64_t n_q,
+                           int64_t d, const int32_t* rows, const double* logw, int64_t m,
+                           double* O);
+
 #ifdef __cplusplus
 }
 #endif

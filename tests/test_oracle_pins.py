@@ -466,3 +466,83 @@ def test_attention_value_scaling_is_linear():
     rows = np.arange(0, 30, 3)
     np.testing.assert_array_equal(oracle.attention(Q, K, 2 * V, rows),
                                   2 * oracle.attention(Q, K, V, rows))
+
+
+# ---------------------------------------------------------------------------
+# Weighted attention (eq. def:att_approx) and exact sink / window rows
+# ---------------------------------------------------------------------------
+def test_weighted_attention_matches_library_sdpa_with_an_additive_mask():
+    """exp(logw_j) * exp(s_j) = exp(s_j + logw_j): the log-weights are the float
+    mask SDPA adds to the scaled scores (including -inf, a dropped key)."""
+    rng = np.random.default_rng(20)
+    Q = rng.standard_normal((23, 16))
+    K = rng.standard_normal((41, 16))
+    V = rng.standard_normal((41, 16))
+    rows = rng.permutation(41)[:29].astype(np.int32)
+    logw = rng.standard_normal(29) * 2
+    logw[[3, 17]] = -np.inf
+    O = oracle.weighted_attention(Q, K, V, rows, logw)
+    mask = torch.from_numpy(np.broadcast_to(logw, (23, 29)).copy())
+    ref = torch.nn.functional.scaled_dot_product_attention(
+        torch.from_numpy(Q)[None], torch.from_numpy(K[rows])[None],
+        torch.from_numpy(V[rows])[None], attn_mask=mask[None])[0]
+    np.testing.assert_allclose(O, ref.numpy(), rtol=1e-12, atol=1e-13)
+
+
+def test_weighted_attention_with_equal_weights_is_attention():
+    rng = np.random.default_rng(21)
+    Q, K, V = (rng.standard_normal((30, 8)) for _ in range(3))
+    rows = np.arange(1, 30, 2)
+    O = oracle.weighted_attention(Q, K, V, rows, np.full(rows.size, 3.7))
+    np.testing.assert_allclose(O, oracle.attention(Q, K, V, rows), rtol=1e-12, atol=1e-13)
+
+
+def test_integer_weight_is_a_repeated_key():
+    """Weight k on a key = that key listed k times with weight 1."""
+    rng = np.random.default_rng(22)
+    Q, K, V = (rng.standard_normal((12, 8)) for _ in range(3))
+    rows = np.array([2, 5, 7, 11])
+    mult = np.array([1, 3, 1, 5])
+    O = oracle.weighted_attention(Q, K, V, rows, np.log(mult))
+    np.testing.assert_allclose(O, oracle.attention(Q, K, V, np.repeat(rows, mult)),
+                               rtol=1e-12, atol=1e-13)
+
+
+def test_minus_inf_weight_drops_the_key():
+    rng = np.random.default_rng(23)
+    Q, K, V = (rng.standard_normal((12, 8)) for _ in range(3))
+    rows = np.array([0, 4, 6, 9, 10])
+    logw = np.array([0.0, -np.inf, 0.0, -np.inf, 0.0])
+    np.testing.assert_array_equal(oracle.weighted_attention(Q, K, V, rows, logw),
+                                  oracle.attention(Q, K, V, rows[np.isfinite(logw)]))
+
+
+def test_sinks_and_window_are_exact_and_the_weights_sum_to_n():
+    rng = np.random.default_rng(24)
+    n, d, ns, nw, n_out, g = 300, 8, 20, 24, 16, 1
+    K, V = rng.standard_normal((n, d)), rng.standard_normal((n, d))
+    pl = oracle.plan(n - ns - nw, n_out, g)
+    U = rng.random(pl["uniforms"]).astype(np.float32)
+    r = oracle.compress(K, V, n_out, g, U, n_sinks=ns, n_window=nw)
+    idx, logw = r["idx"], r["logw"]
+    assert idx.size == ns + n_out + nw == logw.size
+    assert np.array_equal(idx[:ns], np.arange(ns))
+    assert np.array_equal(idx[ns + n_out:], np.arange(n - nw, n))
+    core = idx[ns:ns + n_out]
+    assert core.min() >= ns and core.max() < n - nw and np.unique(core).size == n_out
+    assert np.all(logw[:ns] == 0) and np.all(logw[ns + n_out:] == 0)
+    assert np.exp(logw).sum() == pytest.approx(n, rel=1e-12)
+    # the middle rows are a dataset of their own: thinning them alone gives the same coreset
+    mid = oracle.compress(K[ns:n - nw], V[ns:n - nw], n_out, g, U)
+    assert np.array_equal(core, mid["idx"] + ns)
+
+
+def test_sinks_and_window_with_nothing_to_thin_is_exact_attention():
+    """n - n_sinks - n_window = n_out: every row is kept with weight 1."""
+    rng = np.random.default_rng(25)
+    n, d, ns, nw = 48, 8, 8, 8
+    Q, K, V = (rng.standard_normal((n, d)) for _ in range(3))
+    r = oracle.compress(K, V, n - ns - nw, 1, np.zeros(1, np.float32), n_sinks=ns, n_window=nw)
+    assert np.array_equal(r["idx"], np.arange(n)) and np.all(r["logw"] == 0)
+    np.testing.assert_allclose(oracle.weighted_attention(Q, K, V, r["idx"], r["logw"]),
+                               oracle.exact_attention(Q, K, V), rtol=1e-12, atol=1e-13)

@@ -132,27 +132,47 @@ int thin_compress_traced(const void* K, const void* V, int32_t dtype, int64_t B,
 typedef enum { THIN_HALVE_KH = 0, THIN_HALVE_UNIFORM = 1 } thin_halve_t;
 
 /*
- * Options of thin_compress_ex; {THIN_HALVE_KH, NULL} gives thin_compress.
- *   halve   a thin_halve_t.
- *   delta   (host, nullable) float64 [plan.rounds]: the failure probability
- *           of every KH call of round r (its threshold carries the factor
- *           1/2 + log(2 N_r / delta[r]), App. A), each in (0, 1]; read during
- *           the call only.  NULL = 1/2 for every round (App. I).  Ignored by
- *           THIN_HALVE_UNIFORM.
+ * Options of thin_compress_ex; {THIN_HALVE_KH, NULL, 0, 0, NULL} gives
+ * thin_compress.
+ *   halve     a thin_halve_t.
+ *   delta     (host, nullable) float64 [plan.rounds]: the failure probability
+ *             of every KH call of round r (its threshold carries the factor
+ *             1/2 + log(2 N_r / delta[r]), App. A), each in (0, 1]; read
+ *             during the call only.  NULL = 1/2 for every round (App. I).
+ *             Ignored by THIN_HALVE_UNIFORM.
+ *   n_sinks   rows 0..n_sinks-1 of every slice are kept exactly (attention
+ *             sinks, the n_sinks setting of the experiments of App. I).
+ *   n_window  rows n-n_window..n-1 of every slice are kept exactly (the
+ *             recent window, n_window in App. I).
+ *             The n_mid = n - n_sinks - n_window rows between them are
+ *             thinned to n_out as a dataset of their own: v_max of eq. katt
+ *             is taken over them, and the plan (uniforms, workspace) is
+ *             thin_plan's for n_mid rows.  idx_out is then int32
+ *             [B,H,n_sinks+n_out+n_window]: the sinks, the coreset (rows of
+ *             the whole slice) and the window, in that order.
+ *   logw_out  (device, nullable) float32 [B,H,n_sinks+n_out+n_window]: the
+ *             log-weight of every output row for eq. def:att_approx, 0 for
+ *             an exact row and log(n_mid/n_out) for a coreset row (which
+ *             stands for n_mid/n_out rows); the weights of a slice sum to n.
  */
 typedef struct {
   int32_t halve;
   const double* delta;
+  int64_t n_sinks;
+  int64_t n_window;
+  float* logw_out;
 } thin_compress_opts_t;
 
 /*
- * thin_compress with a choice of halving algorithm and of KH's delta per
- * round.  Same arguments, uniforms layout (the pair draws of a round are
- * consumed the same way by either algorithm), workspace and level structure
- * as thin_compress; opts (host) must not be NULL.  swap_trace (device,
- * nullable): as in thin_compress_traced, with trace_len >= B*H*U when given.
- * Errors: those of thin_compress, and THIN_EINVAL for an unknown halve or a
- * delta[r] outside (0, 1].
+ * thin_compress with a choice of halving algorithm, of KH's delta per round
+ * and of exact sink/window rows.  Same arguments, uniforms layout (the pair
+ * draws of a round are consumed the same way by either algorithm), workspace
+ * and level structure as thin_compress of the thinned rows; opts (host) must
+ * not be NULL.  swap_trace (device, nullable): as in thin_compress_traced,
+ * with trace_len >= B*H*U when given.
+ * Errors: those of thin_compress, and THIN_EINVAL for an unknown halve, a
+ * delta[r] outside (0, 1], a negative n_sinks or n_window, or
+ * n - n_sinks - n_window < n_out.
  */
 int thin_compress_ex(const void* K, const void* V, int32_t dtype, int64_t B, int64_t H,
                      int64_t n, int64_t d, int64_t n_out, int32_t g, const float* uniforms,
@@ -178,6 +198,21 @@ int thin_attention(const void* Q, const void* K, const void* V, int32_t dtype, i
                    int64_t n_out, void* O, int32_t out_dtype, void* stream);
 
 /*
+ * Weighted attention over a weighted coreset (eq. def:att_approx): key j of
+ * slice s carries the weight w_j = exp(logw[s, j]),
+ *   O[s,q,:] = sum_j w_j exp(<Q[s,q],K[s,I_j]>/sqrt d) V[s,I_j] / sum_j w_j exp(...).
+ *   logw  (device, nullable) float32 [B,H,n_out]; -inf drops a key, NULL
+ *         gives thin_attention.  Every query needs at least one key of
+ *         finite log-weight (else its row of O is undefined).
+ * Other arguments, layouts and errors as thin_attention; logw_out of
+ * thin_compress_ex is this call's logw for its idx_out.
+ */
+int thin_attention_ex(const void* Q, const void* K, const void* V, int32_t dtype, int64_t B,
+                      int64_t H, int64_t n_q, int64_t n, int64_t d, const int32_t* idx,
+                      const float* logw, int64_t n_out, void* O, int32_t out_dtype,
+                      void* stream);
+
+/*
  * Diagnostic: out[m*16 + n] = <rows[m], rows[16 + n]> for m, n < 16, computed
  * through the MFMA row-fragment path the pair-score kernel uses.
  *   rows (device) [32, d] of `dtype`;  out (device) float32 [16, 16].
@@ -191,7 +226,7 @@ const char* thin_status_str(int status);
 /*
  * Launch observer, for tracing and per-kernel timing.  While a hook is set,
  * every kernel launch made by thin_compress, thin_compress_traced,
- * thin_compress_ex and thin_attention is bracketed by two calls on the
+ * thin_compress_ex, thin_attention and thin_attention_ex is bracketed by two calls on the
  * calling thread:
  * hook(ctx, kernel, round, 0, stream) right before the launch is enqueued and
  * hook(ctx, kernel, round, 1, stream) right after.  The hook may enqueue
@@ -216,7 +251,8 @@ typedef enum {
   THIN_KERNEL_DECIDE = 5,      /* decision pass of one round              */
   THIN_KERNEL_ATTENTION = 6,   /* coreset attention                       */
   THIN_KERNEL_LOCAL = 7,       /* scores and decisions of one round       */
-  THIN_KERNEL_UNIFORM = 8      /* uniform halving (all rounds, or one)    */
+  THIN_KERNEL_UNIFORM = 8,     /* uniform halving (all rounds, or one)    */
+  THIN_KERNEL_ASSEMBLE = 9     /* sinks + coreset + window, log-weights   */
 } thin_kernel_t;
 typedef void (*thin_launch_hook_t)(void* ctx, int32_t kernel, int32_t round, int32_t phase,
                                    void* stream);

@@ -22,11 +22,11 @@ THIN_FP32, THIN_BF16 = 0, 1
 
 # Every symbol include/thin.h declares.
 EXPORTS = ("thin_plan", "thin_compress", "thin_compress_traced", "thin_compress_ex", "thin_attention",
-           "thin_selftest_gram16", "thin_status_str", "thin_set_launch_hook")
+           "thin_attention_ex", "thin_selftest_gram16", "thin_status_str", "thin_set_launch_hook")
 
 # thin_kernel_t
 KERNEL_NAMES = {0: "trace_clear", 1: "subsample", 2: "fill", 3: "vmax", 4: "scores",
-                5: "decide", 6: "attention", 7: "local", 8: "uniform"}
+                5: "decide", 6: "attention", 7: "local", 8: "uniform", 9: "assemble"}
 HALVE = {"kh": 0, "uniform": 1}  # thin_halve_t
 LaunchHook = C.CFUNCTYPE(None, C.c_void_p, C.c_int32, C.c_int32, C.c_int32, C.c_void_p)
 
@@ -38,7 +38,8 @@ class ThinError(RuntimeError):
 
 
 class CompressOpts(C.Structure):
-    _fields_ = [("halve", C.c_int32), ("delta", C.c_void_p)]
+    _fields_ = [("halve", C.c_int32), ("delta", C.c_void_p), ("n_sinks", C.c_int64),
+                ("n_window", C.c_int64), ("logw_out", C.c_void_p)]
 
 
 class Plan(C.Structure):
@@ -72,13 +73,14 @@ def lib():
     L.thin_compress_ex.argtypes = [P, P, I32, I64, I64, I64, I64, I64, I32, P, I64, P, P, SZ,
                                    C.POINTER(CompressOpts), P, I64, P]
     L.thin_attention.argtypes = [P, P, P, I32, I64, I64, I64, I64, I64, P, I64, P, I32, P]
+    L.thin_attention_ex.argtypes = [P, P, P, I32, I64, I64, I64, I64, I64, P, P, I64, P, I32, P]
     L.thin_selftest_gram16.argtypes = [I32, I64, P, P, P]
     L.thin_status_str.argtypes = [C.c_int]
     L.thin_status_str.restype = C.c_char_p
     L.thin_set_launch_hook.argtypes = [LaunchHook, P]
     L.thin_set_launch_hook.restype = C.c_int
     for f in ("thin_plan", "thin_compress", "thin_compress_traced", "thin_compress_ex",
-              "thin_attention", "thin_selftest_gram16"):
+              "thin_attention", "thin_attention_ex", "thin_selftest_gram16"):
         getattr(L, f).restype = C.c_int
     _lib = L
     return L
@@ -126,26 +128,39 @@ def _shape4(t: torch.Tensor, name: str) -> Tuple[int, int, int, int]:
 def thin_compress(K: torch.Tensor, V: torch.Tensor, n_out: int, g: int,
                   uniforms: torch.Tensor, *, idx_out: Optional[torch.Tensor] = None,
                   workspace: Optional[torch.Tensor] = None, trace: bool = False,
-                  halve: str = "kh", delta=None, stream=None):
-    """Compress of every slice; returns idx [B,H,n_out] int32 (and the uint8
-    swap trace when trace=True).  halve="kh" (kernel halving, KH's delta per
-    round in `delta`, default 1/2) or "uniform"; anything but the defaults
-    goes through thin_compress_ex."""
+                  halve: str = "kh", delta=None, n_sinks: int = 0, n_window: int = 0,
+                  return_logw: bool = False, stream=None):
+    """Compress of every slice; returns idx [B,H,n_out] int32, then the uint8
+    swap trace when trace=True, then the float32 log-weights [B,H,m] when
+    return_logw=True (a tuple when either is asked for).  halve="kh" (kernel
+    halving, KH's delta per round in `delta`, default 1/2) or "uniform".  With
+    n_sinks / n_window the first / last rows of every slice are kept exactly
+    and the rows between them thinned to n_out: idx is then [B,H,m] with
+    m = n_sinks + n_out + n_window, and the uniforms and workspace are those of
+    thin_plan for n - n_sinks - n_window rows.  Anything but the defaults goes
+    through thin_compress_ex."""
     B, H, n, d = _shape4(K, "K")
     if tuple(V.shape) != (B, H, n, d) or V.dtype != K.dtype or not V.is_contiguous():
         raise ThinError(THIN_EINVAL, "V must match K")
     if uniforms.dtype != torch.float32 or not uniforms.is_contiguous():
         raise ThinError(THIN_EINVAL, "uniforms must be contiguous float32")
-    plan = thin_plan(B, H, n, d, n_out, g)
+    if n_sinks < 0 or n_window < 0 or n_sinks + n_window >= n:
+        raise ThinError(THIN_EINVAL, "n_sinks and n_window must leave rows to thin")
+    plan = thin_plan(B, H, n - n_sinks - n_window, d, n_out, g)
     dev = K.device
+    m = n_sinks + n_out + n_window
     if idx_out is None:
-        idx_out = torch.empty((B, H, n_out), dtype=torch.int32, device=dev)
+        idx_out = torch.empty((B, H, m), dtype=torch.int32, device=dev)
+    elif tuple(idx_out.shape) != (B, H, m) or idx_out.dtype != torch.int32 \
+            or not idx_out.is_contiguous():
+        raise ThinError(THIN_EINVAL, "idx_out must be contiguous int32 [B,H,m]")
+    lw = torch.empty((B, H, m), dtype=torch.float32, device=dev) if return_logw else None
     if workspace is None:
         workspace = torch.empty(max(plan["workspace_bytes"], 256), dtype=torch.uint8, device=dev)
     tr = None
     args = [_ptr(K), _ptr(V), _dtype_code(K.dtype), B, H, n, d, n_out, g, _ptr(uniforms),
             uniforms.numel(), _ptr(idx_out), _ptr(workspace), workspace.numel()]
-    if halve != "kh" or delta is not None:
+    if halve != "kh" or delta is not None or n_sinks or n_window or return_logw:
         if halve not in HALVE:
             raise ThinError(THIN_EINVAL, f"unknown halving {halve!r}")
         dl = None
@@ -153,13 +168,16 @@ def thin_compress(K: torch.Tensor, V: torch.Tensor, n_out: int, g: int,
             dl = (C.c_double * max(len(delta), 1))(*[float(x) for x in delta])
             if len(delta) < plan["rounds"]:
                 raise ThinError(THIN_EINVAL, "delta needs one value per round")
-        opts = CompressOpts(HALVE[halve], C.cast(dl, C.c_void_p) if dl is not None else None)
+        opts = CompressOpts(HALVE[halve], C.cast(dl, C.c_void_p) if dl is not None else None,
+                            n_sinks, n_window, _ptr(lw) if return_logw else None)
         if trace:
             tr = torch.empty(max(plan["uniforms_total"], 1), dtype=torch.uint8, device=dev)
         rc = lib().thin_compress_ex(*args, C.byref(opts), _ptr(tr) if trace else None,
                                     tr.numel() if trace else 0, _stream(stream))
         _check(rc, "thin_compress_ex")
-        return (idx_out, tr[: plan["uniforms_total"]]) if trace else idx_out
+        out = [idx_out] + ([tr[: plan["uniforms_total"]]] if trace else []) \
+            + ([lw] if return_logw else [])
+        return out[0] if len(out) == 1 else tuple(out)
     if trace:
         tr = torch.empty(max(plan["uniforms_total"], 1), dtype=torch.uint8, device=dev)
         rc = lib().thin_compress_traced(*args, _ptr(tr), tr.numel(), _stream(stream))
@@ -170,9 +188,10 @@ def thin_compress(K: torch.Tensor, V: torch.Tensor, n_out: int, g: int,
 
 
 def thin_attention(Q: torch.Tensor, K: torch.Tensor, V: torch.Tensor, idx: torch.Tensor, *,
-                   out_dtype: torch.dtype = torch.float32, O: Optional[torch.Tensor] = None,
-                   stream=None) -> torch.Tensor:
-    """Attention of every query over its slice's coreset rows idx[b,h,:]."""
+                   logw: Optional[torch.Tensor] = None, out_dtype: torch.dtype = torch.float32,
+                   O: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    """Attention of every query over its slice's coreset rows idx[b,h,:]; with
+    logw (float32 [B,H,n_out]) key j weighs exp(logw[b,h,j]) (thin_attention_ex)."""
     B, H, n_q, d = _shape4(Q, "Q")
     Bk, Hk, n, dk = _shape4(K, "K")
     if (Bk, Hk, dk) != (B, H, d) or tuple(V.shape) != tuple(K.shape):
@@ -185,6 +204,15 @@ def thin_attention(Q: torch.Tensor, K: torch.Tensor, V: torch.Tensor, idx: torch
     n_out = idx.shape[2]
     if O is None:
         O = torch.empty((B, H, n_q, d), dtype=out_dtype, device=Q.device)
+    if logw is not None:
+        if logw.dtype != torch.float32 or tuple(logw.shape) != (B, H, n_out):
+            raise ThinError(THIN_EINVAL, "logw must be float32 [B,H,n_out]")
+        logw = logw.contiguous()
+        rc = lib().thin_attention_ex(_ptr(Q), _ptr(K), _ptr(V), _dtype_code(Q.dtype), B, H, n_q,
+                                     n, d, _ptr(idx), _ptr(logw), n_out, _ptr(O),
+                                     _dtype_code(O.dtype), _stream(stream))
+        _check(rc, "thin_attention_ex")
+        return O
     rc = lib().thin_attention(_ptr(Q), _ptr(K), _ptr(V), _dtype_code(Q.dtype), B, H, n_q, n, d,
                               _ptr(idx), n_out, _ptr(O), _dtype_code(O.dtype), _stream(stream))
     _check(rc, "thin_attention")

@@ -149,12 +149,16 @@ int check_shape(int64_t B, int64_t H, int64_t n, int64_t d) {
 int compress_impl(const void* K, const void* V, int32_t dtype, int64_t B, int64_t H, int64_t n,
                   int64_t d, int64_t n_out, int32_t g, const float* uniforms, int64_t n_uniforms,
                   int32_t* idx_out, void* workspace, size_t workspace_bytes, uint8_t* trace,
-                  int64_t trace_len, int32_t halve, const double* delta, void* stream) {
+                  int64_t trace_len, int32_t halve, const double* delta, int64_t n_sinks,
+                  int64_t n_window, float* logw_out, void* stream) {
   int rc = check_shape(B, H, n, d);
   if (rc) return rc;
   if (dtype != THIN_FP32 && dtype != THIN_BF16) return THIN_EDTYPE;
+  if (n_sinks < 0 || n_window < 0 || n_sinks > n || n_window > n - n_sinks) return THIN_EINVAL;
+  // the rows between the sinks and the window are thinned as a dataset of their own
+  const int64_t nm = n - n_sinks - n_window;
   Levels lv;
-  if (!make_levels(n, n_out, g, &lv) || lv.max_bucket > kMaxBucket) return THIN_EINVAL;
+  if (!make_levels(nm, n_out, g, &lv) || lv.max_bucket > kMaxBucket) return THIN_EINVAL;
   if (!K || !V || !idx_out) return THIN_EINVAL;
   const int64_t S = B * H;
   const int64_t Utot = S * lv.U;
@@ -169,6 +173,15 @@ int compress_impl(const void* K, const void* V, int32_t dtype, int64_t B, int64_
   if ((reinterpret_cast<uintptr_t>(workspace) & 255u) != 0) return THIN_EWORKSPACE;
   Workspace ws = carve(workspace, S, d, lv);
   hipStream_t st = static_cast<hipStream_t>(stream);
+  const size_t esz = dtype == THIN_FP32 ? 4 : 2;
+  const void* Km = static_cast<const unsigned char*>(K) + (size_t)n_sinks * (size_t)d * esz;
+  const void* Vm = static_cast<const unsigned char*>(V) + (size_t)n_sinks * (size_t)d * esz;
+  // With exact rows the last round writes the coreset to whichever index
+  // buffer it does not read, and one more launch lays out the output.
+  const bool assemble = n_sinks > 0 || n_window > 0 || logw_out;
+  auto last_out = [&](const int32_t* in) {
+    return assemble ? (in == ws.buf_b ? ws.buf_a : ws.buf_b) : idx_out;
+  };
 
   hipError_t e = hipSuccess;
   auto ok = [&](hipError_t x) {
@@ -179,22 +192,25 @@ int compress_impl(const void* K, const void* V, int32_t dtype, int64_t B, int64_
     ok(observed(THIN_KERNEL_TRACE_CLEAR, -1, st, [&] { return thin::launch_zero_u8(trace, Utot, st); }));
   if (lv.sub)
     ok(observed(THIN_KERNEL_SUBSAMPLE, -1, st, [&] {
-      return thin::launch_subsample(S, n, lv.n_kept, uniforms, lv.U, ws.buf_a, st);
+      return thin::launch_subsample(S, nm, lv.n_kept, uniforms, lv.U, ws.buf_a, st);
     }));
   const int32_t* cur = lv.sub ? ws.buf_a : nullptr;
   if (lv.L == 0) {
-    ok(observed(THIN_KERNEL_FILL, -1, st, [&] {
-      return thin::launch_fill_rows(S, n_out, cur, lv.n_kept, idx_out, st);
-    }));
+    if (!assemble)
+      ok(observed(THIN_KERNEL_FILL, -1, st, [&] {
+        return thin::launch_fill_rows(S, n_out, cur, lv.n_kept, idx_out, st);
+      }));
   } else if (halve == THIN_HALVE_UNIFORM && thin::uniform_fused_ok(lv.n_kept)) {
+    int32_t* out = last_out(cur);
     ok(observed(THIN_KERNEL_UNIFORM, -1, st, [&] {
       return thin::launch_uniform_compress(S, lv.n_kept, lv.L, cur, uniforms, lv.U,
-                                           lv.sub ? lv.n_kept : 0, idx_out, n_out, trace, st);
+                                           lv.sub ? lv.n_kept : 0, out, n_out, trace, st);
     }));
+    cur = out;
   } else if (halve == THIN_HALVE_UNIFORM) {
     int64_t u_off = lv.sub ? lv.n_kept : 0;
     for (int32_t r = 0; r < lv.L && e == hipSuccess; ++r) {
-      int32_t* out = (r == lv.L - 1) ? idx_out : (cur == ws.buf_b ? ws.buf_a : ws.buf_b);
+      int32_t* out = (r == lv.L - 1) ? last_out(cur) : (cur == ws.buf_b ? ws.buf_a : ws.buf_b);
       ok(observed(THIN_KERNEL_UNIFORM, r, st, [&] {
         return thin::launch_uniform_halve(S, lv.n_r[r], cur, uniforms, lv.U, u_off, out, trace,
                                           st);
@@ -204,14 +220,15 @@ int compress_impl(const void* K, const void* V, int32_t dtype, int64_t B, int64_
     }
   } else {
     ok(observed(THIN_KERNEL_VMAX, -1, st,
-                [&] { return thin::launch_vmax(dtype, V, S, n, d, ws.vmax_bits, st); }));
+                [&] { return thin::launch_vmax(dtype, Vm, S, nm, n, d, ws.vmax_bits, st); }));
     int64_t u_off = lv.sub ? lv.n_kept : 0;
     for (int32_t r = 0; r < lv.L && e == hipSuccess; ++r) {
-      int32_t* out = (r == lv.L - 1) ? idx_out : (cur == ws.buf_b ? ws.buf_a : ws.buf_b);
+      int32_t* out = (r == lv.L - 1) ? last_out(cur) : (cur == ws.buf_b ? ws.buf_a : ws.buf_b);
       thin::HalveArgs a;
-      a.K = K;
-      a.V = V;
-      a.n = n;
+      a.K = Km;
+      a.V = Vm;
+      a.n = nm;
+      a.ld = n;
       a.vmax_bits = ws.vmax_bits;
       a.idx_in = cur;
       a.n_r = lv.n_r[r];
@@ -254,6 +271,16 @@ int compress_impl(const void* K, const void* V, int32_t dtype, int64_t B, int64_
       cur = out;
     }
   }
+  if (assemble && e == hipSuccess) {
+    // after any round the coreset sits n_out apart per slice; with none, the
+    // (subsampled or identity) rows n_kept apart
+    const int64_t stride = lv.L == 0 ? lv.n_kept : n_out;
+    const float lw = (float)log((double)nm / (double)n_out);
+    ok(observed(THIN_KERNEL_ASSEMBLE, -1, st, [&] {
+      return thin::launch_assemble(S, n, n_sinks, n_out, n_window, cur, stride, idx_out,
+                                   logw_out, lw, st);
+    }));
+  }
   return e == hipSuccess ? THIN_OK : THIN_EHIP;
 }
 
@@ -285,7 +312,8 @@ int thin_compress(const void* K, const void* V, int32_t dtype, int64_t B, int64_
                   int64_t n_uniforms, int32_t* idx_out, void* workspace,
                   size_t workspace_bytes, void* stream) {
   return compress_impl(K, V, dtype, B, H, n, d, n_out, g, uniforms, n_uniforms, idx_out,
-                       workspace, workspace_bytes, nullptr, 0, THIN_HALVE_KH, nullptr, stream);
+                       workspace, workspace_bytes, nullptr, 0, THIN_HALVE_KH, nullptr, 0, 0,
+                       nullptr, stream);
 }
 
 int thin_compress_traced(const void* K, const void* V, int32_t dtype, int64_t B, int64_t H,
@@ -296,7 +324,7 @@ int thin_compress_traced(const void* K, const void* V, int32_t dtype, int64_t B,
   if (!swap_trace) return THIN_EINVAL;
   return compress_impl(K, V, dtype, B, H, n, d, n_out, g, uniforms, n_uniforms, idx_out,
                        workspace, workspace_bytes, swap_trace, trace_len, THIN_HALVE_KH, nullptr,
-                       stream);
+                       0, 0, nullptr, stream);
 }
 
 int thin_compress_ex(const void* K, const void* V, int32_t dtype, int64_t B, int64_t H,
@@ -307,12 +335,20 @@ int thin_compress_ex(const void* K, const void* V, int32_t dtype, int64_t B, int
   if (!opts) return THIN_EINVAL;
   return compress_impl(K, V, dtype, B, H, n, d, n_out, g, uniforms, n_uniforms, idx_out,
                        workspace, workspace_bytes, swap_trace, trace_len, opts->halve,
-                       opts->delta, stream);
+                       opts->delta, opts->n_sinks, opts->n_window, opts->logw_out, stream);
 }
 
 int thin_attention(const void* Q, const void* K, const void* V, int32_t dtype, int64_t B,
                    int64_t H, int64_t n_q, int64_t n, int64_t d, const int32_t* idx,
                    int64_t n_out, void* O, int32_t out_dtype, void* stream) {
+  return thin_attention_ex(Q, K, V, dtype, B, H, n_q, n, d, idx, nullptr, n_out, O, out_dtype,
+                           stream);
+}
+
+int thin_attention_ex(const void* Q, const void* K, const void* V, int32_t dtype, int64_t B,
+                      int64_t H, int64_t n_q, int64_t n, int64_t d, const int32_t* idx,
+                      const float* logw, int64_t n_out, void* O, int32_t out_dtype,
+                      void* stream) {
   int rc = check_shape(B, H, n, d);
   if (rc) return rc;
   if (n_q < 1 || n_q > kMaxRows || n_out < 1 || n_out > ((int64_t)1 << 30)) return THIN_EINVAL;
@@ -321,7 +357,8 @@ int thin_attention(const void* Q, const void* K, const void* V, int32_t dtype, i
   if (!Q || !K || !V || !idx || !O) return THIN_EINVAL;
   hipStream_t st = static_cast<hipStream_t>(stream);
   hipError_t e = observed(THIN_KERNEL_ATTENTION, -1, st, [&] {
-    return thin::launch_attention(dtype, d, out_dtype, Q, K, V, idx, B * H, n, n_q, n_out, O, st);
+    return thin::launch_attention(dtype, d, out_dtype, Q, K, V, idx, logw, B * H, n, n_q, n_out,
+                                  O, st);
   });
   return e == hipSuccess ? THIN_OK : THIN_EHIP;
 }

@@ -1,6 +1,9 @@
 // Coreset attention on gfx950: every query of a slice attends over the n_out
 // rows idx[s, :] of that slice's K/V (Sec. 2.1 eq. unmaskedatt on the
-// coreset; eq. def:att_approx with equal weights, which cancel).
+// coreset; eq. def:att_approx with equal weights, which cancel).  The
+// weighted variant (W) gives key j the weight exp(logw[s, j]): its raw score
+// <q, k_j> gets the bias sqrt(d) * logw[s, j], staged in LDS beside the keys
+// (a key past n_out or of weight 0 has bias -inf, which also masks it).
 //
 // One workgroup = 4 waves = 128 queries of one slice.  The coreset is walked
 // in chunks of 64 keys staged in LDS (gathered through idx); scores S^T =
@@ -31,7 +34,7 @@ struct AttnLds {
   // V chunk: bf16 is stored transposed [D][KC] (+8 elements pad), fp32 row-major.
   static constexpr int v_stride = Elem<T>::bytes == 2 ? (KC + 8) * 2 : D * 4 + 16;
   static constexpr int v_rows = Elem<T>::bytes == 2 ? D : KC;
-  static constexpr int bytes = KC * k_stride + v_rows * v_stride;
+  static constexpr int bytes = KC * k_stride + v_rows * v_stride + KC * 4;
 };
 
 template <typename TO>
@@ -48,21 +51,25 @@ __device__ __forceinline__ void store4<bf16_t>(bf16_t* p, float a, float b, floa
   *reinterpret_cast<uint2*>(p) = make_uint2(__builtin_bit_cast(uint32_t, lo), __builtin_bit_cast(uint32_t, hi));
 }
 
-template <typename T, int D, typename TO>
+template <typename T, int D, typename TO, bool W>
 __global__ __launch_bounds__(64 * WAVES) void coreset_attn_kernel(
     const T* __restrict__ Q, const T* __restrict__ K, const T* __restrict__ V,
-    const int32_t* __restrict__ idx, int64_t n, int64_t n_q, int n_out, TO* __restrict__ O) {
+    const int32_t* __restrict__ idx, const float* __restrict__ logw, int64_t n, int64_t n_q,
+    int n_out, TO* __restrict__ O) {
   constexpr int NV = Frag<T, D>::NV;
   constexpr bool BF = Elem<T>::bytes == 2;
   using L = AttnLds<T, D>;
   __shared__ __align__(16) unsigned char lds[L::bytes];
   unsigned char* sK = lds;
   unsigned char* sV = lds + KC * L::k_stride;
+  float* sB = reinterpret_cast<float*>(sV + L::v_rows * L::v_stride);
 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int m16 = lane & 15, g = lane >> 4;
   const int64_t s = blockIdx.y;
   const int64_t q0 = (int64_t)blockIdx.x * QPB + wave * 16 * QT;
+  const float* Ws = W ? logw + s * (int64_t)n_out : nullptr;
+  const float sqrt_d = (float)sqrt((double)D);
   const T* Ks = K + s * n * D;
   const T* Vs = V + s * n * D;
   const int32_t* Is = idx + s * (int64_t)n_out;
@@ -89,6 +96,8 @@ __global__ __launch_bounds__(64 * WAVES) void coreset_attn_kernel(
   for (int c0 = 0; c0 < n_out; c0 += KC) {
     const int kc = min(KC, n_out - c0);
     __syncthreads();
+    if (W && threadIdx.x < KC)
+      sB[threadIdx.x] = (int)threadIdx.x < kc ? Ws[c0 + threadIdx.x] * sqrt_d : -INFINITY;
     for (int w = threadIdx.x; w < KC * WPR; w += 64 * WAVES) {
       const int key = w / WPR, wi = w % WPR;
       uint4 kw = make_uint4(0, 0, 0, 0), vw = make_uint4(0, 0, 0, 0);
@@ -126,10 +135,14 @@ __global__ __launch_bounds__(64 * WAVES) void coreset_attn_kernel(
       for (int kt = 0; kt < 4; ++kt) {
         floatx4_t z = {0.f, 0.f, 0.f, 0.f};
         z = mma_rows<T, D>(Ak[kt], Bq[qt], z);
+        if (W) {
+          const float4 b = *reinterpret_cast<const float4*>(sB + kt * 16 + 4 * g);
+          z[0] += b.x; z[1] += b.y; z[2] += b.z; z[3] += b.w;
+        }
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
           const int key = kt * 16 + 4 * g + i;
-          sc[kt][i] = key < kc ? z[i] : -INFINITY;
+          sc[kt][i] = W || key < kc ? z[i] : -INFINITY;
           mx = fmaxf(mx, sc[kt][i]);
         }
       }
@@ -233,7 +246,7 @@ struct ResLds {
   static constexpr int NK = 16 * NKT;          // padded key count
   static constexpr int k_stride = D * 2 + 16;  // bytes per K row
   static constexpr int v_stride = NK * 2 + 8;  // bytes per V^T row (8-byte aligned)
-  static constexpr int bytes = NK * k_stride + D * v_stride;
+  static constexpr int bytes = NK * k_stride + D * v_stride + NK * 4;
 };
 
 typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
@@ -251,21 +264,27 @@ __device__ __forceinline__ uint32_t pack_hi(uint32_t x, uint32_t y) { return (x 
 // Target of the output stores of query rows past a workgroup's range (never read).
 __device__ __align__(16) float g_attn_sink[256];
 
-template <int D, int NKT, int QTR, int WR, typename TO>
+template <int D, int NKT, int QTR, int WR, typename TO, bool W>
 __global__ __launch_bounds__(64 * WR) void coreset_attn_res_kernel(
     const bf16_t* __restrict__ Q, const bf16_t* __restrict__ K, const bf16_t* __restrict__ V,
-    const int32_t* __restrict__ idx, int64_t n, int64_t n_q, int n_out, int64_t q_per_wg,
-    TO* __restrict__ O) {
+    const int32_t* __restrict__ idx, const float* __restrict__ logw, int64_t n, int64_t n_q,
+    int n_out, int64_t q_per_wg, TO* __restrict__ O) {
   using L = ResLds<D, NKT>;
   constexpr int NK = L::NK;
   constexpr int NV = Frag<bf16_t, D>::NV;
   extern __shared__ __align__(16) unsigned char lds[];
   unsigned char* sK = lds;
   unsigned char* sV = lds + NK * L::k_stride;
+  float* sB = reinterpret_cast<float*>(sV + D * L::v_stride);
 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int m16 = lane & 15, g = lane >> 4;
   const int64_t s = blockIdx.y;
+  if (W) {
+    const float sqrt_d = (float)sqrt((double)D);
+    for (int k = threadIdx.x; k < NK; k += 64 * WR)
+      sB[k] = k < n_out ? logw[s * (int64_t)n_out + k] * sqrt_d : -INFINITY;
+  }
   const bf16_t* Ks = K + s * n * D;
   const bf16_t* Vs = V + s * n * D;
   const int32_t* Is = idx + s * (int64_t)n_out;
@@ -374,13 +393,18 @@ __global__ __launch_bounds__(64 * WR) void coreset_attn_res_kernel(
     for (int qt = 0; qt < QTR; ++qt) {
       float mx = -INFINITY;
 #pragma unroll
-      for (int kt = 0; kt < NKT; ++kt)
+      for (int kt = 0; kt < NKT; ++kt) {
+        if (W) {
+          const float4 b = *reinterpret_cast<const float4*>(sB + kt * 16 + 4 * g);
+          sc[qt][kt][0] += b.x; sc[qt][kt][1] += b.y; sc[qt][kt][2] += b.z; sc[qt][kt][3] += b.w;
+        }
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
           const int key = kt * 16 + 4 * g + i;
-          if (key >= n_out) sc[qt][kt][i] = -INFINITY;
+          if (!W && key >= n_out) sc[qt][kt][i] = -INFINITY;
           mx = fmaxf(mx, sc[qt][kt][i]);
         }
+      }
       mx = fmaxf(mx, __shfl_xor(mx, 16));
       mx = fmaxf(mx, __shfl_xor(mx, 32));
       float l = 0.f;
@@ -479,12 +503,12 @@ __global__ __launch_bounds__(64 * WR) void coreset_attn_res_kernel(
   }
 }
 
-template <int D, int NKT, int QTR, int WR, typename TO>
-hipError_t launch_attn_res(const void* Q, const void* K, const void* V, const int32_t* idx,
-                           int64_t S, int64_t n, int64_t n_q, int64_t n_out, void* O,
-                           hipStream_t st) {
+template <int D, int NKT, int QTR, int WR, typename TO, bool W>
+hipError_t launch_attn_res_w(const void* Q, const void* K, const void* V, const int32_t* idx,
+                             const float* logw, int64_t S, int64_t n, int64_t n_q,
+                             int64_t n_out, void* O, hipStream_t st) {
   using L = ResLds<D, NKT>;
-  auto kern = coreset_attn_res_kernel<D, NKT, QTR, WR, TO>;
+  auto kern = coreset_attn_res_kernel<D, NKT, QTR, WR, TO, W>;
   const size_t lds = L::bytes;
   if (lds > 64 * 1024) {
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
@@ -501,8 +525,17 @@ hipError_t launch_attn_res(const void* Q, const void* K, const void* V, const in
   const int64_t wgs = (n_q + q_per_wg - 1) / q_per_wg;
   dim3 grid((unsigned)wgs, (unsigned)S), block(64 * WR);
   hipLaunchKernelGGL(kern, grid, block, lds, st, (const bf16_t*)Q, (const bf16_t*)K,
-                     (const bf16_t*)V, idx, n, n_q, (int)n_out, q_per_wg, (TO*)O);
+                     (const bf16_t*)V, idx, logw, n, n_q, (int)n_out, q_per_wg, (TO*)O);
   return hipGetLastError();
+}
+
+template <int D, int NKT, int QTR, int WR, typename TO>
+hipError_t launch_attn_res(const void* Q, const void* K, const void* V, const int32_t* idx,
+                           const float* logw, int64_t S, int64_t n, int64_t n_q, int64_t n_out,
+                           void* O, hipStream_t st) {
+  if (logw)
+    return launch_attn_res_w<D, NKT, QTR, WR, TO, true>(Q, K, V, idx, logw, S, n, n_q, n_out, O, st);
+  return launch_attn_res_w<D, NKT, QTR, WR, TO, false>(Q, K, V, idx, logw, S, n, n_q, n_out, O, st);
 }
 
 // 16-query tiles per wave per step and waves per workgroup of the resident kernel
@@ -515,35 +548,39 @@ hipError_t launch_attn_res(const void* Q, const void* K, const void* V, const in
 
 template <int D, typename TO>
 hipError_t launch_attn_res_d(int64_t n_out, const void* Q, const void* K, const void* V,
-                             const int32_t* idx, int64_t S, int64_t n, int64_t n_q, void* O,
-                             hipStream_t st, bool* used) {
+                             const int32_t* idx, const float* logw, int64_t S, int64_t n,
+                             int64_t n_q, void* O, hipStream_t st, bool* used) {
   *used = true;
-  if (n_out <= 32) return launch_attn_res<D, 2, ATTN_RES_QTR, ATTN_RES_WAVES, TO>(Q, K, V, idx, S, n, n_q, n_out, O, st);
-  if (n_out <= 64) return launch_attn_res<D, 4, ATTN_RES_QTR, ATTN_RES_WAVES, TO>(Q, K, V, idx, S, n, n_q, n_out, O, st);
-  if (n_out <= 128) return launch_attn_res<D, 8, ATTN_RES_QTR, ATTN_RES_WAVES, TO>(Q, K, V, idx, S, n, n_q, n_out, O, st);
-  if (n_out <= 256 && D <= 128) return launch_attn_res<D, 16, ATTN_RES_QTR, ATTN_RES_WAVES, TO>(Q, K, V, idx, S, n, n_q, n_out, O, st);
+  if (n_out <= 32) return launch_attn_res<D, 2, ATTN_RES_QTR, ATTN_RES_WAVES, TO>(Q, K, V, idx, logw, S, n, n_q, n_out, O, st);
+  if (n_out <= 64) return launch_attn_res<D, 4, ATTN_RES_QTR, ATTN_RES_WAVES, TO>(Q, K, V, idx, logw, S, n, n_q, n_out, O, st);
+  if (n_out <= 128) return launch_attn_res<D, 8, ATTN_RES_QTR, ATTN_RES_WAVES, TO>(Q, K, V, idx, logw, S, n, n_q, n_out, O, st);
+  if (n_out <= 256 && D <= 128) return launch_attn_res<D, 16, ATTN_RES_QTR, ATTN_RES_WAVES, TO>(Q, K, V, idx, logw, S, n, n_q, n_out, O, st);
   *used = false;
   return hipSuccess;
 }
 
 template <typename T, int D, typename TO>
 hipError_t launch_attn_t(const void* Q, const void* K, const void* V, const int32_t* idx,
-                         int64_t S, int64_t n, int64_t n_q, int64_t n_out, void* O,
-                         hipStream_t st) {
+                         const float* logw, int64_t S, int64_t n, int64_t n_q, int64_t n_out,
+                         void* O, hipStream_t st) {
   dim3 grid((unsigned)((n_q + QPB - 1) / QPB), (unsigned)S), block(64 * WAVES);
-  hipLaunchKernelGGL((coreset_attn_kernel<T, D, TO>), grid, block, 0, st, (const T*)Q,
-                     (const T*)K, (const T*)V, idx, n, n_q, (int)n_out, (TO*)O);
+  if (logw)
+    hipLaunchKernelGGL((coreset_attn_kernel<T, D, TO, true>), grid, block, 0, st, (const T*)Q,
+                       (const T*)K, (const T*)V, idx, logw, n, n_q, (int)n_out, (TO*)O);
+  else
+    hipLaunchKernelGGL((coreset_attn_kernel<T, D, TO, false>), grid, block, 0, st, (const T*)Q,
+                       (const T*)K, (const T*)V, idx, logw, n, n_q, (int)n_out, (TO*)O);
   return hipGetLastError();
 }
 
 template <typename T, typename TO>
 hipError_t launch_attn_d(int64_t d, const void* Q, const void* K, const void* V,
-                         const int32_t* idx, int64_t S, int64_t n, int64_t n_q, int64_t n_out,
-                         void* O, hipStream_t st) {
+                         const int32_t* idx, const float* logw, int64_t S, int64_t n,
+                         int64_t n_q, int64_t n_out, void* O, hipStream_t st) {
   switch (d) {
-    case 32: return launch_attn_t<T, 32, TO>(Q, K, V, idx, S, n, n_q, n_out, O, st);
-    case 64: return launch_attn_t<T, 64, TO>(Q, K, V, idx, S, n, n_q, n_out, O, st);
-    case 128: return launch_attn_t<T, 128, TO>(Q, K, V, idx, S, n, n_q, n_out, O, st);
+    case 32: return launch_attn_t<T, 32, TO>(Q, K, V, idx, logw, S, n, n_q, n_out, O, st);
+    case 64: return launch_attn_t<T, 64, TO>(Q, K, V, idx, logw, S, n, n_q, n_out, O, st);
+    case 128: return launch_attn_t<T, 128, TO>(Q, K, V, idx, logw, S, n, n_q, n_out, O, st);
     default: return hipErrorInvalidValue;
   }
 }
@@ -551,23 +588,27 @@ hipError_t launch_attn_d(int64_t d, const void* Q, const void* K, const void* V,
 }  // namespace
 
 hipError_t launch_attention(int dtype, int64_t d, int out_dtype, const void* Q, const void* K,
-                            const void* V, const int32_t* idx, int64_t S, int64_t n,
-                            int64_t n_q, int64_t n_out, void* O, hipStream_t st) {
+                            const void* V, const int32_t* idx, const float* logw, int64_t S,
+                            int64_t n, int64_t n_q, int64_t n_out, void* O, hipStream_t st) {
   if (dtype == 0) {
-    if (out_dtype == 0) return launch_attn_d<float, float>(d, Q, K, V, idx, S, n, n_q, n_out, O, st);
-    return launch_attn_d<float, bf16_t>(d, Q, K, V, idx, S, n, n_q, n_out, O, st);
+    if (out_dtype == 0)
+      return launch_attn_d<float, float>(d, Q, K, V, idx, logw, S, n, n_q, n_out, O, st);
+    return launch_attn_d<float, bf16_t>(d, Q, K, V, idx, logw, S, n, n_q, n_out, O, st);
   }
   bool used = false;
   hipError_t e = hipSuccess;
   if (d == 64)
-    e = out_dtype == 0 ? launch_attn_res_d<64, float>(n_out, Q, K, V, idx, S, n, n_q, O, st, &used)
-                       : launch_attn_res_d<64, bf16_t>(n_out, Q, K, V, idx, S, n, n_q, O, st, &used);
+    e = out_dtype == 0
+            ? launch_attn_res_d<64, float>(n_out, Q, K, V, idx, logw, S, n, n_q, O, st, &used)
+            : launch_attn_res_d<64, bf16_t>(n_out, Q, K, V, idx, logw, S, n, n_q, O, st, &used);
   else if (d == 128)
-    e = out_dtype == 0 ? launch_attn_res_d<128, float>(n_out, Q, K, V, idx, S, n, n_q, O, st, &used)
-                       : launch_attn_res_d<128, bf16_t>(n_out, Q, K, V, idx, S, n, n_q, O, st, &used);
+    e = out_dtype == 0
+            ? launch_attn_res_d<128, float>(n_out, Q, K, V, idx, logw, S, n, n_q, O, st, &used)
+            : launch_attn_res_d<128, bf16_t>(n_out, Q, K, V, idx, logw, S, n, n_q, O, st, &used);
   if (used) return e;
-  if (out_dtype == 0) return launch_attn_d<bf16_t, float>(d, Q, K, V, idx, S, n, n_q, n_out, O, st);
-  return launch_attn_d<bf16_t, bf16_t>(d, Q, K, V, idx, S, n, n_q, n_out, O, st);
+  if (out_dtype == 0)
+    return launch_attn_d<bf16_t, float>(d, Q, K, V, idx, logw, S, n, n_q, n_out, O, st);
+  return launch_attn_d<bf16_t, bf16_t>(d, Q, K, V, idx, logw, S, n, n_q, n_out, O, st);
 }
 
 }  // namespace thin

@@ -24,15 +24,17 @@ __device__ __forceinline__ float wave_max_f(float v) {
 }
 
 // ---------------------------------------------------------------------------
-// v_max = max_i ||v_i||_inf over all n rows of a slice (Sec. 2.1, eq. katt).
+// v_max = max_i ||v_i||_inf over the n thinned rows of a slice (Sec. 2.1, eq.
+// katt); consecutive slices start slice_words 16-byte words apart.
 // grid (chunks, S); the per-slice maximum is merged with an integer atomicMax
 // on the float's bit pattern (valid for non-negative floats).
 // ---------------------------------------------------------------------------
 template <typename T>
 __global__ __launch_bounds__(256) void vmax_kernel(const T* V, int64_t words_per_slice,
-                                                   int64_t words_per_block, uint32_t* vmax_bits) {
+                                                   int64_t slice_words, int64_t words_per_block,
+                                                   uint32_t* vmax_bits) {
   const int64_t s = blockIdx.y;
-  const uint4* base = reinterpret_cast<const uint4*>(V) + s * words_per_slice;
+  const uint4* base = reinterpret_cast<const uint4*>(V) + s * slice_words;
   int64_t w0 = (int64_t)blockIdx.x * words_per_block;
   int64_t w1 = w0 + words_per_block;
   if (w1 > words_per_slice) w1 = words_per_slice;
@@ -110,6 +112,29 @@ __global__ void fill_rows_kernel(int64_t n_out, const int32_t* src, int64_t src_
   const int64_t j = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (j >= n_out) return;
   dst[s * n_out + j] = src ? src[s * src_stride + j] : (int32_t)j;
+}
+
+// Output of a compress with exact sink and window rows: row j of slice s is
+// sink j (j < ns), then coreset row ns + src[s * src_stride + j - ns] (src
+// null = the identity) for n_out rows, then window row n - nw + ...; its
+// log-weight (logw nullable) is 0 for exact rows and lw_core for coreset rows.
+__global__ void assemble_kernel(int64_t n, int64_t ns, int64_t n_out, int64_t nw,
+                                const int32_t* src, int64_t src_stride, int32_t* dst,
+                                float* logw, float lw_core) {
+  const int64_t s = blockIdx.y;
+  const int64_t m = ns + n_out + nw;
+  const int64_t j = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (j >= m) return;
+  int64_t r = j;
+  float w = 0.0f;
+  if (j >= ns + n_out) {
+    r = n - nw + (j - ns - n_out);
+  } else if (j >= ns) {
+    r = ns + (src ? (int64_t)src[s * src_stride + j - ns] : j - ns);
+    w = lw_core;
+  }
+  dst[s * m + j] = (int32_t)r;
+  if (logw) logw[s * m + j] = w;
 }
 
 // ---------------------------------------------------------------------------
@@ -535,8 +560,8 @@ void pair_scores_kernel(HalveArgs a) {
   const int jt1 = min(jt0 + (own ? GT : a.ch), NT);
   const int ntile = jt1 - jt0;
 
-  const T* K = reinterpret_cast<const T*>(a.K) + s * a.n * D;
-  const T* V = reinterpret_cast<const T*>(a.V) + s * a.n * D;
+  const T* K = reinterpret_cast<const T*>(a.K) + s * a.ld * D;
+  const T* V = reinterpret_cast<const T*>(a.V) + s * a.ld * D;
   const int32_t* rows_in = a.idx_in ? a.idx_in + s * a.n_r + t * (int64_t)N : nullptr;
   const int64_t row_base = t * (int64_t)N;
   const float vmax = __uint_as_float(a.vmax_bits[s]);
@@ -1466,21 +1491,21 @@ hipError_t launch_decide(const HalveArgs& a0, int64_t nbk, hipStream_t st) {
   return launch_pass_w<6, 3>(a, nbk, st);
 }
 
-hipError_t launch_vmax(int dtype, const void* V, int64_t S, int64_t n, int64_t d,
+hipError_t launch_vmax(int dtype, const void* V, int64_t S, int64_t n, int64_t ld, int64_t d,
                        uint32_t* vmax_bits, hipStream_t st) {
   hipLaunchKernelGGL(zero_u32_kernel, dim3((unsigned)((S + 255) / 256)), dim3(256), 0, st,
                      vmax_bits, S);
   const int64_t bytes = dtype == 0 ? 4 : 2;
-  const int64_t words = n * d * bytes / 16;
+  const int64_t words = n * d * bytes / 16, slice_words = ld * d * bytes / 16;
   const int64_t per_block = 16384;  // 256 KiB of V per workgroup
   const int64_t chunks = (words + per_block - 1) / per_block;
   dim3 grid((unsigned)chunks, (unsigned)S);
   if (dtype == 0)
     hipLaunchKernelGGL(vmax_kernel<float>, grid, dim3(256), 0, st, (const float*)V, words,
-                       per_block, vmax_bits);
+                       slice_words, per_block, vmax_bits);
   else
     hipLaunchKernelGGL(vmax_kernel<bf16_t>, grid, dim3(256), 0, st, (const bf16_t*)V, words,
-                       per_block, vmax_bits);
+                       slice_words, per_block, vmax_bits);
   return hipGetLastError();
 }
 
@@ -1495,6 +1520,16 @@ hipError_t launch_fill_rows(int64_t S, int64_t n_out, const int32_t* src, int64_
                             int32_t* dst, hipStream_t st) {
   dim3 grid((unsigned)((n_out + 255) / 256), (unsigned)S);
   hipLaunchKernelGGL(fill_rows_kernel, grid, dim3(256), 0, st, n_out, src, src_stride, dst);
+  return hipGetLastError();
+}
+
+hipError_t launch_assemble(int64_t S, int64_t n, int64_t ns, int64_t n_out, int64_t nw,
+                           const int32_t* src, int64_t src_stride, int32_t* dst, float* logw,
+                           float lw_core, hipStream_t st) {
+  const int64_t m = ns + n_out + nw;
+  dim3 grid((unsigned)((m + 255) / 256), (unsigned)S);
+  hipLaunchKernelGGL(assemble_kernel, grid, dim3(256), 0, st, n, ns, n_out, nw, src, src_stride,
+                     dst, logw, lw_core);
   return hipGetLastError();
 }
 

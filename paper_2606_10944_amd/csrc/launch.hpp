@@ -10,7 +10,8 @@ namespace thin {
 struct HalveArgs {
   const void* K;
   const void* V;
-  int64_t n;                  // rows per slice of K/V
+  int64_t n;                  // thinned rows per slice
+  int64_t ld;                 // rows between consecutive slices of K/V (>= n)
   const uint32_t* vmax_bits;  // [S] bit pattern of v_max (non-negative float)
   const int32_t* idx_in;      // [S, n_r] rows entering this round, or null = identity
   int64_t n_r;                // rows per slice entering this round
@@ -40,13 +41,19 @@ struct HalveArgs {
 };
 
 // dtype: 0 = fp32, 1 = bf16.  Returns a hipError_t.
-hipError_t launch_vmax(int dtype, const void* V, int64_t S, int64_t n, int64_t d,
+// v_max of n rows per slice, slices ld rows apart.
+hipError_t launch_vmax(int dtype, const void* V, int64_t S, int64_t n, int64_t ld, int64_t d,
                        uint32_t* vmax_bits, hipStream_t st);
 hipError_t launch_subsample(int64_t S, int64_t n, int64_t n_kept, const float* U,
                             int64_t u_slice, int32_t* idx0, hipStream_t st);
 hipError_t launch_fill_rows(int64_t S, int64_t n_out, const int32_t* src, int64_t src_stride,
                             int32_t* dst, hipStream_t st);
 hipError_t launch_zero_u8(uint8_t* p, int64_t count, hipStream_t st);
+// idx [S, ns + n_out + nw] = sinks, ns + coreset (src, stride src_stride; null =
+// identity), window rows of an n-row slice; logw (nullable) 0 or lw_core.
+hipError_t launch_assemble(int64_t S, int64_t n, int64_t ns, int64_t n_out, int64_t nw,
+                           const int32_t* src, int64_t src_stride, int32_t* dst, float* logw,
+                           float lw_core, hipStream_t st);
 // One round of uniform halving of every slice: pair p of a slice keeps row
 // 2p+1 of the round's input iff its uniform is below 1/2.
 hipError_t launch_uniform_halve(int64_t S, int64_t n_r, const int32_t* idx_in, const float* U,
@@ -70,9 +77,10 @@ hipError_t launch_decide(const HalveArgs& a, int64_t nbk, hipStream_t st);
 int64_t halve_local_rows(int dtype, int64_t d);
 hipError_t launch_local(int dtype, int64_t d, const HalveArgs& a, int64_t nbk, hipStream_t st);
 
+// logw (nullable) [S, n_out]: log-weight of every coreset key.
 hipError_t launch_attention(int dtype, int64_t d, int out_dtype, const void* Q, const void* K,
-                            const void* V, const int32_t* idx, int64_t S, int64_t n,
-                            int64_t n_q, int64_t n_out, void* O, hipStream_t st);
+                            const void* V, const int32_t* idx, const float* logw, int64_t S,
+                            int64_t n, int64_t n_q, int64_t n_out, void* O, hipStream_t st);
 
 hipError_t launch_gram16(int dtype, int64_t d, const void* rows, float* out, hipStream_t st);
 

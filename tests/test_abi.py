@@ -110,6 +110,21 @@ def test_compress_ex_validates_options_before_launch():
     assert call(0, [0.5, 0.5, 0.5, 0.5, float("nan")]) == _lib.THIN_EINVAL
 
 
+def test_compress_ex_validates_sinks_and_window_before_launch():
+    L = _lib.lib()
+
+    def call(ns, nw):
+        o = _lib.CompressOpts(0, None, ns, nw, None)
+        return L.thin_compress_ex(FAKE, FAKE, 1, 1, 1, 1024, 64, 32, 2, FAKE, 1 << 20, FAKE,
+                                  C.c_void_p(0x100000), 1 << 30, C.byref(o), None, 0, None)
+
+    assert call(-1, 0) == _lib.THIN_EINVAL
+    assert call(0, -1) == _lib.THIN_EINVAL
+    assert call(1025, 0) == _lib.THIN_EINVAL
+    assert call(500, 500) == _lib.THIN_EINVAL   # 24 rows left for n_out = 32
+    assert call(0, 1024) == _lib.THIN_EINVAL
+
+
 def test_traced_compress_checks_trace_length():
     L = _lib.lib()
     rc = L.thin_compress_traced(FAKE, FAKE, 1, 1, 1, 1024, 64, 32, 2, FAKE, 992, FAKE,
@@ -135,6 +150,22 @@ def test_attention_validates_before_launch():
     assert call(n_q=0) == _lib.THIN_EINVAL
     assert call(O=None) == _lib.THIN_EINVAL
     assert call(dtype=3) == _lib.THIN_EDTYPE
+    assert call(od=2) == _lib.THIN_EDTYPE
+
+
+def test_weighted_attention_validates_before_launch():
+    L = _lib.lib()
+
+    def call(**kw):
+        a = dict(dtype=1, n_q=8, d=64, n_out=4, od=0)
+        a.update(kw)
+        return L.thin_attention_ex(FAKE, FAKE, FAKE, a["dtype"], 1, 1, a["n_q"], 16, a["d"], FAKE,
+                                   FAKE, a["n_out"], FAKE, a["od"], None)
+
+    assert call(d=80) == _lib.THIN_EINVAL
+    assert call(n_out=0) == _lib.THIN_EINVAL
+    assert call(n_q=0) == _lib.THIN_EINVAL
+    assert call(dtype=7) == _lib.THIN_EDTYPE
     assert call(od=2) == _lib.THIN_EDTYPE
 
 

@@ -303,3 +303,125 @@ def test_uniform_halving_runs_every_round_in_one_launch():
         torch.cuda.synchronize()
     got = [(k, r) for k, r, _ in lt.records()]
     assert got == [("subsample", -1), ("uniform", -1)]
+
+
+# ---------------------------------------------------------------------------
+# Exact sink / window rows and weighted attention (eq. def:att_approx)
+# ---------------------------------------------------------------------------
+SINKS = [
+    # the n_sinks = n_window = 32 setting of the long-context experiments, full size
+    dict(name="long", ns=32, nw=32, halve="kh", slices=[0, 37, 63], q_rows=512),
+    # a few sinks and a longer window
+    dict(name="imggen", ns=4, nw=64, halve="kh", slices=None, q_rows=None),
+    dict(name="vit", ns=1, nw=0, halve="kh", slices=[0, 17, 31], q_rows=None),
+    dict(name="tiny", ns=0, nw=9, halve="uniform", slices=None, q_rows=None),
+]
+
+
+def _check_sinks_case(w, ns, nw, halve, slices, q_rows):
+    Q, K, V = W.make_qkv(w)
+    nm = w.n - ns - nw
+    plan = thin_plan(w.B, w.H, nm, w.d, w.n_out, w.g)
+    U = W.make_uniforms(w, plan["uniforms_total"])
+    Kd, Vd = K.to(DEV), V.to(DEV)
+    idx, tr, lw = thin_compress(Kd, Vd, w.n_out, w.g, U.to(DEV), trace=True, halve=halve,
+                                n_sinks=ns, n_window=nw, return_logw=True)
+    O = thin_attention(Q.to(DEV), Kd, Vd, idx, logw=lw)
+    torch.cuda.synchronize()
+    idx, tr, lw, O = idx.cpu().numpy(), tr.cpu().numpy(), lw.cpu().numpy(), O.cpu().numpy()
+    m = ns + w.n_out + nw
+    assert idx.shape == (w.B, w.H, m)
+    Us = U.numpy().reshape(w.S, -1) if U.numel() else np.zeros((w.S, 1), np.float32)
+    ts = tr.reshape(w.S, -1) if tr.size else np.zeros((w.S, 1), np.uint8)
+    q = np.arange(w.n_q) if q_rows is None else \
+        np.random.default_rng(5).choice(w.n_q, q_rows, replace=False)
+    worst = 0.0
+    for s in (range(w.S) if slices is None else slices):
+        b, h = divmod(s, w.H)
+        r = oracle.compress(K[b, h], V[b, h], w.n_out, w.g, Us[s], halve=halve, follow=ts[s],
+                            tol=MARGIN, n_sinks=ns, n_window=nw)
+        assert r["stats"]["hard_mismatch"] == 0, (w.name, s, r["stats"])
+        assert np.array_equal(r["idx"], idx[b, h]), (w.name, s)
+        np.testing.assert_allclose(lw[b, h], r["logw"].astype(np.float32), rtol=1e-7, atol=0)
+        ref = oracle.weighted_attention(Q[b, h][q], K[b, h], V[b, h], r["idx"], r["logw"])
+        worst = max(worst, float(np.abs(ref - O[b, h][q]).max()))
+    assert worst <= _tol(w), (w.name, worst)
+    return worst
+
+
+@pytest.mark.parametrize("case", SINKS, ids=lambda c: f"{c['name']}-s{c['ns']}-w{c['nw']}-{c['halve']}")
+def test_sinks_window_compress_and_weighted_attention_parity(case):
+    w = W.WORKLOADS[case["name"]]
+    err = _check_sinks_case(w, case["ns"], case["nw"], case["halve"], case["slices"],
+                            case["q_rows"])
+    print(f"{case['name']} sinks {case['ns']} window {case['nw']}: attention max err {err:.3g}")
+
+
+SINKS_EDGE = [
+    # nothing left to thin: the coreset is every middle row, no round runs
+    dict(B=2, H=1, n=96, n_out=64, g=1, d=64, dtype="fp32", ns=16, nw=16),
+    # no round, subsample of 69 middle rows to 64
+    dict(B=2, H=1, n=101, n_out=64, g=1, d=128, dtype="bf16", ns=16, nw=16),
+    # odd offsets, ragged buckets, generic attention kernel (d = 32)
+    dict(B=2, H=2, n=1000, n_out=7, g=3, d=32, dtype="bf16", ns=7, nw=13),
+    # fp32 d = 128 with streamed score chunks, weighted generic kernel
+    dict(B=1, H=1, n=1100, n_out=64, g=2, d=128, dtype="fp32", ns=40, nw=36),
+]
+
+
+@pytest.mark.parametrize("cfg", SINKS_EDGE, ids=lambda c: f"n{c['n']}-o{c['n_out']}-s{c['ns']}-w{c['nw']}-d{c['d']}-{c['dtype']}")
+def test_sinks_window_edge_cases(cfg):
+    cfg = dict(cfg)
+    ns, nw = cfg.pop("ns"), cfg.pop("nw")
+    w = W.custom("sinks", seed=17, **cfg)
+    _check_sinks_case(w, ns, nw, "kh", None, None)
+
+
+def test_sinks_window_launch_sequence_ends_with_the_layout():
+    w = W.custom("sl", B=1, H=2, n=5000, n_out=40, g=2, d=64, dtype="bf16", kind="gauss")
+    Q, K, V = W.make_qkv(w)
+    plan = thin_plan(w.B, w.H, w.n - 64, w.d, w.n_out, w.g)
+    U = W.make_uniforms(w, plan["uniforms_total"]).to(DEV)
+    stream = torch.cuda.current_stream()
+    with LaunchTimer(stream) as lt:
+        thin_compress(K.to(DEV), V.to(DEV), w.n_out, w.g, U, n_sinks=32, n_window=32,
+                      stream=stream)
+        torch.cuda.synchronize()
+    got = [k for k, _, _ in lt.records()]
+    assert got[:2] == ["subsample", "vmax"] and got[-1] == "assemble"
+    assert got.count("assemble") == 1
+
+
+@pytest.mark.parametrize("dtype,d,n_out", [("bf16", 128, 192), ("bf16", 64, 29), ("bf16", 32, 300),
+                                           ("bf16", 128, 300), ("fp32", 64, 130)])
+def test_weighted_attention_edge_cases(dtype, d, n_out):
+    """Random log-weights with dropped keys, over the resident kernel (bf16,
+    d = 64 / 128, up to 256 keys) and the chunked one (others); the first 64
+    keys all dropped, so a whole chunk carries no weight."""
+    w = W.custom("wa", B=1, H=2, n=700, n_q=333, d=d, dtype=dtype, kind="gauss")
+    Q, K, V = W.make_qkv(w)
+    rng = np.random.default_rng(d + n_out)
+    idx = rng.integers(0, 700, size=(1, 2, n_out)).astype(np.int32)
+    logw = (rng.standard_normal((1, 2, n_out)) * 3).astype(np.float32)
+    logw[rng.random((1, 2, n_out)) < 0.2] = -np.inf
+    if n_out > 64:
+        logw[:, :, :64] = -np.inf
+    logw[:, :, -1] = 1.0
+    O = thin_attention(Q.to(DEV), K.to(DEV), V.to(DEV), torch.from_numpy(idx).to(DEV),
+                       logw=torch.from_numpy(logw).to(DEV)).cpu().numpy()
+    for h in range(2):
+        ref = oracle.weighted_attention(Q[0, h], K[0, h], V[0, h], idx[0, h],
+                                        logw[0, h].astype(np.float64))
+        assert np.abs(ref - O[0, h]).max() <= _tol(w), (dtype, d, n_out, h)
+
+
+def test_equal_log_weights_match_unweighted_attention():
+    w = W.custom("eq", B=2, H=1, n=1024, n_q=1000, d=128, dtype="bf16", kind="gauss")
+    Q, K, V = W.make_qkv(w)
+    idx = np.sort(np.random.default_rng(6).choice(1024, size=(2, 1, 128), replace=False),
+                  axis=-1).astype(np.int32)
+    Qd, Kd, Vd, Id = Q.to(DEV), K.to(DEV), V.to(DEV), torch.from_numpy(idx).to(DEV)
+    a = thin_attention(Qd, Kd, Vd, Id)
+    b = thin_attention(Qd, Kd, Vd, Id, logw=torch.full((2, 1, 128), 2.5, device=DEV))
+    torch.cuda.synchronize()
+    assert (a - b).abs().max().item() <= 1e-5

@@ -9,10 +9,15 @@ bracketed by HIP events on its stream (thin_set_launch_hook), which gives the
 per-kernel times and the roofline figures.  Prints one JSON line.
 
   python bench.py [--gpus 1] [--steps 20] [--warmup 100] [--workload long]
-                  [--no-cpu-baseline]
+                  [--no-cpu-baseline] [--halve kh|uniform] [--sinks S --window W]
+
+With --sinks / --window the first S and last W keys of every slice are kept
+exactly, the rows between them are thinned to n_out, and attention runs over
+the S + n_out + W weighted keys (eq. def:att_approx).
 """
 import argparse
 import collections
+import dataclasses
 import hashlib
 import json
 import os
@@ -132,16 +137,19 @@ def stored_traffic(workload: str):
     return float(m_val.group(1))
 
 
-def attention_bytes(w, out_bytes: int) -> int:
+def attention_bytes(w, out_bytes: int, weighted: bool = False) -> int:
+    """Queries read and outputs written once; per coreset key its K and V rows,
+    its int32 index and (weighted) its float32 log-weight."""
     b = elem_bytes(w.dtype)
-    return w.S * (w.n_q * w.d * (b + out_bytes) + w.n_out * (2 * w.d * b + 4))
+    return w.S * (w.n_q * w.d * (b + out_bytes) + w.n_out * (2 * w.d * b + 4 + 4 * weighted))
 
 
 def attention_flops(w) -> int:
     return w.S * w.n_q * 4 * w.n_out * w.d
 
 
-def cpu_baseline(w, Q, K, V, U, plan, budget_s: float = 20.0, halve: str = "kh"):
+def cpu_baseline(w, Q, K, V, U, plan, budget_s: float = 20.0, halve: str = "kh",
+                 n_sinks: int = 0, n_window: int = 0):
     """The oracle, single-threaded, on as many whole slices as fit the budget."""
     import numpy as np
     import oracle
@@ -152,8 +160,13 @@ def cpu_baseline(w, Q, K, V, U, plan, budget_s: float = 20.0, halve: str = "kh")
         b, h = divmod(s, w.H)
         Ks, Vs, Qs = K[b, h], V[b, h], Q[b, h]
         t0 = time.perf_counter()
-        r = oracle.compress(Ks, Vs, w.n_out, w.g, Us[s], halve=halve)
-        oracle.attention(Qs, Ks, Vs, r["idx"])
+        if n_sinks or n_window:
+            r = oracle.compress(Ks, Vs, w.n_out, w.g, Us[s], halve=halve, n_sinks=n_sinks,
+                                n_window=n_window)
+            oracle.weighted_attention(Qs, Ks, Vs, r["idx"], r["logw"])
+        else:
+            r = oracle.compress(Ks, Vs, w.n_out, w.g, Us[s], halve=halve)
+            oracle.attention(Qs, Ks, Vs, r["idx"])
         t_used += time.perf_counter() - t0
         done += 1
         if t_used >= budget_s:
@@ -176,6 +189,10 @@ def main():
     ap.add_argument("--halve", choices=["kh", "uniform"], default="kh",
                     help="halving algorithm of compress (kernel halving, the paper's; or "
                          "uniform halving)")
+    ap.add_argument("--sinks", type=int, default=0,
+                    help="keys kept exactly at the start of every slice")
+    ap.add_argument("--window", type=int, default=0,
+                    help="keys kept exactly at the end of every slice")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: the thinning path runs each (batch, head) "
@@ -188,20 +205,26 @@ def main():
     from paper_2606_10944_amd import workloads as W
 
     w = W.WORKLOADS[args.workload]
+    ns, nw = args.sinks, args.window
+    weighted = ns > 0 or nw > 0
+    # the compress byte models see the thinned rows, attention the m output keys
+    wc = dataclasses.replace(w, n=w.n - ns - nw)
+    wa = dataclasses.replace(w, n_out=ns + w.n_out + nw)
     Q, K, V = W.make_qkv(w)
-    plan = thin_plan(w.B, w.H, w.n, w.d, w.n_out, w.g)
+    plan = thin_plan(w.B, w.H, wc.n, w.d, w.n_out, w.g)
     U = W.make_uniforms(w, plan["uniforms_total"])
     dev = torch.device("cuda:0")
     Qd, Kd, Vd, Ud = Q.to(dev), K.to(dev), V.to(dev), U.to(dev)
     ws = torch.empty(plan["workspace_bytes"], dtype=torch.uint8, device=dev)
-    idx = torch.empty((w.B, w.H, w.n_out), dtype=torch.int32, device=dev)
+    idx = torch.empty((w.B, w.H, wa.n_out), dtype=torch.int32, device=dev)
+    lw = torch.empty((w.B, w.H, wa.n_out), dtype=torch.float32, device=dev) if weighted else None
     O = torch.empty((w.B, w.H, w.n_q, w.d), dtype=torch.float32, device=dev)
     stream = torch.cuda.current_stream()
 
     def step():
         thin_compress(Kd, Vd, w.n_out, w.g, Ud, idx_out=idx, workspace=ws, halve=args.halve,
-                      stream=stream)
-        thin_attention(Qd, Kd, Vd, idx, O=O, stream=stream)
+                      n_sinks=ns, n_window=nw, logw_out=lw, stream=stream)
+        thin_attention(Qd, Kd, Vd, idx, logw=lw, O=O, stream=stream)
 
     for _ in range(args.warmup):
         step()
@@ -239,11 +262,13 @@ def main():
     tc = sum(v for k, v in per_step.items() if k != "attention")
     ta = per_step["attention"]
 
-    cb = compress_bytes(w, plan) if args.halve == "kh" else uniform_compress_bytes(w, plan)
-    sb = score_bytes(w, plan)
-    ab = attention_bytes(w, 4)
-    af = attention_flops(w)
-    kev = kappa_evals(plan, w) if args.halve == "kh" else 0
+    cb = compress_bytes(wc, plan) if args.halve == "kh" else uniform_compress_bytes(wc, plan)
+    if weighted:  # the layout launch: m indices and m log-weights per slice
+        cb += w.S * wa.n_out * 8
+    sb = score_bytes(wc, plan)
+    ab = attention_bytes(wa, 4, weighted)
+    af = attention_flops(wa)
+    kev = kappa_evals(plan, wc) if args.halve == "kh" else 0
     # per launch: averages over every score launch of the K steps (a round may
     # take several launches; bytes and time are both summed over the step)
     n_sc = len(score_ms) // args.steps
@@ -252,7 +277,7 @@ def main():
         sc_ms_launch = statistics.mean(score_ms)
         sc_bytes_launch = sum(sb[r] for r in sc_rounds) / n_sc
         sc_gbs = sc_bytes_launch / (sc_ms_launch * 1e-3) / 1e9
-    traffic = stored_traffic(w.name) if args.halve == "kh" else None
+    traffic = stored_traffic(w.name) if args.halve == "kh" and not weighted else None
     attn_gbs = ab / (ta * 1e-3) / 1e9
     attn_tflops = af / (ta * 1e-3) / 1e12
     value = w.S * w.n_q / (ms_step * 1e-3)
@@ -271,7 +296,8 @@ def main():
         "dtype": w.dtype,
         "data": "synthetic",
         "config": {"workload": w.name, "B": w.B, "H": w.H, "n": w.n, "n_q": w.n_q, "d": w.d,
-                   "n_out": w.n_out, "g": w.g, "out_dtype": "fp32", "halve": args.halve},
+                   "n_out": w.n_out, "g": w.g, "out_dtype": "fp32", "halve": args.halve,
+                   "n_sinks": ns, "n_window": nw},
         "roofline": {
             "kernel": "pair_scores_kernel (one launch per Halve round with buckets above "
                       "the local size)",
@@ -301,7 +327,8 @@ def main():
         "gpu": torch.cuda.get_device_name(0),
     }
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(w, Q, K, V, U, plan, halve=args.halve)
+        out["cpu_baseline"] = cpu_baseline(w, Q, K, V, U, plan, halve=args.halve, n_sinks=ns,
+                                           n_window=nw)
     print(json.dumps(out), flush=True)
 
 

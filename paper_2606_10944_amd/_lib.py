@@ -129,7 +129,8 @@ def thin_compress(K: torch.Tensor, V: torch.Tensor, n_out: int, g: int,
                   uniforms: torch.Tensor, *, idx_out: Optional[torch.Tensor] = None,
                   workspace: Optional[torch.Tensor] = None, trace: bool = False,
                   halve: str = "kh", delta=None, n_sinks: int = 0, n_window: int = 0,
-                  return_logw: bool = False, stream=None):
+                  return_logw: bool = False, logw_out: Optional[torch.Tensor] = None,
+                  stream=None):
     """Compress of every slice; returns idx [B,H,n_out] int32, then the uint8
     swap trace when trace=True, then the float32 log-weights [B,H,m] when
     return_logw=True (a tuple when either is asked for).  halve="kh" (kernel
@@ -137,8 +138,9 @@ def thin_compress(K: torch.Tensor, V: torch.Tensor, n_out: int, g: int,
     n_sinks / n_window the first / last rows of every slice are kept exactly
     and the rows between them thinned to n_out: idx is then [B,H,m] with
     m = n_sinks + n_out + n_window, and the uniforms and workspace are those of
-    thin_plan for n - n_sinks - n_window rows.  Anything but the defaults goes
-    through thin_compress_ex."""
+    thin_plan for n - n_sinks - n_window rows.  logw_out (float32 [B,H,m]) is
+    filled with the log-weights and returned as with return_logw=True.
+    Anything but the defaults goes through thin_compress_ex."""
     B, H, n, d = _shape4(K, "K")
     if tuple(V.shape) != (B, H, n, d) or V.dtype != K.dtype or not V.is_contiguous():
         raise ThinError(THIN_EINVAL, "V must match K")
@@ -154,7 +156,14 @@ def thin_compress(K: torch.Tensor, V: torch.Tensor, n_out: int, g: int,
     elif tuple(idx_out.shape) != (B, H, m) or idx_out.dtype != torch.int32 \
             or not idx_out.is_contiguous():
         raise ThinError(THIN_EINVAL, "idx_out must be contiguous int32 [B,H,m]")
-    lw = torch.empty((B, H, m), dtype=torch.float32, device=dev) if return_logw else None
+    lw = None
+    if logw_out is not None:
+        if tuple(logw_out.shape) != (B, H, m) or logw_out.dtype != torch.float32 \
+                or not logw_out.is_contiguous():
+            raise ThinError(THIN_EINVAL, "logw_out must be contiguous float32 [B,H,m]")
+        lw, return_logw = logw_out, True
+    elif return_logw:
+        lw = torch.empty((B, H, m), dtype=torch.float32, device=dev)
     if workspace is None:
         workspace = torch.empty(max(plan["workspace_bytes"], 256), dtype=torch.uint8, device=dev)
     tr = None

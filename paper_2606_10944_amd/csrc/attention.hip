@@ -230,7 +230,7 @@ __global__ __launch_bounds__(64 * WAVES) void coreset_attn_kernel(
 }
 
 // ---------------------------------------------------------------------------
-// bf16, coreset resident in LDS (n_out <= 16*NKT).  One workgroup (WR waves)
+// bf16, coreset resident in LDS (n_out <= 16*NKT, NKT even).  One workgroup (WR waves)
 // stays on one slice and walks a contiguous range of queries, 16*QTR per wave
 // per step, with the next step's query fragments loaded during the current
 // one; the coreset is staged once: K row-major, V transposed (each thread
@@ -247,6 +247,8 @@ struct ResLds {
   static constexpr int k_stride = D * 2 + 16;  // bytes per K row
   static constexpr int v_stride = NK * 2 + 8;  // bytes per V^T row (8-byte aligned)
   static constexpr int bytes = NK * k_stride + D * v_stride + NK * 4;
+  // P.V multiplies 32 keys at a time
+  static_assert(NKT % 2 == 0, "resident coreset needs an even number of 16-key tiles");
 };
 
 typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
@@ -545,6 +547,12 @@ hipError_t launch_attn_res(const void* Q, const void* K, const void* V, const in
 #ifndef ATTN_RES_WAVES
 #define ATTN_RES_WAVES 4
 #endif
+// Coresets of 192 or 256 keys take over 100 KB of LDS, one workgroup per CU:
+// eight waves then hide more latency than four (256 keys, d = 128: 353 -> 280 us
+// on the long workload's queries).
+#ifndef ATTN_RES_WAVES_BIG
+#define ATTN_RES_WAVES_BIG 8
+#endif
 
 template <int D, typename TO>
 hipError_t launch_attn_res_d(int64_t n_out, const void* Q, const void* K, const void* V,
@@ -553,8 +561,11 @@ hipError_t launch_attn_res_d(int64_t n_out, const void* Q, const void* K, const 
   *used = true;
   if (n_out <= 32) return launch_attn_res<D, 2, ATTN_RES_QTR, ATTN_RES_WAVES, TO>(Q, K, V, idx, logw, S, n, n_q, n_out, O, st);
   if (n_out <= 64) return launch_attn_res<D, 4, ATTN_RES_QTR, ATTN_RES_WAVES, TO>(Q, K, V, idx, logw, S, n, n_q, n_out, O, st);
+  if (n_out <= 96) return launch_attn_res<D, 6, ATTN_RES_QTR, ATTN_RES_WAVES, TO>(Q, K, V, idx, logw, S, n, n_q, n_out, O, st);
   if (n_out <= 128) return launch_attn_res<D, 8, ATTN_RES_QTR, ATTN_RES_WAVES, TO>(Q, K, V, idx, logw, S, n, n_q, n_out, O, st);
-  if (n_out <= 256 && D <= 128) return launch_attn_res<D, 16, ATTN_RES_QTR, ATTN_RES_WAVES, TO>(Q, K, V, idx, logw, S, n, n_q, n_out, O, st);
+  // (192 = n_out 128 plus 32 sinks and a 32-row window)
+  if (n_out <= 192 && D <= 128) return launch_attn_res<D, 12, ATTN_RES_QTR, ATTN_RES_WAVES_BIG, TO>(Q, K, V, idx, logw, S, n, n_q, n_out, O, st);
+  if (n_out <= 256 && D <= 128) return launch_attn_res<D, 16, ATTN_RES_QTR, ATTN_RES_WAVES_BIG, TO>(Q, K, V, idx, logw, S, n, n_q, n_out, O, st);
   *used = false;
   return hipSuccess;
 }

@@ -425,3 +425,24 @@ def test_equal_log_weights_match_unweighted_attention():
     b = thin_attention(Qd, Kd, Vd, Id, logw=torch.full((2, 1, 128), 2.5, device=DEV))
     torch.cuda.synchronize()
     assert (a - b).abs().max().item() <= 1e-5
+
+
+@pytest.mark.parametrize("d", [64, 128])
+@pytest.mark.parametrize("n_out", [17, 64, 90, 96, 128, 150, 192, 256])
+def test_resident_attention_tiers(d, n_out):
+    """Every coreset size tier of the resident bf16 kernel (16-key tiles padded
+    to 2, 4, 6, 8, 12, 16), unweighted and weighted."""
+    w = W.custom("rt", B=1, H=2, n=900, n_q=777, d=d, dtype="bf16", kind="gauss")
+    Q, K, V = W.make_qkv(w)
+    rng = np.random.default_rng(n_out * d)
+    idx = rng.integers(0, 900, size=(1, 2, n_out)).astype(np.int32)
+    logw = (rng.standard_normal((1, 2, n_out)) * 2).astype(np.float32)
+    Qd, Kd, Vd, Id = Q.to(DEV), K.to(DEV), V.to(DEV), torch.from_numpy(idx).to(DEV)
+    O = thin_attention(Qd, Kd, Vd, Id).cpu().numpy()
+    Ow = thin_attention(Qd, Kd, Vd, Id, logw=torch.from_numpy(logw).to(DEV)).cpu().numpy()
+    for h in range(2):
+        ref = oracle.attention(Q[0, h], K[0, h], V[0, h], idx[0, h])
+        assert np.abs(ref - O[0, h]).max() <= 2e-3, (d, n_out, h)
+        ref = oracle.weighted_attention(Q[0, h], K[0, h], V[0, h], idx[0, h],
+                                        logw[0, h].astype(np.float64))
+        assert np.abs(ref - Ow[0, h]).max() <= 2e-3, (d, n_out, h, "weighted")

@@ -82,6 +82,14 @@ def lib():
                                      C.c_int, P, P, P, P, C.c_double, P, P, C.POINTER(Stats)]
         L.or_attention_weighted.argtypes = [P, P, P, C.c_int64, C.c_int64, P, P, C.c_int64, P]
         L.or_attention_weighted.restype = None
+        L.or_express_decode.argtypes = [P, P, P, C.c_int64, C.c_int64, C.c_int64, C.c_int,
+                                        C.c_double, C.c_int, P, P, C.c_double, P, P, P, P, P, P,
+                                        C.POINTER(Stats)]
+        L.or_express_decode.restype = C.c_int
+        L.or_express_uniforms.argtypes = [C.c_int64, C.c_int64, C.c_int]
+        L.or_express_uniforms.restype = C.c_int64
+        L.or_express_delta.argtypes = [C.c_int, C.c_int, C.c_int, C.c_double]
+        L.or_express_delta.restype = C.c_double
         L.or_compress_ex.restype = C.c_int
         L.or_uniform_halving.argtypes = [P, C.c_int64, P, P, P, C.POINTER(Stats)]
         L.or_uniform_halving.restype = C.c_int
@@ -244,6 +252,51 @@ def weighted_attention(Q, K, V, rows, logw) -> np.ndarray:
     O = np.empty((n_q, d))
     lib().or_attention_weighted(_p(Q), _p(K), _p(V), n_q, d, _p(rows), _p(lw), rows.size, _p(O))
     return O
+
+
+def express_uniforms(n: int, n_out: int, mbar: int) -> int:
+    """Uniforms a Thinformer decode of n points consumes (Halve calls only)."""
+    u = lib().or_express_uniforms(n, n_out, mbar)
+    if u < 0:
+        raise ValueError("no Express structure without subsampling for these sizes")
+    return u
+
+
+def express_delta(m: int, i: int, mbar: int, delta: float = 0.5) -> float:
+    """Cor. 2: delta_{m,i} for i >= 0, delta_m / 2 (the Halve phase) for i < 0."""
+    return lib().or_express_delta(m, i, mbar, delta)
+
+
+def express_decode(Q, K, V, n_out: int, mbar: int, U, *, delta: float = 0.5,
+                   halve: str = "kh", follow=None, tol: float = 1e-5,
+                   outputs: bool = True) -> dict:
+    """Thinformer decoding of one slice (Alg. 4 over the Express cache of
+    Alg. 1): "O" [n, d] (every point attends over the cache of the points
+    before it plus itself), then the final weighted cache ("idx", "logw", in
+    the order C_0..C_mp, E), the final thinning factor "m", the swap "bits"
+    (indexed like U) and KH "stats"."""
+    Q, K, V = _f64(Q), _f64(K), _f64(V)
+    n, d = K.shape
+    U = np.ascontiguousarray(U, dtype=np.float32)
+    need = express_uniforms(n, n_out, mbar)
+    assert U.size >= need
+    fol = None if follow is None else np.ascontiguousarray(follow, dtype=np.uint8)
+    bits = np.zeros(max(need, 1), np.uint8)
+    O = np.zeros((n, d)) if outputs else None
+    cap = 8 * n_out + 2
+    rows = np.zeros(cap, np.int32)
+    logw = np.zeros(cap)
+    klen = C.c_int64(0)
+    mfin = C.c_int(0)
+    st = Stats()
+    rc = lib().or_express_decode(_p(Q), _p(K), _p(V), n, d, n_out, mbar, delta, HALVES[halve],
+                                 _p(U), _p(fol), tol, _p(bits), _p(O), _p(rows), _p(logw),
+                                 C.byref(klen), C.byref(mfin), C.byref(st))
+    if rc != 0:
+        raise ValueError(f"or_express_decode failed ({rc})")
+    k = klen.value
+    return {"O": O, "idx": rows[:k].copy(), "logw": logw[:k].copy(), "m": mfin.value,
+            "bits": bits[:need], "stats": {f: getattr(st, f) for f, _ in Stats._fields_}}
 
 
 def exact_attention(Q, K, V) -> np.ndarray:

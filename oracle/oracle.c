@@ -376,3 +376,211 @@ void or_attention_weighted(const double* Q, const double* K, const double* V, in
   }
   free(s);
 }
+
+/* ------------------------------------------------------------------ */
+/* Express (Alg. 1) with Compress2 (Alg. 2) and Thinformer decoding   */
+/* (Alg. 4 with WtdAttention, Alg. 5), without subsampling: every     */
+/* thin phase runs at a level m <= mbar, so Subsample keeps all.      */
+/* ------------------------------------------------------------------ */
+#define EX_MAXL 32
+
+typedef struct {
+  const double* K;
+  const double* V;
+  int64_t d, n_out;
+  int mbar;
+  double delta;
+  int halve;
+  const float* U;
+  int64_t upos;
+  const uint8_t* follow;
+  double tol;
+  uint8_t* bits;
+  or_stats_t* st;
+  int m;             /* thinning factor */
+  int64_t n, ell;    /* points seen, points of the current thin group */
+  int32_t* E;        /* Express coreset */
+  int64_t nE;
+  int mp;            /* m ^ mbar of the current Compress2 */
+  int32_t* C[EX_MAXL + 1];
+  int64_t nC[EX_MAXL + 1];
+  int32_t* tmp;
+  int over;          /* a level above mbar was reached */
+  int count_only;    /* only count the uniforms the Halve calls consume */
+} ex_t;
+
+/* Cor. 2: delta_m, the budget of level m, and delta_{m,i}. */
+double or_express_delta(int m, int i, int mbar, double delta) {
+  const double dm = 0.5 * delta * (1.0 / log2(m / 2.0 + 2.0) - 1.0 / log2(m / 2.0 + 3.0));
+  if (i < 0) return dm / 2.0; /* Halve_{m,m} = KH(delta_m / 2) */
+  const int mp = m < mbar ? m : mbar;
+  return ldexp(dm, 2 * (i + 1 - mp)) / (3.0 * mp);
+}
+
+/* One Halve call on rows[0..N): KH under kappa_att with v_max over these rows. */
+static int ex_halve(ex_t* x, const int32_t* rows, int64_t N, double delta, int32_t* out) {
+  const int64_t o = x->upos;
+  int rc;
+  if (x->count_only) {
+    for (int64_t i = 0; i < N / 2; ++i) out[i] = rows[2 * i];
+    rc = 0;
+  } else if (x->halve == OR_HALVE_UNIFORM) {
+    rc = or_uniform_halving(rows, N, x->U + o, out, x->bits ? x->bits + o : NULL, x->st);
+  } else {
+    double vm = 0.0;
+    for (int64_t j = 0; j < N; ++j)
+      for (int64_t c = 0; c < x->d; ++c) {
+        const double a = fabs(x->V[(int64_t)rows[j] * x->d + c]);
+        if (a > vm) vm = a;
+      }
+    rc = or_kernel_halving(x->K, x->V, x->d, vm * vm, OR_KERNEL_KATT, delta, rows, N, x->U + o,
+                           out, x->follow ? x->follow + o : NULL, x->tol,
+                           x->bits ? x->bits + o : NULL, NULL, NULL, NULL, x->st);
+  }
+  x->upos += N / 2;
+  return rc;
+}
+
+/* Compress2(mp, 2^mp n_out).update: C_i is halved when it holds n_out 2^(i+2-mp) points. */
+static int ex_compress2_update(ex_t* x, int32_t p) {
+  x->C[0][x->nC[0]++] = p;
+  for (int i = 0; i < x->mp; ++i) {
+    const int64_t T = (x->n_out << (i + 2)) >> x->mp;
+    if (x->nC[i] == T) {
+      int rc = ex_halve(x, x->C[i], T, or_express_delta(x->m, i, x->mbar, x->delta),
+                        x->C[i + 1] + x->nC[i + 1]);
+      if (rc) return rc;
+      x->nC[i + 1] += T / 2;
+      x->nC[i] = 0;
+    }
+  }
+  return 0;
+}
+
+static void ex_reset_c(ex_t* x) {
+  x->mp = x->m < x->mbar ? x->m : x->mbar;
+  if (x->m > x->mbar) x->over = 1;
+  /* Compress2's smallest groups, 4 n_out / 2^mp points, must be even and >= 2 */
+  if (x->mp >= 1 && ((4 * x->n_out) % ((int64_t)1 << x->mp) != 0 ||
+                     ((4 * x->n_out) >> x->mp) < 2 || (((4 * x->n_out) >> x->mp) & 1)))
+    x->over = 1;
+  for (int i = 0; i <= EX_MAXL; ++i) x->nC[i] = 0;
+}
+
+/* Express.update with point p (Alg. 1). */
+static int ex_update(ex_t* x, int32_t p) {
+  x->n += 1;
+  if (x->n <= x->n_out) {
+    x->E[x->nE++] = p;
+    return 0;
+  }
+  if (x->over) return -1; /* would need Subsample with m > mbar */
+  x->ell += 1;
+  int rc = ex_compress2_update(x, p);
+  if (rc) return rc;
+  if (x->ell == (x->n_out << x->m)) {
+    memcpy(x->E + x->nE, x->C[x->mp], sizeof(int32_t) * (size_t)x->nC[x->mp]);
+    x->nE += x->nC[x->mp];
+    x->ell = 0;
+  }
+  if (x->n == 4 * (x->n_out << x->m)) {
+    const double dl = or_express_delta(x->m, -1, x->mbar, x->delta);
+    rc = ex_halve(x, x->E, x->nE, dl, x->tmp);
+    if (!rc) rc = ex_halve(x, x->tmp, x->nE / 2, dl, x->E);
+    if (rc) return rc;
+    x->nE /= 4;
+    x->m += 2;
+  }
+  if (x->ell == 0) ex_reset_c(x);
+  return 0;
+}
+
+/* Weighted cache (Express.wtd_cache): C_0..C_mp with weights 2^(i-mp), then E
+ * with weight 1; returns its size. */
+static int64_t ex_cache(const ex_t* x, int32_t* rows, double* logw) {
+  int64_t k = 0;
+  for (int i = 0; i <= x->mp; ++i)
+    for (int64_t j = 0; j < x->nC[i]; ++j) {
+      rows[k] = x->C[i][j];
+      logw[k++] = (double)(i - x->mp) * log(2.0);
+    }
+  for (int64_t j = 0; j < x->nE; ++j) {
+    rows[k] = x->E[j];
+    logw[k++] = 0.0;
+  }
+  return k;
+}
+
+/* forward declaration: the uniforms a decode of n points consumes */
+static int ex_run(ex_t* x, const double* Q, int64_t n, double* O, int32_t* rows, double* logw);
+
+int or_express_decode(const double* Q, const double* K, const double* V, int64_t n, int64_t d,
+                      int64_t n_out, int mbar, double delta, int halve, const float* U,
+                      const uint8_t* follow, double tol, uint8_t* bits, double* O,
+                      int32_t* cache_rows, double* cache_logw, int64_t* cache_len,
+                      int* m_final, or_stats_t* st) {
+  if (n < 0 || n_out < 1 || d < 1 || mbar < 0 || mbar > EX_MAXL - 2) return -1;
+  ex_t x;
+  memset(&x, 0, sizeof(x));
+  x.K = K; x.V = V; x.d = d; x.n_out = n_out; x.mbar = mbar; x.delta = delta;
+  x.halve = halve; x.U = U; x.follow = follow; x.tol = tol; x.bits = bits; x.st = st;
+  const int64_t capE = 4 * n_out, capW = 8 * n_out + 2;
+  x.E = (int32_t*)malloc(sizeof(int32_t) * (size_t)capE);
+  x.tmp = (int32_t*)malloc(sizeof(int32_t) * (size_t)capE);
+  int32_t* rows = (int32_t*)malloc(sizeof(int32_t) * (size_t)capW);
+  double* logw = (double*)malloc(sizeof(double) * (size_t)capW);
+  int ok = x.E && x.tmp && rows && logw;
+  for (int i = 0; i <= EX_MAXL && ok; ++i) {
+    x.C[i] = (int32_t*)malloc(sizeof(int32_t) * (size_t)(4 * n_out));
+    ok = x.C[i] != NULL;
+  }
+  int rc = ok ? ex_run(&x, Q, n, O, rows, logw) : -2;
+  if (rc == 0) {
+    int64_t k = ex_cache(&x, rows, logw);
+    if (cache_rows) memcpy(cache_rows, rows, sizeof(int32_t) * (size_t)k);
+    if (cache_logw) memcpy(cache_logw, logw, sizeof(double) * (size_t)k);
+    if (cache_len) *cache_len = k;
+    if (m_final) *m_final = x.m;
+  }
+  for (int i = 0; i <= EX_MAXL; ++i) free(x.C[i]);
+  free(x.E);
+  free(x.tmp);
+  free(rows);
+  free(logw);
+  return rc;
+}
+
+static int ex_run(ex_t* x, const double* Q, int64_t n, double* O, int32_t* rows, double* logw) {
+  int rc = 0;
+  ex_reset_c(x);
+  for (int64_t p = 0; p < n && rc == 0; ++p) {
+    if (O) {
+      /* WtdAttention: the cache plus the token itself in C_0 (weight 2^-mp) */
+      int64_t k = ex_cache(x, rows, logw);
+      rows[k] = (int32_t)p;
+      logw[k++] = -(double)x->mp * log(2.0);
+      or_attention_weighted(Q + p * x->d, x->K, x->V, 1, x->d, rows, logw, k, O + p * x->d);
+    }
+    rc = ex_update(x, (int32_t)p);
+  }
+  return rc;
+}
+
+int64_t or_express_uniforms(int64_t n, int64_t n_out, int mbar) {
+  if (n < 0 || n_out < 1 || mbar < 0 || mbar > EX_MAXL - 2) return -1;
+  ex_t x;
+  memset(&x, 0, sizeof(x));
+  x.n_out = n_out; x.mbar = mbar; x.delta = 0.5; x.count_only = 1;
+  x.E = (int32_t*)malloc(sizeof(int32_t) * (size_t)(4 * n_out));
+  x.tmp = (int32_t*)malloc(sizeof(int32_t) * (size_t)(4 * n_out));
+  int ok = x.E && x.tmp;
+  for (int i = 0; i <= EX_MAXL && ok; ++i) {
+    x.C[i] = (int32_t*)malloc(sizeof(int32_t) * (size_t)(4 * n_out));
+    ok = x.C[i] != NULL;
+  }
+  int rc = ok ? ex_run(&x, NULL, n, NULL, NULL, NULL) : -2;
+  for (int i = 0; i <= EX_MAXL; ++i) free(x.C[i]);
+  free(x.E);
+  free(x.tmp);
+  return rc == 0 ? x.upos : -1;
+}

@@ -546,3 +546,99 @@ def test_sinks_and_window_with_nothing_to_thin_is_exact_attention():
     assert np.array_equal(r["idx"], np.arange(n)) and np.all(r["logw"] == 0)
     np.testing.assert_allclose(oracle.weighted_attention(Q, K, V, r["idx"], r["logw"]),
                                oracle.exact_attention(Q, K, V), rtol=1e-12, atol=1e-13)
+
+
+# ---------------------------------------------------------------------------
+# Express (Alg. 1 / 2) and Thinformer decoding (Alg. 4 / 5)
+# ---------------------------------------------------------------------------
+def _express_inputs(n, d, seed):
+    rng = np.random.default_rng(seed)
+    return (rng.standard_normal((n, d)) for _ in range(3))
+
+
+def test_thinformer_is_exact_for_the_first_four_n_out_points():
+    """The accuracy theorem of Sec. 4: outputs equal exact causal attention
+    for every n <= 4 n_out (no point is thinned before the first Halve phase)."""
+    n_out, n, d = 8, 32, 8
+    Q, K, V = _express_inputs(n, d, 30)
+    U = np.random.default_rng(31).random(max(oracle.express_uniforms(n, n_out, 2), 1))
+    r = oracle.express_decode(Q, K, V, n_out, 2, U.astype(np.float32))
+    ref = torch.nn.functional.scaled_dot_product_attention(
+        torch.from_numpy(Q)[None], torch.from_numpy(K)[None], torch.from_numpy(V)[None],
+        is_causal=True)[0].numpy()
+    np.testing.assert_allclose(r["O"], ref, rtol=1e-12, atol=1e-13)
+    assert r["m"] == 2 and r["idx"].size == n_out  # the cache right after the first Halve phase
+
+
+@pytest.mark.parametrize("n", [1, 7, 8, 9, 31, 33, 100, 128, 129, 200, 511, 512])
+def test_express_cache_weights_count_every_point(n):
+    """A cache point of C_i stands for 2^i points and one of E for 2^m, so
+    2^m * sum of the weights is the number of points seen."""
+    n_out, mbar, d = 8, 4, 4
+    Q, K, V = _express_inputs(n, d, 32)
+    U = np.random.default_rng(33).random(max(oracle.express_uniforms(n, n_out, mbar), 1))
+    r = oracle.express_decode(Q, K, V, n_out, mbar, U.astype(np.float32), outputs=False)
+    assert np.exp(r["logw"]).sum() * 2.0 ** r["m"] == pytest.approx(n, rel=1e-12)
+    assert r["idx"].size <= 6 * n_out  # Thm. 1: cache size at most 6 n_out
+    assert np.unique(r["idx"]).size == r["idx"].size and (r["idx"].size == 0 or r["idx"].max() < n)
+
+
+def _keep_first(rows):
+    return rows[0::2]
+
+
+def _offline_compress2(m, rows):
+    """Offline Compress2 (App. H): 4^(m-1) groups halved, then recurse on m - 1."""
+    if m == 0:
+        return rows
+    g = 4 ** (m - 1)
+    size = rows.size // g
+    return _offline_compress2(m - 1, np.concatenate(
+        [_keep_first(rows[k * size:(k + 1) * size]) for k in range(g)]))
+
+
+def _offline_express(n_out, mbar, rows, m):
+    """Offline-Express (App. F, the recursive procedure) on 2^(m+2) n_out points."""
+    if rows.size <= n_out:
+        return rows
+    q = rows.size // 4
+    parts = [_offline_express(n_out, mbar, rows[:q], m - 2)]
+    for j in (1, 2, 3):
+        assert m <= mbar  # Subsample keeps every point
+        parts.append(_offline_compress2(min(m, mbar), rows[j * q:(j + 1) * q]))
+    return _keep_first(_keep_first(np.concatenate(parts)))
+
+
+@pytest.mark.parametrize("n_out,mbar,levels", [(4, 2, 2), (8, 4, 3), (16, 6, 3), (16, 4, 2)])
+def test_streaming_express_equals_offline_express(n_out, mbar, levels):
+    """The streaming procedure equals the recursive offline one (App. F);
+    with a deterministic Halve (uniform halving with every u >= 1/2 keeps
+    the first point of each pair) both must return the same coreset."""
+    m = 2 * levels - 2
+    n = n_out * 2 ** (m + 2)
+    Q, K, V = _express_inputs(n, 2, 34)
+    U = np.full(max(oracle.express_uniforms(n, n_out, mbar), 1), 0.75, np.float32)
+    r = oracle.express_decode(Q, K, V, n_out, mbar, U, halve="uniform", outputs=False)
+    want = _offline_express(n_out, mbar, np.arange(n, dtype=np.int32), m)
+    assert r["m"] == m + 2 and np.array_equal(r["idx"], want)
+
+
+def test_cor2_delta_schedule_meets_the_union_bound():
+    """Cor. 2's budgets: the level budgets delta_m telescope to at most delta/2,
+    and within level m the two Halve-phase calls and the Compress2 calls
+    (4^(m^mbar - i) calls at depth i per group, 3 groups, weighted 3/8 as in
+    the theorem) add up to exactly delta_m."""
+    delta, mbar = 0.5, 6
+    tot = 0.0
+    for m in range(0, 40, 2):
+        dm = 2 * oracle.express_delta(m, -1, mbar, delta)
+        tot += dm
+        if m == 0:
+            continue
+        mp = min(m, mbar)
+        s = dm / 2 + 3 / 8 * sum(4 ** (mp - i) * oracle.express_delta(m, i, mbar, delta)
+                                 for i in range(mp))
+        assert s == pytest.approx(dm, rel=1e-12)
+    K = 19
+    assert tot == pytest.approx(delta / 2 * (1 - 1 / math.log2(K + 3)), rel=1e-12)
+    assert tot < delta / 2

@@ -213,6 +213,74 @@ int thin_attention_ex(const void* Q, const void* K, const void* V, int32_t dtype
                       void* stream);
 
 /*
+ * Thinformer decoding over an Express cache (Sec. 3-4: Alg. 1 Express with
+ * Compress2 of Alg. 2 in its thin phase, Alg. 4 Thinformer, Alg. 5
+ * WtdAttention), for all B*H slices in lockstep.  Point t (t = 0, 1, ...) of
+ * every slice first attends over the weighted cache of points 0..t-1 plus
+ * itself, then enters the cache.  The cache holds, per slice, the Express
+ * coreset E (weight 1) and the Compress2 coresets C_0..C_mp (weight
+ * 2^(i-mp)); its Halve calls are KH(delta_{m,i}) and, in the Halve phase,
+ * KH(delta_m / 2) with Cor. 2's schedule for the given delta, under
+ * kappa_att with v_max over the rows of each call (or uniform halving).
+ * Every Halve call of N points consumes the next N/2 uniforms of each slice.
+ * Supported: the thin phases at levels m <= mbar only, where Subsample keeps
+ * every point, i.e. n_max <= n_out * 2^(M+2) with M the largest even number
+ * <= mbar; every Compress2 group size 4 n_out / 2^m (2 <= m <= M) an even
+ * integer >= 2; 4 n_out <= 8192.
+ */
+typedef struct thin_express thin_express_t;
+
+typedef struct {
+  int64_t uniforms_per_slice; /* uniforms the Halve calls of n_max points consume */
+  int64_t max_keys;           /* largest key list of one attention call           */
+  size_t workspace_bytes;     /* device workspace of thin_express_create          */
+} thin_express_plan_t;
+
+/* Host-only.  THIN_EINVAL for unsupported sizes (see above). */
+int thin_express_plan(int64_t B, int64_t H, int64_t d, int64_t n_out, int32_t mbar,
+                      int64_t n_max, thin_express_plan_t* plan);
+
+/*
+ * Create the cache state (host memory, freed by thin_express_destroy) over
+ * the caller's device workspace (>= plan.workspace_bytes, 256-byte aligned),
+ * which the object uses until destroyed.  halve: a thin_halve_t.  delta in
+ * (0, 1) (1/2 in the paper's guarantee).  Launches nothing.
+ */
+int thin_express_create(int32_t dtype, int64_t B, int64_t H, int64_t d, int64_t n_out,
+                        int32_t mbar, double delta, int32_t halve, int64_t n_max,
+                        void* workspace, size_t workspace_bytes, thin_express_t** out);
+
+/*
+ * One decoding step for point t = the number of points seen so far:
+ *   Q         (device) [B,H,d]: the point's query.
+ *   K, V      (device) [B,H,n_max,d]: the key/value rows of points 0..t
+ *             (row t written before the call).
+ *   uniforms  (device) float32 [B*H, plan.uniforms_per_slice], n_uniforms
+ *             its size (nullable when the plan needs none).
+ *   O         (device) [B,H,d] of out_dtype: the point's output.
+ *   swap_trace (device, nullable) uint8 indexed like uniforms.
+ * Enqueued on `stream`; calls on one object must be stream-ordered.
+ * Errors: THIN_EINVAL (null arguments, t = n_max, or a point beyond the
+ * supported levels), THIN_EDTYPE, THIN_EUNIFORMS, THIN_EHIP.
+ */
+int thin_express_step(thin_express_t* x, const void* Q, const void* K, const void* V,
+                      const float* uniforms, int64_t n_uniforms, void* O, int32_t out_dtype,
+                      uint8_t* swap_trace, void* stream);
+
+/*
+ * The current weighted cache: idx (device) int32 and logw (device) float32,
+ * each [B,H,plan.max_keys], receive in their first *len entries per slice
+ * the cache in the order C_0, C_1, .., C_mp, E with log-weights
+ * (i - mp) log 2 and 0; *len (host) its size, *m (host, nullable) the
+ * thinning factor m.  Enqueued on `stream`.
+ */
+int thin_express_cache(const thin_express_t* x, int32_t* idx, float* logw, int64_t* len,
+                       int32_t* m, void* stream);
+
+/* Free the host state (the workspace stays the caller's). */
+int thin_express_destroy(thin_express_t* x);
+
+/*
  * Diagnostic: out[m*16 + n] = <rows[m], rows[16 + n]> for m, n < 16, computed
  * through the MFMA row-fragment path the pair-score kernel uses.
  *   rows (device) [32, d] of `dtype`;  out (device) float32 [16, 16].
@@ -226,7 +294,7 @@ const char* thin_status_str(int status);
 /*
  * Launch observer, for tracing and per-kernel timing.  While a hook is set,
  * every kernel launch made by thin_compress, thin_compress_traced,
- * thin_compress_ex, thin_attention and thin_attention_ex is bracketed by two calls on the
+ * thin_compress_ex, thin_attention, thin_attention_ex and thin_express_step is bracketed by two calls on the
  * calling thread:
  * hook(ctx, kernel, round, 0, stream) right before the launch is enqueued and
  * hook(ctx, kernel, round, 1, stream) right after.  The hook may enqueue
@@ -252,7 +320,8 @@ typedef enum {
   THIN_KERNEL_ATTENTION = 6,   /* coreset attention                       */
   THIN_KERNEL_LOCAL = 7,       /* scores and decisions of one round       */
   THIN_KERNEL_UNIFORM = 8,     /* uniform halving (all rounds, or one)    */
-  THIN_KERNEL_ASSEMBLE = 9     /* sinks + coreset + window, log-weights   */
+  THIN_KERNEL_ASSEMBLE = 9,    /* sinks + coreset + window, log-weights   */
+  THIN_KERNEL_EXPRESS = 10     /* Express cache moves, per-call v_max, keys */
 } thin_kernel_t;
 typedef void (*thin_launch_hook_t)(void* ctx, int32_t kernel, int32_t round, int32_t phase,
                                    void* stream);

@@ -22,11 +22,14 @@ THIN_FP32, THIN_BF16 = 0, 1
 
 # Every symbol include/thin.h declares.
 EXPORTS = ("thin_plan", "thin_compress", "thin_compress_traced", "thin_compress_ex", "thin_attention",
-           "thin_attention_ex", "thin_selftest_gram16", "thin_status_str", "thin_set_launch_hook")
+           "thin_attention_ex", "thin_express_plan", "thin_express_create", "thin_express_step",
+           "thin_express_cache", "thin_express_destroy", "thin_selftest_gram16", "thin_status_str",
+           "thin_set_launch_hook")
 
 # thin_kernel_t
 KERNEL_NAMES = {0: "trace_clear", 1: "subsample", 2: "fill", 3: "vmax", 4: "scores",
-                5: "decide", 6: "attention", 7: "local", 8: "uniform", 9: "assemble"}
+                5: "decide", 6: "attention", 7: "local", 8: "uniform", 9: "assemble",
+                10: "express"}
 HALVE = {"kh": 0, "uniform": 1}  # thin_halve_t
 LaunchHook = C.CFUNCTYPE(None, C.c_void_p, C.c_int32, C.c_int32, C.c_int32, C.c_void_p)
 
@@ -35,6 +38,11 @@ class ThinError(RuntimeError):
     def __init__(self, status: int, where: str):
         self.status = status
         super().__init__(f"{where}: {thin_status_str(status)} (status {status})")
+
+
+class ExpressPlan(C.Structure):
+    _fields_ = [("uniforms_per_slice", C.c_int64), ("max_keys", C.c_int64),
+                ("workspace_bytes", C.c_size_t)]
 
 
 class CompressOpts(C.Structure):
@@ -74,13 +82,21 @@ def lib():
                                    C.POINTER(CompressOpts), P, I64, P]
     L.thin_attention.argtypes = [P, P, P, I32, I64, I64, I64, I64, I64, P, I64, P, I32, P]
     L.thin_attention_ex.argtypes = [P, P, P, I32, I64, I64, I64, I64, I64, P, P, I64, P, I32, P]
+    L.thin_express_plan.argtypes = [I64, I64, I64, I64, I32, I64, C.POINTER(ExpressPlan)]
+    L.thin_express_create.argtypes = [I32, I64, I64, I64, I64, I32, C.c_double, I32, I64, P, SZ,
+                                      C.POINTER(C.c_void_p)]
+    L.thin_express_step.argtypes = [P, P, P, P, P, I64, P, I32, P, P]
+    L.thin_express_cache.argtypes = [P, P, P, C.POINTER(C.c_int64), C.POINTER(C.c_int32), P]
+    L.thin_express_destroy.argtypes = [P]
     L.thin_selftest_gram16.argtypes = [I32, I64, P, P, P]
     L.thin_status_str.argtypes = [C.c_int]
     L.thin_status_str.restype = C.c_char_p
     L.thin_set_launch_hook.argtypes = [LaunchHook, P]
     L.thin_set_launch_hook.restype = C.c_int
     for f in ("thin_plan", "thin_compress", "thin_compress_traced", "thin_compress_ex",
-              "thin_attention", "thin_attention_ex", "thin_selftest_gram16"):
+              "thin_attention", "thin_attention_ex", "thin_selftest_gram16", "thin_express_plan",
+              "thin_express_create", "thin_express_step", "thin_express_cache",
+              "thin_express_destroy"):
         getattr(L, f).restype = C.c_int
     _lib = L
     return L
@@ -226,6 +242,85 @@ def thin_attention(Q: torch.Tensor, K: torch.Tensor, V: torch.Tensor, idx: torch
                               _ptr(idx), n_out, _ptr(O), _dtype_code(O.dtype), _stream(stream))
     _check(rc, "thin_attention")
     return O
+
+
+def thin_express_plan(B: int, H: int, d: int, n_out: int, mbar: int, n_max: int) -> dict:
+    p = ExpressPlan()
+    _check(lib().thin_express_plan(B, H, d, n_out, mbar, n_max, C.byref(p)), "thin_express_plan")
+    return {k: getattr(p, k) for k, _ in ExpressPlan._fields_}
+
+
+class ExpressCache:
+    """Thinformer decoding over an Express cache for B*H slices in lockstep
+    (thin_express_*): ``step(Q_t, K, V, U)`` attends point t = ``self.n``
+    (query Q_t [B,H,d]; K, V [B,H,n_max,d] caches holding rows 0..t) over the
+    cache plus itself and then adds it to the cache."""
+
+    def __init__(self, B: int, H: int, d: int, n_out: int, mbar: int, n_max: int, *,
+                 dtype: torch.dtype = torch.bfloat16, delta: float = 0.5, halve: str = "kh",
+                 device="cuda"):
+        if halve not in HALVE:
+            raise ThinError(THIN_EINVAL, f"unknown halving {halve!r}")
+        self.plan = thin_express_plan(B, H, d, n_out, mbar, n_max)
+        self.B, self.H, self.d, self.n_out, self.n_max = B, H, d, n_out, n_max
+        self.dtype = dtype
+        self.ws = torch.empty(max(self.plan["workspace_bytes"], 256), dtype=torch.uint8,
+                              device=device)
+        h = C.c_void_p()
+        _check(lib().thin_express_create(_dtype_code(dtype), B, H, d, n_out, mbar, delta,
+                                         HALVE[halve], n_max, _ptr(self.ws), self.ws.numel(),
+                                         C.byref(h)), "thin_express_create")
+        self._h = h
+        self.n = 0
+
+    def step(self, Q_t: torch.Tensor, K: torch.Tensor, V: torch.Tensor, uniforms, *,
+             O: Optional[torch.Tensor] = None, out_dtype: torch.dtype = torch.float32,
+             trace: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+        B, H, d = self.B, self.H, self.d
+        if tuple(Q_t.shape) != (B, H, d) or not Q_t.is_contiguous() or Q_t.dtype != self.dtype:
+            raise ThinError(THIN_EINVAL, "Q_t must be contiguous [B,H,d] of the cache's dtype")
+        for t, nm in ((K, "K"), (V, "V")):
+            if tuple(t.shape) != (B, H, self.n_max, d) or not t.is_contiguous() \
+                    or t.dtype != self.dtype:
+                raise ThinError(THIN_EINVAL, f"{nm} must be contiguous [B,H,n_max,d]")
+        if uniforms is not None and (uniforms.dtype != torch.float32
+                                     or not uniforms.is_contiguous()):
+            raise ThinError(THIN_EINVAL, "uniforms must be contiguous float32")
+        if O is None:
+            O = torch.empty((B, H, d), dtype=out_dtype, device=Q_t.device)
+        elif tuple(O.shape) != (B, H, d) or not O.is_contiguous():
+            raise ThinError(THIN_EINVAL, "O must be contiguous [B,H,d]")
+        nU = 0 if uniforms is None else uniforms.numel()
+        rc = lib().thin_express_step(self._h, _ptr(Q_t), _ptr(K), _ptr(V),
+                                     None if uniforms is None else _ptr(uniforms), nU, _ptr(O),
+                                     _dtype_code(O.dtype), None if trace is None else _ptr(trace),
+                                     _stream(stream))
+        _check(rc, "thin_express_step")
+        self.n += 1
+        return O
+
+    def cache(self, stream=None):
+        """(idx [B,H,len] int32, logw [B,H,len] float32, m): the current
+        weighted cache in the order C_0, C_1, .., C_mp, E."""
+        k = self.plan["max_keys"]
+        idx = torch.empty((self.B, self.H, k), dtype=torch.int32, device=self.ws.device)
+        lw = torch.empty((self.B, self.H, k), dtype=torch.float32, device=self.ws.device)
+        ln = C.c_int64(0)
+        m = C.c_int32(0)
+        _check(lib().thin_express_cache(self._h, _ptr(idx), _ptr(lw), C.byref(ln), C.byref(m),
+                                        _stream(stream)), "thin_express_cache")
+        return idx[..., :ln.value], lw[..., :ln.value], m.value
+
+    def close(self):
+        if self._h:
+            lib().thin_express_destroy(self._h)
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
 
 
 def thin_selftest_gram16(rows: torch.Tensor, stream=None) -> torch.Tensor:

@@ -3,6 +3,7 @@
 #include <math.h>
 
 #include <algorithm>
+#include <new>
 #include <stdint.h>
 #include <string.h>
 
@@ -139,6 +140,30 @@ hipError_t observed(int32_t kernel, int32_t round, hipStream_t st, F&& launch) {
   return e;
 }
 
+// One KH round over the S*G buckets described by `a`: one local launch for
+// small buckets, else pair scores then decisions, in as many launches as the
+// score region (e_bytes) needs.
+hipError_t kh_round(int32_t dtype, int64_t d, thin::HalveArgs a, int64_t buckets, size_t e_bytes,
+                    int32_t r, hipStream_t st) {
+  if (a.N <= thin::halve_local_rows(dtype, d) && buckets < kLocalMaxBuckets) {
+    a.b0 = 0;
+    return observed(THIN_KERNEL_LOCAL, r, st,
+                    [&] { return thin::launch_local(dtype, d, a, buckets, st); });
+  }
+  const size_t per = thin::halve_score_bytes(a.N);
+  int64_t chunk = (int64_t)(e_bytes / per);
+  if (chunk < 1) chunk = 1;
+  hipError_t e = hipSuccess;
+  for (int64_t b0 = 0; b0 < buckets && e == hipSuccess; b0 += chunk) {
+    a.b0 = b0;
+    const int64_t nbk = buckets - b0 < chunk ? buckets - b0 : chunk;
+    e = observed(THIN_KERNEL_SCORES, r, st, [&] { return thin::launch_scores(dtype, d, a, nbk, st); });
+    if (e == hipSuccess)
+      e = observed(THIN_KERNEL_DECIDE, r, st, [&] { return thin::launch_decide(a, nbk, st); });
+  }
+  return e;
+}
+
 int check_shape(int64_t B, int64_t H, int64_t n, int64_t d) {
   if (B < 1 || H < 1 || n < 1 || n > kMaxRows) return THIN_EINVAL;
   if (B * H > kMaxSlices) return THIN_EINVAL;
@@ -247,26 +272,8 @@ int compress_impl(const void* K, const void* V, int32_t dtype, int64_t B, int64_
       a.rowh2 = ws.rowh2;
       a.rowh2_write = r == 0;
       a.chunk0 = 0;
-      const int64_t buckets = S * lv.G[r];
-      if (lv.N[r] <= thin::halve_local_rows(dtype, d) && buckets < kLocalMaxBuckets) {
-        ok(observed(THIN_KERNEL_LOCAL, r, st, [&] {
-          a.b0 = 0;
-          return thin::launch_local(dtype, d, a, buckets, st);
-        }));
-        u_off += lv.n_r[r] / 2;
-        cur = out;
-        continue;
-      }
-      const size_t per = thin::halve_score_bytes(lv.N[r]);
-      int64_t chunk = (int64_t)(ws.e_bytes / per);
-      if (chunk < 1) chunk = 1;
-      for (int64_t b0 = 0; b0 < buckets && e == hipSuccess; b0 += chunk) {
-        a.b0 = b0;
-        const int64_t nbk = buckets - b0 < chunk ? buckets - b0 : chunk;
-        ok(observed(THIN_KERNEL_SCORES, r, st, [&] { return thin::launch_scores(dtype, d, a, nbk, st); }));
-        if (e == hipSuccess)
-          ok(observed(THIN_KERNEL_DECIDE, r, st, [&] { return thin::launch_decide(a, nbk, st); }));
-      }
+      a.b0 = 0;
+      ok(kh_round(dtype, d, a, S * lv.G[r], ws.e_bytes, r, st));
       u_off += lv.n_r[r] / 2;
       cur = out;
     }
@@ -284,6 +291,261 @@ int compress_impl(const void* K, const void* V, int32_t dtype, int64_t B, int64_
   return e == hipSuccess ? THIN_OK : THIN_EHIP;
 }
 
+
+// ---------------------------------------------------------------------------
+// Express cache (Alg. 1 with Compress2 of Alg. 2) and Thinformer decoding
+// (Alg. 4, WtdAttention of Alg. 5), without subsampling.  The counters run on
+// the host (they depend on the point count only); the index lists live in
+// the caller's workspace and every Halve call is one KH round of a single
+// bucket per slice.  C_0 is always the run of points c0_start .. t-1.
+// ---------------------------------------------------------------------------
+constexpr int kExMaxL = 30;
+
+// Cor. 2: delta_{m,i} (i >= 0) and delta_m / 2 (i < 0, the Halve phase).
+double express_delta(int m, int i, int mbar, double delta) {
+  const double dm = 0.5 * delta * (1.0 / log2(m / 2.0 + 2.0) - 1.0 / log2(m / 2.0 + 3.0));
+  if (i < 0) return dm / 2.0;
+  const int mp = m < mbar ? m : mbar;
+  return ldexp(dm, 2 * (i + 1 - mp)) / (3.0 * mp);
+}
+
+struct ExLayout {
+  size_t vmax, E, C[kExMaxL + 1], iota, t1, t2, keys, logw, lbt, h2, rowh2, score;
+  size_t e_bytes, bytes;
+};
+
+ExLayout ex_layout(int64_t S, int64_t n_out, int32_t mbar, int64_t n_max, int64_t kmax) {
+  ExLayout L{};
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t o = off;
+    off += align256(bytes);
+    return o;
+  };
+  const size_t s4 = (size_t)S * 4;
+  L.vmax = take(s4);
+  L.E = take(s4 * 4 * n_out);  // up to 4 n_out before the Halve phase
+  for (int i = 1; i <= mbar; ++i) L.C[i] = take(s4 * 2 * n_out);
+  L.iota = take(s4 * 2 * n_out);
+  L.t1 = take(s4 * 2 * n_out);
+  L.t2 = take(s4 * n_out);
+  L.keys = take(s4 * kmax);
+  L.logw = take(s4 * kmax);
+  L.lbt = take(s4 * 2 * n_out);
+  L.h2 = take(s4 * 2 * n_out);
+  L.rowh2 = take(s4 * n_max);
+  const size_t per = thin::halve_score_bytes(4 * n_out);
+  const size_t all = (size_t)S * per, cap = per > kScoreCap ? per : kScoreCap;
+  L.e_bytes = all < cap ? all : cap;
+  L.score = take(L.e_bytes);
+  L.bytes = off;
+  return L;
+}
+
+}  // namespace
+
+struct thin_express {
+  int32_t dtype, halve, mbar;
+  int64_t B, H, S, d, n_out, n_max, u_slice, kmax;
+  double delta;
+  unsigned char* ws;
+  ExLayout L;
+  // Alg. 1 / 2 counters
+  int32_t m, mp;
+  int64_t n, ell, nE, c0_start, upos;
+  int64_t nC[kExMaxL + 1];
+  bool over;
+};
+
+namespace {
+
+template <typename P>
+P* ex_ptr(const thin_express* x, size_t off) {
+  return reinterpret_cast<P*>(x->ws + off);
+}
+
+// Row stride of C_i in the current Compress2: its group size for i < mp, n_out for C_mp.
+int64_t ex_stride(const thin_express* x, int i) {
+  return i < x->mp ? (x->n_out << (i + 2)) >> x->mp : x->n_out;
+}
+
+void ex_reset(thin_express* x) {
+  x->mp = x->m < x->mbar ? x->m : x->mbar;
+  if (x->m > x->mbar) x->over = true;  // the next thin phase would need Subsample
+  const int64_t t0 = 4 * x->n_out;
+  if (x->mp >= 1 && (t0 % ((int64_t)1 << x->mp) != 0 || (t0 >> x->mp) < 2 || ((t0 >> x->mp) & 1)))
+    x->over = true;
+  for (int i = 0; i <= kExMaxL; ++i) x->nC[i] = 0;
+  x->c0_start = x->n;
+}
+
+// Device side of one update (null: count only).
+struct ExRun {
+  const void* K;
+  const void* V;
+  const float* U;
+  uint8_t* trace;
+  hipStream_t st;
+};
+
+hipError_t ex_halve(thin_express* x, const ExRun* run, const int32_t* in, int64_t N, double delta,
+                    int32_t* out) {
+  const int64_t o = x->upos;
+  x->upos += N / 2;
+  if (!run) return hipSuccess;
+  hipStream_t st = run->st;
+  if (x->halve == THIN_HALVE_UNIFORM)
+    return observed(THIN_KERNEL_UNIFORM, -1, st, [&] {
+      return thin::launch_uniform_halve(x->S, N, in, run->U, x->u_slice, o, out, run->trace, st);
+    });
+  uint32_t* vmax = ex_ptr<uint32_t>(x, x->L.vmax);
+  hipError_t e = observed(THIN_KERNEL_EXPRESS, -1, st, [&] {
+    return thin::launch_vmax_rows(x->dtype, run->V, x->n_max, x->d, in, N, x->S, vmax, st);
+  });
+  if (e != hipSuccess) return e;
+  thin::HalveArgs a{};
+  a.K = run->K;
+  a.V = run->V;
+  a.n = x->n_max;
+  a.ld = x->n_max;
+  a.vmax_bits = vmax;
+  a.idx_in = in;
+  a.n_r = N;
+  a.N = (int32_t)N;
+  a.G = 1;
+  a.S = x->S;
+  a.idx_out = out;
+  a.U = run->U;
+  a.u_slice = x->u_slice;
+  a.u_off = o;
+  a.trace = run->trace;
+  a.log_c = log(0.5 + log(2.0 * (double)N / delta));
+  a.E = ex_ptr<float>(x, x->L.score);
+  a.lbt = ex_ptr<float>(x, x->L.lbt);
+  a.h2 = ex_ptr<float>(x, x->L.h2);
+  a.rowh2 = ex_ptr<float>(x, x->L.rowh2);
+  a.rowh2_write = 1;
+  a.chunk0 = 0;
+  a.b0 = 0;
+  return kh_round(x->dtype, x->d, a, x->S, x->L.e_bytes, -1, st);
+}
+
+hipError_t ex_iota(const thin_express* x, const ExRun* run, int32_t* dst, int64_t stride,
+                   int64_t start, int64_t len) {
+  if (!run) return hipSuccess;
+  return observed(THIN_KERNEL_EXPRESS, -1, run->st, [&] {
+    return thin::launch_rows_iota(dst, stride, start, len, x->S, run->st);
+  });
+}
+
+hipError_t ex_copy(const thin_express* x, const ExRun* run, const int32_t* src, int64_t sstride,
+                   int32_t* dst, int64_t dstride, int64_t len) {
+  if (!run) return hipSuccess;
+  return observed(THIN_KERNEL_EXPRESS, -1, run->st, [&] {
+    return thin::launch_rows_copy(src, sstride, dst, dstride, len, x->S, run->st);
+  });
+}
+
+// Express.update with the next point (Alg. 1), Compress2.update inside (Alg. 2).
+hipError_t ex_update(thin_express* x, const ExRun* run) {
+  const int64_t p = x->n;  // the point's position
+  int32_t* E = ex_ptr<int32_t>(x, x->L.E);
+  const int64_t sE = 4 * x->n_out;
+  hipError_t e = hipSuccess;
+  x->n += 1;
+  if (x->n <= x->n_out) {  // exact phase
+    e = ex_iota(x, run, E + x->nE, sE, p, 1);
+    x->nE += 1;
+    x->c0_start = x->n;
+    return e;
+  }
+  x->ell += 1;
+  x->nC[0] += 1;  // C_0 = points c0_start .. p
+  int32_t* t1 = ex_ptr<int32_t>(x, x->L.t1);
+  for (int i = 0; i < x->mp && e == hipSuccess; ++i) {
+    const int64_t T = (x->n_out << (i + 2)) >> x->mp;
+    if (x->nC[i] != T) continue;
+    const int32_t* in;
+    if (i == 0) {
+      int32_t* io = ex_ptr<int32_t>(x, x->L.iota);
+      e = ex_iota(x, run, io, T, x->c0_start, T);
+      in = io;
+    } else {
+      in = ex_ptr<int32_t>(x, x->L.C[i]);
+    }
+    if (e == hipSuccess) e = ex_halve(x, run, in, T, express_delta(x->m, i, x->mbar, x->delta), t1);
+    if (e == hipSuccess)
+      e = ex_copy(x, run, t1, T / 2, ex_ptr<int32_t>(x, x->L.C[i + 1]) + x->nC[i + 1],
+                  ex_stride(x, i + 1), T / 2);
+    x->nC[i + 1] += T / 2;
+    x->nC[i] = 0;
+    if (i == 0) x->c0_start = x->n;
+  }
+  if (e == hipSuccess && x->ell == (x->n_out << x->m)) {  // E gets the group's coreset
+    if (x->mp == 0)
+      e = ex_iota(x, run, E + x->nE, sE, x->c0_start, x->nC[0]);
+    else
+      e = ex_copy(x, run, ex_ptr<int32_t>(x, x->L.C[x->mp]), ex_stride(x, x->mp), E + x->nE, sE,
+                  x->nC[x->mp]);
+    x->nE += x->nC[x->mp];
+    x->ell = 0;
+  }
+  if (e == hipSuccess && x->n == 4 * (x->n_out << x->m)) {  // Halve phase: E halved twice
+    const double dl = express_delta(x->m, -1, x->mbar, x->delta);
+    int32_t* t2 = ex_ptr<int32_t>(x, x->L.t2);
+    e = ex_halve(x, run, E, x->nE, dl, t1);
+    if (e == hipSuccess) e = ex_halve(x, run, t1, x->nE / 2, dl, t2);
+    if (e == hipSuccess) e = ex_copy(x, run, t2, x->nE / 4, E, sE, x->nE / 4);
+    x->nE /= 4;
+    x->m += 2;
+  }
+  if (x->ell == 0) ex_reset(x);
+  return e;
+}
+
+// Segments of the weighted cache: C_0 (points c0_start.. c0_start+len0-1),
+// C_1..C_mp, E.
+thin::ExpressSegs ex_segs(const thin_express* x, int64_t len0) {
+  thin::ExpressSegs g{};
+  const float ln2 = (float)log(2.0);
+  g.seg[g.n++] = {nullptr, 0, x->c0_start, len0, -(float)x->mp * ln2};
+  for (int i = 1; i <= x->mp; ++i)
+    if (x->nC[i] > 0)
+      g.seg[g.n++] = {ex_ptr<int32_t>(x, x->L.C[i]), ex_stride(x, i), 0, x->nC[i],
+                      (float)(i - x->mp) * ln2};
+  if (x->nE > 0) g.seg[g.n++] = {ex_ptr<int32_t>(x, x->L.E), 4 * x->n_out, 0, x->nE, 0.0f};
+  return g;
+}
+
+int64_t seg_total(const thin::ExpressSegs& g) {
+  int64_t t = 0;
+  for (int k = 0; k < g.n; ++k) t += g.seg[k].len;
+  return t;
+}
+
+// Size checks shared by plan and create; counts uniforms and the largest key
+// list over n_max points.
+int ex_check(int64_t B, int64_t H, int64_t d, int64_t n_out, int32_t mbar, int64_t n_max,
+             int64_t* u_slice, int64_t* kmax) {
+  if (B < 1 || H < 1 || B * H > kMaxSlices || !supported_d(d)) return THIN_EINVAL;
+  if (n_out < 1 || 4 * n_out > kMaxBucket || mbar < 0 || mbar > kExMaxL - 2) return THIN_EINVAL;
+  if (n_max < 1 || n_max > kMaxRows) return THIN_EINVAL;
+  thin_express x{};
+  x.n_out = n_out;
+  x.mbar = mbar;
+  x.delta = 0.5;
+  ex_reset(&x);
+  int64_t km = 1;
+  for (int64_t t = 0; t < n_max; ++t) {
+    if (x.n >= n_out && x.over) return THIN_EINVAL;
+    const int64_t k = seg_total(ex_segs(&x, t - x.c0_start + 1));
+    if (k > km) km = k;
+    ex_update(&x, nullptr);
+  }
+  *u_slice = x.upos;
+  *kmax = km;
+  return THIN_OK;
+}
 }  // namespace
 
 extern "C" {
@@ -387,6 +649,105 @@ const char* thin_status_str(int status) {
     case THIN_EHIP: return "THIN_EHIP: HIP runtime error";
     default: return "THIN: unknown status";
   }
+}
+
+}  // extern "C"
+
+extern "C" {
+
+int thin_express_plan(int64_t B, int64_t H, int64_t d, int64_t n_out, int32_t mbar,
+                      int64_t n_max, thin_express_plan_t* plan) {
+  if (!plan) return THIN_EINVAL;
+  int64_t u = 0, k = 0;
+  const int rc = ex_check(B, H, d, n_out, mbar, n_max, &u, &k);
+  if (rc) return rc;
+  plan->uniforms_per_slice = u;
+  plan->max_keys = k;
+  plan->workspace_bytes = ex_layout(B * H, n_out, mbar, n_max, k).bytes;
+  return THIN_OK;
+}
+
+int thin_express_create(int32_t dtype, int64_t B, int64_t H, int64_t d, int64_t n_out,
+                        int32_t mbar, double delta, int32_t halve, int64_t n_max,
+                        void* workspace, size_t workspace_bytes, thin_express_t** out) {
+  if (!out) return THIN_EINVAL;
+  *out = nullptr;
+  if (dtype != THIN_FP32 && dtype != THIN_BF16) return THIN_EDTYPE;
+  if (halve != THIN_HALVE_KH && halve != THIN_HALVE_UNIFORM) return THIN_EINVAL;
+  if (!(delta > 0.0 && delta < 1.0)) return THIN_EINVAL;
+  int64_t u = 0, k = 0;
+  const int rc = ex_check(B, H, d, n_out, mbar, n_max, &u, &k);
+  if (rc) return rc;
+  const ExLayout L = ex_layout(B * H, n_out, mbar, n_max, k);
+  if (!workspace || workspace_bytes < L.bytes) return THIN_EWORKSPACE;
+  if ((reinterpret_cast<uintptr_t>(workspace) & 255u) != 0) return THIN_EWORKSPACE;
+  thin_express* x = new (std::nothrow) thin_express();
+  if (!x) return THIN_EINVAL;
+  x->dtype = dtype;
+  x->halve = halve;
+  x->mbar = mbar;
+  x->B = B;
+  x->H = H;
+  x->S = B * H;
+  x->d = d;
+  x->n_out = n_out;
+  x->n_max = n_max;
+  x->u_slice = u;
+  x->kmax = k;
+  x->delta = delta;
+  x->ws = static_cast<unsigned char*>(workspace);
+  x->L = L;
+  ex_reset(x);
+  *out = x;
+  return THIN_OK;
+}
+
+int thin_express_step(thin_express_t* x, const void* Q, const void* K, const void* V,
+                      const float* uniforms, int64_t n_uniforms, void* O, int32_t out_dtype,
+                      uint8_t* swap_trace, void* stream) {
+  if (!x || !Q || !K || !V || !O) return THIN_EINVAL;
+  if (out_dtype != THIN_FP32 && out_dtype != THIN_BF16) return THIN_EDTYPE;
+  if (x->n >= x->n_max || (x->n >= x->n_out && x->over)) return THIN_EINVAL;
+  if (x->u_slice > 0 && !uniforms) return THIN_EINVAL;
+  if (n_uniforms < x->S * x->u_slice) return THIN_EUNIFORMS;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  const int64_t t = x->n;
+  // WtdAttention: the cache plus the point itself, which joins C_0
+  const thin::ExpressSegs g = ex_segs(x, t - x->c0_start + 1);
+  const int64_t m = seg_total(g);
+  int32_t* keys = ex_ptr<int32_t>(x, x->L.keys);
+  float* logw = ex_ptr<float>(x, x->L.logw);
+  hipError_t e = observed(THIN_KERNEL_EXPRESS, -1, st, [&] {
+    return thin::launch_express_keys(g, x->S, m, m, keys, logw, st);
+  });
+  if (e == hipSuccess)
+    e = observed(THIN_KERNEL_ATTENTION, -1, st, [&] {
+      return thin::launch_attention(x->dtype, x->d, out_dtype, Q, K, V, keys, logw, x->S,
+                                    x->n_max, 1, m, O, st);
+    });
+  const ExRun run{K, V, uniforms, swap_trace, st};
+  if (e == hipSuccess) e = ex_update(x, &run);
+  return e == hipSuccess ? THIN_OK : THIN_EHIP;
+}
+
+int thin_express_cache(const thin_express_t* x, int32_t* idx, float* logw, int64_t* len,
+                       int32_t* m, void* stream) {
+  if (!x || !idx || !logw || !len) return THIN_EINVAL;
+  const thin::ExpressSegs g = ex_segs(x, x->nC[0]);
+  const int64_t k = seg_total(g);
+  *len = k;
+  if (m) *m = x->m;
+  if (k == 0) return THIN_OK;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  const hipError_t e = observed(THIN_KERNEL_EXPRESS, -1, st, [&] {
+    return thin::launch_express_keys(g, x->S, k, x->kmax, idx, logw, st);
+  });
+  return e == hipSuccess ? THIN_OK : THIN_EHIP;
+}
+
+int thin_express_destroy(thin_express_t* x) {
+  delete x;
+  return THIN_OK;
 }
 
 }  // extern "C"

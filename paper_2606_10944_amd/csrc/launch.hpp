@@ -77,6 +77,33 @@ hipError_t launch_decide(const HalveArgs& a, int64_t nbk, hipStream_t st);
 int64_t halve_local_rows(int dtype, int64_t d);
 hipError_t launch_local(int dtype, int64_t d, const HalveArgs& a, int64_t nbk, hipStream_t st);
 
+// Express cache (express.hip).  A segment of a slice's key list: src null =
+// the rows start .. start+len-1, else src[s * stride + 0 .. len-1]; every key
+// of the segment has log-weight logw.
+struct ExpressSeg {
+  const int32_t* src;
+  int64_t stride;
+  int64_t start;
+  int64_t len;
+  float logw;
+};
+constexpr int kExpressMaxSegs = 34;
+struct ExpressSegs {
+  ExpressSeg seg[kExpressMaxSegs];
+  int n;
+};
+hipError_t launch_rows_iota(int32_t* dst, int64_t dst_stride, int64_t start, int64_t len,
+                            int64_t S, hipStream_t st);
+hipError_t launch_rows_copy(const int32_t* src, int64_t src_stride, int32_t* dst,
+                            int64_t dst_stride, int64_t len, int64_t S, hipStream_t st);
+// v_max bits per slice over the rows idx[s, 0..N) of V (slices ld rows apart).
+hipError_t launch_vmax_rows(int dtype, const void* V, int64_t ld, int64_t d, const int32_t* idx,
+                            int64_t N, int64_t S, uint32_t* vmax_bits, hipStream_t st);
+// idx / logw [S, out_stride]: the segments laid out one after another in the
+// first m entries of each slice (their lengths sum to m).
+hipError_t launch_express_keys(const ExpressSegs& segs, int64_t S, int64_t m, int64_t out_stride,
+                               int32_t* idx, float* logw, hipStream_t st);
+
 // logw (nullable) [S, n_out]: log-weight of every coreset key.
 hipError_t launch_attention(int dtype, int64_t d, int out_dtype, const void* Q, const void* K,
                             const void* V, const int32_t* idx, const float* logw, int64_t S,

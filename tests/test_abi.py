@@ -193,3 +193,35 @@ def test_launch_hook_can_be_set_and_cleared():
     assert _compress(dtype=5) == _lib.THIN_EDTYPE
     assert L.thin_set_launch_hook(_lib.LaunchHook(), None) == _lib.THIN_OK
     assert calls == []
+
+
+@pytest.mark.parametrize("n_out,mbar,n_max", [(8, 4, 512), (8, 4, 300), (16, 4, 1000),
+                                              (128, 6, 16384), (128, 8, 100000), (4, 2, 64),
+                                              (32, 5, 2000)])
+def test_express_plan_counts_the_oracles_uniforms(n_out, mbar, n_max):
+    p = _lib.thin_express_plan(2, 3, 64, n_out, mbar, n_max)
+    assert p["uniforms_per_slice"] == oracle.express_uniforms(n_max, n_out, mbar)
+    assert 1 <= p["max_keys"] <= 6 * n_out + 1 and p["workspace_bytes"] > 0
+
+
+def test_express_rejects_unsupported_sizes():
+    L = _lib.lib()
+    plan = _lib.ExpressPlan()
+
+    def rc(B=1, H=1, d=64, n_out=8, mbar=4, n_max=512):
+        return L.thin_express_plan(B, H, d, n_out, mbar, n_max, C.byref(plan))
+
+    assert rc() == _lib.THIN_OK
+    assert rc(n_max=513) == _lib.THIN_EINVAL          # the next thin phase needs m = 6 > mbar
+    assert rc(mbar=5, n_max=513) == _lib.THIN_EINVAL  # m = 6 > 5 as well
+    assert rc(n_out=4, mbar=4, n_max=300) == _lib.THIN_EINVAL  # groups of 4*4/16 = 1 point
+    assert rc(d=80) == _lib.THIN_EINVAL
+    assert rc(n_out=4096) == _lib.THIN_EINVAL         # 4 n_out above the largest bucket
+    assert rc(n_max=0) == _lib.THIN_EINVAL
+    h = C.c_void_p()
+    assert L.thin_express_create(1, 1, 1, 64, 8, 4, 0.0, 0, 512, FAKE, 1 << 30,
+                                 C.byref(h)) == _lib.THIN_EINVAL   # delta = 0
+    assert L.thin_express_create(1, 1, 1, 64, 8, 4, 0.5, 0, 512, None, 1 << 30,
+                                 C.byref(h)) == _lib.THIN_EWORKSPACE
+    assert L.thin_express_create(1, 1, 1, 64, 8, 4, 0.5, 0, 512, C.c_void_p(0x100010), 1 << 30,
+                                 C.byref(h)) == _lib.THIN_EWORKSPACE  # not 256-byte aligned

@@ -1,0 +1,69 @@
+"""Thinformer decoding over the Express cache (thin_express_*) against the
+CPU oracle: every point's output (max-abs 2e-3 for bf16 inputs, 1e-5 for
+fp32) and the final weighted cache (indices bit-exact, KH decisions in
+follow mode at a 1e-5 relative margin as for the compress path; uniform
+halving bit-exact including its swap bits)."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2606_10944_amd import ExpressCache, thin_express_plan
+from paper_2606_10944_amd import workloads as W
+
+pytestmark = pytest.mark.gpu
+DEV = torch.device("cuda:0")
+MARGIN = 1e-5
+
+CASES = [
+    # exact phase, levels 0, 2, 4 and their Halve phases (all KH calls local)
+    dict(B=2, H=2, d=64, dtype="bf16", n_out=8, mbar=4, n=512, halve="kh"),
+    dict(B=1, H=3, d=32, dtype="bf16", n_out=8, mbar=4, n=400, halve="uniform"),
+    dict(B=1, H=2, d=128, dtype="fp32", n_out=16, mbar=4, n=1024, halve="kh"),
+    # n_out = 128: Halve phase on 512 points (pair scores + decisions), a partial level 2
+    dict(B=1, H=2, d=128, dtype="bf16", n_out=128, mbar=6, n=1800, halve="kh"),
+]
+
+
+def _run(c):
+    w = W.custom("ex", B=c["B"], H=c["H"], n=c["n"], d=c["d"], dtype=c["dtype"], kind="gauss")
+    Q, K, V = W.make_qkv(w)
+    plan = thin_express_plan(w.B, w.H, w.d, c["n_out"], c["mbar"], w.n)
+    U = W.make_uniforms(w, w.S * plan["uniforms_per_slice"])
+    dt = torch.bfloat16 if c["dtype"] == "bf16" else torch.float32
+    ex = ExpressCache(w.B, w.H, w.d, c["n_out"], c["mbar"], w.n, dtype=dt, halve=c["halve"])
+    Qd, Kd, Vd, Ud = Q.to(DEV), K.to(DEV), V.to(DEV), U.to(DEV)
+    tr = torch.zeros(max(U.numel(), 1), dtype=torch.uint8, device=DEV)
+    O = torch.empty((w.B, w.H, w.n, w.d), dtype=torch.float32, device=DEV)
+    for t in range(w.n):
+        O[:, :, t] = ex.step(Qd[:, :, t].contiguous(), Kd, Vd, Ud, trace=tr)
+    idx, lw, m = ex.cache()
+    torch.cuda.synchronize()
+    ex.close()
+    return w, Q, K, V, U, O.cpu().numpy(), idx.cpu().numpy(), lw.cpu().numpy(), m, \
+        tr.cpu().numpy(), plan
+
+
+@pytest.mark.parametrize("c", CASES, ids=lambda c: f"o{c['n_out']}-mbar{c['mbar']}-n{c['n']}-d{c['d']}-{c['dtype']}-{c['halve']}")
+def test_express_decode_parity(c):
+    w, Q, K, V, U, O, idx, lw, m, tr, plan = _run(c)
+    us = plan["uniforms_per_slice"]
+    Us = U.numpy().reshape(w.S, -1) if us else np.zeros((w.S, 1), np.float32)
+    ts = tr[: w.S * us].reshape(w.S, -1) if us else np.zeros((w.S, 1), np.uint8)
+    tol = 2e-3 if c["dtype"] == "bf16" else 1e-5
+    near = 0
+    for s in range(w.S):
+        b, h = divmod(s, w.H)
+        r = oracle.express_decode(Q[b, h], K[b, h], V[b, h], c["n_out"], c["mbar"], Us[s],
+                                  halve=c["halve"], follow=ts[s] if c["halve"] == "kh" else None,
+                                  tol=MARGIN)
+        assert r["stats"]["hard_mismatch"] == 0, (s, r["stats"])
+        near += r["stats"]["near_ties"]
+        if c["halve"] == "uniform":
+            assert np.array_equal(r["bits"], ts[s]), s
+        assert r["m"] == m
+        assert np.array_equal(r["idx"], idx[b, h]), s
+        np.testing.assert_allclose(lw[b, h], r["logw"].astype(np.float32), rtol=1e-6, atol=1e-7)
+        err = np.abs(r["O"] - O[b, h]).max()
+        assert err <= tol, (s, err)
+    print(f"near ties {near}")

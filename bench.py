@@ -14,6 +14,11 @@ per-kernel times and the roofline figures.  Prints one JSON line.
 With --sinks / --window the first S and last W keys of every slice are kept
 exactly, the rows between them are thinned to n_out, and attention runs over
 the S + n_out + W weighted keys (eq. def:att_approx).
+
+--mode decode measures Thinformer decoding over the Express cache instead
+(Alg. 4): B=1, H=32 slices, d=128, bf16, n_out=128, mbar=8, 16384 points
+decoded one at a time (each attends over the cache plus itself, then enters
+it); one step = one point of every slice.
 """
 import argparse
 import collections
@@ -179,6 +184,109 @@ def cpu_baseline(w, Q, K, V, U, plan, budget_s: float = 20.0, halve: str = "kh",
                       f"{t_used:.1f} s"}
 
 
+DECODE = dict(B=1, H=32, d=128, dtype="bf16", n_out=128, mbar=8, n=16384)
+
+
+def decode_main(args):
+    """Thinformer decoding over the Express cache (one JSON line)."""
+    import numpy as np
+    import torch
+
+    from paper_2606_10944_amd import ExpressCache, LaunchTimer, thin_express_plan
+    from paper_2606_10944_amd import workloads as W
+    c = DECODE
+    w = W.custom("decode", B=c["B"], H=c["H"], n=c["n"], d=c["d"], dtype=c["dtype"],
+                 kind="heavy_tail")
+    Q, K, V = W.make_qkv(w)
+    plan = thin_express_plan(w.B, w.H, w.d, c["n_out"], c["mbar"], w.n)
+    U = W.make_uniforms(w, w.S * plan["uniforms_per_slice"])
+    dev = torch.device("cuda:0")
+    Qd, Kd, Vd, Ud = Q.to(dev), K.to(dev), V.to(dev), U.to(dev)
+    Qt = [Qd[:, :, t].contiguous() for t in range(w.n)]
+    O = torch.empty((w.B, w.H, w.d), dtype=torch.float32, device=dev)
+    stream = torch.cuda.current_stream()
+
+    def run(n_steps, timer=None, keys=None):
+        ex = ExpressCache(w.B, w.H, w.d, c["n_out"], c["mbar"], w.n, dtype=torch.bfloat16)
+        for t in range(n_steps):
+            if keys is not None:
+                keys.append(ex.next_keys())
+            ex.step(Qt[t], Kd, Vd, Ud, O=O, stream=stream)
+        return ex
+
+    for _ in range(max(args.warmup // 50, 1)):
+        run(1024).close()
+    torch.cuda.synchronize()
+    t0 = torch.cuda.Event(enable_timing=True)
+    t1 = torch.cuda.Event(enable_timing=True)
+    t0.record(stream)
+    ex = run(w.n)
+    t1.record(stream)
+    torch.cuda.synchronize()
+    ex.close()
+    ms_total = t0.elapsed_time(t1)
+    # per-kernel times over the last 2048 points (where the cache is largest)
+    keys = []
+    ex = ExpressCache(w.B, w.H, w.d, c["n_out"], c["mbar"], w.n, dtype=torch.bfloat16)
+    tail = 2048
+    for t in range(w.n - tail):
+        ex.step(Qt[t], Kd, Vd, Ud, O=O, stream=stream)
+    torch.cuda.synchronize()
+    with LaunchTimer(stream, capacity=16 * tail) as lt:
+        for t in range(w.n - tail, w.n):
+            keys.append(ex.next_keys())
+            ex.step(Qt[t], Kd, Vd, Ud, O=O, stream=stream)
+        torch.cuda.synchronize()
+    ex.close()
+    rec = lt.records()
+    per = collections.defaultdict(float)
+    for name, _, ms in rec:
+        per[name] += ms / tail
+    att = [ms for name, _, ms in rec if name == "attention"]
+    att_ms = statistics.mean(att)
+    # algorithmic bytes of one attention launch: per slice the query row, the
+    # output row (fp32) and per key its K and V rows, index and log-weight
+    kb = elem_bytes(w.dtype)
+    att_bytes = w.S * (statistics.mean(keys) * (2 * w.d * kb + 8) + w.d * (kb + 4))
+    gbs = att_bytes / (att_ms * 1e-3) / 1e9
+    value = w.S * w.n / (ms_total * 1e-3)
+    out = {
+        "metric": "Thinformer decoding over the Express cache: points/s over B·H slices",
+        "value": value, "unit": "points/s", "n_gpus": 1, "steps": w.n, "warmup": args.warmup,
+        "ms_per_step": ms_total / w.n, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": w.dtype, "data": "synthetic",
+        "config": {"workload": "express-decode", "B": w.B, "H": w.H, "n": w.n, "d": w.d,
+                   "n_out": c["n_out"], "mbar": c["mbar"], "delta": 0.5, "halve": "kh"},
+        "roofline": {
+            "kernel": "coreset attention of one query per slice over the weighted cache "
+                      "(last 2048 points)",
+            "bound": "hbm", "achieved": gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+            "frac": gbs / HBM_PEAK_GBS, "traffic": None,
+            "algorithmic_bytes_per_launch": att_bytes, "ms_per_launch": att_ms,
+            "mean_keys": statistics.mean(keys)},
+        "ms_per_step_by_kernel_last_2048": dict(per),
+        "gpu": torch.cuda.get_device_name(0),
+    }
+    if not args.no_cpu_baseline:
+        import oracle
+        oracle.lib()
+        Us = U.numpy().reshape(w.S, -1)
+        t_used, done = 0.0, 0
+        for s in range(w.S):
+            t_a = time.perf_counter()
+            oracle.express_decode(Q[0, s], K[0, s], V[0, s], c["n_out"], c["mbar"], Us[s])
+            t_used += time.perf_counter() - t_a
+            done += 1
+            if t_used >= 20.0:
+                break
+        out["cpu_baseline"] = {
+            "value": done * w.n / t_used, "unit": "points/s", "cores": 1, "kind": "oracle",
+            "sample": f"{done} of {w.S} slices decoded over all {w.n} points, float64, one "
+                      f"thread, {t_used:.1f} s"}
+    _ = np  # noqa: F841
+    print(json.dumps(out), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -193,11 +301,16 @@ def main():
                     help="keys kept exactly at the start of every slice")
     ap.add_argument("--window", type=int, default=0,
                     help="keys kept exactly at the end of every slice")
+    ap.add_argument("--mode", choices=["compress", "decode"], default="compress",
+                    help="compress + attention (default) or Express decoding")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: the thinning path runs each (batch, head) "
               "slice independently and this build has no multi-GPU mode.", file=sys.stderr)
         sys.exit(2)
+    if args.mode == "decode":
+        decode_main(args)
+        return
 
     import torch
 

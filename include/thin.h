@@ -277,6 +277,10 @@ int thin_express_step(thin_express_t* x, const void* Q, const void* K, const voi
 int thin_express_cache(const thin_express_t* x, int32_t* idx, float* logw, int64_t* len,
                        int32_t* m, void* stream);
 
+/* Host-only: *keys = the size of the key list the next step attends over
+ * (the cache plus the point itself), *t = the next point's position. */
+int thin_express_next(const thin_express_t* x, int64_t* keys, int64_t* t);
+
 /* Free the host state (the workspace stays the caller's). */
 int thin_express_destroy(thin_express_t* x);
 

@@ -23,7 +23,8 @@ THIN_FP32, THIN_BF16 = 0, 1
 # Every symbol include/thin.h declares.
 EXPORTS = ("thin_plan", "thin_compress", "thin_compress_traced", "thin_compress_ex", "thin_attention",
            "thin_attention_ex", "thin_express_plan", "thin_express_create", "thin_express_step",
-           "thin_express_cache", "thin_express_destroy", "thin_selftest_gram16", "thin_status_str",
+           "thin_express_cache", "thin_express_next", "thin_express_destroy",
+           "thin_selftest_gram16", "thin_status_str",
            "thin_set_launch_hook")
 
 # thin_kernel_t
@@ -87,6 +88,7 @@ def lib():
                                       C.POINTER(C.c_void_p)]
     L.thin_express_step.argtypes = [P, P, P, P, P, I64, P, I32, P, P]
     L.thin_express_cache.argtypes = [P, P, P, C.POINTER(C.c_int64), C.POINTER(C.c_int32), P]
+    L.thin_express_next.argtypes = [P, C.POINTER(C.c_int64), C.POINTER(C.c_int64)]
     L.thin_express_destroy.argtypes = [P]
     L.thin_selftest_gram16.argtypes = [I32, I64, P, P, P]
     L.thin_status_str.argtypes = [C.c_int]
@@ -96,7 +98,7 @@ def lib():
     for f in ("thin_plan", "thin_compress", "thin_compress_traced", "thin_compress_ex",
               "thin_attention", "thin_attention_ex", "thin_selftest_gram16", "thin_express_plan",
               "thin_express_create", "thin_express_step", "thin_express_cache",
-              "thin_express_destroy"):
+              "thin_express_next", "thin_express_destroy"):
         getattr(L, f).restype = C.c_int
     _lib = L
     return L
@@ -298,6 +300,12 @@ class ExpressCache:
         _check(rc, "thin_express_step")
         self.n += 1
         return O
+
+    def next_keys(self) -> int:
+        """Keys the next step attends over (host-only)."""
+        k, t = C.c_int64(0), C.c_int64(0)
+        _check(lib().thin_express_next(self._h, C.byref(k), C.byref(t)), "thin_express_next")
+        return k.value
 
     def cache(self, stream=None):
         """(idx [B,H,len] int32, logw [B,H,len] float32, m): the current

@@ -310,11 +310,12 @@ double express_delta(int m, int i, int mbar, double delta) {
 }
 
 struct ExLayout {
-  size_t vmax, E, C[kExMaxL + 1], iota, t1, t2, keys, logw, lbt, h2, rowh2, score;
+  size_t vmax, E, C[kExMaxL + 1], iota, t1, t2, part, lbt, h2, rowh2, score;
   size_t e_bytes, bytes;
 };
 
-ExLayout ex_layout(int64_t S, int64_t n_out, int32_t mbar, int64_t n_max, int64_t kmax) {
+ExLayout ex_layout(int64_t S, int64_t d, int64_t n_out, int32_t mbar, int64_t n_max,
+                   int64_t kmax) {
   ExLayout L{};
   size_t off = 0;
   auto take = [&](size_t bytes) {
@@ -329,8 +330,8 @@ ExLayout ex_layout(int64_t S, int64_t n_out, int32_t mbar, int64_t n_max, int64_
   L.iota = take(s4 * 2 * n_out);
   L.t1 = take(s4 * 2 * n_out);
   L.t2 = take(s4 * n_out);
-  L.keys = take(s4 * kmax);
-  L.logw = take(s4 * kmax);
+  (void)kmax;
+  L.part = take(s4 * thin::kDecodeMaxSplit * (d + 2));
   L.lbt = take(s4 * 2 * n_out);
   L.h2 = take(s4 * 2 * n_out);
   L.rowh2 = take(s4 * n_max);
@@ -663,7 +664,7 @@ int thin_express_plan(int64_t B, int64_t H, int64_t d, int64_t n_out, int32_t mb
   if (rc) return rc;
   plan->uniforms_per_slice = u;
   plan->max_keys = k;
-  plan->workspace_bytes = ex_layout(B * H, n_out, mbar, n_max, k).bytes;
+  plan->workspace_bytes = ex_layout(B * H, d, n_out, mbar, n_max, k).bytes;
   return THIN_OK;
 }
 
@@ -678,7 +679,7 @@ int thin_express_create(int32_t dtype, int64_t B, int64_t H, int64_t d, int64_t 
   int64_t u = 0, k = 0;
   const int rc = ex_check(B, H, d, n_out, mbar, n_max, &u, &k);
   if (rc) return rc;
-  const ExLayout L = ex_layout(B * H, n_out, mbar, n_max, k);
+  const ExLayout L = ex_layout(B * H, d, n_out, mbar, n_max, k);
   if (!workspace || workspace_bytes < L.bytes) return THIN_EWORKSPACE;
   if ((reinterpret_cast<uintptr_t>(workspace) & 255u) != 0) return THIN_EWORKSPACE;
   thin_express* x = new (std::nothrow) thin_express();
@@ -715,16 +716,10 @@ int thin_express_step(thin_express_t* x, const void* Q, const void* K, const voi
   // WtdAttention: the cache plus the point itself, which joins C_0
   const thin::ExpressSegs g = ex_segs(x, t - x->c0_start + 1);
   const int64_t m = seg_total(g);
-  int32_t* keys = ex_ptr<int32_t>(x, x->L.keys);
-  float* logw = ex_ptr<float>(x, x->L.logw);
-  hipError_t e = observed(THIN_KERNEL_EXPRESS, -1, st, [&] {
-    return thin::launch_express_keys(g, x->S, m, m, keys, logw, st);
+  hipError_t e = observed(THIN_KERNEL_ATTENTION, -1, st, [&] {
+    return thin::launch_decode_attention(x->dtype, x->d, out_dtype, Q, K, V, g, x->S, x->n_max, m,
+                                         ex_ptr<float>(x, x->L.part), O, st);
   });
-  if (e == hipSuccess)
-    e = observed(THIN_KERNEL_ATTENTION, -1, st, [&] {
-      return thin::launch_attention(x->dtype, x->d, out_dtype, Q, K, V, keys, logw, x->S,
-                                    x->n_max, 1, m, O, st);
-    });
   const ExRun run{K, V, uniforms, swap_trace, st};
   if (e == hipSuccess) e = ex_update(x, &run);
   return e == hipSuccess ? THIN_OK : THIN_EHIP;
@@ -743,6 +738,13 @@ int thin_express_cache(const thin_express_t* x, int32_t* idx, float* logw, int64
     return thin::launch_express_keys(g, x->S, k, x->kmax, idx, logw, st);
   });
   return e == hipSuccess ? THIN_OK : THIN_EHIP;
+}
+
+int thin_express_next(const thin_express_t* x, int64_t* keys, int64_t* t) {
+  if (!x || !keys || !t) return THIN_EINVAL;
+  *keys = seg_total(ex_segs(x, x->n - x->c0_start + 1));
+  *t = x->n;
+  return THIN_OK;
 }
 
 int thin_express_destroy(thin_express_t* x) {

@@ -80,7 +80,220 @@ __global__ void express_keys_kernel(ExpressSegs segs, int64_t m, int64_t out_str
   logw[s * out_stride + j] = g.logw;
 }
 
+// ---------------------------------------------------------------------------
+// Weighted attention of one query per slice (a decoding step, Alg. 5) over
+// the m keys of the cache segments (read in place: no key list is written),
+// each key with its segment's log-weight.  The keys of a slice
+// are split over `split` workgroups; in a workgroup, wave w takes keys
+// k0 + w, k0 + w + 4, ..; a key's row is spread over the lanes (EPL elements
+// each), its score reduced across the wave, and each wave keeps an online
+// softmax (log2 domain) of its keys.  The waves merge in LDS and the
+// workgroup writes its unnormalised partial (max, sum, acc[D]); a second
+// kernel merges a slice's partials and normalises.
+// ---------------------------------------------------------------------------
+constexpr int kDecWaves = 4;
+constexpr int kDecUnroll = 4;
+
+// Row and log-weight of key j of slice s (segments as in express_keys_kernel).
+// (k, off) is a cursor: segment k starts at key off; a wave's keys increase,
+// so the cursor only moves forward.
+__device__ __forceinline__ int64_t seg_key(const ExpressSegs& segs, int64_t s, int64_t j, int& k,
+                                           int64_t& off, float* lw) {
+  while (k + 1 < segs.n && j >= off + segs.seg[k].len) off += segs.seg[k++].len;
+  const ExpressSeg& g = segs.seg[k];
+  *lw = g.logw;
+  return g.src ? (int64_t)g.src[s * g.stride + (j - off)] : g.start + (j - off);
+}
+
+template <typename T>
+__device__ __forceinline__ void load_elems(const T* p, float* out, int n);
+template <>
+__device__ __forceinline__ void load_elems<float>(const float* p, float* out, int n) {
+  for (int e = 0; e < n; ++e) out[e] = p[e];
+}
+template <>
+__device__ __forceinline__ void load_elems<bf16_t>(const bf16_t* p, float* out, int n) {
+  const uint16_t* q = reinterpret_cast<const uint16_t*>(p);
+  for (int e = 0; e < n; ++e) out[e] = __uint_as_float((uint32_t)q[e] << 16);
+}
+
+template <typename T, int D>
+__global__ __launch_bounds__(64 * kDecWaves) void decode_attn_partial_kernel(
+    const T* __restrict__ Q, const T* __restrict__ K, const T* __restrict__ V, ExpressSegs segs,
+    int64_t ld, int64_t m, int split, float* __restrict__ part) {
+  constexpr int EPL = D >= 64 ? D / 64 : 1;  // elements per lane
+  constexpr int ACT = D / EPL;               // active lanes
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int64_t s = blockIdx.y;
+  const int64_t k0 = m * blockIdx.x / split, k1 = m * (blockIdx.x + 1) / split;
+  const bool act = lane < ACT;
+  const float c2 = (float)(1.4426950408889634 / sqrt((double)D));
+  const float l2e = 1.4426950408889634f;
+  float q[EPL];
+  if (act) load_elems<T>(Q + s * D + lane * EPL, q, EPL);
+  else
+    for (int e = 0; e < EPL; ++e) q[e] = 0.f;
+  const T* Ks = K + s * ld * D;
+  const T* Vs = V + s * ld * D;
+  float mrun = -INFINITY, lrun = 0.f, acc[EPL];
+  for (int e = 0; e < EPL; ++e) acc[e] = 0.f;
+  int kseg = 0;
+  int64_t koff = 0;
+  for (int64_t j0 = k0 + wave; j0 < k1; j0 += kDecWaves * kDecUnroll) {
+    float kv[kDecUnroll][EPL], vv[kDecUnroll][EPL], sc[kDecUnroll];
+#pragma unroll
+    for (int u = 0; u < kDecUnroll; ++u) {
+      const int64_t j = j0 + (int64_t)u * kDecWaves;
+      const bool ok = j < k1;
+      float lw = 0.f;
+      const int64_t r = ok ? seg_key(segs, s, j, kseg, koff, &lw) : 0;
+      sc[u] = ok ? lw * l2e : -INFINITY;
+      if (act && ok) {
+        load_elems<T>(Ks + r * D + lane * EPL, kv[u], EPL);
+        load_elems<T>(Vs + r * D + lane * EPL, vv[u], EPL);
+      } else {
+        for (int e = 0; e < EPL; ++e) kv[u][e] = vv[u][e] = 0.f;
+      }
+    }
+    float mx = mrun;
+#pragma unroll
+    for (int u = 0; u < kDecUnroll; ++u) {
+      float d = 0.f;
+      for (int e = 0; e < EPL; ++e) d = __builtin_fmaf(q[e], kv[u][e], d);
+#pragma unroll
+      for (int off = 32; off >= 1; off >>= 1) d += __shfl_xor(d, off);
+      d = __shfl(d, 0);  // one score for every lane
+      sc[u] = sc[u] == -INFINITY ? -INFINITY : __builtin_fmaf(d, c2, sc[u]);
+      mx = fmaxf(mx, sc[u]);
+    }
+    if (mx == -INFINITY) continue;  // nothing of positive weight yet
+    const float scale = mrun == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(mrun - mx);
+    lrun *= scale;
+    for (int e = 0; e < EPL; ++e) acc[e] *= scale;
+#pragma unroll
+    for (int u = 0; u < kDecUnroll; ++u) {
+      const float p = sc[u] == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(sc[u] - mx);
+      lrun += p;
+      for (int e = 0; e < EPL; ++e) acc[e] = __builtin_fmaf(p, vv[u][e], acc[e]);
+    }
+    mrun = mx;
+  }
+  __shared__ float s_m[kDecWaves], s_l[kDecWaves], s_acc[kDecWaves][D];
+  if (lane == 0) {
+    s_m[wave] = mrun;
+    s_l[wave] = lrun;
+  }
+  if (act)
+    for (int e = 0; e < EPL; ++e) s_acc[wave][lane * EPL + e] = acc[e];
+  __syncthreads();
+  float M = -INFINITY;
+  for (int w = 0; w < kDecWaves; ++w) M = fmaxf(M, s_m[w]);
+  float* out = part + (s * split + blockIdx.x) * (int64_t)(D + 2);
+  for (int c = threadIdx.x; c < D; c += 64 * kDecWaves) {
+    float a = 0.f;
+    for (int w = 0; w < kDecWaves; ++w)
+      if (s_m[w] != -INFINITY) a += s_acc[w][c] * __builtin_amdgcn_exp2f(s_m[w] - M);
+    out[2 + c] = a;
+  }
+  if (threadIdx.x == 0) {
+    float L = 0.f;
+    for (int w = 0; w < kDecWaves; ++w)
+      if (s_m[w] != -INFINITY) L += s_l[w] * __builtin_amdgcn_exp2f(s_m[w] - M);
+    out[0] = M;
+    out[1] = L;
+  }
+}
+
+template <typename TO>
+__device__ __forceinline__ void store_out(TO* p, float v);
+template <>
+__device__ __forceinline__ void store_out<float>(float* p, float v) { *p = v; }
+template <>
+__device__ __forceinline__ void store_out<bf16_t>(bf16_t* p, float v) {
+  *reinterpret_cast<__bf16*>(p) = (__bf16)v;
+}
+
+// One workgroup per slice: the partials' maxima and sums are staged in LDS
+// (one load each), then thread c merges column c of every partial.
+template <int D, typename TO>
+__global__ __launch_bounds__(128) void decode_attn_merge_kernel(const float* __restrict__ part,
+                                                                int split, TO* __restrict__ O) {
+  const int64_t s = blockIdx.x;
+  const float* p = part + s * split * (int64_t)(D + 2);
+  __shared__ float s_w[kDecodeMaxSplit], s_l[kDecodeMaxSplit];
+  __shared__ float s_M;
+  if (threadIdx.x < split) {
+    s_w[threadIdx.x] = p[threadIdx.x * (D + 2)];
+    s_l[threadIdx.x] = p[threadIdx.x * (D + 2) + 1];
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    float M = -INFINITY;
+    for (int k = 0; k < split; ++k) M = fmaxf(M, s_w[k]);
+    s_M = M;
+  }
+  __syncthreads();
+  if (threadIdx.x < split)  // each partial's scale exp2(m_k - M), 0 for an empty one
+    s_w[threadIdx.x] = s_w[threadIdx.x] == -INFINITY ? 0.f
+                                                     : __builtin_amdgcn_exp2f(s_w[threadIdx.x] - s_M);
+  __syncthreads();
+  float L = 0.f;
+  for (int k = 0; k < split; ++k) L = __builtin_fmaf(s_l[k], s_w[k], L);
+  for (int c = threadIdx.x; c < D; c += blockDim.x) {
+    float v[kDecodeMaxSplit];
+#pragma unroll
+    for (int k = 0; k < kDecodeMaxSplit; ++k) v[k] = k < split ? p[k * (D + 2) + 2 + c] : 0.f;
+    float a = 0.f;
+#pragma unroll
+    for (int k = 0; k < kDecodeMaxSplit; ++k) a = __builtin_fmaf(v[k], k < split ? s_w[k] : 0.f, a);
+    store_out<TO>(O + s * D + c, a / L);
+  }
+}
+
+template <typename T, int D, typename TO>
+hipError_t launch_decode_t(const void* Q, const void* K, const void* V, const ExpressSegs& segs,
+                           int64_t S, int64_t ld, int64_t m, int split, float* part, void* O,
+                           hipStream_t st) {
+  hipLaunchKernelGGL((decode_attn_partial_kernel<T, D>), dim3((unsigned)split, (unsigned)S),
+                     dim3(64 * kDecWaves), 0, st, (const T*)Q, (const T*)K, (const T*)V, segs, ld,
+                     m, split, part);
+  hipLaunchKernelGGL((decode_attn_merge_kernel<D, TO>), dim3((unsigned)S), dim3(128), 0, st,
+                     (const float*)part, split, (TO*)O);
+  return hipGetLastError();
+}
+
+template <typename T, typename TO>
+hipError_t launch_decode_d(int64_t d, const void* Q, const void* K, const void* V,
+                           const ExpressSegs& g, int64_t S, int64_t ld, int64_t m, int split,
+                           float* part, void* O, hipStream_t st) {
+  switch (d) {
+    case 32: return launch_decode_t<T, 32, TO>(Q, K, V, g, S, ld, m, split, part, O, st);
+    case 64: return launch_decode_t<T, 64, TO>(Q, K, V, g, S, ld, m, split, part, O, st);
+    case 128: return launch_decode_t<T, 128, TO>(Q, K, V, g, S, ld, m, split, part, O, st);
+    default: return hipErrorInvalidValue;
+  }
+}
+
 }  // namespace
+
+int decode_attention_split(int64_t m) {
+  const int64_t sp = (m + kDecodeKeysPerGroup - 1) / kDecodeKeysPerGroup;
+  return (int)(sp < 1 ? 1 : (sp > kDecodeMaxSplit ? kDecodeMaxSplit : sp));
+}
+
+hipError_t launch_decode_attention(int dtype, int64_t d, int out_dtype, const void* Q,
+                                   const void* K, const void* V, const ExpressSegs& g, int64_t S,
+                                   int64_t ld, int64_t m, float* part, void* O, hipStream_t st) {
+  if (m < 1 || g.n < 1) return hipErrorInvalidValue;
+  const int split = decode_attention_split(m);
+  if (dtype == 0)
+    return out_dtype == 0
+               ? launch_decode_d<float, float>(d, Q, K, V, g, S, ld, m, split, part, O, st)
+               : launch_decode_d<float, bf16_t>(d, Q, K, V, g, S, ld, m, split, part, O, st);
+  return out_dtype == 0
+             ? launch_decode_d<bf16_t, float>(d, Q, K, V, g, S, ld, m, split, part, O, st)
+             : launch_decode_d<bf16_t, bf16_t>(d, Q, K, V, g, S, ld, m, split, part, O, st);
+}
 
 hipError_t launch_rows_iota(int32_t* dst, int64_t dst_stride, int64_t start, int64_t len,
                             int64_t S, hipStream_t st) {

@@ -103,6 +103,18 @@ hipError_t launch_vmax_rows(int dtype, const void* V, int64_t ld, int64_t d, con
 // first m entries of each slice (their lengths sum to m).
 hipError_t launch_express_keys(const ExpressSegs& segs, int64_t S, int64_t m, int64_t out_stride,
                                int32_t* idx, float* logw, hipStream_t st);
+// Weighted attention of one query per slice (Q [S, d], O [S, d]) over the m
+// keys of the segments (rows of K / V, slices ld rows apart): the keys of a
+// slice split over decode_attention_split(m) workgroups, whose partials
+// (S * split * (d + 2) floats in `part`) a second launch merges.
+constexpr int kDecodeKeysPerGroup = 16;
+constexpr int kDecodeMaxSplit = 16;
+int decode_attention_split(int64_t m);
+hipError_t launch_decode_attention(int dtype, int64_t d, int out_dtype, const void* Q,
+                                   const void* K, const void* V, const ExpressSegs& segs,
+                                   int64_t S, int64_t ld, int64_t m, float* part, void* O,
+                                   hipStream_t st);
+
 
 // logw (nullable) [S, n_out]: log-weight of every coreset key.
 hipError_t launch_attention(int dtype, int64_t d, int out_dtype, const void* Q, const void* K,

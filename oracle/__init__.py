@@ -83,10 +83,10 @@ def lib():
         L.or_attention_weighted.argtypes = [P, P, P, C.c_int64, C.c_int64, P, P, C.c_int64, P]
         L.or_attention_weighted.restype = None
         L.or_express_decode.argtypes = [P, P, P, C.c_int64, C.c_int64, C.c_int64, C.c_int,
-                                        C.c_double, C.c_int, P, P, C.c_double, P, P, P, P, P, P,
-                                        C.POINTER(Stats)]
+                                        C.c_double, C.c_int, P, P, P, C.c_double, P, P, P, P, P,
+                                        P, C.POINTER(Stats)]
         L.or_express_decode.restype = C.c_int
-        L.or_express_uniforms.argtypes = [C.c_int64, C.c_int64, C.c_int]
+        L.or_express_uniforms.argtypes = [C.c_int64, C.c_int64, C.c_int, C.POINTER(C.c_int64)]
         L.or_express_uniforms.restype = C.c_int64
         L.or_express_delta.argtypes = [C.c_int, C.c_int, C.c_int, C.c_double]
         L.or_express_delta.restype = C.c_double
@@ -255,11 +255,19 @@ def weighted_attention(Q, K, V, rows, logw) -> np.ndarray:
 
 
 def express_uniforms(n: int, n_out: int, mbar: int) -> int:
-    """Uniforms a Thinformer decode of n points consumes (Halve calls only)."""
-    u = lib().or_express_uniforms(n, n_out, mbar)
+    """Uniforms a Thinformer decode of n points consumes at most (Halve calls)."""
+    u = lib().or_express_uniforms(n, n_out, mbar, None)
     if u < 0:
-        raise ValueError("no Express structure without subsampling for these sizes")
+        raise ValueError("no Express structure for these sizes")
     return u
+
+
+def express_draws(n: int, n_out: int, mbar: int) -> int:
+    """Subsample draws (one per stratum above mbar) a decode of n points needs."""
+    k = C.c_int64(0)
+    if lib().or_express_uniforms(n, n_out, mbar, C.byref(k)) < 0:
+        raise ValueError("no Express structure for these sizes")
+    return k.value
 
 
 def express_delta(m: int, i: int, mbar: int, delta: float = 0.5) -> float:
@@ -269,18 +277,22 @@ def express_delta(m: int, i: int, mbar: int, delta: float = 0.5) -> float:
 
 def express_decode(Q, K, V, n_out: int, mbar: int, U, *, delta: float = 0.5,
                    halve: str = "kh", follow=None, tol: float = 1e-5,
-                   outputs: bool = True) -> dict:
+                   outputs: bool = True, sub_u=None) -> dict:
     """Thinformer decoding of one slice (Alg. 4 over the Express cache of
     Alg. 1): "O" [n, d] (every point attends over the cache of the points
     before it plus itself), then the final weighted cache ("idx", "logw", in
     the order C_0..C_mp, E), the final thinning factor "m", the swap "bits"
-    (indexed like U) and KH "stats"."""
+    (indexed like U) and KH "stats".  sub_u: Subsample's draws, one per
+    stratum above mbar (None: 0 each, the first point of every stratum)."""
     Q, K, V = _f64(Q), _f64(K), _f64(V)
     n, d = K.shape
     U = np.ascontiguousarray(U, dtype=np.float32)
     need = express_uniforms(n, n_out, mbar)
     assert U.size >= need
     fol = None if follow is None else np.ascontiguousarray(follow, dtype=np.uint8)
+    su = None if sub_u is None else np.ascontiguousarray(sub_u, dtype=np.float32)
+    if su is not None:
+        assert su.size >= express_draws(n, n_out, mbar)
     bits = np.zeros(max(need, 1), np.uint8)
     O = np.zeros((n, d)) if outputs else None
     cap = 8 * n_out + 2
@@ -290,7 +302,7 @@ def express_decode(Q, K, V, n_out: int, mbar: int, U, *, delta: float = 0.5,
     mfin = C.c_int(0)
     st = Stats()
     rc = lib().or_express_decode(_p(Q), _p(K), _p(V), n, d, n_out, mbar, delta, HALVES[halve],
-                                 _p(U), _p(fol), tol, _p(bits), _p(O), _p(rows), _p(logw),
+                                 _p(U), _p(su), _p(fol), tol, _p(bits), _p(O), _p(rows), _p(logw),
                                  C.byref(klen), C.byref(mfin), C.byref(st))
     if rc != 0:
         raise ValueError(f"or_express_decode failed ({rc})")

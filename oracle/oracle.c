@@ -378,9 +378,8 @@ void or_attention_weighted(const double* Q, const double* K, const double* V, in
 }
 
 /* ------------------------------------------------------------------ */
-/* Express (Alg. 1) with Compress2 (Alg. 2) and Thinformer decoding   */
-/* (Alg. 4 with WtdAttention, Alg. 5), without subsampling: every     */
-/* thin phase runs at a level m <= mbar, so Subsample keeps all.      */
+/* Express (Alg. 1) with Subsample (Alg. 3) and Compress2 (Alg. 2),  */
+/* and Thinformer decoding (Alg. 4 with WtdAttention, Alg. 5).        */
 /* ------------------------------------------------------------------ */
 #define EX_MAXL 32
 
@@ -405,8 +404,11 @@ typedef struct {
   int32_t* C[EX_MAXL + 1];
   int64_t nC[EX_MAXL + 1];
   int32_t* tmp;
-  int over;          /* a level above mbar was reached */
+  int over;          /* a Compress2 group size is not an even integer >= 2 */
   int count_only;    /* only count the uniforms the Halve calls consume */
+  const float* sub_u; /* Subsample draws, one per stratum (NULL: 0 each) */
+  int64_t sub_pos;   /* draws used */
+  int64_t sub_n, sub_i; /* Subsample: points seen since its reset, the kept one */
 } ex_t;
 
 /* Cor. 2: delta_m, the budget of level m, and delta_{m,i}. */
@@ -457,9 +459,25 @@ static int ex_compress2_update(ex_t* x, int32_t p) {
   return 0;
 }
 
+/* Subsample(m, mbar).keep (Alg. 3): above mbar one point of each stratum of
+ * 2^(m - mbar) points, at offset floor(u R) from the stratum's start. */
+static int ex_keep(ex_t* x) {
+  x->sub_n += 1;
+  if (x->m <= x->mbar) return 1;
+  const int64_t R = (int64_t)1 << (x->m - x->mbar);
+  if ((x->sub_n - 1) % R == 0) {
+    const double u = x->sub_u ? (double)x->sub_u[x->sub_pos] : 0.0;
+    x->sub_pos += 1;
+    int64_t off = (int64_t)floor(u * (double)R);
+    if (off > R - 1) off = R - 1;
+    x->sub_i = x->sub_n + off;
+  }
+  return x->sub_n == x->sub_i;
+}
+
 static void ex_reset_c(ex_t* x) {
   x->mp = x->m < x->mbar ? x->m : x->mbar;
-  if (x->m > x->mbar) x->over = 1;
+  x->sub_n = 0;
   /* Compress2's smallest groups, 4 n_out / 2^mp points, must be even and >= 2 */
   if (x->mp >= 1 && ((4 * x->n_out) % ((int64_t)1 << x->mp) != 0 ||
                      ((4 * x->n_out) >> x->mp) < 2 || (((4 * x->n_out) >> x->mp) & 1)))
@@ -474,9 +492,9 @@ static int ex_update(ex_t* x, int32_t p) {
     x->E[x->nE++] = p;
     return 0;
   }
-  if (x->over) return -1; /* would need Subsample with m > mbar */
+  if (x->over) return -1;
   x->ell += 1;
-  int rc = ex_compress2_update(x, p);
+  int rc = ex_keep(x) ? ex_compress2_update(x, p) : 0;
   if (rc) return rc;
   if (x->ell == (x->n_out << x->m)) {
     memcpy(x->E + x->nE, x->C[x->mp], sizeof(int32_t) * (size_t)x->nC[x->mp]);
@@ -516,12 +534,13 @@ static int ex_run(ex_t* x, const double* Q, int64_t n, double* O, int32_t* rows,
 
 int or_express_decode(const double* Q, const double* K, const double* V, int64_t n, int64_t d,
                       int64_t n_out, int mbar, double delta, int halve, const float* U,
-                      const uint8_t* follow, double tol, uint8_t* bits, double* O,
-                      int32_t* cache_rows, double* cache_logw, int64_t* cache_len,
+                      const float* sub_u, const uint8_t* follow, double tol, uint8_t* bits,
+                      double* O, int32_t* cache_rows, double* cache_logw, int64_t* cache_len,
                       int* m_final, or_stats_t* st) {
   if (n < 0 || n_out < 1 || d < 1 || mbar < 0 || mbar > EX_MAXL - 2) return -1;
   ex_t x;
   memset(&x, 0, sizeof(x));
+  x.sub_u = sub_u;
   x.K = K; x.V = V; x.d = d; x.n_out = n_out; x.mbar = mbar; x.delta = delta;
   x.halve = halve; x.U = U; x.follow = follow; x.tol = tol; x.bits = bits; x.st = st;
   const int64_t capE = 4 * n_out, capW = 8 * n_out + 2;
@@ -566,7 +585,9 @@ static int ex_run(ex_t* x, const double* Q, int64_t n, double* O, int32_t* rows,
   return rc;
 }
 
-int64_t or_express_uniforms(int64_t n, int64_t n_out, int mbar) {
+/* Uniforms (upper bound: every stratum keeps its first point, so every Halve
+ * call happens as early as it can) and Subsample draws of n points. */
+int64_t or_express_uniforms(int64_t n, int64_t n_out, int mbar, int64_t* draws) {
   if (n < 0 || n_out < 1 || mbar < 0 || mbar > EX_MAXL - 2) return -1;
   ex_t x;
   memset(&x, 0, sizeof(x));
@@ -582,5 +603,6 @@ int64_t or_express_uniforms(int64_t n, int64_t n_out, int mbar) {
   for (int i = 0; i <= EX_MAXL; ++i) free(x.C[i]);
   free(x.E);
   free(x.tmp);
+  if (draws) *draws = x.sub_pos;
   return rc == 0 ? x.upos : -1;
 }

@@ -104,20 +104,23 @@ void or_attention(const double* Q, const double* K, const double* V, int64_t n_q
  * point p.  Halve_{m,i} = KH(delta_{m,i}) and Halve_{m,m} = KH(delta_m / 2)
  * (Cor. 2) under kappa_att with v_max over the rows of each call (halve =
  * OR_HALVE_UNIFORM: uniform halving instead).  Every Halve call of N points
- * consumes the next N/2 uniforms of U (follow/bits indexed alike).  Only
- * levels m <= mbar are supported (no subsampling): returns -1 once a point
- * would need a thin phase at m > mbar.  O (nullable) [n, d]; the final cache
+ * consumes the next N/2 uniforms of U (follow/bits indexed alike).  Above
+ * mbar, Subsample (Alg. 3) keeps the point at offset floor(u R) of every
+ * stratum of R = 2^(m - mbar) points, u = sub_u[k] for the k-th stratum
+ * (sub_u NULL: u = 0).  Returns -1 if a Compress2 group size 4 n_out / 2^mp
+ * is not an even integer >= 2.  O (nullable) [n, d]; the final cache
  * (C_0..C_mp with log-weights (i - mp) log 2, then E with 0) goes to
  * cache_rows / cache_logw (capacity 8 n_out + 2), its size to cache_len and
  * the final thinning factor m to m_final.
  */
 int or_express_decode(const double* Q, const double* K, const double* V, int64_t n, int64_t d,
                       int64_t n_out, int mbar, double delta, int halve, const float* U,
-                      const uint8_t* follow, double tol, uint8_t* bits, double* O,
-                      int32_t* cache_rows, double* cache_logw, int64_t* cache_len,
+                      const float* sub_u, const uint8_t* follow, double tol, uint8_t* bits,
+                      double* O, int32_t* cache_rows, double* cache_logw, int64_t* cache_len,
                       int* m_final, or_stats_t* st);
-/* Uniforms a decode of n points consumes (or -1). */
-int64_t or_express_uniforms(int64_t n, int64_t n_out, int mbar);
+/* Uniforms a decode of n points consumes at most (or -1); *draws (nullable)
+ * the Subsample draws it needs. */
+int64_t or_express_uniforms(int64_t n, int64_t n_out, int mbar, int64_t* draws);
 /* Cor. 2: delta_{m,i} (i >= 0) or delta_m / 2 (i < 0, the Halve phase). */
 double or_express_delta(int m, int i, int mbar, double delta);
 

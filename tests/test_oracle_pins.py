@@ -573,7 +573,8 @@ def test_thinformer_is_exact_for_the_first_four_n_out_points():
 @pytest.mark.parametrize("n", [1, 7, 8, 9, 31, 33, 100, 128, 129, 200, 511, 512])
 def test_express_cache_weights_count_every_point(n):
     """A cache point of C_i stands for 2^i points and one of E for 2^m, so
-    2^m * sum of the weights is the number of points seen."""
+    2^m * sum of the weights is the number of points seen (no subsampling
+    up to 512 points at mbar = 4)."""
     n_out, mbar, d = 8, 4, 4
     Q, K, V = _express_inputs(n, d, 32)
     U = np.random.default_rng(33).random(max(oracle.express_uniforms(n, n_out, mbar), 1))
@@ -597,30 +598,48 @@ def _offline_compress2(m, rows):
         [_keep_first(rows[k * size:(k + 1) * size]) for k in range(g)]))
 
 
-def _offline_express(n_out, mbar, rows, m):
-    """Offline-Express (App. F, the recursive procedure) on 2^(m+2) n_out points."""
+def _offline_subsample(m, mbar, rows, draws):
+    """Offline Subsample: one point of every 2^(m - mbar), at offset floor(u R)."""
+    if m <= mbar:
+        return rows
+    R = 2 ** (m - mbar)
+    return np.array([rows[k + min(R - 1, int(np.floor(next(draws) * R)))]
+                     for k in range(0, rows.size, R)], dtype=rows.dtype)
+
+
+def _offline_express(n_out, mbar, rows, m, draws):
+    """Offline-Express (App. F, the recursive procedure) on 2^(m+2) n_out points;
+    the draws are taken in the order the recursion meets the strata."""
     if rows.size <= n_out:
         return rows
     q = rows.size // 4
-    parts = [_offline_express(n_out, mbar, rows[:q], m - 2)]
+    parts = [_offline_express(n_out, mbar, rows[:q], m - 2, draws)]
     for j in (1, 2, 3):
-        assert m <= mbar  # Subsample keeps every point
-        parts.append(_offline_compress2(min(m, mbar), rows[j * q:(j + 1) * q]))
+        kept = _offline_subsample(m, mbar, rows[j * q:(j + 1) * q], draws)
+        parts.append(_offline_compress2(min(m, mbar), kept))
     return _keep_first(_keep_first(np.concatenate(parts)))
 
 
-@pytest.mark.parametrize("n_out,mbar,levels", [(4, 2, 2), (8, 4, 3), (16, 6, 3), (16, 4, 2)])
+@pytest.mark.parametrize("n_out,mbar,levels", [(4, 2, 2), (8, 4, 3), (16, 6, 3), (16, 4, 2),
+                                               (4, 2, 3), (8, 2, 4), (16, 3, 4)])
 def test_streaming_express_equals_offline_express(n_out, mbar, levels):
     """The streaming procedure equals the recursive offline one (App. F);
     with a deterministic Halve (uniform halving with every u >= 1/2 keeps
-    the first point of each pair) both must return the same coreset."""
+    the first point of each pair) and the same Subsample draws (levels above
+    mbar) both must return the same coreset."""
     m = 2 * levels - 2
     n = n_out * 2 ** (m + 2)
     Q, K, V = _express_inputs(n, 2, 34)
     U = np.full(max(oracle.express_uniforms(n, n_out, mbar), 1), 0.75, np.float32)
-    r = oracle.express_decode(Q, K, V, n_out, mbar, U, halve="uniform", outputs=False)
-    want = _offline_express(n_out, mbar, np.arange(n, dtype=np.int32), m)
+    nd = oracle.express_draws(n, n_out, mbar)
+    draws = (np.random.default_rng(35).integers(0, 1 << 24, max(nd, 1)) * 2.0 ** -24)
+    draws = draws.astype(np.float32)
+    r = oracle.express_decode(Q, K, V, n_out, mbar, U, halve="uniform", outputs=False,
+                              sub_u=draws)
+    want = _offline_express(n_out, mbar, np.arange(n, dtype=np.int32), m,
+                            iter(draws.astype(np.float64)))
     assert r["m"] == m + 2 and np.array_equal(r["idx"], want)
+    assert (m <= mbar) == (nd == 0)
 
 
 def test_cor2_delta_schedule_meets_the_union_bound():
@@ -642,3 +661,20 @@ def test_cor2_delta_schedule_meets_the_union_bound():
     K = 19
     assert tot == pytest.approx(delta / 2 * (1 - 1 / math.log2(K + 3)), rel=1e-12)
     assert tot < delta / 2
+
+
+def test_express_subsample_cache_weights_count_whole_strata():
+    """Above mbar a kept point stands for its stratum of 2^(m - mbar) points:
+    at the end of every level (all strata complete) 2^m * the weight sum
+    counts every point, and the cache stays within 6 n_out."""
+    n_out, mbar, d = 8, 2, 4
+    for levels in (3, 4):
+        n = n_out * 4 ** levels
+        Q, K, V = _express_inputs(n, d, 36)
+        U = np.random.default_rng(37).random(oracle.express_uniforms(n, n_out, mbar))
+        nd = oracle.express_draws(n, n_out, mbar)
+        draws = np.random.default_rng(38).random(nd).astype(np.float32)
+        r = oracle.express_decode(Q, K, V, n_out, mbar, U.astype(np.float32), outputs=False,
+                                  sub_u=draws)
+        assert np.exp(r["logw"]).sum() * 2.0 ** r["m"] == pytest.approx(n, rel=1e-12)
+        assert r["idx"].size == n_out and np.unique(r["idx"]).size == n_out

@@ -16,9 +16,10 @@ exactly, the rows between them are thinned to n_out, and attention runs over
 the S + n_out + W weighted keys (eq. def:att_approx).
 
 --mode decode measures Thinformer decoding over the Express cache instead
-(Alg. 4): B=1, H=32 slices, d=128, bf16, n_out=128, mbar=8, 16384 points
-decoded one at a time (each attends over the cache plus itself, then enters
-it); one step = one point of every slice.
+(Alg. 4): B=1, H=32 slices, d=128, bf16, n_out=128, mbar=5 (log2 n_out - 2,
+the decoding experiments' choice: Subsample runs from point 8192 on), 16384
+points decoded one at a time (each attends over the cache plus itself, then
+enters it); one step = one point of every slice.
 """
 import argparse
 import collections
@@ -184,7 +185,7 @@ def cpu_baseline(w, Q, K, V, U, plan, budget_s: float = 20.0, halve: str = "kh",
                       f"{t_used:.1f} s"}
 
 
-DECODE = dict(B=1, H=32, d=128, dtype="bf16", n_out=128, mbar=8, n=16384)
+DECODE = dict(B=1, H=32, d=128, dtype="bf16", n_out=128, mbar=5, n=16384)
 
 
 def decode_main(args):
@@ -200,6 +201,9 @@ def decode_main(args):
     Q, K, V = W.make_qkv(w)
     plan = thin_express_plan(w.B, w.H, w.d, c["n_out"], c["mbar"], w.n)
     U = W.make_uniforms(w, w.S * plan["uniforms_per_slice"])
+    # Subsample's draws (host, shared by the slices), from their own seeded stream
+    draws = torch.from_numpy(np.random.default_rng(w.seed + 1).random(
+        max(plan["subsample_draws"], 1)).astype(np.float32))
     dev = torch.device("cuda:0")
     Qd, Kd, Vd, Ud = Q.to(dev), K.to(dev), V.to(dev), U.to(dev)
     Qt = [Qd[:, :, t].contiguous() for t in range(w.n)]
@@ -211,7 +215,7 @@ def decode_main(args):
         for t in range(n_steps):
             if keys is not None:
                 keys.append(ex.next_keys())
-            ex.step(Qt[t], Kd, Vd, Ud, O=O, stream=stream)
+            ex.step(Qt[t], Kd, Vd, Ud, draws=draws, O=O, stream=stream)
         return ex
 
     for _ in range(max(args.warmup // 50, 1)):
@@ -230,12 +234,12 @@ def decode_main(args):
     ex = ExpressCache(w.B, w.H, w.d, c["n_out"], c["mbar"], w.n, dtype=torch.bfloat16)
     tail = 2048
     for t in range(w.n - tail):
-        ex.step(Qt[t], Kd, Vd, Ud, O=O, stream=stream)
+        ex.step(Qt[t], Kd, Vd, Ud, draws=draws, O=O, stream=stream)
     torch.cuda.synchronize()
     with LaunchTimer(stream, capacity=16 * tail) as lt:
         for t in range(w.n - tail, w.n):
             keys.append(ex.next_keys())
-            ex.step(Qt[t], Kd, Vd, Ud, O=O, stream=stream)
+            ex.step(Qt[t], Kd, Vd, Ud, draws=draws, O=O, stream=stream)
         torch.cuda.synchronize()
     ex.close()
     rec = lt.records()
@@ -274,7 +278,8 @@ def decode_main(args):
         t_used, done = 0.0, 0
         for s in range(w.S):
             t_a = time.perf_counter()
-            oracle.express_decode(Q[0, s], K[0, s], V[0, s], c["n_out"], c["mbar"], Us[s])
+            oracle.express_decode(Q[0, s], K[0, s], V[0, s], c["n_out"], c["mbar"], Us[s],
+                                  sub_u=draws.numpy())
             t_used += time.perf_counter() - t_a
             done += 1
             if t_used >= 20.0:

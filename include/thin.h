@@ -223,17 +223,22 @@ int thin_attention_ex(const void* Q, const void* K, const void* V, int32_t dtype
  * KH(delta_m / 2) with Cor. 2's schedule for the given delta, under
  * kappa_att with v_max over the rows of each call (or uniform halving).
  * Every Halve call of N points consumes the next N/2 uniforms of each slice.
- * Supported: the thin phases at levels m <= mbar only, where Subsample keeps
- * every point, i.e. n_max <= n_out * 2^(M+2) with M the largest even number
- * <= mbar; every Compress2 group size 4 n_out / 2^m (2 <= m <= M) an even
- * integer >= 2; 4 n_out <= 8192.
+ * Above mbar, Subsample (Alg. 3) keeps the point at offset floor(u R) of each
+ * stratum of R = 2^(m - mbar) points, u the stratum's draw; the draws are
+ * host memory, one per stratum in order, shared by all slices (the slices
+ * run in lockstep, so they keep the same positions).
+ * Supported: every Compress2 group size 4 n_out / 2^mp (1 <= mp <= mbar, as
+ * reached by n_max points) an even integer >= 2; 4 n_out <= 8192.
  */
 typedef struct thin_express thin_express_t;
 
 typedef struct {
-  int64_t uniforms_per_slice; /* uniforms the Halve calls of n_max points consume */
+  int64_t uniforms_per_slice; /* uniforms the Halve calls of n_max points consume
+                                 at most (every Halve call as early as the
+                                 draws allow)                                    */
   int64_t max_keys;           /* largest key list of one attention call           */
   size_t workspace_bytes;     /* device workspace of thin_express_create          */
+  int64_t subsample_draws;    /* Subsample draws n_max points need                */
 } thin_express_plan_t;
 
 /* Host-only.  THIN_EINVAL for unsupported sizes (see above). */
@@ -257,15 +262,19 @@ int thin_express_create(int32_t dtype, int64_t B, int64_t H, int64_t d, int64_t 
  *             (row t written before the call).
  *   uniforms  (device) float32 [B*H, plan.uniforms_per_slice], n_uniforms
  *             its size (nullable when the plan needs none).
+ *   draws     (host) float32 [n_draws] Subsample draws, read only at the
+ *             first point of a stratum (nullable when the plan needs none).
  *   O         (device) [B,H,d] of out_dtype: the point's output.
  *   swap_trace (device, nullable) uint8 indexed like uniforms.
  * Enqueued on `stream`; calls on one object must be stream-ordered.
- * Errors: THIN_EINVAL (null arguments, t = n_max, or a point beyond the
- * supported levels), THIN_EDTYPE, THIN_EUNIFORMS, THIN_EHIP.
+ * Errors: THIN_EINVAL (null arguments, t = n_max, a missing draw, or a
+ * point beyond the supported levels), THIN_EDTYPE, THIN_EUNIFORMS,
+ * THIN_EHIP; nothing is enqueued or changed on an error found before launch.
  */
 int thin_express_step(thin_express_t* x, const void* Q, const void* K, const void* V,
-                      const float* uniforms, int64_t n_uniforms, void* O, int32_t out_dtype,
-                      uint8_t* swap_trace, void* stream);
+                      const float* uniforms, int64_t n_uniforms, const float* draws,
+                      int64_t n_draws, void* O, int32_t out_dtype, uint8_t* swap_trace,
+                      void* stream);
 
 /*
  * The current weighted cache: idx (device) int32 and logw (device) float32,
@@ -298,7 +307,8 @@ const char* thin_status_str(int status);
 /*
  * Launch observer, for tracing and per-kernel timing.  While a hook is set,
  * every kernel launch made by thin_compress, thin_compress_traced,
- * thin_compress_ex, thin_attention, thin_attention_ex and thin_express_step is bracketed by two calls on the
+ * thin_compress_ex, thin_attention, thin_attention_ex and thin_express_step
+ * is bracketed by two calls on the
  * calling thread:
  * hook(ctx, kernel, round, 0, stream) right before the launch is enqueued and
  * hook(ctx, kernel, round, 1, stream) right after.  The hook may enqueue

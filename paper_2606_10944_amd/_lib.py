@@ -43,7 +43,7 @@ class ThinError(RuntimeError):
 
 class ExpressPlan(C.Structure):
     _fields_ = [("uniforms_per_slice", C.c_int64), ("max_keys", C.c_int64),
-                ("workspace_bytes", C.c_size_t)]
+                ("workspace_bytes", C.c_size_t), ("subsample_draws", C.c_int64)]
 
 
 class CompressOpts(C.Structure):
@@ -86,7 +86,7 @@ def lib():
     L.thin_express_plan.argtypes = [I64, I64, I64, I64, I32, I64, C.POINTER(ExpressPlan)]
     L.thin_express_create.argtypes = [I32, I64, I64, I64, I64, I32, C.c_double, I32, I64, P, SZ,
                                       C.POINTER(C.c_void_p)]
-    L.thin_express_step.argtypes = [P, P, P, P, P, I64, P, I32, P, P]
+    L.thin_express_step.argtypes = [P, P, P, P, P, I64, P, I64, P, I32, P, P]
     L.thin_express_cache.argtypes = [P, P, P, C.POINTER(C.c_int64), C.POINTER(C.c_int32), P]
     L.thin_express_next.argtypes = [P, C.POINTER(C.c_int64), C.POINTER(C.c_int64)]
     L.thin_express_destroy.argtypes = [P]
@@ -256,7 +256,9 @@ class ExpressCache:
     """Thinformer decoding over an Express cache for B*H slices in lockstep
     (thin_express_*): ``step(Q_t, K, V, U)`` attends point t = ``self.n``
     (query Q_t [B,H,d]; K, V [B,H,n_max,d] caches holding rows 0..t) over the
-    cache plus itself and then adds it to the cache."""
+    cache plus itself and then adds it to the cache.  ``draws`` (host float32
+    array of plan["subsample_draws"] values, one per Subsample stratum, shared
+    by all slices) is needed once a level above mbar is reached."""
 
     def __init__(self, B: int, H: int, d: int, n_out: int, mbar: int, n_max: int, *,
                  dtype: torch.dtype = torch.bfloat16, delta: float = 0.5, halve: str = "kh",
@@ -276,8 +278,9 @@ class ExpressCache:
         self.n = 0
 
     def step(self, Q_t: torch.Tensor, K: torch.Tensor, V: torch.Tensor, uniforms, *,
-             O: Optional[torch.Tensor] = None, out_dtype: torch.dtype = torch.float32,
-             trace: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+             draws=None, O: Optional[torch.Tensor] = None,
+             out_dtype: torch.dtype = torch.float32, trace: Optional[torch.Tensor] = None,
+             stream=None) -> torch.Tensor:
         B, H, d = self.B, self.H, self.d
         if tuple(Q_t.shape) != (B, H, d) or not Q_t.is_contiguous() or Q_t.dtype != self.dtype:
             raise ThinError(THIN_EINVAL, "Q_t must be contiguous [B,H,d] of the cache's dtype")
@@ -293,8 +296,13 @@ class ExpressCache:
         elif tuple(O.shape) != (B, H, d) or not O.is_contiguous():
             raise ThinError(THIN_EINVAL, "O must be contiguous [B,H,d]")
         nU = 0 if uniforms is None else uniforms.numel()
+        if draws is not None and (not isinstance(draws, torch.Tensor) or draws.is_cuda
+                                  or draws.dtype != torch.float32 or not draws.is_contiguous()):
+            raise ThinError(THIN_EINVAL, "draws must be a contiguous float32 CPU tensor")
+        nD = 0 if draws is None else draws.numel()
         rc = lib().thin_express_step(self._h, _ptr(Q_t), _ptr(K), _ptr(V),
-                                     None if uniforms is None else _ptr(uniforms), nU, _ptr(O),
+                                     None if uniforms is None else _ptr(uniforms), nU,
+                                     None if draws is None else _ptr(draws), nD, _ptr(O),
                                      _dtype_code(O.dtype), None if trace is None else _ptr(trace),
                                      _stream(stream))
         _check(rc, "thin_express_step")

@@ -293,11 +293,11 @@ int compress_impl(const void* K, const void* V, int32_t dtype, int64_t B, int64_
 
 
 // ---------------------------------------------------------------------------
-// Express cache (Alg. 1 with Compress2 of Alg. 2) and Thinformer decoding
-// (Alg. 4, WtdAttention of Alg. 5), without subsampling.  The counters run on
-// the host (they depend on the point count only); the index lists live in
-// the caller's workspace and every Halve call is one KH round of a single
-// bucket per slice.  C_0 is always the run of points c0_start .. t-1.
+// Express cache (Alg. 1 with Subsample of Alg. 3 and Compress2 of Alg. 2) and
+// Thinformer decoding (Alg. 4, WtdAttention of Alg. 5).  The counters run on
+// the host (they depend on the point count and the Subsample draws only); the
+// index lists live in the caller's workspace and every Halve call is one KH
+// round of a single bucket per slice.
 // ---------------------------------------------------------------------------
 constexpr int kExMaxL = 30;
 
@@ -310,7 +310,7 @@ double express_delta(int m, int i, int mbar, double delta) {
 }
 
 struct ExLayout {
-  size_t vmax, E, C[kExMaxL + 1], iota, t1, t2, part, lbt, h2, rowh2, score;
+  size_t vmax, E, C[kExMaxL + 1], t1, t2, part, lbt, h2, rowh2, score;
   size_t e_bytes, bytes;
 };
 
@@ -326,8 +326,7 @@ ExLayout ex_layout(int64_t S, int64_t d, int64_t n_out, int32_t mbar, int64_t n_
   const size_t s4 = (size_t)S * 4;
   L.vmax = take(s4);
   L.E = take(s4 * 4 * n_out);  // up to 4 n_out before the Halve phase
-  for (int i = 1; i <= mbar; ++i) L.C[i] = take(s4 * 2 * n_out);
-  L.iota = take(s4 * 2 * n_out);
+  for (int i = 0; i <= mbar; ++i) L.C[i] = take(s4 * 2 * n_out);
   L.t1 = take(s4 * 2 * n_out);
   L.t2 = take(s4 * n_out);
   (void)kmax;
@@ -351,10 +350,11 @@ struct thin_express {
   double delta;
   unsigned char* ws;
   ExLayout L;
-  // Alg. 1 / 2 counters
+  // Alg. 1 / 2 / 3 counters
   int32_t m, mp;
-  int64_t n, ell, nE, c0_start, upos;
+  int64_t n, ell, nE, upos;
   int64_t nC[kExMaxL + 1];
+  int64_t sub_n, sub_i, sub_pos;  // Subsample: points since its reset, the kept one, draws used
   bool over;
 };
 
@@ -372,12 +372,33 @@ int64_t ex_stride(const thin_express* x, int i) {
 
 void ex_reset(thin_express* x) {
   x->mp = x->m < x->mbar ? x->m : x->mbar;
-  if (x->m > x->mbar) x->over = true;  // the next thin phase would need Subsample
-  const int64_t t0 = 4 * x->n_out;
+  const int64_t t0 = 4 * x->n_out;  // Compress2's smallest groups: 4 n_out / 2^mp points
   if (x->mp >= 1 && (t0 % ((int64_t)1 << x->mp) != 0 || (t0 >> x->mp) < 2 || ((t0 >> x->mp) & 1)))
     x->over = true;
   for (int i = 0; i <= kExMaxL; ++i) x->nC[i] = 0;
-  x->c0_start = x->n;
+  x->sub_n = 0;
+}
+
+// Subsample(m, mbar) needs a draw for the next point (a stratum starts).
+bool ex_needs_draw(const thin_express* x) {
+  return x->m > x->mbar && (x->sub_n % ((int64_t)1 << (x->m - x->mbar))) == 0;
+}
+
+// Subsample(m, mbar).keep for the next point (Alg. 3): above mbar one point
+// of every stratum of R = 2^(m - mbar), at offset floor(u R) of its start
+// (draws null: u = 0).
+bool ex_keep(thin_express* x, const float* draws) {
+  x->sub_n += 1;
+  if (x->m <= x->mbar) return true;
+  const int64_t R = (int64_t)1 << (x->m - x->mbar);
+  if ((x->sub_n - 1) % R == 0) {
+    const double u = draws ? (double)draws[x->sub_pos] : 0.0;
+    x->sub_pos += 1;
+    int64_t off = (int64_t)floor(u * (double)R);
+    if (off > R - 1) off = R - 1;
+    x->sub_i = x->sub_n + off;
+  }
+  return x->sub_n == x->sub_i;
 }
 
 // Device side of one update (null: count only).
@@ -431,14 +452,6 @@ hipError_t ex_halve(thin_express* x, const ExRun* run, const int32_t* in, int64_
   return kh_round(x->dtype, x->d, a, x->S, x->L.e_bytes, -1, st);
 }
 
-hipError_t ex_iota(const thin_express* x, const ExRun* run, int32_t* dst, int64_t stride,
-                   int64_t start, int64_t len) {
-  if (!run) return hipSuccess;
-  return observed(THIN_KERNEL_EXPRESS, -1, run->st, [&] {
-    return thin::launch_rows_iota(dst, stride, start, len, x->S, run->st);
-  });
-}
-
 hipError_t ex_copy(const thin_express* x, const ExRun* run, const int32_t* src, int64_t sstride,
                    int32_t* dst, int64_t dstride, int64_t len) {
   if (!run) return hipSuccess;
@@ -448,46 +461,34 @@ hipError_t ex_copy(const thin_express* x, const ExRun* run, const int32_t* src, 
 }
 
 // Express.update with the next point (Alg. 1), Compress2.update inside (Alg. 2).
-hipError_t ex_update(thin_express* x, const ExRun* run) {
-  const int64_t p = x->n;  // the point's position
+// The point itself was already appended, to E (exact phase) or, if Subsample
+// keeps it (`keep`), to C_0, by the step's attention launch.
+hipError_t ex_update(thin_express* x, const ExRun* run, bool keep) {
   int32_t* E = ex_ptr<int32_t>(x, x->L.E);
   const int64_t sE = 4 * x->n_out;
   hipError_t e = hipSuccess;
   x->n += 1;
   if (x->n <= x->n_out) {  // exact phase
-    e = ex_iota(x, run, E + x->nE, sE, p, 1);
     x->nE += 1;
-    x->c0_start = x->n;
     return e;
   }
   x->ell += 1;
-  x->nC[0] += 1;  // C_0 = points c0_start .. p
+  if (keep) x->nC[0] += 1;
   int32_t* t1 = ex_ptr<int32_t>(x, x->L.t1);
-  for (int i = 0; i < x->mp && e == hipSuccess; ++i) {
+  for (int i = 0; keep && i < x->mp && e == hipSuccess; ++i) {
     const int64_t T = (x->n_out << (i + 2)) >> x->mp;
     if (x->nC[i] != T) continue;
-    const int32_t* in;
-    if (i == 0) {
-      int32_t* io = ex_ptr<int32_t>(x, x->L.iota);
-      e = ex_iota(x, run, io, T, x->c0_start, T);
-      in = io;
-    } else {
-      in = ex_ptr<int32_t>(x, x->L.C[i]);
-    }
-    if (e == hipSuccess) e = ex_halve(x, run, in, T, express_delta(x->m, i, x->mbar, x->delta), t1);
+    const int32_t* in = ex_ptr<int32_t>(x, x->L.C[i]);
+    e = ex_halve(x, run, in, T, express_delta(x->m, i, x->mbar, x->delta), t1);
     if (e == hipSuccess)
       e = ex_copy(x, run, t1, T / 2, ex_ptr<int32_t>(x, x->L.C[i + 1]) + x->nC[i + 1],
                   ex_stride(x, i + 1), T / 2);
     x->nC[i + 1] += T / 2;
     x->nC[i] = 0;
-    if (i == 0) x->c0_start = x->n;
   }
   if (e == hipSuccess && x->ell == (x->n_out << x->m)) {  // E gets the group's coreset
-    if (x->mp == 0)
-      e = ex_iota(x, run, E + x->nE, sE, x->c0_start, x->nC[0]);
-    else
-      e = ex_copy(x, run, ex_ptr<int32_t>(x, x->L.C[x->mp]), ex_stride(x, x->mp), E + x->nE, sE,
-                  x->nC[x->mp]);
+    e = ex_copy(x, run, ex_ptr<int32_t>(x, x->L.C[x->mp]), ex_stride(x, x->mp), E + x->nE, sE,
+                x->nC[x->mp]);
     x->nE += x->nC[x->mp];
     x->ell = 0;
   }
@@ -504,12 +505,14 @@ hipError_t ex_update(thin_express* x, const ExRun* run) {
   return e;
 }
 
-// Segments of the weighted cache: C_0 (points c0_start.. c0_start+len0-1),
-// C_1..C_mp, E.
-thin::ExpressSegs ex_segs(const thin_express* x, int64_t len0) {
+// Segments of the weighted cache: C_0, then (self) the point t joining C_0
+// with its weight, C_1..C_mp, E.
+thin::ExpressSegs ex_segs(const thin_express* x, bool self) {
   thin::ExpressSegs g{};
   const float ln2 = (float)log(2.0);
-  g.seg[g.n++] = {nullptr, 0, x->c0_start, len0, -(float)x->mp * ln2};
+  g.seg[g.n++] = {ex_ptr<int32_t>(x, x->L.C[0]), ex_stride(x, 0), 0, x->nC[0],
+                  -(float)x->mp * ln2};
+  if (self) g.seg[g.n++] = {nullptr, 0, x->n, 1, -(float)x->mp * ln2};
   for (int i = 1; i <= x->mp; ++i)
     if (x->nC[i] > 0)
       g.seg[g.n++] = {ex_ptr<int32_t>(x, x->L.C[i]), ex_stride(x, i), 0, x->nC[i],
@@ -527,7 +530,7 @@ int64_t seg_total(const thin::ExpressSegs& g) {
 // Size checks shared by plan and create; counts uniforms and the largest key
 // list over n_max points.
 int ex_check(int64_t B, int64_t H, int64_t d, int64_t n_out, int32_t mbar, int64_t n_max,
-             int64_t* u_slice, int64_t* kmax) {
+             int64_t* u_slice, int64_t* kmax, int64_t* draws) {
   if (B < 1 || H < 1 || B * H > kMaxSlices || !supported_d(d)) return THIN_EINVAL;
   if (n_out < 1 || 4 * n_out > kMaxBucket || mbar < 0 || mbar > kExMaxL - 2) return THIN_EINVAL;
   if (n_max < 1 || n_max > kMaxRows) return THIN_EINVAL;
@@ -536,15 +539,19 @@ int ex_check(int64_t B, int64_t H, int64_t d, int64_t n_out, int32_t mbar, int64
   x.mbar = mbar;
   x.delta = 0.5;
   ex_reset(&x);
+  // every stratum keeps its first point (draws of 0): each Halve call comes
+  // as early as it can, so the uniforms counted bound those of any draws
   int64_t km = 1;
   for (int64_t t = 0; t < n_max; ++t) {
     if (x.n >= n_out && x.over) return THIN_EINVAL;
-    const int64_t k = seg_total(ex_segs(&x, t - x.c0_start + 1));
+    const int64_t k = seg_total(ex_segs(&x, true));
     if (k > km) km = k;
-    ex_update(&x, nullptr);
+    const bool keep = x.n >= n_out ? ex_keep(&x, nullptr) : true;
+    ex_update(&x, nullptr, keep);
   }
   *u_slice = x.upos;
   *kmax = km;
+  *draws = x.sub_pos;
   return THIN_OK;
 }
 }  // namespace
@@ -659,11 +666,12 @@ extern "C" {
 int thin_express_plan(int64_t B, int64_t H, int64_t d, int64_t n_out, int32_t mbar,
                       int64_t n_max, thin_express_plan_t* plan) {
   if (!plan) return THIN_EINVAL;
-  int64_t u = 0, k = 0;
-  const int rc = ex_check(B, H, d, n_out, mbar, n_max, &u, &k);
+  int64_t u = 0, k = 0, dr = 0;
+  const int rc = ex_check(B, H, d, n_out, mbar, n_max, &u, &k, &dr);
   if (rc) return rc;
   plan->uniforms_per_slice = u;
   plan->max_keys = k;
+  plan->subsample_draws = dr;
   plan->workspace_bytes = ex_layout(B * H, d, n_out, mbar, n_max, k).bytes;
   return THIN_OK;
 }
@@ -676,8 +684,8 @@ int thin_express_create(int32_t dtype, int64_t B, int64_t H, int64_t d, int64_t 
   if (dtype != THIN_FP32 && dtype != THIN_BF16) return THIN_EDTYPE;
   if (halve != THIN_HALVE_KH && halve != THIN_HALVE_UNIFORM) return THIN_EINVAL;
   if (!(delta > 0.0 && delta < 1.0)) return THIN_EINVAL;
-  int64_t u = 0, k = 0;
-  const int rc = ex_check(B, H, d, n_out, mbar, n_max, &u, &k);
+  int64_t u = 0, k = 0, dr = 0;
+  const int rc = ex_check(B, H, d, n_out, mbar, n_max, &u, &k, &dr);
   if (rc) return rc;
   const ExLayout L = ex_layout(B * H, d, n_out, mbar, n_max, k);
   if (!workspace || workspace_bytes < L.bytes) return THIN_EWORKSPACE;
@@ -704,31 +712,45 @@ int thin_express_create(int32_t dtype, int64_t B, int64_t H, int64_t d, int64_t 
 }
 
 int thin_express_step(thin_express_t* x, const void* Q, const void* K, const void* V,
-                      const float* uniforms, int64_t n_uniforms, void* O, int32_t out_dtype,
-                      uint8_t* swap_trace, void* stream) {
+                      const float* uniforms, int64_t n_uniforms, const float* draws,
+                      int64_t n_draws, void* O, int32_t out_dtype, uint8_t* swap_trace,
+                      void* stream) {
   if (!x || !Q || !K || !V || !O) return THIN_EINVAL;
   if (out_dtype != THIN_FP32 && out_dtype != THIN_BF16) return THIN_EDTYPE;
   if (x->n >= x->n_max || (x->n >= x->n_out && x->over)) return THIN_EINVAL;
   if (x->u_slice > 0 && !uniforms) return THIN_EINVAL;
   if (n_uniforms < x->S * x->u_slice) return THIN_EUNIFORMS;
+  const bool thin_phase = x->n >= x->n_out;
+  if (thin_phase && ex_needs_draw(x) && (!draws || x->sub_pos >= n_draws)) return THIN_EINVAL;
   hipStream_t st = static_cast<hipStream_t>(stream);
-  const int64_t t = x->n;
   // WtdAttention: the cache plus the point itself, which joins C_0
-  const thin::ExpressSegs g = ex_segs(x, t - x->c0_start + 1);
+  const thin::ExpressSegs g = ex_segs(x, true);
   const int64_t m = seg_total(g);
+  // the point enters E (exact phase) or, when Subsample keeps it, C_0
+  const bool keep = thin_phase ? ex_keep(x, draws) : true;
+  int32_t* app = nullptr;
+  int64_t app_stride = 0;
+  if (!thin_phase) {
+    app = ex_ptr<int32_t>(x, x->L.E) + x->nE;
+    app_stride = 4 * x->n_out;
+  } else if (keep) {
+    app = ex_ptr<int32_t>(x, x->L.C[0]) + x->nC[0];
+    app_stride = ex_stride(x, 0);
+  }
+  const int32_t t = (int32_t)x->n;
   hipError_t e = observed(THIN_KERNEL_ATTENTION, -1, st, [&] {
     return thin::launch_decode_attention(x->dtype, x->d, out_dtype, Q, K, V, g, x->S, x->n_max, m,
-                                         ex_ptr<float>(x, x->L.part), O, st);
+                                         ex_ptr<float>(x, x->L.part), O, app, app_stride, t, st);
   });
   const ExRun run{K, V, uniforms, swap_trace, st};
-  if (e == hipSuccess) e = ex_update(x, &run);
+  if (e == hipSuccess) e = ex_update(x, &run, keep);
   return e == hipSuccess ? THIN_OK : THIN_EHIP;
 }
 
 int thin_express_cache(const thin_express_t* x, int32_t* idx, float* logw, int64_t* len,
                        int32_t* m, void* stream) {
   if (!x || !idx || !logw || !len) return THIN_EINVAL;
-  const thin::ExpressSegs g = ex_segs(x, x->nC[0]);
+  const thin::ExpressSegs g = ex_segs(x, false);
   const int64_t k = seg_total(g);
   *len = k;
   if (m) *m = x->m;
@@ -742,7 +764,7 @@ int thin_express_cache(const thin_express_t* x, int32_t* idx, float* logw, int64
 
 int thin_express_next(const thin_express_t* x, int64_t* keys, int64_t* t) {
   if (!x || !keys || !t) return THIN_EINVAL;
-  *keys = seg_total(ex_segs(x, x->n - x->c0_start + 1));
+  *keys = seg_total(ex_segs(x, true));
   *t = x->n;
   return THIN_OK;
 }

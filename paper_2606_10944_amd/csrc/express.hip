@@ -15,13 +15,6 @@ __device__ __forceinline__ float wave_max(float v) {
   return v;
 }
 
-// dst[s * dst_stride + j] = start + j  (j < len)
-__global__ void rows_iota_kernel(int32_t* dst, int64_t dst_stride, int64_t start, int64_t len) {
-  const int64_t s = blockIdx.y;
-  const int64_t j = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (j < len) dst[s * dst_stride + j] = (int32_t)(start + j);
-}
-
 // dst[s * dst_stride + j] = src[s * src_stride + j]  (j < len)
 __global__ void rows_copy_kernel(const int32_t* src, int64_t src_stride, int32_t* dst,
                                  int64_t dst_stride, int64_t len) {
@@ -214,11 +207,16 @@ __device__ __forceinline__ void store_out<bf16_t>(bf16_t* p, float v) {
 }
 
 // One workgroup per slice: the partials' maxima and sums are staged in LDS
-// (one load each), then thread c merges column c of every partial.
+// (one load each), then thread c merges column c of every partial.  With
+// app non-null, thread 0 also writes the point's position app_val to
+// app[s * app_stride] (the point entering its cache list).
 template <int D, typename TO>
 __global__ __launch_bounds__(128) void decode_attn_merge_kernel(const float* __restrict__ part,
-                                                                int split, TO* __restrict__ O) {
+                                                                int split, TO* __restrict__ O,
+                                                                int32_t* app, int64_t app_stride,
+                                                                int32_t app_val) {
   const int64_t s = blockIdx.x;
+  if (app && threadIdx.x == 0) app[s * app_stride] = app_val;
   const float* p = part + s * split * (int64_t)(D + 2);
   __shared__ float s_w[kDecodeMaxSplit], s_l[kDecodeMaxSplit];
   __shared__ float s_M;
@@ -250,26 +248,32 @@ __global__ __launch_bounds__(128) void decode_attn_merge_kernel(const float* __r
   }
 }
 
+struct Append {
+  int32_t* dst;
+  int64_t stride;
+  int32_t val;
+};
+
 template <typename T, int D, typename TO>
 hipError_t launch_decode_t(const void* Q, const void* K, const void* V, const ExpressSegs& segs,
                            int64_t S, int64_t ld, int64_t m, int split, float* part, void* O,
-                           hipStream_t st) {
+                           const Append& ap, hipStream_t st) {
   hipLaunchKernelGGL((decode_attn_partial_kernel<T, D>), dim3((unsigned)split, (unsigned)S),
                      dim3(64 * kDecWaves), 0, st, (const T*)Q, (const T*)K, (const T*)V, segs, ld,
                      m, split, part);
   hipLaunchKernelGGL((decode_attn_merge_kernel<D, TO>), dim3((unsigned)S), dim3(128), 0, st,
-                     (const float*)part, split, (TO*)O);
+                     (const float*)part, split, (TO*)O, ap.dst, ap.stride, ap.val);
   return hipGetLastError();
 }
 
 template <typename T, typename TO>
 hipError_t launch_decode_d(int64_t d, const void* Q, const void* K, const void* V,
                            const ExpressSegs& g, int64_t S, int64_t ld, int64_t m, int split,
-                           float* part, void* O, hipStream_t st) {
+                           float* part, void* O, const Append& ap, hipStream_t st) {
   switch (d) {
-    case 32: return launch_decode_t<T, 32, TO>(Q, K, V, g, S, ld, m, split, part, O, st);
-    case 64: return launch_decode_t<T, 64, TO>(Q, K, V, g, S, ld, m, split, part, O, st);
-    case 128: return launch_decode_t<T, 128, TO>(Q, K, V, g, S, ld, m, split, part, O, st);
+    case 32: return launch_decode_t<T, 32, TO>(Q, K, V, g, S, ld, m, split, part, O, ap, st);
+    case 64: return launch_decode_t<T, 64, TO>(Q, K, V, g, S, ld, m, split, part, O, ap, st);
+    case 128: return launch_decode_t<T, 128, TO>(Q, K, V, g, S, ld, m, split, part, O, ap, st);
     default: return hipErrorInvalidValue;
   }
 }
@@ -283,24 +287,18 @@ int decode_attention_split(int64_t m) {
 
 hipError_t launch_decode_attention(int dtype, int64_t d, int out_dtype, const void* Q,
                                    const void* K, const void* V, const ExpressSegs& g, int64_t S,
-                                   int64_t ld, int64_t m, float* part, void* O, hipStream_t st) {
+                                   int64_t ld, int64_t m, float* part, void* O, int32_t* app,
+                                   int64_t app_stride, int32_t app_val, hipStream_t st) {
   if (m < 1 || g.n < 1) return hipErrorInvalidValue;
   const int split = decode_attention_split(m);
+  const Append ap{app, app_stride, app_val};
   if (dtype == 0)
     return out_dtype == 0
-               ? launch_decode_d<float, float>(d, Q, K, V, g, S, ld, m, split, part, O, st)
-               : launch_decode_d<float, bf16_t>(d, Q, K, V, g, S, ld, m, split, part, O, st);
+               ? launch_decode_d<float, float>(d, Q, K, V, g, S, ld, m, split, part, O, ap, st)
+               : launch_decode_d<float, bf16_t>(d, Q, K, V, g, S, ld, m, split, part, O, ap, st);
   return out_dtype == 0
-             ? launch_decode_d<bf16_t, float>(d, Q, K, V, g, S, ld, m, split, part, O, st)
-             : launch_decode_d<bf16_t, bf16_t>(d, Q, K, V, g, S, ld, m, split, part, O, st);
-}
-
-hipError_t launch_rows_iota(int32_t* dst, int64_t dst_stride, int64_t start, int64_t len,
-                            int64_t S, hipStream_t st) {
-  if (len <= 0) return hipSuccess;
-  dim3 grid((unsigned)((len + 255) / 256), (unsigned)S);
-  hipLaunchKernelGGL(rows_iota_kernel, grid, dim3(256), 0, st, dst, dst_stride, start, len);
-  return hipGetLastError();
+             ? launch_decode_d<bf16_t, float>(d, Q, K, V, g, S, ld, m, split, part, O, ap, st)
+             : launch_decode_d<bf16_t, bf16_t>(d, Q, K, V, g, S, ld, m, split, part, O, ap, st);
 }
 
 hipError_t launch_rows_copy(const int32_t* src, int64_t src_stride, int32_t* dst,

@@ -92,8 +92,6 @@ struct ExpressSegs {
   ExpressSeg seg[kExpressMaxSegs];
   int n;
 };
-hipError_t launch_rows_iota(int32_t* dst, int64_t dst_stride, int64_t start, int64_t len,
-                            int64_t S, hipStream_t st);
 hipError_t launch_rows_copy(const int32_t* src, int64_t src_stride, int32_t* dst,
                             int64_t dst_stride, int64_t len, int64_t S, hipStream_t st);
 // v_max bits per slice over the rows idx[s, 0..N) of V (slices ld rows apart).
@@ -106,13 +104,15 @@ hipError_t launch_express_keys(const ExpressSegs& segs, int64_t S, int64_t m, in
 // Weighted attention of one query per slice (Q [S, d], O [S, d]) over the m
 // keys of the segments (rows of K / V, slices ld rows apart): the keys of a
 // slice split over decode_attention_split(m) workgroups, whose partials
-// (S * split * (d + 2) floats in `part`) a second launch merges.
+// (S * split * (d + 2) floats in `part`) a second launch merges; that launch
+// also writes app_val to app[s * app_stride] when app is non-null.
 constexpr int kDecodeKeysPerGroup = 16;
 constexpr int kDecodeMaxSplit = 16;
 int decode_attention_split(int64_t m);
 hipError_t launch_decode_attention(int dtype, int64_t d, int out_dtype, const void* Q,
                                    const void* K, const void* V, const ExpressSegs& segs,
                                    int64_t S, int64_t ld, int64_t m, float* part, void* O,
+                                   int32_t* app, int64_t app_stride, int32_t app_val,
                                    hipStream_t st);
 
 

@@ -197,10 +197,12 @@ def test_launch_hook_can_be_set_and_cleared():
 
 @pytest.mark.parametrize("n_out,mbar,n_max", [(8, 4, 512), (8, 4, 300), (16, 4, 1000),
                                               (128, 6, 16384), (128, 8, 100000), (4, 2, 64),
-                                              (32, 5, 2000)])
+                                              (32, 5, 2000), (8, 2, 2000), (8, 4, 5000),
+                                              (128, 5, 40000)])
 def test_express_plan_counts_the_oracles_uniforms(n_out, mbar, n_max):
     p = _lib.thin_express_plan(2, 3, 64, n_out, mbar, n_max)
     assert p["uniforms_per_slice"] == oracle.express_uniforms(n_max, n_out, mbar)
+    assert p["subsample_draws"] == oracle.express_draws(n_max, n_out, mbar)
     assert 1 <= p["max_keys"] <= 6 * n_out + 1 and p["workspace_bytes"] > 0
 
 
@@ -212,8 +214,9 @@ def test_express_rejects_unsupported_sizes():
         return L.thin_express_plan(B, H, d, n_out, mbar, n_max, C.byref(plan))
 
     assert rc() == _lib.THIN_OK
-    assert rc(n_max=513) == _lib.THIN_EINVAL          # the next thin phase needs m = 6 > mbar
-    assert rc(mbar=5, n_max=513) == _lib.THIN_EINVAL  # m = 6 > 5 as well
+    assert rc(n_max=5000) == _lib.THIN_OK             # m = 6 > mbar: Subsample, groups of 2
+    assert rc(mbar=5, n_max=512) == _lib.THIN_OK
+    assert rc(mbar=5, n_max=513) == _lib.THIN_EINVAL  # m = 6: groups of 4*8/2^5 = 1 point
     assert rc(n_out=4, mbar=4, n_max=300) == _lib.THIN_EINVAL  # groups of 4*4/16 = 1 point
     assert rc(d=80) == _lib.THIN_EINVAL
     assert rc(n_out=4096) == _lib.THIN_EINVAL         # 4 n_out above the largest bucket

@@ -22,6 +22,11 @@ CASES = [
     dict(B=1, H=2, d=128, dtype="fp32", n_out=16, mbar=4, n=1024, halve="kh"),
     # n_out = 128: Halve phase on 512 points (pair scores + decisions), a partial level 2
     dict(B=1, H=2, d=128, dtype="bf16", n_out=128, mbar=6, n=1800, halve="kh"),
+    # Subsample above mbar (strata of 4 and 16 points)
+    dict(B=1, H=2, d=64, dtype="bf16", n_out=8, mbar=2, n=1500, halve="kh"),
+    dict(B=2, H=1, d=64, dtype="fp32", n_out=8, mbar=2, n=2100, halve="uniform"),
+    # the decoding experiments' setting mbar = log2(n_out) - 2, past 8192 points
+    dict(B=1, H=2, d=128, dtype="bf16", n_out=128, mbar=5, n=9000, halve="kh"),
 ]
 
 
@@ -30,23 +35,25 @@ def _run(c):
     Q, K, V = W.make_qkv(w)
     plan = thin_express_plan(w.B, w.H, w.d, c["n_out"], c["mbar"], w.n)
     U = W.make_uniforms(w, w.S * plan["uniforms_per_slice"])
+    nd = plan["subsample_draws"]
+    draws = torch.from_numpy(np.random.default_rng(7).random(max(nd, 1)).astype(np.float32))
     dt = torch.bfloat16 if c["dtype"] == "bf16" else torch.float32
     ex = ExpressCache(w.B, w.H, w.d, c["n_out"], c["mbar"], w.n, dtype=dt, halve=c["halve"])
     Qd, Kd, Vd, Ud = Q.to(DEV), K.to(DEV), V.to(DEV), U.to(DEV)
     tr = torch.zeros(max(U.numel(), 1), dtype=torch.uint8, device=DEV)
     O = torch.empty((w.B, w.H, w.n, w.d), dtype=torch.float32, device=DEV)
     for t in range(w.n):
-        O[:, :, t] = ex.step(Qd[:, :, t].contiguous(), Kd, Vd, Ud, trace=tr)
+        O[:, :, t] = ex.step(Qd[:, :, t].contiguous(), Kd, Vd, Ud, draws=draws, trace=tr)
     idx, lw, m = ex.cache()
     torch.cuda.synchronize()
     ex.close()
     return w, Q, K, V, U, O.cpu().numpy(), idx.cpu().numpy(), lw.cpu().numpy(), m, \
-        tr.cpu().numpy(), plan
+        tr.cpu().numpy(), plan, draws.numpy()
 
 
 @pytest.mark.parametrize("c", CASES, ids=lambda c: f"o{c['n_out']}-mbar{c['mbar']}-n{c['n']}-d{c['d']}-{c['dtype']}-{c['halve']}")
 def test_express_decode_parity(c):
-    w, Q, K, V, U, O, idx, lw, m, tr, plan = _run(c)
+    w, Q, K, V, U, O, idx, lw, m, tr, plan, draws = _run(c)
     us = plan["uniforms_per_slice"]
     Us = U.numpy().reshape(w.S, -1) if us else np.zeros((w.S, 1), np.float32)
     ts = tr[: w.S * us].reshape(w.S, -1) if us else np.zeros((w.S, 1), np.uint8)
@@ -56,7 +63,7 @@ def test_express_decode_parity(c):
         b, h = divmod(s, w.H)
         r = oracle.express_decode(Q[b, h], K[b, h], V[b, h], c["n_out"], c["mbar"], Us[s],
                                   halve=c["halve"], follow=ts[s] if c["halve"] == "kh" else None,
-                                  tol=MARGIN)
+                                  tol=MARGIN, sub_u=draws)
         assert r["stats"]["hard_mismatch"] == 0, (s, r["stats"])
         near += r["stats"]["near_ties"]
         if c["halve"] == "uniform":

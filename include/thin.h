@@ -294,6 +294,39 @@ int thin_express_next(const thin_express_t* x, int64_t* keys, int64_t* t);
 int thin_express_destroy(thin_express_t* x);
 
 /*
+ * Masked prefill: the outputs of Thinformer decoding (thin_express_step) for
+ * every point of a whole sequence at once (Alg. 4; the offline form of the
+ * Express recursion, App. F).  Point p attends over the cache of points
+ * 0..p-1 plus itself, exactly as a decoding step would, with the same
+ * uniforms layout (every Halve call's N/2 draws at the offset it has in
+ * decoding) and the same Subsample draws (host, one per stratum).
+ * The Compress2 calls of a level run batched by depth (their outputs kept),
+ * the Halve phases level by level, then one attention launch.  Host tables
+ * are copied into the workspace and the stream is synchronized once.
+ *   Q, K, V (device) [B,H,n,d] of `dtype`;  O (device) [B,H,n,d] of out_dtype.
+ *   uniforms (device) [B*H, plan.uniforms_per_slice];  draws (host).
+ *   swap_trace (device, nullable) uint8 indexed like uniforms.
+ * Sizes as for thin_express_plan with n_max = n, and n <= 2^30.
+ * Errors: THIN_EINVAL, THIN_EDTYPE, THIN_EUNIFORMS, THIN_EWORKSPACE, THIN_EHIP.
+ */
+typedef struct {
+  int64_t uniforms_per_slice; /* as thin_express_plan for n points          */
+  int64_t subsample_draws;    /* Subsample draws the n points need          */
+  size_t workspace_bytes;     /* device workspace of thin_express_prefill   */
+} thin_prefill_plan_t;
+
+/* Host-only. */
+int thin_express_prefill_plan(int64_t B, int64_t H, int64_t n, int64_t d, int64_t n_out,
+                              int32_t mbar, thin_prefill_plan_t* plan);
+
+int thin_express_prefill(int32_t dtype, int64_t B, int64_t H, int64_t n, int64_t d,
+                         int64_t n_out, int32_t mbar, double delta, int32_t halve,
+                         const void* Q, const void* K, const void* V, const float* uniforms,
+                         int64_t n_uniforms, const float* draws, int64_t n_draws, void* O,
+                         int32_t out_dtype, void* workspace, size_t workspace_bytes,
+                         uint8_t* swap_trace, void* stream);
+
+/*
  * Diagnostic: out[m*16 + n] = <rows[m], rows[16 + n]> for m, n < 16, computed
  * through the MFMA row-fragment path the pair-score kernel uses.
  *   rows (device) [32, d] of `dtype`;  out (device) float32 [16, 16].

@@ -24,6 +24,7 @@ THIN_FP32, THIN_BF16 = 0, 1
 EXPORTS = ("thin_plan", "thin_compress", "thin_compress_traced", "thin_compress_ex", "thin_attention",
            "thin_attention_ex", "thin_express_plan", "thin_express_create", "thin_express_step",
            "thin_express_cache", "thin_express_next", "thin_express_destroy",
+           "thin_express_prefill_plan", "thin_express_prefill",
            "thin_selftest_gram16", "thin_status_str",
            "thin_set_launch_hook")
 
@@ -44,6 +45,11 @@ class ThinError(RuntimeError):
 class ExpressPlan(C.Structure):
     _fields_ = [("uniforms_per_slice", C.c_int64), ("max_keys", C.c_int64),
                 ("workspace_bytes", C.c_size_t), ("subsample_draws", C.c_int64)]
+
+
+class PrefillPlan(C.Structure):
+    _fields_ = [("uniforms_per_slice", C.c_int64), ("subsample_draws", C.c_int64),
+                ("workspace_bytes", C.c_size_t)]
 
 
 class CompressOpts(C.Structure):
@@ -90,6 +96,9 @@ def lib():
     L.thin_express_cache.argtypes = [P, P, P, C.POINTER(C.c_int64), C.POINTER(C.c_int32), P]
     L.thin_express_next.argtypes = [P, C.POINTER(C.c_int64), C.POINTER(C.c_int64)]
     L.thin_express_destroy.argtypes = [P]
+    L.thin_express_prefill_plan.argtypes = [I64, I64, I64, I64, I64, I32, C.POINTER(PrefillPlan)]
+    L.thin_express_prefill.argtypes = [I32, I64, I64, I64, I64, I64, I32, C.c_double, I32, P, P,
+                                       P, P, I64, P, I64, P, I32, P, SZ, P, P]
     L.thin_selftest_gram16.argtypes = [I32, I64, P, P, P]
     L.thin_status_str.argtypes = [C.c_int]
     L.thin_status_str.restype = C.c_char_p
@@ -98,7 +107,8 @@ def lib():
     for f in ("thin_plan", "thin_compress", "thin_compress_traced", "thin_compress_ex",
               "thin_attention", "thin_attention_ex", "thin_selftest_gram16", "thin_express_plan",
               "thin_express_create", "thin_express_step", "thin_express_cache",
-              "thin_express_next", "thin_express_destroy"):
+              "thin_express_next", "thin_express_destroy", "thin_express_prefill_plan",
+              "thin_express_prefill"):
         getattr(L, f).restype = C.c_int
     _lib = L
     return L
@@ -337,6 +347,46 @@ class ExpressCache:
             self.close()
         except Exception:
             pass
+
+
+def thin_express_prefill_plan(B: int, H: int, n: int, d: int, n_out: int, mbar: int) -> dict:
+    p = PrefillPlan()
+    _check(lib().thin_express_prefill_plan(B, H, n, d, n_out, mbar, C.byref(p)),
+           "thin_express_prefill_plan")
+    return {k: getattr(p, k) for k, _ in PrefillPlan._fields_}
+
+
+def thin_express_prefill(Q: torch.Tensor, K: torch.Tensor, V: torch.Tensor, n_out: int,
+                         mbar: int, uniforms, *, draws=None, delta: float = 0.5,
+                         halve: str = "kh", out_dtype: torch.dtype = torch.float32,
+                         O: Optional[torch.Tensor] = None, workspace=None,
+                         trace: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    """Masked prefill (thin_express_prefill): every point's Thinformer output
+    over the Express cache of the points before it plus itself, O [B,H,n,d]."""
+    B, H, n, d = _shape4(Q, "Q")
+    for t, nm in ((K, "K"), (V, "V")):
+        if tuple(t.shape) != (B, H, n, d) or not t.is_contiguous() or t.dtype != Q.dtype:
+            raise ThinError(THIN_EINVAL, f"{nm} must match Q")
+    if halve not in HALVE:
+        raise ThinError(THIN_EINVAL, f"unknown halving {halve!r}")
+    plan = thin_express_prefill_plan(B, H, n, d, n_out, mbar)
+    if workspace is None:
+        workspace = torch.empty(max(plan["workspace_bytes"], 256), dtype=torch.uint8,
+                                device=Q.device)
+    if O is None:
+        O = torch.empty((B, H, n, d), dtype=out_dtype, device=Q.device)
+    if draws is not None and (not isinstance(draws, torch.Tensor) or draws.is_cuda
+                              or draws.dtype != torch.float32 or not draws.is_contiguous()):
+        raise ThinError(THIN_EINVAL, "draws must be a contiguous float32 CPU tensor")
+    nU = 0 if uniforms is None else uniforms.numel()
+    rc = lib().thin_express_prefill(
+        _dtype_code(Q.dtype), B, H, n, d, n_out, mbar, delta, HALVE[halve], _ptr(Q), _ptr(K),
+        _ptr(V), None if uniforms is None else _ptr(uniforms), nU,
+        None if draws is None else _ptr(draws), 0 if draws is None else draws.numel(), _ptr(O),
+        _dtype_code(O.dtype), _ptr(workspace), workspace.numel(),
+        None if trace is None else _ptr(trace), _stream(stream))
+    _check(rc, "thin_express_prefill")
+    return O
 
 
 def thin_selftest_gram16(rows: torch.Tensor, stream=None) -> torch.Tensor:

@@ -4,6 +4,7 @@
 
 #include <algorithm>
 #include <new>
+#include <vector>
 #include <stdint.h>
 #include <string.h>
 
@@ -249,7 +250,7 @@ int compress_impl(const void* K, const void* V, int32_t dtype, int64_t B, int64_
     int64_t u_off = lv.sub ? lv.n_kept : 0;
     for (int32_t r = 0; r < lv.L && e == hipSuccess; ++r) {
       int32_t* out = (r == lv.L - 1) ? last_out(cur) : (cur == ws.buf_b ? ws.buf_a : ws.buf_b);
-      thin::HalveArgs a;
+      thin::HalveArgs a{};
       a.K = Km;
       a.V = Vm;
       a.n = nm;
@@ -344,6 +345,22 @@ ExLayout ex_layout(int64_t S, int64_t d, int64_t n_out, int32_t mbar, int64_t n_
 
 }  // namespace
 
+// Halve calls of a count-only run, for the prefill: the uniform offset of
+// every call, by level and Compress2 depth (depth -1: the Halve phase).
+struct ExpressCalls {
+  std::vector<std::vector<std::vector<int64_t>>> calls;  // [m / 2][depth + 1] -> offsets
+  void add(int m, int depth, int64_t u) {
+    if ((int)calls.size() <= m / 2) calls.resize(m / 2 + 1);
+    auto& lv = calls[m / 2];
+    if ((int)lv.size() <= depth + 1) lv.resize(depth + 2);
+    lv[depth + 1].push_back(u);
+  }
+  int64_t count(int m, int depth) const {
+    if ((int)calls.size() <= m / 2 || (int)calls[m / 2].size() <= depth + 1) return 0;
+    return (int64_t)calls[m / 2][depth + 1].size();
+  }
+};
+
 struct thin_express {
   int32_t dtype, halve, mbar;
   int64_t B, H, S, d, n_out, n_max, u_slice, kmax;
@@ -356,6 +373,7 @@ struct thin_express {
   int64_t nC[kExMaxL + 1];
   int64_t sub_n, sub_i, sub_pos;  // Subsample: points since its reset, the kept one, draws used
   bool over;
+  ExpressCalls* rec;  // count-only runs: records every Halve call (nullable)
 };
 
 namespace {
@@ -411,10 +429,13 @@ struct ExRun {
 };
 
 hipError_t ex_halve(thin_express* x, const ExRun* run, const int32_t* in, int64_t N, double delta,
-                    int32_t* out) {
+                    int32_t* out, int depth) {
   const int64_t o = x->upos;
   x->upos += N / 2;
-  if (!run) return hipSuccess;
+  if (!run) {
+    if (x->rec) x->rec->add(x->m, depth, o);
+    return hipSuccess;
+  }
   hipStream_t st = run->st;
   if (x->halve == THIN_HALVE_UNIFORM)
     return observed(THIN_KERNEL_UNIFORM, -1, st, [&] {
@@ -422,7 +443,7 @@ hipError_t ex_halve(thin_express* x, const ExRun* run, const int32_t* in, int64_
     });
   uint32_t* vmax = ex_ptr<uint32_t>(x, x->L.vmax);
   hipError_t e = observed(THIN_KERNEL_EXPRESS, -1, st, [&] {
-    return thin::launch_vmax_rows(x->dtype, run->V, x->n_max, x->d, in, N, x->S, vmax, st);
+    return thin::launch_vmax_rows(x->dtype, run->V, x->n_max, x->d, in, N, N, 1, x->S, vmax, st);
   });
   if (e != hipSuccess) return e;
   thin::HalveArgs a{};
@@ -479,7 +500,7 @@ hipError_t ex_update(thin_express* x, const ExRun* run, bool keep) {
     const int64_t T = (x->n_out << (i + 2)) >> x->mp;
     if (x->nC[i] != T) continue;
     const int32_t* in = ex_ptr<int32_t>(x, x->L.C[i]);
-    e = ex_halve(x, run, in, T, express_delta(x->m, i, x->mbar, x->delta), t1);
+    e = ex_halve(x, run, in, T, express_delta(x->m, i, x->mbar, x->delta), t1, i);
     if (e == hipSuccess)
       e = ex_copy(x, run, t1, T / 2, ex_ptr<int32_t>(x, x->L.C[i + 1]) + x->nC[i + 1],
                   ex_stride(x, i + 1), T / 2);
@@ -495,8 +516,8 @@ hipError_t ex_update(thin_express* x, const ExRun* run, bool keep) {
   if (e == hipSuccess && x->n == 4 * (x->n_out << x->m)) {  // Halve phase: E halved twice
     const double dl = express_delta(x->m, -1, x->mbar, x->delta);
     int32_t* t2 = ex_ptr<int32_t>(x, x->L.t2);
-    e = ex_halve(x, run, E, x->nE, dl, t1);
-    if (e == hipSuccess) e = ex_halve(x, run, t1, x->nE / 2, dl, t2);
+    e = ex_halve(x, run, E, x->nE, dl, t1, -1);
+    if (e == hipSuccess) e = ex_halve(x, run, t1, x->nE / 2, dl, t2, -1);
     if (e == hipSuccess) e = ex_copy(x, run, t2, x->nE / 4, E, sE, x->nE / 4);
     x->nE /= 4;
     x->m += 2;
@@ -661,6 +682,249 @@ const char* thin_status_str(int status) {
 
 }  // extern "C"
 
+namespace {
+
+// ---------------------------------------------------------------------------
+// Masked prefill (Alg. 4 for every point of a sequence at once).  A
+// count-only run of the Express counters records every Halve call (its
+// uniform offset, by level and depth), the kept points and, for every
+// point, the cache it attends over.  Then: every Compress2 depth of a level
+// is one KH launch over all its calls (per-bucket uniform offsets and
+// v_max; every output kept in a node store), the Halve phases run level by
+// level, and one launch attends every point over its block's segments plus
+// its causal run.
+// ---------------------------------------------------------------------------
+struct PfLayout {
+  int64_t n, n_out, S;
+  int32_t mbar;
+  int levels;                                  // levels m = 0, 2, .. reached
+  std::vector<std::vector<size_t>> region;     // [m/2][depth] node store of the calls
+  std::vector<std::vector<int64_t>> rstride;   // [m/2][depth] its row stride per slice
+  std::vector<size_t> enode;                   // [m/2] E after the Halve phase of level m - 2
+  size_t kept, keptrow, keptflag, hp, ein, vmax, lbt, h2, rowh2, score, utab, blocks, tiles, segs;
+  size_t e_bytes, bytes;
+  int64_t max_blocks, max_tiles, max_segs, max_utab;
+};
+
+int64_t group_T(int64_t n_out, int mp, int i) { return (n_out << (i + 2)) >> mp; }
+
+PfLayout pf_layout(int64_t S, int64_t n_out, int32_t mbar, int64_t n, const ExpressCalls& cap) {
+  PfLayout L{};
+  L.n = n;
+  L.n_out = n_out;
+  L.S = S;
+  L.mbar = mbar;
+  L.levels = (int)cap.calls.size();
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t o = off;
+    off += align256(bytes);
+    return o;
+  };
+  const size_t s4 = (size_t)S * 4;
+  L.kept = take(s4 * n);
+  L.keptrow = take(4 * (size_t)n);
+  L.keptflag = take((size_t)n);
+  L.hp = take(s4 * 2 * n_out);
+  L.ein = take(s4 * 4 * n_out);
+  L.region.resize(L.levels + 1);
+  L.rstride.resize(L.levels + 1);
+  L.enode.resize(L.levels + 2);
+  int64_t gmax = 1, pmax = 2 * n_out, ucount = 0;
+  for (int lv = 0; lv < L.levels; ++lv) {
+    const int m = 2 * lv, mp = m < mbar ? m : mbar;
+    L.region[lv].assign(mp, 0);
+    L.rstride[lv].assign(mp, 0);
+    for (int dd = -1; dd < mp; ++dd) {
+      const int64_t c = cap.count(m, dd);
+      ucount += c;
+      if (dd < 0) continue;
+      const int64_t T = group_T(n_out, mp, dd);
+      L.rstride[lv][dd] = c * (T / 2) > 0 ? c * (T / 2) : 1;
+      L.region[lv][dd] = take(s4 * (size_t)L.rstride[lv][dd]);
+      gmax = std::max(gmax, c);
+      pmax = std::max(pmax, c * (T / 2));
+    }
+    L.enode[lv + 1] = take(s4 * n_out);
+  }
+  L.vmax = take(s4 * gmax);
+  L.lbt = take(s4 * pmax);
+  L.h2 = take(s4 * pmax);
+  L.rowh2 = take(s4 * n);
+  const size_t per = thin::halve_score_bytes(4 * n_out);
+  const size_t all = (size_t)S * per, capb = per > kScoreCap ? per : kScoreCap;
+  L.e_bytes = all < capb ? all : capb;
+  L.score = take(L.e_bytes);
+  // host-built tables: uniform offsets, blocks (at most one per point),
+  // tiles (a block's points in runs of 128) and block segments
+  L.max_utab = std::max<int64_t>(ucount, 1);
+  L.max_blocks = n + 1;
+  L.max_tiles = n + n / 128 + 2;
+  L.max_segs = (n + 1) * (int64_t)(mbar + 3);
+  L.utab = take(8 * (size_t)L.max_utab);
+  L.blocks = take(sizeof(thin::PrefillBlock) * (size_t)L.max_blocks);
+  L.tiles = take(sizeof(thin::PrefillTile) * (size_t)L.max_tiles);
+  L.segs = take(sizeof(thin::ExpressSeg) * (size_t)L.max_segs);
+  L.bytes = off;
+  return L;
+}
+
+// The count-only run of n points: records the calls, the kept points, and,
+// given a layout, the blocks of points sharing one cache.
+struct PfHost {
+  ExpressCalls rec;
+  std::vector<int32_t> keptrow;
+  std::vector<uint8_t> keptflag;
+  std::vector<int64_t> kept_base;  // [m/2]: kept-list index of level m's first point
+  std::vector<thin::PrefillBlock> blocks;
+  std::vector<thin::PrefillTile> tiles;
+  std::vector<thin::ExpressSeg> segs;
+};
+
+int pf_run(int64_t n_out, int32_t mbar, int64_t n, const float* draws, int64_t n_draws,
+           const PfLayout* L, unsigned char* ws, PfHost* h) {
+  thin_express x{};
+  x.n_out = n_out;
+  x.mbar = mbar;
+  x.delta = 0.5;
+  x.n_max = n;
+  x.rec = &h->rec;
+  ex_reset(&x);
+  h->keptflag.assign((size_t)n, 0);
+  int64_t causal0 = 0;
+  std::vector<int64_t> sig, last;
+  const float ln2 = (float)log(2.0);
+  auto dev = [&](size_t off) { return reinterpret_cast<int32_t*>(ws + off); };
+  for (int64_t p = 0; p < n; ++p) {
+    if (x.n >= n_out && x.over) return THIN_EINVAL;
+    while ((int64_t)h->kept_base.size() <= x.m / 2) h->kept_base.push_back((int64_t)h->keptrow.size());
+    if (L) {
+      // the cache point p attends over: E (its exact part once complete),
+      // C_1..C_mp (outputs of their calls), and C_0 plus p as the causal run
+      sig.assign({x.m, x.n >= n_out ? x.nE : -1, causal0});
+      for (int i = 1; i <= x.mp; ++i) sig.push_back(x.nC[i]);
+      if (p == 0 || sig != last) {
+        thin::PrefillBlock b{};
+        b.q0 = (int32_t)p;
+        b.causal0 = (int32_t)causal0;
+        b.seg0 = (int32_t)h->segs.size();
+        b.w0 = -(float)x.mp * ln2;
+        const int lv = x.m / 2;
+        if (x.n >= n_out) {
+          if (x.m == 0) {
+            h->segs.push_back({dev(L->kept), n, 0, x.nE, 0.0f});
+          } else {
+            h->segs.push_back({dev(L->enode[lv]), n_out, 0, n_out, 0.0f});
+            const int64_t gdone = (x.nE - n_out) / n_out;
+            if (gdone > 0)
+              h->segs.push_back({dev(L->region[lv][x.mp - 1]), L->rstride[lv][x.mp - 1], 0,
+                                 gdone * n_out, 0.0f});
+          }
+        }
+        for (int i = 1; i <= x.mp; ++i) {
+          if (x.nC[i] == 0) continue;
+          const int64_t half = group_T(n_out, x.mp, i - 1) / 2;
+          const int64_t first = h->rec.count(x.m, i - 1) - x.nC[i] / half;
+          h->segs.push_back({dev(L->region[lv][i - 1]) + first * half, L->rstride[lv][i - 1], 0,
+                             x.nC[i], (float)(i - x.mp) * ln2});
+        }
+        b.nseg = (int32_t)h->segs.size() - b.seg0;
+        if (!h->blocks.empty()) h->blocks.back().q1 = (int32_t)p;
+        h->blocks.push_back(b);
+        last = sig;
+      }
+    }
+    // Subsample, then the update
+    const bool thin_phase = x.n >= n_out;
+    if (thin_phase && ex_needs_draw(&x) && draws && x.sub_pos >= n_draws) return THIN_EINVAL;
+    const bool keep = thin_phase ? ex_keep(&x, draws) : true;
+    h->keptflag[p] = keep ? 1 : 0;
+    if (keep) h->keptrow.push_back((int32_t)p);
+    const int m_before = x.m;
+    const int64_t c0 = h->rec.count(m_before, 0);
+    ex_update(&x, nullptr, keep);
+    if (x.n == n_out)
+      causal0 = n_out;
+    else if (x.n > n_out && (h->rec.count(m_before, 0) != c0 || x.ell == 0))
+      causal0 = p + 1;  // C_0 emptied: by Halve_0 or at the end of a group
+  }
+  if (L) {
+    if (!h->blocks.empty()) h->blocks.back().q1 = (int32_t)n;
+    for (int64_t k = 0; k < (int64_t)h->blocks.size(); ++k)
+      for (int32_t q = h->blocks[k].q0; q < h->blocks[k].q1; q += 128)
+        h->tiles.push_back({(int32_t)k, q});
+    if ((int64_t)h->blocks.size() > L->max_blocks || (int64_t)h->tiles.size() > L->max_tiles ||
+        (int64_t)h->segs.size() > L->max_segs)
+      return THIN_EINVAL;
+    for (const auto& b : h->blocks)
+      if (b.nseg > 32) return THIN_EINVAL;
+  }
+  return THIN_OK;
+}
+
+int pf_check(int64_t B, int64_t H, int64_t n, int64_t d, int64_t n_out, int32_t mbar,
+             PfLayout* L, int64_t* u_slice, int64_t* draws) {
+  int64_t k = 0;
+  const int rc = ex_check(B, H, d, n_out, mbar, n, u_slice, &k, draws);
+  if (rc) return rc;
+  if (n > ((int64_t)1 << 30)) return THIN_EINVAL;
+  PfHost h;
+  if (pf_run(n_out, mbar, n, nullptr, 0, nullptr, nullptr, &h)) return THIN_EINVAL;
+  *L = pf_layout(B * H, n_out, mbar, n, h.rec);
+  return THIN_OK;
+}
+
+// One batched depth (G calls per slice of N rows each) or a single call.
+hipError_t pf_halve(int32_t dtype, int64_t d, int32_t halve, const PfLayout& L,
+                    unsigned char* ws, const void* K, const void* V, const float* U,
+                    int64_t u_slice, uint8_t* trace, const int32_t* in, int64_t in_stride,
+                    int64_t N, int64_t G, const int64_t* u_bucket, int64_t u_off, double delta,
+                    int32_t* out, int64_t out_stride, hipStream_t st) {
+  const int64_t S = L.S;
+  if (halve == THIN_HALVE_UNIFORM)
+    return observed(THIN_KERNEL_UNIFORM, -1, st, [&] {
+      return thin::launch_uniform_halve(S, G * N, in, U, u_slice, u_off, out, trace, st, N,
+                                        u_bucket, in_stride, out_stride);
+    });
+  uint32_t* vmax = reinterpret_cast<uint32_t*>(ws + L.vmax);
+  hipError_t e = observed(THIN_KERNEL_EXPRESS, -1, st, [&] {
+    return thin::launch_vmax_rows(dtype, V, L.n, d, in, in_stride, N, G, S, vmax, st);
+  });
+  if (e != hipSuccess) return e;
+  thin::HalveArgs a{};
+  a.K = K;
+  a.V = V;
+  a.n = L.n;
+  a.ld = L.n;
+  a.vmax_bits = vmax;
+  a.vmax_per_bucket = 1;
+  a.idx_in = in;
+  a.in_stride = in_stride;
+  a.n_r = G * N;
+  a.N = (int32_t)N;
+  a.G = (int32_t)G;
+  a.S = S;
+  a.idx_out = out;
+  a.out_stride = out_stride;
+  a.U = U;
+  a.u_slice = u_slice;
+  a.u_off = u_off;
+  a.u_bucket = u_bucket;
+  a.trace = trace;
+  a.log_c = log(0.5 + log(2.0 * (double)N / delta));
+  a.E = reinterpret_cast<float*>(ws + L.score);
+  a.lbt = reinterpret_cast<float*>(ws + L.lbt);
+  a.h2 = reinterpret_cast<float*>(ws + L.h2);
+  a.rowh2 = reinterpret_cast<float*>(ws + L.rowh2);
+  a.rowh2_write = 1;
+  if (N <= thin::halve_local_rows(dtype, d))  // every call in one local launch
+    return observed(THIN_KERNEL_LOCAL, -1, st,
+                    [&] { return thin::launch_local(dtype, d, a, S * G, st); });
+  return kh_round(dtype, d, a, S * G, L.e_bytes, -1, st);
+}
+
+}  // namespace
+
 extern "C" {
 
 int thin_express_plan(int64_t B, int64_t H, int64_t d, int64_t n_out, int32_t mbar,
@@ -772,6 +1036,138 @@ int thin_express_next(const thin_express_t* x, int64_t* keys, int64_t* t) {
 int thin_express_destroy(thin_express_t* x) {
   delete x;
   return THIN_OK;
+}
+
+}  // extern "C"
+
+extern "C" {
+
+int thin_express_prefill_plan(int64_t B, int64_t H, int64_t n, int64_t d, int64_t n_out,
+                              int32_t mbar, thin_prefill_plan_t* plan) {
+  if (!plan) return THIN_EINVAL;
+  PfLayout L;
+  int64_t u = 0, dr = 0;
+  const int rc = pf_check(B, H, n, d, n_out, mbar, &L, &u, &dr);
+  if (rc) return rc;
+  plan->uniforms_per_slice = u;
+  plan->subsample_draws = dr;
+  plan->workspace_bytes = L.bytes;
+  return THIN_OK;
+}
+
+int thin_express_prefill(int32_t dtype, int64_t B, int64_t H, int64_t n, int64_t d,
+                         int64_t n_out, int32_t mbar, double delta, int32_t halve,
+                         const void* Q, const void* K, const void* V, const float* uniforms,
+                         int64_t n_uniforms, const float* draws, int64_t n_draws, void* O,
+                         int32_t out_dtype, void* workspace, size_t workspace_bytes,
+                         uint8_t* swap_trace, void* stream) {
+  if (dtype != THIN_FP32 && dtype != THIN_BF16) return THIN_EDTYPE;
+  if (out_dtype != THIN_FP32 && out_dtype != THIN_BF16) return THIN_EDTYPE;
+  if (halve != THIN_HALVE_KH && halve != THIN_HALVE_UNIFORM) return THIN_EINVAL;
+  if (!(delta > 0.0 && delta < 1.0)) return THIN_EINVAL;
+  if (!Q || !K || !V || !O) return THIN_EINVAL;
+  PfLayout L;
+  int64_t u_slice = 0, ndraw = 0;
+  int rc = pf_check(B, H, n, d, n_out, mbar, &L, &u_slice, &ndraw);
+  if (rc) return rc;
+  const int64_t S = B * H;
+  if (u_slice > 0 && !uniforms) return THIN_EINVAL;
+  if (n_uniforms < S * u_slice) return THIN_EUNIFORMS;
+  if (ndraw > 0 && (!draws || n_draws < ndraw)) return THIN_EINVAL;
+  if (!workspace || workspace_bytes < L.bytes) return THIN_EWORKSPACE;
+  if ((reinterpret_cast<uintptr_t>(workspace) & 255u) != 0) return THIN_EWORKSPACE;
+  unsigned char* ws = static_cast<unsigned char*>(workspace);
+  PfHost h;
+  rc = pf_run(n_out, mbar, n, draws, n_draws, &L, ws, &h);
+  if (rc) return rc;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  // uniform offsets of every call, by level and depth, one table
+  std::vector<int64_t> utab;
+  std::vector<std::vector<size_t>> uoff(L.levels);
+  for (int lv = 0; lv < L.levels && lv < (int)h.rec.calls.size(); ++lv) {
+    uoff[lv].assign(h.rec.calls[lv].size(), 0);
+    for (size_t k = 0; k < h.rec.calls[lv].size(); ++k) {
+      uoff[lv][k] = utab.size();
+      utab.insert(utab.end(), h.rec.calls[lv][k].begin(), h.rec.calls[lv][k].end());
+    }
+  }
+  if ((int64_t)utab.size() > L.max_utab) return THIN_EINVAL;
+  hipError_t e = hipSuccess;
+  auto ok = [&](hipError_t v) {
+    if (v != hipSuccess && e == hipSuccess) e = v;
+    return e == hipSuccess;
+  };
+  auto up = [&](size_t off, const void* src, size_t bytes) {
+    if (bytes) ok(hipMemcpyAsync(ws + off, src, bytes, hipMemcpyHostToDevice, st));
+  };
+  up(L.utab, utab.data(), utab.size() * 8);
+  up(L.blocks, h.blocks.data(), h.blocks.size() * sizeof(thin::PrefillBlock));
+  up(L.tiles, h.tiles.data(), h.tiles.size() * sizeof(thin::PrefillTile));
+  up(L.segs, h.segs.data(), h.segs.size() * sizeof(thin::ExpressSeg));
+  up(L.keptrow, h.keptrow.data(), h.keptrow.size() * 4);
+  up(L.keptflag, h.keptflag.data(), h.keptflag.size());
+  // the host tables are pageable and freed on return: finish the copies first
+  if (e == hipSuccess) ok(hipStreamSynchronize(st));
+  auto dev = [&](size_t off) { return reinterpret_cast<int32_t*>(ws + off); };
+  int32_t* kept = dev(L.kept);
+  const int64_t nk = (int64_t)h.keptrow.size();
+  if (e == hipSuccess && nk > 0)
+    ok(observed(THIN_KERNEL_EXPRESS, -1, st, [&] {
+      return thin::launch_rows_copy(dev(L.keptrow), 0, kept, n, nk, S, st);
+    }));
+  const int64_t* ut = reinterpret_cast<const int64_t*>(ws + L.utab);
+  // Compress2 of every group: one launch per (level, depth)
+  for (int lv = 1; lv < L.levels && e == hipSuccess; ++lv) {
+    const int m = 2 * lv, mp = m < mbar ? m : mbar;
+    for (int i = 0; i < mp && e == hipSuccess; ++i) {
+      const int64_t G = h.rec.count(m, i);
+      if (G == 0) break;
+      const int64_t T = group_T(n_out, mp, i);
+      const int32_t* in = i == 0 ? kept + h.kept_base[lv] : dev(L.region[lv][i - 1]);
+      const int64_t in_stride = i == 0 ? n : L.rstride[lv][i - 1];
+      ok(pf_halve(dtype, d, halve, L, ws, K, V, uniforms, u_slice, swap_trace, in, in_stride, T,
+                  G, ut + uoff[lv][i + 1], 0, express_delta(m, i, mbar, delta),
+                  dev(L.region[lv][i]), L.rstride[lv][i], st));
+    }
+  }
+  // Halve phases, level by level: E (the previous Express coreset, then the
+  // three groups' coresets) halved twice
+  for (int lv = 0; lv < L.levels && e == hipSuccess; ++lv) {
+    const int m = 2 * lv, mp = m < mbar ? m : mbar;
+    if (h.rec.count(m, -1) < 2) break;
+    const double dl = express_delta(m, -1, mbar, delta);
+    const int32_t* in = kept;  // level 0: E is the first 4 n_out points
+    int64_t in_stride = n;
+    if (m > 0) {
+      ok(observed(THIN_KERNEL_EXPRESS, -1, st, [&] {
+        return thin::launch_rows_copy(dev(L.enode[lv]), n_out, dev(L.ein), 4 * n_out, n_out, S,
+                                      st);
+      }));
+      ok(observed(THIN_KERNEL_EXPRESS, -1, st, [&] {
+        return thin::launch_rows_copy(dev(L.region[lv][mp - 1]), L.rstride[lv][mp - 1],
+                                      dev(L.ein) + n_out, 4 * n_out, 3 * n_out, S, st);
+      }));
+      in = dev(L.ein);
+      in_stride = 4 * n_out;
+    }
+    const std::vector<int64_t>& hp = h.rec.calls[lv][0];
+    if (e == hipSuccess)
+      ok(pf_halve(dtype, d, halve, L, ws, K, V, uniforms, u_slice, swap_trace, in, in_stride,
+                  4 * n_out, 1, nullptr, hp[0], dl, dev(L.hp), 2 * n_out, st));
+    if (e == hipSuccess)
+      ok(pf_halve(dtype, d, halve, L, ws, K, V, uniforms, u_slice, swap_trace, dev(L.hp),
+                  2 * n_out, 2 * n_out, 1, nullptr, hp[1], dl, dev(L.enode[lv + 1]), n_out, st));
+  }
+  if (e == hipSuccess)
+    ok(observed(THIN_KERNEL_ATTENTION, -1, st, [&] {
+      return thin::launch_prefill_attention(
+          dtype, d, out_dtype, Q, K, V, S, n,
+          reinterpret_cast<const thin::PrefillTile*>(ws + L.tiles), (int64_t)h.tiles.size(),
+          reinterpret_cast<const thin::PrefillBlock*>(ws + L.blocks),
+          reinterpret_cast<const thin::ExpressSeg*>(ws + L.segs),
+          reinterpret_cast<const uint8_t*>(ws + L.keptflag), O, st);
+    }));
+  return e == hipSuccess ? THIN_OK : THIN_EHIP;
 }
 
 }  // extern "C"

@@ -570,6 +570,255 @@ hipError_t launch_attn_res_d(int64_t n_out, const void* Q, const void* K, const 
   return hipSuccess;
 }
 
+// ---------------------------------------------------------------------------
+// Masked (causal) prefill over the Express cache (Alg. 4 for every point at
+// once).  One workgroup = up to 128 queries [q0, q1) of one block of one
+// slice.  The block's keys are its segments (rows of the cache, each
+// segment with one log-weight) followed by the causal candidates, positions
+// causal0 .. q1-1 with the block's C_0 log-weight w0: candidate r is seen by
+// query p iff r == p (the point itself) or r < p and r was kept (kept[r]).
+// Same arithmetic as coreset_attn_kernel with per-key biases sqrt(d) * logw.
+// ---------------------------------------------------------------------------
+template <typename T, int D, typename TO>
+__global__ __launch_bounds__(64 * WAVES) void prefill_attn_kernel(
+    const T* __restrict__ Q, const T* __restrict__ K, const T* __restrict__ V, int64_t n,
+    const PrefillTile* __restrict__ tiles, const PrefillBlock* __restrict__ blocks,
+    const ExpressSeg* __restrict__ segs, const uint8_t* __restrict__ kept, TO* __restrict__ O) {
+  constexpr int NV = Frag<T, D>::NV;
+  constexpr bool BF = Elem<T>::bytes == 2;
+  using L = AttnLds<T, D>;
+  __shared__ __align__(16) unsigned char lds[L::bytes];
+  __shared__ int32_t s_pos[KC];  // -1: a cache key; else the candidate's position (bit 30: not kept)
+  __shared__ int64_t s_seg_end[32];
+  unsigned char* sK = lds;
+  unsigned char* sV = lds + KC * L::k_stride;
+  float* sB = reinterpret_cast<float*>(sV + L::v_rows * L::v_stride);
+
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int m16 = lane & 15, g = lane >> 4;
+  const int64_t s = blockIdx.y;
+  const PrefillTile tile = tiles[blockIdx.x];
+  const PrefillBlock B = blocks[tile.blk];
+  const int64_t q0 = tile.q0;
+  const int64_t q1 = min((int64_t)B.q1, q0 + QPB);
+  const ExpressSeg* bs = segs + B.seg0;
+  const int nseg = min(B.nseg, 32);
+  if (threadIdx.x == 0) {
+    int64_t e = 0;
+    for (int k = 0; k < nseg; ++k) s_seg_end[k] = (e += bs[k].len);
+  }
+  __syncthreads();
+  const int64_t F = nseg ? s_seg_end[nseg - 1] : 0;
+  const int64_t M = F + (q1 - B.causal0);
+  const T* Ks = K + s * n * D;
+  const T* Vs = V + s * n * D;
+  const float sqrt_d = (float)sqrt((double)D);
+  const float c2 = (float)(kLog2e / sqrt((double)D));
+  const int64_t qw = q0 + wave * 16 * QT;
+
+  uint4 Bq[QT][NV];
+#pragma unroll
+  for (int qt = 0; qt < QT; ++qt) {
+    const int64_t q = qw + qt * 16 + m16;
+    load_frag<T, D>(Q + s * n * D, q, g, q < q1, Bq[qt]);
+  }
+  float mrun[QT], lrun[QT];
+  floatx4_t acc[QT][D / 16];
+#pragma unroll
+  for (int qt = 0; qt < QT; ++qt) {
+    mrun[qt] = -INFINITY;
+    lrun[qt] = 0.0f;
+#pragma unroll
+    for (int dt = 0; dt < D / 16; ++dt) acc[qt][dt] = (floatx4_t){0.f, 0.f, 0.f, 0.f};
+  }
+
+  constexpr int WPR = D * Elem<T>::bytes / 16;
+  for (int64_t c0 = 0; c0 < M; c0 += KC) {
+    const int kc = (int)min((int64_t)KC, M - c0);
+    __syncthreads();
+    if (threadIdx.x < KC) {
+      const int64_t kk = c0 + threadIdx.x;
+      int32_t pos = -1;
+      float bias = -INFINITY;
+      if ((int)threadIdx.x < kc) {
+        if (kk < F) {
+          int k = 0;
+          while (k + 1 < nseg && kk >= s_seg_end[k]) ++k;
+          bias = bs[k].logw * sqrt_d;
+        } else {
+          const int64_t r = B.causal0 + (kk - F);
+          pos = (int32_t)r | (kept[r] ? 0 : (1 << 30));
+          bias = B.w0 * sqrt_d;
+        }
+      }
+      s_pos[threadIdx.x] = pos;
+      sB[threadIdx.x] = bias;
+    }
+    for (int w = threadIdx.x; w < KC * WPR; w += 64 * WAVES) {
+      const int key = w / WPR, wi = w % WPR;
+      uint4 kw = make_uint4(0, 0, 0, 0), vw = make_uint4(0, 0, 0, 0);
+      if (key < kc) {
+        const int64_t kk = c0 + key;
+        int64_t r;
+        if (kk < F) {
+          int k = 0;
+          while (k + 1 < nseg && kk >= s_seg_end[k]) ++k;
+          const ExpressSeg& sg = bs[k];
+          const int64_t j = kk - (k ? s_seg_end[k - 1] : 0);
+          r = sg.src ? (int64_t)sg.src[s * sg.stride + j] : sg.start + j;
+        } else {
+          r = B.causal0 + (kk - F);
+        }
+        r = r < 0 ? 0 : (r >= n ? n - 1 : r);
+        kw = reinterpret_cast<const uint4*>(Ks + r * D)[wi];
+        vw = reinterpret_cast<const uint4*>(Vs + r * D)[wi];
+      }
+      *reinterpret_cast<uint4*>(sK + key * L::k_stride + wi * 16) = kw;
+      if (BF) {
+        const uint16_t* e = reinterpret_cast<const uint16_t*>(&vw);
+#pragma unroll
+        for (int j = 0; j < 8; ++j)
+          *reinterpret_cast<uint16_t*>(sV + (wi * 8 + j) * L::v_stride + key * 2) = e[j];
+      } else {
+        *reinterpret_cast<uint4*>(sV + key * L::v_stride + wi * 16) = vw;
+      }
+    }
+    __syncthreads();
+
+    uint4 Ak[4][NV];
+#pragma unroll
+    for (int kt = 0; kt < 4; ++kt) {
+      const uint4* pk = reinterpret_cast<const uint4*>(sK + (kt * 16 + m16) * L::k_stride);
+#pragma unroll
+      for (int v = 0; v < NV; ++v) Ak[kt][v] = pk[4 * v + g];
+    }
+
+#pragma unroll
+    for (int qt = 0; qt < QT; ++qt) {
+      const int64_t p = qw + qt * 16 + m16;  // this lane's query position
+      float sc[4][4];
+      float mx = -INFINITY;
+#pragma unroll
+      for (int kt = 0; kt < 4; ++kt) {
+        floatx4_t z = {0.f, 0.f, 0.f, 0.f};
+        z = mma_rows<T, D>(Ak[kt], Bq[qt], z);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int key = kt * 16 + 4 * g + i;
+          const int32_t ps = s_pos[key];
+          const int64_t r = ps & ~(1 << 30);
+          const bool seen = ps < 0 || r == p || (!(ps & (1 << 30)) && r < p);
+          sc[kt][i] = seen ? z[i] + sB[key] : -INFINITY;
+          mx = fmaxf(mx, sc[kt][i]);
+        }
+      }
+      mx = fmaxf(mx, __shfl_xor(mx, 16));
+      mx = fmaxf(mx, __shfl_xor(mx, 32));
+      const float mnew = fmaxf(mrun[qt], mx);
+      const float scale = (mrun[qt] == -INFINITY || mnew == -INFINITY)
+                              ? 0.0f : __builtin_amdgcn_exp2f((mrun[qt] - mnew) * c2);
+      mrun[qt] = mnew;
+      float psum = 0.0f;
+      float pr[4][4];
+#pragma unroll
+      for (int kt = 0; kt < 4; ++kt)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const float pv = sc[kt][i] == -INFINITY ? 0.0f : __builtin_amdgcn_exp2f((sc[kt][i] - mnew) * c2);
+          pr[kt][i] = pv;
+          psum += pv;
+        }
+      lrun[qt] = lrun[qt] * scale + psum;
+#pragma unroll
+      for (int dt = 0; dt < D / 16; ++dt) acc[qt][dt] *= scale;
+      if (BF) {
+#pragma unroll
+        for (int c = 0; c < 2; ++c) {
+          uint16_t hb[8], lb[8];
+#pragma unroll
+          for (int j = 0; j < 8; ++j) {
+            const float pv = pr[2 * c + (j >> 2)][j & 3];
+            hb[j] = float_to_bf16(pv);
+            lb[j] = float_to_bf16(pv - bf16_to_float(hb[j]));
+          }
+          uint4 hw, lw;
+          hw.x = (uint32_t)hb[0] | ((uint32_t)hb[1] << 16);
+          hw.y = (uint32_t)hb[2] | ((uint32_t)hb[3] << 16);
+          hw.z = (uint32_t)hb[4] | ((uint32_t)hb[5] << 16);
+          hw.w = (uint32_t)hb[6] | ((uint32_t)hb[7] << 16);
+          lw.x = (uint32_t)lb[0] | ((uint32_t)lb[1] << 16);
+          lw.y = (uint32_t)lb[2] | ((uint32_t)lb[3] << 16);
+          lw.z = (uint32_t)lb[4] | ((uint32_t)lb[5] << 16);
+          lw.w = (uint32_t)lb[6] | ((uint32_t)lb[7] << 16);
+          const bf16x8_t bhi = __builtin_bit_cast(bf16x8_t, hw);
+          const bf16x8_t blo = __builtin_bit_cast(bf16x8_t, lw);
+#pragma unroll
+          for (int dt = 0; dt < D / 16; ++dt) {
+            const unsigned char* row = sV + (dt * 16 + m16) * L::v_stride;
+            uint2 lo = *reinterpret_cast<const uint2*>(row + (32 * c + 4 * g) * 2);
+            uint2 hi = *reinterpret_cast<const uint2*>(row + (32 * c + 16 + 4 * g) * 2);
+            const bf16x8_t av = __builtin_bit_cast(bf16x8_t, make_uint4(lo.x, lo.y, hi.x, hi.y));
+            acc[qt][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, bhi, acc[qt][dt], 0, 0, 0);
+            acc[qt][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, blo, acc[qt][dt], 0, 0, 0);
+          }
+        }
+      } else {
+#pragma unroll
+        for (int kt = 0; kt < 4; ++kt)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const int key = kt * 16 + 4 * g + i;
+#pragma unroll
+            for (int dt = 0; dt < D / 16; ++dt) {
+              const float av = *reinterpret_cast<const float*>(sV + key * L::v_stride + (dt * 16 + m16) * 4);
+              acc[qt][dt] = __builtin_amdgcn_mfma_f32_16x16x4f32(av, pr[kt][i], acc[qt][dt], 0, 0, 0);
+            }
+          }
+      }
+    }
+  }
+
+#pragma unroll
+  for (int qt = 0; qt < QT; ++qt) {
+    float l = lrun[qt];
+    l += __shfl_xor(l, 16);
+    l += __shfl_xor(l, 32);
+    const float inv = 1.0f / l;
+    const int64_t q = qw + qt * 16 + m16;
+    if (q < q1) {
+      TO* orow = O + (s * n + q) * D;
+#pragma unroll
+      for (int dt = 0; dt < D / 16; ++dt)
+        store4<TO>(orow + dt * 16 + 4 * g, acc[qt][dt][0] * inv, acc[qt][dt][1] * inv,
+                   acc[qt][dt][2] * inv, acc[qt][dt][3] * inv);
+    }
+  }
+}
+
+template <typename T, int D, typename TO>
+hipError_t launch_prefill_t(const void* Q, const void* K, const void* V, int64_t S, int64_t n,
+                            const PrefillTile* tiles, int64_t ntiles, const PrefillBlock* blocks,
+                            const ExpressSeg* segs, const uint8_t* kept, void* O,
+                            hipStream_t st) {
+  dim3 grid((unsigned)ntiles, (unsigned)S), block(64 * WAVES);
+  hipLaunchKernelGGL((prefill_attn_kernel<T, D, TO>), grid, block, 0, st, (const T*)Q,
+                     (const T*)K, (const T*)V, n, tiles, blocks, segs, kept, (TO*)O);
+  return hipGetLastError();
+}
+
+template <typename T, typename TO>
+hipError_t launch_prefill_d(int64_t d, const void* Q, const void* K, const void* V, int64_t S,
+                            int64_t n, const PrefillTile* tiles, int64_t ntiles,
+                            const PrefillBlock* blocks, const ExpressSeg* segs,
+                            const uint8_t* kept, void* O, hipStream_t st) {
+  switch (d) {
+    case 32: return launch_prefill_t<T, 32, TO>(Q, K, V, S, n, tiles, ntiles, blocks, segs, kept, O, st);
+    case 64: return launch_prefill_t<T, 64, TO>(Q, K, V, S, n, tiles, ntiles, blocks, segs, kept, O, st);
+    case 128: return launch_prefill_t<T, 128, TO>(Q, K, V, S, n, tiles, ntiles, blocks, segs, kept, O, st);
+    default: return hipErrorInvalidValue;
+  }
+}
+
 template <typename T, int D, typename TO>
 hipError_t launch_attn_t(const void* Q, const void* K, const void* V, const int32_t* idx,
                          const float* logw, int64_t S, int64_t n, int64_t n_q, int64_t n_out,
@@ -597,6 +846,21 @@ hipError_t launch_attn_d(int64_t d, const void* Q, const void* K, const void* V,
 }
 
 }  // namespace
+
+hipError_t launch_prefill_attention(int dtype, int64_t d, int out_dtype, const void* Q,
+                                    const void* K, const void* V, int64_t S, int64_t n,
+                                    const PrefillTile* tiles, int64_t ntiles,
+                                    const PrefillBlock* blocks, const ExpressSeg* segs,
+                                    const uint8_t* kept, void* O, hipStream_t st) {
+  if (ntiles < 1) return hipSuccess;
+  if (dtype == 0)
+    return out_dtype == 0
+               ? launch_prefill_d<float, float>(d, Q, K, V, S, n, tiles, ntiles, blocks, segs, kept, O, st)
+               : launch_prefill_d<float, bf16_t>(d, Q, K, V, S, n, tiles, ntiles, blocks, segs, kept, O, st);
+  return out_dtype == 0
+             ? launch_prefill_d<bf16_t, float>(d, Q, K, V, S, n, tiles, ntiles, blocks, segs, kept, O, st)
+             : launch_prefill_d<bf16_t, bf16_t>(d, Q, K, V, S, n, tiles, ntiles, blocks, segs, kept, O, st);
+}
 
 hipError_t launch_attention(int dtype, int64_t d, int out_dtype, const void* Q, const void* K,
                             const void* V, const int32_t* idx, const float* logw, int64_t S,

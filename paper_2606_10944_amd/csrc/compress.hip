@@ -17,6 +17,18 @@ constexpr double kLog2e = 1.44269504088896340736;
 // pair's own diagonal exponent only for data far outside attention ranges.
 constexpr float kExpClamp = 64.0f;
 
+// Row strides of the index lists (0 = packed: n_r in, n_r / 2 out) and the
+// first uniform of bucket t's P pairs within its slice.
+__device__ __forceinline__ int64_t in_stride(const HalveArgs& a) {
+  return a.in_stride ? a.in_stride : a.n_r;
+}
+__device__ __forceinline__ int64_t out_stride(const HalveArgs& a) {
+  return a.out_stride ? a.out_stride : (a.n_r >> 1);
+}
+__device__ __forceinline__ int64_t bucket_u(const HalveArgs& a, int64_t t, int P) {
+  return a.u_bucket ? a.u_bucket[t] : a.u_off + t * (int64_t)P;
+}
+
 __device__ __forceinline__ float wave_max_f(float v) {
 #pragma unroll
   for (int off = 32; off >= 1; off >>= 1) v = fmaxf(v, __shfl_xor(v, off));
@@ -562,9 +574,9 @@ void pair_scores_kernel(HalveArgs a) {
 
   const T* K = reinterpret_cast<const T*>(a.K) + s * a.ld * D;
   const T* V = reinterpret_cast<const T*>(a.V) + s * a.ld * D;
-  const int32_t* rows_in = a.idx_in ? a.idx_in + s * a.n_r + t * (int64_t)N : nullptr;
+  const int32_t* rows_in = a.idx_in ? a.idx_in + s * in_stride(a) + t * (int64_t)N : nullptr;
   const int64_t row_base = t * (int64_t)N;
-  const float vmax = __uint_as_float(a.vmax_bits[s]);
+  const float vmax = __uint_as_float(a.vmax_bits[a.vmax_per_bucket ? bucket : s]);
   const float vm2f = vmax * vmax;
   const double vm2d = (double)vmax * (double)vmax;
   const double inv_sqrt_d = 1.0 / sqrt((double)D);
@@ -857,9 +869,9 @@ void pair_scores_kernel(HalveArgs a) {
   // float64 (the order of the separate pass); then decide_block.
   auto local_decisions = [&]() {
     const int nblk = (P + 31) / 32;
-    const float* Ub = a.U + s * a.u_slice + a.u_off + t * (int64_t)P;
-    uint8_t* trace = a.trace ? a.trace + s * a.u_slice + a.u_off + t * (int64_t)P : nullptr;
-    int32_t* out = a.idx_out + s * (a.n_r >> 1) + t * (int64_t)P;
+    const float* Ub = a.U + s * a.u_slice + bucket_u(a, t, P);
+    uint8_t* trace = a.trace ? a.trace + s * a.u_slice + bucket_u(a, t, P) : nullptr;
+    int32_t* out = a.idx_out + s * out_stride(a) + t * (int64_t)P;
     const int pl = lane & 31;
     double carry = -INFINITY;
     uint32_t masks[NBW];
@@ -1062,11 +1074,11 @@ __global__ __launch_bounds__(64 * (BW + 2)) void halve_pass_kernel(HalveArgs a) 
   const int P = N >> 1;
   const int NT = (N + 15) >> 4;
   const int nblk = (P + BP - 1) / BP;
-  const int32_t* rows_in = a.idx_in ? a.idx_in + s * a.n_r + t * (int64_t)N : nullptr;
+  const int32_t* rows_in = a.idx_in ? a.idx_in + s * in_stride(a) + t * (int64_t)N : nullptr;
   const int64_t row_base = t * (int64_t)N;
-  const float* Ub = a.U + s * a.u_slice + a.u_off + t * (int64_t)P;
-  uint8_t* trace = a.trace ? a.trace + s * a.u_slice + a.u_off + t * (int64_t)P : nullptr;
-  int32_t* out = a.idx_out + s * (a.n_r >> 1) + t * (int64_t)P;
+  const float* Ub = a.U + s * a.u_slice + bucket_u(a, t, P);
+  uint8_t* trace = a.trace ? a.trace + s * a.u_slice + bucket_u(a, t, P) : nullptr;
+  int32_t* out = a.idx_out + s * out_stride(a) + t * (int64_t)P;
   const int64_t pb = s * (a.n_r >> 1) + t * (int64_t)P;
   const float* Eb = a.E + bl * a.e_tiles * (int64_t)TILE;
   // a valid address for the row loads of round 0 (their values are replaced)
@@ -1537,27 +1549,33 @@ hipError_t launch_assemble(int64_t S, int64_t n, int64_t ns, int64_t n_out, int6
 // idx_in[2p] (idx_in null = the identity).  The pairs of a round are
 // consecutive in the slice's current order, bucket after bucket, as are
 // their draws, so the buckets need no separate treatment.
+// With u_bucket, bucket t (N rows, N/2 pairs) draws from u_bucket[t] on; the
+// lists are in_stride / out_stride apart per slice (0: packed).
 __global__ void uniform_halve_kernel(int64_t n_r, const int32_t* idx_in, const float* U,
                                      int64_t u_slice, int64_t u_off, int32_t* idx_out,
-                                     uint8_t* trace) {
+                                     uint8_t* trace, int64_t N, const int64_t* u_bucket,
+                                     int64_t in_stride, int64_t out_stride) {
   const int64_t s = blockIdx.y;
   const int64_t p = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   const int64_t P = n_r >> 1;
   if (p >= P) return;
-  const int64_t ui = s * u_slice + u_off + p;
+  const int64_t ui =
+      s * u_slice + (u_bucket ? u_bucket[p / (N >> 1)] + p % (N >> 1) : u_off + p);
   const int swap = U[ui] < 0.5f;
   const int64_t j = 2 * p + swap;
-  idx_out[s * P + p] = idx_in ? idx_in[s * n_r + j] : (int32_t)j;
+  idx_out[s * (out_stride ? out_stride : P) + p] =
+      idx_in ? idx_in[s * (in_stride ? in_stride : n_r) + j] : (int32_t)j;
   if (trace) trace[ui] = (uint8_t)swap;
 }
 
 hipError_t launch_uniform_halve(int64_t S, int64_t n_r, const int32_t* idx_in, const float* U,
                                 int64_t u_slice, int64_t u_off, int32_t* idx_out,
-                                uint8_t* trace, hipStream_t st) {
+                                uint8_t* trace, hipStream_t st, int64_t N,
+                                const int64_t* u_bucket, int64_t in_stride, int64_t out_stride) {
   const int64_t P = n_r / 2;
   dim3 grid((unsigned)((P + 255) / 256), (unsigned)S);
   hipLaunchKernelGGL(uniform_halve_kernel, grid, dim3(256), 0, st, n_r, idx_in, U, u_slice,
-                     u_off, idx_out, trace);
+                     u_off, idx_out, trace, N > 0 ? N : n_r, u_bucket, in_stride, out_stride);
   return hipGetLastError();
 }
 

@@ -23,19 +23,22 @@ __global__ void rows_copy_kernel(const int32_t* src, int64_t src_stride, int32_t
   if (j < len) dst[s * dst_stride + j] = src[s * src_stride + j];
 }
 
-// v_max of one Halve call (eq. katt over the rows it thins): the largest
-// |V[s, idx[s, j], c]| over its N rows, as the float's bit pattern.  One
-// workgroup per slice; a row is d * bytes / 16 16-byte words.
+// v_max of a Halve call (eq. katt over the rows it thins): the largest
+// |V[s, row, c]| over its N rows idx[s * in_stride + t * N + j], as the
+// float's bit pattern at vmax_bits[s * G + t].  One workgroup per call (G
+// calls per slice); a row is d * bytes / 16 16-byte words.
 template <typename T>
 __global__ __launch_bounds__(256) void vmax_rows_kernel(const T* V, int64_t ld, int64_t d,
-                                                        const int32_t* idx, int64_t N,
+                                                        const int32_t* idx, int64_t in_stride,
+                                                        int64_t N, int64_t G,
                                                         uint32_t* vmax_bits) {
-  const int64_t s = blockIdx.x;
+  const int64_t s = blockIdx.x / G, t = blockIdx.x % G;
   const int64_t wpr = d * Elem<T>::bytes / 16;
   const u32x4* base = reinterpret_cast<const u32x4*>(V + s * ld * d);
+  const int32_t* rows = idx + s * in_stride + t * N;
   uint32_t m = 0u;
   for (int64_t w = threadIdx.x; w < N * wpr; w += blockDim.x) {
-    const int64_t row = idx[s * N + w / wpr];
+    const int64_t row = rows[w / wpr];
     const u32x4 x = base[row * wpr + w % wpr];
 #pragma unroll
     for (int c = 0; c < 4; ++c) {
@@ -53,7 +56,7 @@ __global__ __launch_bounds__(256) void vmax_rows_kernel(const T* V, int64_t ld, 
   if (lane == 0) part[wave] = mf;
   __syncthreads();
   if (threadIdx.x == 0)
-    vmax_bits[s] = __float_as_uint(fmaxf(fmaxf(part[0], part[1]), fmaxf(part[2], part[3])));
+    vmax_bits[blockIdx.x] = __float_as_uint(fmaxf(fmaxf(part[0], part[1]), fmaxf(part[2], part[3])));
 }
 
 // Key j of slice s: the segment k with off_k <= j < off_k + len_k gives
@@ -311,13 +314,15 @@ hipError_t launch_rows_copy(const int32_t* src, int64_t src_stride, int32_t* dst
 }
 
 hipError_t launch_vmax_rows(int dtype, const void* V, int64_t ld, int64_t d, const int32_t* idx,
-                            int64_t N, int64_t S, uint32_t* vmax_bits, hipStream_t st) {
+                            int64_t in_stride, int64_t N, int64_t G, int64_t S,
+                            uint32_t* vmax_bits, hipStream_t st) {
+  const dim3 grid((unsigned)(S * G));
   if (dtype == 0)
-    hipLaunchKernelGGL(vmax_rows_kernel<float>, dim3((unsigned)S), dim3(256), 0, st,
-                       (const float*)V, ld, d, idx, N, vmax_bits);
+    hipLaunchKernelGGL(vmax_rows_kernel<float>, grid, dim3(256), 0, st, (const float*)V, ld, d,
+                       idx, in_stride, N, G, vmax_bits);
   else
-    hipLaunchKernelGGL(vmax_rows_kernel<bf16_t>, dim3((unsigned)S), dim3(256), 0, st,
-                       (const bf16_t*)V, ld, d, idx, N, vmax_bits);
+    hipLaunchKernelGGL(vmax_rows_kernel<bf16_t>, grid, dim3(256), 0, st, (const bf16_t*)V, ld, d,
+                       idx, in_stride, N, G, vmax_bits);
   return hipGetLastError();
 }
 

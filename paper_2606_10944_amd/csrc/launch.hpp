@@ -38,6 +38,11 @@ struct HalveArgs {
   int64_t nbk;                // buckets of a score launch (set by launch_scores)
   int32_t ipb;                // score workgroups per bucket in a launch (set by launch_scores)
   int32_t il;                 // buckets interleaved per XCD in a score launch (set by launch_scores)
+  // Optional (zero / null: the packed layout above)
+  const int64_t* u_bucket;    // [G] first uniform of bucket t within its slice (else u_off + t*N/2)
+  int32_t vmax_per_bucket;    // vmax_bits indexed by bucket (s * G + t) instead of slice
+  int64_t in_stride;          // idx_in row stride per slice (0: n_r)
+  int64_t out_stride;         // idx_out row stride per slice (0: n_r / 2)
 };
 
 // dtype: 0 = fp32, 1 = bf16.  Returns a hipError_t.
@@ -58,7 +63,9 @@ hipError_t launch_assemble(int64_t S, int64_t n, int64_t ns, int64_t n_out, int6
 // 2p+1 of the round's input iff its uniform is below 1/2.
 hipError_t launch_uniform_halve(int64_t S, int64_t n_r, const int32_t* idx_in, const float* U,
                                 int64_t u_slice, int64_t u_off, int32_t* idx_out,
-                                uint8_t* trace, hipStream_t st);
+                                uint8_t* trace, hipStream_t st, int64_t N = 0,
+                                const int64_t* u_bucket = nullptr, int64_t in_stride = 0,
+                                int64_t out_stride = 0);
 // Every round of uniform halving in one launch (one workgroup per slice,
 // indices in LDS); only for n_kept <= 32768 (uniform_fused_ok).
 bool uniform_fused_ok(int64_t n_kept);
@@ -94,9 +101,11 @@ struct ExpressSegs {
 };
 hipError_t launch_rows_copy(const int32_t* src, int64_t src_stride, int32_t* dst,
                             int64_t dst_stride, int64_t len, int64_t S, hipStream_t st);
-// v_max bits per slice over the rows idx[s, 0..N) of V (slices ld rows apart).
+// v_max bits of G calls per slice, call t over the rows idx[s * in_stride +
+// t * N + 0..N) of V (slices ld rows apart), into vmax_bits[s * G + t].
 hipError_t launch_vmax_rows(int dtype, const void* V, int64_t ld, int64_t d, const int32_t* idx,
-                            int64_t N, int64_t S, uint32_t* vmax_bits, hipStream_t st);
+                            int64_t in_stride, int64_t N, int64_t G, int64_t S,
+                            uint32_t* vmax_bits, hipStream_t st);
 // idx / logw [S, out_stride]: the segments laid out one after another in the
 // first m entries of each slice (their lengths sum to m).
 hipError_t launch_express_keys(const ExpressSegs& segs, int64_t S, int64_t m, int64_t out_stride,
@@ -115,6 +124,22 @@ hipError_t launch_decode_attention(int dtype, int64_t d, int out_dtype, const vo
                                    int32_t* app, int64_t app_stride, int32_t app_val,
                                    hipStream_t st);
 
+
+// Masked prefill over the Express cache: a block of queries [q0, q1) sees the
+// segments [seg0, seg0 + nseg) (at most 32) and the causal candidates
+// causal0 .. q1-1 with log-weight w0; a tile is up to 128 queries of a block.
+struct PrefillBlock {
+  int32_t q0, q1, causal0, seg0, nseg;
+  float w0;
+};
+struct PrefillTile {
+  int32_t blk, q0;
+};
+hipError_t launch_prefill_attention(int dtype, int64_t d, int out_dtype, const void* Q,
+                                    const void* K, const void* V, int64_t S, int64_t n,
+                                    const PrefillTile* tiles, int64_t ntiles,
+                                    const PrefillBlock* blocks, const ExpressSeg* segs,
+                                    const uint8_t* kept, void* O, hipStream_t st);
 
 // logw (nullable) [S, n_out]: log-weight of every coreset key.
 hipError_t launch_attention(int dtype, int64_t d, int out_dtype, const void* Q, const void* K,

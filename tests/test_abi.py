@@ -228,3 +228,18 @@ def test_express_rejects_unsupported_sizes():
                                  C.byref(h)) == _lib.THIN_EWORKSPACE
     assert L.thin_express_create(1, 1, 1, 64, 8, 4, 0.5, 0, 512, C.c_void_p(0x100010), 1 << 30,
                                  C.byref(h)) == _lib.THIN_EWORKSPACE  # not 256-byte aligned
+
+
+@pytest.mark.parametrize("n_out,mbar,n", [(8, 4, 512), (8, 2, 1500), (128, 5, 9000), (16, 4, 1000)])
+def test_prefill_plan_matches_decoding(n_out, mbar, n):
+    p = _lib.thin_express_prefill_plan(1, 2, n, 64, n_out, mbar)
+    assert p["uniforms_per_slice"] == oracle.express_uniforms(n, n_out, mbar)
+    assert p["subsample_draws"] == oracle.express_draws(n, n_out, mbar)
+    assert p["workspace_bytes"] > 0
+    L = _lib.lib()
+    assert L.thin_express_prefill(1, 1, 2, n, 64, n_out, mbar, 0.5, 0, FAKE, FAKE, FAKE, FAKE,
+                                  1 << 30, None, 0, FAKE, 0, None, 0, None, None) in (
+        _lib.THIN_EWORKSPACE, _lib.THIN_EINVAL)
+    assert L.thin_express_prefill(1, 1, 2, n, 64, n_out, mbar, 1.5, 0, FAKE, FAKE, FAKE, FAKE,
+                                  1 << 30, None, 0, FAKE, 0, FAKE, 1 << 40, None, None) == \
+        _lib.THIN_EINVAL

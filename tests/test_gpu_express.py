@@ -8,7 +8,7 @@ import pytest
 import torch
 
 import oracle
-from paper_2606_10944_amd import ExpressCache, thin_express_plan
+from paper_2606_10944_amd import ExpressCache, thin_express_plan, thin_express_prefill
 from paper_2606_10944_amd import workloads as W
 
 pytestmark = pytest.mark.gpu
@@ -74,3 +74,35 @@ def test_express_decode_parity(c):
         err = np.abs(r["O"] - O[b, h]).max()
         assert err <= tol, (s, err)
     print(f"near ties {near}")
+
+
+@pytest.mark.parametrize("c", CASES, ids=lambda c: f"o{c['n_out']}-mbar{c['mbar']}-n{c['n']}-d{c['d']}-{c['dtype']}-{c['halve']}")
+def test_express_prefill_parity(c):
+    """Masked prefill: every point's output equals Thinformer decoding's (the
+    oracle, following the prefill's own KH decisions at near ties)."""
+    w = W.custom("ex", B=c["B"], H=c["H"], n=c["n"], d=c["d"], dtype=c["dtype"], kind="gauss")
+    Q, K, V = W.make_qkv(w)
+    plan = thin_express_plan(w.B, w.H, w.d, c["n_out"], c["mbar"], w.n)
+    us = plan["uniforms_per_slice"]
+    U = W.make_uniforms(w, w.S * us)
+    draws = torch.from_numpy(np.random.default_rng(7).random(
+        max(plan["subsample_draws"], 1)).astype(np.float32))
+    tr = torch.zeros(max(U.numel(), 1), dtype=torch.uint8, device=DEV)
+    O = thin_express_prefill(Q.to(DEV), K.to(DEV), V.to(DEV), c["n_out"], c["mbar"], U.to(DEV),
+                             draws=draws, halve=c["halve"], trace=tr)
+    torch.cuda.synchronize()
+    O, tr = O.cpu().numpy(), tr.cpu().numpy()
+    Us = U.numpy().reshape(w.S, -1) if us else np.zeros((w.S, 1), np.float32)
+    ts = tr[: w.S * us].reshape(w.S, -1) if us else np.zeros((w.S, 1), np.uint8)
+    tol = 2e-3 if c["dtype"] == "bf16" else 1e-5
+    for s in range(w.S):
+        b, h = divmod(s, w.H)
+        r = oracle.express_decode(Q[b, h], K[b, h], V[b, h], c["n_out"], c["mbar"], Us[s],
+                                  halve=c["halve"], follow=ts[s] if c["halve"] == "kh" else None,
+                                  tol=MARGIN, sub_u=draws.numpy())
+        assert r["stats"]["hard_mismatch"] == 0, (s, r["stats"])
+        if c["halve"] == "uniform":
+            assert np.array_equal(r["bits"], ts[s]), s
+        err = np.abs(r["O"] - O[b, h]).max(axis=-1)
+        bad = np.nonzero(err > tol)[0]
+        assert bad.size == 0, (s, bad[:10], err[bad[:10]])

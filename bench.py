@@ -20,6 +20,10 @@ the S + n_out + W weighted keys (eq. def:att_approx).
 the decoding experiments' choice: Subsample runs from point 8192 on), 16384
 points decoded one at a time (each attends over the cache plus itself, then
 enters it); one step = one point of every slice.
+
+--mode prefill measures the masked prefill over the Express cache (every
+point's Thinformer output at once): B=1, H=32, d=128, bf16, 65536 points,
+n_out=256 (h = 8), mbar=6 (h - 2); one step = one whole prefill.
 """
 import argparse
 import collections
@@ -292,6 +296,90 @@ def decode_main(args):
     print(json.dumps(out), flush=True)
 
 
+PREFILL = dict(B=1, H=32, d=128, dtype="bf16", n_out=256, mbar=6, n=65536)
+
+
+def prefill_main(args):
+    """Masked prefill over the Express cache (one JSON line)."""
+    import numpy as np
+    import torch
+
+    from paper_2606_10944_amd import LaunchTimer, thin_express_prefill, thin_express_prefill_plan
+    from paper_2606_10944_amd import workloads as W
+    c = PREFILL
+    w = W.custom("prefill", B=c["B"], H=c["H"], n=c["n"], d=c["d"], dtype=c["dtype"],
+                 kind="heavy_tail")
+    Q, K, V = W.make_qkv(w)
+    plan = thin_express_prefill_plan(w.B, w.H, w.n, w.d, c["n_out"], c["mbar"])
+    U = W.make_uniforms(w, w.S * plan["uniforms_per_slice"])
+    draws = torch.from_numpy(np.random.default_rng(w.seed + 1).random(
+        max(plan["subsample_draws"], 1)).astype(np.float32))
+    dev = torch.device("cuda:0")
+    Qd, Kd, Vd, Ud = Q.to(dev), K.to(dev), V.to(dev), U.to(dev)
+    ws = torch.empty(plan["workspace_bytes"], dtype=torch.uint8, device=dev)
+    O = torch.empty((w.B, w.H, w.n, w.d), dtype=torch.float32, device=dev)
+    stream = torch.cuda.current_stream()
+
+    def step():
+        thin_express_prefill(Qd, Kd, Vd, c["n_out"], c["mbar"], Ud, draws=draws, O=O,
+                             workspace=ws, stream=stream)
+
+    steps, warm = max(args.steps // 4, 3), max(args.warmup // 20, 2)
+    for _ in range(warm):
+        step()
+    torch.cuda.synchronize()
+    t0 = torch.cuda.Event(enable_timing=True)
+    t1 = torch.cuda.Event(enable_timing=True)
+    t0.record(stream)
+    for _ in range(steps):
+        step()
+    t1.record(stream)
+    torch.cuda.synchronize()
+    ms = t0.elapsed_time(t1) / steps
+    with LaunchTimer(stream) as lt:
+        step()
+        torch.cuda.synchronize()
+    per = collections.defaultdict(float)
+    for name, _, t in lt.records():
+        per[name] += t
+    att_ms = per["attention"]
+    kb = elem_bytes(w.dtype)
+    att_bytes = w.S * (plan["staged_keys"] * 2 * w.d * kb + w.n * w.d * (kb + 4))
+    att_flops = 4 * w.d * plan["attention_keys"] * w.S
+    gbs = att_bytes / (att_ms * 1e-3) / 1e9
+    tfl = att_flops / (att_ms * 1e-3) / 1e12
+    out = {
+        "metric": "masked prefill over the Express cache: points/s over B·H slices",
+        "value": w.S * w.n / (ms * 1e-3), "unit": "points/s", "n_gpus": 1, "steps": steps,
+        "warmup": warm, "ms_per_step": ms, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": w.dtype, "data": "synthetic",
+        "config": {"workload": "express-prefill", "B": w.B, "H": w.H, "n": w.n, "d": w.d,
+                   "n_out": c["n_out"], "mbar": c["mbar"], "delta": 0.5, "halve": "kh"},
+        "roofline": {
+            "kernel": "prefill_attn_kernel (block-causal weighted attention of every point)",
+            "bound": "hbm", "achieved": gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+            "frac": gbs / HBM_PEAK_GBS, "traffic": None, "algorithmic_bytes_per_launch": att_bytes,
+            "ms_per_launch": att_ms, "mfma_tflops": tfl,
+            "mfma_frac": tfl / BF16_MFMA_PEAK_TFLOPS,
+            "keys_per_point": plan["attention_keys"] / w.n},
+        "ms_by_kernel": dict(per),
+        "gpu": torch.cuda.get_device_name(0),
+    }
+    if not args.no_cpu_baseline:
+        import oracle
+        oracle.lib()
+        Us = U.numpy().reshape(w.S, -1)
+        t_a = time.perf_counter()
+        oracle.express_decode(Q[0, 0], K[0, 0], V[0, 0], c["n_out"], c["mbar"], Us[0],
+                              sub_u=draws.numpy())
+        t_used = time.perf_counter() - t_a
+        out["cpu_baseline"] = {
+            "value": w.n / t_used, "unit": "points/s", "cores": 1, "kind": "oracle",
+            "sample": f"1 of {w.S} slices, all {w.n} points, float64, one thread, "
+                      f"{t_used:.1f} s"}
+    print(json.dumps(out), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -306,8 +394,8 @@ def main():
                     help="keys kept exactly at the start of every slice")
     ap.add_argument("--window", type=int, default=0,
                     help="keys kept exactly at the end of every slice")
-    ap.add_argument("--mode", choices=["compress", "decode"], default="compress",
-                    help="compress + attention (default) or Express decoding")
+    ap.add_argument("--mode", choices=["compress", "decode", "prefill"], default="compress",
+                    help="compress + attention (default), Express decoding or masked prefill")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: the thinning path runs each (batch, head) "
@@ -315,6 +403,9 @@ def main():
         sys.exit(2)
     if args.mode == "decode":
         decode_main(args)
+        return
+    if args.mode == "prefill":
+        prefill_main(args)
         return
 
     import torch

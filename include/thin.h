@@ -313,6 +313,10 @@ typedef struct {
   int64_t uniforms_per_slice; /* as thin_express_plan for n points          */
   int64_t subsample_draws;    /* Subsample draws the n points need          */
   size_t workspace_bytes;     /* device workspace of thin_express_prefill   */
+  int64_t attention_keys;     /* per slice: keys summed over the points
+                                 (Subsample draws of 0)                     */
+  int64_t staged_keys;        /* per slice: keys the attention launch
+                                 gathers, summed over its 128-point tiles   */
 } thin_prefill_plan_t;
 
 /* Host-only. */

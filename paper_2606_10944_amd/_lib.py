@@ -49,7 +49,8 @@ class ExpressPlan(C.Structure):
 
 class PrefillPlan(C.Structure):
     _fields_ = [("uniforms_per_slice", C.c_int64), ("subsample_draws", C.c_int64),
-                ("workspace_bytes", C.c_size_t)]
+                ("workspace_bytes", C.c_size_t), ("attention_keys", C.c_int64),
+                ("staged_keys", C.c_int64)]
 
 
 class CompressOpts(C.Structure):

@@ -701,9 +701,16 @@ struct PfLayout {
   std::vector<std::vector<size_t>> region;     // [m/2][depth] node store of the calls
   std::vector<std::vector<int64_t>> rstride;   // [m/2][depth] its row stride per slice
   std::vector<size_t> enode;                   // [m/2] E after the Halve phase of level m - 2
-  size_t kept, keptrow, keptflag, hp, ein, vmax, lbt, h2, rowh2, score, utab, blocks, tiles, segs;
+  size_t kept, keptrow, keptflag, hp, ein, vmax, lbt, h2, rowh2, score, utab, tiles, segs, c0, w0;
   size_t e_bytes, bytes;
-  int64_t max_blocks, max_tiles, max_segs, max_utab;
+  int64_t max_tiles, max_segs, max_utab;
+};
+
+// A run of points attending over one cache (host only): the segments
+// [seg0, seg0 + nseg) and C_0 from causal0 with log-weight w0.
+struct PfBlock {
+  int32_t q0, q1, causal0, seg0, nseg;
+  float w0;
 };
 
 int64_t group_T(int64_t n_out, int mp, int i) { return (n_out << (i + 2)) >> mp; }
@@ -755,16 +762,16 @@ PfLayout pf_layout(int64_t S, int64_t n_out, int32_t mbar, int64_t n, const Expr
   const size_t all = (size_t)S * per, capb = per > kScoreCap ? per : kScoreCap;
   L.e_bytes = all < capb ? all : capb;
   L.score = take(L.e_bytes);
-  // host-built tables: uniform offsets, blocks (at most one per point),
-  // tiles (a block's points in runs of 128) and block segments
+  // host-built tables: uniform offsets, tiles of 128 points, their cache
+  // pieces, and every point's C_0 start and log-weight
   L.max_utab = std::max<int64_t>(ucount, 1);
-  L.max_blocks = n + 1;
-  L.max_tiles = n + n / 128 + 2;
-  L.max_segs = (n + 1) * (int64_t)(mbar + 3);
+  L.max_tiles = n / 128 + 2;
+  L.max_segs = L.max_tiles * thin::kPrefillMaxSegs;
   L.utab = take(8 * (size_t)L.max_utab);
-  L.blocks = take(sizeof(thin::PrefillBlock) * (size_t)L.max_blocks);
   L.tiles = take(sizeof(thin::PrefillTile) * (size_t)L.max_tiles);
-  L.segs = take(sizeof(thin::ExpressSeg) * (size_t)L.max_segs);
+  L.segs = take(sizeof(thin::PrefillSeg) * (size_t)L.max_segs);
+  L.c0 = take(4 * (size_t)n);
+  L.w0 = take(4 * (size_t)n);
   L.bytes = off;
   return L;
 }
@@ -776,9 +783,15 @@ struct PfHost {
   std::vector<int32_t> keptrow;
   std::vector<uint8_t> keptflag;
   std::vector<int64_t> kept_base;  // [m/2]: kept-list index of level m's first point
-  std::vector<thin::PrefillBlock> blocks;
-  std::vector<thin::PrefillTile> tiles;
+  std::vector<PfBlock> blocks;
   std::vector<thin::ExpressSeg> segs;
+  std::vector<int64_t> piece;  // per segment: the size of its pieces (a call's output, n_out)
+  std::vector<thin::PrefillTile> tiles;
+  std::vector<thin::PrefillSeg> psegs;
+  std::vector<int32_t> c0;
+  std::vector<float> w0;
+  int64_t query_keys = 0;   // sum over points of the keys each attends over
+  int64_t staged_keys = 0;  // sum over 128-point tiles of the keys each stages
 };
 
 int pf_run(int64_t n_out, int32_t mbar, int64_t n, const float* draws, int64_t n_draws,
@@ -794,17 +807,22 @@ int pf_run(int64_t n_out, int32_t mbar, int64_t n, const float* draws, int64_t n
   int64_t causal0 = 0;
   std::vector<int64_t> sig, last;
   const float ln2 = (float)log(2.0);
-  auto dev = [&](size_t off) { return reinterpret_cast<int32_t*>(ws + off); };
+  // without a layout the segments carry no addresses (sizes only)
+  auto dev = [&](size_t off) { return L ? reinterpret_cast<int32_t*>(ws + off) : nullptr; };
+  auto reg = [&](int lv, int i) -> size_t { return L ? L->region[lv][i] : 0; };
+  auto rst = [&](int lv, int i) -> int64_t { return L ? L->rstride[lv][i] : 0; };
+  auto eno = [&](int lv) -> size_t { return L ? L->enode[lv] : 0; };
+  const size_t kept_off = L ? L->kept : 0;
   for (int64_t p = 0; p < n; ++p) {
     if (x.n >= n_out && x.over) return THIN_EINVAL;
     while ((int64_t)h->kept_base.size() <= x.m / 2) h->kept_base.push_back((int64_t)h->keptrow.size());
-    if (L) {
+    {
       // the cache point p attends over: E (its exact part once complete),
       // C_1..C_mp (outputs of their calls), and C_0 plus p as the causal run
       sig.assign({x.m, x.n >= n_out ? x.nE : -1, causal0});
       for (int i = 1; i <= x.mp; ++i) sig.push_back(x.nC[i]);
       if (p == 0 || sig != last) {
-        thin::PrefillBlock b{};
+        PfBlock b{};
         b.q0 = (int32_t)p;
         b.causal0 = (int32_t)causal0;
         b.seg0 = (int32_t)h->segs.size();
@@ -812,27 +830,36 @@ int pf_run(int64_t n_out, int32_t mbar, int64_t n, const float* draws, int64_t n
         const int lv = x.m / 2;
         if (x.n >= n_out) {
           if (x.m == 0) {
-            h->segs.push_back({dev(L->kept), n, 0, x.nE, 0.0f});
+            h->segs.push_back({dev(kept_off), n, 0, x.nE, 0.0f});
+            h->piece.push_back(n_out);
           } else {
-            h->segs.push_back({dev(L->enode[lv]), n_out, 0, n_out, 0.0f});
+            h->segs.push_back({dev(eno(lv)), n_out, 0, n_out, 0.0f});
+            h->piece.push_back(n_out);
             const int64_t gdone = (x.nE - n_out) / n_out;
-            if (gdone > 0)
-              h->segs.push_back({dev(L->region[lv][x.mp - 1]), L->rstride[lv][x.mp - 1], 0,
-                                 gdone * n_out, 0.0f});
+            if (gdone > 0) {
+              h->segs.push_back({dev(reg(lv, x.mp - 1)), rst(lv, x.mp - 1), 0, gdone * n_out,
+                                 0.0f});
+              h->piece.push_back(n_out);
+            }
           }
         }
         for (int i = 1; i <= x.mp; ++i) {
           if (x.nC[i] == 0) continue;
           const int64_t half = group_T(n_out, x.mp, i - 1) / 2;
           const int64_t first = h->rec.count(x.m, i - 1) - x.nC[i] / half;
-          h->segs.push_back({dev(L->region[lv][i - 1]) + first * half, L->rstride[lv][i - 1], 0,
-                             x.nC[i], (float)(i - x.mp) * ln2});
+          int32_t* base = dev(reg(lv, i - 1));
+          h->segs.push_back({base ? base + first * half : nullptr, rst(lv, i - 1), 0, x.nC[i],
+                             (float)(i - x.mp) * ln2});
+          h->piece.push_back(half);
         }
         b.nseg = (int32_t)h->segs.size() - b.seg0;
         if (!h->blocks.empty()) h->blocks.back().q1 = (int32_t)p;
         h->blocks.push_back(b);
         last = sig;
       }
+      int64_t fixed = 0;
+      for (int k = h->blocks.back().seg0; k < (int)h->segs.size(); ++k) fixed += h->segs[k].len;
+      h->query_keys += fixed + (x.n >= n_out ? x.nC[0] : x.n) + 1;
     }
     // Subsample, then the update
     const bool thin_phase = x.n >= n_out;
@@ -848,22 +875,60 @@ int pf_run(int64_t n_out, int32_t mbar, int64_t n, const float* draws, int64_t n
     else if (x.n > n_out && (h->rec.count(m_before, 0) != c0 || x.ell == 0))
       causal0 = p + 1;  // C_0 emptied: by Halve_0 or at the end of a group
   }
-  if (L) {
-    if (!h->blocks.empty()) h->blocks.back().q1 = (int32_t)n;
-    for (int64_t k = 0; k < (int64_t)h->blocks.size(); ++k)
-      for (int32_t q = h->blocks[k].q0; q < h->blocks[k].q1; q += 128)
-        h->tiles.push_back({(int32_t)k, q});
-    if ((int64_t)h->blocks.size() > L->max_blocks || (int64_t)h->tiles.size() > L->max_tiles ||
-        (int64_t)h->segs.size() > L->max_segs)
-      return THIN_EINVAL;
-    for (const auto& b : h->blocks)
-      if (b.nseg > 32) return THIN_EINVAL;
+  if (!h->blocks.empty()) h->blocks.back().q1 = (int32_t)n;
+  // tiles of 128 points: the pieces of the blocks a tile overlaps, a piece
+  // seen by consecutive blocks kept once with the union of their points
+  h->c0.assign((size_t)n, 0);
+  h->w0.assign((size_t)n, 0.0f);
+  size_t bi = 0;
+  for (int64_t t0 = 0; t0 < n; t0 += 128) {
+    const int64_t t1 = std::min<int64_t>(t0 + 128, n);
+    thin::PrefillTile tl{(int32_t)t0, (int32_t)t1, (int32_t)t1, (int32_t)h->psegs.size(), 0};
+    while (bi < h->blocks.size() && h->blocks[bi].q1 <= t0) ++bi;
+    for (size_t b = bi; b < h->blocks.size() && h->blocks[b].q0 < t1; ++b) {
+      const PfBlock& B = h->blocks[b];
+      const int32_t lo = (int32_t)std::max<int64_t>(B.q0, t0), hi = (int32_t)std::min<int64_t>(B.q1, t1);
+      for (int32_t p = lo; p < hi; ++p) {
+        h->c0[p] = B.causal0;
+        h->w0[p] = B.w0;
+      }
+      tl.causal_lo = std::min(tl.causal_lo, B.causal0);
+      for (int k = B.seg0; k < B.seg0 + B.nseg; ++k) {
+        const thin::ExpressSeg& g = h->segs[k];
+        const int64_t pc = h->piece[k];
+        for (int64_t j = 0; j < g.len; j += pc) {
+          thin::ExpressSeg a = g;
+          if (a.src) a.src += j; else a.start += j;
+          a.len = std::min(pc, g.len - j);
+          bool merged = false;
+          for (size_t q = tl.seg0; q < h->psegs.size(); ++q) {
+            thin::PrefillSeg& e = h->psegs[q];
+            if (e.g.src == a.src && e.g.start == a.start && e.g.len == a.len &&
+                e.g.logw == a.logw && e.g.stride == a.stride && e.vhi == lo) {
+              e.vhi = hi;
+              merged = true;
+              break;
+            }
+          }
+          if (!merged) h->psegs.push_back({a, lo, hi});
+        }
+      }
+    }
+    tl.nseg = (int32_t)h->psegs.size() - tl.seg0;
+    if (tl.nseg > thin::kPrefillMaxSegs) return THIN_EINVAL;
+    int64_t keys = t1 - tl.causal_lo;
+    for (int q = tl.seg0; q < tl.seg0 + tl.nseg; ++q) keys += h->psegs[q].g.len;
+    h->staged_keys += keys;
+    h->tiles.push_back(tl);
   }
+  if (L && ((int64_t)h->tiles.size() > L->max_tiles || (int64_t)h->psegs.size() > L->max_segs))
+    return THIN_EINVAL;
   return THIN_OK;
 }
 
 int pf_check(int64_t B, int64_t H, int64_t n, int64_t d, int64_t n_out, int32_t mbar,
-             PfLayout* L, int64_t* u_slice, int64_t* draws) {
+             PfLayout* L, int64_t* u_slice, int64_t* draws, int64_t* query_keys = nullptr,
+             int64_t* staged_keys = nullptr) {
   int64_t k = 0;
   const int rc = ex_check(B, H, d, n_out, mbar, n, u_slice, &k, draws);
   if (rc) return rc;
@@ -871,6 +936,8 @@ int pf_check(int64_t B, int64_t H, int64_t n, int64_t d, int64_t n_out, int32_t 
   PfHost h;
   if (pf_run(n_out, mbar, n, nullptr, 0, nullptr, nullptr, &h)) return THIN_EINVAL;
   *L = pf_layout(B * H, n_out, mbar, n, h.rec);
+  if (query_keys) *query_keys = h.query_keys;
+  if (staged_keys) *staged_keys = h.staged_keys;
   return THIN_OK;
 }
 
@@ -1046,12 +1113,14 @@ int thin_express_prefill_plan(int64_t B, int64_t H, int64_t n, int64_t d, int64_
                               int32_t mbar, thin_prefill_plan_t* plan) {
   if (!plan) return THIN_EINVAL;
   PfLayout L;
-  int64_t u = 0, dr = 0;
-  const int rc = pf_check(B, H, n, d, n_out, mbar, &L, &u, &dr);
+  int64_t u = 0, dr = 0, qk = 0, sk = 0;
+  const int rc = pf_check(B, H, n, d, n_out, mbar, &L, &u, &dr, &qk, &sk);
   if (rc) return rc;
   plan->uniforms_per_slice = u;
   plan->subsample_draws = dr;
   plan->workspace_bytes = L.bytes;
+  plan->attention_keys = qk;
+  plan->staged_keys = sk;
   return THIN_OK;
 }
 
@@ -1101,9 +1170,10 @@ int thin_express_prefill(int32_t dtype, int64_t B, int64_t H, int64_t n, int64_t
     if (bytes) ok(hipMemcpyAsync(ws + off, src, bytes, hipMemcpyHostToDevice, st));
   };
   up(L.utab, utab.data(), utab.size() * 8);
-  up(L.blocks, h.blocks.data(), h.blocks.size() * sizeof(thin::PrefillBlock));
   up(L.tiles, h.tiles.data(), h.tiles.size() * sizeof(thin::PrefillTile));
-  up(L.segs, h.segs.data(), h.segs.size() * sizeof(thin::ExpressSeg));
+  up(L.segs, h.psegs.data(), h.psegs.size() * sizeof(thin::PrefillSeg));
+  up(L.c0, h.c0.data(), h.c0.size() * 4);
+  up(L.w0, h.w0.data(), h.w0.size() * 4);
   up(L.keptrow, h.keptrow.data(), h.keptrow.size() * 4);
   up(L.keptflag, h.keptflag.data(), h.keptflag.size());
   // the host tables are pageable and freed on return: finish the copies first
@@ -1163,8 +1233,8 @@ int thin_express_prefill(int32_t dtype, int64_t B, int64_t H, int64_t n, int64_t
       return thin::launch_prefill_attention(
           dtype, d, out_dtype, Q, K, V, S, n,
           reinterpret_cast<const thin::PrefillTile*>(ws + L.tiles), (int64_t)h.tiles.size(),
-          reinterpret_cast<const thin::PrefillBlock*>(ws + L.blocks),
-          reinterpret_cast<const thin::ExpressSeg*>(ws + L.segs),
+          reinterpret_cast<const thin::PrefillSeg*>(ws + L.segs),
+          reinterpret_cast<const int32_t*>(ws + L.c0), reinterpret_cast<const float*>(ws + L.w0),
           reinterpret_cast<const uint8_t*>(ws + L.keptflag), O, st);
     }));
   return e == hipSuccess ? THIN_OK : THIN_EHIP;

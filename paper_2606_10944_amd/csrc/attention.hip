@@ -572,24 +572,31 @@ hipError_t launch_attn_res_d(int64_t n_out, const void* Q, const void* K, const 
 
 // ---------------------------------------------------------------------------
 // Masked (causal) prefill over the Express cache (Alg. 4 for every point at
-// once).  One workgroup = up to 128 queries [q0, q1) of one block of one
-// slice.  The block's keys are its segments (rows of the cache, each
-// segment with one log-weight) followed by the causal candidates, positions
-// causal0 .. q1-1 with the block's C_0 log-weight w0: candidate r is seen by
-// query p iff r == p (the point itself) or r < p and r was kept (kept[r]).
-// Same arithmetic as coreset_attn_kernel with per-key biases sqrt(d) * logw.
+// once).  One workgroup = the up to 128 points [q0, q1) of a tile of one
+// slice.  Its keys are the tile's cache pieces (rows of the cache, each with
+// one log-weight, piece k seen by the points vlo..vhi-1), then the causal
+// candidates causal_lo .. q1-1: candidate r is seen by point p iff r == p
+// (the point itself) or r was kept and c0[p] <= r < p (p's C_0), with p's
+// log-weight w0[p].  Same arithmetic as coreset_attn_kernel, with per-key
+// biases sqrt(d) * logw.
 // ---------------------------------------------------------------------------
 template <typename T, int D, typename TO>
 __global__ __launch_bounds__(64 * WAVES) void prefill_attn_kernel(
     const T* __restrict__ Q, const T* __restrict__ K, const T* __restrict__ V, int64_t n,
-    const PrefillTile* __restrict__ tiles, const PrefillBlock* __restrict__ blocks,
-    const ExpressSeg* __restrict__ segs, const uint8_t* __restrict__ kept, TO* __restrict__ O) {
+    const PrefillTile* __restrict__ tiles, const PrefillSeg* __restrict__ segs,
+    const int32_t* __restrict__ c0s, const float* __restrict__ w0s,
+    const uint8_t* __restrict__ kept, TO* __restrict__ O) {
   constexpr int NV = Frag<T, D>::NV;
   constexpr bool BF = Elem<T>::bytes == 2;
   using L = AttnLds<T, D>;
   __shared__ __align__(16) unsigned char lds[L::bytes];
-  __shared__ int32_t s_pos[KC];  // -1: a cache key; else the candidate's position (bit 30: not kept)
-  __shared__ int64_t s_seg_end[32];
+  __shared__ int32_t s_pos[KC];   // causal candidate: position (bit 30: not kept); piece key: -1
+  __shared__ int32_t s_vlo[KC], s_vhi[KC];
+  __shared__ int32_t s_row[KC];
+  __shared__ int64_t s_seg_end[kPrefillMaxSegs];
+  __shared__ PrefillSeg s_seg[kPrefillMaxSegs];
+  __shared__ int32_t s_c0[QPB];
+  __shared__ float s_w0[QPB];
   unsigned char* sK = lds;
   unsigned char* sV = lds + KC * L::k_stride;
   float* sB = reinterpret_cast<float*>(sV + L::v_rows * L::v_stride);
@@ -598,18 +605,21 @@ __global__ __launch_bounds__(64 * WAVES) void prefill_attn_kernel(
   const int m16 = lane & 15, g = lane >> 4;
   const int64_t s = blockIdx.y;
   const PrefillTile tile = tiles[blockIdx.x];
-  const PrefillBlock B = blocks[tile.blk];
-  const int64_t q0 = tile.q0;
-  const int64_t q1 = min((int64_t)B.q1, q0 + QPB);
-  const ExpressSeg* bs = segs + B.seg0;
-  const int nseg = min(B.nseg, 32);
+  const int64_t q0 = tile.q0, q1 = tile.q1;
+  const int nseg = min(tile.nseg, kPrefillMaxSegs);
+  if ((int)threadIdx.x < nseg) s_seg[threadIdx.x] = segs[tile.seg0 + threadIdx.x];
+  if ((int)threadIdx.x < QPB && q0 + threadIdx.x < q1) {
+    s_c0[threadIdx.x] = c0s[q0 + threadIdx.x];
+    s_w0[threadIdx.x] = w0s[q0 + threadIdx.x];
+  }
+  __syncthreads();
   if (threadIdx.x == 0) {
     int64_t e = 0;
-    for (int k = 0; k < nseg; ++k) s_seg_end[k] = (e += bs[k].len);
+    for (int k = 0; k < nseg; ++k) s_seg_end[k] = (e += s_seg[k].g.len);
   }
   __syncthreads();
   const int64_t F = nseg ? s_seg_end[nseg - 1] : 0;
-  const int64_t M = F + (q1 - B.causal0);
+  const int64_t M = F + (q1 - tile.causal_lo);
   const T* Ks = K + s * n * D;
   const T* Vs = V + s * n * D;
   const float sqrt_d = (float)sqrt((double)D);
@@ -633,43 +643,43 @@ __global__ __launch_bounds__(64 * WAVES) void prefill_attn_kernel(
   }
 
   constexpr int WPR = D * Elem<T>::bytes / 16;
-  for (int64_t c0 = 0; c0 < M; c0 += KC) {
-    const int kc = (int)min((int64_t)KC, M - c0);
+  for (int64_t ck = 0; ck < M; ck += KC) {
+    const int kc = (int)min((int64_t)KC, M - ck);
     __syncthreads();
+    // the chunk's keys: row, bias and visibility, one thread per key
     if (threadIdx.x < KC) {
-      const int64_t kk = c0 + threadIdx.x;
-      int32_t pos = -1;
+      const int64_t kk = ck + threadIdx.x;
+      int32_t pos = -1, vlo = 0, vhi = 0;
       float bias = -INFINITY;
+      int64_t r = 0;
       if ((int)threadIdx.x < kc) {
         if (kk < F) {
           int k = 0;
           while (k + 1 < nseg && kk >= s_seg_end[k]) ++k;
-          bias = bs[k].logw * sqrt_d;
+          const ExpressSeg& sg = s_seg[k].g;
+          const int64_t j = kk - (k ? s_seg_end[k - 1] : 0);
+          r = sg.src ? (int64_t)sg.src[s * sg.stride + j] : sg.start + j;
+          bias = sg.logw * sqrt_d;
+          vlo = s_seg[k].vlo;
+          vhi = s_seg[k].vhi;
         } else {
-          const int64_t r = B.causal0 + (kk - F);
+          r = tile.causal_lo + (kk - F);
           pos = (int32_t)r | (kept[r] ? 0 : (1 << 30));
-          bias = B.w0 * sqrt_d;
         }
+        r = r < 0 ? 0 : (r >= n ? n - 1 : r);
       }
       s_pos[threadIdx.x] = pos;
+      s_vlo[threadIdx.x] = vlo;
+      s_vhi[threadIdx.x] = vhi;
+      s_row[threadIdx.x] = (int32_t)r;
       sB[threadIdx.x] = bias;
     }
+    __syncthreads();
     for (int w = threadIdx.x; w < KC * WPR; w += 64 * WAVES) {
       const int key = w / WPR, wi = w % WPR;
       uint4 kw = make_uint4(0, 0, 0, 0), vw = make_uint4(0, 0, 0, 0);
       if (key < kc) {
-        const int64_t kk = c0 + key;
-        int64_t r;
-        if (kk < F) {
-          int k = 0;
-          while (k + 1 < nseg && kk >= s_seg_end[k]) ++k;
-          const ExpressSeg& sg = bs[k];
-          const int64_t j = kk - (k ? s_seg_end[k - 1] : 0);
-          r = sg.src ? (int64_t)sg.src[s * sg.stride + j] : sg.start + j;
-        } else {
-          r = B.causal0 + (kk - F);
-        }
-        r = r < 0 ? 0 : (r >= n ? n - 1 : r);
+        const int64_t r = s_row[key];
         kw = reinterpret_cast<const uint4*>(Ks + r * D)[wi];
         vw = reinterpret_cast<const uint4*>(Vs + r * D)[wi];
       }
@@ -695,7 +705,10 @@ __global__ __launch_bounds__(64 * WAVES) void prefill_attn_kernel(
 
 #pragma unroll
     for (int qt = 0; qt < QT; ++qt) {
-      const int64_t p = qw + qt * 16 + m16;  // this lane's query position
+      const int64_t p = qw + qt * 16 + m16;  // this lane's point
+      const int li = (int)min(p - q0, (int64_t)QPB - 1);
+      const int32_t pc0 = p < q1 ? s_c0[li] : 0;
+      const float pw0 = p < q1 ? s_w0[li] * sqrt_d : 0.f;
       float sc[4][4];
       float mx = -INFINITY;
 #pragma unroll
@@ -706,10 +719,16 @@ __global__ __launch_bounds__(64 * WAVES) void prefill_attn_kernel(
         for (int i = 0; i < 4; ++i) {
           const int key = kt * 16 + 4 * g + i;
           const int32_t ps = s_pos[key];
-          const int64_t r = ps & ~(1 << 30);
-          const bool seen = ps < 0 || r == p || (!(ps & (1 << 30)) && r < p);
-          sc[kt][i] = seen ? z[i] + sB[key] : -INFINITY;
-          mx = fmaxf(mx, sc[kt][i]);
+          float v;
+          if (ps < 0) {
+            v = (p >= s_vlo[key] && p < s_vhi[key]) ? z[i] + sB[key] : -INFINITY;
+          } else {
+            const int64_t r = ps & ~(1 << 30);
+            const bool seen = r == p || (!(ps & (1 << 30)) && r < p && r >= pc0);
+            v = seen ? z[i] + pw0 : -INFINITY;
+          }
+          sc[kt][i] = v;
+          mx = fmaxf(mx, v);
         }
       }
       mx = fmaxf(mx, __shfl_xor(mx, 16));
@@ -797,24 +816,24 @@ __global__ __launch_bounds__(64 * WAVES) void prefill_attn_kernel(
 
 template <typename T, int D, typename TO>
 hipError_t launch_prefill_t(const void* Q, const void* K, const void* V, int64_t S, int64_t n,
-                            const PrefillTile* tiles, int64_t ntiles, const PrefillBlock* blocks,
-                            const ExpressSeg* segs, const uint8_t* kept, void* O,
+                            const PrefillTile* tiles, int64_t ntiles, const PrefillSeg* segs,
+                            const int32_t* c0, const float* w0, const uint8_t* kept, void* O,
                             hipStream_t st) {
   dim3 grid((unsigned)ntiles, (unsigned)S), block(64 * WAVES);
   hipLaunchKernelGGL((prefill_attn_kernel<T, D, TO>), grid, block, 0, st, (const T*)Q,
-                     (const T*)K, (const T*)V, n, tiles, blocks, segs, kept, (TO*)O);
+                     (const T*)K, (const T*)V, n, tiles, segs, c0, w0, kept, (TO*)O);
   return hipGetLastError();
 }
 
 template <typename T, typename TO>
 hipError_t launch_prefill_d(int64_t d, const void* Q, const void* K, const void* V, int64_t S,
                             int64_t n, const PrefillTile* tiles, int64_t ntiles,
-                            const PrefillBlock* blocks, const ExpressSeg* segs,
+                            const PrefillSeg* segs, const int32_t* c0, const float* w0,
                             const uint8_t* kept, void* O, hipStream_t st) {
   switch (d) {
-    case 32: return launch_prefill_t<T, 32, TO>(Q, K, V, S, n, tiles, ntiles, blocks, segs, kept, O, st);
-    case 64: return launch_prefill_t<T, 64, TO>(Q, K, V, S, n, tiles, ntiles, blocks, segs, kept, O, st);
-    case 128: return launch_prefill_t<T, 128, TO>(Q, K, V, S, n, tiles, ntiles, blocks, segs, kept, O, st);
+    case 32: return launch_prefill_t<T, 32, TO>(Q, K, V, S, n, tiles, ntiles, segs, c0, w0, kept, O, st);
+    case 64: return launch_prefill_t<T, 64, TO>(Q, K, V, S, n, tiles, ntiles, segs, c0, w0, kept, O, st);
+    case 128: return launch_prefill_t<T, 128, TO>(Q, K, V, S, n, tiles, ntiles, segs, c0, w0, kept, O, st);
     default: return hipErrorInvalidValue;
   }
 }
@@ -850,16 +869,16 @@ hipError_t launch_attn_d(int64_t d, const void* Q, const void* K, const void* V,
 hipError_t launch_prefill_attention(int dtype, int64_t d, int out_dtype, const void* Q,
                                     const void* K, const void* V, int64_t S, int64_t n,
                                     const PrefillTile* tiles, int64_t ntiles,
-                                    const PrefillBlock* blocks, const ExpressSeg* segs,
+                                    const PrefillSeg* segs, const int32_t* c0, const float* w0,
                                     const uint8_t* kept, void* O, hipStream_t st) {
   if (ntiles < 1) return hipSuccess;
   if (dtype == 0)
     return out_dtype == 0
-               ? launch_prefill_d<float, float>(d, Q, K, V, S, n, tiles, ntiles, blocks, segs, kept, O, st)
-               : launch_prefill_d<float, bf16_t>(d, Q, K, V, S, n, tiles, ntiles, blocks, segs, kept, O, st);
+               ? launch_prefill_d<float, float>(d, Q, K, V, S, n, tiles, ntiles, segs, c0, w0, kept, O, st)
+               : launch_prefill_d<float, bf16_t>(d, Q, K, V, S, n, tiles, ntiles, segs, c0, w0, kept, O, st);
   return out_dtype == 0
-             ? launch_prefill_d<bf16_t, float>(d, Q, K, V, S, n, tiles, ntiles, blocks, segs, kept, O, st)
-             : launch_prefill_d<bf16_t, bf16_t>(d, Q, K, V, S, n, tiles, ntiles, blocks, segs, kept, O, st);
+             ? launch_prefill_d<bf16_t, float>(d, Q, K, V, S, n, tiles, ntiles, segs, c0, w0, kept, O, st)
+             : launch_prefill_d<bf16_t, bf16_t>(d, Q, K, V, S, n, tiles, ntiles, segs, c0, w0, kept, O, st);
 }
 
 hipError_t launch_attention(int dtype, int64_t d, int out_dtype, const void* Q, const void* K,

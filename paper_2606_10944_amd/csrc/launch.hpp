@@ -125,20 +125,23 @@ hipError_t launch_decode_attention(int dtype, int64_t d, int out_dtype, const vo
                                    hipStream_t st);
 
 
-// Masked prefill over the Express cache: a block of queries [q0, q1) sees the
-// segments [seg0, seg0 + nseg) (at most 32) and the causal candidates
-// causal0 .. q1-1 with log-weight w0; a tile is up to 128 queries of a block.
-struct PrefillBlock {
-  int32_t q0, q1, causal0, seg0, nseg;
-  float w0;
-};
+// Masked prefill over the Express cache: a tile is the points [q0, q1) (at
+// most 128); its keys are the pieces [seg0, seg0 + nseg) (at most 256), piece
+// k seen by the points vlo..vhi-1, then the causal candidates causal_lo ..
+// q1-1, candidate r seen by point p iff r == p, or kept[r] and
+// c0[p] <= r < p, with p's C_0 log-weight w0[p].
 struct PrefillTile {
-  int32_t blk, q0;
+  int32_t q0, q1, causal_lo, seg0, nseg;
 };
+struct PrefillSeg {
+  ExpressSeg g;
+  int32_t vlo, vhi;
+};
+constexpr int kPrefillMaxSegs = 256;
 hipError_t launch_prefill_attention(int dtype, int64_t d, int out_dtype, const void* Q,
                                     const void* K, const void* V, int64_t S, int64_t n,
                                     const PrefillTile* tiles, int64_t ntiles,
-                                    const PrefillBlock* blocks, const ExpressSeg* segs,
+                                    const PrefillSeg* segs, const int32_t* c0, const float* w0,
                                     const uint8_t* kept, void* O, hipStream_t st);
 
 // logw (nullable) [S, n_out]: log-weight of every coreset key.

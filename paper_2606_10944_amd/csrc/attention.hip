@@ -681,16 +681,37 @@ __global__ __launch_bounds__(64 * WAVES) void prefill_attn_kernel(
       if (key < kc) {
         const int64_t r = s_row[key];
         kw = reinterpret_cast<const uint4*>(Ks + r * D)[wi];
-        vw = reinterpret_cast<const uint4*>(Vs + r * D)[wi];
+        if (!BF) vw = reinterpret_cast<const uint4*>(Vs + r * D)[wi];
       }
       *reinterpret_cast<uint4*>(sK + key * L::k_stride + wi * 16) = kw;
-      if (BF) {
-        const uint16_t* e = reinterpret_cast<const uint16_t*>(&vw);
+      if (!BF) *reinterpret_cast<uint4*>(sV + key * L::v_stride + wi * 16) = vw;
+    }
+    if (BF) {
+      // V^T: each thread transposes 8 keys x 8 columns in registers and
+      // writes 8 16-byte rows (one per column)
+      for (int b = threadIdx.x; b < (KC / 8) * WPR; b += 64 * WAVES) {
+        const int kb = b / WPR, db = b % WPR;
+        uint32_t v8[8][4];
 #pragma unroll
-        for (int j = 0; j < 8; ++j)
-          *reinterpret_cast<uint16_t*>(sV + (wi * 8 + j) * L::v_stride + key * 2) = e[j];
-      } else {
-        *reinterpret_cast<uint4*>(sV + key * L::v_stride + wi * 16) = vw;
+        for (int r8 = 0; r8 < 8; ++r8) {
+          const int key = kb * 8 + r8;
+          uint4 x = make_uint4(0, 0, 0, 0);
+          if (key < kc) x = reinterpret_cast<const uint4*>(Vs + (int64_t)s_row[key] * D)[db];
+          v8[r8][0] = x.x; v8[r8][1] = x.y; v8[r8][2] = x.z; v8[r8][3] = x.w;
+        }
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const int k = e >> 1;
+          uint4 o;
+          if ((e & 1) == 0) {
+            o.x = pack_lo(v8[0][k], v8[1][k]); o.y = pack_lo(v8[2][k], v8[3][k]);
+            o.z = pack_lo(v8[4][k], v8[5][k]); o.w = pack_lo(v8[6][k], v8[7][k]);
+          } else {
+            o.x = pack_hi(v8[0][k], v8[1][k]); o.y = pack_hi(v8[2][k], v8[3][k]);
+            o.z = pack_hi(v8[4][k], v8[5][k]); o.w = pack_hi(v8[6][k], v8[7][k]);
+          }
+          *reinterpret_cast<uint4*>(sV + (db * 8 + e) * L::v_stride + kb * 16) = o;
+        }
       }
     }
     __syncthreads();

@@ -27,6 +27,10 @@ CASES = [
     dict(B=2, H=1, d=64, dtype="fp32", n_out=8, mbar=2, n=2100, halve="uniform"),
     # the decoding experiments' setting mbar = log2(n_out) - 2, past 8192 points
     dict(B=1, H=2, d=128, dtype="bf16", n_out=128, mbar=5, n=9000, halve="kh"),
+    # fewer points than n_out (exact phase only, no uniforms), and exactly the
+    # points that end in the first Halve phase
+    dict(B=1, H=2, d=64, dtype="fp32", n_out=8, mbar=2, n=5, halve="kh"),
+    dict(B=2, H=1, d=64, dtype="bf16", n_out=8, mbar=2, n=32, halve="kh"),
 ]
 
 

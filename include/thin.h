@@ -22,6 +22,14 @@
  *     synchronisation.
  *   - Supported: dtype THIN_FP32 or THIN_BF16 (Q, K, V share it), d in
  *     {32, 64, 128}, B*H <= 65535 slices (THIN_EINVAL beyond).
+ *   - Device status word: the first 4 bytes (int32) of every workspace
+ *     (thin_compress*, the Express object's, thin_express_prefill's).  A call
+ *     that runs kernel-halving decisions clears it first (an Express object:
+ *     at its first step); a decision pass whose bounded wait for another
+ *     wavefront's progress runs out sets it to THIN_STATUS_WAIT_EXHAUSTED
+ *     and still ends normally.  Nonzero means that call's (that object's)
+ *     coreset is not the one Algorithm A.1 defines; read it with
+ *     thin_workspace_status after the call.
  */
 #ifndef THIN_H
 #define THIN_H
@@ -43,6 +51,9 @@ typedef enum {
 } thin_status_t;
 
 typedef enum { THIN_FP32 = 0, THIN_BF16 = 1 } thin_dtype_t;
+
+/* Bits of the device status word. */
+#define THIN_STATUS_WAIT_EXHAUSTED 1
 
 /*
  * Level structure of one compress call (identical for every slice).
@@ -95,7 +106,11 @@ int thin_plan(int64_t B, int64_t H, int64_t n, int64_t d, int64_t n_out, int32_t
  *
  * kappa_att((k,v),(k',v')) = exp(<k,k'>/sqrt(d)) (<v,v'> + v_max^2) with
  * v_max = max over all n rows of ||v||_inf (Sec. 2.1, eq. katt); delta = 1/2
- * (App. I).  With n_out == n the result is 0..n-1.
+ * (App. I).  With n_out == n the result is 0..n-1.  The kernel values are
+ * evaluated in float32 under per-pair power-of-two scales chosen from the
+ * keys' norms, so no exponent overflows whatever the keys; keys whose
+ * ||k||^2/sqrt(d) exceeds about 1.1e7 (kappa_att itself far beyond float64)
+ * are not supported.
  * Errors: THIN_EINVAL (sizes / null pointers / no level structure),
  * THIN_EDTYPE, THIN_EUNIFORMS (n_uniforms < plan.uniforms_total),
  * THIN_EWORKSPACE, THIN_EHIP.
@@ -296,18 +311,27 @@ int thin_express_destroy(thin_express_t* x);
 /*
  * Masked prefill: the outputs of Thinformer decoding (thin_express_step) for
  * every point of a whole sequence at once (Alg. 4; the offline form of the
- * Express recursion, App. F).  Point p attends over the cache of points
- * 0..p-1 plus itself, exactly as a decoding step would, with the same
- * uniforms layout (every Halve call's N/2 draws at the offset it has in
+ * Express recursion, App. H, Algorithm H.3).  Point p attends over the cache
+ * of points 0..p-1 plus itself, exactly as a decoding step would, with the
+ * same uniforms layout (every Halve call's N/2 draws at the offset it has in
  * decoding) and the same Subsample draws (host, one per stratum).
  * The Compress2 calls of a level run batched by depth (their outputs kept),
- * the Halve phases level by level, then one attention launch.  Host tables
- * are copied into the workspace and the stream is synchronized once.
+ * the Halve phases level by level, then one attention launch.  The call plans
+ * on the host (tables of Halve calls, query tiles and cache pieces), writes
+ * the tables into the caller's host staging buffer and enqueues one copy of
+ * it into the workspace; nothing synchronises.
  *   Q, K, V (device) [B,H,n,d] of `dtype`;  O (device) [B,H,n,d] of out_dtype.
  *   uniforms (device) [B*H, plan.uniforms_per_slice];  draws (host).
+ *   host_staging (host) at least plan.host_staging_bytes: its contents must
+ *               stay unchanged until the stream has executed this call (for
+ *               instance until an event recorded after it has completed).
+ *               Pinned memory (hipHostMalloc) keeps the copy asynchronous;
+ *               with pageable memory the runtime may block the host during
+ *               the copy.
  *   swap_trace (device, nullable) uint8 indexed like uniforms.
  * Sizes as for thin_express_plan with n_max = n, and n <= 2^30.
- * Errors: THIN_EINVAL, THIN_EDTYPE, THIN_EUNIFORMS, THIN_EWORKSPACE, THIN_EHIP.
+ * Errors: THIN_EINVAL, THIN_EDTYPE, THIN_EUNIFORMS, THIN_EWORKSPACE (also for
+ * a missing or short host_staging), THIN_EHIP.
  */
 typedef struct {
   int64_t uniforms_per_slice; /* as thin_express_plan for n points          */
@@ -317,6 +341,7 @@ typedef struct {
                                  (Subsample draws of 0)                     */
   int64_t staged_keys;        /* per slice: keys the attention launch
                                  gathers, summed over its 128-point tiles   */
+  size_t host_staging_bytes;  /* host staging buffer of thin_express_prefill */
 } thin_prefill_plan_t;
 
 /* Host-only. */
@@ -328,7 +353,8 @@ int thin_express_prefill(int32_t dtype, int64_t B, int64_t H, int64_t n, int64_t
                          const void* Q, const void* K, const void* V, const float* uniforms,
                          int64_t n_uniforms, const float* draws, int64_t n_draws, void* O,
                          int32_t out_dtype, void* workspace, size_t workspace_bytes,
-                         uint8_t* swap_trace, void* stream);
+                         void* host_staging, size_t host_staging_bytes, uint8_t* swap_trace,
+                         void* stream);
 
 /*
  * Diagnostic: out[m*16 + n] = <rows[m], rows[16 + n]> for m, n < 16, computed
@@ -342,7 +368,17 @@ int thin_selftest_gram16(int32_t dtype, int64_t d, const void* rows, float* out,
 const char* thin_status_str(int status);
 
 /*
- * Launch observer, for tracing and per-kernel timing.  While a hook is set,
+ * Enqueue a copy of a workspace's device status word (see the conventions
+ * above) into *status (host; pinned memory keeps the copy asynchronous) on
+ * `stream`; read *status after synchronising the stream.
+ * Errors: THIN_EINVAL (null pointer), THIN_EHIP.
+ */
+int thin_workspace_status(const void* workspace, int32_t* status, void* stream);
+
+/*
+ * Launch observer, a diagnostic for tracing and per-kernel timing (not part
+ * of the compute contract; the library keeps no state between calls apart
+ * from it).  While a hook is set,
  * every kernel launch made by thin_compress, thin_compress_traced,
  * thin_compress_ex, thin_attention, thin_attention_ex and thin_express_step
  * is bracketed by two calls on the
@@ -357,9 +393,9 @@ const char* thin_status_str(int status);
  * when a slice keeps at most 32768 rows, else one launch per round).  A round
  * runs either as SCORES + DECIDE launches or, when its buckets are small
  * enough for one workgroup to hold all their scores in LDS, as one LOCAL
- * launch.  The setting is process-wide:
- * change it only while no other thread is inside the library.  hook = NULL
- * turns it off (the default).  Returns THIN_OK.
+ * launch.  The setting belongs to the calling thread (thread-local): only
+ * launches made by that thread are observed, and calls on other threads are
+ * unaffected.  hook = NULL turns it off (the default).  Returns THIN_OK.
  */
 typedef enum {
   THIN_KERNEL_TRACE_CLEAR = 0, /* zeroing of the swap trace               */
@@ -372,7 +408,8 @@ typedef enum {
   THIN_KERNEL_LOCAL = 7,       /* scores and decisions of one round       */
   THIN_KERNEL_UNIFORM = 8,     /* uniform halving (all rounds, or one)    */
   THIN_KERNEL_ASSEMBLE = 9,    /* sinks + coreset + window, log-weights   */
-  THIN_KERNEL_EXPRESS = 10     /* Express cache moves, per-call v_max, keys */
+  THIN_KERNEL_EXPRESS = 10,    /* Express cache moves, per-call v_max, keys */
+  THIN_KERNEL_STATUS = 11      /* clearing of the device status word      */
 } thin_kernel_t;
 typedef void (*thin_launch_hook_t)(void* ctx, int32_t kernel, int32_t round, int32_t phase,
                                    void* stream);

@@ -88,6 +88,8 @@ def lib():
         L.or_express_decode.restype = C.c_int
         L.or_express_uniforms.argtypes = [C.c_int64, C.c_int64, C.c_int, C.POINTER(C.c_int64)]
         L.or_express_uniforms.restype = C.c_int64
+        L.or_express_keys.argtypes = [C.c_int64, C.c_int64, C.c_int, P, P]
+        L.or_express_keys.restype = C.c_int
         L.or_express_delta.argtypes = [C.c_int, C.c_int, C.c_int, C.c_double]
         L.or_express_delta.restype = C.c_double
         L.or_compress_ex.restype = C.c_int
@@ -268,6 +270,16 @@ def express_draws(n: int, n_out: int, mbar: int) -> int:
     if lib().or_express_uniforms(n, n_out, mbar, C.byref(k)) < 0:
         raise ValueError("no Express structure for these sizes")
     return k.value
+
+
+def express_keys(n: int, n_out: int, mbar: int, sub_u=None) -> np.ndarray:
+    """Keys every point attends over in Thinformer decoding of n points (its
+    weighted cache plus itself), int64 [n]; sub_u as in express_decode."""
+    keys = np.zeros(max(n, 1), np.int64)
+    su = None if sub_u is None else np.ascontiguousarray(sub_u, dtype=np.float32)
+    if lib().or_express_keys(n, n_out, mbar, _p(su), _p(keys)) != 0:
+        raise ValueError("no Express structure for these sizes")
+    return keys[:n]
 
 
 def express_delta(m: int, i: int, mbar: int, delta: float = 0.5) -> float:

@@ -530,7 +530,8 @@ static int64_t ex_cache(const ex_t* x, int32_t* rows, double* logw) {
 }
 
 /* forward declaration: the uniforms a decode of n points consumes */
-static int ex_run(ex_t* x, const double* Q, int64_t n, double* O, int32_t* rows, double* logw);
+static int ex_run(ex_t* x, const double* Q, int64_t n, double* O, int32_t* rows, double* logw,
+                  int64_t* keys);
 
 int or_express_decode(const double* Q, const double* K, const double* V, int64_t n, int64_t d,
                       int64_t n_out, int mbar, double delta, int halve, const float* U,
@@ -553,7 +554,7 @@ int or_express_decode(const double* Q, const double* K, const double* V, int64_t
     x.C[i] = (int32_t*)malloc(sizeof(int32_t) * (size_t)(4 * n_out));
     ok = x.C[i] != NULL;
   }
-  int rc = ok ? ex_run(&x, Q, n, O, rows, logw) : -2;
+  int rc = ok ? ex_run(&x, Q, n, O, rows, logw, NULL) : -2;
   if (rc == 0) {
     int64_t k = ex_cache(&x, rows, logw);
     if (cache_rows) memcpy(cache_rows, rows, sizeof(int32_t) * (size_t)k);
@@ -569,10 +570,17 @@ int or_express_decode(const double* Q, const double* K, const double* V, int64_t
   return rc;
 }
 
-static int ex_run(ex_t* x, const double* Q, int64_t n, double* O, int32_t* rows, double* logw) {
+static int ex_run(ex_t* x, const double* Q, int64_t n, double* O, int32_t* rows, double* logw,
+                  int64_t* keys) {
   int rc = 0;
   ex_reset_c(x);
   for (int64_t p = 0; p < n && rc == 0; ++p) {
+    if (keys) {
+      /* the size of WtdAttention's key list for point p: the cache plus p */
+      int64_t k = x->nE + 1;
+      for (int i = 0; i <= x->mp; ++i) k += x->nC[i];
+      keys[p] = k;
+    }
     if (O) {
       /* WtdAttention: the cache plus the token itself in C_0 (weight 2^-mp) */
       int64_t k = ex_cache(x, rows, logw);
@@ -599,10 +607,33 @@ int64_t or_express_uniforms(int64_t n, int64_t n_out, int mbar, int64_t* draws) 
     x.C[i] = (int32_t*)malloc(sizeof(int32_t) * (size_t)(4 * n_out));
     ok = x.C[i] != NULL;
   }
-  int rc = ok ? ex_run(&x, NULL, n, NULL, NULL, NULL) : -2;
+  int rc = ok ? ex_run(&x, NULL, n, NULL, NULL, NULL, NULL) : -2;
   for (int i = 0; i <= EX_MAXL; ++i) free(x.C[i]);
   free(x.E);
   free(x.tmp);
   if (draws) *draws = x.sub_pos;
   return rc == 0 ? x.upos : -1;
+}
+
+/* keys[p] = the number of keys point p attends over in Thinformer decoding
+ * (its weighted cache plus itself), p < n; sub_u as in or_express_decode.
+ * The sizes do not depend on the halving decisions, so no kernel is
+ * evaluated. */
+int or_express_keys(int64_t n, int64_t n_out, int mbar, const float* sub_u, int64_t* keys) {
+  if (n < 0 || n_out < 1 || mbar < 0 || mbar > EX_MAXL - 2 || !keys) return -1;
+  ex_t x;
+  memset(&x, 0, sizeof(x));
+  x.n_out = n_out; x.mbar = mbar; x.delta = 0.5; x.count_only = 1; x.sub_u = sub_u;
+  x.E = (int32_t*)malloc(sizeof(int32_t) * (size_t)(4 * n_out));
+  x.tmp = (int32_t*)malloc(sizeof(int32_t) * (size_t)(4 * n_out));
+  int ok = x.E && x.tmp;
+  for (int i = 0; i <= EX_MAXL && ok; ++i) {
+    x.C[i] = (int32_t*)malloc(sizeof(int32_t) * (size_t)(4 * n_out));
+    ok = x.C[i] != NULL;
+  }
+  int rc = ok ? ex_run(&x, NULL, n, NULL, NULL, NULL, keys) : -2;
+  for (int i = 0; i <= EX_MAXL; ++i) free(x.C[i]);
+  free(x.E);
+  free(x.tmp);
+  return rc;
 }

@@ -118,6 +118,10 @@ int or_express_decode(const double* Q, const double* K, const double* V, int64_t
                       const float* sub_u, const uint8_t* follow, double tol, uint8_t* bits,
                       double* O, int32_t* cache_rows, double* cache_logw, int64_t* cache_len,
                       int* m_final, or_stats_t* st);
+
+/* Per-point key counts of Thinformer decoding: keys[p] = size of point p's
+ * weighted cache plus one (the point itself), p < n.  Returns 0. */
+int or_express_keys(int64_t n, int64_t n_out, int mbar, const float* sub_u, int64_t* keys);
 /* Uniforms a decode of n points consumes at most (or -1); *draws (nullable)
  * the Subsample draws it needs. */
 int64_t or_express_uniforms(int64_t n, int64_t n_out, int mbar, int64_t* draws);

@@ -8,4 +8,4 @@ from ._lib import (THIN_BF16, THIN_EDTYPE, THIN_EHIP, THIN_EINVAL, THIN_EUNIFORM
                    THIN_EWORKSPACE, THIN_FP32, THIN_OK, ExpressCache, LaunchTimer, ThinError,
                    thin_attention, thin_compress, thin_express_plan, thin_express_prefill,
                    thin_express_prefill_plan, thin_plan,
-                   thin_selftest_gram16, thin_status_str)
+                   thin_selftest_gram16, thin_status_str, workspace_status)

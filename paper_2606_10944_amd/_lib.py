@@ -19,19 +19,20 @@ LIB_PATH = os.path.join(_HERE, "libthin.so")
 
 THIN_OK, THIN_EINVAL, THIN_EDTYPE, THIN_EUNIFORMS, THIN_EWORKSPACE, THIN_EHIP = range(6)
 THIN_FP32, THIN_BF16 = 0, 1
+THIN_STATUS_WAIT_EXHAUSTED = 1
 
 # Every symbol include/thin.h declares.
 EXPORTS = ("thin_plan", "thin_compress", "thin_compress_traced", "thin_compress_ex", "thin_attention",
            "thin_attention_ex", "thin_express_plan", "thin_express_create", "thin_express_step",
            "thin_express_cache", "thin_express_next", "thin_express_destroy",
            "thin_express_prefill_plan", "thin_express_prefill",
-           "thin_selftest_gram16", "thin_status_str",
+           "thin_selftest_gram16", "thin_status_str", "thin_workspace_status",
            "thin_set_launch_hook")
 
 # thin_kernel_t
 KERNEL_NAMES = {0: "trace_clear", 1: "subsample", 2: "fill", 3: "vmax", 4: "scores",
                 5: "decide", 6: "attention", 7: "local", 8: "uniform", 9: "assemble",
-                10: "express"}
+                10: "express", 11: "status"}
 HALVE = {"kh": 0, "uniform": 1}  # thin_halve_t
 LaunchHook = C.CFUNCTYPE(None, C.c_void_p, C.c_int32, C.c_int32, C.c_int32, C.c_void_p)
 
@@ -50,7 +51,7 @@ class ExpressPlan(C.Structure):
 class PrefillPlan(C.Structure):
     _fields_ = [("uniforms_per_slice", C.c_int64), ("subsample_draws", C.c_int64),
                 ("workspace_bytes", C.c_size_t), ("attention_keys", C.c_int64),
-                ("staged_keys", C.c_int64)]
+                ("staged_keys", C.c_int64), ("host_staging_bytes", C.c_size_t)]
 
 
 class CompressOpts(C.Structure):
@@ -99,7 +100,8 @@ def lib():
     L.thin_express_destroy.argtypes = [P]
     L.thin_express_prefill_plan.argtypes = [I64, I64, I64, I64, I64, I32, C.POINTER(PrefillPlan)]
     L.thin_express_prefill.argtypes = [I32, I64, I64, I64, I64, I64, I32, C.c_double, I32, P, P,
-                                       P, P, I64, P, I64, P, I32, P, SZ, P, P]
+                                       P, P, I64, P, I64, P, I32, P, SZ, P, SZ, P, P]
+    L.thin_workspace_status.argtypes = [P, P, P]
     L.thin_selftest_gram16.argtypes = [I32, I64, P, P, P]
     L.thin_status_str.argtypes = [C.c_int]
     L.thin_status_str.restype = C.c_char_p
@@ -109,7 +111,7 @@ def lib():
               "thin_attention", "thin_attention_ex", "thin_selftest_gram16", "thin_express_plan",
               "thin_express_create", "thin_express_step", "thin_express_cache",
               "thin_express_next", "thin_express_destroy", "thin_express_prefill_plan",
-              "thin_express_prefill"):
+              "thin_express_prefill", "thin_workspace_status"):
         getattr(L, f).restype = C.c_int
     _lib = L
     return L
@@ -140,6 +142,30 @@ def _stream(stream) -> C.c_void_p:
 def _check(rc: int, where: str):
     if rc != THIN_OK:
         raise ThinError(rc, where)
+
+
+def workspace_status(workspace: torch.Tensor, stream=None) -> int:
+    """The device status word of a workspace once the work enqueued on
+    `stream` so far has run (this synchronises that stream): 0, or
+    THIN_STATUS_WAIT_EXHAUSTED if a decision pass's bounded wait gave up."""
+    out = torch.zeros(1, dtype=torch.int32, pin_memory=True)
+    _check(lib().thin_workspace_status(_ptr(workspace), _ptr(out), _stream(stream)),
+           "thin_workspace_status")
+    (stream if stream is not None else torch.cuda.current_stream()).synchronize()
+    return int(out[0])
+
+
+# Pinned host buffers handed to asynchronous calls, each kept until an event
+# recorded after its call has completed.
+_pending = []
+
+
+def _keep_until_done(buf: torch.Tensor, stream) -> None:
+    global _pending
+    _pending = [(e, b) for e, b in _pending if not e.query()]
+    ev = torch.cuda.Event()
+    ev.record(stream if stream is not None else torch.cuda.current_stream())
+    _pending.append((ev, buf))
 
 
 def thin_plan(B: int, H: int, n: int, d: int, n_out: int, g: int) -> dict:
@@ -320,6 +346,10 @@ class ExpressCache:
         self.n += 1
         return O
 
+    def status(self, stream=None) -> int:
+        """The object's device status word (see workspace_status)."""
+        return workspace_status(self.ws, stream)
+
     def next_keys(self) -> int:
         """Keys the next step attends over (host-only)."""
         k, t = C.c_int64(0), C.c_int64(0)
@@ -380,13 +410,15 @@ def thin_express_prefill(Q: torch.Tensor, K: torch.Tensor, V: torch.Tensor, n_ou
                               or draws.dtype != torch.float32 or not draws.is_contiguous()):
         raise ThinError(THIN_EINVAL, "draws must be a contiguous float32 CPU tensor")
     nU = 0 if uniforms is None else uniforms.numel()
+    staging = torch.empty(max(plan["host_staging_bytes"], 1), dtype=torch.uint8, pin_memory=True)
     rc = lib().thin_express_prefill(
         _dtype_code(Q.dtype), B, H, n, d, n_out, mbar, delta, HALVE[halve], _ptr(Q), _ptr(K),
         _ptr(V), None if uniforms is None else _ptr(uniforms), nU,
         None if draws is None else _ptr(draws), 0 if draws is None else draws.numel(), _ptr(O),
-        _dtype_code(O.dtype), _ptr(workspace), workspace.numel(),
-        None if trace is None else _ptr(trace), _stream(stream))
+        _dtype_code(O.dtype), _ptr(workspace), workspace.numel(), _ptr(staging),
+        staging.numel(), None if trace is None else _ptr(trace), _stream(stream))
     _check(rc, "thin_express_prefill")
+    _keep_until_done(staging, stream)
     return O
 
 

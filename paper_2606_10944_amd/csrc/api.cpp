@@ -89,13 +89,23 @@ size_t score_region(int64_t S, int64_t d, const Levels& lv) {
   return region;
 }
 
+// Per-block row-scale maxima of the largest round (floats).
+size_t block_scales(int64_t S, const Levels& lv) {
+  size_t m = 1;
+  for (int32_t r = 0; r < lv.L; ++r)
+    m = std::max(m, (size_t)(S * lv.G[r]) * (size_t)((lv.N[r] + 63) / 64));
+  return m;
+}
+
 struct Workspace {
+  int32_t* status;  // the device status word (thin.h), first in every workspace
   uint32_t* vmax_bits;
   int32_t* buf_a;  // [S, n_kept]
   int32_t* buf_b;  // [S, n_kept / 2]
   float* lbt;      // [S, n_kept / 2]
   float* h2;       // [S, n_kept / 2]
   float* rowh2;    // [S, n]
+  float* mB;       // [buckets, ceil(N / 64)] of the largest round
   float* E;        // score region
   size_t e_bytes;
   size_t bytes;
@@ -106,6 +116,8 @@ Workspace carve(void* base, int64_t S, int64_t d, const Levels& lv) {
   unsigned char* p = static_cast<unsigned char*>(base);
   const size_t pairs = (size_t)S * (size_t)(lv.n_kept / 2);
   size_t off = 0;
+  w.status = reinterpret_cast<int32_t*>(p + off);
+  off += 256;
   w.vmax_bits = reinterpret_cast<uint32_t*>(p + off);
   off += align256((size_t)S * 4);
   w.buf_a = reinterpret_cast<int32_t*>(p + off);
@@ -118,6 +130,8 @@ Workspace carve(void* base, int64_t S, int64_t d, const Levels& lv) {
   off += align256(pairs * 4);
   w.rowh2 = reinterpret_cast<float*>(p + off);
   off += align256((size_t)S * (size_t)lv.n * 4);
+  w.mB = reinterpret_cast<float*>(p + off);
+  off += align256(block_scales(S, lv) * 4);
   w.E = reinterpret_cast<float*>(p + off);
   w.e_bytes = score_region(S, d, lv);
   off += align256(w.e_bytes);
@@ -129,8 +143,10 @@ size_t workspace_size(int64_t S, int64_t d, const Levels& lv) {
   return carve(nullptr, S, d, lv).bytes;
 }
 
-thin_launch_hook_t g_hook = nullptr;
-void* g_hook_ctx = nullptr;
+// The launch observer is a diagnostic of the calling thread (thread-local):
+// calls from other threads never see it.
+thread_local thin_launch_hook_t g_hook = nullptr;
+thread_local void* g_hook_ctx = nullptr;
 
 // Enqueue one launch between the observer's two calls.
 template <typename F>
@@ -221,6 +237,11 @@ int compress_impl(const void* K, const void* V, int32_t dtype, int64_t B, int64_
       return thin::launch_subsample(S, nm, lv.n_kept, uniforms, lv.U, ws.buf_a, st);
     }));
   const int32_t* cur = lv.sub ? ws.buf_a : nullptr;
+  // the status word is cleared by the v_max launch of the KH path; calls
+  // that make no KH decision clear it here
+  if (lv.L == 0 || halve != THIN_HALVE_KH)
+    ok(observed(THIN_KERNEL_STATUS, -1, st,
+                [&] { return thin::launch_zero_status(ws.status, st); }));
   if (lv.L == 0) {
     if (!assemble)
       ok(observed(THIN_KERNEL_FILL, -1, st, [&] {
@@ -245,8 +266,9 @@ int compress_impl(const void* K, const void* V, int32_t dtype, int64_t B, int64_
       cur = out;
     }
   } else {
-    ok(observed(THIN_KERNEL_VMAX, -1, st,
-                [&] { return thin::launch_vmax(dtype, Vm, S, nm, n, d, ws.vmax_bits, st); }));
+    ok(observed(THIN_KERNEL_VMAX, -1, st, [&] {
+      return thin::launch_vmax(dtype, Vm, S, nm, n, d, ws.vmax_bits, st, ws.status);
+    }));
     int64_t u_off = lv.sub ? lv.n_kept : 0;
     for (int32_t r = 0; r < lv.L && e == hipSuccess; ++r) {
       int32_t* out = (r == lv.L - 1) ? last_out(cur) : (cur == ws.buf_b ? ws.buf_a : ws.buf_b);
@@ -272,6 +294,8 @@ int compress_impl(const void* K, const void* V, int32_t dtype, int64_t B, int64_
       a.h2 = ws.h2;
       a.rowh2 = ws.rowh2;
       a.rowh2_write = r == 0;
+      a.mB = ws.mB;
+      a.status = ws.status;
       a.chunk0 = 0;
       a.b0 = 0;
       ok(kh_round(dtype, d, a, S * lv.G[r], ws.e_bytes, r, st));
@@ -311,7 +335,7 @@ double express_delta(int m, int i, int mbar, double delta) {
 }
 
 struct ExLayout {
-  size_t vmax, E, C[kExMaxL + 1], t1, t2, part, lbt, h2, rowh2, score;
+  size_t status, vmax, E, C[kExMaxL + 1], t1, t2, part, lbt, h2, rowh2, mB, score;
   size_t e_bytes, bytes;
 };
 
@@ -325,6 +349,7 @@ ExLayout ex_layout(int64_t S, int64_t d, int64_t n_out, int32_t mbar, int64_t n_
     return o;
   };
   const size_t s4 = (size_t)S * 4;
+  L.status = take(4);
   L.vmax = take(s4);
   L.E = take(s4 * 4 * n_out);  // up to 4 n_out before the Halve phase
   for (int i = 0; i <= mbar; ++i) L.C[i] = take(s4 * 2 * n_out);
@@ -335,6 +360,7 @@ ExLayout ex_layout(int64_t S, int64_t d, int64_t n_out, int32_t mbar, int64_t n_
   L.lbt = take(s4 * 2 * n_out);
   L.h2 = take(s4 * 2 * n_out);
   L.rowh2 = take(s4 * n_max);
+  L.mB = take(s4 * (size_t)((4 * n_out + 63) / 64));
   const size_t per = thin::halve_score_bytes(4 * n_out);
   const size_t all = (size_t)S * per, cap = per > kScoreCap ? per : kScoreCap;
   L.e_bytes = all < cap ? all : cap;
@@ -468,6 +494,8 @@ hipError_t ex_halve(thin_express* x, const ExRun* run, const int32_t* in, int64_
   a.h2 = ex_ptr<float>(x, x->L.h2);
   a.rowh2 = ex_ptr<float>(x, x->L.rowh2);
   a.rowh2_write = 1;
+  a.mB = ex_ptr<float>(x, x->L.mB);
+  a.status = ex_ptr<int32_t>(x, x->L.status);
   a.chunk0 = 0;
   a.b0 = 0;
   return kh_round(x->dtype, x->d, a, x->S, x->L.e_bytes, -1, st);
@@ -662,6 +690,13 @@ int thin_selftest_gram16(int32_t dtype, int64_t d, const void* rows, float* out,
   return e == hipSuccess ? THIN_OK : THIN_EHIP;
 }
 
+int thin_workspace_status(const void* workspace, int32_t* status, void* stream) {
+  if (!workspace || !status) return THIN_EINVAL;
+  const hipError_t e = hipMemcpyAsync(status, workspace, sizeof(int32_t), hipMemcpyDeviceToHost,
+                                      static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? THIN_OK : THIN_EHIP;
+}
+
 int thin_set_launch_hook(thin_launch_hook_t hook, void* ctx) {
   g_hook = hook;
   g_hook_ctx = ctx;
@@ -701,9 +736,11 @@ struct PfLayout {
   std::vector<std::vector<size_t>> region;     // [m/2][depth] node store of the calls
   std::vector<std::vector<int64_t>> rstride;   // [m/2][depth] its row stride per slice
   std::vector<size_t> enode;                   // [m/2] E after the Halve phase of level m - 2
-  size_t kept, keptrow, keptflag, hp, ein, vmax, lbt, h2, rowh2, score, utab, tiles, segs, c0, w0;
+  size_t status, kept, keptrow, keptflag, hp, ein, vmax, lbt, h2, rowh2, mB, score, utab, tiles,
+      segs, c0, w0;
   size_t e_bytes, bytes;
   int64_t max_tiles, max_segs, max_utab;
+  size_t tab0;  // the host-built tables occupy [tab0, bytes): one copy from the caller's staging
 };
 
 // A run of points attending over one cache (host only): the segments
@@ -729,15 +766,14 @@ PfLayout pf_layout(int64_t S, int64_t n_out, int32_t mbar, int64_t n, const Expr
     return o;
   };
   const size_t s4 = (size_t)S * 4;
+  L.status = take(4);
   L.kept = take(s4 * n);
-  L.keptrow = take(4 * (size_t)n);
-  L.keptflag = take((size_t)n);
   L.hp = take(s4 * 2 * n_out);
   L.ein = take(s4 * 4 * n_out);
   L.region.resize(L.levels + 1);
   L.rstride.resize(L.levels + 1);
   L.enode.resize(L.levels + 2);
-  int64_t gmax = 1, pmax = 2 * n_out, ucount = 0;
+  int64_t gmax = 1, pmax = 2 * n_out, ucount = 0, bmax = (4 * n_out + 63) / 64;
   for (int lv = 0; lv < L.levels; ++lv) {
     const int m = 2 * lv, mp = m < mbar ? m : mbar;
     L.region[lv].assign(mp, 0);
@@ -751,6 +787,7 @@ PfLayout pf_layout(int64_t S, int64_t n_out, int32_t mbar, int64_t n, const Expr
       L.region[lv][dd] = take(s4 * (size_t)L.rstride[lv][dd]);
       gmax = std::max(gmax, c);
       pmax = std::max(pmax, c * (T / 2));
+      bmax = std::max(bmax, c * ((T + 63) / 64));
     }
     L.enode[lv + 1] = take(s4 * n_out);
   }
@@ -758,12 +795,14 @@ PfLayout pf_layout(int64_t S, int64_t n_out, int32_t mbar, int64_t n, const Expr
   L.lbt = take(s4 * pmax);
   L.h2 = take(s4 * pmax);
   L.rowh2 = take(s4 * n);
+  L.mB = take(s4 * (size_t)bmax);
   const size_t per = thin::halve_score_bytes(4 * n_out);
   const size_t all = (size_t)S * per, capb = per > kScoreCap ? per : kScoreCap;
   L.e_bytes = all < capb ? all : capb;
   L.score = take(L.e_bytes);
   // host-built tables: uniform offsets, tiles of 128 points, their cache
-  // pieces, and every point's C_0 start and log-weight
+  // pieces, every point's C_0 start and log-weight, the kept points
+  L.tab0 = off;
   L.max_utab = std::max<int64_t>(ucount, 1);
   L.max_tiles = n / 128 + 2;
   L.max_segs = L.max_tiles * thin::kPrefillMaxSegs;
@@ -772,6 +811,8 @@ PfLayout pf_layout(int64_t S, int64_t n_out, int32_t mbar, int64_t n, const Expr
   L.segs = take(sizeof(thin::PrefillSeg) * (size_t)L.max_segs);
   L.c0 = take(4 * (size_t)n);
   L.w0 = take(4 * (size_t)n);
+  L.keptrow = take(4 * (size_t)n);
+  L.keptflag = take((size_t)n);
   L.bytes = off;
   return L;
 }
@@ -984,6 +1025,8 @@ hipError_t pf_halve(int32_t dtype, int64_t d, int32_t halve, const PfLayout& L,
   a.h2 = reinterpret_cast<float*>(ws + L.h2);
   a.rowh2 = reinterpret_cast<float*>(ws + L.rowh2);
   a.rowh2_write = 1;
+  a.mB = reinterpret_cast<float*>(ws + L.mB);
+  a.status = reinterpret_cast<int32_t*>(ws + L.status);
   if (N <= thin::halve_local_rows(dtype, d))  // every call in one local launch
     return observed(THIN_KERNEL_LOCAL, -1, st,
                     [&] { return thin::launch_local(dtype, d, a, S * G, st); });
@@ -1069,7 +1112,12 @@ int thin_express_step(thin_express_t* x, const void* Q, const void* K, const voi
     app_stride = ex_stride(x, 0);
   }
   const int32_t t = (int32_t)x->n;
-  hipError_t e = observed(THIN_KERNEL_ATTENTION, -1, st, [&] {
+  hipError_t e = hipSuccess;
+  if (t == 0)  // the status word covers every step since the first
+    e = observed(THIN_KERNEL_STATUS, -1, st, [&] {
+      return thin::launch_zero_status(ex_ptr<int32_t>(x, x->L.status), st);
+    });
+  if (e == hipSuccess) e = observed(THIN_KERNEL_ATTENTION, -1, st, [&] {
     return thin::launch_decode_attention(x->dtype, x->d, out_dtype, Q, K, V, g, x->S, x->n_max, m,
                                          ex_ptr<float>(x, x->L.part), O, app, app_stride, t, st);
   });
@@ -1121,6 +1169,7 @@ int thin_express_prefill_plan(int64_t B, int64_t H, int64_t n, int64_t d, int64_
   plan->workspace_bytes = L.bytes;
   plan->attention_keys = qk;
   plan->staged_keys = sk;
+  plan->host_staging_bytes = L.bytes - L.tab0;
   return THIN_OK;
 }
 
@@ -1129,7 +1178,8 @@ int thin_express_prefill(int32_t dtype, int64_t B, int64_t H, int64_t n, int64_t
                          const void* Q, const void* K, const void* V, const float* uniforms,
                          int64_t n_uniforms, const float* draws, int64_t n_draws, void* O,
                          int32_t out_dtype, void* workspace, size_t workspace_bytes,
-                         uint8_t* swap_trace, void* stream) {
+                         void* host_staging, size_t host_staging_bytes, uint8_t* swap_trace,
+                         void* stream) {
   if (dtype != THIN_FP32 && dtype != THIN_BF16) return THIN_EDTYPE;
   if (out_dtype != THIN_FP32 && out_dtype != THIN_BF16) return THIN_EDTYPE;
   if (halve != THIN_HALVE_KH && halve != THIN_HALVE_UNIFORM) return THIN_EINVAL;
@@ -1145,6 +1195,7 @@ int thin_express_prefill(int32_t dtype, int64_t B, int64_t H, int64_t n, int64_t
   if (ndraw > 0 && (!draws || n_draws < ndraw)) return THIN_EINVAL;
   if (!workspace || workspace_bytes < L.bytes) return THIN_EWORKSPACE;
   if ((reinterpret_cast<uintptr_t>(workspace) & 255u) != 0) return THIN_EWORKSPACE;
+  if (!host_staging || host_staging_bytes < L.bytes - L.tab0) return THIN_EWORKSPACE;
   unsigned char* ws = static_cast<unsigned char*>(workspace);
   PfHost h;
   rc = pf_run(n_out, mbar, n, draws, n_draws, &L, ws, &h);
@@ -1166,19 +1217,24 @@ int thin_express_prefill(int32_t dtype, int64_t B, int64_t H, int64_t n, int64_t
     if (v != hipSuccess && e == hipSuccess) e = v;
     return e == hipSuccess;
   };
-  auto up = [&](size_t off, const void* src, size_t bytes) {
-    if (bytes) ok(hipMemcpyAsync(ws + off, src, bytes, hipMemcpyHostToDevice, st));
+  // the tables are laid out in the caller's staging buffer as in the
+  // workspace, then one asynchronous copy moves them (the caller keeps the
+  // staging buffer until the stream has passed this call)
+  unsigned char* hs = static_cast<unsigned char*>(host_staging);
+  auto put = [&](size_t off, const void* src, size_t bytes) {
+    if (bytes) memcpy(hs + (off - L.tab0), src, bytes);
   };
-  up(L.utab, utab.data(), utab.size() * 8);
-  up(L.tiles, h.tiles.data(), h.tiles.size() * sizeof(thin::PrefillTile));
-  up(L.segs, h.psegs.data(), h.psegs.size() * sizeof(thin::PrefillSeg));
-  up(L.c0, h.c0.data(), h.c0.size() * 4);
-  up(L.w0, h.w0.data(), h.w0.size() * 4);
-  up(L.keptrow, h.keptrow.data(), h.keptrow.size() * 4);
-  up(L.keptflag, h.keptflag.data(), h.keptflag.size());
-  // the host tables are pageable and freed on return: finish the copies first
-  if (e == hipSuccess) ok(hipStreamSynchronize(st));
+  put(L.utab, utab.data(), utab.size() * 8);
+  put(L.tiles, h.tiles.data(), h.tiles.size() * sizeof(thin::PrefillTile));
+  put(L.segs, h.psegs.data(), h.psegs.size() * sizeof(thin::PrefillSeg));
+  put(L.c0, h.c0.data(), h.c0.size() * 4);
+  put(L.w0, h.w0.data(), h.w0.size() * 4);
+  put(L.keptrow, h.keptrow.data(), h.keptrow.size() * 4);
+  put(L.keptflag, h.keptflag.data(), h.keptflag.size());
+  ok(hipMemcpyAsync(ws + L.tab0, hs, L.bytes - L.tab0, hipMemcpyHostToDevice, st));
   auto dev = [&](size_t off) { return reinterpret_cast<int32_t*>(ws + off); };
+  ok(observed(THIN_KERNEL_STATUS, -1, st,
+              [&] { return thin::launch_zero_status(dev(L.status), st); }));
   int32_t* kept = dev(L.kept);
   const int64_t nk = (int64_t)h.keptrow.size();
   if (e == hipSuccess && nk > 0)

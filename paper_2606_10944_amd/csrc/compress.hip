@@ -13,9 +13,6 @@ namespace {
 
 constexpr double kLn2 = 0.69314718055994530942;
 constexpr double kLog2e = 1.44269504088896340736;
-// Cross-term exponents (base 2) are clamped here; they exceed the column
-// pair's own diagonal exponent only for data far outside attention ranges.
-constexpr float kExpClamp = 64.0f;
 
 // Row strides of the index lists (0 = packed: n_r in, n_r / 2 out) and the
 // first uniform of bucket t's P pairs within its slice.
@@ -88,9 +85,11 @@ __global__ __launch_bounds__(256) void vmax_kernel(const T* V, int64_t words_per
   }
 }
 
-__global__ void zero_u32_kernel(uint32_t* p, int64_t count) {
+// p[0..count) = 0, and *also = 0 (nullable).
+__global__ void zero_u32_kernel(uint32_t* p, int64_t count, int32_t* also) {
   int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (i < count) p[i] = 0u;
+  if (also && i == 0) *also = 0;
 }
 
 __global__ void zero_u8_kernel(uint8_t* p, int64_t count) {
@@ -316,12 +315,26 @@ __device__ __forceinline__ void quarter_pair_dots(const uint4* fk, const uint4* 
 }
 
 // Scale exponent of a row: its diagonal exponent ||k||^2/sqrt(d) in base 2,
-// rounded to float (sk = <k,k>).  The scale of a pair is the larger of its
-// two rows' values; that float is used wherever the pair's kappa values are
-// scaled by exp(-h).  Rounding is monotonic, so the larger rounded value is
-// the rounded larger exponent, whichever side forms it.
+// rounded up to an integer (sk = <k,k>).  The scale of a pair is the larger
+// of its two rows' values; that value is used wherever the pair's kappa
+// values are scaled by 2^-h.  Integer scales keep every shifted scale
+// (below) exact, and 2^(shifted - h) an exact power of two.
 __device__ __forceinline__ float row_h2f(double sk, double inv_sqrt_d) {
-  return (float)((sk * inv_sqrt_d) * kLog2e);
+  return (float)ceil((sk * inv_sqrt_d) * kLog2e);
+}
+
+// Extra scale of the scores of a block of rows i against pair p.  By
+// Cauchy-Schwarz, <k_i,k_q>/sqrt(d) <= (e_i + e_q)/2 for the diagonal
+// exponents e, so every cross exponent of a row of the block against a row q
+// of pair p is at most (m_B + h_p)/2, m_B = the block's largest row scale.
+// Scaling those kappa values by 2^-(h_p + shift) with
+// shift = max(0, ceil((m_B - h_p)/2)) keeps every exponent <= 0 (no float32
+// overflow, whatever the keys); the block's scores are then 2^-shift times
+// their value at scale h_p, which the decisions undo exactly (ldexp) when
+// they add the block's sums in float64.  Both arguments are integers, so
+// every kernel that forms the shift gets the same value.
+__device__ __forceinline__ float scale_shift(float mB, float h2) {
+  return fmaxf(0.0f, ceilf(0.5f * (mB - h2)));
 }
 __device__ __forceinline__ float pair_h2f(float row_h2) {
   return fmaxf(row_h2, from_partner(row_h2));
@@ -378,10 +391,14 @@ __device__ __forceinline__ void frag_pair_terms(const uint4* fk, const uint4* fv
 //      pairs: one wavefront decides a block (ballot on alpha < a (1 - 2u),
 //      the exact form of "u < min(1, (1 - alpha/a)_+ / 2)"), then every
 //      wavefront adds the block's signed scores to the later pairs' alpha.
-// Scaling: all kappa values feeding pair p are multiplied by exp(-h_p) (h_p
-// as in pair_h2f).  This keeps fp32 exps in range (kappa_att overflows fp32
-// for large keys); the decision only depends on alpha/a, which the common
-// factor leaves unchanged.  E is float32; alpha accumulates in float64.
+// Scaling: alpha_p is accumulated at the scale 2^h_p (h_p as in pair_h2f),
+// the scale of pair p's own terms b and a; the decision only depends on
+// alpha/a, which a common factor leaves unchanged.  The scores of the rows of
+// one 64-row block B against p are stored at the scale 2^(h_p + shift(B,p))
+// (scale_shift), which keeps every float32 exponent of the Gram epilogue at
+// or below 0 whatever the keys (kappa_att overflows float32 for large keys);
+// the decisions multiply each block's signed sum by 2^shift (exact) when they
+// add it to alpha.  E is float32; alpha accumulates in float64.
 //
 // Score layout of one bucket (BR = 16 RT rows = BP pairs per block, NT =
 // ceil(N/16) row tiles): panel B (the block's BP pairs as i) holds one tile
@@ -431,9 +448,11 @@ struct ScoreShape {
   static constexpr int CHUNKS = 2 * NV;        // 1 KB fragment chunks per tile (K, then V)
   static constexpr int LPT = (CHUNKS + kScoreWaves - 1) / kScoreWaves;
   // stages, score tile buffers, pair scale exponents of the group's rows,
-  // row scale exponents of the stages, row indices of the streamed rows
+  // row scale exponents of the stages, the half-blocks' largest row scales,
+  // row indices of the streamed rows
   static constexpr int LDS = kScoreStages * CHUNKS * 1024 + kScoreStages * BLOCKS * kETileLds * 4 +
-                             GT * 16 * 4 + kScoreStages * 16 * 4 + kScoreRowsStaged * 8;
+                             GT * 16 * 4 + kScoreStages * 16 * 4 + 2 * BLOCKS * 4 +
+                             kScoreRowsStaged * 8;
 };
 
 // Block (group-local) and half of half-block slot h of wave w.
@@ -587,8 +606,9 @@ void pair_scores_kernel(HalveArgs a) {
   float* s_e = reinterpret_cast<float*>(smem + NS * CH * 1024);
   float* s_h2 = s_e + (LOCAL ? (int)panel_tiles(nb, NT, 4) : NS * NBW) * kETileLds;  // [GT * 16]
   float* s_hst = s_h2 + GT * 16;                                     // [NS * 16], staged rows
-  int64_t* s_rows = reinterpret_cast<int64_t*>(s_hst + NS * 16);
-  float* s_lbt = s_hst + NS * 16;  // LOCAL: pair terms [P] and [P] (no staged rows there)
+  float* s_mh = s_hst + NS * 16;  // [2 * NBW]: largest row scale of each half-block
+  int64_t* s_rows = reinterpret_cast<int64_t*>(s_mh + 2 * NBW);
+  float* s_lbt = s_mh + 2 * NBW;  // LOCAL: pair terms [P] and [P] (no staged rows there)
   float* s_h2p = s_lbt + P;
 
   // ---- this wave's half-blocks: fragments and, in chunk 0, pair terms ----
@@ -615,15 +635,28 @@ void pair_scores_kernel(HalveArgs a) {
       ridx[k] = j < j_end ? (rows_in ? (int64_t)rows_in[j] : row_base + j) : 0;
     }
   }
-  __builtin_amdgcn_sched_barrier(0);
-  uint4 Ak[HB][2][NV], Av[HB][2][NV];
+  // This wave's rows; a streamed chunk also reads their scale exponents
+  // from the per-row table (requested before the fragments, so that waiting
+  // for them does not wait for the fragments).
+  int64_t ar[HB][2];
+  float arh[HB][2];
 #pragma unroll
   for (int h = 0; h < HB; ++h)
 #pragma unroll
     for (int rt = 0; rt < 2; ++rt) {
       const int j = hb_blk[h] * 64 + hb_half[h] * 32 + rt * 16 + m16;
       const bool valid = hb_ok[h] && j < N;
-      const int64_t r = valid ? (rows_in ? (int64_t)rows_in[j] : row_base + j) : 0;
+      ar[h][rt] = valid ? (rows_in ? (int64_t)rows_in[j] : row_base + j) : -1;
+      arh[h][rt] = (!own && valid) ? a.rowh2[s * a.n + ar[h][rt]] : 0.0f;
+    }
+  __builtin_amdgcn_sched_barrier(0);
+  uint4 Ak[HB][2][NV], Av[HB][2][NV];
+#pragma unroll
+  for (int h = 0; h < HB; ++h)
+#pragma unroll
+    for (int rt = 0; rt < 2; ++rt) {
+      const bool valid = ar[h][rt] >= 0;
+      const int64_t r = valid ? ar[h][rt] : 0;
       load_frag<T, D>(K, r, g, valid, Ak[h][rt]);
       load_frag<T, D>(V, r, g, valid, Av[h][rt]);
     }
@@ -641,6 +674,7 @@ void pair_scores_kernel(HalveArgs a) {
       for (int rt = 0; rt < 2; ++rt) {
         float rh2, h2f, lbt;
         frag_pair_terms<T, D>(Ak[h][rt], Av[h][rt], vm2d, inv_sqrt_d, rh2, h2f, lbt);
+        arh[h][rt] = ar[h][rt] >= 0 ? rh2 : 0.0f;
         const int j = hb_blk[h] * 64 + hb_half[h] * 32 + rt * 16 + m16;
         if (g == 0) s_h2[((hb_blk[h] - grp * NBW) * 4 + hb_half[h] * 2 + rt) * 16 + m16] = h2f;
         if (g == 0 && j < N && (j & 1) == 0) {
@@ -666,6 +700,15 @@ void pair_scores_kernel(HalveArgs a) {
       if (j < j_end) s_rows[j - jt0 * 16] = ridx[k];
     }
   }
+  // the largest row scale of each half-block (rows past the bucket: 0, and
+  // every row scale is >= 0), published in LDS before the tile loop's first
+  // barrier; hb_m[h] = the largest of slot h's block, read after it
+#pragma unroll
+  for (int h = 0; h < HB; ++h) {
+    const float mh = wave_max_f(fmaxf(arh[h][0], arh[h][1]));
+    if (lane == 0) s_mh[(hb_blk[h] - grp * NBW) * 2 + hb_half[h]] = mh;
+  }
+  float hb_m[HB];
 
   // ---- column tiles ----
   // Streamed chunk c of tile jt: lane l holds row jt*16 + l%16 (clamped to
@@ -752,11 +795,11 @@ void pair_scores_kernel(HalveArgs a) {
   do {                                                                                 \
     float* eb_ = LOCAL ? s_e + (panel_tiles(hb_blk[H], NT, 4) + jt_ - 4 * hb_blk[H]) * kETileLds \
                        : s_e + ((BUF) * NBW + hb_blk[H] - grp * NBW) * kETileLds;      \
+    const float he_ = (H2) + scale_shift(hb_m[H], (H2));                               \
     _Pragma("unroll") for (int rt = 0; rt < 2; ++rt) {                                 \
       float kap[4];                                                                    \
       _Pragma("unroll") for (int e = 0; e < 4; ++e)                                    \
-        kap[e] = __builtin_amdgcn_exp2f(fminf(gk[0][H][rt][e] * c2 - (H2), kExpClamp)) * \
-                 gv[0][H][rt][e];                                                      \
+        kap[e] = __builtin_amdgcn_exp2f(gk[0][H][rt][e] * c2 - he_) * gv[0][H][rt][e]; \
       const float F0 = kap[1] - kap[0];                                                \
       const float F1 = kap[3] - kap[2];                                                \
       const float mine_ = odd ? F1 : F0;                                               \
@@ -881,6 +924,7 @@ void pair_scores_kernel(HalveArgs a) {
       const int npb = min(32, P - 32 * m);
       const int gp = 32 * m + min(pl, npb - 1);
       const double thr = block_threshold(s_lbt[gp], s_h2p[gp], Ub[gp], npb, lane, a.log_c, carry);
+      const float h2p = s_h2p[gp];
       double alpha = 0.0;
 #pragma unroll
       for (int b = 0; b < m; ++b) {
@@ -888,14 +932,16 @@ void pair_scores_kernel(HalveArgs a) {
         float sum = 0.0f;
 #pragma unroll
         for (int i = 0; i < 32; ++i) sum += ((masks[b] >> i) & 1u) ? -col[i] : col[i];
-        alpha += (double)sum;
+        alpha += ldexp((double)sum, (int)scale_shift(fmaxf(s_mh[2 * b], s_mh[2 * b + 1]), h2p));
       }
       float ef[32];
       const float* oc = s_e + (panel_tiles(m, NT, 4) + (gp >> 3) - 4 * m) * kETileLds + (gp & 7) * kETileStride;
 #pragma unroll
       for (int i = 0; i < 32; ++i) ef[i] = oc[i];
       float unused = 0.0f;
-      masks[m] = decide_block<false>(alpha, thr, ef, ef, npb, unused);
+      // the block's own scores are at its shifted scale: decide there
+      const int sh = (int)scale_shift(fmaxf(s_mh[2 * m], s_mh[2 * m + 1]), h2p);
+      masks[m] = decide_block<false>(ldexp(alpha, -sh), ldexp(thr, -sh), ef, ef, npb, unused);
       const uint32_t bit = (masks[m] >> pl) & 1u;
       if (lane < npb) {
         const int32_t r0 = rows_in ? rows_in[2 * gp] : (int32_t)(row_base + 2 * gp);
@@ -908,6 +954,15 @@ void pair_scores_kernel(HalveArgs a) {
 
   const bool odd = (m16 & 1) != 0;
   __syncthreads();
+#pragma unroll
+  for (int h = 0; h < HB; ++h) {
+    const int lb = hb_blk[h] - grp * NBW;
+    hb_m[h] = fmaxf(s_mh[2 * lb], s_mh[2 * lb + 1]);
+  }
+  // the decision pass reads each block's largest row scale from here
+  if (!LOCAL && own && (int)threadIdx.x < NBW && grp * NBW + (int)threadIdx.x < nb)
+    a.mB[bucket * nb + grp * NBW + threadIdx.x] =
+        fmaxf(s_mh[2 * threadIdx.x], s_mh[2 * threadIdx.x + 1]);
   if (own) {
     SCORE_OWN_COMMIT(0, 0);
     if (ntile > 1) SCORE_OWN_COMMIT(1, 1);
@@ -1012,14 +1067,18 @@ void pair_scores_kernel(HalveArgs a) {
 // The decider never waits on global memory.  Every wait is bounded.
 constexpr int kSpinLimit = 1 << 16;
 
-// Returns the last value read (>= target unless the spin limit ran out).
-__device__ __forceinline__ int wait_at_least(const int* flag, int target) {
+// Returns the last value read (>= target unless the spin limit ran out).  A
+// wait that runs out sets the call's status word (status nullable): the
+// kernel still ends normally, and the caller learns that this call's
+// decisions cannot be trusted.
+__device__ __forceinline__ int wait_at_least(const int* flag, int target, int32_t* status) {
   int v = 0;
   for (int it = 0; it < kSpinLimit; ++it) {
     v = __hip_atomic_load(flag, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_WORKGROUP);
-    if (v >= target) break;
+    if (v >= target) return v;
     __builtin_amdgcn_s_sleep(1);
   }
+  if (status) __hip_atomic_store(status, kStatusWaitExhausted, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   return v;
 }
 __device__ __forceinline__ void publish(int* flag, int value) {
@@ -1051,7 +1110,12 @@ struct PassLds {
   }
   __host__ __device__ static size_t slot_off(int P) { return flag_off(P) + 64; }
   __host__ __device__ static size_t colbuf_off(int P) { return slot_off(P) + NSLOT * kSlot; }
-  __host__ __device__ static size_t bytes(int P) { return colbuf_off(P) + BW * kColBuf; }
+  // pair scale exponents [P] f32 | largest row scale of every block [nblk] f32
+  __host__ __device__ static size_t h2_off(int P) { return colbuf_off(P) + BW * kColBuf; }
+  __host__ __device__ static size_t mb_off(int P) { return h2_off(P) + (((size_t)P * 4 + 15) & ~(size_t)15); }
+  __host__ __device__ static size_t bytes(int P) {
+    return mb_off(P) + (((size_t)(P + BP - 1) / BP * 4 + 15) & ~(size_t)15);
+  }
 };
 
 template <int BW, int NCB>
@@ -1095,7 +1159,13 @@ __global__ __launch_bounds__(64 * (BW + 2)) void halve_pass_kernel(HalveArgs a) 
   auto sl_own = [&](unsigned char* b) { return reinterpret_cast<u32x4*>(b + BP * 8 + 2 * BP * 4); };
   auto sl_next = [&](unsigned char* b) { return reinterpret_cast<u32x4*>(b + BP * 8 + 2 * BP * 4 + BP * L::CW * 16); };
 
-  for (int p = threadIdx.x; p < P; p += 64 * (BW + 2)) s_alpha[p] = 0.0;
+  float* s_h2 = reinterpret_cast<float*>(smem + L::h2_off(P));
+  float* s_mB = reinterpret_cast<float*>(smem + L::mb_off(P));
+  for (int p = threadIdx.x; p < P; p += 64 * (BW + 2)) {
+    s_alpha[p] = 0.0;
+    s_h2[p] = a.h2[pb + p];
+  }
+  for (int b = threadIdx.x; b < nblk; b += 64 * (BW + 2)) s_mB[b] = a.mB[bucket * nblk + b];
   if (threadIdx.x < 16) s_cnt[threadIdx.x] = threadIdx.x < 2 ? -1 : 0;
   __syncthreads();
 
@@ -1121,19 +1191,22 @@ __global__ __launch_bounds__(64 * (BW + 2)) void halve_pass_kernel(HalveArgs a) 
     double anear = 0.0;             // this lane's pair: the previous block's contribution
     for (int m = 0; m < nblk; ++m) {
       const int npb = min(BP, P - m * BP);
-      wait_at_least(&s_cnt[1], m);
+      wait_at_least(&s_cnt[1], m, a.status);
       // the bulk wave that owns this block's pairs (64-pair chunk m / 2) has
       // added blocks 0 .. m-2 to them
-      if (m >= 2) wait_at_least(&s_cnt[2 + (m >> 1) % BW], m - 1);
+      if (m >= 2) wait_at_least(&s_cnt[2 + (m >> 1) % BW], m - 1, a.status);
       unsigned char* sb = slot(m);
       const int p = lane;
       const int pl = lane & (BP - 1);
       const bool active = p < npb;
       const int gp = m * BP + p;
       const double alpha_in = s_alpha[min(gp, P - 1)] + anear;
-      const double thr = sl_thr(sb)[pl];
+      // the block's own scores are at its shifted scale: decide there
+      const float mBm = s_mB[m];
+      const int sh = (int)scale_shift(mBm, s_h2[min(gp, P - 1)]);
+      const double thr = ldexp(sl_thr(sb)[pl], -sh);
       const int32_t r0 = sl_rows(sb)[pl], r1 = sl_rows(sb)[BP + pl];
-      double alpha = alpha_in;
+      double alpha = ldexp(alpha_in, -sh);
       // this pair's scores against the block's pairs, held in registers
       // before the loop (the loop is the decider's critical path and must
       // not wait on LDS); widened to float64 inside the loop, off the chain.
@@ -1171,7 +1244,7 @@ __global__ __launch_bounds__(64 * (BW + 2)) void halve_pass_kernel(HalveArgs a) 
         if (trace) trace[gp] = (uint8_t)bit;
       }
       // the next block's pairs take this block's signed scores
-      anear = (double)near;
+      anear = ldexp((double)near, (int)scale_shift(mBm, s_h2[min((m + 1) * BP + pl, P - 1)]));
     }
   } else if (wave == 1) {
     // ---- fetcher: block m's inputs into slot m % 3 ----
@@ -1209,7 +1282,7 @@ __global__ __launch_bounds__(64 * (BW + 2)) void halve_pass_kernel(HalveArgs a) 
     const int npb_ = min(BP, P - (B) * BP);                                            \
     const double thr_ = block_threshold(flbt[K], fh2[K], fu[K], npb_, lane, a.log_c, carry); \
     /* slot B%3 held block B-3, which the decider has left once B-2 is decided */    \
-    if ((B) >= L::NSLOT) wait_at_least(&s_cnt[0], (B) - (L::NSLOT - 1));              \
+    if ((B) >= L::NSLOT) wait_at_least(&s_cnt[0], (B) - (L::NSLOT - 1), a.status);    \
     unsigned char* sb_ = slot(B);                                                      \
     _Pragma("unroll") for (int r_ = 0; r_ < 4; ++r_) {                                 \
       sl_own(sb_)[(lane / QW + 8 * r_) * L::CW + lane % QW] = fo[K][r_];               \
@@ -1290,7 +1363,7 @@ __global__ __launch_bounds__(64 * (BW + 2)) void halve_pass_kernel(HalveArgs a) 
 #pragma unroll
       for (int r = 0; r < NCB; ++r) {
         const bool live = more;
-        if (live && decided < b) decided = wait_at_least(&s_cnt[0], b);
+        if (live && decided < b) decided = wait_at_least(&s_cnt[0], b, a.status);
         const uint32_t smask = s_mask[min(b, nblk - 1)];
         u32x4 col[QW];
         if constexpr (L::COAL) {
@@ -1305,7 +1378,8 @@ __global__ __launch_bounds__(64 * (BW + 2)) void halve_pass_kernel(HalveArgs a) 
         float sum;
         PASS_SUM(col, smask, sum);
         const int p = 64 * c + lane;
-        if (live && p >= (b + 2) * BP && p < P) s_alpha[p] += (double)sum;
+        if (live && p >= (b + 2) * BP && p < P)
+          s_alpha[p] += ldexp((double)sum, (int)scale_shift(s_mB[b], s_h2[p]));
         fetch_next(cb[r]);
         if (live) {
           c += BW;
@@ -1504,9 +1578,9 @@ hipError_t launch_decide(const HalveArgs& a0, int64_t nbk, hipStream_t st) {
 }
 
 hipError_t launch_vmax(int dtype, const void* V, int64_t S, int64_t n, int64_t ld, int64_t d,
-                       uint32_t* vmax_bits, hipStream_t st) {
+                       uint32_t* vmax_bits, hipStream_t st, int32_t* status) {
   hipLaunchKernelGGL(zero_u32_kernel, dim3((unsigned)((S + 255) / 256)), dim3(256), 0, st,
-                     vmax_bits, S);
+                     vmax_bits, S, status);
   const int64_t bytes = dtype == 0 ? 4 : 2;
   const int64_t words = n * d * bytes / 16, slice_words = ld * d * bytes / 16;
   const int64_t per_block = 16384;  // 256 KiB of V per workgroup
@@ -1637,6 +1711,11 @@ hipError_t launch_uniform_compress(int64_t S, int64_t n_kept, int32_t L, const i
   }
   hipLaunchKernelGGL(uniform_compress_kernel, dim3((unsigned)S), dim3(kUniformThreads), lds, st,
                      n_kept, L, idx0, U, u_slice, u_off0, idx_out, n_out, trace);
+  return hipGetLastError();
+}
+
+hipError_t launch_zero_status(int32_t* status, hipStream_t st) {
+  hipLaunchKernelGGL(zero_u32_kernel, dim3(1), dim3(64), 0, st, nullptr, 0, status);
   return hipGetLastError();
 }
 

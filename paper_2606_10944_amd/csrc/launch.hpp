@@ -43,12 +43,21 @@ struct HalveArgs {
   int32_t vmax_per_bucket;    // vmax_bits indexed by bucket (s * G + t) instead of slice
   int64_t in_stride;          // idx_in row stride per slice (0: n_r)
   int64_t out_stride;         // idx_out row stride per slice (0: n_r / 2)
+  // Required by the two-launch path
+  float* mB;                  // [buckets, ceil(N / 64)] largest row scale of every 64-row block
+  int32_t* status;            // nullable: set nonzero if a bounded wait of the decisions gave up
 };
+
+// Device status word (the first word of every workspace): 0 = every bounded
+// wait of the call's decision passes completed.
+constexpr int32_t kStatusWaitExhausted = 1;
 
 // dtype: 0 = fp32, 1 = bf16.  Returns a hipError_t.
 // v_max of n rows per slice, slices ld rows apart.
+// status (nullable) is cleared by the same launch.
 hipError_t launch_vmax(int dtype, const void* V, int64_t S, int64_t n, int64_t ld, int64_t d,
-                       uint32_t* vmax_bits, hipStream_t st);
+                       uint32_t* vmax_bits, hipStream_t st, int32_t* status = nullptr);
+hipError_t launch_zero_status(int32_t* status, hipStream_t st);
 hipError_t launch_subsample(int64_t S, int64_t n, int64_t n_kept, const float* U,
                             int64_t u_slice, int32_t* idx0, hipStream_t st);
 hipError_t launch_fill_rows(int64_t S, int64_t n_out, const int32_t* src, int64_t src_stride,

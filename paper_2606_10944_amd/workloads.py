@@ -17,6 +17,13 @@ datasets are not available; the recipes are synthetic:
 * ``long``   B=4  H=16 n=16384 d=128 bf16  Q,K,V ~ N(0,1), 5% of key rows x4  n_out=128 g=3
 * ``stress`` B=1  H=32 n=65536 d=128 bf16  Q,K,V ~ N(0,1)                  n_out=256 g=4
 
+Kind ``heavy_tail_mean`` (a parity case, not a benchmark) is ``long``'s recipe
+with a key mean shared by the rows of a slice: k = z + mu_s, ||mu_s||^2 = 2d
+exactly (a random direction per slice), then 5% of the rows x4.  Keys with a
+common direction are usual in attention layers; here the cross exponents
+<k_i,k_j>/sqrt(d) of the large rows exceed a smaller pair's own diagonal
+exponents by up to ~90 (natural units).
+
 Workload i (1-based, in the order above) uses seed i-1.  ``SeedSequence(seed)
 .spawn(4)`` gives independent PCG64 streams for Q, K, V and the uniforms.
 Values are drawn in float64 and cast once (bf16 by torch's round-to-nearest-
@@ -31,7 +38,7 @@ from typing import Optional, Tuple
 import numpy as np
 import torch
 
-KINDS = ("gauss_d4", "layernorm", "mixture", "heavy_tail", "gauss")
+KINDS = ("gauss_d4", "layernorm", "mixture", "heavy_tail", "gauss", "heavy_tail_mean")
 
 
 @dataclass(frozen=True)
@@ -118,6 +125,18 @@ def make_qkv(w: Workload) -> Tuple[torch.Tensor, torch.Tensor, torch.Tensor]:
         for s in range(S):
             rows = gk.choice(n, size=m, replace=False)
             k2[s, rows, :] *= 4.0
+        v = gv.standard_normal(shape_kv)
+    elif w.kind == "heavy_tail_mean":
+        q = gq.standard_normal(shape_q)
+        k = gk.standard_normal(shape_kv).reshape(S, n, d)
+        mu = gk.standard_normal((S, 1, d))
+        mu *= np.sqrt(2.0 * d) / np.linalg.norm(mu, axis=-1, keepdims=True)
+        k += mu
+        m = int(0.05 * n)
+        for s in range(S):
+            rows = gk.choice(n, size=m, replace=False)
+            k[s, rows, :] *= 4.0
+        k = k.reshape(shape_kv)
         v = gv.standard_normal(shape_kv)
     elif w.kind == "gauss":
         q = gq.standard_normal(shape_q)

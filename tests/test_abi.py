@@ -235,11 +235,51 @@ def test_prefill_plan_matches_decoding(n_out, mbar, n):
     p = _lib.thin_express_prefill_plan(1, 2, n, 64, n_out, mbar)
     assert p["uniforms_per_slice"] == oracle.express_uniforms(n, n_out, mbar)
     assert p["subsample_draws"] == oracle.express_draws(n, n_out, mbar)
-    assert p["workspace_bytes"] > 0
+    assert p["workspace_bytes"] > 0 and p["host_staging_bytes"] > 0
+    # App. G's per-point key counts (Subsample draws of 0), summed
+    assert p["attention_keys"] == int(oracle.express_keys(n, n_out, mbar).sum())
     L = _lib.lib()
     assert L.thin_express_prefill(1, 1, 2, n, 64, n_out, mbar, 0.5, 0, FAKE, FAKE, FAKE, FAKE,
-                                  1 << 30, None, 0, FAKE, 0, None, 0, None, None) in (
+                                  1 << 30, None, 0, FAKE, 0, None, 0, None, 0, None, None) in (
         _lib.THIN_EWORKSPACE, _lib.THIN_EINVAL)
     assert L.thin_express_prefill(1, 1, 2, n, 64, n_out, mbar, 1.5, 0, FAKE, FAKE, FAKE, FAKE,
-                                  1 << 30, None, 0, FAKE, 0, FAKE, 1 << 40, None, None) == \
-        _lib.THIN_EINVAL
+                                  1 << 30, None, 0, FAKE, 0, FAKE, 1 << 40, FAKE, 1 << 40, None,
+                                  None) == _lib.THIN_EINVAL
+
+
+def test_prefill_requires_host_staging():
+    n_out, mbar, n = 8, 4, 512
+    p = _lib.thin_express_prefill_plan(1, 2, n, 64, n_out, mbar)
+    L = _lib.lib()
+    draws = (C.c_float * 1)()
+    args = [1, 1, 2, n, 64, n_out, mbar, 0.5, 0, FAKE, FAKE, FAKE, FAKE, 1 << 30, draws, 1,
+            FAKE, 0, FAKE, 1 << 40]
+    assert L.thin_express_prefill(*args, None, 0, None, None) == _lib.THIN_EWORKSPACE
+    assert L.thin_express_prefill(*args, FAKE, p["host_staging_bytes"] - 1, None, None) == \
+        _lib.THIN_EWORKSPACE
+
+
+def test_workspace_status_validates_pointers():
+    L = _lib.lib()
+    st = C.c_int32(0)
+    assert L.thin_workspace_status(None, C.byref(st), None) == _lib.THIN_EINVAL
+    assert L.thin_workspace_status(FAKE, None, None) == _lib.THIN_EINVAL
+
+
+def test_shared_mean_workload_reaches_large_cross_exponents():
+    """The heavy_tail_mean recipe is a parity case for kappa_att's range: some
+    cross exponent <k_i,k_q>/sqrt(d) of an earlier row i against a row q of a
+    pair exceeds that pair's larger diagonal exponent ||k||^2/sqrt(d) by more
+    than 64 log(2) = 44.4 (natural units), i.e. by more than 2^64 in kappa."""
+    import numpy as np
+    w = W.custom("hm", B=1, H=1, n=1024, d=128, dtype="bf16", kind="heavy_tail_mean", seed=3)
+    _, K, _ = W.make_qkv(w)
+    k = K[0, 0].double().numpy()
+    X = k @ k.T / np.sqrt(w.d)
+    e = np.diag(X)
+    worst = -np.inf
+    for p in range(1, w.n // 2):
+        hp = max(e[2 * p], e[2 * p + 1])
+        worst = max(worst, X[: 2 * p, 2 * p: 2 * p + 2].max() - hp)
+    assert worst > 64 * np.log(2.0), worst
+    assert abs(np.linalg.norm(k.mean(axis=0)) ** 2 / (2 * w.d) - 1.0) < 0.5

@@ -608,7 +608,7 @@ def _offline_subsample(m, mbar, rows, draws):
 
 
 def _offline_express(n_out, mbar, rows, m, draws):
-    """Offline-Express (App. F, the recursive procedure) on 2^(m+2) n_out points;
+    """Offline-Express (App. H, Algorithm H.3, the recursive procedure) on 2^(m+2) n_out points;
     the draws are taken in the order the recursion meets the strata."""
     if rows.size <= n_out:
         return rows
@@ -623,7 +623,7 @@ def _offline_express(n_out, mbar, rows, m, draws):
 @pytest.mark.parametrize("n_out,mbar,levels", [(4, 2, 2), (8, 4, 3), (16, 6, 3), (16, 4, 2),
                                                (4, 2, 3), (8, 2, 4), (16, 3, 4)])
 def test_streaming_express_equals_offline_express(n_out, mbar, levels):
-    """The streaming procedure equals the recursive offline one (App. F);
+    """The streaming procedure equals the recursive offline one (App. H, Algorithm H.3);
     with a deterministic Halve (uniform halving with every u >= 1/2 keeps
     the first point of each pair) and the same Subsample draws (levels above
     mbar) both must return the same coreset."""
@@ -678,3 +678,46 @@ def test_express_subsample_cache_weights_count_whole_strata():
                                   sub_u=draws)
         assert np.exp(r["logw"]).sum() * 2.0 ** r["m"] == pytest.approx(n, rel=1e-12)
         assert r["idx"].size == n_out and np.unique(r["idx"]).size == n_out
+
+
+def _wtd_attention_cost(n, n_out, mbar):
+    """App. G, proposition "Cost of WtdAttention" (eq. streaming_express_query),
+    in keys (the d factor common to every term dropped): the keys summed over
+    the first n queries of Thinformer decoding, m_n = 2 ceil(log4(n / (4 n_out)))."""
+    if n <= 4 * n_out:
+        return n * (n + 1) // 2
+    mn, q = 0, 4 * n_out
+    while q < n:
+        q *= 4
+        mn += 2
+    base = 2 * n_out * (4 * n_out + 1)
+    if mn <= mbar:
+        return base + (7 * n_out * n_out - n_out) * (2 ** (mn + 2) - 4) // 2 \
+            - 3 * (mn // 2) * n_out * n_out
+    return base + 6 * n_out * (n - 4 * n_out)
+
+
+@pytest.mark.parametrize("n_out,mbar", [(4, 2), (8, 2), (8, 4), (16, 4), (16, 5), (32, 3), (32, 6)])
+def test_wtd_attention_query_cost_proposition(n_out, mbar):
+    """The oracle's per-point key counts against App. G's proposition.  Its
+    proof counts a thin-phase query's cache without the query's own key (the
+    exact phase counts it), while WtdAttention (Alg. 5) adds the query to C_0,
+    so with the query counted the sum is the proposition's value plus one per
+    thin-phase point: equal in the exact phase and at every level end
+    n = n_out 4^k with m_n <= mbar (the proposition's endpoints), below it
+    elsewhere; at most the cache bound 6 n_out (+ the query) once m_n > mbar."""
+    n_max = n_out * 4 ** (mbar // 2 + 2)
+    keys = oracle.express_keys(n_max, n_out, mbar)
+    cum = np.concatenate([[0], np.cumsum(keys)])
+    assert np.all(keys <= 6 * n_out + 1)
+    ends = 0
+    for n in range(1, n_max + 1):
+        bound = _wtd_attention_cost(n, n_out, mbar) + max(n - 4 * n_out, 0)
+        assert cum[n] <= bound, (n, cum[n], bound)
+        if n <= 4 * n_out:
+            assert cum[n] == n * (n + 1) // 2
+        k = round(math.log(n / n_out, 4)) if n >= n_out else -1
+        if k >= 2 and n == n_out * 4 ** k and 2 * k - 2 <= mbar:
+            assert cum[n] == bound, (n, cum[n], bound)
+            ends += 1
+    assert ends >= 1

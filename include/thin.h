@@ -121,6 +121,32 @@ int thin_compress(const void* K, const void* V, int32_t dtype, int64_t B, int64_
                   size_t workspace_bytes, void* stream);
 
 /*
+ * thin_compress for callers that cannot allocate device memory (code under
+ * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc):
+ * no workspace argument; the workspace is a static device array of
+ * THIN_STATIC_SCRATCH_BYTES that every GPU the library runs on holds from
+ * the time the library's code is loaded on it until the process ends.  The
+ * call allocates nothing (no hipMalloc / hipFree).
+ *   Arguments, layouts and results as thin_compress (KH, delta = 1/2), on
+ *   the calling thread's current device (the device of `stream`).
+ *   status  (device, nullable) int32: receives the call's device status word
+ *           (see the conventions above), ordered after its kernels.
+ * The score region takes what the other regions leave, so rounds whose
+ * buckets' scores do not all fit run in several launches (same result).
+ * Calls on one GPU share the array, which keeps the last call's contents:
+ * calls that overlap in time on one GPU (different streams or threads) race
+ * and must not be made; calls ordered on one stream are fine.
+ * Errors: those of thin_compress, and THIN_EWORKSPACE when the call needs
+ * more than THIN_STATIC_SCRATCH_BYTES (index lists, pair terms and row
+ * scales grow with B*H*n; the long workload B=4 H=16 n=16384 and the stress
+ * workload B=1 H=32 n=65536 fit).
+ */
+#define THIN_STATIC_SCRATCH_BYTES ((size_t)128 << 20)
+int thin_compress_static(const void* K, const void* V, int32_t dtype, int64_t B, int64_t H,
+                         int64_t n, int64_t d, int64_t n_out, int32_t g, const float* uniforms,
+                         int64_t n_uniforms, int32_t* idx_out, int32_t* status, void* stream);
+
+/*
  * thin_compress plus a record of every swap decision, for checking a run
  * against a reference implementation.
  *   swap_trace  (device) uint8 [B*H*U], indexed exactly like `uniforms`:

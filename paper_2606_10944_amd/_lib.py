@@ -22,7 +22,7 @@ THIN_FP32, THIN_BF16 = 0, 1
 THIN_STATUS_WAIT_EXHAUSTED = 1
 
 # Every symbol include/thin.h declares.
-EXPORTS = ("thin_plan", "thin_compress", "thin_compress_traced", "thin_compress_ex", "thin_attention",
+EXPORTS = ("thin_plan", "thin_compress", "thin_compress_static", "thin_compress_traced", "thin_compress_ex", "thin_attention",
            "thin_attention_ex", "thin_express_plan", "thin_express_create", "thin_express_step",
            "thin_express_cache", "thin_express_next", "thin_express_destroy",
            "thin_express_prefill_plan", "thin_express_prefill",
@@ -85,6 +85,7 @@ def lib():
     P, I64, I32, SZ = C.c_void_p, C.c_int64, C.c_int32, C.c_size_t
     L.thin_plan.argtypes = [I64, I64, I64, I64, I64, I32, C.POINTER(Plan)]
     L.thin_compress.argtypes = [P, P, I32, I64, I64, I64, I64, I64, I32, P, I64, P, P, SZ, P]
+    L.thin_compress_static.argtypes = [P, P, I32, I64, I64, I64, I64, I64, I32, P, I64, P, P, P]
     L.thin_compress_traced.argtypes = [P, P, I32, I64, I64, I64, I64, I64, I32, P, I64, P, P,
                                        SZ, P, I64, P]
     L.thin_compress_ex.argtypes = [P, P, I32, I64, I64, I64, I64, I64, I32, P, I64, P, P, SZ,
@@ -107,7 +108,8 @@ def lib():
     L.thin_status_str.restype = C.c_char_p
     L.thin_set_launch_hook.argtypes = [LaunchHook, P]
     L.thin_set_launch_hook.restype = C.c_int
-    for f in ("thin_plan", "thin_compress", "thin_compress_traced", "thin_compress_ex",
+    for f in ("thin_plan", "thin_compress", "thin_compress_static", "thin_compress_traced",
+              "thin_compress_ex",
               "thin_attention", "thin_attention_ex", "thin_selftest_gram16", "thin_express_plan",
               "thin_express_create", "thin_express_step", "thin_express_cache",
               "thin_express_next", "thin_express_destroy", "thin_express_prefill_plan",

@@ -6,7 +6,8 @@ import sys
 HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 SO = os.path.join(HERE, "libthin.so")
-SOURCES = ["csrc/compress.hip", "csrc/attention.hip", "csrc/express.hip", "csrc/api.cpp"]
+SOURCES = ["csrc/compress.hip", "csrc/attention.hip", "csrc/express.hip", "csrc/api.cpp",
+           "csrc/noalloc.hip"]
 FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared",
     # no packed fp32 instructions in device code

@@ -74,7 +74,7 @@ constexpr int64_t kLocalMaxBuckets = 2048;
 
 size_t score_bytes(int64_t N) { return thin::halve_score_bytes(N); }
 
-size_t score_region(int64_t S, int64_t d, const Levels& lv) {
+size_t score_region(int64_t S, int64_t d, const Levels& lv, size_t cap_bytes = kScoreCap) {
   size_t region = 0;
   // rounds whose buckets run as one local launch (for either dtype) need none
   const int64_t local = std::min(thin::halve_local_rows(0, d), thin::halve_local_rows(1, d));
@@ -82,7 +82,7 @@ size_t score_region(int64_t S, int64_t d, const Levels& lv) {
     if (lv.N[r] <= local && S * lv.G[r] < kLocalMaxBuckets) continue;
     const size_t per = score_bytes(lv.N[r]);
     const size_t all = (size_t)(S * lv.G[r]) * per;
-    const size_t cap = per > kScoreCap ? per : kScoreCap;
+    const size_t cap = per > cap_bytes ? per : cap_bytes;
     const size_t need = all < cap ? all : cap;
     if (need > region) region = need;
   }
@@ -111,7 +111,7 @@ struct Workspace {
   size_t bytes;
 };
 
-Workspace carve(void* base, int64_t S, int64_t d, const Levels& lv) {
+Workspace carve(void* base, int64_t S, int64_t d, const Levels& lv, size_t cap = kScoreCap) {
   Workspace w;
   unsigned char* p = static_cast<unsigned char*>(base);
   const size_t pairs = (size_t)S * (size_t)(lv.n_kept / 2);
@@ -133,14 +133,14 @@ Workspace carve(void* base, int64_t S, int64_t d, const Levels& lv) {
   w.mB = reinterpret_cast<float*>(p + off);
   off += align256(block_scales(S, lv) * 4);
   w.E = reinterpret_cast<float*>(p + off);
-  w.e_bytes = score_region(S, d, lv);
+  w.e_bytes = score_region(S, d, lv, cap);
   off += align256(w.e_bytes);
   w.bytes = off;
   return w;
 }
 
-size_t workspace_size(int64_t S, int64_t d, const Levels& lv) {
-  return carve(nullptr, S, d, lv).bytes;
+size_t workspace_size(int64_t S, int64_t d, const Levels& lv, size_t cap = kScoreCap) {
+  return carve(nullptr, S, d, lv, cap).bytes;
 }
 
 // The launch observer is a diagnostic of the calling thread (thread-local):
@@ -192,7 +192,7 @@ int compress_impl(const void* K, const void* V, int32_t dtype, int64_t B, int64_
                   int64_t d, int64_t n_out, int32_t g, const float* uniforms, int64_t n_uniforms,
                   int32_t* idx_out, void* workspace, size_t workspace_bytes, uint8_t* trace,
                   int64_t trace_len, int32_t halve, const double* delta, int64_t n_sinks,
-                  int64_t n_window, float* logw_out, void* stream) {
+                  int64_t n_window, float* logw_out, void* stream, size_t cap = kScoreCap) {
   int rc = check_shape(B, H, n, d);
   if (rc) return rc;
   if (dtype != THIN_FP32 && dtype != THIN_BF16) return THIN_EDTYPE;
@@ -211,9 +211,9 @@ int compress_impl(const void* K, const void* V, int32_t dtype, int64_t B, int64_
   if (halve == THIN_HALVE_KH && delta)
     for (int32_t r = 0; r < lv.L; ++r)
       if (!(delta[r] > 0.0 && delta[r] <= 1.0)) return THIN_EINVAL;
-  if (!workspace || workspace_bytes < workspace_size(S, d, lv)) return THIN_EWORKSPACE;
+  if (!workspace || workspace_bytes < workspace_size(S, d, lv, cap)) return THIN_EWORKSPACE;
   if ((reinterpret_cast<uintptr_t>(workspace) & 255u) != 0) return THIN_EWORKSPACE;
-  Workspace ws = carve(workspace, S, d, lv);
+  Workspace ws = carve(workspace, S, d, lv, cap);
   hipStream_t st = static_cast<hipStream_t>(stream);
   const size_t esz = dtype == THIN_FP32 ? 4 : 2;
   const void* Km = static_cast<const unsigned char*>(K) + (size_t)n_sinks * (size_t)d * esz;
@@ -316,6 +316,43 @@ int compress_impl(const void* K, const void* V, int32_t dtype, int64_t B, int64_
   return e == hipSuccess ? THIN_OK : THIN_EHIP;
 }
 
+
+}  // namespace
+
+namespace thin {
+
+// thin_compress into a workspace of a fixed size `bytes`: the score region
+// takes what the other regions leave (rounds whose buckets do not all fit
+// run in several launches).  *need (nullable) receives the bytes the call
+// uses; THIN_EWORKSPACE if not even one bucket of every round fits.  With
+// workspace == NULL only the arguments' sizes are checked (nothing runs).
+int compress_fixed(const void* K, const void* V, int32_t dtype, int64_t B, int64_t H, int64_t n,
+                   int64_t d, int64_t n_out, int32_t g, const float* uniforms,
+                   int64_t n_uniforms, int32_t* idx_out, void* workspace, size_t bytes,
+                   size_t* need, void* stream) {
+  int rc = check_shape(B, H, n, d);
+  if (rc) return rc;
+  Levels lv;
+  if (!make_levels(n, n_out, g, &lv) || lv.max_bucket > kMaxBucket) return THIN_EINVAL;
+  const int64_t S = B * H;
+  // the largest single bucket's scores (0 if every round is local), and
+  // every region but the scores
+  const size_t one = align256(score_region(S, d, lv, 0));
+  const size_t fixed = workspace_size(S, d, lv, 0) - one;
+  if (fixed + one > bytes) return THIN_EWORKSPACE;
+  const size_t cap = (bytes - fixed) & ~(size_t)255;
+  const size_t used = workspace_size(S, d, lv, cap);
+  if (used > bytes) return THIN_EWORKSPACE;
+  if (need) *need = used;
+  if (!workspace) return THIN_OK;
+  return compress_impl(K, V, dtype, B, H, n, d, n_out, g, uniforms, n_uniforms, idx_out,
+                       workspace, bytes, nullptr, 0, THIN_HALVE_KH, nullptr, 0, 0, nullptr,
+                       stream, cap);
+}
+
+}  // namespace thin
+
+namespace {
 
 // ---------------------------------------------------------------------------
 // Express cache (Alg. 1 with Subsample of Alg. 3 and Compress2 of Alg. 2) and

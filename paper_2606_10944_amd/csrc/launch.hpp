@@ -52,6 +52,14 @@ struct HalveArgs {
 // wait of the call's decision passes completed.
 constexpr int32_t kStatusWaitExhausted = 1;
 
+// thin_compress (KH, no trace) into a workspace of exactly `bytes` (api.cpp):
+// the score region takes what the other regions leave.  workspace == NULL:
+// validation only.  *need receives the bytes used.  Returns a thin_status_t.
+int compress_fixed(const void* K, const void* V, int32_t dtype, int64_t B, int64_t H, int64_t n,
+                   int64_t d, int64_t n_out, int32_t g, const float* uniforms,
+                   int64_t n_uniforms, int32_t* idx_out, void* workspace, size_t bytes,
+                   size_t* need, void* stream);
+
 // dtype: 0 = fp32, 1 = bf16.  Returns a hipError_t.
 // v_max of n rows per slice, slices ld rows apart.
 // status (nullable) is cleared by the same launch.

@@ -283,3 +283,14 @@ def test_shared_mean_workload_reaches_large_cross_exponents():
         worst = max(worst, X[: 2 * p, 2 * p: 2 * p + 2].max() - hp)
     assert worst > 64 * np.log(2.0), worst
     assert abs(np.linalg.norm(k.mean(axis=0)) ** 2 / (2 * w.d) - 1.0) < 0.5
+
+
+def test_static_compress_rejects_what_does_not_fit_before_any_launch():
+    """thin_compress_static checks sizes against its fixed array before it
+    touches a device: B*H = 256 slices of 65536 rows need more than it holds."""
+    L = _lib.lib()
+    rc = L.thin_compress_static(FAKE, FAKE, 1, 8, 32, 65536, 128, 256, 4, FAKE, 1 << 40, FAKE,
+                                None, None)
+    assert rc == _lib.THIN_EWORKSPACE
+    assert L.thin_compress_static(FAKE, FAKE, 1, 1, 1, 1000, 80, 8, 1, FAKE, 1 << 20, FAKE,
+                                  None, None) == _lib.THIN_EINVAL  # d unsupported

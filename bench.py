@@ -99,14 +99,21 @@ def kappa_evals(plan, w) -> int:
     return tot * w.S
 
 
-def score_bytes(w, plan) -> list:
-    """Algorithmic HBM bytes of each round's pair-score launch: the round's K and
-    V rows read once, their int32 indices (not in round 0 without subsample),
-    the float32 pair scores written (8 x 32 tiles over each 64-row block and
-    the columns from its diagonal on) and two float32 pair terms per pair."""
+def round_bytes(w, plan) -> list:
+    """Algorithmic HBM bytes of each Halve round (the per-round term of the
+    compress byte model): the round's K and V rows read once and their int32
+    indices, S n_r (2 d b + 4)."""
     b = elem_bytes(w.dtype)
+    n_kept, L = plan["n_kept"], plan["rounds"]
+    return [w.S * (n_kept >> r) * (2 * w.d * b + 4) for r in range(L)]
+
+
+def score_buffer_bytes(w, plan) -> list:
+    """Bytes this design adds to each round's pair-score launch (not part of
+    the algorithm): the float32 pair scores written (8 x 32 tiles over each
+    64-row block and the columns from its diagonal on) and two float32 pair
+    terms per pair; the decision pass reads them back."""
     n_kept, L, g = plan["n_kept"], plan["rounds"], w.g
-    sub = n_kept < w.n
     out = []
     for r in range(L):
         n_r = n_kept >> r
@@ -115,10 +122,7 @@ def score_bytes(w, plan) -> list:
         N = n_r // G
         NT, nb = (N + 15) // 16, (N + 63) // 64
         tiles = nb * NT - 4 * nb * (nb - 1) // 2
-        by = n_r * 2 * w.d * b + G * tiles * 1024 + (n_r // 2) * 8
-        if r > 0 or sub:
-            by += n_r * 4
-        out.append(w.S * by)
+        out.append(w.S * (G * tiles * 1024 + (n_r // 2) * 8))
     return out
 
 
@@ -158,6 +162,24 @@ def attention_flops(w) -> int:
     return w.S * w.n_q * 4 * w.n_out * w.d
 
 
+def host_cpu() -> dict:
+    """CPU model and logical core count of the host that runs the oracle."""
+    model = "unknown"
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    try:
+        avail = len(os.sched_getaffinity(0))
+    except AttributeError:
+        avail = os.cpu_count()
+    return {"cpu_model": model, "host_cores": os.cpu_count(), "cores_available": avail}
+
+
 def cpu_baseline(w, Q, K, V, U, plan, budget_s: float = 20.0, halve: str = "kh",
                  n_sinks: int = 0, n_window: int = 0):
     """The oracle, single-threaded, on as many whole slices as fit the budget."""
@@ -183,7 +205,7 @@ def cpu_baseline(w, Q, K, V, U, plan, budget_s: float = 20.0, halve: str = "kh",
             break
     _ = np  # noqa: F841
     return {"value": done * w.n_q / t_used, "unit": "(B·H·n)/s", "cores": 1,
-            "kind": "oracle",
+            "kind": "oracle", **host_cpu(),
             "sample": f"{done} of {w.S} slices of the {w.name} workload (compress + "
                       f"attention of all {w.n_q} queries per slice), float64, one thread, "
                       f"{t_used:.1f} s"}
@@ -474,7 +496,8 @@ def main():
     cb = compress_bytes(wc, plan) if args.halve == "kh" else uniform_compress_bytes(wc, plan)
     if weighted:  # the layout launch: m indices and m log-weights per slice
         cb += w.S * wa.n_out * 8
-    sb = score_bytes(wc, plan)
+    rb = round_bytes(wc, plan)
+    ib = score_buffer_bytes(wc, plan)
     ab = attention_bytes(wa, 4, weighted)
     af = attention_flops(wa)
     kev = kappa_evals(plan, wc) if args.halve == "kh" else 0
@@ -484,9 +507,29 @@ def main():
     sc_rounds = sorted({r for name, r, _ in rec if name == "scores"})  # the others run local
     if n_sc:
         sc_ms_launch = statistics.mean(score_ms)
-        sc_bytes_launch = sum(sb[r] for r in sc_rounds) / n_sc
+        sc_bytes_launch = sum(rb[r] for r in sc_rounds) / n_sc
+        sc_impl_launch = sum(ib[r] for r in sc_rounds) / n_sc
         sc_gbs = sc_bytes_launch / (sc_ms_launch * 1e-3) / 1e9
+        # per round: its score launches' time per step and the fraction of
+        # the HBM roofline its algorithmic bytes reach
+        by_round = {}
+        for r in sc_rounds:
+            ms_r = sum(ms for name, rr, ms in rec if name == "scores" and rr == r) / args.steps
+            by_round[r] = {"ms": ms_r, "frac": rb[r] / (ms_r * 1e-3) / 1e9 / HBM_PEAK_GBS}
     traffic = stored_traffic(w.name) if args.halve == "kh" and not weighted else None
+    # bf16 output (half the output bytes; the precision of the parity tests
+    # is fp32 output): the same attention timed on its own, after the steps
+    Ob = torch.empty((w.B, w.H, w.n_q, w.d), dtype=torch.bfloat16, device=dev)
+    thin_attention(Qd, Kd, Vd, idx, logw=lw, O=Ob, stream=stream)
+    b0 = torch.cuda.Event(enable_timing=True)
+    b1 = torch.cuda.Event(enable_timing=True)
+    b0.record(stream)
+    for _ in range(args.steps):
+        thin_attention(Qd, Kd, Vd, idx, logw=lw, O=Ob, stream=stream)
+    b1.record(stream)
+    torch.cuda.synchronize()
+    ta16 = b0.elapsed_time(b1) / args.steps
+    ab16 = attention_bytes(wa, 2, weighted)
     attn_gbs = ab / (ta * 1e-3) / 1e9
     attn_tflops = af / (ta * 1e-3) / 1e12
     value = w.S * w.n_q / (ms_step * 1e-3)
@@ -513,8 +556,11 @@ def main():
             "bound": "hbm", "achieved": sc_gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
             "frac": sc_gbs / HBM_PEAK_GBS,
             "traffic": traffic,
-            "algorithmic_bytes_per_launch": sc_bytes_launch, "ms_per_launch": sc_ms_launch,
-            "launches_per_step": n_sc, "rounds": sc_rounds,
+            "traffic_over_algorithmic": traffic / sc_bytes_launch if traffic else None,
+            "algorithmic_bytes_per_launch": sc_bytes_launch,
+            "impl_bytes_per_launch": sc_impl_launch,
+            "ms_per_launch": sc_ms_launch,
+            "launches_per_step": n_sc, "rounds": sc_rounds, "by_round": by_round,
         } if n_sc else {
             # uniform halving evaluates no kernel: attention is the dominant kernel
             "kernel": "coreset attention (one launch per step)",
@@ -531,6 +577,14 @@ def main():
             "mfma_frac": attn_tflops / (BF16_MFMA_PEAK_TFLOPS if w.dtype == "bf16"
                                         else FP32_MFMA_PEAK_TFLOPS),
             "algorithmic_bytes": ab, "flops": af,
+        },
+        "attention_bf16_out": {
+            "ms": ta16, "hbm_gbs": ab16 / (ta16 * 1e-3) / 1e9,
+            "hbm_frac": ab16 / (ta16 * 1e-3) / 1e9 / HBM_PEAK_GBS,
+            "mfma_tflops": af / (ta16 * 1e-3) / 1e12,
+            "mfma_frac": af / (ta16 * 1e-3) / 1e12 / (BF16_MFMA_PEAK_TFLOPS if w.dtype == "bf16"
+                                                      else FP32_MFMA_PEAK_TFLOPS),
+            "algorithmic_bytes": ab16,
         },
         "ms_per_step_by_kernel": dict(per_step),
         "gpu": torch.cuda.get_device_name(0),

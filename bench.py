@@ -311,7 +311,7 @@ def decode_main(args):
             if t_used >= 20.0:
                 break
         out["cpu_baseline"] = {
-            "value": done * w.n / t_used, "unit": "points/s", "cores": 1, "kind": "oracle",
+            "value": done * w.n / t_used, "unit": "points/s", "cores": 1, "kind": "oracle", **host_cpu(),
             "sample": f"{done} of {w.S} slices decoded over all {w.n} points, float64, one "
                       f"thread, {t_used:.1f} s"}
     _ = np  # noqa: F841
@@ -396,7 +396,7 @@ def prefill_main(args):
                               sub_u=draws.numpy())
         t_used = time.perf_counter() - t_a
         out["cpu_baseline"] = {
-            "value": w.n / t_used, "unit": "points/s", "cores": 1, "kind": "oracle",
+            "value": w.n / t_used, "unit": "points/s", "cores": 1, "kind": "oracle", **host_cpu(),
             "sample": f"1 of {w.S} slices, all {w.n} points, float64, one thread, "
                       f"{t_used:.1f} s"}
     print(json.dumps(out), flush=True)

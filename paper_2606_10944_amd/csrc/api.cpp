@@ -633,7 +633,7 @@ int ex_check(int64_t B, int64_t H, int64_t d, int64_t n_out, int32_t mbar, int64
     const int64_t k = seg_total(ex_segs(&x, true));
     if (k > km) km = k;
     const bool keep = x.n >= n_out ? ex_keep(&x, nullptr) : true;
-    ex_update(&x, nullptr, keep);
+    (void)ex_update(&x, nullptr, keep);  // count only: launches nothing
   }
   *u_slice = x.upos;
   *kmax = km;
@@ -947,7 +947,7 @@ int pf_run(int64_t n_out, int32_t mbar, int64_t n, const float* draws, int64_t n
     if (keep) h->keptrow.push_back((int32_t)p);
     const int m_before = x.m;
     const int64_t c0 = h->rec.count(m_before, 0);
-    ex_update(&x, nullptr, keep);
+    (void)ex_update(&x, nullptr, keep);  // count only: launches nothing
     if (x.n == n_out)
       causal0 = n_out;
     else if (x.n > n_out && (h->rec.count(m_before, 0) != c0 || x.ell == 0))

@@ -79,19 +79,24 @@ __global__ void express_keys_kernel(ExpressSegs segs, int64_t m, int64_t out_str
 // ---------------------------------------------------------------------------
 // Weighted attention of one query per slice (a decoding step, Alg. 5) over
 // the m keys of the cache segments (read in place: no key list is written),
-// each key with its segment's log-weight.  The keys of a slice
-// are split over `split` workgroups; in a workgroup, wave w takes keys
-// k0 + w, k0 + w + 4, ..; a key's row is spread over the lanes (EPL elements
-// each), its score reduced across the wave, and each wave keeps an online
-// softmax (log2 domain) of its keys.  The waves merge in LDS and the
-// workgroup writes its unnormalised partial (max, sum, acc[D]); a second
-// kernel merges a slice's partials and normalises.
+// each key with its segment's log-weight.  The keys of a slice are split
+// over `split` workgroups of 16 waves; a wave takes a contiguous run of keys
+// and reads them with 16-byte loads, a key row spread over LPK lanes, so one
+// load instruction brings 64 / LPK keys (4 bf16 rows of d = 128) and a wave
+// keeps kDecUnroll such loads of K and of V in flight.  Each lane group of a
+// key keeps an online softmax (log2 domain) of its keys; the groups merge by
+// lane shuffles, the waves in LDS.  split == 1: the workgroup normalises and
+// writes the output row itself (one launch per step); else it writes its
+// unnormalised partial (max, sum, acc[D]) and a second kernel merges them.
 // ---------------------------------------------------------------------------
-constexpr int kDecWaves = 4;
-constexpr int kDecUnroll = 4;
+#ifndef DEC_WAVES
+#define DEC_WAVES 16
+#endif
+constexpr int kDecWaves = DEC_WAVES;
+constexpr int kDecUnroll = 8;
 
 // Row and log-weight of key j of slice s (segments as in express_keys_kernel).
-// (k, off) is a cursor: segment k starts at key off; a wave's keys increase,
+// (k, off) is a cursor: segment k starts at key off; a lane's keys increase,
 // so the cursor only moves forward.
 __device__ __forceinline__ int64_t seg_key(const ExpressSegs& segs, int64_t s, int64_t j, int& k,
                                            int64_t& off, float* lw) {
@@ -101,102 +106,29 @@ __device__ __forceinline__ int64_t seg_key(const ExpressSegs& segs, int64_t s, i
   return g.src ? (int64_t)g.src[s * g.stride + (j - off)] : g.start + (j - off);
 }
 
-template <typename T>
-__device__ __forceinline__ void load_elems(const T* p, float* out, int n);
-template <>
-__device__ __forceinline__ void load_elems<float>(const float* p, float* out, int n) {
-  for (int e = 0; e < n; ++e) out[e] = p[e];
-}
-template <>
-__device__ __forceinline__ void load_elems<bf16_t>(const bf16_t* p, float* out, int n) {
-  const uint16_t* q = reinterpret_cast<const uint16_t*>(p);
-  for (int e = 0; e < n; ++e) out[e] = __uint_as_float((uint32_t)q[e] << 16);
+// seg_key over a segment table staged in LDS.
+__device__ __forceinline__ int64_t seg_key_lds(const ExpressSeg* seg, int n, int64_t s, int64_t j,
+                                               int& k, int64_t& off, float* lw) {
+  while (k + 1 < n && j >= off + seg[k].len) off += seg[k++].len;
+  const ExpressSeg& g = seg[k];
+  *lw = g.logw;
+  return g.src ? (int64_t)g.src[s * g.stride + (j - off)] : g.start + (j - off);
 }
 
-template <typename T, int D>
-__global__ __launch_bounds__(64 * kDecWaves) void decode_attn_partial_kernel(
-    const T* __restrict__ Q, const T* __restrict__ K, const T* __restrict__ V, ExpressSegs segs,
-    int64_t ld, int64_t m, int split, float* __restrict__ part) {
-  constexpr int EPL = D >= 64 ? D / 64 : 1;  // elements per lane
-  constexpr int ACT = D / EPL;               // active lanes
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int64_t s = blockIdx.y;
-  const int64_t k0 = m * blockIdx.x / split, k1 = m * (blockIdx.x + 1) / split;
-  const bool act = lane < ACT;
-  const float c2 = (float)(1.4426950408889634 / sqrt((double)D));
-  const float l2e = 1.4426950408889634f;
-  float q[EPL];
-  if (act) load_elems<T>(Q + s * D + lane * EPL, q, EPL);
-  else
-    for (int e = 0; e < EPL; ++e) q[e] = 0.f;
-  const T* Ks = K + s * ld * D;
-  const T* Vs = V + s * ld * D;
-  float mrun = -INFINITY, lrun = 0.f, acc[EPL];
-  for (int e = 0; e < EPL; ++e) acc[e] = 0.f;
-  int kseg = 0;
-  int64_t koff = 0;
-  for (int64_t j0 = k0 + wave; j0 < k1; j0 += kDecWaves * kDecUnroll) {
-    float kv[kDecUnroll][EPL], vv[kDecUnroll][EPL], sc[kDecUnroll];
+// The EPW elements of a 16-byte word as floats.
+template <typename T>
+__device__ __forceinline__ void word_to_floats(const u32x4& w, float* out);
+template <>
+__device__ __forceinline__ void word_to_floats<float>(const u32x4& w, float* out) {
 #pragma unroll
-    for (int u = 0; u < kDecUnroll; ++u) {
-      const int64_t j = j0 + (int64_t)u * kDecWaves;
-      const bool ok = j < k1;
-      float lw = 0.f;
-      const int64_t r = ok ? seg_key(segs, s, j, kseg, koff, &lw) : 0;
-      sc[u] = ok ? lw * l2e : -INFINITY;
-      if (act && ok) {
-        load_elems<T>(Ks + r * D + lane * EPL, kv[u], EPL);
-        load_elems<T>(Vs + r * D + lane * EPL, vv[u], EPL);
-      } else {
-        for (int e = 0; e < EPL; ++e) kv[u][e] = vv[u][e] = 0.f;
-      }
-    }
-    float mx = mrun;
+  for (int c = 0; c < 4; ++c) out[c] = __uint_as_float(w[c]);
+}
+template <>
+__device__ __forceinline__ void word_to_floats<bf16_t>(const u32x4& w, float* out) {
 #pragma unroll
-    for (int u = 0; u < kDecUnroll; ++u) {
-      float d = 0.f;
-      for (int e = 0; e < EPL; ++e) d = __builtin_fmaf(q[e], kv[u][e], d);
-#pragma unroll
-      for (int off = 32; off >= 1; off >>= 1) d += __shfl_xor(d, off);
-      d = __shfl(d, 0);  // one score for every lane
-      sc[u] = sc[u] == -INFINITY ? -INFINITY : __builtin_fmaf(d, c2, sc[u]);
-      mx = fmaxf(mx, sc[u]);
-    }
-    if (mx == -INFINITY) continue;  // nothing of positive weight yet
-    const float scale = mrun == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(mrun - mx);
-    lrun *= scale;
-    for (int e = 0; e < EPL; ++e) acc[e] *= scale;
-#pragma unroll
-    for (int u = 0; u < kDecUnroll; ++u) {
-      const float p = sc[u] == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(sc[u] - mx);
-      lrun += p;
-      for (int e = 0; e < EPL; ++e) acc[e] = __builtin_fmaf(p, vv[u][e], acc[e]);
-    }
-    mrun = mx;
-  }
-  __shared__ float s_m[kDecWaves], s_l[kDecWaves], s_acc[kDecWaves][D];
-  if (lane == 0) {
-    s_m[wave] = mrun;
-    s_l[wave] = lrun;
-  }
-  if (act)
-    for (int e = 0; e < EPL; ++e) s_acc[wave][lane * EPL + e] = acc[e];
-  __syncthreads();
-  float M = -INFINITY;
-  for (int w = 0; w < kDecWaves; ++w) M = fmaxf(M, s_m[w]);
-  float* out = part + (s * split + blockIdx.x) * (int64_t)(D + 2);
-  for (int c = threadIdx.x; c < D; c += 64 * kDecWaves) {
-    float a = 0.f;
-    for (int w = 0; w < kDecWaves; ++w)
-      if (s_m[w] != -INFINITY) a += s_acc[w][c] * __builtin_amdgcn_exp2f(s_m[w] - M);
-    out[2 + c] = a;
-  }
-  if (threadIdx.x == 0) {
-    float L = 0.f;
-    for (int w = 0; w < kDecWaves; ++w)
-      if (s_m[w] != -INFINITY) L += s_l[w] * __builtin_amdgcn_exp2f(s_m[w] - M);
-    out[0] = M;
-    out[1] = L;
+  for (int c = 0; c < 4; ++c) {
+    out[2 * c] = __uint_as_float(w[c] << 16);
+    out[2 * c + 1] = __uint_as_float(w[c] & 0xffff0000u);
   }
 }
 
@@ -207,6 +139,148 @@ __device__ __forceinline__ void store_out<float>(float* p, float v) { *p = v; }
 template <>
 __device__ __forceinline__ void store_out<bf16_t>(bf16_t* p, float v) {
   *reinterpret_cast<__bf16*>(p) = (__bf16)v;
+}
+
+// Merge of two online-softmax states (m, l, acc) in the log2 domain; an empty
+// state has m = -inf.
+template <int EPW>
+__device__ __forceinline__ void softmax_merge(float& m, float& l, float* acc, float m2, float l2,
+                                              const float* acc2) {
+  const float M = fmaxf(m, m2);
+  const float a = m == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m - M);
+  const float b = m2 == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m2 - M);
+  l = l * a + l2 * b;
+#pragma unroll
+  for (int e = 0; e < EPW; ++e) acc[e] = acc[e] * a + acc2[e] * b;
+  m = M;
+}
+
+template <typename T, int D, typename TO>
+__global__ __launch_bounds__(64 * kDecWaves) void decode_attn_kernel(
+    const T* __restrict__ Q, const T* __restrict__ K, const T* __restrict__ V, ExpressSegs segs,
+    int64_t ld, int64_t m, int split, float* __restrict__ part, TO* __restrict__ O, int32_t* app,
+    int64_t app_stride, int32_t app_val) {
+  constexpr int LPK = D * Elem<T>::bytes / 16;  // lanes per key row (16 bytes each)
+  constexpr int KPI = 64 / LPK;                 // keys per load instruction
+  constexpr int EPW = 16 / Elem<T>::bytes;      // elements per 16-byte word
+  static_assert(LPK >= 1 && LPK <= 64 && 64 % LPK == 0, "row of 16..1024 bytes");
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int sub = lane / LPK, pos = lane % LPK;
+  const int64_t s = blockIdx.y;
+  const int64_t k0 = m * blockIdx.x / split, k1 = m * (blockIdx.x + 1) / split;
+  // this wave's contiguous run of keys
+  const int64_t per = (k1 - k0 + kDecWaves - 1) / kDecWaves;
+  const int64_t w0 = min(k1, k0 + per * wave), w1 = min(k1, w0 + per);
+  const float c2 = (float)(1.4426950408889634 / sqrt((double)D));
+  const float l2e = 1.4426950408889634f;
+  float q[EPW];
+  word_to_floats<T>(reinterpret_cast<const u32x4*>(Q + s * D)[pos], q);
+  const u32x4* Ks = reinterpret_cast<const u32x4*>(K + s * ld * D);
+  const u32x4* Vs = reinterpret_cast<const u32x4*>(V + s * ld * D);
+  // the segment table in LDS (the kernel argument is read through memory:
+  // scanning it there would put a memory latency on every segment step)
+  __shared__ ExpressSeg s_seg[kExpressMaxSegs];
+  __shared__ int s_nseg;
+  if (threadIdx.x < segs.n) s_seg[threadIdx.x] = segs.seg[threadIdx.x];
+  if (threadIdx.x == 0) s_nseg = segs.n;
+  __syncthreads();
+  float mrun = -INFINITY, lrun = 0.f, acc[EPW];
+#pragma unroll
+  for (int e = 0; e < EPW; ++e) acc[e] = 0.f;
+  int kseg = 0;
+  int64_t koff = 0;
+  for (int64_t j0 = w0; j0 < w1; j0 += KPI * kDecUnroll) {
+    u32x4 kw[kDecUnroll], vw[kDecUnroll];
+    float sc[kDecUnroll];
+    int64_t r[kDecUnroll];
+    // every row index of the batch first (the list reads are independent),
+    // then every row: two dependent memory latencies per batch, not two per key
+#pragma unroll
+    for (int u = 0; u < kDecUnroll; ++u) {
+      const int64_t j = j0 + u * KPI + sub;
+      const bool ok = j < w1;
+      float lw = 0.f;
+      r[u] = ok ? seg_key_lds(s_seg, s_nseg, s, j, kseg, koff, &lw) : -1;
+      sc[u] = ok ? lw * l2e : -INFINITY;
+    }
+#pragma unroll
+    for (int u = 0; u < kDecUnroll; ++u) {
+      const bool ok = r[u] >= 0;
+      kw[u] = ok ? Ks[r[u] * LPK + pos] : (u32x4){0u, 0u, 0u, 0u};
+      vw[u] = ok ? Vs[r[u] * LPK + pos] : (u32x4){0u, 0u, 0u, 0u};
+    }
+    float mx = mrun;
+#pragma unroll
+    for (int u = 0; u < kDecUnroll; ++u) {
+      float kf[EPW];
+      word_to_floats<T>(kw[u], kf);
+      float d = 0.f;
+#pragma unroll
+      for (int e = 0; e < EPW; ++e) d = __builtin_fmaf(q[e], kf[e], d);
+#pragma unroll
+      for (int off = LPK / 2; off >= 1; off >>= 1) d += __shfl_xor(d, off);
+      sc[u] = sc[u] == -INFINITY ? -INFINITY : __builtin_fmaf(d, c2, sc[u]);
+      mx = fmaxf(mx, sc[u]);
+    }
+    if (mx == -INFINITY) continue;  // nothing of positive weight yet
+    const float scale = mrun == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(mrun - mx);
+    lrun *= scale;
+#pragma unroll
+    for (int e = 0; e < EPW; ++e) acc[e] *= scale;
+#pragma unroll
+    for (int u = 0; u < kDecUnroll; ++u) {
+      const float p = sc[u] == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(sc[u] - mx);
+      float vf[EPW];
+      word_to_floats<T>(vw[u], vf);
+      lrun += p;
+#pragma unroll
+      for (int e = 0; e < EPW; ++e) acc[e] = __builtin_fmaf(p, vf[e], acc[e]);
+    }
+    mrun = mx;
+  }
+  // the wave's KPI key groups merge into lanes 0..LPK-1
+#pragma unroll
+  for (int off = LPK; off < 64; off <<= 1) {
+    const float m2 = __shfl_xor(mrun, off), l2 = __shfl_xor(lrun, off);
+    float a2[EPW];
+#pragma unroll
+    for (int e = 0; e < EPW; ++e) a2[e] = __shfl_xor(acc[e], off);
+    softmax_merge<EPW>(mrun, lrun, acc, m2, l2, a2);
+  }
+  __shared__ float s_m[kDecWaves], s_l[kDecWaves], s_acc[kDecWaves][D];
+  if (lane == 0) {
+    s_m[wave] = mrun;
+    s_l[wave] = lrun;
+  }
+  if (lane < LPK) {
+#pragma unroll
+    for (int e = 0; e < EPW; ++e) s_acc[wave][pos * EPW + e] = acc[e];
+  }
+  __syncthreads();
+  float M = -INFINITY;
+#pragma unroll
+  for (int w = 0; w < kDecWaves; ++w) M = fmaxf(M, s_m[w]);
+  const int c = threadIdx.x;
+  if (c < D) {
+    float a = 0.f, L = 0.f;
+#pragma unroll
+    for (int w = 0; w < kDecWaves; ++w) {
+      const float f = s_m[w] == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(s_m[w] - M);
+      a = __builtin_fmaf(s_acc[w][c], f, a);
+      L = __builtin_fmaf(s_l[w], f, L);
+    }
+    if (split == 1) {
+      store_out<TO>(O + s * D + c, a / L);
+    } else {
+      float* out = part + (s * split + blockIdx.x) * (int64_t)(D + 2);
+      out[2 + c] = a;
+      if (c == 0) {
+        out[0] = M;
+        out[1] = L;
+      }
+    }
+  }
+  if (split == 1 && app && threadIdx.x == 0) app[s * app_stride] = app_val;
 }
 
 // One workgroup per slice: the partials' maxima and sums are staged in LDS
@@ -261,11 +335,12 @@ template <typename T, int D, typename TO>
 hipError_t launch_decode_t(const void* Q, const void* K, const void* V, const ExpressSegs& segs,
                            int64_t S, int64_t ld, int64_t m, int split, float* part, void* O,
                            const Append& ap, hipStream_t st) {
-  hipLaunchKernelGGL((decode_attn_partial_kernel<T, D>), dim3((unsigned)split, (unsigned)S),
+  hipLaunchKernelGGL((decode_attn_kernel<T, D, TO>), dim3((unsigned)split, (unsigned)S),
                      dim3(64 * kDecWaves), 0, st, (const T*)Q, (const T*)K, (const T*)V, segs, ld,
-                     m, split, part);
-  hipLaunchKernelGGL((decode_attn_merge_kernel<D, TO>), dim3((unsigned)S), dim3(128), 0, st,
-                     (const float*)part, split, (TO*)O, ap.dst, ap.stride, ap.val);
+                     m, split, part, (TO*)O, ap.dst, ap.stride, ap.val);
+  if (split > 1)
+    hipLaunchKernelGGL((decode_attn_merge_kernel<D, TO>), dim3((unsigned)S), dim3(128), 0, st,
+                       (const float*)part, split, (TO*)O, ap.dst, ap.stride, ap.val);
   return hipGetLastError();
 }
 

@@ -129,10 +129,14 @@ hipError_t launch_express_keys(const ExpressSegs& segs, int64_t S, int64_t m, in
                                int32_t* idx, float* logw, hipStream_t st);
 // Weighted attention of one query per slice (Q [S, d], O [S, d]) over the m
 // keys of the segments (rows of K / V, slices ld rows apart): the keys of a
-// slice split over decode_attention_split(m) workgroups, whose partials
-// (S * split * (d + 2) floats in `part`) a second launch merges; that launch
-// also writes app_val to app[s * app_stride] when app is non-null.
-constexpr int kDecodeKeysPerGroup = 16;
+// slice split over decode_attention_split(m) workgroups; with one, it writes
+// the output itself, else a second launch merges their partials (S * split *
+// (d + 2) floats in `part`).  The last launch also writes app_val to
+// app[s * app_stride] when app is non-null.
+#ifndef DEC_KPG
+#define DEC_KPG 1024
+#endif
+constexpr int kDecodeKeysPerGroup = DEC_KPG;
 constexpr int kDecodeMaxSplit = 16;
 int decode_attention_split(int64_t m);
 hipError_t launch_decode_attention(int dtype, int64_t d, int out_dtype, const void* Q,

@@ -654,8 +654,13 @@ __global__ __launch_bounds__(64 * WAVES) void prefill_attn_kernel(
       int64_t r = 0;
       if ((int)threadIdx.x < kc) {
         if (kk < F) {
-          int k = 0;
-          while (k + 1 < nseg && kk >= s_seg_end[k]) ++k;
+          // the piece holding key kk: the first k with kk < s_seg_end[k]
+          // (binary search: a tile has up to kPrefillMaxSegs pieces)
+          int k = 0, hi = nseg - 1;
+          while (k < hi) {
+            const int mid = (k + hi) >> 1;
+            if (kk < s_seg_end[mid]) hi = mid; else k = mid + 1;
+          }
           const ExpressSeg& sg = s_seg[k].g;
           const int64_t j = kk - (k ? s_seg_end[k - 1] : 0);
           r = sg.src ? (int64_t)sg.src[s * sg.stride + j] : sg.start + j;

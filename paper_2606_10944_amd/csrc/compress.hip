@@ -1113,8 +1113,12 @@ struct PassLds {
   // pair scale exponents [P] f32 | largest row scale of every block [nblk] f32
   __host__ __device__ static size_t h2_off(int P) { return colbuf_off(P) + BW * kColBuf; }
   __host__ __device__ static size_t mb_off(int P) { return h2_off(P) + (((size_t)P * 4 + 15) & ~(size_t)15); }
-  __host__ __device__ static size_t bytes(int P) {
+  // rows of bulk sums completed per 64-pair chunk [nch] i32
+  __host__ __device__ static size_t chunk_off(int P) {
     return mb_off(P) + (((size_t)(P + BP - 1) / BP * 4 + 15) & ~(size_t)15);
+  }
+  __host__ __device__ static size_t bytes(int P) {
+    return chunk_off(P) + (((size_t)(P + 63) / 64 * 4 + 15) & ~(size_t)15);
   }
 };
 
@@ -1166,6 +1170,8 @@ __global__ __launch_bounds__(64 * (BW + 2)) void halve_pass_kernel(HalveArgs a) 
     s_h2[p] = a.h2[pb + p];
   }
   for (int b = threadIdx.x; b < nblk; b += 64 * (BW + 2)) s_mB[b] = a.mB[bucket * nblk + b];
+  int* s_chunk = reinterpret_cast<int*>(smem + L::chunk_off(P));
+  for (int c = threadIdx.x; c < (P + 63) / 64; c += 64 * (BW + 2)) s_chunk[c] = 0;
   if (threadIdx.x < 16) s_cnt[threadIdx.x] = threadIdx.x < 2 ? -1 : 0;
   __syncthreads();
 
@@ -1192,9 +1198,9 @@ __global__ __launch_bounds__(64 * (BW + 2)) void halve_pass_kernel(HalveArgs a) 
     for (int m = 0; m < nblk; ++m) {
       const int npb = min(BP, P - m * BP);
       wait_at_least(&s_cnt[1], m, a.status);
-      // the bulk wave that owns this block's pairs (64-pair chunk m / 2) has
-      // added blocks 0 .. m-2 to them
-      if (m >= 2) wait_at_least(&s_cnt[2 + (m >> 1) % BW], m - 1, a.status);
+      // the bulk sums of blocks 0 .. m-2 are in this block's pairs (64-pair
+      // chunk m / 2)
+      if (m >= 2) wait_at_least(&s_chunk[m >> 1], m - 1, a.status);
       unsigned char* sb = slot(m);
       const int p = lane;
       const int pl = lane & (BP - 1);
@@ -1309,28 +1315,32 @@ __global__ __launch_bounds__(64 * (BW + 2)) void halve_pass_kernel(HalveArgs a) 
   } else {
     // ---- bulk updates, blocks 0 .. nblk-3 ----
     // Bulk wave w = wave-2 owns the 64-pair chunks c = w, w + BW, ... of the
-    // bucket.  Row b (block b's signed scores) adds to the pairs of block
-    // b+2 on; the wave's items are (row, chunk) in row order, chunks from the
-    // one holding block b+2's first pair (its lanes before that pair, in
-    // block b+1, load but do not add).  The items form one stream held in an
-    // NCB-slot register ring: each consumed slot is refilled at once with the
-    // item NCB later, so the loads run ahead across rows whatever the
-    // decisions.  Lane l sums column l of the chunk in ascending order (the
-    // order of the decider's sums); with COAL the chunk is loaded a score
-    // tile (8 columns, 1 KiB) per instruction, 8 lanes to a column, and
-    // turned through the wave's LDS column buffer.  Entering row b the wave
-    // publishes b (rows completed); past its last item, nblk.
+    // bucket (blocks 2c, 2c+1).  Row b (block b's signed scores) adds to the
+    // pairs of block b+2 on, so chunk c takes rows 0 .. 2c-1 (row 2c-1 only
+    // in its second block).  A wave's items are (row, chunk) chunk by chunk
+    // in increasing c, rows in order within a chunk: items are taken in the
+    // order the decider needs them (chunk c before block 2c), and a chunk's
+    // progress does not wait for the wave's later chunks.  The items form one
+    // stream held in an NCB-slot register ring: each consumed slot is
+    // refilled at once with the item NCB later, so the loads run ahead
+    // whatever the decisions.  Lane l sums column l of the chunk in ascending
+    // order (the order of the decider's sums); with COAL the chunk is loaded
+    // a score tile (8 columns, 1 KiB) per instruction, 8 lanes to a column,
+    // and turned through the wave's LDS column buffer.  After row b of chunk
+    // c the wave publishes b + 1 in s_chunk[c] (rows completed).
     const int w = wave - 2;
     const int nch = (P + 63) >> 6;
     const int nrow = nblk - 2;
-    auto first_c = [&](int b) {  // this wave's first chunk in row b (>= nch: none)
-      const int c0 = (b + 2) >> 1;
-      return c0 + ((w - c0) % BW + BW) % BW;
+    auto last_row = [&](int c) { return min(2 * c - 1, nrow - 1); };  // < 0: no item
+    auto first_chunk = [&]() {
+      int c = w;
+      while (c < nch && last_row(c) < 0) c += BW;
+      return c;
     };
-    int fb = 0, fc = first_c(0);  // next item to load
+    int fb = 0, fc = first_chunk();  // next item to load
     u32x4* colbuf = reinterpret_cast<u32x4*>(smem + L::colbuf_off(P) + (size_t)w * L::kColBuf);
     auto fetch_next = [&](u32x4* dst) {
-      const bool live = fb < nrow && fc < nch;
+      const bool live = fc < nch;
       // COAL: word lane % QW of column 8 k + lane / QW of the chunk; else
       // word k of column lane (past the stream's end: valid columns, never
       // used)
@@ -1344,17 +1354,17 @@ __global__ __launch_bounds__(64 * (BW + 2)) void halve_pass_kernel(HalveArgs a) 
 #pragma unroll
         for (int k = 0; k < 8; ++k) dst[k] = c_[k];
       }
-      if (live) {
+      if (live && ++fb > last_row(fc)) {
+        fb = 0;
         fc += BW;
-        if (fc >= nch) fc = first_c(++fb);
       }
     };
     u32x4 cb[NCB][8];
 #pragma unroll
     for (int r = 0; r < NCB; ++r) fetch_next(cb[r]);
-    int b = 0, c = first_c(0);  // next item to use
-    int decided = -1;           // last decided block seen
-    bool more = nrow > 0 && c < nch;
+    int b = 0, c = first_chunk();  // next item to use
+    int decided = -1;              // last decided block seen
+    bool more = c < nch;
     // Every slot of a turn is used and refilled whether or not the stream
     // has ended (loads past the end are of valid columns, nothing is added):
     // all paths then issue the same loads, and the wait before a slot's use
@@ -1382,16 +1392,15 @@ __global__ __launch_bounds__(64 * (BW + 2)) void halve_pass_kernel(HalveArgs a) 
           s_alpha[p] += ldexp((double)sum, (int)scale_shift(s_mB[b], s_h2[p]));
         fetch_next(cb[r]);
         if (live) {
-          c += BW;
-          if (c >= nch) {
-            c = first_c(++b);
-            more = b < nrow && c < nch;
-            if (more) publish(&s_cnt[2 + w], b);
+          publish(&s_chunk[c], b + 1);
+          if (++b > last_row(c)) {
+            b = 0;
+            c += BW;
+            more = c < nch;
           }
         }
       }
     }
-    publish(&s_cnt[2 + w], nblk);
   }
 #undef PASS_SUM
 #undef PASS_COL

@@ -581,7 +581,7 @@ hipError_t launch_attn_res_d(int64_t n_out, const void* Q, const void* K, const 
 // biases sqrt(d) * logw.
 // ---------------------------------------------------------------------------
 template <typename T, int D, typename TO>
-__global__ __launch_bounds__(64 * WAVES) void prefill_attn_kernel(
+__global__ __launch_bounds__(64 * WAVES) __attribute__((amdgpu_waves_per_eu(2))) void prefill_attn_kernel(
     const T* __restrict__ Q, const T* __restrict__ K, const T* __restrict__ V, int64_t n,
     const PrefillTile* __restrict__ tiles, const PrefillSeg* __restrict__ segs,
     const int32_t* __restrict__ c0s, const float* __restrict__ w0s,
@@ -643,41 +643,60 @@ __global__ __launch_bounds__(64 * WAVES) void prefill_attn_kernel(
   }
 
   constexpr int WPR = D * Elem<T>::bytes / 16;
+  // A chunk's keys (row, bias, visibility; one thread per key) are gathered
+  // into registers one chunk ahead, so their list reads overlap the previous
+  // chunk's arithmetic; they reach LDS at the top of the chunk.
+  // (registers hold the raw loaded values; anything computed from them is
+  // left to the commit, so that no wait for the loads precedes the compute)
+  int32_t m_vlo = 0, m_vhi = 0, m_raw = 0, m_cpos = -1;
+  uint8_t m_kept = 1;
+  float m_bias = -INFINITY;
+  bool m_piece = false;
+  auto gather_meta = [&](int64_t ck_) {
+    if (threadIdx.x >= KC) return;
+    const int kc_ = (int)min((int64_t)KC, M - ck_);
+    const int64_t kk = ck_ + threadIdx.x;
+    m_vlo = 0;
+    m_vhi = 0;
+    m_bias = -INFINITY;
+    m_piece = false;
+    m_cpos = -1;
+    m_raw = 0;
+    m_kept = 1;
+    if ((int)threadIdx.x < kc_) {
+      if (kk < F) {
+        // the piece holding key kk: the first k with kk < s_seg_end[k]
+        // (binary search: a tile has up to kPrefillMaxSegs pieces)
+        int k = 0, hi = nseg - 1;
+        while (k < hi) {
+          const int mid = (k + hi) >> 1;
+          if (kk < s_seg_end[mid]) hi = mid; else k = mid + 1;
+        }
+        const ExpressSeg& sg = s_seg[k].g;
+        const int64_t j = kk - (k ? s_seg_end[k - 1] : 0);
+        m_raw = sg.src ? sg.src[s * sg.stride + j] : (int32_t)(sg.start + j);
+        m_bias = sg.logw * sqrt_d;
+        m_vlo = s_seg[k].vlo;
+        m_vhi = s_seg[k].vhi;
+        m_piece = true;
+      } else {
+        m_cpos = (int32_t)(tile.causal_lo + (kk - F));
+        m_kept = kept[m_cpos];
+      }
+    }
+  };
+  gather_meta(0);
   for (int64_t ck = 0; ck < M; ck += KC) {
     const int kc = (int)min((int64_t)KC, M - ck);
     __syncthreads();
-    // the chunk's keys: row, bias and visibility, one thread per key
     if (threadIdx.x < KC) {
-      const int64_t kk = ck + threadIdx.x;
-      int32_t pos = -1, vlo = 0, vhi = 0;
-      float bias = -INFINITY;
-      int64_t r = 0;
-      if ((int)threadIdx.x < kc) {
-        if (kk < F) {
-          // the piece holding key kk: the first k with kk < s_seg_end[k]
-          // (binary search: a tile has up to kPrefillMaxSegs pieces)
-          int k = 0, hi = nseg - 1;
-          while (k < hi) {
-            const int mid = (k + hi) >> 1;
-            if (kk < s_seg_end[mid]) hi = mid; else k = mid + 1;
-          }
-          const ExpressSeg& sg = s_seg[k].g;
-          const int64_t j = kk - (k ? s_seg_end[k - 1] : 0);
-          r = sg.src ? (int64_t)sg.src[s * sg.stride + j] : sg.start + j;
-          bias = sg.logw * sqrt_d;
-          vlo = s_seg[k].vlo;
-          vhi = s_seg[k].vhi;
-        } else {
-          r = tile.causal_lo + (kk - F);
-          pos = (int32_t)r | (kept[r] ? 0 : (1 << 30));
-        }
-        r = r < 0 ? 0 : (r >= n ? n - 1 : r);
-      }
-      s_pos[threadIdx.x] = pos;
-      s_vlo[threadIdx.x] = vlo;
-      s_vhi[threadIdx.x] = vhi;
+      int64_t r = m_piece ? (int64_t)m_raw : (m_cpos >= 0 ? (int64_t)m_cpos : 0);
+      r = r < 0 ? 0 : (r >= n ? n - 1 : r);
+      s_pos[threadIdx.x] = m_cpos >= 0 ? (m_cpos | (m_kept ? 0 : (1 << 30))) : -1;
+      s_vlo[threadIdx.x] = m_vlo;
+      s_vhi[threadIdx.x] = m_vhi;
       s_row[threadIdx.x] = (int32_t)r;
-      sB[threadIdx.x] = bias;
+      sB[threadIdx.x] = m_bias;
     }
     __syncthreads();
     for (int w = threadIdx.x; w < KC * WPR; w += 64 * WAVES) {
@@ -720,14 +739,7 @@ __global__ __launch_bounds__(64 * WAVES) void prefill_attn_kernel(
       }
     }
     __syncthreads();
-
-    uint4 Ak[4][NV];
-#pragma unroll
-    for (int kt = 0; kt < 4; ++kt) {
-      const uint4* pk = reinterpret_cast<const uint4*>(sK + (kt * 16 + m16) * L::k_stride);
-#pragma unroll
-      for (int v = 0; v < NV; ++v) Ak[kt][v] = pk[4 * v + g];
-    }
+    if (ck + KC < M) gather_meta(ck + KC);
 
 #pragma unroll
     for (int qt = 0; qt < QT; ++qt) {
@@ -739,8 +751,14 @@ __global__ __launch_bounds__(64 * WAVES) void prefill_attn_kernel(
       float mx = -INFINITY;
 #pragma unroll
       for (int kt = 0; kt < 4; ++kt) {
+        // the key tile's fragments from LDS for each query tile (re-read
+        // rather than held: the registers keep two workgroups per CU)
+        uint4 ak[NV];
+        const uint4* pk = reinterpret_cast<const uint4*>(sK + (kt * 16 + m16) * L::k_stride);
+#pragma unroll
+        for (int v = 0; v < NV; ++v) ak[v] = pk[4 * v + g];
         floatx4_t z = {0.f, 0.f, 0.f, 0.f};
-        z = mma_rows<T, D>(Ak[kt], Bq[qt], z);
+        z = mma_rows<T, D>(ak, Bq[qt], z);
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
           const int key = kt * 16 + 4 * g + i;

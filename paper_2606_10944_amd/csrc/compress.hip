@@ -1483,9 +1483,11 @@ hipError_t launch_local_td(const HalveArgs& a0, int64_t nbk, hipStream_t st) {
   using SS = ScoreShape<T, D>;
   auto kern = pair_scores_kernel<T, D, true, true>;
   const int64_t NT = (a0.N + 15) / 16, nb = (a0.N + 63) / 64, P = a0.N / 2;
+  // stages, score tiles, pair scale exponents of the rows, staged row
+  // scales, half-block row scale maxima, pair terms [2][P]
   const size_t lds = (size_t)kScoreStages * SS::CHUNKS * 1024 +
                      (size_t)panel_tiles(nb, NT, 4) * kETileLds * 4 + SS::GT * 16 * 4 +
-                     kScoreStages * 16 * 4 + 2 * P * 4;
+                     kScoreStages * 16 * 4 + 2 * SS::BLOCKS * 4 + 2 * P * 4;
   if (lds > 64 * 1024) {
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);

@@ -1050,8 +1050,9 @@ void pair_scores_kernel(HalveArgs a) {
 
 // Decision pass of one bucket per workgroup, in three roles that run ahead
 // of or behind each other, synchronised by progress counters in LDS:
-//  - wave 1 (fetcher) stages each block's inputs in a ring of three LDS
-//    slots, up to two blocks ahead of the decider: the block's own scores, the scores
+//  - wave 1 (fetcher) stages each block's inputs in a ring of FD + 1 LDS
+//    slots, up to FD blocks ahead of the decider (FD blocks' loads in flight):
+//    the block's own scores, the scores
 //    against the next block's pairs, the row indices, and the thresholds
 //    a(1 - 2u), which depend on no decision (the running maximum of b over
 //    the bucket is carried from block to block);
@@ -1085,9 +1086,9 @@ __device__ __forceinline__ void publish(int* flag, int value) {
   __hip_atomic_store(flag, value, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
 }
 
-template <int BW, int NCB>
+template <int BW, int NCB, int FD>
 struct PassLds {
-  static constexpr int BP = 32, QW = 8, NSLOT = 3;
+  static constexpr int BP = 32, QW = 8, NSLOT = FD + 1;
   // alpha [P] f64 | decisions of every block [nblk] u32 | counters [16]:
   // last decided block, last staged block, rows completed by each bulk wave |
   // NSLOT input slots, each: thresholds [BP] f64, rows [2][BP] i32, own
@@ -1122,9 +1123,9 @@ struct PassLds {
   }
 };
 
-template <int BW, int NCB>
+template <int BW, int NCB, int FD>
 __global__ __launch_bounds__(64 * (BW + 2)) void halve_pass_kernel(HalveArgs a) {
-  using L = PassLds<BW, NCB>;
+  using L = PassLds<BW, NCB, FD>;
   constexpr int RT = 4;
   constexpr int BR = 16 * RT;
   constexpr int BP = BR / 2;
@@ -1260,9 +1261,9 @@ __global__ __launch_bounds__(64 * (BW + 2)) void halve_pass_kernel(HalveArgs a) 
     // block's last pair read that pair's inputs.  One block is fetched while
     // the previous one is staged.
     __builtin_amdgcn_s_setprio(2);
-    u32x4 fo[2][4], fn[2][4];
-    float flbt[2], fh2[2], fu[2];
-    int32_t fr0[2], fr1[2];
+    u32x4 fo[FD][4], fn[FD][4];
+    float flbt[FD], fh2[FD], fu[FD];
+    int32_t fr0[FD], fr1[FD];
 #define PASS_FETCH(B, K)                                                                \
   do {                                                                                 \
     const int b_ = min(B, nblk - 1);                                                   \
@@ -1287,7 +1288,7 @@ __global__ __launch_bounds__(64 * (BW + 2)) void halve_pass_kernel(HalveArgs a) 
   do {                                                                                 \
     const int npb_ = min(BP, P - (B) * BP);                                            \
     const double thr_ = block_threshold(flbt[K], fh2[K], fu[K], npb_, lane, a.log_c, carry); \
-    /* slot B%3 held block B-3, which the decider has left once B-2 is decided */    \
+    /* slot B % NSLOT held block B - NSLOT, left once B - NSLOT + 1 is decided */    \
     if ((B) >= L::NSLOT) wait_at_least(&s_cnt[0], (B) - (L::NSLOT - 1), a.status);    \
     unsigned char* sb_ = slot(B);                                                      \
     _Pragma("unroll") for (int r_ = 0; r_ < 4; ++r_) {                                 \
@@ -1301,13 +1302,17 @@ __global__ __launch_bounds__(64 * (BW + 2)) void halve_pass_kernel(HalveArgs a) 
     }                                                                                  \
     publish(&s_cnt[1], B);                                                             \
   } while (0)
-    PASS_FETCH(0, 0);
-    for (int m = 0; m < nblk; m += 2) {
-      PASS_FETCH(m + 1, 1);
-      PASS_STAGE(m, 0);
-      if (m + 1 < nblk) {
-        PASS_FETCH(m + 2, 0);
-        PASS_STAGE(m + 1, 1);
+    // FD blocks' loads in flight: block m is staged from register set m % FD,
+    // which then takes the loads of block m + FD
+#pragma unroll
+    for (int k = 0; k < FD; ++k) PASS_FETCH(k, k);
+    for (int m = 0; m < nblk; m += FD) {
+#pragma unroll
+      for (int k = 0; k < FD; ++k) {
+        if (m + k < nblk) {
+          PASS_STAGE(m + k, k);
+          PASS_FETCH(m + k + FD, k);
+        }
       }
     }
 #undef PASS_FETCH
@@ -1531,10 +1536,10 @@ hipError_t launch_scores_t(int64_t d, const HalveArgs& a, int64_t nbk, hipStream
   }
 }
 
-template <int BW, int NCB>
+template <int BW, int NCB, int FD>
 hipError_t launch_pass_w(const HalveArgs& a, int64_t nbk, hipStream_t st) {
-  const size_t lds = PassLds<BW, NCB>::bytes((int)(a.N / 2));
-  auto kern = halve_pass_kernel<BW, NCB>;
+  const size_t lds = PassLds<BW, NCB, FD>::bytes((int)(a.N / 2));
+  auto kern = halve_pass_kernel<BW, NCB, FD>;
   if (lds > 64 * 1024) {
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
@@ -1577,15 +1582,39 @@ hipError_t launch_local(int dtype, int64_t d, const HalveArgs& a, int64_t nbk, h
   return dtype == 0 ? launch_local_t<float>(d, a, nbk, st) : launch_local_t<bf16_t>(d, a, nbk, st);
 }
 
+// Decision pass shapes <bulk waves, chunks in flight per bulk wave, blocks in
+// flight in the fetcher> for small (<= 256 pairs after the first two
+// blocks), medium (<= 512) and large buckets.  Large buckets run one per CU
+// (64 buckets of 2048 rows on the long workload), where ten bulk waves keep
+// the decider fed (round 3 there: 69.7 -> 58.7 us against six); a deeper
+// fetcher gained nothing.
+#ifndef PASS_FD_S
+#define PASS_FD_S 2
+#endif
+#ifndef PASS_BW_M
+#define PASS_BW_M 6
+#define PASS_NCB_M 3
+#define PASS_FD_M 2
+#endif
+#ifndef PASS_BW_L
+#define PASS_BW_L 10
+#define PASS_NCB_L 3
+#define PASS_FD_L 2
+#endif
+constexpr size_t kPassMaxLds = (size_t)160 << 10;  // LDS of a gfx950 CU
 hipError_t launch_decide(const HalveArgs& a0, int64_t nbk, hipStream_t st) {
   const HalveArgs a = with_layout(a0);
   // bulk waves x prefetched chunks x 64 pairs should cover the pairs after
   // the first two blocks
   const int64_t later = a.N / 2 - 64;
-  if (later <= 64) return launch_pass_w<1, 1>(a, nbk, st);
-  if (later <= 256) return launch_pass_w<2, 2>(a, nbk, st);
-  if (later <= 512) return launch_pass_w<4, 2>(a, nbk, st);
-  return launch_pass_w<6, 3>(a, nbk, st);
+  if (later <= 64) return launch_pass_w<1, 1, PASS_FD_S>(a, nbk, st);
+  if (later <= 256) return launch_pass_w<2, 2, PASS_FD_S>(a, nbk, st);
+  if (later <= 512) return launch_pass_w<PASS_BW_M, PASS_NCB_M, PASS_FD_M>(a, nbk, st);
+  // the large shape's column buffers take 9 KiB of LDS per bulk wave: past
+  // the 160 KiB of a CU (buckets above 4096 rows) the medium shape runs
+  if (PassLds<PASS_BW_L, PASS_NCB_L, PASS_FD_L>::bytes((int)(a.N / 2)) <= kPassMaxLds)
+    return launch_pass_w<PASS_BW_L, PASS_NCB_L, PASS_FD_L>(a, nbk, st);
+  return launch_pass_w<PASS_BW_M, PASS_NCB_M, PASS_FD_M>(a, nbk, st);
 }
 
 hipError_t launch_vmax(int dtype, const void* V, int64_t S, int64_t n, int64_t ld, int64_t d,

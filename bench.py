@@ -24,6 +24,10 @@ enters it); one step = one point of every slice.
 --mode prefill measures the masked prefill over the Express cache (every
 point's Thinformer output at once): B=1, H=32, d=128, bf16, 65536 points,
 n_out=256 (h = 8), mbar=6 (h - 2); one step = one whole prefill.
+
+--mode peaks measures the GPU's own ceilings beside the spec figures the
+rooflines use: library GEMM rates (bf16, fp16, fp32) and 1 GiB copy, fill
+and read-reduce bandwidth.
 """
 import argparse
 import collections
@@ -402,6 +406,52 @@ def prefill_main(args):
     print(json.dumps(out), flush=True)
 
 
+def peaks_main(args):
+    """Measured ceilings of the GPU beside the spec sheet: library GEMMs
+    (torch.matmul, hipBLASLt) on square operands and device-wide copy, fill
+    and read-reduce over 1 GiB of fp32, each timed with HIP events."""
+    import torch
+    dev = torch.device("cuda:0")
+
+    def timed(fn, n):
+        for _ in range(5):
+            fn()
+        torch.cuda.synchronize()
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(n):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / n * 1e-3
+
+    gemm = {}
+    for dt, name in ((torch.bfloat16, "bf16"), (torch.float16, "fp16"), (torch.float32, "fp32")):
+        for M in (8192, 16384):
+            a = torch.randn(M, M, device=dev, dtype=dt)
+            b = torch.randn(M, M, device=dev, dtype=dt)
+            t = timed(lambda: torch.matmul(a, b), 10 if M == 16384 else 20)
+            gemm[f"{name}_{M}"] = 2 * M ** 3 / t / 1e12
+            del a, b
+    x = torch.empty(1 << 28, device=dev, dtype=torch.float32)
+    y = torch.empty_like(x)
+    nb = x.numel() * 4
+    bw = {"copy_read_write": 2 * nb / timed(lambda: y.copy_(x), 20) / 1e12,
+          "fill_write": nb / timed(lambda: x.fill_(1.0), 20) / 1e12,
+          "sum_read": nb / timed(lambda: x.sum(), 20) / 1e12}
+    best_bf16 = max(gemm["bf16_8192"], gemm["bf16_16384"])
+    print(json.dumps({
+        "metric": "measured peaks (library GEMM TFLOP/s, 1 GiB copy/fill/read TB/s)",
+        "value": best_bf16, "unit": "TFLOP/s (bf16 GEMM)", "n_gpus": 1,
+        "higher_is_better": True, "vs_baseline": None, "data": "synthetic",
+        "gemm_tflops": gemm, "bandwidth_tbs": bw,
+        "spec": {"bf16_dense_tflops": BF16_MFMA_PEAK_TFLOPS, "fp32_tflops": FP32_MFMA_PEAK_TFLOPS,
+                 "hbm_tbs": HBM_PEAK_GBS / 1e3},
+        "gpu": torch.cuda.get_device_name(0),
+    }), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -416,8 +466,10 @@ def main():
                     help="keys kept exactly at the start of every slice")
     ap.add_argument("--window", type=int, default=0,
                     help="keys kept exactly at the end of every slice")
-    ap.add_argument("--mode", choices=["compress", "decode", "prefill"], default="compress",
-                    help="compress + attention (default), Express decoding or masked prefill")
+    ap.add_argument("--mode", choices=["compress", "decode", "prefill", "peaks"],
+                    default="compress",
+                    help="compress + attention (default), Express decoding, masked prefill, or "
+                         "the GPU's measured GEMM and bandwidth ceilings")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: the thinning path runs each (batch, head) "
@@ -425,6 +477,9 @@ def main():
         sys.exit(2)
     if args.mode == "decode":
         decode_main(args)
+        return
+    if args.mode == "peaks":
+        peaks_main(args)
         return
     if args.mode == "prefill":
         prefill_main(args)

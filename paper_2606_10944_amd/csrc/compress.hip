@@ -411,20 +411,23 @@ __host__ __device__ inline int64_t panel_tiles(int64_t B, int64_t NT, int64_t RT
 }
 
 // Work decomposition of pair_scores_kernel.  A group is BLOCKS consecutive
-// decision blocks (64 rows each) of one bucket; the group's waves hold its
+// decision blocks (64 rows each) of one bucket; the group's W waves hold its
 // rows as MFMA fragments, HB half-blocks (32 rows) per wave, paired so that
 // every wave has the same amount of work: with HB = 2, wave w holds the first
 // half of block w and the second half of block BLOCKS-1-w.  Workgroups are
-// small enough (4 waves) that two fit on a CU, so one's row loads overlap the
-// other's arithmetic.  A workgroup handles one
+// small enough that two fit on a CU, so one's row loads overlap the other's
+// arithmetic.  Launches with streamed chunks take W = 4 waves of HB = 2 (the
+// streamed tiles are software-pipelined across a wave's two slots); launches
+// of own chunks only (and the local kernel) take W = 8 waves of HB = 1 where
+// that gives the same groups (fragments of up to 4 words per lane): half the
+// registers per wave, so twice the waves per SIMD hide each other's
+// latencies (long workload round 0: 204 -> 183 us; the small workloads'
+// local rounds 5-15% faster).  A workgroup handles one
 // (bucket, group, chunk): chunk 0 covers the group's own column tiles, which
 // the owning waves write to LDS from their registers (so the bucket's rows
 // are read from HBM once); chunk c >= 1 covers kScoreChunk column tiles after
 // the group, streamed from global memory through registers DEPTH tiles ahead.
-#ifndef SCORE_WAVES
-#define SCORE_WAVES 4
-#endif
-constexpr int kScoreWaves = SCORE_WAVES;
+constexpr int kScoreWaves = 4;  // waves of a launch with streamed chunks
 #ifndef SCORE_DEPTH
 #define SCORE_DEPTH 3
 #endif
@@ -439,14 +442,14 @@ constexpr int kScoreRowsStaged = (kScoreChunk + 2 * SCORE_DEPTH + 1) * 16;
 constexpr int kETileStride = 36;
 constexpr int kETileLds = 8 * kETileStride;
 
-template <typename T, int D>
+template <typename T, int D, int W>
 struct ScoreShape {
   static constexpr int NV = Frag<T, D>::NV;
-  static constexpr int HB = NV >= 8 ? 1 : 2;   // half-blocks per wave
-  static constexpr int BLOCKS = kScoreWaves * HB / 2;  // decision blocks per group
+  static constexpr int HB = (W == 4 && NV < 8) ? 2 : 1;  // half-blocks per wave
+  static constexpr int BLOCKS = W * HB / 2;    // decision blocks per group
   static constexpr int GT = 4 * BLOCKS;        // 16-row tiles per group
   static constexpr int CHUNKS = 2 * NV;        // 1 KB fragment chunks per tile (K, then V)
-  static constexpr int LPT = (CHUNKS + kScoreWaves - 1) / kScoreWaves;
+  static constexpr int LPT = (CHUNKS + W - 1) / W;
   // stages, score tile buffers, pair scale exponents of the group's rows,
   // row scale exponents of the stages, the half-blocks' largest row scales,
   // row indices of the streamed rows
@@ -455,11 +458,18 @@ struct ScoreShape {
                              kScoreRowsStaged * 8;
 };
 
-// Block (group-local) and half of half-block slot h of wave w.
-template <int HB>
+// Waves of the launches of own chunks only and of the local kernel (the
+// same groups as the streamed launches': see above).
+template <typename T, int D>
+constexpr int own_waves() {
+  return Frag<T, D>::NV < 8 ? 8 : kScoreWaves;
+}
+
+// Block (group-local) and half of half-block slot h of wave w (W waves).
+template <int HB, int W>
 __device__ __forceinline__ void half_block(int w, int h, int& b, int& half) {
   if (HB == 2) {
-    b = h == 0 ? w : kScoreWaves - 1 - w;
+    b = h == 0 ? w : W - 1 - w;
     half = h;
   } else {
     b = w >> 1;
@@ -529,10 +539,10 @@ __device__ __align__(16) float g_score_sink[256];
 // the same arithmetic as halve_pass_kernel (the scores never leave the CU).
 // OWN_ONLY: a launch of own chunks only (no streamed code, so the register
 // budget allows the own tiles to be software-pipelined as the streamed ones).
-template <typename T, int D, bool LOCAL, bool OWN_ONLY>
-__global__ __launch_bounds__(64 * kScoreWaves) __attribute__((amdgpu_waves_per_eu(2)))
+template <typename T, int D, bool LOCAL, bool OWN_ONLY, int W>
+__global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(2)))
 void pair_scores_kernel(HalveArgs a) {
-  using SS = ScoreShape<T, D>;
+  using SS = ScoreShape<T, D, W>;
   constexpr int NV = SS::NV, HB = SS::HB, NBW = SS::BLOCKS, GT = SS::GT;
   constexpr int CH = SS::CHUNKS, LPT = SS::LPT;
   constexpr int BP = 32;
@@ -617,7 +627,7 @@ void pair_scores_kernel(HalveArgs a) {
 #pragma unroll
   for (int h = 0; h < HB; ++h) {
     int b, half;
-    half_block<HB>(wave, h, b, half);
+    half_block<HB, W>(wave, h, b, half);
     hb_blk[h] = grp * NBW + b;
     hb_half[h] = half;
     hb_ok[h] = hb_blk[h] < nb;
@@ -625,13 +635,13 @@ void pair_scores_kernel(HalveArgs a) {
   // Streamed chunk: the row indices of its column rows are requested first,
   // so that their latency and the fragments' overlap (the index loads are
   // the older ones, and staging them in LDS waits for them only).
-  constexpr int RPT = (kScoreRowsStaged + 64 * kScoreWaves - 1) / (64 * kScoreWaves);
+  constexpr int RPT = (kScoreRowsStaged + 64 * W - 1) / (64 * W);
   const int j_end = own ? 0 : min(N, (jt1 + 2 * DEPTH + 1) * 16);
   int64_t ridx[RPT];
   if (!own) {
 #pragma unroll
     for (int k = 0; k < RPT; ++k) {
-      const int j = jt0 * 16 + (int)threadIdx.x + k * 64 * kScoreWaves;
+      const int j = jt0 * 16 + (int)threadIdx.x + k * 64 * W;
       ridx[k] = j < j_end ? (rows_in ? (int64_t)rows_in[j] : row_base + j) : 0;
     }
   }
@@ -696,7 +706,7 @@ void pair_scores_kernel(HalveArgs a) {
     // behind the ring's loads
 #pragma unroll
     for (int k = 0; k < RPT; ++k) {
-      const int j = jt0 * 16 + (int)threadIdx.x + k * 64 * kScoreWaves;
+      const int j = jt0 * 16 + (int)threadIdx.x + k * 64 * W;
       if (j < j_end) s_rows[j - jt0 * 16] = ridx[k];
     }
   }
@@ -724,7 +734,7 @@ void pair_scores_kernel(HalveArgs a) {
     const int64_t row_ = s_rows[j_ - jt0 * 16];                                      \
     hst[SLOT] = a.rowh2[s * a.n + row_];                                             \
     _Pragma("unroll") for (int k_ = 0; k_ < LPT; ++k_) {                             \
-      const int c_ = min(wave + k_ * kScoreWaves, CH - 1);                           \
+      const int c_ = min(wave + k_ * W, CH - 1);                                     \
       const T* src_ = c_ < NV ? K : V;                                               \
       stg[SLOT][k_] = reinterpret_cast<const u32x4*>(src_ + row_ * D)[4 * (c_ % NV) + g]; \
     }                                                                                \
@@ -733,7 +743,7 @@ void pair_scores_kernel(HalveArgs a) {
   do {                                                                               \
     if (wave == 0 && g == 0) s_hst[(STAGE) * 16 + m16] = hst[SLOT];                  \
     _Pragma("unroll") for (int k_ = 0; k_ < LPT; ++k_) {                             \
-      const int c_ = wave + k_ * kScoreWaves;                                        \
+      const int c_ = wave + k_ * W;                                                  \
       if (c_ < CH) reinterpret_cast<u32x4*>(smem + ((STAGE) * CH + c_) * 1024)[lane] = stg[SLOT][k_]; \
     }                                                                                \
   } while (0)
@@ -748,7 +758,7 @@ void pair_scores_kernel(HalveArgs a) {
 #define SCORE_OWN_COMMIT(STAGE, TL)                                                  \
   do {                                                                               \
     const int b_ = (TL) >> 2, half_ = ((TL) >> 1) & 1, rt_ = (TL) & 1;              \
-    const int owner_ = HB == 2 ? (half_ == 0 ? b_ : kScoreWaves - 1 - b_) : 2 * b_ + half_; \
+    const int owner_ = HB == 2 ? (half_ == 0 ? b_ : W - 1 - b_) : 2 * b_ + half_;  \
     const int slot_ = HB == 2 ? half_ : 0;                                           \
     if (wave == owner_) {                                                            \
       if (slot_ == 0) {                                                              \
@@ -813,7 +823,7 @@ void pair_scores_kernel(HalveArgs a) {
   // streamed chunk's padding tiles go to the sink.
 #define SCORE_FLUSH(OWN, IF, BUF)                                                       \
   do {                                                                                 \
-    if (!LOCAL && (NBW == kScoreWaves || wave < NBW)) {                                \
+    if (!LOCAL && (NBW == W || wave < NBW)) {                                          \
       const int bw_ = grp * NBW + wave;                                                \
       const int jtf_ = jt0 + (IF);                                                     \
       if (!(OWN) || (bw_ < nb && jtf_ >= 4 * bw_)) {                                   \
@@ -1434,15 +1444,22 @@ __global__ __launch_bounds__(64) void gram16_kernel(const T* rows, float* out) {
 #endif
 template <typename T, int D>
 hipError_t launch_scores_td(const HalveArgs& a, int64_t nbk, hipStream_t st) {
-  using SS = ScoreShape<T, D>;
-  auto kern_mixed = pair_scores_kernel<T, D, false, false>;
-  auto kern_own = pair_scores_kernel<T, D, false, true>;
-  const size_t lds = SS::LDS;
+  constexpr int WO = own_waves<T, D>();
+  using SS = ScoreShape<T, D, kScoreWaves>;
+  using SO = ScoreShape<T, D, WO>;
+  static_assert(SO::GT == SS::GT, "own-only and streamed launches share the groups");
+  auto kern_mixed = pair_scores_kernel<T, D, false, false, kScoreWaves>;
+  auto kern_own = pair_scores_kernel<T, D, false, true, WO>;
+  const size_t lds = SS::LDS, lds_own = SO::LDS;
   if (lds > 64 * 1024) {
-    for (const void* k : {reinterpret_cast<const void*>(kern_mixed), reinterpret_cast<const void*>(kern_own)}) {
-      hipError_t e = hipFuncSetAttribute(k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-      if (e != hipSuccess) return e;
-    }
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern_mixed),
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e != hipSuccess) return e;
+  }
+  if (lds_own > 64 * 1024) {
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern_own),
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds_own);
+    if (e != hipSuccess) return e;
   }
   const int64_t NT = (a.N + 15) / 16;
   const int64_t groups = (NT + SS::GT - 1) / SS::GT;
@@ -1467,7 +1484,7 @@ hipError_t launch_scores_td(const HalveArgs& a, int64_t nbk, hipStream_t st) {
     const int64_t wgs = 8 * per_xcd * ipb;
     // a launch of own chunks only takes the own-only instantiation
     if (chunk0 == 0 && nz == 1)
-      hipLaunchKernelGGL(kern_own, dim3((unsigned)wgs), dim3(64 * kScoreWaves), lds, st, x);
+      hipLaunchKernelGGL(kern_own, dim3((unsigned)wgs), dim3(64 * WO), lds_own, st, x);
     else
       hipLaunchKernelGGL(kern_mixed, dim3((unsigned)wgs), dim3(64 * kScoreWaves), lds, st, x);
   };
@@ -1485,8 +1502,9 @@ hipError_t launch_scores_td(const HalveArgs& a, int64_t nbk, hipStream_t st) {
 
 template <typename T, int D>
 hipError_t launch_local_td(const HalveArgs& a0, int64_t nbk, hipStream_t st) {
-  using SS = ScoreShape<T, D>;
-  auto kern = pair_scores_kernel<T, D, true, true>;
+  constexpr int WO = own_waves<T, D>();
+  using SS = ScoreShape<T, D, WO>;
+  auto kern = pair_scores_kernel<T, D, true, true, WO>;
   const int64_t NT = (a0.N + 15) / 16, nb = (a0.N + 63) / 64, P = a0.N / 2;
   // stages, score tiles, pair scale exponents of the rows, staged row
   // scales, half-block row scale maxima, pair terms [2][P]
@@ -1502,7 +1520,7 @@ hipError_t launch_local_td(const HalveArgs& a0, int64_t nbk, hipStream_t st) {
   a.chunk0 = 0;
   a.ch = kScoreChunk;
   a.e_tiles = 0;
-  hipLaunchKernelGGL(kern, dim3((unsigned)nbk), dim3(64 * kScoreWaves), lds, st, a);
+  hipLaunchKernelGGL(kern, dim3((unsigned)nbk), dim3(64 * WO), lds, st, a);
   return hipGetLastError();
 }
 
@@ -1519,9 +1537,9 @@ hipError_t launch_local_t(int64_t d, const HalveArgs& a, int64_t nbk, hipStream_
 template <typename T>
 int64_t local_rows_t(int64_t d) {
   switch (d) {
-    case 32: return ScoreShape<T, 32>::GT * 16;
-    case 64: return ScoreShape<T, 64>::GT * 16;
-    case 128: return ScoreShape<T, 128>::GT * 16;
+    case 32: return ScoreShape<T, 32, own_waves<T, 32>()>::GT * 16;
+    case 64: return ScoreShape<T, 64, own_waves<T, 64>()>::GT * 16;
+    case 128: return ScoreShape<T, 128, own_waves<T, 128>()>::GT * 16;
     default: return 0;
   }
 }

@@ -27,7 +27,7 @@ __global__ void rows_copy_kernel(const int32_t* src, int64_t src_stride, int32_t
 // |V[s, row, c]| over its N rows idx[s * in_stride + t * N + j], as the
 // float's bit pattern at vmax_bits[s * G + t].  One workgroup per call (G
 // calls per slice); a row is d * bytes / 16 16-byte words.
-template <typename T>
+template <typename T, int kU>
 __global__ __launch_bounds__(256) void vmax_rows_kernel(const T* V, int64_t ld, int64_t d,
                                                         const int32_t* idx, int64_t in_stride,
                                                         int64_t N, int64_t G,
@@ -37,18 +37,35 @@ __global__ __launch_bounds__(256) void vmax_rows_kernel(const T* V, int64_t ld, 
   const u32x4* base = reinterpret_cast<const u32x4*>(V + s * ld * d);
   const int32_t* rows = idx + s * in_stride + t * N;
   uint32_t m = 0u;
-  for (int64_t w = threadIdx.x; w < N * wpr; w += blockDim.x) {
-    const int64_t row = rows[w / wpr];
-    const u32x4 x = base[row * wpr + w % wpr];
+  // kU words per thread per pass: every row index of a pass is requested,
+  // then every word, so a pass waits for two memory latencies, not 2 kU
+  // (wpr is a power of two for every supported d and element size)
+  const int sh = __builtin_ctzll((unsigned long long)wpr);
+  const int32_t total = (int32_t)(N * wpr);
+  for (int32_t w0 = threadIdx.x; w0 < total; w0 += kU * (int32_t)blockDim.x) {
+    int64_t row[kU];
 #pragma unroll
-    for (int c = 0; c < 4; ++c) {
-      if (Elem<T>::bytes == 4) {
-        m = max(m, x[c] & 0x7fffffffu);
-      } else {
-        m = max(m, (x[c] << 16) & 0x7fffffffu);
-        m = max(m, x[c] & 0x7fff0000u);
-      }
+    for (int u = 0; u < kU; ++u) {
+      const int32_t w = w0 + u * (int32_t)blockDim.x;
+      row[u] = w < total ? (int64_t)rows[w >> sh] : -1;
     }
+    u32x4 x[kU];
+#pragma unroll
+    for (int u = 0; u < kU; ++u) {
+      const int32_t w = w0 + u * (int32_t)blockDim.x;
+      x[u] = row[u] >= 0 ? base[row[u] * wpr + (w & (int32_t)(wpr - 1))] : (u32x4){0u, 0u, 0u, 0u};
+    }
+#pragma unroll
+    for (int u = 0; u < kU; ++u)
+#pragma unroll
+      for (int c = 0; c < 4; ++c) {
+        if (Elem<T>::bytes == 4) {
+          m = max(m, x[u][c] & 0x7fffffffu);
+        } else {
+          m = max(m, (x[u][c] << 16) & 0x7fffffffu);
+          m = max(m, x[u][c] & 0x7fff0000u);
+        }
+      }
   }
   const float mf = wave_max(__uint_as_float(m));
   __shared__ float part[4];
@@ -391,13 +408,26 @@ hipError_t launch_rows_copy(const int32_t* src, int64_t src_stride, int32_t* dst
 hipError_t launch_vmax_rows(int dtype, const void* V, int64_t ld, int64_t d, const int32_t* idx,
                             int64_t in_stride, int64_t N, int64_t G, int64_t S,
                             uint32_t* vmax_bits, hipStream_t st) {
+  // a call's words are counted in 32 bits
+  const int64_t words = N * d * (dtype == 0 ? 4 : 2) / 16;
+  if (words >= ((int64_t)1 << 31)) return hipErrorInvalidValue;
   const dim3 grid((unsigned)(S * G));
-  if (dtype == 0)
-    hipLaunchKernelGGL(vmax_rows_kernel<float>, grid, dim3(256), 0, st, (const float*)V, ld, d,
-                       idx, in_stride, N, G, vmax_bits);
-  else
-    hipLaunchKernelGGL(vmax_rows_kernel<bf16_t>, grid, dim3(256), 0, st, (const bf16_t*)V, ld, d,
-                       idx, in_stride, N, G, vmax_bits);
+  // calls of at most two words per thread take one word per pass
+  if (dtype == 0) {
+    if (words <= 512)
+      hipLaunchKernelGGL((vmax_rows_kernel<float, 1>), grid, dim3(256), 0, st, (const float*)V, ld,
+                         d, idx, in_stride, N, G, vmax_bits);
+    else
+      hipLaunchKernelGGL((vmax_rows_kernel<float, 8>), grid, dim3(256), 0, st, (const float*)V, ld,
+                         d, idx, in_stride, N, G, vmax_bits);
+  } else {
+    if (words <= 512)
+      hipLaunchKernelGGL((vmax_rows_kernel<bf16_t, 1>), grid, dim3(256), 0, st, (const bf16_t*)V,
+                         ld, d, idx, in_stride, N, G, vmax_bits);
+    else
+      hipLaunchKernelGGL((vmax_rows_kernel<bf16_t, 8>), grid, dim3(256), 0, st, (const bf16_t*)V,
+                         ld, d, idx, in_stride, N, G, vmax_bits);
+  }
   return hipGetLastError();
 }
 

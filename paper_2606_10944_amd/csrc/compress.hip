@@ -1058,6 +1058,129 @@ void pair_scores_kernel(HalveArgs a) {
 #undef SCORE_OWN_COMMIT
 }
 
+// Buckets of at most 64 rows (one decision block of P <= 32 pairs): one
+// wavefront per bucket, eight buckets per workgroup, the whole round in
+// registers and a 4 KiB score tile in LDS.  The arithmetic is the local
+// kernel's, step for step (the same Gram words in the same order, the same
+// epilogue, scales, thresholds and decision loop), so both take the same
+// decisions; what changes is the size of the work unit: the local kernel
+// gives a whole workgroup of eight waves to a bucket, which at 16-64 rows
+// leaves most of them idle (the prefill's Compress2 calls are 16-row buckets,
+// 98304 of them in one launch).  RT = 16-row tiles per bucket (N <= 16 RT).
+constexpr int kTinyWaves = 8;
+#ifndef TINY_MIN_BUCKETS
+#define TINY_MIN_BUCKETS 1024
+#endif
+constexpr int64_t kTinyMinBuckets = TINY_MIN_BUCKETS;  // launches with fewer take the local kernel
+constexpr int kTinyStride = 33;  // floats per score row in LDS (rows i, columns p)
+
+template <typename T, int D, int RT>
+__global__ __launch_bounds__(64 * kTinyWaves) void tiny_halve_kernel(HalveArgs a) {
+  constexpr int NV = Frag<T, D>::NV;
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const int m16 = lane & 15, g = lane >> 4;
+  const bool odd = (m16 & 1) != 0;
+  const int64_t bl = (int64_t)blockIdx.x * kTinyWaves + wave;
+  if (bl >= a.nbk) return;  // no barrier below: a wave without a bucket just ends
+  const int N = a.N, P = N >> 1;
+  const int64_t bucket = a.b0 + bl;
+  const int64_t s = bucket / a.G, t = bucket % a.G;
+  const T* K = reinterpret_cast<const T*>(a.K) + s * a.ld * D;
+  const T* V = reinterpret_cast<const T*>(a.V) + s * a.ld * D;
+  const int32_t* rows_in = a.idx_in ? a.idx_in + s * in_stride(a) + t * (int64_t)N : nullptr;
+  const int64_t row_base = t * (int64_t)N;
+  const float vmax = __uint_as_float(a.vmax_bits[a.vmax_per_bucket ? bucket : s]);
+  const float vm2f = vmax * vmax;
+  const double vm2d = (double)vmax * (double)vmax;
+  const double inv_sqrt_d = 1.0 / sqrt((double)D);
+  const float c2 = (float)(kLog2e * inv_sqrt_d);
+
+  __shared__ float s_e[kTinyWaves][32 * kTinyStride];  // E(i, p) at [i * stride + p]
+  __shared__ float s_h2p[kTinyWaves][32], s_lbt[kTinyWaves][32];
+  float* e = s_e[wave];
+
+  // rows and their fragments
+  int64_t ar[RT];
+  uint4 Ak[RT][NV], Av[RT][NV];
+#pragma unroll
+  for (int rt = 0; rt < RT; ++rt) {
+    const int j = rt * 16 + m16;
+    ar[rt] = j < N ? (rows_in ? (int64_t)rows_in[j] : row_base + j) : -1;
+  }
+#pragma unroll
+  for (int rt = 0; rt < RT; ++rt) {
+    const bool valid = ar[rt] >= 0;
+    load_frag<T, D>(K, valid ? ar[rt] : 0, g, valid, Ak[rt]);
+    load_frag<T, D>(V, valid ? ar[rt] : 0, g, valid, Av[rt]);
+  }
+  // pair terms; the block's largest row scale (rows past the bucket: 0)
+  float h2c[RT];
+  float mB = 0.0f;
+#pragma unroll
+  for (int rt = 0; rt < RT; ++rt) {
+    float rh2, h2f, lbt;
+    frag_pair_terms<T, D>(Ak[rt], Av[rt], vm2d, inv_sqrt_d, rh2, h2f, lbt);
+    const int j = rt * 16 + m16;
+    h2c[rt] = j < N ? h2f : 0.0f;
+    mB = fmaxf(mB, ar[rt] >= 0 ? rh2 : 0.0f);
+    if (g == 0 && j < N && (j & 1) == 0) {
+      s_h2p[wave][j >> 1] = h2f;
+      s_lbt[wave][j >> 1] = lbt;
+    }
+    if (a.rowh2_write && g == 0 && j < N) a.rowh2[s * a.n + ar[rt]] = rh2;
+  }
+  mB = wave_max_f(mB);
+  // scores of every row tile against every column tile from its diagonal on
+#pragma unroll
+  for (int ct = 0; ct < RT; ++ct) {
+    const float he = h2c[ct] + scale_shift(mB, h2c[ct]);
+#pragma unroll
+    for (int rt = 0; rt <= ct; ++rt) {
+      floatx4_t gk = {0.f, 0.f, 0.f, 0.f};
+      floatx4_t gv = {vm2f, vm2f, vm2f, vm2f};  // <v,v'> + v_max^2
+#pragma unroll
+      for (int v = 0; v < NV; ++v) {
+        gk = mma_word<T>(Ak[rt][v], Ak[ct][v], gk);
+        gv = mma_word<T>(Av[rt][v], Av[ct][v], gv);
+      }
+      float kap[4];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) kap[q] = __builtin_amdgcn_exp2f(gk[q] * c2 - he) * gv[q];
+      const float F0 = kap[1] - kap[0];
+      const float F1 = kap[3] - kap[2];
+      const float mine = odd ? F1 : F0;
+      const float other = from_partner(odd ? F0 : F1);
+      // lane (g, m16): pair i = 8 rt + 2 g + odd of the row tile against pair
+      // p = 8 ct + m16 / 2 of the column tile
+      e[(8 * rt + 2 * g + (odd ? 1 : 0)) * kTinyStride + 8 * ct + (m16 >> 1)] =
+          odd ? other - mine : mine - other;
+    }
+  }
+  // the wave's score writes are complete before any lane reads another's
+  asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+  // the block's decisions (no earlier block: alpha starts at zero)
+  const int pl = lane & 31;
+  const int gp = min(pl, P - 1);
+  const float* Ub = a.U + s * a.u_slice + bucket_u(a, t, P);
+  double carry = -INFINITY;
+  const double thr = block_threshold(s_lbt[wave][gp], s_h2p[wave][gp], Ub[gp], P, lane, a.log_c,
+                                     carry);
+  const int sh = (int)scale_shift(mB, s_h2p[wave][gp]);
+  float ef[32];
+#pragma unroll
+  for (int i = 0; i < 32; ++i) ef[i] = e[i * kTinyStride + gp];
+  float unused = 0.0f;
+  const uint32_t smask = decide_block<false>(ldexp(0.0, -sh), ldexp(thr, -sh), ef, ef, P, unused);
+  if (lane < P) {
+    const uint32_t bit = (smask >> pl) & 1u;
+    const int32_t r0 = rows_in ? rows_in[2 * gp] : (int32_t)(row_base + 2 * gp);
+    const int32_t r1 = rows_in ? rows_in[2 * gp + 1] : (int32_t)(row_base + 2 * gp + 1);
+    a.idx_out[s * out_stride(a) + t * (int64_t)P + gp] = bit ? r1 : r0;
+    if (a.trace) a.trace[s * a.u_slice + bucket_u(a, t, P) + gp] = (uint8_t)bit;
+  }
+}
+
 // Decision pass of one bucket per workgroup, in three roles that run ahead
 // of or behind each other, synchronised by progress counters in LDS:
 //  - wave 1 (fetcher) stages each block's inputs in a ring of FD + 1 LDS
@@ -1500,8 +1623,34 @@ hipError_t launch_scores_td(const HalveArgs& a, int64_t nbk, hipStream_t st) {
   return hipGetLastError();
 }
 
+// One wave per bucket for buckets of up to 16 RT rows whose fragments fit
+// (RT NV <= 16 words per lane and operand).
+template <typename T, int D>
+constexpr int tiny_tiles() {
+  return Frag<T, D>::NV <= 4 ? 4 : 16 / Frag<T, D>::NV;
+}
+
+template <typename T, int D, int RT>
+hipError_t launch_tiny_td(const HalveArgs& a0, int64_t nbk, hipStream_t st) {
+  HalveArgs a = a0;
+  a.nbk = nbk;
+  const unsigned wgs = (unsigned)((nbk + kTinyWaves - 1) / kTinyWaves);
+  hipLaunchKernelGGL((tiny_halve_kernel<T, D, RT>), dim3(wgs), dim3(64 * kTinyWaves), 0, st, a);
+  return hipGetLastError();
+}
+
 template <typename T, int D>
 hipError_t launch_local_td(const HalveArgs& a0, int64_t nbk, hipStream_t st) {
+  // with few buckets one wave per bucket leaves the GPU idle and a bucket's
+  // latency (its tiles one after another) sets the time: the local kernel's
+  // eight waves per bucket are faster there
+  if (nbk >= kTinyMinBuckets) {
+    if (a0.N <= 16) return launch_tiny_td<T, D, 1>(a0, nbk, st);
+    if constexpr (tiny_tiles<T, D>() >= 2)
+      if (a0.N <= 32) return launch_tiny_td<T, D, 2>(a0, nbk, st);
+    if constexpr (tiny_tiles<T, D>() >= 4)
+      if (a0.N <= 64) return launch_tiny_td<T, D, 4>(a0, nbk, st);
+  }
   constexpr int WO = own_waves<T, D>();
   using SS = ScoreShape<T, D, WO>;
   auto kern = pair_scores_kernel<T, D, true, true, WO>;

@@ -180,6 +180,9 @@ CUSTOM = [
     dict(B=1, H=1, n=1024, n_out=64, g=2, d=128, dtype="fp32", kind="gauss_d4"),
     # bf16 d = 32: local rounds, then 512- and 1024-row buckets
     dict(B=1, H=2, n=4096, n_out=8, g=6, d=32, dtype="bf16", kind="gauss"),
+    # 64 slices: rounds of 16384, 4096 and 1024 buckets of 16, 32 and 64 rows
+    # (one wavefront per bucket), then the local and score kernels
+    dict(B=4, H=16, n=4096, n_out=16, g=3, d=32, dtype="bf16", kind="heavy_tail"),
     # keys with a shared mean and 5% of rows x4 (cross exponents far above
     # small pairs' diagonal ones): local rounds, then 512-row buckets
     dict(B=2, H=1, n=4096, n_out=64, g=2, d=128, dtype="bf16", kind="heavy_tail_mean"),

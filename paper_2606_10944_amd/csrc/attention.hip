@@ -498,13 +498,41 @@ __global__ __launch_bounds__(64 * WR) void coreset_attn_res_kernel(
           __builtin_nontemporal_store((f4_t){vb[0], vb[1], vb[2], vb[3]}, reinterpret_cast<f4_t*>(db));
         }
       } else {
+        // bf16: lane (g, m16) holds columns 16 dt + 4g .. +3 of query m16.
+        // Lanes g = 2h and 2h + 1 (16 apart) exchange one of two adjacent
+        // tiles (one row swap per packed word), so that each stores 16
+        // contiguous bytes: the even lane columns 16 dt_e + 8h .. +7, the odd
+        // lane 16 dt_o + 8h .. +7; the four lanes of a query then write 64
+        // contiguous bytes per tile pair, not 8-byte pieces.
         const int64_t q = qw + qt * 16 + m16;
-        if (q < q_end) {
-          TO* orow = O + (s * n_q + q) * D;
+        const bool oddrow = (g & 1) != 0;
+        const int h = g >> 1;
+        TO* orow = O + (s * n_q + min(q, q_end - 1)) * D;
 #pragma unroll
-          for (int dt = 0; dt < D / 16; ++dt)
-            store4<TO>(orow + dt * 16 + 4 * g, acc[qt][dt][0] * inv_l[qt], acc[qt][dt][1] * inv_l[qt],
-                       acc[qt][dt][2] * inv_l[qt], acc[qt][dt][3] * inv_l[qt]);
+        for (int k = 0; k < D / 32; ++k) {
+          typedef __bf16 b2 __attribute__((ext_vector_type(2)));
+          uint32_t ev[2], od[2];
+#pragma unroll
+          for (int j = 0; j < 2; ++j) {
+            const b2 e2 = {(__bf16)(acc[qt][2 * k][2 * j] * inv_l[qt]),
+                           (__bf16)(acc[qt][2 * k][2 * j + 1] * inv_l[qt])};
+            const b2 o2 = {(__bf16)(acc[qt][2 * k + 1][2 * j] * inv_l[qt]),
+                           (__bf16)(acc[qt][2 * k + 1][2 * j + 1] * inv_l[qt])};
+            ev[j] = __builtin_bit_cast(uint32_t, e2);
+            od[j] = __builtin_bit_cast(uint32_t, o2);
+          }
+          // even row lanes receive the partner's even tile, odd row lanes the
+          // partner's odd tile
+          uint32_t got[2];
+#pragma unroll
+          for (int j = 0; j < 2; ++j) {
+            const auto r = __builtin_amdgcn_permlane16_swap(ev[j], od[j], false, false);
+            got[j] = oddrow ? r[0] : r[1];
+          }
+          const uint4 w = oddrow ? make_uint4(got[0], got[1], od[0], od[1])
+                                 : make_uint4(ev[0], ev[1], got[0], got[1]);
+          if (q < q_end)
+            *reinterpret_cast<uint4*>(orow + 16 * (2 * k + (oddrow ? 1 : 0)) + 8 * h) = w;
         }
       }
 #pragma unroll

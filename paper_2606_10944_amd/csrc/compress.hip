@@ -1778,9 +1778,12 @@ hipError_t launch_decide(const HalveArgs& a0, int64_t nbk, hipStream_t st) {
   if (later <= 256) return launch_pass_w<2, 2, PASS_FD_S>(a, nbk, st);
   if (later <= 512) return launch_pass_w<PASS_BW_M, PASS_NCB_M, PASS_FD_M>(a, nbk, st);
   // the large shape's column buffers take 9 KiB of LDS per bulk wave: past
-  // the 160 KiB of a CU (buckets above 4096 rows) the medium shape runs
+  // the 160 KiB of a CU (buckets above 4096 rows) eight bulk waves run, past
+  // that the medium shape
   if (PassLds<PASS_BW_L, PASS_NCB_L, PASS_FD_L>::bytes((int)(a.N / 2)) <= kPassMaxLds)
     return launch_pass_w<PASS_BW_L, PASS_NCB_L, PASS_FD_L>(a, nbk, st);
+  if (PassLds<8, 3, 2>::bytes((int)(a.N / 2)) <= kPassMaxLds)
+    return launch_pass_w<8, 3, 2>(a, nbk, st);
   return launch_pass_w<PASS_BW_M, PASS_NCB_M, PASS_FD_M>(a, nbk, st);
 }
 

@@ -489,9 +489,40 @@ __device__ __forceinline__ void half_block(int w, int h, int& b, int& half) {
 // pair i >= p has been added; decisions past the block's npb pairs are
 // dropped.  With NEAR, en[i] = E(i, q) for a pair q of the next block, and
 // near receives q's signed sum over the block (float32, in ascending i).
+#ifndef DECIDE_ASM
+#define DECIDE_ASM 1
+#endif
 template <bool NEAR>
 __device__ __forceinline__ uint32_t decide_block(double alpha, double thr, const float* ef,
                                                  const float* en, int npb, float& near) {
+#if DECIDE_ASM
+  // One step: compare (vector, into VCC), test bit i of VCC (scalar, into
+  // SCC), select +-1.0 as a float64 pair on SCC, FMA; then, off the chain,
+  // the float32 +-1 for the signed sum and the decision shifted into a
+  // scalar mask (decision i at bit 31 - i: mask + mask + SCC).  Four
+  // instructions on the chain against five to six for the same arithmetic
+  // in compiled C++, which builds the sign with shifts and masks.
+  uint32_t rmask = 0;
+  const double one = 1.0, mone = -1.0;
+#pragma unroll
+  for (int i = 0; i < 32; ++i) {
+    const double e = (double)ef[i];
+    double sg;
+    float sf;
+    asm volatile(
+        "v_cmp_lt_f64_e32 vcc, %[a], %[t]\n\t"
+        "s_bitcmp1_b32 vcc_lo, %[i]\n\t"
+        "s_cselect_b64 %[sg], %[mo], %[o]\n\t"
+        "v_fmac_f64_e32 %[a], %[sg], %[e]\n\t"
+        "s_cselect_b32 %[sf], -1.0, 1.0\n\t"
+        "s_addc_u32 %[m], %[m], %[m]"
+        : [a] "+v"(alpha), [sg] "=&s"(sg), [sf] "=&s"(sf), [m] "+s"(rmask)
+        : [t] "v"(thr), [e] "v"(e), [i] "n"(i), [mo] "s"(mone), [o] "s"(one)
+        : "vcc", "scc");
+    if (NEAR) near = __builtin_fmaf(en[i], sf, near);
+  }
+  uint32_t smask = __builtin_bitreverse32(rmask);
+#else
   uint32_t smask = 0;
 #pragma unroll
   for (int i = 0; i < 32; ++i) {
@@ -503,6 +534,7 @@ __device__ __forceinline__ uint32_t decide_block(double alpha, double thr, const
     alpha = __builtin_fma(e, __hiloint2double((int)(0x3ff00000u | (d << 31)), 0), alpha);
     if (NEAR) near = __builtin_fmaf(en[i], __uint_as_float(0x3f800000u | (d << 31)), near);
   }
+#endif
   if (npb < 32) smask &= (1u << npb) - 1u;
   return smask;
 }
@@ -1442,10 +1474,8 @@ __global__ __launch_bounds__(64 * (BW + 2)) void halve_pass_kernel(HalveArgs a) 
     for (int m = 0; m < nblk; m += FD) {
 #pragma unroll
       for (int k = 0; k < FD; ++k) {
-        if (m + k < nblk) {
-          PASS_STAGE(m + k, k);
-          PASS_FETCH(m + k + FD, k);
-        }
+        if (m + k < nblk) PASS_STAGE(m + k, k);
+        PASS_FETCH(m + k + FD, k);
       }
     }
 #undef PASS_FETCH

@@ -97,9 +97,30 @@ size_t block_scales(int64_t S, const Levels& lv) {
   return m;
 }
 
+// Decision helpers' sizes over the rounds that may use them (thin::pass_helpers):
+// tagged decision words, chunk flags, partial alphas.
+struct HelperSizes {
+  size_t masks = 0, flags = 0, alphas = 0;
+};
+HelperSizes helper_sizes(int64_t S, const Levels& lv) {
+  HelperSizes h;
+  for (int32_t r = 0; r < lv.L; ++r) {
+    const int64_t buckets = S * lv.G[r], P = lv.N[r] / 2;
+    if (buckets > thin::kHelperMaxBuckets || P < thin::kHelperMinPairs || P % 64 != 0) continue;
+    h.masks = std::max(h.masks, (size_t)(buckets * ((P + 31) / 32)));
+    h.flags = std::max(h.flags, (size_t)(buckets * ((P + 63) / 64)));
+    h.alphas = std::max(h.alphas, (size_t)(buckets * P));
+  }
+  return h;
+}
+
 struct Workspace {
   int32_t* status;  // the device status word (thin.h), first in every workspace
   uint32_t* vmax_bits;
+  uint64_t* gmask;  // decision helpers (null when no round may use them); zeroed with vmax_bits
+  uint32_t* gflag;
+  uint64_t* galpha;
+  int64_t zero_words;  // words from vmax_bits through gflag
   int32_t* buf_a;  // [S, n_kept]
   int32_t* buf_b;  // [S, n_kept / 2]
   float* lbt;      // [S, n_kept / 2]
@@ -119,7 +140,16 @@ Workspace carve(void* base, int64_t S, int64_t d, const Levels& lv, size_t cap =
   w.status = reinterpret_cast<int32_t*>(p + off);
   off += 256;
   w.vmax_bits = reinterpret_cast<uint32_t*>(p + off);
+  const size_t vmax_off = off;
   off += align256((size_t)S * 4);
+  const HelperSizes hs = helper_sizes(S, lv);
+  w.gmask = hs.masks ? reinterpret_cast<uint64_t*>(p + off) : nullptr;
+  off += align256(hs.masks * 8);
+  w.gflag = hs.flags ? reinterpret_cast<uint32_t*>(p + off) : nullptr;
+  off += align256(hs.flags * 4);
+  w.zero_words = (int64_t)((off - vmax_off) / 4);
+  w.galpha = hs.alphas ? reinterpret_cast<uint64_t*>(p + off) : nullptr;
+  off += align256(hs.alphas * 8);
   w.buf_a = reinterpret_cast<int32_t*>(p + off);
   off += align256((size_t)S * (size_t)lv.n_kept * 4);
   w.buf_b = reinterpret_cast<int32_t*>(p + off);
@@ -170,6 +200,11 @@ hipError_t kh_round(int32_t dtype, int64_t d, thin::HalveArgs a, int64_t buckets
   const size_t per = thin::halve_score_bytes(a.N);
   int64_t chunk = (int64_t)(e_bytes / per);
   if (chunk < 1) chunk = 1;
+  if (chunk < buckets) {  // several launches: the helpers' tags are per round
+    a.gmask = nullptr;
+    a.gflag = nullptr;
+    a.galpha = nullptr;
+  }
   hipError_t e = hipSuccess;
   for (int64_t b0 = 0; b0 < buckets && e == hipSuccess; b0 += chunk) {
     a.b0 = b0;
@@ -267,7 +302,7 @@ int compress_impl(const void* K, const void* V, int32_t dtype, int64_t B, int64_
     }
   } else {
     ok(observed(THIN_KERNEL_VMAX, -1, st, [&] {
-      return thin::launch_vmax(dtype, Vm, S, nm, n, d, ws.vmax_bits, st, ws.status);
+      return thin::launch_vmax(dtype, Vm, S, nm, n, d, ws.vmax_bits, st, ws.status, ws.zero_words);
     }));
     int64_t u_off = lv.sub ? lv.n_kept : 0;
     for (int32_t r = 0; r < lv.L && e == hipSuccess; ++r) {
@@ -296,6 +331,10 @@ int compress_impl(const void* K, const void* V, int32_t dtype, int64_t B, int64_
       a.rowh2_write = r == 0;
       a.mB = ws.mB;
       a.status = ws.status;
+      a.gmask = ws.gmask;
+      a.gflag = ws.gflag;
+      a.galpha = ws.galpha;
+      a.pass_tag = r + 1;
       a.chunk0 = 0;
       a.b0 = 0;
       ok(kh_round(dtype, d, a, S * lv.G[r], ws.e_bytes, r, st));

@@ -1251,6 +1251,76 @@ __device__ __forceinline__ void publish(int* flag, int value) {
   __hip_atomic_store(flag, value, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
 }
 
+// Decision helpers: rows 0 .. hand_row(c) of chunk c are added by helper
+// workgroups, the last kPassHand rows before the chunk's first block by the
+// bucket's own bulk waves (the hand-over then has kPassHand + 1 blocks of
+// decisions to arrive before the decider needs the chunk).
+#ifndef PASS_HAND
+#define PASS_HAND 6
+#endif
+constexpr int kPassHand = PASS_HAND;
+__device__ __forceinline__ int hand_row(int c) { return 2 * c - 2 - kPassHand; }
+// Every access to the words the helpers share with the bucket's workgroup
+// (decisions, flags, partials) is a read-modify-write atomic at agent scope:
+// all of them are then performed at one place, the L2 of the XCD that runs
+// the bucket's workgroup and its helpers (pass_helpers keeps them on one),
+// so a flag seen there covers the partials written before it.
+// The word reads and the flag updates are made once per wave (lane 0, the
+// result broadcast): lanes that each update one flag would each see another
+// old value.
+__device__ __forceinline__ uint64_t shared_read(uint64_t* p) {
+  uint64_t v = 0;
+  if ((threadIdx.x & 63) == 0) v = __hip_atomic_fetch_add(p, (uint64_t)0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  return __shfl(v, 0);
+}
+__device__ __forceinline__ uint32_t shared_read(uint32_t* p) {
+  uint32_t v = 0;
+  if ((threadIdx.x & 63) == 0) v = __hip_atomic_fetch_add(p, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  return __shfl(v, 0);
+}
+// flag = max(flag, v); returns the old value (wave-uniform)
+__device__ __forceinline__ uint32_t shared_max(uint32_t* p, uint32_t v) {
+  uint32_t old = 0;
+  if ((threadIdx.x & 63) == 0) old = __hip_atomic_fetch_max(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  return __shfl(old, 0);
+}
+// per lane (each lane its own word)
+__device__ __forceinline__ uint64_t shared_read_lane(uint64_t* p) {
+  return __hip_atomic_fetch_add(p, (uint64_t)0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void shared_write(uint64_t* p, uint64_t v) {
+  (void)__hip_atomic_exchange(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+// Tag of block m's decisions in a round: nonzero, distinct per round and block.
+__device__ __forceinline__ uint32_t helper_tag(int32_t round_tag, int m) {
+  return ((uint32_t)round_tag << 16) | (uint32_t)(m + 1);
+}
+// The decisions in a tagged word once its tag is `tag` (`w` read ahead;
+// bounded wait at agent scope, like wait_at_least).
+__device__ __forceinline__ uint32_t decided_mask(uint64_t* p, uint64_t w, uint32_t tag,
+                                                 int32_t* status) {
+  for (int it = 0; (uint32_t)(w >> 32) != tag; ++it) {
+    if (it == kSpinLimit) {
+      if (status) __hip_atomic_store(status, kStatusWaitExhausted, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      break;
+    }
+    __builtin_amdgcn_s_sleep(2);
+    w = shared_read(p);
+  }
+  return (uint32_t)w;
+}
+__device__ __forceinline__ void wait_flag(uint32_t* p, uint32_t value, int32_t* status) {
+  uint32_t v = shared_read(p);
+  for (int it = 0; v < value; ++it) {
+    if (it == kSpinLimit) {
+      if (status) __hip_atomic_store(status, kStatusWaitExhausted, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      break;
+    }
+    __builtin_amdgcn_s_sleep(2);
+    v = shared_read(p);
+  }
+}
+
 template <int BW, int NCB, int FD>
 struct PassLds {
   static constexpr int BP = 32, QW = 8, NSLOT = FD + 1;
@@ -1288,7 +1358,7 @@ struct PassLds {
   }
 };
 
-template <int BW, int NCB, int FD>
+template <int BW, int NCB, int FD, bool HELP>
 __global__ __launch_bounds__(64 * (BW + 2)) void halve_pass_kernel(HalveArgs a) {
   using L = PassLds<BW, NCB, FD>;
   constexpr int RT = 4;
@@ -1300,7 +1370,11 @@ __global__ __launch_bounds__(64 * (BW + 2)) void halve_pass_kernel(HalveArgs a) 
 
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int64_t bl = blockIdx.x;
+  // with helpers: workgroups [0, nbk) take their bucket's decisions, then
+  // come helper 1 of every bucket, helper 2, ...
+  const int HLP = HELP ? a.pass_h : 0;  // launches without helpers compile none of their code
+  const int role = HLP ? (int)(blockIdx.x / a.nbk) : 0;
+  const int64_t bl = HLP ? (int64_t)(blockIdx.x % a.nbk) : (int64_t)blockIdx.x;
   const int64_t bucket = a.b0 + bl;
   const int64_t s = bucket / a.G;
   const int64_t t = bucket % a.G;
@@ -1308,6 +1382,7 @@ __global__ __launch_bounds__(64 * (BW + 2)) void halve_pass_kernel(HalveArgs a) 
   const int P = N >> 1;
   const int NT = (N + 15) >> 4;
   const int nblk = (P + BP - 1) / BP;
+  const int nch = (P + 63) >> 6;
   const int32_t* rows_in = a.idx_in ? a.idx_in + s * in_stride(a) + t * (int64_t)N : nullptr;
   const int64_t row_base = t * (int64_t)N;
   const float* Ub = a.U + s * a.u_slice + bucket_u(a, t, P);
@@ -1357,7 +1432,92 @@ __global__ __launch_bounds__(64 * (BW + 2)) void halve_pass_kernel(HalveArgs a) 
   reinterpret_cast<const u32x4*>(Eb + (panel_tiles(B, NT, RT) + ((P_) >> 3) - (B) * RT) * TILE + \
                                  ((P_) & 7) * BP)
 
-  if (wave == 0) {
+  if (role > 0) {
+    // ---- helper (waves 2..): the early rows of chunks ----
+    // Helper wave hw of T = HLP BW takes chunks c = hw, hw + T, ... whose
+    // hand_row(c) >= 0 and that it claims first (the bucket's workgroup
+    // claims a chunk it reaches unclaimed and adds all its rows itself, so a
+    // helper that is not resident delays nothing), rows 0 .. hand_row(c) in
+    // order (a row's decisions from gmask, read with the row's scores and
+    // checked by their tag), into a float64 alpha per pair in a register:
+    // the same additions in the same order as the bucket's own bulk waves.
+    // Then the chunk's partials go to galpha and, once written (vmcnt(0)),
+    // its flag to "done".  All at agent scope: the bucket's workgroup runs on
+    // another compute unit.
+    if (wave < 2) return;
+    const int T = HLP * BW;
+    const int hw = (role - 1) * BW + (wave - 2);
+    uint64_t* gm = a.gmask + bl * nblk;
+    uint32_t* gf = a.gflag + bl * nch;
+    const uint32_t claimed = 2u * (uint32_t)a.pass_tag, done = claimed + 1u;
+    // next item to load: row fb of chunk fc
+    int fc = hw, fb = 0;
+    auto h_enter = [&]() {  // from fc on, the first chunk with rows that this wave claims
+      while (fc < nch && (hand_row(fc) < 0 || shared_max(gf + fc, claimed) >= claimed)) fc += T;
+      fb = 0;
+    };
+    h_enter();
+    u32x4* colbuf = reinterpret_cast<u32x4*>(smem + L::colbuf_off(P) + (size_t)(wave - 2) * L::kColBuf);
+    auto h_fetch = [&](u32x4* dst, uint64_t& word, int& ib, int& ic) {
+      const bool live = fc < nch;
+      ib = fb;
+      ic = live ? fc : nch;
+      if constexpr (L::COAL) {
+#pragma unroll
+        for (int k = 0; k < 8; ++k)
+          dst[k] = (live ? PASS_COL(fb, min(64 * fc + 8 * k + lane / QW, P - 1))
+                         : PASS_COL(0, lane / QW))[lane % QW];
+      } else {
+        const u32x4* c_ = live ? PASS_COL(fb, min(64 * fc + lane, P - 1)) : PASS_COL(0, 0);
+#pragma unroll
+        for (int k = 0; k < 8; ++k) dst[k] = c_[k];
+      }
+      word = shared_read(gm + (live ? fb : 0));
+      if (live && ++fb > hand_row(fc)) {
+        fc += T;
+        h_enter();
+      }
+    };
+    u32x4 cb[NCB][8];
+    uint64_t mw[NCB];
+    int ib[NCB], ic[NCB];
+#pragma unroll
+    for (int r = 0; r < NCB; ++r) h_fetch(cb[r], mw[r], ib[r], ic[r]);
+    bool more = ic[0] < nch;
+    double acc = 0.0;
+    while (more) {
+#pragma unroll
+      for (int r = 0; r < NCB; ++r) {
+        const int b = ib[r], c = ic[r];
+        const bool live = c < nch;
+        const uint32_t smask = live ? decided_mask(gm + b, mw[r], helper_tag(a.pass_tag, b), a.status) : 0u;
+        u32x4 col[QW];
+        if constexpr (L::COAL) {
+#pragma unroll
+          for (int k = 0; k < 8; ++k) colbuf[(8 * k + lane / QW) * L::CW + lane % QW] = cb[r][k];
+#pragma unroll
+          for (int q = 0; q < QW; ++q) col[q] = colbuf[lane * L::CW + q];
+        } else {
+#pragma unroll
+          for (int q = 0; q < QW; ++q) col[q] = cb[r][q];
+        }
+        float sum;
+        PASS_SUM(col, smask, sum);
+        const int p = 64 * c + lane;
+        if (live && b == 0) acc = 0.0;
+        if (live && p < P) acc += ldexp((double)sum, (int)scale_shift(s_mB[b], s_h2[p]));
+        h_fetch(cb[r], mw[r], ib[r], ic[r]);
+        if (live && b == hand_row(c)) {
+          if (p < P) shared_write(a.galpha + bl * P + p, __double_as_longlong(acc));
+          __atomic_signal_fence(__ATOMIC_SEQ_CST);
+          __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0): the partials are written
+          __atomic_signal_fence(__ATOMIC_SEQ_CST);
+          (void)shared_max(gf + c, done);
+        }
+        more = ic[(r + 1) % NCB] < nch;
+      }
+    }
+  } else if (wave == 0) {
     // ---- decider ----
     __builtin_amdgcn_s_setprio(3);  // ahead of the bulk waves sharing its SIMD
     double anear = 0.0;             // this lane's pair: the previous block's contribution
@@ -1410,6 +1570,8 @@ __global__ __launch_bounds__(64 * (BW + 2)) void halve_pass_kernel(HalveArgs a) 
       const uint32_t smask = decide_block<true>(alpha, thr, ef, en, npb, near);
       if (lane == 0) s_mask[m] = smask;
       publish(&s_cnt[0], m);
+      if (HLP && lane == 0)
+        shared_write(a.gmask + bl * nblk + m, ((uint64_t)helper_tag(a.pass_tag, m) << 32) | smask);
       const uint32_t bit = (smask >> (p & 31)) & 1u;
       if (active) {
         out[gp] = bit ? r1 : r0;
@@ -1489,26 +1651,44 @@ __global__ __launch_bounds__(64 * (BW + 2)) void halve_pass_kernel(HalveArgs a) 
     // in increasing c, rows in order within a chunk: items are taken in the
     // order the decider needs them (chunk c before block 2c), and a chunk's
     // progress does not wait for the wave's later chunks.  The items form one
-    // stream held in an NCB-slot register ring: each consumed slot is
-    // refilled at once with the item NCB later, so the loads run ahead
-    // whatever the decisions.  Lane l sums column l of the chunk in ascending
-    // order (the order of the decider's sums); with COAL the chunk is loaded
-    // a score tile (8 columns, 1 KiB) per instruction, 8 lanes to a column,
-    // and turned through the wave's LDS column buffer.  After row b of chunk
-    // c the wave publishes b + 1 in s_chunk[c] (rows completed).
+    // stream held in an NCB-slot register ring (with each slot's row and
+    // chunk): each consumed slot is refilled at once with the item NCB later,
+    // so the loads run ahead whatever the decisions.  Lane l sums column l of
+    // the chunk in ascending order (the order of the decider's sums); with
+    // COAL the chunk is loaded a score tile (8 columns, 1 KiB) per
+    // instruction, 8 lanes to a column, and turned through the wave's LDS
+    // column buffer.  After row b of chunk c the wave publishes b + 1 in
+    // s_chunk[c] (rows completed).  With helpers, a chunk a helper has
+    // claimed starts from the helper's partial alpha over rows
+    // 0 .. hand_row(c) (taken from galpha once the chunk's flag is "done")
+    // and continues with rows hand_row(c) + 1 on; a chunk the wave reaches
+    // unclaimed it claims and takes whole.
     const int w = wave - 2;
-    const int nch = (P + 63) >> 6;
     const int nrow = nblk - 2;
     auto last_row = [&](int c) { return min(2 * c - 1, nrow - 1); };  // < 0: no item
-    auto first_chunk = [&]() {
-      int c = w;
-      while (c < nch && last_row(c) < 0) c += BW;
-      return c;
+    uint32_t* gf = HLP ? a.gflag + bl * nch : nullptr;
+    const uint32_t claimed = 2u * (uint32_t)a.pass_tag, done = claimed + 1u;
+    // next item to load: row fb of chunk fc; fh: fb is the first row after
+    // a helper's partial
+    int fc = w, fb = 0;
+    bool fh = false;
+    auto enter = [&]() {  // from fc on, the first chunk with items
+      while (fc < nch && last_row(fc) < 0) fc += BW;
+      fb = 0;
+      fh = false;
+      if (fc < nch && HLP && hand_row(fc) >= 0 && shared_max(gf + fc, claimed) >= claimed) {
+        fb = hand_row(fc) + 1;
+        fh = true;
+      }
     };
-    int fb = 0, fc = first_chunk();  // next item to load
+    enter();
     u32x4* colbuf = reinterpret_cast<u32x4*>(smem + L::colbuf_off(P) + (size_t)w * L::kColBuf);
-    auto fetch_next = [&](u32x4* dst) {
+    auto fetch_next = [&](u32x4* dst, int& ib, int& ic, bool& ih) {
       const bool live = fc < nch;
+      ib = fb;
+      ic = live ? fc : nch;
+      ih = live && fh;
+      fh = false;
       // COAL: word lane % QW of column 8 k + lane / QW of the chunk; else
       // word k of column lane (past the stream's end: valid columns, never
       // used)
@@ -1523,16 +1703,17 @@ __global__ __launch_bounds__(64 * (BW + 2)) void halve_pass_kernel(HalveArgs a) 
         for (int k = 0; k < 8; ++k) dst[k] = c_[k];
       }
       if (live && ++fb > last_row(fc)) {
-        fb = 0;
         fc += BW;
+        enter();
       }
     };
     u32x4 cb[NCB][8];
+    int ib[NCB], ic[NCB];
+    bool ih[NCB];
 #pragma unroll
-    for (int r = 0; r < NCB; ++r) fetch_next(cb[r]);
-    int b = 0, c = first_chunk();  // next item to use
-    int decided = -1;              // last decided block seen
-    bool more = c < nch;
+    for (int r = 0; r < NCB; ++r) fetch_next(cb[r], ib[r], ic[r], ih[r]);
+    int decided = -1;  // last decided block seen
+    bool more = ic[0] < nch;
     // Every slot of a turn is used and refilled whether or not the stream
     // has ended (loads past the end are of valid columns, nothing is added):
     // all paths then issue the same loads, and the wait before a slot's use
@@ -1540,9 +1721,19 @@ __global__ __launch_bounds__(64 * (BW + 2)) void halve_pass_kernel(HalveArgs a) 
     while (more) {
 #pragma unroll
       for (int r = 0; r < NCB; ++r) {
-        const bool live = more;
+        const int b = ib[r], c = ic[r];
+        const bool live = c < nch;
+        if (live && ih[r]) {
+          // the helper's partial alpha of the chunk's pairs (rows 0 .. hand_row(c))
+          wait_flag(gf + c, done, a.status);
+          __atomic_signal_fence(__ATOMIC_SEQ_CST);
+          const int pc = 64 * c + lane;
+          if (pc < P)
+            s_alpha[pc] = __longlong_as_double((long long)shared_read_lane(a.galpha + bl * P + pc));
+          publish(&s_chunk[c], hand_row(c) + 1);
+        }
         if (live && decided < b) decided = wait_at_least(&s_cnt[0], b, a.status);
-        const uint32_t smask = s_mask[min(b, nblk - 1)];
+        const uint32_t smask = s_mask[live ? b : 0];
         u32x4 col[QW];
         if constexpr (L::COAL) {
 #pragma unroll
@@ -1558,15 +1749,9 @@ __global__ __launch_bounds__(64 * (BW + 2)) void halve_pass_kernel(HalveArgs a) 
         const int p = 64 * c + lane;
         if (live && p >= (b + 2) * BP && p < P)
           s_alpha[p] += ldexp((double)sum, (int)scale_shift(s_mB[b], s_h2[p]));
-        fetch_next(cb[r]);
-        if (live) {
-          publish(&s_chunk[c], b + 1);
-          if (++b > last_row(c)) {
-            b = 0;
-            c += BW;
-            more = c < nch;
-          }
-        }
+        fetch_next(cb[r], ib[r], ic[r], ih[r]);
+        if (live) publish(&s_chunk[c], b + 1);
+        more = ic[(r + 1) % NCB] < nch;
       }
     }
   }
@@ -1733,17 +1918,51 @@ hipError_t launch_scores_t(int64_t d, const HalveArgs& a, int64_t nbk, hipStream
   }
 }
 
-template <int BW, int NCB, int FD>
-hipError_t launch_pass_w(const HalveArgs& a, int64_t nbk, hipStream_t st) {
+// Helper workgroups per bucket for a decision launch: rounds of at most
+// kHelperMaxBuckets buckets of at least kHelperMinPairs pairs (one launch
+// per round: the tags of gmask and gflag are per round), as many as the
+// device's compute units hold beside the buckets' own, at most kMaxHelpers.
+int pass_helpers(const HalveArgs& a, int64_t nbk) {
+  const int64_t P = a.N / 2;
+  if (!a.gmask || !a.gflag || !a.galpha || a.pass_tag <= 0 || a.b0 != 0) return 0;
+  // helper k of bucket b is workgroup k nbk + b: on the bucket's XCD (the
+  // dispatcher deals workgroups to the 8 XCDs in turn) when 8 divides nbk
+  if (P < kHelperMinPairs || P % 64 != 0 || nbk < 1 || nbk > kHelperMaxBuckets || nbk % 8 != 0) return 0;
+  int dev = 0, cus = 0;
+  if (hipGetDevice(&dev) != hipSuccess ||
+      hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+    return 0;
+  const int64_t h = cus / nbk - 1;
+  return (int)(h < 0 ? 0 : (h > kMaxHelpers ? kMaxHelpers : h));
+}
+
+template <int BW, int NCB, int FD, bool HELP>
+hipError_t launch_pass_k(const HalveArgs& a, int64_t grid, hipStream_t st) {
   const size_t lds = PassLds<BW, NCB, FD>::bytes((int)(a.N / 2));
-  auto kern = halve_pass_kernel<BW, NCB, FD>;
+  auto kern = halve_pass_kernel<BW, NCB, FD, HELP>;
   if (lds > 64 * 1024) {
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess) return e;
   }
-  hipLaunchKernelGGL(kern, dim3((unsigned)nbk), dim3(64 * (BW + 2)), lds, st, a);
+  hipLaunchKernelGGL(kern, dim3((unsigned)grid), dim3(64 * (BW + 2)), lds, st, a);
   return hipGetLastError();
+}
+
+// HELPERS: the shape may take decision helpers (the large shapes).  Helpers
+// follow the buckets' own workgroups in the grid; a helper waits only for
+// decisions, and a bucket's workgroup never waits for a helper that has not
+// claimed a chunk, so any residency order completes.
+template <int BW, int NCB, int FD, bool HELPERS = false>
+hipError_t launch_pass_w(const HalveArgs& a0, int64_t nbk, hipStream_t st) {
+  HalveArgs a = a0;
+  a.nbk = nbk;
+  a.pass_h = 0;
+  if constexpr (HELPERS) {
+    a.pass_h = pass_helpers(a, nbk);
+    if (a.pass_h > 0) return launch_pass_k<BW, NCB, FD, true>(a, nbk * (1 + a.pass_h), st);
+  }
+  return launch_pass_k<BW, NCB, FD, false>(a, nbk, st);
 }
 
 }  // namespace
@@ -1811,16 +2030,17 @@ hipError_t launch_decide(const HalveArgs& a0, int64_t nbk, hipStream_t st) {
   // the 160 KiB of a CU (buckets above 4096 rows) eight bulk waves run, past
   // that the medium shape
   if (PassLds<PASS_BW_L, PASS_NCB_L, PASS_FD_L>::bytes((int)(a.N / 2)) <= kPassMaxLds)
-    return launch_pass_w<PASS_BW_L, PASS_NCB_L, PASS_FD_L>(a, nbk, st);
+    return launch_pass_w<PASS_BW_L, PASS_NCB_L, PASS_FD_L, true>(a, nbk, st);
   if (PassLds<8, 3, 2>::bytes((int)(a.N / 2)) <= kPassMaxLds)
-    return launch_pass_w<8, 3, 2>(a, nbk, st);
-  return launch_pass_w<PASS_BW_M, PASS_NCB_M, PASS_FD_M>(a, nbk, st);
+    return launch_pass_w<8, 3, 2, true>(a, nbk, st);
+  return launch_pass_w<PASS_BW_M, PASS_NCB_M, PASS_FD_M, true>(a, nbk, st);
 }
 
 hipError_t launch_vmax(int dtype, const void* V, int64_t S, int64_t n, int64_t ld, int64_t d,
-                       uint32_t* vmax_bits, hipStream_t st, int32_t* status) {
-  hipLaunchKernelGGL(zero_u32_kernel, dim3((unsigned)((S + 255) / 256)), dim3(256), 0, st,
-                     vmax_bits, S, status);
+                       uint32_t* vmax_bits, hipStream_t st, int32_t* status, int64_t zero_words) {
+  const int64_t zw = zero_words > S ? zero_words : S;
+  hipLaunchKernelGGL(zero_u32_kernel, dim3((unsigned)((zw + 255) / 256)), dim3(256), 0, st,
+                     vmax_bits, zw, status);
   const int64_t bytes = dtype == 0 ? 4 : 2;
   const int64_t words = n * d * bytes / 16, slice_words = ld * d * bytes / 16;
   const int64_t per_block = 16384;  // 256 KiB of V per workgroup

@@ -46,6 +46,17 @@ struct HalveArgs {
   // Required by the two-launch path
   float* mB;                  // [buckets, ceil(N / 64)] largest row scale of every 64-row block
   int32_t* status;            // nullable: set nonzero if a bounded wait of the decisions gave up
+  // Decision helpers (gmask null: none).  A round that runs as one launch may
+  // spread each bucket's bulk sums over helper workgroups on other compute
+  // units: the bucket's workgroup publishes every block's decisions in gmask,
+  // helpers add the early rows of a chunk of pairs and hand over the partial
+  // alpha in galpha (gflag marks it ready).  gmask and gflag hold zero or
+  // values of earlier rounds of the same call (their tags differ).
+  uint64_t* gmask;            // [nbk, nblk] (tag(round, block) << 32) | decisions
+  uint32_t* gflag;            // [nbk, nch] round tag once the chunk's partial is written
+  uint64_t* galpha;           // [nbk, N / 2] partial alpha of every pair (float64 bits)
+  int32_t pass_tag;           // round tag, nonzero and distinct per round of a call
+  int32_t pass_h;             // helper workgroups per bucket (set by launch_decide)
 };
 
 // Device status word (the first word of every workspace): 0 = every bounded
@@ -62,9 +73,11 @@ int compress_fixed(const void* K, const void* V, int32_t dtype, int64_t B, int64
 
 // dtype: 0 = fp32, 1 = bf16.  Returns a hipError_t.
 // v_max of n rows per slice, slices ld rows apart.
-// status (nullable) is cleared by the same launch.
+// status (nullable) is cleared by the same launch, and max(S, zero_words)
+// words from vmax_bits on (the decision helpers' flags follow the bits).
 hipError_t launch_vmax(int dtype, const void* V, int64_t S, int64_t n, int64_t ld, int64_t d,
-                       uint32_t* vmax_bits, hipStream_t st, int32_t* status = nullptr);
+                       uint32_t* vmax_bits, hipStream_t st, int32_t* status = nullptr,
+                       int64_t zero_words = 0);
 hipError_t launch_zero_status(int32_t* status, hipStream_t st);
 hipError_t launch_subsample(int64_t S, int64_t n, int64_t n_kept, const float* U,
                             int64_t u_slice, int32_t* idx0, hipStream_t st);
@@ -96,6 +109,10 @@ size_t halve_score_bytes(int64_t N);
 // Pair scores, then the decision pass, for nbk buckets starting at a.b0.
 hipError_t launch_scores(int dtype, int64_t d, const HalveArgs& a, int64_t nbk, hipStream_t st);
 hipError_t launch_decide(const HalveArgs& a, int64_t nbk, hipStream_t st);
+// Decision helpers (HalveArgs.gmask): eligible rounds and the most helpers.
+constexpr int64_t kHelperMaxBuckets = 128;
+constexpr int64_t kHelperMinPairs = 2048;
+constexpr int kMaxHelpers = 7;
 // Buckets of at most halve_local_rows(dtype, d) rows: the whole round (scores
 // in LDS, then the decisions) in one launch, no score buffer.
 int64_t halve_local_rows(int dtype, int64_t d);

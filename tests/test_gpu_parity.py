@@ -202,6 +202,29 @@ def test_custom_shapes_parity(cfg):
     _check_attention(w, Q, K, V, idx, O.cpu().numpy(), range(w.S))
 
 
+# Decision passes whose buckets' early rows are added by helper workgroups
+# (rounds of at most 128 buckets, a multiple of 8, of at least 4096 rows):
+# every slice, or four of the 8192-row case, against the oracle.
+HELPER_CASES = [
+    # one round of 8 buckets of 4096 rows (seven helpers per bucket)
+    (dict(B=1, H=8, n=4096, n_out=32, g=6, d=64, dtype="bf16", kind="gauss"), range(8)),
+    # fp32, d = 128: 8 buckets of 4096 rows
+    (dict(B=1, H=8, n=4096, n_out=64, g=5, d=128, dtype="fp32", kind="gauss_d4"), range(8)),
+    # 16 buckets of 8192 rows, then 16 of 4096
+    (dict(B=2, H=8, n=8192, n_out=64, g=6, d=64, dtype="bf16", kind="heavy_tail"), (0, 5, 10, 15)),
+]
+
+
+@pytest.mark.parametrize("cfg,slices", HELPER_CASES,
+                         ids=lambda c: f"S{c['B'] * c['H']}-n{c['n']}-d{c['d']}-{c['dtype']}"
+                         if isinstance(c, dict) else "")
+def test_decision_helpers_parity(cfg, slices):
+    w = W.custom("helpers", seed=13, **cfg)
+    Q, K, V = W.make_qkv(w)
+    plan, U, idx, tr = _compress_gpu(w, Q, K, V)
+    _check_compress(w, K, V, U, idx, tr, slices)
+
+
 def test_nout_equal_n_is_identity_and_exact_attention():
     w = W.custom("ident", B=2, H=1, n=96, n_out=96, g=1, d=64, dtype="fp32")
     Q, K, V = W.make_qkv(w)

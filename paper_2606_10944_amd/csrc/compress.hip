@@ -1256,7 +1256,7 @@ __device__ __forceinline__ void publish(int* flag, int value) {
 // bucket's own bulk waves (the hand-over then has kPassHand + 1 blocks of
 // decisions to arrive before the decider needs the chunk).
 #ifndef PASS_HAND
-#define PASS_HAND 6
+#define PASS_HAND 10
 #endif
 constexpr int kPassHand = PASS_HAND;
 __device__ __forceinline__ int hand_row(int c) { return 2 * c - 2 - kPassHand; }
@@ -1472,7 +1472,11 @@ __global__ __launch_bounds__(64 * (BW + 2)) void halve_pass_kernel(HalveArgs a) 
 #pragma unroll
         for (int k = 0; k < 8; ++k) dst[k] = c_[k];
       }
-      word = shared_read(gm + (live ? fb : 0));
+      // lane 0's read, broadcast only when the item is used: the wave does
+      // not wait for it here
+      word = 0;
+      if (lane == 0)
+        word = __hip_atomic_fetch_add(gm + (live ? fb : 0), (uint64_t)0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       if (live && ++fb > hand_row(fc)) {
         fc += T;
         h_enter();
@@ -1490,7 +1494,8 @@ __global__ __launch_bounds__(64 * (BW + 2)) void halve_pass_kernel(HalveArgs a) 
       for (int r = 0; r < NCB; ++r) {
         const int b = ib[r], c = ic[r];
         const bool live = c < nch;
-        const uint32_t smask = live ? decided_mask(gm + b, mw[r], helper_tag(a.pass_tag, b), a.status) : 0u;
+        const uint64_t w0 = __shfl(mw[r], 0);
+        const uint32_t smask = live ? decided_mask(gm + b, w0, helper_tag(a.pass_tag, b), a.status) : 0u;
         u32x4 col[QW];
         if constexpr (L::COAL) {
 #pragma unroll

@@ -410,24 +410,21 @@ __host__ __device__ inline int64_t panel_tiles(int64_t B, int64_t NT, int64_t RT
   return B * NT - RT * B * (B - 1) / 2;
 }
 
-// Work decomposition of pair_scores_kernel.  A group is BLOCKS consecutive
-// decision blocks (64 rows each) of one bucket; the group's W waves hold its
-// rows as MFMA fragments, HB half-blocks (32 rows) per wave, paired so that
-// every wave has the same amount of work: with HB = 2, wave w holds the first
-// half of block w and the second half of block BLOCKS-1-w.  Workgroups are
-// small enough that two fit on a CU, so one's row loads overlap the other's
-// arithmetic.  Launches with streamed chunks take W = 4 waves of HB = 2 (the
-// streamed tiles are software-pipelined across a wave's two slots); launches
-// of own chunks only (and the local kernel) take W = 8 waves of HB = 1 where
-// that gives the same groups (fragments of up to 4 words per lane): half the
-// registers per wave, so twice the waves per SIMD hide each other's
-// latencies (long workload round 0: 204 -> 183 us; the small workloads'
-// local rounds 5-15% faster).  A workgroup handles one
-// (bucket, group, chunk): chunk 0 covers the group's own column tiles, which
-// the owning waves write to LDS from their registers (so the bucket's rows
-// are read from HBM once); chunk c >= 1 covers kScoreChunk column tiles after
-// the group, streamed from global memory through registers DEPTH tiles ahead.
-constexpr int kScoreWaves = 4;  // waves of a launch with streamed chunks
+// Work decomposition of pair_scores_kernel.  A group is BLOCKS = W / 2
+// consecutive decision blocks (64 rows each) of one bucket; each of the
+// group's W waves holds one half-block (32 rows) of it as MFMA fragments
+// (HB = 1 half-block per wave).  W = 8 where a half-block's fragments take at
+// most four words per lane (bf16, and fp32 up to d = 64: about 128 registers
+// per wave, four waves per SIMD, two workgroups per CU, whose latencies hide
+// each other's), else W = 4 (fp32, d = 128).  Every launch of a bucket size
+// uses the same W, so own and streamed chunks share their groups.  (Four
+// waves of two half-blocks each, the two slots software-pipelined, needed
+// 253 registers: two waves per SIMD, and the streamed rounds of the long
+// workload ran 4-7 % slower.)  A workgroup handles one (bucket, group,
+// chunk): chunk 0 covers the group's own column tiles, which the owning
+// waves write to LDS from their registers (so the bucket's rows are read
+// from HBM once); chunk c >= 1 covers kScoreChunk column tiles after the
+// group, streamed from global memory through registers DEPTH tiles ahead.
 #ifndef SCORE_DEPTH
 #define SCORE_DEPTH 3
 #endif
@@ -445,7 +442,7 @@ constexpr int kETileLds = 8 * kETileStride;
 template <typename T, int D, int W>
 struct ScoreShape {
   static constexpr int NV = Frag<T, D>::NV;
-  static constexpr int HB = (W == 4 && NV < 8) ? 2 : 1;  // half-blocks per wave
+  static constexpr int HB = 1;                 // half-blocks per wave
   static constexpr int BLOCKS = W * HB / 2;    // decision blocks per group
   static constexpr int GT = 4 * BLOCKS;        // 16-row tiles per group
   static constexpr int CHUNKS = 2 * NV;        // 1 KB fragment chunks per tile (K, then V)
@@ -458,23 +455,16 @@ struct ScoreShape {
                              kScoreRowsStaged * 8;
 };
 
-// Waves of the launches of own chunks only and of the local kernel (the
-// same groups as the streamed launches': see above).
+// Waves of every score launch and of the local kernel (see above).
 template <typename T, int D>
-constexpr int own_waves() {
-  return Frag<T, D>::NV < 8 ? 8 : kScoreWaves;
+constexpr int score_waves() {
+  return Frag<T, D>::NV < 8 ? 8 : 4;
 }
 
-// Block (group-local) and half of half-block slot h of wave w (W waves).
-template <int HB, int W>
-__device__ __forceinline__ void half_block(int w, int h, int& b, int& half) {
-  if (HB == 2) {
-    b = h == 0 ? w : W - 1 - w;
-    half = h;
-  } else {
-    b = w >> 1;
-    half = w & 1;
-  }
+// Block (group-local) and half of the half-block of wave w.
+__device__ __forceinline__ void half_block(int w, int& b, int& half) {
+  b = w >> 1;
+  half = w & 1;
 }
 
 // The decisions of one block of 32 pairs (lane p: pair p of the block, with
@@ -659,7 +649,7 @@ void pair_scores_kernel(HalveArgs a) {
 #pragma unroll
   for (int h = 0; h < HB; ++h) {
     int b, half;
-    half_block<HB, W>(wave, h, b, half);
+    half_block(wave, b, half);
     hb_blk[h] = grp * NBW + b;
     hb_half[h] = half;
     hb_ok[h] = hb_blk[h] < nb;
@@ -790,14 +780,8 @@ void pair_scores_kernel(HalveArgs a) {
 #define SCORE_OWN_COMMIT(STAGE, TL)                                                  \
   do {                                                                               \
     const int b_ = (TL) >> 2, half_ = ((TL) >> 1) & 1, rt_ = (TL) & 1;              \
-    const int owner_ = HB == 2 ? (half_ == 0 ? b_ : W - 1 - b_) : 2 * b_ + half_;  \
-    const int slot_ = HB == 2 ? half_ : 0;                                           \
-    if (wave == owner_) {                                                            \
-      if (slot_ == 0) {                                                              \
-        if (rt_ == 0) SCORE_OWN_WRITE(STAGE, 0, 0); else SCORE_OWN_WRITE(STAGE, 0, 1); \
-      } else {                                                                       \
-        if (rt_ == 0) SCORE_OWN_WRITE(STAGE, HB - 1, 0); else SCORE_OWN_WRITE(STAGE, HB - 1, 1); \
-      }                                                                              \
+    if (wave == 2 * b_ + half_) {                                                    \
+      if (rt_ == 0) SCORE_OWN_WRITE(STAGE, 0, 0); else SCORE_OWN_WRITE(STAGE, 0, 1);   \
     }                                                                                \
   } while (0)
 
@@ -868,12 +852,22 @@ void pair_scores_kernel(HalveArgs a) {
       }                                                                                \
     }                                                                                  \
   } while (0)
-  // 16 MFMAs, each followed by up to 3 vector (or transcendental) instructions
-#define SCORE_INTERLEAVE()                                                              \
+  // Streamed tiles: the column fragments are read from the stage word by
+  // word beside the MFMAs that use them (all of them at once would take 32
+  // more registers, past the 128 that four waves per SIMD allow)
+#define SCORE_MMA_LDS(H, STAGE)                                                         \
   do {                                                                                 \
-    _Pragma("unroll") for (int k_ = 0; k_ < 2 * NV * 2; ++k_) {                        \
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                               \
-      __builtin_amdgcn_sched_group_barrier(0x402, 3, 0);                               \
+    _Pragma("unroll") for (int rt_ = 0; rt_ < 2; ++rt_) {                              \
+      gk[0][H][rt_] = (floatx4_t){0.f, 0.f, 0.f, 0.f};                                 \
+      gv[0][H][rt_] = (floatx4_t){vm2f, vm2f, vm2f, vm2f};                             \
+    }                                                                                  \
+    _Pragma("unroll") for (int v_ = 0; v_ < NV; ++v_) {                                \
+      const uint4 bk1_ = reinterpret_cast<const uint4*>(smem + ((STAGE) * CH + v_) * 1024)[lane]; \
+      const uint4 bv1_ = reinterpret_cast<const uint4*>(smem + ((STAGE) * CH + NV + v_) * 1024)[lane]; \
+      _Pragma("unroll") for (int rt_ = 0; rt_ < 2; ++rt_) {                            \
+        gk[0][H][rt_] = mma_word<T>(Ak[H][rt_][v_], bk1_, gk[0][H][rt_]);              \
+        gv[0][H][rt_] = mma_word<T>(Av[H][rt_][v_], bv1_, gv[0][H][rt_]);              \
+      }                                                                                \
     }                                                                                  \
   } while (0)
 
@@ -891,63 +885,16 @@ void pair_scores_kernel(HalveArgs a) {
       SCORE_COMMIT(((U) + 2) % NS, ((U) + 2) % DEPTH);                                 \
       SCORE_ISSUE(jt_ + 2 + DEPTH, ((U) + 2) % DEPTH);                                 \
     }                                                                                  \
-    SCORE_BFRAG((U) % NS);                                                             \
+    if (OWN) SCORE_BFRAG((U) % NS);                                                    \
     const float h2_ = jt_ * 16 + m16 >= N ? 0.0f                                       \
                       : (OWN) ? s_h2[i_ * 16 + m16] : pair_h2f(s_hst[((U) % NS) * 16 + m16]);        \
     _Pragma("unroll") for (int h = 0; h < HB; ++h) {                                   \
       if (!SCORE_ACTIVE(OWN, h, jt_)) continue;                                        \
-      SCORE_MMA_H(h);                                                                  \
+      if (OWN) SCORE_MMA_H(h); else SCORE_MMA_LDS(h, (U) % NS);                        \
       SCORE_EPI_H(h, h2_, (U) % NS);                                                   \
     }                                                                                  \
     __syncthreads();                                                                   \
   } while (0)
-  // Streamed tiles with two half-block slots are software-pipelined across
-  // the slots: the MFMAs of one slot are interleaved with the exp epilogue of
-  // the other (slot 1 of the previous tile, then slot 0 of this tile), so
-  // the matrix core and the vector ALU of a SIMD work at the same time.  A
-  // tile's scores are then complete one tile later, and written one more
-  // tile later.
-  float h2_prev = 0.0f;
-#define SCORE_TILE_P(I, U, FIRST)                                                       \
-  do {                                                                                 \
-    const int i_ = (I);                                                                \
-    const int jt_ = jt0 + i_;                                                          \
-    if (i_ >= 2) SCORE_FLUSH(false, i_ - 2, ((U) + 1) % NS);                           \
-    SCORE_COMMIT(((U) + 2) % NS, ((U) + 2) % DEPTH);                                   \
-    SCORE_ISSUE(jt_ + 2 + DEPTH, ((U) + 2) % DEPTH);                                   \
-    SCORE_BFRAG((U) % NS);                                                             \
-    const float h2c_ = jt_ * 16 + m16 >= N ? 0.0f : pair_h2f(s_hst[((U) % NS) * 16 + m16]);           \
-    SCORE_MMA_H(0);                                                                    \
-    if (!(FIRST)) SCORE_EPI_H(1, h2_prev, ((U) + NS - 1) % NS);                        \
-    SCORE_INTERLEAVE();                                                                \
-    SCORE_MMA_H(1);                                                                    \
-    SCORE_EPI_H(0, h2c_, (U) % NS);                                                    \
-    SCORE_INTERLEAVE();                                                                \
-    h2_prev = h2c_;                                                                    \
-    __syncthreads();                                                                   \
-  } while (0)
-
-  // Own tiles with two half-block slots (own-only launches), pipelined the
-  // same way; a slot's MFMAs and epilogue are skipped before its block's
-  // diagonal tile.
-#define SCORE_TILE_OP(I, U, FIRST)                                                      \
-  do {                                                                                 \
-    const int i_ = (I);                                                                \
-    const int jt_ = jt0 + i_;                                                          \
-    if (i_ >= 2) SCORE_FLUSH(true, i_ - 2, ((U) + 1) % NS);                            \
-    if (i_ + 2 < ntile) SCORE_OWN_COMMIT(((U) + 2) % NS, i_ + 2);                      \
-    SCORE_BFRAG((U) % NS);                                                             \
-    const float h2c_ = jt_ * 16 + m16 >= N ? 0.0f : s_h2[i_ * 16 + m16];               \
-    if (SCORE_ACTIVE(true, 0, jt_)) SCORE_MMA_H(0);                                    \
-    if (!(FIRST) && SCORE_ACTIVE(true, 1, jt_ - 1)) SCORE_EPI_H(1, h2_prev, ((U) + NS - 1) % NS); \
-    SCORE_INTERLEAVE();                                                                \
-    if (SCORE_ACTIVE(true, 1, jt_)) SCORE_MMA_H(1);                                    \
-    if (SCORE_ACTIVE(true, 0, jt_)) SCORE_EPI_H(0, h2c_, (U) % NS);                    \
-    SCORE_INTERLEAVE();                                                                \
-    h2_prev = h2c_;                                                                    \
-    __syncthreads();                                                                   \
-  } while (0)
-
   // LOCAL: the decisions of the bucket's P <= 32 NBW pairs from the scores
   // in LDS (wave 0).  Block m: thresholds as in halve_pass_kernel; alpha =
   // the float32 signed sums of every earlier block, added in block order in
@@ -1009,28 +956,12 @@ void pair_scores_kernel(HalveArgs a) {
     SCORE_OWN_COMMIT(0, 0);
     if (ntile > 1) SCORE_OWN_COMMIT(1, 1);
     __syncthreads();
-    if constexpr (OWN_ONLY && !LOCAL && HB == 2) {
-      for (int ib = 0; ib < ntile; ib += DEPTH) {
+    for (int ib = 0; ib < ntile; ib += DEPTH) {
 #pragma unroll
-        for (int u = 0; u < DEPTH; ++u)
-          if (ib + u < ntile) SCORE_TILE_OP(ib + u, u, ib + u == 0);  // uniform over the workgroup
-      }
-      const int last = ntile - 1;
-      {
-        const int jt_ = jt0 + last;
-        if (SCORE_ACTIVE(true, 1, jt_)) SCORE_EPI_H(1, h2_prev, last % NS);
-      }
-      __syncthreads();
-      if (last >= 1) SCORE_FLUSH(true, last - 1, (last - 1) % NS);
-      SCORE_FLUSH(true, last, last % NS);
-    } else {
-      for (int ib = 0; ib < ntile; ib += DEPTH) {
-#pragma unroll
-        for (int u = 0; u < DEPTH; ++u)
-          if (ib + u < ntile) SCORE_TILE(true, ib + u, u);  // uniform over the workgroup
-      }
-      SCORE_FLUSH(true, ntile - 1, (ntile - 1) % NS);
+      for (int u = 0; u < DEPTH; ++u)
+        if (ib + u < ntile) SCORE_TILE(true, ib + u, u);  // uniform over the workgroup
     }
+    SCORE_FLUSH(true, ntile - 1, (ntile - 1) % NS);
     if constexpr (LOCAL) {
       __syncthreads();
       if (wave == 0) local_decisions();
@@ -1049,36 +980,16 @@ void pair_scores_kernel(HalveArgs a) {
     // issued after them (stores count in vmcnt on this architecture).  The
     // chunk runs whole ring turns (tiles past ntile are padding).
     const int nturn = (ntile + DEPTH - 1) / DEPTH;
-    if constexpr (HB == 2) {
-      SCORE_TILE_P(0, 0, true);
 #pragma unroll
-      for (int u = 1; u < DEPTH; ++u) SCORE_TILE_P(u, u, false);
-      for (int ib = DEPTH; ib < nturn * DEPTH; ib += DEPTH) {
+    for (int u = 0; u < DEPTH; ++u) SCORE_TILE(false, u, u);
+    for (int ib = DEPTH; ib < nturn * DEPTH; ib += DEPTH) {
 #pragma unroll
-        for (int u = 0; u < DEPTH; ++u) SCORE_TILE_P(ib + u, u, false);
-      }
-      const int last = nturn * DEPTH - 1;
-      {
-        const int jt_ = jt0 + last;  // (names the tile for the LOCAL layout only)
-        SCORE_EPI_H(1, h2_prev, last % NS);
-      }
-      __syncthreads();
-      SCORE_FLUSH(false, last - 1, (last - 1) % NS);
-      SCORE_FLUSH(false, last, last % NS);
-    } else {
-#pragma unroll
-      for (int u = 0; u < DEPTH; ++u) SCORE_TILE(false, u, u);
-      for (int ib = DEPTH; ib < nturn * DEPTH; ib += DEPTH) {
-#pragma unroll
-        for (int u = 0; u < DEPTH; ++u) SCORE_TILE(false, ib + u, u);
-      }
-      SCORE_FLUSH(false, nturn * DEPTH - 1, (nturn * DEPTH - 1) % NS);
+      for (int u = 0; u < DEPTH; ++u) SCORE_TILE(false, ib + u, u);
     }
+    SCORE_FLUSH(false, nturn * DEPTH - 1, (nturn * DEPTH - 1) % NS);
   }
 #undef SCORE_TILE
-#undef SCORE_TILE_P
-#undef SCORE_TILE_OP
-#undef SCORE_INTERLEAVE
+#undef SCORE_MMA_LDS
 #undef SCORE_FLUSH
 #undef SCORE_EPI_H
 #undef SCORE_MMA_H
@@ -1787,13 +1698,11 @@ __global__ __launch_bounds__(64) void gram16_kernel(const T* rows, float* out) {
 #endif
 template <typename T, int D>
 hipError_t launch_scores_td(const HalveArgs& a, int64_t nbk, hipStream_t st) {
-  constexpr int WO = own_waves<T, D>();
-  using SS = ScoreShape<T, D, kScoreWaves>;
-  using SO = ScoreShape<T, D, WO>;
-  static_assert(SO::GT == SS::GT, "own-only and streamed launches share the groups");
-  auto kern_mixed = pair_scores_kernel<T, D, false, false, kScoreWaves>;
+  constexpr int WO = score_waves<T, D>();
+  using SS = ScoreShape<T, D, WO>;  // own and streamed chunks share the groups
+  auto kern_mixed = pair_scores_kernel<T, D, false, false, WO>;
   auto kern_own = pair_scores_kernel<T, D, false, true, WO>;
-  const size_t lds = SS::LDS, lds_own = SO::LDS;
+  const size_t lds = SS::LDS, lds_own = SS::LDS;
   if (lds > 64 * 1024) {
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern_mixed),
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
@@ -1829,7 +1738,7 @@ hipError_t launch_scores_td(const HalveArgs& a, int64_t nbk, hipStream_t st) {
     if (chunk0 == 0 && nz == 1)
       hipLaunchKernelGGL(kern_own, dim3((unsigned)wgs), dim3(64 * WO), lds_own, st, x);
     else
-      hipLaunchKernelGGL(kern_mixed, dim3((unsigned)wgs), dim3(64 * kScoreWaves), lds, st, x);
+      hipLaunchKernelGGL(kern_mixed, dim3((unsigned)wgs), dim3(64 * WO), lds, st, x);
   };
   if (a.rowh2_write && nch > 1) {
     // the streamed chunks read the row scales the own chunks write: two launches
@@ -1871,7 +1780,7 @@ hipError_t launch_local_td(const HalveArgs& a0, int64_t nbk, hipStream_t st) {
     if constexpr (tiny_tiles<T, D>() >= 4)
       if (a0.N <= 64) return launch_tiny_td<T, D, 4>(a0, nbk, st);
   }
-  constexpr int WO = own_waves<T, D>();
+  constexpr int WO = score_waves<T, D>();
   using SS = ScoreShape<T, D, WO>;
   auto kern = pair_scores_kernel<T, D, true, true, WO>;
   const int64_t NT = (a0.N + 15) / 16, nb = (a0.N + 63) / 64, P = a0.N / 2;
@@ -1906,9 +1815,9 @@ hipError_t launch_local_t(int64_t d, const HalveArgs& a, int64_t nbk, hipStream_
 template <typename T>
 int64_t local_rows_t(int64_t d) {
   switch (d) {
-    case 32: return ScoreShape<T, 32, own_waves<T, 32>()>::GT * 16;
-    case 64: return ScoreShape<T, 64, own_waves<T, 64>()>::GT * 16;
-    case 128: return ScoreShape<T, 128, own_waves<T, 128>()>::GT * 16;
+    case 32: return ScoreShape<T, 32, score_waves<T, 32>()>::GT * 16;
+    case 64: return ScoreShape<T, 64, score_waves<T, 64>()>::GT * 16;
+    case 128: return ScoreShape<T, 128, score_waves<T, 128>()>::GT * 16;
     default: return 0;
   }
 }

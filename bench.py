@@ -543,7 +543,10 @@ def main():
     per_step = collections.defaultdict(float)
     for name, _, ms in rec:
         per_step[name] += ms / args.steps
-    score_ms = [ms for name, _, ms in rec if name == "scores"]
+    # pair_scores_kernel: the score launches of two-launch rounds and the
+    # local launches (scores and decisions in one) of the others
+    PS = ("scores", "local")
+    score_ms = [ms for name, _, ms in rec if name in PS]
     L = plan["rounds"]
     tc = sum(v for k, v in per_step.items() if k != "attention")
     ta = per_step["attention"]
@@ -559,17 +562,18 @@ def main():
     # per launch: averages over every score launch of the K steps (a round may
     # take several launches; bytes and time are both summed over the step)
     n_sc = len(score_ms) // args.steps
-    sc_rounds = sorted({r for name, r, _ in rec if name == "scores"})  # the others run local
+    sc_rounds = sorted({r for name, r, _ in rec if name in PS})
+    two_launch = {r for name, r, _ in rec if name == "scores"}  # rounds with a score buffer
     if n_sc:
         sc_ms_launch = statistics.mean(score_ms)
         sc_bytes_launch = sum(rb[r] for r in sc_rounds) / n_sc
-        sc_impl_launch = sum(ib[r] for r in sc_rounds) / n_sc
+        sc_impl_launch = sum(ib[r] for r in two_launch) / n_sc
         sc_gbs = sc_bytes_launch / (sc_ms_launch * 1e-3) / 1e9
         # per round: its score launches' time per step and the fraction of
         # the HBM roofline its algorithmic bytes reach
         by_round = {}
         for r in sc_rounds:
-            ms_r = sum(ms for name, rr, ms in rec if name == "scores" and rr == r) / args.steps
+            ms_r = sum(ms for name, rr, ms in rec if name in PS and rr == r) / args.steps
             by_round[r] = {"ms": ms_r, "frac": rb[r] / (ms_r * 1e-3) / 1e9 / HBM_PEAK_GBS}
     traffic = stored_traffic(w.name) if args.halve == "kh" and not weighted else None
     # bf16 output (half the output bytes; the precision of the parity tests
@@ -606,8 +610,9 @@ def main():
                    "n_out": w.n_out, "g": w.g, "out_dtype": "fp32", "halve": args.halve,
                    "n_sinks": ns, "n_window": nw},
         "roofline": {
-            "kernel": "pair_scores_kernel (one launch per Halve round with buckets above "
-                      "the local size)",
+            "kernel": "pair_scores_kernel (one launch per Halve round: the score launch of "
+                      "a round above the local bucket size, else the local launch, scores "
+                      "and decisions in one)",
             "bound": "hbm", "achieved": sc_gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
             "frac": sc_gbs / HBM_PEAK_GBS,
             "traffic": traffic,

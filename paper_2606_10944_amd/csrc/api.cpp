@@ -66,12 +66,6 @@ bool make_levels(int64_t n, int64_t n_out, int32_t g, Levels* lv) {
 // several launches.
 constexpr size_t kScoreCap = (size_t)2 << 30;
 
-// Rounds of small buckets run as one local launch (scores in LDS, then the
-// decisions) up to this many buckets.  Beyond it the two-launch path is as
-// fast (its score kernel overlaps loads and arithmetic across workgroups and
-// its decision pass runs more buckets per CU), so many-bucket rounds keep it.
-constexpr int64_t kLocalMaxBuckets = 2048;
-
 size_t score_bytes(int64_t N) { return thin::halve_score_bytes(N); }
 
 size_t score_region(int64_t S, int64_t d, const Levels& lv, size_t cap_bytes = kScoreCap) {
@@ -79,7 +73,7 @@ size_t score_region(int64_t S, int64_t d, const Levels& lv, size_t cap_bytes = k
   // rounds whose buckets run as one local launch (for either dtype) need none
   const int64_t local = std::min(thin::halve_local_rows(0, d), thin::halve_local_rows(1, d));
   for (int32_t r = 0; r < lv.L; ++r) {
-    if (lv.N[r] <= local && S * lv.G[r] < kLocalMaxBuckets) continue;
+    if (lv.N[r] <= local) continue;
     const size_t per = score_bytes(lv.N[r]);
     const size_t all = (size_t)(S * lv.G[r]) * per;
     const size_t cap = per > cap_bytes ? per : cap_bytes;
@@ -188,11 +182,13 @@ hipError_t observed(int32_t kernel, int32_t round, hipStream_t st, F&& launch) {
 }
 
 // One KH round over the S*G buckets described by `a`: one local launch for
-// small buckets, else pair scores then decisions, in as many launches as the
-// score region (e_bytes) needs.
+// buckets up to the local kernel's size (however many: with 4096 buckets of
+// 256 rows the local launch beats scores + decisions by ~5 %, with 16384 of
+// 16 rows or 4096 of 64 rows by 2-2.5x), else pair scores then decisions, in
+// as many launches as the score region (e_bytes) needs.
 hipError_t kh_round(int32_t dtype, int64_t d, thin::HalveArgs a, int64_t buckets, size_t e_bytes,
                     int32_t r, hipStream_t st) {
-  if (a.N <= thin::halve_local_rows(dtype, d) && buckets < kLocalMaxBuckets) {
+  if (a.N <= thin::halve_local_rows(dtype, d)) {
     a.b0 = 0;
     return observed(THIN_KERNEL_LOCAL, r, st,
                     [&] { return thin::launch_local(dtype, d, a, buckets, st); });

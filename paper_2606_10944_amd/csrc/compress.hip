@@ -1957,7 +1957,13 @@ hipError_t launch_vmax(int dtype, const void* V, int64_t S, int64_t n, int64_t l
                      vmax_bits, zw, status);
   const int64_t bytes = dtype == 0 ? 4 : 2;
   const int64_t words = n * d * bytes / 16, slice_words = ld * d * bytes / 16;
-  const int64_t per_block = 16384;  // 256 KiB of V per workgroup
+  // 256 KiB of V per workgroup, less for small inputs so that the scan has
+  // about 1024 workgroups (one workgroup reads ~40 GB/s; 64 of them made the
+  // ViT-like workload's scan take 13 us), in whole turns of the 8-load loop
+  constexpr int64_t kVmaxTurn = 8 * 256;
+  int64_t per_block = 16384;
+  const int64_t want = (words * S + 1023) / 1024;
+  if (want < per_block) per_block = std::max<int64_t>(kVmaxTurn, (want + kVmaxTurn - 1) / kVmaxTurn * kVmaxTurn);
   const int64_t chunks = (words + per_block - 1) / per_block;
   dim3 grid((unsigned)chunks, (unsigned)S);
   if (dtype == 0)

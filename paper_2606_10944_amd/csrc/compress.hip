@@ -430,6 +430,10 @@ __host__ __device__ inline int64_t panel_tiles(int64_t B, int64_t NT, int64_t RT
 #endif
 constexpr int kScoreStages = 3;
 constexpr int kScoreChunk = 32;
+#ifndef SCORE_MIN_WGS
+#define SCORE_MIN_WGS 128
+#endif
+constexpr int64_t kScoreMinWorkgroups = SCORE_MIN_WGS;  // half the CUs
 // Streamed rows whose indices a workgroup stages: its chunk, rounded up to
 // whole ring turns, plus the ring's look-ahead.
 constexpr int kScoreRowsStaged = (kScoreChunk + 2 * SCORE_DEPTH + 1) * 16;
@@ -1697,7 +1701,7 @@ __global__ __launch_bounds__(64) void gram16_kernel(const T* rows, float* out) {
 #define SCORE_IL 16
 #endif
 template <typename T, int D>
-hipError_t launch_scores_td(const HalveArgs& a, int64_t nbk, hipStream_t st) {
+hipError_t launch_scores_td(const HalveArgs& a0, int64_t nbk, hipStream_t st) {
   constexpr int WO = score_waves<T, D>();
   using SS = ScoreShape<T, D, WO>;  // own and streamed chunks share the groups
   auto kern_mixed = pair_scores_kernel<T, D, false, false, WO>;
@@ -1713,9 +1717,24 @@ hipError_t launch_scores_td(const HalveArgs& a, int64_t nbk, hipStream_t st) {
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds_own);
     if (e != hipSuccess) return e;
   }
-  const int64_t NT = (a.N + 15) / 16;
+  const int64_t NT = (a0.N + 15) / 16;
   const int64_t groups = (NT + SS::GT - 1) / SS::GT;
   const int64_t rest = NT > SS::GT ? NT - SS::GT : 0;  // tiles after the first group
+  // Column tiles per streamed chunk (one workgroup's tiles, taken one after
+  // the other): kScoreChunk, or fewer when the launch would leave the device
+  // short of workgroups (a few large buckets: each chunk's tiles are then the
+  // launch's critical path)
+  HalveArgs a = a0;
+  auto workgroups = [&](int64_t c) {
+    int64_t w = 0;
+    for (int64_t g = 0; g < groups; ++g) {
+      const int64_t rest_g = NT - (g + 1) * SS::GT;
+      w += 1 + (rest_g > 0 ? (rest_g + c - 1) / c : 0);
+    }
+    return w * nbk;
+  };
+  for (const int c : {15, 9, 6})
+    if (workgroups(a.ch) <= kScoreMinWorkgroups && c < a.ch) a.ch = c;
   const int64_t nch = 1 + (rest + a.ch - 1) / a.ch;
   // one workgroup per (bucket, group, chunk) with work, buckets padded to a
   // multiple of the eight XCDs (the padding workgroups return at once)

@@ -435,8 +435,9 @@ constexpr int kScoreChunk = 32;
 #endif
 constexpr int64_t kScoreMinWorkgroups = SCORE_MIN_WGS;  // half the CUs
 // Streamed rows whose indices a workgroup stages: its chunk, rounded up to
-// whole ring turns, plus the ring's look-ahead.
-constexpr int kScoreRowsStaged = (kScoreChunk + 2 * SCORE_DEPTH + 1) * 16;
+// whole ring turns, plus the ring's look-ahead and the one tile whose index
+// is read ahead of its load.
+constexpr int kScoreRowsStaged = (kScoreChunk + 2 * SCORE_DEPTH + 2) * 16;
 // A score tile (8 column pairs x 32 row pairs) in LDS: column stride 36
 // floats, so the scattered single-float writes of a half-wave hit 32
 // different banks.
@@ -662,7 +663,7 @@ void pair_scores_kernel(HalveArgs a) {
   // so that their latency and the fragments' overlap (the index loads are
   // the older ones, and staging them in LDS waits for them only).
   constexpr int RPT = (kScoreRowsStaged + 64 * W - 1) / (64 * W);
-  const int j_end = own ? 0 : min(N, (jt1 + 2 * DEPTH + 1) * 16);
+  const int j_end = own ? 0 : min(N, (jt1 + 2 * DEPTH + 2) * 16);
   int64_t ridx[RPT];
   if (!own) {
 #pragma unroll
@@ -752,12 +753,15 @@ void pair_scores_kernel(HalveArgs a) {
   // of K (c < NV) or V.  Own tiles are the owners' fragments, same layout.
   // Streamed rows also bring their scale exponents from the per-row table
   // (written by the first round's own chunks), staged in LDS with the rows.
+  // Tiles are issued in order, and each one reads the next one's row index
+  // from LDS (rnx), so that no issue waits for an LDS read.
   u32x4 stg[DEPTH][LPT];
   float hst[DEPTH];
+  int64_t rnx = 0;
 #define SCORE_ISSUE(JT, SLOT)                                                        \
   do {                                                                               \
-    const int j_ = min((JT) * 16 + m16, N - 1);                                      \
-    const int64_t row_ = s_rows[j_ - jt0 * 16];                                      \
+    const int64_t row_ = rnx;                                                        \
+    rnx = s_rows[min(((JT) + 1) * 16 + m16, N - 1) - jt0 * 16];                      \
     hst[SLOT] = a.rowh2[s * a.n + row_];                                             \
     _Pragma("unroll") for (int k_ = 0; k_ < LPT; ++k_) {                             \
       const int c_ = min(wave + k_ * W, CH - 1);                                     \
@@ -875,14 +879,14 @@ void pair_scores_kernel(HalveArgs a) {
     }                                                                                  \
   } while (0)
 
-  // One column tile (tile I of the chunk, ring position U = I mod 3): the
-  // previous tile is written out, tile I+2 staged (and, streamed, tile
-  // I+2+DEPTH loaded), then Grams and scores of tile I.
+  // One column tile (tile I of the chunk, ring position U = I mod 3): tile
+  // I+2 staged (and, streamed, tile I+2+DEPTH loaded), Grams and scores of
+  // tile I, then the previous tile written out (its LDS read after this
+  // tile's work, so that it waits at the barrier's wait only).
 #define SCORE_TILE(OWN, I, U)                                                           \
   do {                                                                                 \
     const int i_ = (I);                                                                \
     const int jt_ = jt0 + i_;                                                          \
-    if (i_ > 0) SCORE_FLUSH(OWN, i_ - 1, ((U) + NS - 1) % NS);                         \
     if (OWN) {                                                                         \
       if (i_ + 2 < ntile) SCORE_OWN_COMMIT(((U) + 2) % NS, i_ + 2);                    \
     } else {                                                                           \
@@ -897,6 +901,7 @@ void pair_scores_kernel(HalveArgs a) {
       if (OWN) SCORE_MMA_H(h); else SCORE_MMA_LDS(h, (U) % NS);                        \
       SCORE_EPI_H(h, h2_, (U) % NS);                                                   \
     }                                                                                  \
+    if (i_ > 0) SCORE_FLUSH(OWN, i_ - 1, ((U) + NS - 1) % NS);                         \
     __syncthreads();                                                                   \
   } while (0)
   // LOCAL: the decisions of the bucket's P <= 32 NBW pairs from the scores
@@ -971,6 +976,7 @@ void pair_scores_kernel(HalveArgs a) {
       if (wave == 0) local_decisions();
     }
   } else if constexpr (!LOCAL && !OWN_ONLY) {
+    rnx = s_rows[min(jt0 * 16 + m16, N - 1) - jt0 * 16];  // staged before the barrier above
 #pragma unroll
     for (int k = 0; k < DEPTH; ++k) SCORE_ISSUE(jt0 + k, k);
     SCORE_COMMIT(0, 0);

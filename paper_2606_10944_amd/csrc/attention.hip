@@ -176,24 +176,11 @@ __global__ __launch_bounds__(64 * WAVES) void coreset_attn_kernel(
       if (BF) {
 #pragma unroll
         for (int c = 0; c < 2; ++c) {
-          uint16_t hb[8], lb[8];
+          float pv[8];
 #pragma unroll
-          for (int j = 0; j < 8; ++j) {
-            const float pv = pr[2 * c + (j >> 2)][j & 3];
-            hb[j] = float_to_bf16(pv);
-            lb[j] = float_to_bf16(pv - bf16_to_float(hb[j]));
-          }
-          uint4 hw, lw;
-          hw.x = (uint32_t)hb[0] | ((uint32_t)hb[1] << 16);
-          hw.y = (uint32_t)hb[2] | ((uint32_t)hb[3] << 16);
-          hw.z = (uint32_t)hb[4] | ((uint32_t)hb[5] << 16);
-          hw.w = (uint32_t)hb[6] | ((uint32_t)hb[7] << 16);
-          lw.x = (uint32_t)lb[0] | ((uint32_t)lb[1] << 16);
-          lw.y = (uint32_t)lb[2] | ((uint32_t)lb[3] << 16);
-          lw.z = (uint32_t)lb[4] | ((uint32_t)lb[5] << 16);
-          lw.w = (uint32_t)lb[6] | ((uint32_t)lb[7] << 16);
-          const bf16x8_t bhi = __builtin_bit_cast(bf16x8_t, hw);
-          const bf16x8_t blo = __builtin_bit_cast(bf16x8_t, lw);
+          for (int j = 0; j < 8; ++j) pv[j] = pr[2 * c + (j >> 2)][j & 3];
+          bf16x8_t bhi, blo;
+          split_bf16x8(pv, bhi, blo);
 #pragma unroll
           for (int dt = 0; dt < D / 16; ++dt) {
             const unsigned char* row = sV + (dt * 16 + m16) * L::v_stride;
@@ -258,15 +245,6 @@ struct ResLds {
   // P.V multiplies 32 keys at a time
   static_assert(NKT % 2 == 0, "resident coreset needs an even number of 16-key tiles");
 };
-
-typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
-// Two floats to packed bf16 (round to nearest even, v_cvt_pk_bf16_f32).
-__device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
-  const bf16x2_t v = {(__bf16)a, (__bf16)b};
-  return __builtin_bit_cast(uint32_t, v);
-}
-__device__ __forceinline__ float bf16_lo_to_float(uint32_t w) { return __uint_as_float(w << 16); }
-__device__ __forceinline__ float bf16_hi_to_float(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
 
 __device__ __forceinline__ uint32_t pack_lo(uint32_t x, uint32_t y) { return (x & 0xffffu) | (y << 16); }
 __device__ __forceinline__ uint32_t pack_hi(uint32_t x, uint32_t y) { return (x >> 16) | (y & 0xffff0000u); }
@@ -438,16 +416,10 @@ __global__ __launch_bounds__(64 * WR) void coreset_attn_res_kernel(
       bf16x8_t bhi[QTR], blo[QTR];
 #pragma unroll
       for (int qt = 0; qt < QTR; ++qt) {
-        uint32_t hw[4], lw[4];
+        float pv[8];
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          const float p0 = sc[qt][2 * c + (j >> 1)][2 * (j & 1)];
-          const float p1 = sc[qt][2 * c + (j >> 1)][2 * (j & 1) + 1];
-          hw[j] = pack_bf16x2(p0, p1);
-          lw[j] = pack_bf16x2(p0 - bf16_lo_to_float(hw[j]), p1 - bf16_hi_to_float(hw[j]));
-        }
-        bhi[qt] = __builtin_bit_cast(bf16x8_t, make_uint4(hw[0], hw[1], hw[2], hw[3]));
-        blo[qt] = __builtin_bit_cast(bf16x8_t, make_uint4(lw[0], lw[1], lw[2], lw[3]));
+        for (int e = 0; e < 8; ++e) pv[e] = sc[qt][2 * c + (e >> 2)][e & 3];
+        split_bf16x8(pv, bhi[qt], blo[qt]);
       }
 #pragma unroll
       for (int dt = 0; dt < D / 16; ++dt) {
@@ -833,24 +805,11 @@ __global__ __launch_bounds__(64 * PF_WAVES) __attribute__((amdgpu_waves_per_eu(4
       if (BF) {
 #pragma unroll
         for (int c = 0; c < 2; ++c) {
-          uint16_t hb[8], lb[8];
+          float pv[8];
 #pragma unroll
-          for (int j = 0; j < 8; ++j) {
-            const float pv = pr[2 * c + (j >> 2)][j & 3];
-            hb[j] = float_to_bf16(pv);
-            lb[j] = float_to_bf16(pv - bf16_to_float(hb[j]));
-          }
-          uint4 hw, lw;
-          hw.x = (uint32_t)hb[0] | ((uint32_t)hb[1] << 16);
-          hw.y = (uint32_t)hb[2] | ((uint32_t)hb[3] << 16);
-          hw.z = (uint32_t)hb[4] | ((uint32_t)hb[5] << 16);
-          hw.w = (uint32_t)hb[6] | ((uint32_t)hb[7] << 16);
-          lw.x = (uint32_t)lb[0] | ((uint32_t)lb[1] << 16);
-          lw.y = (uint32_t)lb[2] | ((uint32_t)lb[3] << 16);
-          lw.z = (uint32_t)lb[4] | ((uint32_t)lb[5] << 16);
-          lw.w = (uint32_t)lb[6] | ((uint32_t)lb[7] << 16);
-          const bf16x8_t bhi = __builtin_bit_cast(bf16x8_t, hw);
-          const bf16x8_t blo = __builtin_bit_cast(bf16x8_t, lw);
+          for (int j = 0; j < 8; ++j) pv[j] = pr[2 * c + (j >> 2)][j & 3];
+          bf16x8_t bhi, blo;
+          split_bf16x8(pv, bhi, blo);
 #pragma unroll
           for (int dt = 0; dt < D / 16; ++dt) {
             const unsigned char* row = sV + (dt * 16 + m16) * L::v_stride;

@@ -53,12 +53,29 @@ __device__ __forceinline__ float bf16_to_float(uint16_t b) {
   return __uint_as_float(((uint32_t)b) << 16);
 }
 
-// Round-to-nearest-even float -> bf16 (finite inputs; NaN kept quiet).
-__device__ __forceinline__ uint16_t float_to_bf16(float f) {
-  uint32_t u = __float_as_uint(f);
-  if ((u & 0x7f800000u) == 0x7f800000u) return (uint16_t)((u >> 16) | ((u & 0xffffu) ? 0x40u : 0u));
-  u += 0x7fffu + ((u >> 16) & 1u);
-  return (uint16_t)(u >> 16);
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+
+// Two floats to two bf16 (round to nearest even) in one word, a in the low
+// half: one packed conversion instruction on gfx950.
+__device__ __forceinline__ uint32_t cvt_pk_bf16(float a, float b) {
+  const bf16x2_t v = {(__bf16)a, (__bf16)b};
+  return __builtin_bit_cast(uint32_t, v);
+}
+
+// Eight values (probabilities of the P V product) as bf16 high parts and the
+// bf16 rounding of what each high part leaves: hi + lo carries about 16
+// significant bits of each value, so two bf16 MFMAs give P V to about the
+// accuracy of float32 P.
+__device__ __forceinline__ void split_bf16x8(const float* p, bf16x8_t& hi, bf16x8_t& lo) {
+  uint32_t h[4], l[4];
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    h[k] = cvt_pk_bf16(p[2 * k], p[2 * k + 1]);
+    l[k] = cvt_pk_bf16(p[2 * k] - __uint_as_float(h[k] << 16),
+                       p[2 * k + 1] - __uint_as_float(h[k] & 0xffff0000u));
+  }
+  hi = __builtin_bit_cast(bf16x8_t, make_uint4(h[0], h[1], h[2], h[3]));
+  lo = __builtin_bit_cast(bf16x8_t, make_uint4(l[0], l[1], l[2], l[3]));
 }
 
 // acc += A_frag x B_frag over one row fragment.

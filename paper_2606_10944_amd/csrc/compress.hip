@@ -151,7 +151,6 @@ __global__ void assemble_kernel(int64_t n, int64_t ns, int64_t n_out, int64_t nw
 // ---------------------------------------------------------------------------
 // Cross-lane helpers (VALU only, no LDS crossbar).
 // ---------------------------------------------------------------------------
-typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
 
 // Value of lane l ^ 1 (DPP quad_perm [1,0,3,2]).
 __device__ __forceinline__ uint32_t from_partner(uint32_t v) {

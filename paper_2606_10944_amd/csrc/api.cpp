@@ -3,7 +3,10 @@
 #include <math.h>
 
 #include <algorithm>
+#include <map>
+#include <mutex>
 #include <new>
+#include <tuple>
 #include <vector>
 #include <stdint.h>
 #include <string.h>
@@ -1036,12 +1039,42 @@ int pf_run(int64_t n_out, int32_t mbar, int64_t n, const float* draws, int64_t n
   }
   if (L && ((int64_t)h->tiles.size() > L->max_tiles || (int64_t)h->psegs.size() > L->max_segs))
     return THIN_EINVAL;
+  // C_0 starts never move back; the prefill kernel turns each causal
+  // candidate's visibility into an interval of points on that account
+  for (int64_t p = 1; p < n; ++p)
+    if (h->c0[p] < h->c0[p - 1]) return THIN_EINVAL;
   return THIN_OK;
 }
+
+// The layout and key counts of a prefill depend on its sizes only (the
+// Subsample draws move points, not the cache structure), so a count-only run
+// per size is kept: a prefill then runs the host counters once, with its
+// draws.  (At most kPfCacheMax sizes; the cache is emptied when full.)
+struct PfChecked {
+  PfLayout L;
+  int64_t u_slice, draws, query_keys, staged_keys;
+};
+constexpr size_t kPfCacheMax = 16;
 
 int pf_check(int64_t B, int64_t H, int64_t n, int64_t d, int64_t n_out, int32_t mbar,
              PfLayout* L, int64_t* u_slice, int64_t* draws, int64_t* query_keys = nullptr,
              int64_t* staged_keys = nullptr) {
+  // (a cached entry's arguments all passed the checks below)
+  static std::mutex mu;
+  static std::map<std::tuple<int64_t, int64_t, int64_t, int64_t, int64_t, int32_t>, PfChecked> cache;
+  const auto key = std::make_tuple(B, H, d, n, n_out, mbar);
+  {
+    std::lock_guard<std::mutex> lock(mu);
+    const auto it = cache.find(key);
+    if (it != cache.end()) {
+      *L = it->second.L;
+      *u_slice = it->second.u_slice;
+      *draws = it->second.draws;
+      if (query_keys) *query_keys = it->second.query_keys;
+      if (staged_keys) *staged_keys = it->second.staged_keys;
+      return THIN_OK;
+    }
+  }
   int64_t k = 0;
   const int rc = ex_check(B, H, d, n_out, mbar, n, u_slice, &k, draws);
   if (rc) return rc;
@@ -1051,6 +1084,9 @@ int pf_check(int64_t B, int64_t H, int64_t n, int64_t d, int64_t n_out, int32_t 
   *L = pf_layout(B * H, n_out, mbar, n, h.rec);
   if (query_keys) *query_keys = h.query_keys;
   if (staged_keys) *staged_keys = h.staged_keys;
+  std::lock_guard<std::mutex> lock(mu);
+  if (cache.size() >= kPfCacheMax) cache.clear();
+  cache[key] = PfChecked{*L, *u_slice, *draws, h.query_keys, h.staged_keys};
   return THIN_OK;
 }
 

@@ -585,8 +585,13 @@ hipError_t launch_attn_res_d(int64_t n_out, const void* Q, const void* K, const 
 // one log-weight, piece k seen by the points vlo..vhi-1), then the causal
 // candidates causal_lo .. q1-1: candidate r is seen by point p iff r == p
 // (the point itself) or r was kept and c0[p] <= r < p (p's C_0), with p's
-// log-weight w0[p].  Same arithmetic as coreset_attn_kernel, with per-key
-// biases sqrt(d) * logw.
+// log-weight w0[p].  C_0 starts never move back (c0 is non-decreasing in p),
+// so the points of the tile that see a candidate are an interval too:
+// [r, max(r + 1, first tile point whose C_0 starts after r)) if r was kept,
+// else [r, r + 1).  Every key then carries one interval of the tile's points
+// (offsets from q0 in [0, 128], start in bits 0-15, end in bits 16-30); a
+// causal key is flagged by bit 31 and takes the point's bias.  Same
+// arithmetic as coreset_attn_kernel, with per-key biases sqrt(d) * logw.
 // ---------------------------------------------------------------------------
 template <typename T, int D, typename TO>
 __global__ __launch_bounds__(64 * PF_WAVES) __attribute__((amdgpu_waves_per_eu(4))) void prefill_attn_kernel(
@@ -598,8 +603,8 @@ __global__ __launch_bounds__(64 * PF_WAVES) __attribute__((amdgpu_waves_per_eu(4
   constexpr bool BF = Elem<T>::bytes == 2;
   using L = AttnLds<T, D>;
   __shared__ __align__(16) unsigned char lds[L::bytes];
-  __shared__ int32_t s_pos[KC];   // causal candidate: position (bit 30: not kept); piece key: -1
-  __shared__ int32_t s_vlo[KC], s_vhi[KC];
+  // a key's interval of the tile's points that see it (packed as above)
+  __shared__ __align__(16) uint32_t s_vis[KC];
   __shared__ int32_t s_row[KC];
   __shared__ int64_t s_seg_end[kPrefillMaxSegs];
   __shared__ PrefillSeg s_seg[kPrefillMaxSegs];
@@ -656,7 +661,10 @@ __global__ __launch_bounds__(64 * PF_WAVES) __attribute__((amdgpu_waves_per_eu(4
   // chunk's arithmetic; they reach LDS at the top of the chunk.
   // (registers hold the raw loaded values; anything computed from them is
   // left to the commit, so that no wait for the loads precedes the compute)
-  int32_t m_vlo = 0, m_vhi = 0, m_raw = 0, m_cpos = -1;
+  // m_vis / m_vis_nk: the key's packed visibility (a causal candidate's if
+  // kept / if not kept; the list read of kept[] is only waited for at commit)
+  uint32_t m_vis = 0, m_vis_nk = 0;
+  int32_t m_raw = 0, m_cpos = -1;
   uint8_t m_kept = 1;
   float m_bias = -INFINITY;
   bool m_piece = false;
@@ -664,8 +672,14 @@ __global__ __launch_bounds__(64 * PF_WAVES) __attribute__((amdgpu_waves_per_eu(4
     if (threadIdx.x >= KC) return;
     const int kc_ = (int)min((int64_t)KC, M - ck_);
     const int64_t kk = ck_ + threadIdx.x;
-    m_vlo = 0;
-    m_vhi = 0;
+    // points [lo, hi) as offsets in the tile, clipped to it
+    auto vis = [&](int64_t lo, int64_t hi) {
+      const uint32_t a = (uint32_t)min(max(lo - q0, (int64_t)0), (int64_t)QPB);
+      const uint32_t b = (uint32_t)min(max(hi - q0, (int64_t)0), (int64_t)QPB);
+      return a | (b << 16);
+    };
+    m_vis = 0;
+    m_vis_nk = 0;
     m_bias = -INFINITY;
     m_piece = false;
     m_cpos = -1;
@@ -684,12 +698,19 @@ __global__ __launch_bounds__(64 * PF_WAVES) __attribute__((amdgpu_waves_per_eu(4
         const int64_t j = kk - (k ? s_seg_end[k - 1] : 0);
         m_raw = sg.src ? sg.src[s * sg.stride + j] : (int32_t)(sg.start + j);
         m_bias = sg.logw * sqrt_d;
-        m_vlo = s_seg[k].vlo;
-        m_vhi = s_seg[k].vhi;
+        m_vis = m_vis_nk = vis(s_seg[k].vlo, s_seg[k].vhi);
         m_piece = true;
       } else {
         m_cpos = (int32_t)(tile.causal_lo + (kk - F));
         m_kept = kept[m_cpos];
+        // the tile's points whose C_0 starts at or before the candidate: a prefix
+        int lo = 0, hi = (int)(q1 - q0);
+        while (lo < hi) {
+          const int mid = (lo + hi) >> 1;
+          if (s_c0[mid] <= m_cpos) lo = mid + 1; else hi = mid;
+        }
+        m_vis = vis(m_cpos, max((int64_t)m_cpos + 1, q0 + lo)) | 0x80000000u;
+        m_vis_nk = vis(m_cpos, (int64_t)m_cpos + 1) | 0x80000000u;
       }
     }
   };
@@ -700,9 +721,7 @@ __global__ __launch_bounds__(64 * PF_WAVES) __attribute__((amdgpu_waves_per_eu(4
     if (threadIdx.x < KC) {
       int64_t r = m_piece ? (int64_t)m_raw : (m_cpos >= 0 ? (int64_t)m_cpos : 0);
       r = r < 0 ? 0 : (r >= n ? n - 1 : r);
-      s_pos[threadIdx.x] = m_cpos >= 0 ? (m_cpos | (m_kept ? 0 : (1 << 30))) : -1;
-      s_vlo[threadIdx.x] = m_vlo;
-      s_vhi[threadIdx.x] = m_vhi;
+      s_vis[threadIdx.x] = m_kept ? m_vis : m_vis_nk;
       s_row[threadIdx.x] = (int32_t)r;
       sB[threadIdx.x] = m_bias;
     }
@@ -752,10 +771,26 @@ __global__ __launch_bounds__(64 * PF_WAVES) __attribute__((amdgpu_waves_per_eu(4
 #pragma unroll
     for (int qt = 0; qt < PF_QT; ++qt) {
       const int64_t p = qw + qt * 16 + m16;  // this lane's point
+      const uint32_t pl = (uint32_t)(p - q0);  // its offset in the tile
       const int li = (int)min(p - q0, (int64_t)QPB - 1);
-      const int32_t pc0 = p < q1 ? s_c0[li] : 0;
       const float pw0 = p < q1 ? s_w0[li] * sqrt_d : 0.f;
+      // the lane's 16 keys: bias where the point sees the key, else -inf
       float sc[4][4];
+#pragma unroll
+      for (int kt = 0; kt < 4; ++kt) {
+        const uint4 w4 = *reinterpret_cast<const uint4*>(&s_vis[kt * 16 + 4 * g]);
+        const float4 b4 = *reinterpret_cast<const float4*>(&sB[kt * 16 + 4 * g]);
+        const uint32_t wv[4] = {w4.x, w4.y, w4.z, w4.w};
+        const float kb[4] = {b4.x, b4.y, b4.z, b4.w};
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const bool seen = pl >= (wv[i] & 0xffffu) && pl < ((wv[i] >> 16) & 0x7fffu);
+          sc[kt][i] = seen ? ((int32_t)wv[i] < 0 ? pw0 : kb[i]) : -INFINITY;
+        }
+      }
+      // (keeps the masks' LDS reads from being scheduled among the MFMAs
+      // below, where their registers would push values out to scratch)
+      __builtin_amdgcn_sched_barrier(0);
       float mx = -INFINITY;
 #pragma unroll
       for (int kt = 0; kt < 4; ++kt) {
@@ -769,18 +804,8 @@ __global__ __launch_bounds__(64 * PF_WAVES) __attribute__((amdgpu_waves_per_eu(4
         z = mma_rows<T, D>(ak, Bq[qt], z);
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          const int key = kt * 16 + 4 * g + i;
-          const int32_t ps = s_pos[key];
-          float v;
-          if (ps < 0) {
-            v = (p >= s_vlo[key] && p < s_vhi[key]) ? z[i] + sB[key] : -INFINITY;
-          } else {
-            const int64_t r = ps & ~(1 << 30);
-            const bool seen = r == p || (!(ps & (1 << 30)) && r < p && r >= pc0);
-            v = seen ? z[i] + pw0 : -INFINITY;
-          }
-          sc[kt][i] = v;
-          mx = fmaxf(mx, v);
+          sc[kt][i] += z[i];  // -inf stays -inf
+          mx = fmaxf(mx, sc[kt][i]);
         }
       }
       mx = fmaxf(mx, __shfl_xor(mx, 16));

@@ -811,8 +811,8 @@ struct PfLayout {
   std::vector<std::vector<size_t>> region;     // [m/2][depth] node store of the calls
   std::vector<std::vector<int64_t>> rstride;   // [m/2][depth] its row stride per slice
   std::vector<size_t> enode;                   // [m/2] E after the Halve phase of level m - 2
-  size_t status, kept, keptrow, keptflag, hp, ein, vmax, lbt, h2, rowh2, mB, score, utab, tiles,
-      segs, c0, w0;
+  size_t status, kept, keptrow, keptflag, hp, ein, vmax, absmax, lbt, h2, rowh2, mB, score, utab,
+      tiles, segs, c0, w0;
   size_t e_bytes, bytes;
   int64_t max_tiles, max_segs, max_utab;
   size_t tab0;  // the host-built tables occupy [tab0, bytes): one copy from the caller's staging
@@ -867,6 +867,7 @@ PfLayout pf_layout(int64_t S, int64_t n_out, int32_t mbar, int64_t n, const Expr
     L.enode[lv + 1] = take(s4 * n_out);
   }
   L.vmax = take(s4 * gmax);
+  L.absmax = take(s4 * n);  // every row's largest |V| entry (the calls' v_max)
   L.lbt = take(s4 * pmax);
   L.h2 = take(s4 * pmax);
   L.rowh2 = take(s4 * n);
@@ -1104,7 +1105,8 @@ hipError_t pf_halve(int32_t dtype, int64_t d, int32_t halve, const PfLayout& L,
     });
   uint32_t* vmax = reinterpret_cast<uint32_t*>(ws + L.vmax);
   hipError_t e = observed(THIN_KERNEL_EXPRESS, -1, st, [&] {
-    return thin::launch_vmax_rows(dtype, V, L.n, d, in, in_stride, N, G, S, vmax, st);
+    return thin::launch_vmax_table(reinterpret_cast<const uint32_t*>(ws + L.absmax), L.n, in,
+                                   in_stride, N, G, S, vmax, st);
   });
   if (e != hipSuccess) return e;
   thin::HalveArgs a{};
@@ -1343,6 +1345,10 @@ int thin_express_prefill(int32_t dtype, int64_t B, int64_t H, int64_t n, int64_t
   auto dev = [&](size_t off) { return reinterpret_cast<int32_t*>(ws + off); };
   ok(observed(THIN_KERNEL_STATUS, -1, st,
               [&] { return thin::launch_zero_status(dev(L.status), st); }));
+  ok(observed(THIN_KERNEL_EXPRESS, -1, st, [&] {
+    return thin::launch_row_absmax(dtype, V, n, d, S, reinterpret_cast<uint32_t*>(ws + L.absmax),
+                                   st);
+  }));
   int32_t* kept = dev(L.kept);
   const int64_t nk = (int64_t)h.keptrow.size();
   if (e == hipSuccess && nk > 0)

@@ -76,6 +76,56 @@ __global__ __launch_bounds__(256) void vmax_rows_kernel(const T* V, int64_t ld, 
     vmax_bits[blockIdx.x] = __float_as_uint(fmaxf(fmaxf(part[0], part[1]), fmaxf(part[2], part[3])));
 }
 
+// The largest |V[s, r, c]| of every row r < n of every slice (rows n apart),
+// as the float's bit pattern at absmax[s * n + r]: one thread per 16-byte
+// word, the 2^wsh words of a row reduced by lane shuffles.  A Halve call's
+// v_max is then the largest entry of its rows (vmax_table_kernel): the same
+// integer maxima as vmax_rows_kernel, taken in another order.
+template <typename T>
+__global__ __launch_bounds__(256) void row_absmax_kernel(const T* V, int64_t words, int wsh,
+                                                         uint32_t* absmax) {
+  const int64_t w = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  uint32_t m = 0u;
+  if (w < words) {
+    const u32x4 x = reinterpret_cast<const u32x4*>(V)[w];
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      if (Elem<T>::bytes == 4) {
+        m = max(m, x[c] & 0x7fffffffu);
+      } else {
+        m = max(m, (x[c] << 16) & 0x7fffffffu);
+        m = max(m, x[c] & 0x7fff0000u);
+      }
+    }
+  }
+  for (int off = 1; off < (1 << wsh); off <<= 1) m = max(m, (uint32_t)__shfl_xor((int)m, off));
+  if (w < words && (w & ((1 << wsh) - 1)) == 0) absmax[w >> wsh] = m;
+}
+
+// v_max of G Halve calls per slice from the row table above: call t of slice
+// s over the rows idx[s * in_stride + t * N + j] (negative: no row), into
+// vmax_bits[s * G + t].  One workgroup per call.
+__global__ __launch_bounds__(256) void vmax_table_kernel(const uint32_t* absmax, int64_t n,
+                                                         const int32_t* idx, int64_t in_stride,
+                                                         int64_t N, int64_t G,
+                                                         uint32_t* vmax_bits) {
+  const int64_t s = blockIdx.x / G, t = blockIdx.x % G;
+  const uint32_t* tab = absmax + s * n;
+  const int32_t* rows = idx + s * in_stride + t * N;
+  uint32_t m = 0u;
+  for (int64_t j = threadIdx.x; j < N; j += blockDim.x) {
+    const int32_t r = rows[j];
+    m = max(m, r >= 0 ? tab[r] : 0u);
+  }
+  const float mf = wave_max(__uint_as_float(m));
+  __shared__ float part[4];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  if (lane == 0) part[wave] = mf;
+  __syncthreads();
+  if (threadIdx.x == 0)
+    vmax_bits[blockIdx.x] = __float_as_uint(fmaxf(fmaxf(part[0], part[1]), fmaxf(part[2], part[3])));
+}
+
 // Key j of slice s: the segment k with off_k <= j < off_k + len_k gives
 // src_k[s * stride_k + j - off_k] (src_k null: start_k + j - off_k) and logw_k;
 // slice s's keys start at s * out_stride.
@@ -402,6 +452,33 @@ hipError_t launch_rows_copy(const int32_t* src, int64_t src_stride, int32_t* dst
   dim3 grid((unsigned)((len + 255) / 256), (unsigned)S);
   hipLaunchKernelGGL(rows_copy_kernel, grid, dim3(256), 0, st, src, src_stride, dst, dst_stride,
                      len);
+  return hipGetLastError();
+}
+
+hipError_t launch_row_absmax(int dtype, const void* V, int64_t n, int64_t d, int64_t S,
+                             uint32_t* absmax, hipStream_t st) {
+  const int64_t wpr = d * (dtype == 0 ? 4 : 2) / 16;  // a power of two, 1..64
+  if (wpr < 1 || wpr > 64 || (wpr & (wpr - 1)) != 0) return hipErrorInvalidValue;
+  const int64_t words = S * n * wpr;
+  if (words <= 0) return hipSuccess;
+  const int64_t blocks = (words + 255) / 256;
+  if (blocks >= ((int64_t)1 << 31)) return hipErrorInvalidValue;
+  const int wsh = __builtin_ctzll((unsigned long long)wpr);
+  if (dtype == 0)
+    hipLaunchKernelGGL((row_absmax_kernel<float>), dim3((unsigned)blocks), dim3(256), 0, st,
+                       (const float*)V, words, wsh, absmax);
+  else
+    hipLaunchKernelGGL((row_absmax_kernel<bf16_t>), dim3((unsigned)blocks), dim3(256), 0, st,
+                       (const bf16_t*)V, words, wsh, absmax);
+  return hipGetLastError();
+}
+
+hipError_t launch_vmax_table(const uint32_t* absmax, int64_t n, const int32_t* idx,
+                             int64_t in_stride, int64_t N, int64_t G, int64_t S,
+                             uint32_t* vmax_bits, hipStream_t st) {
+  if (S * G <= 0) return hipSuccess;
+  hipLaunchKernelGGL(vmax_table_kernel, dim3((unsigned)(S * G)), dim3(256), 0, st, absmax, n, idx,
+                     in_stride, N, G, vmax_bits);
   return hipGetLastError();
 }
 

@@ -140,6 +140,14 @@ hipError_t launch_rows_copy(const int32_t* src, int64_t src_stride, int32_t* dst
 hipError_t launch_vmax_rows(int dtype, const void* V, int64_t ld, int64_t d, const int32_t* idx,
                             int64_t in_stride, int64_t N, int64_t G, int64_t S,
                             uint32_t* vmax_bits, hipStream_t st);
+// The largest |V| entry of every row of S slices of n rows (V [S, n, d]),
+// float bits at absmax[s * n + r]; then the v_max of G calls per slice from
+// that table (calls as in launch_vmax_rows), equal to launch_vmax_rows'.
+hipError_t launch_row_absmax(int dtype, const void* V, int64_t n, int64_t d, int64_t S,
+                             uint32_t* absmax, hipStream_t st);
+hipError_t launch_vmax_table(const uint32_t* absmax, int64_t n, const int32_t* idx,
+                             int64_t in_stride, int64_t N, int64_t G, int64_t S,
+                             uint32_t* vmax_bits, hipStream_t st);
 // idx / logw [S, out_stride]: the segments laid out one after another in the
 // first m entries of each slice (their lengths sum to m).
 hipError_t launch_express_keys(const ExpressSegs& segs, int64_t S, int64_t m, int64_t out_stride,

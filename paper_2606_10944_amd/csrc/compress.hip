@@ -31,6 +31,11 @@ __device__ __forceinline__ float wave_max_f(float v) {
   for (int off = 32; off >= 1; off >>= 1) v = fmaxf(v, __shfl_xor(v, off));
   return v;
 }
+__device__ __forceinline__ double wave_max_d(double v) {
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) v = fmax(v, __shfl_xor(v, off));
+  return v;
+}
 
 // ---------------------------------------------------------------------------
 // v_max = max_i ||v_i||_inf over the n thinned rows of a slice (Sec. 2.1, eq.
@@ -646,6 +651,11 @@ void pair_scores_kernel(HalveArgs a) {
   int64_t* s_rows = reinterpret_cast<int64_t*>(s_mh + 2 * NBW);
   float* s_lbt = s_mh + 2 * NBW;  // LOCAL: pair terms [P] and [P] (no staged rows there)
   float* s_h2p = s_lbt + P;
+  // LOCAL decisions: per block and lane the threshold and the bulk alpha of
+  // the earlier blocks but the last ([NBW][64] each), and each block's mask
+  double* s_thr = reinterpret_cast<double*>((reinterpret_cast<uintptr_t>(s_h2p + P) + 7) & ~(uintptr_t)7);
+  double* s_alpha = s_thr + 64 * NBW;
+  uint32_t* s_mask = reinterpret_cast<uint32_t*>(s_alpha + 64 * NBW);
 
   // ---- this wave's half-blocks: fragments and, in chunk 0, pair terms ----
   int hb_blk[HB], hb_half[HB];
@@ -904,48 +914,74 @@ void pair_scores_kernel(HalveArgs a) {
     __syncthreads();                                                                   \
   } while (0)
   // LOCAL: the decisions of the bucket's P <= 32 NBW pairs from the scores
-  // in LDS (wave 0).  Block m: thresholds as in halve_pass_kernel; alpha =
-  // the float32 signed sums of every earlier block, added in block order in
-  // float64 (the order of the separate pass); then decide_block.
+  // in LDS, with the arithmetic of halve_pass_kernel: block m's thresholds,
+  // then alpha = the float32 signed sums of every earlier block added in
+  // block order in float64, then decide_block.  Every wave of the workgroup
+  // takes part.  First wave m < nblk forms block m's thresholds (the carry
+  // of the earlier blocks is the largest of their pairs' values, which the
+  // sequential scan carries forward).  Then block by block, one barrier
+  // each: wave 0 adds the previous block's sums to the alpha the helpers
+  // have built and decides the block; meanwhile waves 1.. add that previous
+  // block's sums to the alpha of the blocks after this one, in block order,
+  // so every alpha is the same float64 sum as one wave's.
   auto local_decisions = [&]() {
     const int nblk = (P + 31) / 32;
     const float* Ub = a.U + s * a.u_slice + bucket_u(a, t, P);
     uint8_t* trace = a.trace ? a.trace + s * a.u_slice + bucket_u(a, t, P) : nullptr;
     int32_t* out = a.idx_out + s * out_stride(a) + t * (int64_t)P;
     const int pl = lane & 31;
-    double carry = -INFINITY;
-    uint32_t masks[NBW];
+    auto pair_of = [&](int m) { return 32 * m + min(pl, min(32, P - 32 * m) - 1); };
+    // block b's signed sums at pair gp's scale (gp in a later block)
+    auto bulk = [&](int b, uint32_t mask, int gp) {
+      const float* col = s_e + (panel_tiles(b, NT, 4) + (gp >> 3) - 4 * b) * kETileLds + (gp & 7) * kETileStride;
+      float sum = 0.0f;
 #pragma unroll
-    for (int m = 0; m < NBW; ++m) {
-      if (m >= nblk) break;
+      for (int i = 0; i < 32; ++i) sum += ((mask >> i) & 1u) ? -col[i] : col[i];
+      return ldexp((double)sum, (int)scale_shift(fmaxf(s_mh[2 * b], s_mh[2 * b + 1]), s_h2p[gp]));
+    };
+    if (wave < nblk) {
+      const int m = wave;
       const int npb = min(32, P - 32 * m);
-      const int gp = 32 * m + min(pl, npb - 1);
-      const double thr = block_threshold(s_lbt[gp], s_h2p[gp], Ub[gp], npb, lane, a.log_c, carry);
-      const float h2p = s_h2p[gp];
-      double alpha = 0.0;
-#pragma unroll
-      for (int b = 0; b < m; ++b) {
-        const float* col = s_e + (panel_tiles(b, NT, 4) + (gp >> 3) - 4 * b) * kETileLds + (gp & 7) * kETileStride;
-        float sum = 0.0f;
-#pragma unroll
-        for (int i = 0; i < 32; ++i) sum += ((masks[b] >> i) & 1u) ? -col[i] : col[i];
-        alpha += ldexp((double)sum, (int)scale_shift(fmaxf(s_mh[2 * b], s_mh[2 * b + 1]), h2p));
+      const int gp = pair_of(m);
+      double carry = -INFINITY;
+      for (int b = 0; b < m; ++b) {  // earlier blocks are whole
+        const int q = 32 * b + pl;
+        carry = fmax(carry, (double)s_lbt[q] + (double)s_h2p[q] * (0.5 * kLn2));
       }
-      float ef[32];
-      const float* oc = s_e + (panel_tiles(m, NT, 4) + (gp >> 3) - 4 * m) * kETileLds + (gp & 7) * kETileStride;
+      carry = wave_max_d(carry);
+      s_thr[64 * m + lane] = block_threshold(s_lbt[gp], s_h2p[gp], Ub[gp], npb, lane, a.log_c, carry);
+    }
+    for (int k = threadIdx.x; k < 64 * NBW; k += 64 * W) s_alpha[k] = 0.0;
+    __syncthreads();
+    uint32_t prev = 0u;  // wave 0: the last block's mask
+    for (int m = 0; m < nblk; ++m) {
+      if (wave == 0) {
+        const int npb = min(32, P - 32 * m);
+        const int gp = pair_of(m);
+        double alpha = s_alpha[64 * m + lane];
+        if (m > 0) alpha += bulk(m - 1, prev, gp);
+        float ef[32];
+        const float* oc = s_e + (panel_tiles(m, NT, 4) + (gp >> 3) - 4 * m) * kETileLds + (gp & 7) * kETileStride;
 #pragma unroll
-      for (int i = 0; i < 32; ++i) ef[i] = oc[i];
-      float unused = 0.0f;
-      // the block's own scores are at its shifted scale: decide there
-      const int sh = (int)scale_shift(fmaxf(s_mh[2 * m], s_mh[2 * m + 1]), h2p);
-      masks[m] = decide_block<false>(ldexp(alpha, -sh), ldexp(thr, -sh), ef, ef, npb, unused);
-      const uint32_t bit = (masks[m] >> pl) & 1u;
-      if (lane < npb) {
-        const int32_t r0 = rows_in ? rows_in[2 * gp] : (int32_t)(row_base + 2 * gp);
-        const int32_t r1 = rows_in ? rows_in[2 * gp + 1] : (int32_t)(row_base + 2 * gp + 1);
-        out[gp] = bit ? r1 : r0;
-        if (trace) trace[gp] = (uint8_t)bit;
+        for (int i = 0; i < 32; ++i) ef[i] = oc[i];
+        float unused = 0.0f;
+        // the block's own scores are at its shifted scale: decide there
+        const int sh = (int)scale_shift(fmaxf(s_mh[2 * m], s_mh[2 * m + 1]), s_h2p[gp]);
+        prev = decide_block<false>(ldexp(alpha, -sh), ldexp(s_thr[64 * m + lane], -sh), ef, ef, npb,
+                                   unused);
+        if (lane == 0) s_mask[m] = prev;
+        const uint32_t bit = (prev >> pl) & 1u;
+        if (lane < npb) {
+          const int32_t r0 = rows_in ? rows_in[2 * gp] : (int32_t)(row_base + 2 * gp);
+          const int32_t r1 = rows_in ? rows_in[2 * gp + 1] : (int32_t)(row_base + 2 * gp + 1);
+          out[gp] = bit ? r1 : r0;
+          if (trace) trace[gp] = (uint8_t)bit;
+        }
+      } else if (m > 0 && m + wave < nblk) {
+        const int j = m + wave;  // a later block: block m - 1's sums join its alpha
+        s_alpha[64 * j + lane] += bulk(m - 1, s_mask[m - 1], pair_of(j));
       }
+      __syncthreads();
     }
   };
 
@@ -972,7 +1008,7 @@ void pair_scores_kernel(HalveArgs a) {
     SCORE_FLUSH(true, ntile - 1, (ntile - 1) % NS);
     if constexpr (LOCAL) {
       __syncthreads();
-      if (wave == 0) local_decisions();
+      local_decisions();
     }
   } else if constexpr (!LOCAL && !OWN_ONLY) {
     rnx = s_rows[min(jt0 * 16 + m16, N - 1) - jt0 * 16];  // staged before the barrier above
@@ -1809,10 +1845,12 @@ hipError_t launch_local_td(const HalveArgs& a0, int64_t nbk, hipStream_t st) {
   auto kern = pair_scores_kernel<T, D, true, true, WO>;
   const int64_t NT = (a0.N + 15) / 16, nb = (a0.N + 63) / 64, P = a0.N / 2;
   // stages, score tiles, pair scale exponents of the rows, staged row
-  // scales, half-block row scale maxima, pair terms [2][P]
+  // scales, half-block row scale maxima, pair terms [2][P], then (8-byte
+  // aligned) the decisions' thresholds and alphas [2][BLOCKS][64] and masks
   const size_t lds = (size_t)kScoreStages * SS::CHUNKS * 1024 +
                      (size_t)panel_tiles(nb, NT, 4) * kETileLds * 4 + SS::GT * 16 * 4 +
-                     kScoreStages * 16 * 4 + 2 * SS::BLOCKS * 4 + 2 * P * 4;
+                     kScoreStages * 16 * 4 + 2 * SS::BLOCKS * 4 + 2 * P * 4 + 8 +
+                     2 * 64 * SS::BLOCKS * 8 + SS::BLOCKS * 4;
   if (lds > 64 * 1024) {
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);

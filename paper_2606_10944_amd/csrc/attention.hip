@@ -814,19 +814,25 @@ __global__ __launch_bounds__(64 * PF_WAVES) __attribute__((amdgpu_waves_per_eu(4
       const float scale = (mrun[qt] == -INFINITY || mnew == -INFINITY)
                               ? 0.0f : __builtin_amdgcn_exp2f((mrun[qt] - mnew) * c2);
       mrun[qt] = mnew;
+      // exp2(-inf) = 0 for the keys the point does not see; a row that sees
+      // none yet subtracts 0 instead of -inf
+      const float mref = mnew == -INFINITY ? 0.0f : mnew;
       float psum = 0.0f;
       float pr[4][4];
 #pragma unroll
       for (int kt = 0; kt < 4; ++kt)
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          const float pv = sc[kt][i] == -INFINITY ? 0.0f : __builtin_amdgcn_exp2f((sc[kt][i] - mnew) * c2);
+          const float pv = __builtin_amdgcn_exp2f((sc[kt][i] - mref) * c2);
           pr[kt][i] = pv;
           psum += pv;
         }
       lrun[qt] = lrun[qt] * scale + psum;
+      // (the running maxima of most chunks stay put: no rescale then)
+      if (__any(scale != 1.0f)) {
 #pragma unroll
-      for (int dt = 0; dt < D / 16; ++dt) acc[qt][dt] *= scale;
+        for (int dt = 0; dt < D / 16; ++dt) acc[qt][dt] *= scale;
+      }
       if (BF) {
 #pragma unroll
         for (int c = 0; c < 2; ++c) {

@@ -247,6 +247,22 @@ def test_prefill_plan_matches_decoding(n_out, mbar, n):
                                   None) == _lib.THIN_EINVAL
 
 
+def test_prefill_plan_is_kept_per_size():
+    """The prefill's layout is computed once per size: a repeated plan is
+    identical, and a cached size does not let arguments that differ from it
+    (negative batch and heads of the same product, another d) past the checks."""
+    a = _lib.thin_express_prefill_plan(1, 2, 777, 64, 16, 4)
+    b = _lib.thin_express_prefill_plan(1, 2, 777, 64, 16, 4)
+    assert a == b
+    for args in [(-1, -2, 777, 64, 16, 4), (2, 1, 777, 48, 16, 4), (1, 2, 0, 64, 16, 4)]:
+        with pytest.raises(_lib.ThinError):
+            _lib.thin_express_prefill_plan(*args)
+    # another slice count of the same sequence: same uniforms per slice, larger workspace
+    c = _lib.thin_express_prefill_plan(2, 2, 777, 64, 16, 4)
+    assert c["uniforms_per_slice"] == a["uniforms_per_slice"]
+    assert c["workspace_bytes"] > a["workspace_bytes"]
+
+
 def test_prefill_requires_host_staging():
     n_out, mbar, n = 8, 4, 512
     p = _lib.thin_express_prefill_plan(1, 2, n, 64, n_out, mbar)

@@ -1345,10 +1345,11 @@ int thin_express_prefill(int32_t dtype, int64_t B, int64_t H, int64_t n, int64_t
   auto dev = [&](size_t off) { return reinterpret_cast<int32_t*>(ws + off); };
   ok(observed(THIN_KERNEL_STATUS, -1, st,
               [&] { return thin::launch_zero_status(dev(L.status), st); }));
-  ok(observed(THIN_KERNEL_EXPRESS, -1, st, [&] {
-    return thin::launch_row_absmax(dtype, V, n, d, S, reinterpret_cast<uint32_t*>(ws + L.absmax),
-                                   st);
-  }));
+  if (halve == THIN_HALVE_KH)  // the KH calls' v_max come from this table
+    ok(observed(THIN_KERNEL_EXPRESS, -1, st, [&] {
+      return thin::launch_row_absmax(dtype, V, n, d, S,
+                                     reinterpret_cast<uint32_t*>(ws + L.absmax), st);
+    }));
   int32_t* kept = dev(L.kept);
   const int64_t nk = (int64_t)h.keptrow.size();
   if (e == hipSuccess && nk > 0)

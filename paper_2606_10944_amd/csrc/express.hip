@@ -126,6 +126,26 @@ __global__ __launch_bounds__(256) void vmax_table_kernel(const uint32_t* absmax,
     vmax_bits[blockIdx.x] = __float_as_uint(fmaxf(fmaxf(part[0], part[1]), fmaxf(part[2], part[3])));
 }
 
+// vmax_table_kernel for calls of at most 64 rows: one wave per call (call
+// c = 4 blockIdx.x + wave, c < calls), lane j reads row j.
+__global__ __launch_bounds__(256) void vmax_table_small_kernel(const uint32_t* absmax, int64_t n,
+                                                               const int32_t* idx,
+                                                               int64_t in_stride, int64_t N,
+                                                               int64_t G, int64_t calls,
+                                                               uint32_t* vmax_bits) {
+  const int lane = threadIdx.x & 63;
+  const int64_t c = 4 * (int64_t)blockIdx.x + (threadIdx.x >> 6);
+  if (c >= calls) return;  // whole waves
+  const int64_t s = c / G, t = c % G;
+  uint32_t m = 0u;
+  if (lane < N) {
+    const int32_t r = idx[s * in_stride + t * N + lane];
+    m = r >= 0 ? absmax[s * n + r] : 0u;
+  }
+  const float mf = wave_max(__uint_as_float(m));
+  if (lane == 0) vmax_bits[c] = __float_as_uint(mf);
+}
+
 // Key j of slice s: the segment k with off_k <= j < off_k + len_k gives
 // src_k[s * stride_k + j - off_k] (src_k null: start_k + j - off_k) and logw_k;
 // slice s's keys start at s * out_stride.
@@ -477,6 +497,11 @@ hipError_t launch_vmax_table(const uint32_t* absmax, int64_t n, const int32_t* i
                              int64_t in_stride, int64_t N, int64_t G, int64_t S,
                              uint32_t* vmax_bits, hipStream_t st) {
   if (S * G <= 0) return hipSuccess;
+  if (N <= 64) {  // calls of at most 64 rows: one wave each, four to a workgroup
+    hipLaunchKernelGGL(vmax_table_small_kernel, dim3((unsigned)((S * G + 3) / 4)), dim3(256), 0, st,
+                       absmax, n, idx, in_stride, N, G, S * G, vmax_bits);
+    return hipGetLastError();
+  }
   hipLaunchKernelGGL(vmax_table_kernel, dim3((unsigned)(S * G)), dim3(256), 0, st, absmax, n, idx,
                      in_stride, N, G, vmax_bits);
   return hipGetLastError();

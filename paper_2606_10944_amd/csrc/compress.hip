@@ -566,10 +566,10 @@ __device__ __align__(16) float g_score_sink[256];
 
 // LOCAL: the whole round for buckets of at most GT*16 rows in one launch:
 // one workgroup per bucket computes the bucket's scores into LDS (its own
-// chunk is the whole bucket), then wave 0 takes the decisions from LDS with
-// the same arithmetic as halve_pass_kernel (the scores never leave the CU).
-// OWN_ONLY: a launch of own chunks only (no streamed code, so the register
-// budget allows the own tiles to be software-pipelined as the streamed ones).
+// chunk is the whole bucket), then takes the decisions from LDS with the same
+// arithmetic as halve_pass_kernel (the scores never leave the CU).
+// OWN_ONLY: a launch of own chunks only (an instantiation without the
+// streamed code, which needs fewer registers).
 template <typename T, int D, bool LOCAL, bool OWN_ONLY, int W>
 __global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(2)))
 void pair_scores_kernel(HalveArgs a) {

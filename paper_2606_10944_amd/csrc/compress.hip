@@ -428,20 +428,23 @@ __host__ __device__ inline int64_t panel_tiles(int64_t B, int64_t NT, int64_t RT
 // chunk): chunk 0 covers the group's own column tiles, which the owning
 // waves write to LDS from their registers (so the bucket's rows are read
 // from HBM once); chunk c >= 1 covers kScoreChunk column tiles after the
-// group, streamed from global memory through registers DEPTH tiles ahead.
+// group (kScoreChunkLong in launches of many workgroups, fewer in launches of
+// few), streamed from global memory through registers DEPTH tiles ahead.
 #ifndef SCORE_DEPTH
 #define SCORE_DEPTH 3
 #endif
 constexpr int kScoreStages = 3;
 constexpr int kScoreChunk = 32;
+constexpr int kScoreChunkLong = 48;
 #ifndef SCORE_MIN_WGS
 #define SCORE_MIN_WGS 128
 #endif
 constexpr int64_t kScoreMinWorkgroups = SCORE_MIN_WGS;  // half the CUs
-// Streamed rows whose indices a workgroup stages: its chunk, rounded up to
-// whole ring turns, plus the ring's look-ahead and the one tile whose index
-// is read ahead of its load.
-constexpr int kScoreRowsStaged = (kScoreChunk + 2 * SCORE_DEPTH + 2) * 16;
+constexpr int64_t kScoreLongWorkgroups = 1024;         // four per CU
+// Streamed rows whose indices a workgroup stages: its chunk (at most
+// kScoreChunkLong), rounded up to whole ring turns, plus the ring's
+// look-ahead and the one tile whose index is read ahead of its load.
+constexpr int kScoreRowsStaged = (kScoreChunkLong + 2 * SCORE_DEPTH + 2) * 16;
 // A score tile (8 column pairs x 32 row pairs) in LDS: column stride 36
 // floats, so the scattered single-float writes of a half-wave hit 32
 // different banks.
@@ -1762,9 +1765,11 @@ hipError_t launch_scores_td(const HalveArgs& a0, int64_t nbk, hipStream_t st) {
   const int64_t groups = (NT + SS::GT - 1) / SS::GT;
   const int64_t rest = NT > SS::GT ? NT - SS::GT : 0;  // tiles after the first group
   // Column tiles per streamed chunk (one workgroup's tiles, taken one after
-  // the other): kScoreChunk, or fewer when the launch would leave the device
-  // short of workgroups (a few large buckets: each chunk's tiles are then the
-  // launch's critical path)
+  // the other): kScoreChunkLong while the launch keeps at least four
+  // workgroups per CU (each workgroup loads its group's fragments once, for
+  // more tiles), else kScoreChunk, or fewer when the launch would leave the
+  // device short of workgroups (a few large buckets: each chunk's tiles are
+  // then the launch's critical path)
   HalveArgs a = a0;
   auto workgroups = [&](int64_t c) {
     int64_t w = 0;
@@ -1774,6 +1779,7 @@ hipError_t launch_scores_td(const HalveArgs& a0, int64_t nbk, hipStream_t st) {
     }
     return w * nbk;
   };
+  if (workgroups(kScoreChunkLong) >= kScoreLongWorkgroups) a.ch = kScoreChunkLong;
   for (const int c : {15, 9, 6})
     if (workgroups(a.ch) <= kScoreMinWorkgroups && c < a.ch) a.ch = c;
   const int64_t nch = 1 + (rest + a.ch - 1) / a.ch;
